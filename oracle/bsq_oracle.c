@@ -1,0 +1,443 @@
+/*
+ * CPU oracle for the binary spherical (BSQ) weight codec and the products
+ * that consume it.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the
+ * benchmark's CPU baseline may load this library. It shares no code, header,
+ * table or constant generator with the HIP library under
+ * paper_2607_08643_amd/csrc, and it must stay plain: every loop below follows
+ * the order in which the paper (Section III) states the method, with the
+ * readings listed next to each step where the paper is silent.
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math -fopenmp -shared
+ * (no contraction, no fast-math; rows are independent, so the OpenMP row loop
+ * gives the same bits for every thread count).
+ *
+ * Canonical fp32 arithmetic contract for the encoder (the GPU reproduces it
+ * bit for bit, because stage-2 codes depend on the stage-1 reconstruction):
+ *   - fmaf() is the fused multiply-add of IEEE 754 (one rounding);
+ *   - '/' is IEEE division, round to nearest even;
+ *   - fp32 -> fp16 is round to nearest even, with finite overflow saturated;
+ *   - subnormals are kept.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORC_OK 0
+#define ORC_ERR_ARG 1
+#define ORC_ERR_NONFINITE 6
+
+#define KIND_IDENTITY 0
+#define KIND_LINEAR 1
+#define KIND_MLP 2
+
+#define MAX_CODE_BITS 16
+#define MAX_HIDDEN 256
+#define MAX_STAGES 4
+
+/* ------------------------------------------------------------------------ */
+/* binary16 conversions, written from the IEEE 754 binary16 definition.      */
+/* ------------------------------------------------------------------------ */
+
+/* fp32 -> fp16 bits, round to nearest, ties to even. Values whose rounded
+ * magnitude exceeds 65504 become infinity (IEEE behaviour). */
+uint16_t orc_f32_to_f16(float f)
+{
+    uint32_t x;
+    memcpy(&x, &f, 4);
+    uint16_t sign = (uint16_t)((x >> 16) & 0x8000u);
+    if (isnan(f)) return (uint16_t)(sign | 0x7e00u);
+    if (isinf(f)) return (uint16_t)(sign | 0x7c00u);
+    double a = fabs((double)f);
+    if (a == 0.0) return sign;
+    int e2;
+    frexp(a, &e2);            /* a in [2^(e2-1), 2^e2) */
+    int E = e2 - 1;           /* unbiased binary exponent of a */
+    if (E < -14) {
+        /* subnormal range: spacing 2^-24; n = 1024 is the smallest normal */
+        double n = nearbyint(a * 0x1p24);
+        return (uint16_t)(sign | (uint16_t)n);
+    }
+    double n = nearbyint(ldexp(a, 10 - E));   /* in [1024, 2048] */
+    uint32_t bits = ((uint32_t)(E + 15) << 10) + ((uint32_t)n - 1024u);
+    if (bits >= 0x7c00u) return (uint16_t)(sign | 0x7c00u);
+    return (uint16_t)(sign | bits);
+}
+
+float orc_f16_to_f32(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int ex = (h >> 10) & 0x1f;
+    int man = h & 0x3ff;
+    double v;
+    if (ex == 0x1f) v = man ? NAN : INFINITY;
+    else if (ex == 0) v = ldexp((double)man, -24);
+    else v = ldexp((double)(1024 + man), ex - 25);
+    return (float)(sign ? -v : v);
+}
+
+/* Gain storage rule: fp16, round to nearest even, finite overflow saturated
+ * to +-65504 (the largest finite binary16). */
+uint16_t orc_gain_to_f16(float alpha)
+{
+    uint16_t h = orc_f32_to_f16(alpha);
+    if ((h & 0x7fffu) == 0x7c00u) h = (uint16_t)((h & 0x8000u) | 0x7bffu);
+    return h;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Decoders (Section III-C; Table "BSQ codec components").                   */
+/* ------------------------------------------------------------------------ */
+
+/* Spherical code value: q_j = sign_j / sqrt(b). The stored bit is 1 for +.  */
+float orc_code_scale(int b)
+{
+    return (float)(1.0 / sqrt((double)b));
+}
+
+/* D_theta(q) for one b-bit code.
+ *  identity: y = q (requires d == b)
+ *  linear:   y_m = beta_m + sum_j M[m][j] q_j          (fmaf chain over j)
+ *  mlp:      a_k = relu(b1_k + sum_j W1[k][j] q_j)      (fmaf chain over j)
+ *            y_m = b2_m + sum_k W2[m][k] a_k            (fmaf chain over k)
+ *  relu(a) = (a > 0) ? a : +0.0f. */
+int orc_decoder_eval(int kind, int d, int b, int h,
+                     const float *W1, const float *b1,
+                     const float *W2, const float *b2,
+                     uint32_t code, float *y)
+{
+    if (b < 1 || b > MAX_CODE_BITS || d < 1 || d > MAX_CODE_BITS) return ORC_ERR_ARG;
+    float q[MAX_CODE_BITS];
+    float c = orc_code_scale(b);
+    for (int j = 0; j < b; ++j) q[j] = ((code >> j) & 1u) ? c : -c;
+    if (kind == KIND_IDENTITY) {
+        if (d != b) return ORC_ERR_ARG;
+        for (int j = 0; j < d; ++j) y[j] = q[j];
+    } else if (kind == KIND_LINEAR) {
+        for (int m = 0; m < d; ++m) {
+            float acc = b1[m];
+            for (int j = 0; j < b; ++j) acc = fmaf(W1[m * b + j], q[j], acc);
+            y[m] = acc;
+        }
+    } else if (kind == KIND_MLP) {
+        if (h < 1 || h > MAX_HIDDEN) return ORC_ERR_ARG;
+        float a[MAX_HIDDEN];
+        for (int k = 0; k < h; ++k) {
+            float acc = b1[k];
+            for (int j = 0; j < b; ++j) acc = fmaf(W1[k * b + j], q[j], acc);
+            a[k] = (acc > 0.0f) ? acc : 0.0f;
+        }
+        for (int m = 0; m < d; ++m) {
+            float acc = b2[m];
+            for (int k = 0; k < h; ++k) acc = fmaf(W2[m * h + k], a[k], acc);
+            y[m] = acc;
+        }
+    } else {
+        return ORC_ERR_ARG;
+    }
+    return ORC_OK;
+}
+
+/* Every code's decoded vector, table[code * d + m]. This is the function
+ * above evaluated for each of the 2^b codes (memoised; same bits). */
+int orc_decoder_table(int kind, int d, int b, int h,
+                      const float *W1, const float *b1,
+                      const float *W2, const float *b2, float *table)
+{
+    uint32_t n = 1u << b;
+    for (uint32_t code = 0; code < n; ++code) {
+        int rc = orc_decoder_eval(kind, d, b, h, W1, b1, W2, b2, code, table + (size_t)code * d);
+        if (rc) return rc;
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Protected input channels (Section III-E, eq. protected_channel_selection) */
+/* ------------------------------------------------------------------------ */
+
+/* Column energy key_j = g_j^2 * sum_i w_ij^2 in fp64, rows summed in order
+ * i = 0 .. d_out-1; g defaults to 1. Ranking by key is ranking by
+ * g_j * ||W[:, j]||_2 since both are monotone in it. */
+void orc_column_keys(const float *w, int64_t d_out, int64_t d_in, const float *g, double *key)
+{
+    for (int64_t j = 0; j < d_in; ++j) {
+        double s = 0.0;
+        for (int64_t i = 0; i < d_out; ++i) {
+            double v = (double)w[i * d_in + j];
+            s = s + v * v;
+        }
+        if (g) {
+            double gj = (double)g[j];
+            s = (gj * gj) * s;
+        }
+        key[j] = s;
+    }
+}
+
+static const double *g_sort_keys;
+static int cmp_key_desc_index_asc(const void *pa, const void *pb)
+{
+    int64_t a = *(const int64_t *)pa, b = *(const int64_t *)pb;
+    double ka = g_sort_keys[a], kb = g_sort_keys[b];
+    if (ka > kb) return -1;
+    if (ka < kb) return 1;
+    return (a < b) ? -1 : (a > b);
+}
+static int cmp_i32_asc(const void *pa, const void *pb)
+{
+    int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    return (a > b) - (a < b);
+}
+
+/* P = TopK_j(key, k): the k largest keys, equal keys -> lower column first;
+ * returned in ascending column order. Not thread-safe (qsort comparator
+ * state); the oracle calls it from one thread. */
+int orc_protect_select(const float *w, int64_t d_out, int64_t d_in, const float *g,
+                       int64_t k, int32_t *idx, double *key_out)
+{
+    if (k < 0 || k > d_in) return ORC_ERR_ARG;
+    double *key = key_out ? key_out : (double *)malloc(sizeof(double) * (size_t)d_in);
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)(d_in > 0 ? d_in : 1));
+    if (!key || !order) return ORC_ERR_ARG;
+    orc_column_keys(w, d_out, d_in, g, key);
+    for (int64_t j = 0; j < d_in; ++j) order[j] = j;
+    g_sort_keys = key;
+    qsort(order, (size_t)d_in, sizeof(int64_t), cmp_key_desc_index_asc);
+    for (int64_t p = 0; p < k; ++p) idx[p] = (int32_t)order[p];
+    qsort(idx, (size_t)k, sizeof(int32_t), cmp_i32_asc);
+    free(order);
+    if (!key_out) free(key);
+    return ORC_OK;
+}
+
+/* Q8 of the protected columns (eq. protected_8bit_scatter; reading: symmetric
+ * int8, one fp32 scale per protected column):
+ *   m_j = max_i |w_ij|;  s_j = m_j / 127;
+ *   q_ij = clamp(round_half_even(w_ij / s_j), -127, 127), and q = 0 when s_j = 0.
+ * Layout: q8[i * k + p] for protected column idx[p]. */
+void orc_q8(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int64_t k,
+            int8_t *q8, float *scale)
+{
+    for (int64_t p = 0; p < k; ++p) {
+        int64_t j = idx[p];
+        float m = 0.0f;
+        for (int64_t i = 0; i < d_out; ++i) {
+            float a = fabsf(w[i * d_in + j]);
+            if (a > m) m = a;
+        }
+        float s = m / 127.0f;
+        scale[p] = s;
+        for (int64_t i = 0; i < d_out; ++i) {
+            int8_t q = 0;
+            if (s != 0.0f) {
+                float t = nearbyintf(w[i * d_in + j] / s);
+                if (t > 127.0f) t = 127.0f;
+                if (t < -127.0f) t = -127.0f;
+                q = (int8_t)t;
+            }
+            q8[i * k + p] = q;
+        }
+    }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Encoder: sphere map + sign code + residual stage (Sections III-C, III-D). */
+/* ------------------------------------------------------------------------ */
+
+/* Encode one matrix w [d_out][d_in] (fp32, row-major) into S stages.
+ *
+ * Chunk (i, c) is w[i, c*d : (c+1)*d] (reading: d consecutive inputs of one
+ * output row). With the identity encoder z = r, and for ||z|| > 0 the sign
+ * of u = z / ||z|| equals the sign of z, so the code of a chunk is
+ *   bit_j = (z_j >= 0)                   (reading: +0 and -0 give 1)
+ *   code  = sum_j bit_j << j             (element j -> bit j, LSB first)
+ * Stage s (r^(0) = chunk with protected positions zeroed):
+ *   y      = D_s(q)
+ *   num    = fmaf chain over unprotected j of r_j * y_j, from +0
+ *   den    = fmaf chain over unprotected j of y_j * y_j, from +0
+ *   alpha  = den > 0 ? num / den : 0;   NaN -> 0
+ *   gain   = fp16(alpha) (saturating);  a = (float)gain
+ *   r_j    = fmaf(-a, y_j, r_j) for unprotected j
+ * (reading: each stage stores a least-squares fp16 gain so that the stage
+ * never increases the reconstruction error, whatever its decoder).
+ *
+ * Outputs, each row padded to `pitch` chunks (padding: code 0, gain +0):
+ *   codes[s]  uint8 (d <= 8) or uint16 (d > 8), [d_out][pitch]
+ *   gains[s]  fp16 bits,                         [d_out][pitch]
+ *   idx[k] ascending protected columns, q8[d_out][k], scale[k].
+ *
+ * tables[s] is the decoder table of stage s (orc_decoder_table). */
+int orc_encode(int d, int stages, const float *const *tables,
+               const float *w, int64_t d_out, int64_t d_in, const float *g,
+               int64_t k, int64_t pitch,
+               void *const *codes, uint16_t *const *gains,
+               int32_t *idx, int8_t *q8, float *scale, int nthreads)
+{
+    if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    if (d_in % d != 0 || k < 0 || k > d_in) return ORC_ERR_ARG;
+    int64_t C = d_in / d;
+    if (pitch < C) return ORC_ERR_ARG;
+    for (int64_t t = 0; t < d_out * d_in; ++t)
+        if (!isfinite(w[t])) return ORC_ERR_NONFINITE;
+
+    /* protected set, Q8 payload and the complement mask */
+    unsigned char *prot = (unsigned char *)calloc((size_t)(d_in > 0 ? d_in : 1), 1);
+    if (!prot) return ORC_ERR_ARG;
+    if (k > 0) {
+        int rc = orc_protect_select(w, d_out, d_in, g, k, idx, NULL);
+        if (rc) { free(prot); return rc; }
+        orc_q8(w, d_out, d_in, idx, k, q8, scale);
+        for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
+    }
+
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 16)
+#endif
+    for (int64_t i = 0; i < d_out; ++i) {
+        float r[MAX_CODE_BITS];
+        for (int64_t c = 0; c < pitch; ++c) {
+            if (c >= C) {
+                for (int s = 0; s < stages; ++s) {
+                    if (d <= 8) ((uint8_t *)codes[s])[i * pitch + c] = 0;
+                    else ((uint16_t *)codes[s])[i * pitch + c] = 0;
+                    gains[s][i * pitch + c] = 0;
+                }
+                continue;
+            }
+            for (int j = 0; j < d; ++j) {
+                int64_t col = c * d + j;
+                r[j] = prot[col] ? 0.0f : w[i * d_in + col];
+            }
+            for (int s = 0; s < stages; ++s) {
+                uint32_t code = 0;
+                for (int j = 0; j < d; ++j)
+                    if (r[j] >= 0.0f) code |= 1u << j;
+                const float *y = tables[s] + (size_t)code * d;
+                float num = 0.0f, den = 0.0f;
+                for (int j = 0; j < d; ++j) {
+                    if (prot[c * d + j]) continue;
+                    num = fmaf(r[j], y[j], num);
+                    den = fmaf(y[j], y[j], den);
+                }
+                float alpha = (den > 0.0f) ? num / den : 0.0f;
+                if (alpha != alpha) alpha = 0.0f;
+                uint16_t gh = orc_gain_to_f16(alpha);
+                float a = orc_f16_to_f32(gh);
+                for (int j = 0; j < d; ++j) {
+                    if (prot[c * d + j]) continue;
+                    r[j] = fmaf(-a, y[j], r[j]);
+                }
+                if (d <= 8) ((uint8_t *)codes[s])[i * pitch + c] = (uint8_t)code;
+                else ((uint16_t *)codes[s])[i * pitch + c] = (uint16_t)code;
+                gains[s][i * pitch + c] = gh;
+            }
+        }
+    }
+    free(prot);
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Decoder assembly (eq. parallel_stage_decode, eq. protected_8bit_scatter). */
+/* ------------------------------------------------------------------------ */
+
+/* W_hat[i][j] = sum over stages of gain_s * D_s(code_s)[j], as an fmaf chain
+ * over s from +0 (each stage decoded independently, then summed); protected
+ * columns are then overwritten with q8 * scale. */
+int orc_decode(int d, int stages, const float *const *tables,
+               int64_t d_out, int64_t d_in, int64_t pitch,
+               const void *const *codes, const uint16_t *const *gains,
+               const int32_t *idx, const int8_t *q8, const float *scale, int64_t k,
+               float *w_hat, int nthreads)
+{
+    if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    if (d_in % d != 0) return ORC_ERR_ARG;
+    int64_t C = d_in / d;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 16)
+#endif
+    for (int64_t i = 0; i < d_out; ++i) {
+        for (int64_t c = 0; c < C; ++c) {
+            for (int j = 0; j < d; ++j) {
+                float v = 0.0f;
+                for (int s = 0; s < stages; ++s) {
+                    uint32_t code = (d <= 8) ? ((const uint8_t *)codes[s])[i * pitch + c]
+                                             : ((const uint16_t *)codes[s])[i * pitch + c];
+                    float a = orc_f16_to_f32(gains[s][i * pitch + c]);
+                    v = fmaf(a, tables[s][(size_t)code * d + j], v);
+                }
+                w_hat[i * d_in + c * d + j] = v;
+            }
+        }
+        for (int64_t p = 0; p < k; ++p)
+            w_hat[i * d_in + idx[p]] = (float)q8[i * k + p] * scale[p];
+    }
+    return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Fused product route, fp64: y_i = sum_c sum_s gain * <D_s(code), x~_c>      */
+/*   + sum_p scale_p q8_ip x_{idx_p} + sum_r B_ir (A x)_r                     */
+/* x~ is x with the protected positions zeroed. This route never forms W_hat. */
+/* ------------------------------------------------------------------------ */
+int orc_gemv_fused(int d, int stages, const float *const *tables,
+                   int64_t d_out, int64_t d_in, int64_t pitch,
+                   const void *const *codes, const uint16_t *const *gains,
+                   const int32_t *idx, const int8_t *q8, const float *scale, int64_t k,
+                   const double *x, int rank, const double *A, const double *B,
+                   double *y, int nthreads)
+{
+    if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    int64_t C = d_in / d;
+    double *xt = (double *)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
+    double t[64];
+    if (!xt || rank > 64) { free(xt); return ORC_ERR_ARG; }
+    for (int64_t j = 0; j < d_in; ++j) xt[j] = x[j];
+    for (int64_t p = 0; p < k; ++p) xt[idx[p]] = 0.0;
+    for (int r = 0; r < rank; ++r) {
+        double acc = 0.0;
+        for (int64_t j = 0; j < d_in; ++j) acc += A[(int64_t)r * d_in + j] * x[j];
+        t[r] = acc;
+    }
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 16)
+#endif
+    for (int64_t i = 0; i < d_out; ++i) {
+        double acc = 0.0;
+        for (int64_t c = 0; c < C; ++c) {
+            for (int s = 0; s < stages; ++s) {
+                uint32_t code = (d <= 8) ? ((const uint8_t *)codes[s])[i * pitch + c]
+                                         : ((const uint16_t *)codes[s])[i * pitch + c];
+                double a = (double)orc_f16_to_f32(gains[s][i * pitch + c]);
+                const float *yv = tables[s] + (size_t)code * d;
+                double dot = 0.0;
+                for (int j = 0; j < d; ++j) dot += (double)yv[j] * xt[c * d + j];
+                acc += a * dot;
+            }
+        }
+        for (int64_t p = 0; p < k; ++p)
+            acc += (double)scale[p] * (double)q8[i * k + p] * x[idx[p]];
+        for (int r = 0; r < rank; ++r) acc += B[i * rank + r] * t[r];
+        y[i] = acc;
+    }
+    free(xt);
+    return ORC_OK;
+}
+
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
