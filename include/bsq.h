@@ -1,0 +1,232 @@
+/*
+ * bsq.h -- C ABI of libbsq.so, an MI355X (gfx950) implementation of the
+ * binary spherical (BSQ) weight codec of BiSCo-LLM and of the products that
+ * consume its bit-packed sign streams.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers named "device" point into GPU memory owned by the caller; the
+ *   library never allocates, frees or retains memory. Host structs are read
+ *   during the call only.
+ * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *   Every entry point that launches work is asynchronous on that stream.
+ * - Arguments are validated on the host before anything is launched; a
+ *   non-BSQ_OK return means nothing was enqueued. Device-side conditions
+ *   (non-finite input) are reported through a device error word that the
+ *   caller reads after synchronising.
+ * - No C++ exception crosses this boundary.
+ * - Calls are re-entrant; two calls that share an output or workspace buffer
+ *   on different streams race.
+ *
+ * Data layout of an encoded matrix W [d_out][d_in] (row-major)
+ * ------------------------------------------------------------
+ * chunk (i, c) = W[i, c*d : (c+1)*d], C = d_in / d chunks per row, and every
+ * row is padded to `pitch` = roundup(C, 16) chunks (padding: code 0, gain +0).
+ *   codes[s]   uint8 (d = 8) or uint16 little-endian (d = 16), [d_out][pitch]:
+ *              bit j of a code is 1 iff element j of the stage target is >= 0
+ *              (+0 and -0 give 1), element j -> bit j (LSB first);
+ *   gains[s]   fp16 bits, [d_out][pitch]: per-chunk least-squares gain of
+ *              stage s (round to nearest even, finite overflow saturated);
+ *   prot_idx   int32 [k], the protected input columns in ascending order;
+ *   prot_q8    int8  [d_out][k], symmetric int8 codes of those columns;
+ *   prot_scale fp32  [k], one scale per protected column.
+ * A stack of n_mats matrices of one shape stores these arrays back to back,
+ * matrix-major ([n_mats][...]).
+ */
+#ifndef BSQ_H
+#define BSQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BSQ_ABI_VERSION 1
+#define BSQ_MAX_STAGES 4
+#define BSQ_PITCH_ALIGN 16
+#define BSQ_MAX_HIDDEN 64
+#define BSQ_MAX_LORA_RANK 16
+#define BSQ_MAX_GROUP 8
+
+typedef enum {
+    BSQ_OK = 0,
+    BSQ_ERR_ARG = 1,              /* null pointer or value out of range */
+    BSQ_ERR_SHAPE = 2,            /* d_in not a multiple of d, empty where not allowed, ... */
+    BSQ_ERR_DTYPE = 3,            /* unsupported element type for this argument */
+    BSQ_ERR_ALIGN = 4,            /* a buffer is not aligned as documented */
+    BSQ_ERR_BUFFER_TOO_SMALL = 5, /* workspace or codec buffer smaller than required */
+    BSQ_ERR_NONFINITE = 6,        /* bit 0 of a device error word: NaN/Inf in the input */
+    BSQ_ERR_DEVICE = 7,           /* a HIP launch or runtime call failed */
+    BSQ_ERR_UNSUPPORTED = 8       /* valid configuration that this build does not implement */
+} bsq_status;
+
+typedef enum { BSQ_F32 = 0, BSQ_BF16 = 1 } bsq_dtype;
+
+/* Decoder families of the paper's codec ablation (Section IV-D, Table
+ * "BSQ codec components"): identity (y = q), linear, and the compact
+ * symmetric decoder without residual blocks (one hidden ReLU layer). */
+typedef enum { BSQ_DEC_IDENTITY = 0, BSQ_DEC_LINEAR = 1, BSQ_DEC_MLP = 2 } bsq_dec_kind;
+
+typedef struct {
+    int32_t d;           /* chunk length: 8 or 16 (Section III-A, codebook_dim) */
+    int32_t b;           /* code bits per stage (codebook_bits); must equal d */
+    int32_t stages;      /* residual stages S, 1..4 (Section III-D; default 2) */
+    int32_t dec_kind;    /* bsq_dec_kind */
+    int32_t hidden;      /* MLP hidden width h, 1..64; ignored for other kinds */
+    int32_t protect_num; /* protected-channel ratio rho = num/den (eq. protected_channel_selection); */
+    int32_t protect_den; /*   num = 0 disables the protected path; k = ceil(d_in*num/den) */
+} bsq_config;
+
+/* Parameters of one stage's decoder, fp32, row-major, device pointers.
+ *   MLP:      W1 [h][b], b1 [h], W2 [d][h], b2 [d];
+ *             y = W2 relu(W1 q + b1) + b2, relu(a) = a > 0 ? a : +0
+ *   LINEAR:   W1 = M [d][b], b1 = beta [d]; y = M q + beta   (W2, b2 unused)
+ *   IDENTITY: y = q                                           (all unused)
+ * with q_j = +-1/sqrt(b) (Section III-C, sphere map and sign binarisation). */
+typedef struct {
+    const float *W1;
+    const float *b1;
+    const float *W2;
+    const float *b2;
+} bsq_decoder;
+
+/* One encoded matrix (or a stack of n_mats of one shape), device pointers.
+ * prot_* may be NULL when k == 0. */
+typedef struct {
+    void *codes[BSQ_MAX_STAGES];
+    uint16_t *gains[BSQ_MAX_STAGES];
+    int32_t *prot_idx;
+    int8_t *prot_q8;
+    float *prot_scale;
+    int64_t d_out;
+    int64_t d_in;
+    int64_t pitch;   /* chunks per row including padding: roundup(d_in/d, 16) */
+    int64_t k;       /* protected columns per matrix */
+    int64_t n_mats;  /* matrices stored back to back; 1 for a single matrix */
+} bsq_layer;
+
+/* Optional LoRA compensation term y += B (A x) (Section III-F). bf16,
+ * device pointers: A [rank][d_in], B [d_out][rank]; rank 1..16. */
+typedef struct {
+    const uint16_t *A;
+    const uint16_t *B;
+    int32_t rank;
+} bsq_lora;
+
+/* Storage accounting of eq. real_size for one matrix:
+ * S_tot = S_code + S_dec + S_8bit + S_LoRA + S_meta (bytes). S_dec counts the
+ * stage decoders once (a model counts them once per category, because every
+ * layer of a category shares them). Buffer sizes include the row padding. */
+typedef struct {
+    int64_t pitch;
+    int64_t k;
+    int64_t chunks;             /* d_out * d_in / d */
+    int64_t code_plane_bytes;   /* one stage's code buffer, padded */
+    int64_t gain_plane_bytes;   /* one stage's gain buffer, padded */
+    int64_t idx_bytes, q8_bytes, scale_bytes;
+    double S_code, S_dec, S_8bit, S_LoRA, S_meta, S_tot;
+    double bpw_nominal;         /* S * b / d (Section III-A) */
+    double bpw_real;            /* 8 * S_tot / (d_out * d_in) */
+} bsq_sizes;
+
+/* Operations for bsq_workspace_bytes. */
+typedef enum { BSQ_OP_ENCODE = 0, BSQ_OP_GEMV = 1, BSQ_OP_GEMM = 2 } bsq_op;
+
+/* ---------------------------------------------------------------------- */
+
+/* Library ABI version (BSQ_ABI_VERSION). */
+int32_t bsq_version(void);
+
+/* Static description of a status code; never NULL. */
+const char *bsq_status_str(int32_t status);
+
+/* Validate a configuration (host only, launches nothing). */
+bsq_status bsq_config_check(const bsq_config *cfg);
+
+/* Sizes of the encoded buffers and the eq. real_size accounting for one
+ * d_out x d_in matrix with an optional LoRA of the given rank (0 = none).
+ * Host only. */
+bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in,
+                           int32_t lora_rank, bsq_sizes *out);
+
+/* Bytes of device workspace an operation needs (host only). For ENCODE,
+ * n_mats is the stack size and M is ignored; for GEMV n_mats is the group
+ * size; for GEMM M is the number of tokens. */
+bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats,
+                               int64_t d_out, int64_t d_in, int64_t M, size_t *bytes);
+
+/* A prepared codec: the stage decoders evaluated on all 2^b codes
+ * (Section III-G, batched parallel residual decoding needs only D_s(code)).
+ * The buffer holds, per stage, an fp32 table [2^b][d] filled in the same fp32
+ * operation order as the encoder's definition (so encode and decode are exact)
+ * and a bf16 copy [2^b][d] for the products. One codec per (category, stage
+ * set) serves every layer of that category.
+ * bsq_codec_bytes: required size (host only).
+ * bsq_codec_prepare: `dec` is a host array of `stages` bsq_decoder structs
+ * whose tensors are device pointers; `codec` is a device buffer of at least
+ * bsq_codec_bytes, 256-byte aligned. Asynchronous on `stream`. */
+bsq_status bsq_codec_bytes(const bsq_config *cfg, size_t *bytes);
+bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec,
+                             void *codec, size_t codec_bytes, void *stream);
+
+/* Encode n_mats matrices of one shape (Sections III-C to III-E):
+ * protected-column scores key_j = g_j^2 sum_i W_ij^2 (fp64, rows in order),
+ * TopK with ties to the lower column, int8 quantisation of those columns, then
+ * per chunk and stage: sign code, decoded vector D_s(code), least-squares fp16
+ * gain over the unprotected positions, residual update (fmaf chains in element
+ * order). The outputs are bit-identical to the definition.
+ *   W      device, bf16 or fp32, [n_mats][d_out][d_in] row-major, 16-byte aligned
+ *   g      device fp32 [n_mats][d_in] activation statistic, or NULL for ones
+ *   out    host struct of device output buffers sized by bsq_layer_sizes
+ *          (times n_mats); out->d_out/d_in/pitch/k/n_mats must match
+ *   err    device int32 error word; the caller zeroes it before the call; the
+ *          library ORs 1 into it when W holds NaN or Inf (BSQ_ERR_NONFINITE)
+ *   ws     device workspace of bsq_workspace_bytes(ENCODE) bytes, 256-aligned */
+bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype,
+                      int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
+                      const bsq_layer *out, int32_t *err, void *ws, size_t ws_bytes,
+                      void *stream);
+
+/* Decode (eq. parallel_stage_decode, eq. protected_8bit_scatter):
+ * W_hat[i][j] = sum_s gain_s * D_s(code_s)[j] as an fmaf chain over the stages
+ * in fp32, then W_hat[:, idx_p] = q8[:, p] * scale_p. Bit-identical to the
+ * definition for BSQ_F32 output; BSQ_BF16 rounds that value to nearest even.
+ *   W_hat  device [n_mats][d_out][d_in] of out_dtype, 16-byte aligned */
+bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
+                      void *W_hat, int32_t out_dtype, void *stream);
+
+/* Fused decode-GEMV for a group of n matrices that read the same x (for
+ * example q/k/v or gate/up), batch 1, without forming W_hat:
+ *   y_g = W_hat_g x + B_g (A_g x)    for g = 0 .. n-1
+ * computed as sum_c sum_s gain * <D_s(code), x~_c> + sum_p q8_p s_p x_{idx_p}
+ * + B (A x), where x~ is x with the protected positions zeroed.
+ *   codecs  host array [n] of prepared codec device pointers (one per category)
+ *   layers  host array [n]; all share d_in (and cfg); n_mats must be 1
+ *   loras   host array [n] or NULL; an entry with rank 0 means no LoRA
+ *   x       device [d_in], bf16 or fp32
+ *   y       host array [n] of device outputs [d_out_g], y_dtype (bf16 or fp32)
+ *   ws      device workspace of bsq_workspace_bytes(GEMV, n, max d_out, d_in)
+ * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
+ * fp32 decoder table and fp32 arithmetic throughout. */
+bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
+                    const bsq_layer *layers, const bsq_lora *loras,
+                    const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                    void *ws, size_t ws_bytes, void *stream);
+
+/* Fused decode-GEMM for M tokens (decode one weight tile to bf16 in LDS,
+ * then MFMA), Y = X W_hat^T + (X A^T) B^T:
+ *   X  device bf16 [M][ldx] (ldx >= d_in, multiple of 8)
+ *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
+ *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M) */
+bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
+                    const bsq_lora *lora, const void *X, int32_t x_dtype, int64_t M,
+                    int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,
+                    void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BSQ_H */

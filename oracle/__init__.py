@@ -298,7 +298,7 @@ def sizes(cfg: Config, d_out: int, d_in: int, lora_rank: int = 0) -> dict:
     return dict(S_code=s_code, S_dec=s_dec, S_8bit=s_8bit, S_LoRA=s_lora, S_meta=s_meta,
                 S_tot=tot, chunks=d_out * C, k=k,
                 bpw_nominal=cfg.stages * cfg.b / cfg.d,
-                bpw_real=8 * tot / (d_out * d_in))
+                bpw_real=(8 * tot / (d_out * d_in)) if d_out * d_in else 0.0)
 
 
 # --------------------------------------------------------------------------

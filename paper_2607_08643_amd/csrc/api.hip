@@ -1,0 +1,269 @@
+// C ABI of libbsq.so (include/bsq.h): host-side validation of every argument
+// before anything is launched, then dispatch to the kernels.
+#include <cmath>
+
+#include "bsq_internal.h"
+
+using namespace bsq;
+
+namespace {
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int64_t k_of(const bsq_config &c, int64_t d_in)
+{
+    if (c.protect_num == 0) return 0;
+    return (d_in * c.protect_num + c.protect_den - 1) / c.protect_den;
+}
+
+int64_t pitch_of(const bsq_config &c, int64_t d_in)
+{
+    const int64_t C = d_in / c.d;
+    return (C + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN * BSQ_PITCH_ALIGN;
+}
+
+bsq_status check_cfg(const bsq_config *c)
+{
+    if (!c) return BSQ_ERR_ARG;
+    if (c->d < 1 || c->d > 16 || c->b < 1 || c->b > 16) return BSQ_ERR_ARG;
+    if (c->stages < 1 || c->stages > BSQ_MAX_STAGES) return BSQ_ERR_ARG;
+    if (c->dec_kind < BSQ_DEC_IDENTITY || c->dec_kind > BSQ_DEC_MLP) return BSQ_ERR_ARG;
+    if (c->dec_kind == BSQ_DEC_MLP && (c->hidden < 1 || c->hidden > BSQ_MAX_HIDDEN)) return BSQ_ERR_ARG;
+    if (c->protect_num < 0 || c->protect_den < 1 || c->protect_num > c->protect_den) return BSQ_ERR_ARG;
+    if (c->d != 8 && c->d != 16) return BSQ_ERR_UNSUPPORTED;
+    if (c->b != c->d) return BSQ_ERR_UNSUPPORTED;
+    return BSQ_OK;
+}
+
+bsq_status check_shape(const bsq_config &c, int64_t d_out, int64_t d_in)
+{
+    if (d_out < 0 || d_in < 1) return BSQ_ERR_SHAPE;
+    if (d_in % c.d != 0) return BSQ_ERR_SHAPE;
+    if (d_in > (int64_t(1) << 18) || d_out > (int64_t(1) << 31)) return BSQ_ERR_UNSUPPORTED;
+    return BSQ_OK;
+}
+
+bsq_status check_layer(const bsq_config &c, const bsq_layer *L, bool need_planes)
+{
+    if (!L) return BSQ_ERR_ARG;
+    bsq_status s = check_shape(c, L->d_out, L->d_in);
+    if (s != BSQ_OK) return s;
+    if (L->n_mats < 1) return BSQ_ERR_ARG;
+    if (L->pitch != pitch_of(c, L->d_in)) return BSQ_ERR_ARG;
+    if (L->k != k_of(c, L->d_in)) return BSQ_ERR_ARG;
+    if (need_planes && L->d_out > 0) {
+        for (int i = 0; i < c.stages; ++i) {
+            if (!L->codes[i] || !L->gains[i]) return BSQ_ERR_ARG;
+            if (!aligned(L->codes[i], 16) || !aligned(L->gains[i], 16)) return BSQ_ERR_ALIGN;
+        }
+    }
+    if (L->k > 0 && (!L->prot_idx || !L->prot_scale)) return BSQ_ERR_ARG;
+    if (L->k > 0 && L->d_out > 0 && !L->prot_q8) return BSQ_ERR_ARG;
+    if (L->k > 0 && !aligned(L->prot_idx, 4)) return BSQ_ERR_ALIGN;
+    if (L->k > 0 && !aligned(L->prot_scale, 4)) return BSQ_ERR_ALIGN;
+    return BSQ_OK;
+}
+
+bsq_status check_lora(const bsq_lora *l)
+{
+    if (!l || l->rank == 0) return BSQ_OK;
+    if (l->rank < 0 || l->rank > BSQ_MAX_LORA_RANK) return BSQ_ERR_ARG;
+    if (!l->A || !l->B) return BSQ_ERR_ARG;
+    if (!aligned(l->A, 2) || !aligned(l->B, 2)) return BSQ_ERR_ALIGN;
+    return BSQ_OK;
+}
+
+bsq_status from_hip(hipError_t e) { return e == hipSuccess ? BSQ_OK : BSQ_ERR_DEVICE; }
+
+}  // namespace
+
+extern "C" {
+
+int32_t bsq_version(void) { return BSQ_ABI_VERSION; }
+
+const char *bsq_status_str(int32_t s)
+{
+    switch (s) {
+    case BSQ_OK: return "ok";
+    case BSQ_ERR_ARG: return "invalid argument";
+    case BSQ_ERR_SHAPE: return "invalid shape";
+    case BSQ_ERR_DTYPE: return "unsupported dtype";
+    case BSQ_ERR_ALIGN: return "misaligned buffer";
+    case BSQ_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case BSQ_ERR_NONFINITE: return "non-finite input";
+    case BSQ_ERR_DEVICE: return "device error";
+    case BSQ_ERR_UNSUPPORTED: return "unsupported configuration";
+    default: return "unknown status";
+    }
+}
+
+bsq_status bsq_config_check(const bsq_config *cfg) { return check_cfg(cfg); }
+
+bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, int32_t lora_rank, bsq_sizes *out)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!out) return BSQ_ERR_ARG;
+    if ((s = check_shape(*cfg, d_out, d_in)) != BSQ_OK) return s;
+    if (lora_rank < 0 || lora_rank > BSQ_MAX_LORA_RANK) return BSQ_ERR_ARG;
+    const bsq_config &c = *cfg;
+    const int64_t C = d_in / c.d, k = k_of(c, d_in), P = pitch_of(c, d_in);
+    const int64_t code_bytes = (c.d <= 8) ? 1 : 2;
+    out->pitch = P;
+    out->k = k;
+    out->chunks = d_out * C;
+    out->code_plane_bytes = d_out * P * code_bytes;
+    out->gain_plane_bytes = d_out * P * 2;
+    out->idx_bytes = k * 4;
+    out->q8_bytes = d_out * k;
+    out->scale_bytes = k * 4;
+    int64_t dec_params = 0;
+    if (c.dec_kind == BSQ_DEC_MLP) dec_params = int64_t(c.hidden) * c.b + c.hidden + int64_t(c.d) * c.hidden + c.d;
+    else if (c.dec_kind == BSQ_DEC_LINEAR) dec_params = int64_t(c.d) * c.b + c.d;
+    out->S_code = double(c.stages) * double(d_out) * double(C) * double(c.b) / 8.0;
+    out->S_dec = double(c.stages) * double(dec_params) * 4.0;
+    out->S_8bit = double(d_out) * double(k);
+    out->S_LoRA = 2.0 * double(lora_rank) * double(d_in + d_out);
+    out->S_meta = double(c.stages) * double(d_out) * double(C) * 2.0 + 8.0 * double(k);
+    out->S_tot = out->S_code + out->S_dec + out->S_8bit + out->S_LoRA + out->S_meta;
+    out->bpw_nominal = double(c.stages) * double(c.b) / double(c.d);
+    out->bpw_real = (d_out > 0) ? 8.0 * out->S_tot / (double(d_out) * double(d_in)) : 0.0;
+    return BSQ_OK;
+}
+
+bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats, int64_t d_out, int64_t d_in,
+                               int64_t M, size_t *bytes)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!bytes) return BSQ_ERR_ARG;
+    if ((s = check_shape(*cfg, d_out, d_in)) != BSQ_OK) return s;
+    if (n_mats < 1) return BSQ_ERR_ARG;
+    switch (op) {
+    case BSQ_OP_ENCODE: *bytes = encode_ws_layout(*cfg, n_mats, d_in, nullptr, nullptr); return BSQ_OK;
+    case BSQ_OP_GEMV:
+        if (n_mats > BSQ_MAX_GROUP) return BSQ_ERR_ARG;
+        *bytes = gemv_ws_bytes(*cfg, n_mats, d_in);
+        return BSQ_OK;
+    case BSQ_OP_GEMM:
+        if (M < 0) return BSQ_ERR_ARG;
+        *bytes = gemm_ws_bytes(*cfg, d_in, M);
+        return BSQ_OK;
+    default: return BSQ_ERR_ARG;
+    }
+}
+
+bsq_status bsq_codec_bytes(const bsq_config *cfg, size_t *bytes)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!bytes) return BSQ_ERR_ARG;
+    *bytes = codec_total_bytes(*cfg);
+    return BSQ_OK;
+}
+
+bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec, void *codec, size_t codec_bytes,
+                             void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!codec) return BSQ_ERR_ARG;
+    if (!aligned(codec, 256)) return BSQ_ERR_ALIGN;
+    if (codec_bytes < codec_total_bytes(*cfg)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    if (cfg->dec_kind != BSQ_DEC_IDENTITY) {
+        if (!dec) return BSQ_ERR_ARG;
+        for (int i = 0; i < cfg->stages; ++i) {
+            if (!dec[i].W1 || !dec[i].b1) return BSQ_ERR_ARG;
+            if (cfg->dec_kind == BSQ_DEC_MLP && (!dec[i].W2 || !dec[i].b2)) return BSQ_ERR_ARG;
+        }
+    }
+    bsq_decoder none[BSQ_MAX_STAGES] = {};
+    return from_hip(launch_codec_tables(*cfg, dec ? dec : none, codec, static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype, int64_t n_mats,
+                      int64_t d_out, int64_t d_in, const float *g, const bsq_layer *out, int32_t *err, void *ws,
+                      size_t ws_bytes, void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    const bsq_config &c = *cfg;
+    if (!codec || !out || !err || !ws) return BSQ_ERR_ARG;
+    if (!W && d_out > 0) return BSQ_ERR_ARG;
+    if (w_dtype != BSQ_F32 && w_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if ((s = check_shape(c, d_out, d_in)) != BSQ_OK) return s;
+    if (n_mats < 1) return BSQ_ERR_ARG;
+    if ((s = check_layer(c, out, true)) != BSQ_OK) return s;
+    if (out->d_out != d_out || out->d_in != d_in || out->n_mats != n_mats) return BSQ_ERR_ARG;
+    if (!aligned(W, 16) || !aligned(codec, 256) || !aligned(ws, 256) || !aligned(err, 4)) return BSQ_ERR_ALIGN;
+    if (out->k > 0 && d_in > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
+    if (g && !aligned(g, 4)) return BSQ_ERR_ALIGN;
+    const size_t need = encode_ws_layout(c, n_mats, d_in, nullptr, nullptr);
+    if (ws_bytes < need) return BSQ_ERR_BUFFER_TOO_SMALL;
+    EncodeWs w{};
+    encode_ws_layout(c, n_mats, d_in, static_cast<char *>(ws), &w);
+    return from_hip(launch_encode(c, codec, W, w_dtype, n_mats, d_out, d_in, g, *out, err, w,
+                                  static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer *layer, void *W_hat,
+                      int32_t out_dtype, void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!codec || !layer) return BSQ_ERR_ARG;
+    if (!W_hat && layer->d_out > 0) return BSQ_ERR_ARG;
+    if (out_dtype != BSQ_F32 && out_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if ((s = check_layer(*cfg, layer, true)) != BSQ_OK) return s;
+    if (!aligned(W_hat, 16) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
+    return from_hip(launch_decode(*cfg, codec, *layer, W_hat, out_dtype, static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                    const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                    void *ws, size_t ws_bytes, void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (n < 1 || n > BSQ_MAX_GROUP) return BSQ_ERR_ARG;
+    if (!codecs || !layers || !x || !y || !ws) return BSQ_ERR_ARG;
+    if (x_dtype != BSQ_F32 && x_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if (y_dtype != BSQ_F32 && y_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    for (int m = 0; m < n; ++m) {
+        if ((s = check_layer(*cfg, &layers[m], true)) != BSQ_OK) return s;
+        if (layers[m].n_mats != 1 || layers[m].d_in != layers[0].d_in) return BSQ_ERR_ARG;
+        if (!codecs[m] || (!y[m] && layers[m].d_out > 0)) return BSQ_ERR_ARG;
+        if (!aligned(codecs[m], 256)) return BSQ_ERR_ALIGN;
+        if (!aligned(y[m], y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+        if (loras && (s = check_lora(&loras[m])) != BSQ_OK) return s;
+    }
+    if (!aligned(ws, 256) || !aligned(x, x_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+    if (x_dtype == BSQ_BF16 && layers[0].pitch * cfg->d / 128 > 512) return BSQ_ERR_UNSUPPORTED;
+    if (ws_bytes < gemv_ws_bytes(*cfg, n, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    return from_hip(launch_gemv(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws,
+                                static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer, const bsq_lora *lora,
+                    const void *X, int32_t x_dtype, int64_t M, int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,
+                    void *ws, size_t ws_bytes, void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!codec || !ws || !layer) return BSQ_ERR_ARG;
+    if (M > 0 && (!X || (!Y && layer->d_out > 0))) return BSQ_ERR_ARG;
+    if (x_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if (y_dtype != BSQ_F32 && y_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if ((s = check_layer(*cfg, layer, true)) != BSQ_OK) return s;
+    if (layer->n_mats != 1) return BSQ_ERR_ARG;
+    if ((s = check_lora(lora)) != BSQ_OK) return s;
+    if (M < 0 || ldx < layer->d_in || ldy < layer->d_out || ldx % 8 != 0) return BSQ_ERR_SHAPE;
+    if (!aligned(X, 16) || !aligned(ws, 256) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
+    if (!aligned(Y, y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+    if (ws_bytes < gemm_ws_bytes(*cfg, layer->d_in, M)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    if (layer->k > 4096) return BSQ_ERR_UNSUPPORTED;
+    return from_hip(launch_gemm(*cfg, codec, *layer, lora, X, M, ldx, Y, y_dtype, ldy, ws,
+                                static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

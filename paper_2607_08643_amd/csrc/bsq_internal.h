@@ -1,0 +1,89 @@
+// Internal declarations of libbsq: codec buffer layout, device helpers and
+// the host-side launchers of every kernel. Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/bsq.h"
+
+namespace bsq {
+
+// ---------------------------------------------------------------------------
+// Codec buffer: for each stage an fp32 table [2^b][d] (exact decoder values),
+// then for each stage a bf16 table [2^b][d] (the same values rounded to
+// nearest even, consumed by the products).
+// ---------------------------------------------------------------------------
+inline size_t codec_entries(const bsq_config &c) { return (size_t(1) << c.b) * size_t(c.d); }
+inline size_t codec_tab32_offset(const bsq_config &c, int s) { return size_t(s) * codec_entries(c) * 4; }
+inline size_t codec_tab16_offset(const bsq_config &c, int s)
+{
+    return size_t(c.stages) * codec_entries(c) * 4 + size_t(s) * codec_entries(c) * 2;
+}
+inline size_t codec_total_bytes(const bsq_config &c) { return size_t(c.stages) * codec_entries(c) * 6; }
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ---------------------------------------------------------------------------
+// Device helpers.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
+
+// fp32 -> bf16, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) == 0x7f800000u) return uint16_t((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return uint16_t(u >> 16);
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint16_t h)
+{
+    _Float16 v;
+    __builtin_memcpy(&v, &h, 2);
+    return float(v);
+}
+
+// Gain storage rule: fp16 round to nearest even (hardware conversion in the
+// default rounding mode), finite overflow saturated to +-65504.
+__device__ __forceinline__ uint16_t gain_to_f16(float a)
+{
+    _Float16 h = _Float16(a);
+    uint16_t u;
+    __builtin_memcpy(&u, &h, 2);
+    if ((u & 0x7fffu) == 0x7c00u) u = uint16_t((u & 0x8000u) | 0x7bffu);
+    return u;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (defined in the .hip files; all asynchronous on `st`).
+// ---------------------------------------------------------------------------
+hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, void *codec, hipStream_t st);
+
+struct EncodeWs {
+    double *keys;       // [n_mats][d_in]
+    float *absmax;      // [n_mats][d_in]
+    int32_t *colmap;    // [n_mats][d_in]: protected column -> its position p
+    uint32_t *bitmap;   // [n_mats][words]: bit j set iff column j is protected
+    int64_t words;      // ceil(d_in / 32)
+};
+size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, char *base, EncodeWs *ws);
+hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W, int w_dtype,
+                         int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
+                         const bsq_layer &out, int32_t *err, const EncodeWs &ws, hipStream_t st);
+
+hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
+                         void *w_hat, int out_dtype, hipStream_t st);
+
+size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t d_in);
+hipError_t launch_gemv(const bsq_config &cfg, int n, const void *const *codecs,
+                       const bsq_layer *layers, const bsq_lora *loras, const void *x, int x_dtype,
+                       void *const *y, int y_dtype, void *ws, hipStream_t st);
+
+size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_in, int64_t M);
+hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
+                       const bsq_lora *lora, const void *X, int64_t M, int64_t ldx, void *Y,
+                       int y_dtype, int64_t ldy, void *ws, hipStream_t st);
+
+}  // namespace bsq

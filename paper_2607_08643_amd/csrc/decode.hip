@@ -1,0 +1,158 @@
+// Decoder assembly (eq. parallel_stage_decode and eq. protected_8bit_scatter):
+// every stage is decoded independently from its code plane and the stage
+// terms are summed (the stage index is folded into each thread's work, so the
+// stages decode in parallel rather than one after the other); the protected
+// columns are then taken from the int8 payload. The stage sum is the fmaf
+// chain of the definition, so the fp32 output is bit-identical to it.
+#include "bsq_internal.h"
+
+namespace bsq {
+namespace {
+
+struct DecodeArgs {
+    int64_t d_out, d_in, pitch, C, k, words;
+    const void *codes[BSQ_MAX_STAGES];
+    const uint16_t *gains[BSQ_MAX_STAGES];
+    const float *tab32[BSQ_MAX_STAGES];
+    const int32_t *idx;
+    const int8_t *q8;
+    const float *scale;
+    void *out;
+};
+
+// Position p of column j in the ascending protected list (j is known to be in it).
+__device__ __forceinline__ int find_pos(const int32_t *idx, int64_t k, int32_t j)
+{
+    int64_t lo = 0, hi = k - 1;
+    while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        if (idx[mid] < j) lo = mid + 1;
+        else hi = mid;
+    }
+    return int(lo);
+}
+
+template <int D, int S, bool BF16OUT>
+__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
+{
+    extern __shared__ uint32_t s_mem[];
+    // [words] protected bitmap of this matrix, then (D == 8) the fp32 tables
+    uint32_t *s_bits = s_mem;
+    float *s_tab = reinterpret_cast<float *>(s_mem + ((a.words + 3) & ~int64_t(3)));
+    const int64_t m = blockIdx.y;
+    const int32_t *idx = a.idx ? a.idx + m * a.k : nullptr;
+    if (a.k > 0) {
+        for (int64_t w = threadIdx.x; w < a.words; w += blockDim.x) s_bits[w] = 0u;
+        __syncthreads();
+        for (int64_t p = threadIdx.x; p < a.k; p += blockDim.x) {
+            const int32_t j = idx[p];
+            if (j >= 0 && j < a.d_in) atomicOr(&s_bits[j >> 5], 1u << (j & 31));
+        }
+    }
+    if constexpr (D == 8) {
+        for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
+            int s = e / (256 * 8), r = e - s * 256 * 8;
+            s_tab[e] = a.tab32[s][r];
+        }
+    }
+    __syncthreads();
+
+    const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (gid >= a.d_out * a.C) return;
+    const int64_t i = gid / a.C;
+    const int64_t c = gid - i * a.C;
+    const int64_t plane = (m * a.d_out + i) * a.pitch + c;
+
+    float v[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j) v[j] = 0.0f;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[plane])
+                                       : uint32_t(static_cast<const uint16_t *>(a.codes[s])[plane]);
+        const float g = f16_bits_to_f32(a.gains[s][plane]);
+        const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
+        const float4 *y4 = reinterpret_cast<const float4 *>(y);
+#pragma unroll
+        for (int q = 0; q < D / 4; ++q) {
+            float4 t = y4[q];
+            v[4 * q + 0] = __builtin_fmaf(g, t.x, v[4 * q + 0]);
+            v[4 * q + 1] = __builtin_fmaf(g, t.y, v[4 * q + 1]);
+            v[4 * q + 2] = __builtin_fmaf(g, t.z, v[4 * q + 2]);
+            v[4 * q + 3] = __builtin_fmaf(g, t.w, v[4 * q + 3]);
+        }
+    }
+    if (a.k > 0) {
+        const int64_t col0 = c * D;
+        const uint32_t pm = (s_bits[col0 >> 5] >> (col0 & 31)) & ((1u << D) - 1u);
+        if (pm) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                if (!((pm >> j) & 1u)) continue;
+                const int p = find_pos(idx, a.k, int32_t(col0 + j));
+                v[j] = float(a.q8[(m * a.d_out + i) * a.k + p]) * a.scale[m * a.k + p];
+            }
+        }
+    }
+    const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
+    if constexpr (BF16OUT) {
+        uint16_t h[D];
+#pragma unroll
+        for (int j = 0; j < D; ++j) h[j] = f32_to_bf16(v[j]);
+        uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + o);
+#pragma unroll
+        for (int q = 0; q < D / 8; ++q) dst[q] = reinterpret_cast<const uint4 *>(h)[q];
+    } else {
+        float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + o);
+#pragma unroll
+        for (int q = 0; q < D / 4; ++q) dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+    }
+}
+
+template <int D, bool BF16OUT>
+hipError_t launch_decode_t(int stages, const DecodeArgs &a, int64_t n_mats, hipStream_t st)
+{
+    const int64_t n = a.d_out * a.C;
+    if (n == 0 || n_mats == 0) return hipSuccess;
+    const dim3 grid(unsigned((n + 255) / 256), unsigned(n_mats));
+    const size_t shm = size_t((a.words + 3) & ~int64_t(3)) * 4 + ((D == 8) ? size_t(stages) * 256 * 8 * 4 : 0);
+    switch (stages) {
+    case 1: hipLaunchKernelGGL((decode_kernel<D, 1, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    case 2: hipLaunchKernelGGL((decode_kernel<D, 2, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    case 3: hipLaunchKernelGGL((decode_kernel<D, 3, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    default: hipLaunchKernelGGL((decode_kernel<D, 4, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_layer &L, void *w_hat,
+                         int out_dtype, hipStream_t st)
+{
+    DecodeArgs a{};
+    a.d_out = L.d_out;
+    a.d_in = L.d_in;
+    a.pitch = L.pitch;
+    a.C = L.d_in / cfg.d;
+    a.k = L.k;
+    a.words = (L.k > 0) ? (L.d_in + 31) / 32 : 0;
+    const char *cb = static_cast<const char *>(codec);
+    for (int s = 0; s < cfg.stages; ++s) {
+        a.codes[s] = L.codes[s];
+        a.gains[s] = L.gains[s];
+        a.tab32[s] = reinterpret_cast<const float *>(cb + codec_tab32_offset(cfg, s));
+    }
+    a.idx = L.prot_idx;
+    a.q8 = L.prot_q8;
+    a.scale = L.prot_scale;
+    a.out = w_hat;
+    const bool bf = (out_dtype == BSQ_BF16);
+    if (cfg.d == 8)
+        return bf ? launch_decode_t<8, true>(cfg.stages, a, L.n_mats, st)
+                  : launch_decode_t<8, false>(cfg.stages, a, L.n_mats, st);
+    return bf ? launch_decode_t<16, true>(cfg.stages, a, L.n_mats, st)
+              : launch_decode_t<16, false>(cfg.stages, a, L.n_mats, st);
+}
+
+}  // namespace bsq

@@ -1,0 +1,426 @@
+// Encoder (Sections III-C to III-E): protected-channel scores and TopK, int8
+// quantisation of the protected columns, then per chunk and stage the sign
+// code, the decoded vector, the least-squares fp16 gain and the residual.
+//
+// Every floating-point step follows the canonical order of the definition
+// (fp64 sequential column sums; fmaf chains in element order; IEEE division;
+// round-to-nearest-even fp16), so codes, gains, indices and the int8 payload
+// are bit-identical to it. A stack of n_mats matrices of one category is
+// encoded by the same launches (the category-batched layout of Section III-G),
+// which also gives the sequential column sums enough parallelism.
+#include <type_traits>
+
+#include "bsq_internal.h"
+
+namespace bsq {
+namespace {
+
+constexpr int TOPK_THREADS = 1024;
+
+// ---------------------------------------------------------------------------
+// Column energy key_j = g_j^2 * sum_i w_ij^2 (fp64, rows in order) and the
+// column absmax for Q8. One lane per column: adjacent lanes read adjacent
+// columns of a row, so every row read is coalesced.
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ float load_elem(const T *p);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float *p) { return *p; }
+template <>
+__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p) { return bf16_to_f32(*p); }
+
+template <typename T>
+__global__ __launch_bounds__(256) void colscore_kernel(const T *__restrict__ W, int64_t d_out, int64_t d_in,
+                                                       const float *__restrict__ g, double *__restrict__ keys,
+                                                       float *__restrict__ absmax)
+{
+    const int64_t m = blockIdx.y;
+    const int64_t col = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (col >= d_in) return;
+    const T *p = W + m * d_out * d_in + col;
+    double s = 0.0;
+    float mx = 0.0f;
+    int64_t i = 0;
+    constexpr int U = 16;
+    for (; i + U <= d_out; i += U) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = load_elem<T>(p + (i + u) * d_in);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            double dv = double(v[u]);
+            s = s + dv * dv;
+            float a = __builtin_fabsf(v[u]);
+            if (a > mx) mx = a;
+        }
+    }
+    for (; i < d_out; ++i) {
+        float v = load_elem<T>(p + i * d_in);
+        double dv = double(v);
+        s = s + dv * dv;
+        float a = __builtin_fabsf(v);
+        if (a > mx) mx = a;
+    }
+    if (g) {
+        double gj = double(g[m * d_in + col]);
+        s = (gj * gj) * s;
+    }
+    keys[m * d_in + col] = s;
+    absmax[m * d_in + col] = mx;
+}
+
+// Exclusive prefix sum over a 1024-thread block; returns the block total.
+__device__ int block_exclusive_scan(int v, int *s_wave, int &total)
+{
+    const int t = threadIdx.x, lane = t & 63, w = t >> 6;
+    int x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        int y = __shfl_up(x, o, 64);
+        if (lane >= o) x += y;
+    }
+    if (lane == 63) s_wave[w] = x;
+    __syncthreads();
+    if (t == 0) {
+        int run = 0;
+        for (int i = 0; i < TOPK_THREADS / 64; ++i) {
+            int c = s_wave[i];
+            s_wave[i] = run;
+            run += c;
+        }
+        s_wave[TOPK_THREADS / 64] = run;
+    }
+    __syncthreads();
+    int excl = x - v + s_wave[w];
+    total = s_wave[TOPK_THREADS / 64];
+    __syncthreads();
+    return excl;
+}
+
+// ---------------------------------------------------------------------------
+// P = TopK(key, k), ties to the lower column, stored ascending; also the
+// per-column scale s_p = absmax / 127, the column -> p map and the bitmap of
+// protected columns. One block per matrix: an MSB-first radix select over the
+// 64-bit key patterns (non-negative doubles order like their bit patterns)
+// finds the k-th largest key T; then all keys > T and the lowest-index keys
+// equal to T are compacted in column order.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__restrict__ keys_all,
+                                                            const float *__restrict__ absmax_all,
+                                                            int64_t d_in, int64_t k, int64_t words,
+                                                            int32_t *__restrict__ idx_all,
+                                                            float *__restrict__ scale_all,
+                                                            int32_t *__restrict__ colmap_all,
+                                                            uint32_t *__restrict__ bitmap_all)
+{
+    extern __shared__ uint32_t s_bits[];  // [words]
+    __shared__ uint32_t hist[256];
+    __shared__ unsigned long long s_prefix;
+    __shared__ long long s_remaining;
+    __shared__ int s_wave[TOPK_THREADS / 64 + 1];
+
+    const int64_t m = blockIdx.x;
+    const int t = threadIdx.x;
+    const unsigned long long *keys = reinterpret_cast<const unsigned long long *>(keys_all + m * d_in);
+    const float *absmax = absmax_all + m * d_in;
+    int32_t *idx = idx_all + m * k;
+    float *scale = scale_all + m * k;
+    int32_t *colmap = colmap_all + m * d_in;
+    uint32_t *bitmap = bitmap_all + m * words;
+
+    if (t == 0) {
+        s_prefix = 0ull;
+        s_remaining = k;
+    }
+    unsigned long long mask = 0ull;
+    for (int pass = 0; pass < 8; ++pass) {
+        const int shift = 56 - 8 * pass;
+        for (int b = t; b < 256; b += TOPK_THREADS) hist[b] = 0u;
+        __syncthreads();
+        const unsigned long long prefix = s_prefix;
+        for (int64_t j = t; j < d_in; j += TOPK_THREADS) {
+            unsigned long long u = keys[j];
+            if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255ull], 1u);
+        }
+        __syncthreads();
+        if (t == 0) {
+            long long rem = s_remaining, cum = 0;
+            for (int dgt = 255; dgt >= 0; --dgt) {
+                long long h = hist[dgt];
+                if (cum + h >= rem) {
+                    s_prefix = prefix | (static_cast<unsigned long long>(dgt) << shift);
+                    s_remaining = rem - cum;
+                    break;
+                }
+                cum += h;
+            }
+        }
+        mask |= 255ull << shift;
+        __syncthreads();
+    }
+    const unsigned long long T = s_prefix;
+    const long long need_eq = s_remaining;
+
+    // each thread owns a contiguous run of columns, so scans follow column order
+    const int64_t per = (d_in + TOPK_THREADS - 1) / TOPK_THREADS;
+    const int64_t j0 = t * per, j1 = (j0 + per < d_in) ? j0 + per : d_in;
+    int n_eq = 0;
+    for (int64_t j = j0; j < j1; ++j) n_eq += (keys[j] == T);
+    int tot;
+    int eq_rank = block_exclusive_scan(n_eq, s_wave, tot);
+    int n_sel = 0;
+    {
+        int r = eq_rank;
+        for (int64_t j = j0; j < j1; ++j) {
+            unsigned long long u = keys[j];
+            bool sel = (u > T) || (u == T && r < need_eq);
+            if (u == T) ++r;
+            n_sel += sel;
+        }
+    }
+    int pos = block_exclusive_scan(n_sel, s_wave, tot);
+    for (int64_t w = t; w < words; w += TOPK_THREADS) s_bits[w] = 0u;
+    __syncthreads();
+    {
+        int r = eq_rank;
+        for (int64_t j = j0; j < j1; ++j) {
+            unsigned long long u = keys[j];
+            bool sel = (u > T) || (u == T && r < need_eq);
+            if (u == T) ++r;
+            if (sel) {
+                idx[pos] = int32_t(j);
+                scale[pos] = absmax[j] / 127.0f;
+                colmap[j] = pos;
+                atomicOr(&s_bits[j >> 5], 1u << (j & 31));
+                ++pos;
+            } else {
+                colmap[j] = -1;
+            }
+        }
+    }
+    __syncthreads();
+    for (int64_t w = t; w < words; w += TOPK_THREADS) bitmap[w] = s_bits[w];
+}
+
+// ---------------------------------------------------------------------------
+// Per-chunk encoder. One thread per chunk (padding chunks included, which get
+// code 0 and gain +0).
+// ---------------------------------------------------------------------------
+struct EncodeArgs {
+    const void *W;
+    int64_t d_out, d_in, pitch, C, k, words, total;
+    void *codes[BSQ_MAX_STAGES];
+    uint16_t *gains[BSQ_MAX_STAGES];
+    const float *tab32[BSQ_MAX_STAGES];
+    int8_t *q8;
+    const float *scale;
+    const int32_t *colmap;
+    const uint32_t *bitmap;
+    int32_t *err;
+};
+
+template <int D, int S, typename T>
+__global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
+{
+    extern __shared__ float s_tab[];  // D == 8: [S][256][8]
+    if constexpr (D == 8) {
+        for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
+            int s = e / (256 * 8), r = e - s * 256 * 8;
+            s_tab[e] = a.tab32[s][r];
+        }
+        __syncthreads();
+    }
+    const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (gid >= a.total) return;
+    const int64_t per_mat = a.d_out * a.pitch;
+    const int64_t m = gid / per_mat;
+    const int64_t rem = gid - m * per_mat;
+    const int64_t i = rem / a.pitch;
+    const int64_t c = rem - i * a.pitch;
+    using code_t = typename std::conditional<D == 8, uint8_t, uint16_t>::type;
+
+    if (c >= a.C) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            static_cast<code_t *>(a.codes[s])[gid] = 0;
+            a.gains[s][gid] = 0;
+        }
+        return;
+    }
+
+    // load the chunk
+    float w[D];
+    const T *src = static_cast<const T *>(a.W) + (m * a.d_out + i) * a.d_in + c * D;
+    constexpr int NV = D * int(sizeof(T)) / 16;
+    uint4 raw[NV];
+#pragma unroll
+    for (int v = 0; v < NV; ++v) raw[v] = reinterpret_cast<const uint4 *>(src)[v];
+    if constexpr (sizeof(T) == 4) {
+        const float *f = reinterpret_cast<const float *>(raw);
+#pragma unroll
+        for (int j = 0; j < D; ++j) w[j] = f[j];
+    } else {
+        const uint16_t *h = reinterpret_cast<const uint16_t *>(raw);
+#pragma unroll
+        for (int j = 0; j < D; ++j) w[j] = bf16_to_f32(h[j]);
+    }
+    bool finite = true;
+#pragma unroll
+    for (int j = 0; j < D; ++j) finite &= __builtin_isfinite(w[j]);
+    if (!finite) atomicOr(a.err, 1);
+
+    // protected positions of this chunk: Q8 payload, then masked out of BSQ
+    uint32_t pm = 0;
+    if (a.bitmap) {
+        const int64_t col0 = c * D;
+        pm = (a.bitmap[m * a.words + (col0 >> 5)] >> (col0 & 31)) & ((1u << D) - 1u);
+        if (pm) {
+#pragma unroll
+            for (int j = 0; j < D; ++j) {
+                if (!((pm >> j) & 1u)) continue;
+                const int32_t p = a.colmap[m * a.d_in + col0 + j];
+                const float sc = a.scale[m * a.k + p];
+                int8_t q = 0;
+                if (sc != 0.0f) {
+                    float tq = __builtin_rintf(w[j] / sc);
+                    if (tq > 127.0f) tq = 127.0f;
+                    if (tq < -127.0f) tq = -127.0f;
+                    q = int8_t(tq);
+                }
+                a.q8[(m * a.d_out + i) * a.k + p] = q;
+            }
+        }
+    }
+    float r[D];
+#pragma unroll
+    for (int j = 0; j < D; ++j) r[j] = ((pm >> j) & 1u) ? 0.0f : w[j];
+
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        uint32_t code = 0;
+#pragma unroll
+        for (int j = 0; j < D; ++j) code |= (r[j] >= 0.0f ? 1u : 0u) << j;
+        const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
+        float yv[D];
+        if constexpr (D == 8) {
+            const float4 *y4 = reinterpret_cast<const float4 *>(y);
+            float4 lo = y4[0], hi = y4[1];
+            yv[0] = lo.x; yv[1] = lo.y; yv[2] = lo.z; yv[3] = lo.w;
+            yv[4] = hi.x; yv[5] = hi.y; yv[6] = hi.z; yv[7] = hi.w;
+        } else {
+            const float4 *y4 = reinterpret_cast<const float4 *>(y);
+#pragma unroll
+            for (int v = 0; v < D / 4; ++v) {
+                float4 q = y4[v];
+                yv[4 * v + 0] = q.x; yv[4 * v + 1] = q.y; yv[4 * v + 2] = q.z; yv[4 * v + 3] = q.w;
+            }
+        }
+        float num = 0.0f, den = 0.0f;
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            if ((pm >> j) & 1u) continue;
+            num = __builtin_fmaf(r[j], yv[j], num);
+            den = __builtin_fmaf(yv[j], yv[j], den);
+        }
+        float alpha = (den > 0.0f) ? num / den : 0.0f;
+        if (alpha != alpha) alpha = 0.0f;
+        const uint16_t gh = gain_to_f16(alpha);
+        const float ga = f16_bits_to_f32(gh);
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            if ((pm >> j) & 1u) continue;
+            r[j] = __builtin_fmaf(-ga, yv[j], r[j]);
+        }
+        static_cast<code_t *>(a.codes[s])[gid] = code_t(code);
+        a.gains[s][gid] = gh;
+    }
+}
+
+template <int D, typename T>
+hipError_t launch_encode_chunks(int stages, const EncodeArgs &a, hipStream_t st)
+{
+    const dim3 grid(unsigned((a.total + 255) / 256));
+    const size_t shm = (D == 8) ? size_t(stages) * 256 * 8 * 4 : 0;
+    switch (stages) {
+    case 1: hipLaunchKernelGGL((encode_kernel<D, 1, T>), grid, dim3(256), shm, st, a); break;
+    case 2: hipLaunchKernelGGL((encode_kernel<D, 2, T>), grid, dim3(256), shm, st, a); break;
+    case 3: hipLaunchKernelGGL((encode_kernel<D, 3, T>), grid, dim3(256), shm, st, a); break;
+    default: hipLaunchKernelGGL((encode_kernel<D, 4, T>), grid, dim3(256), shm, st, a); break;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, char *base, EncodeWs *ws)
+{
+    (void)cfg;
+    const int64_t words = (d_in + 31) / 32;
+    size_t off = 0;
+    const size_t o_keys = off;
+    off = align256(off + size_t(n_mats) * d_in * 8);
+    const size_t o_abs = off;
+    off = align256(off + size_t(n_mats) * d_in * 4);
+    const size_t o_map = off;
+    off = align256(off + size_t(n_mats) * d_in * 4);
+    const size_t o_bits = off;
+    off = align256(off + size_t(n_mats) * words * 4);
+    if (ws) {
+        ws->keys = reinterpret_cast<double *>(base + o_keys);
+        ws->absmax = reinterpret_cast<float *>(base + o_abs);
+        ws->colmap = reinterpret_cast<int32_t *>(base + o_map);
+        ws->bitmap = reinterpret_cast<uint32_t *>(base + o_bits);
+        ws->words = words;
+    }
+    return off;
+}
+
+hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W, int w_dtype,
+                         int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
+                         const bsq_layer &out, int32_t *err, const EncodeWs &ws, hipStream_t st)
+{
+    const int64_t k = out.k;
+    hipError_t e = hipSuccess;
+    if (k > 0) {
+        dim3 grid(unsigned((d_in + 255) / 256), unsigned(n_mats));
+        if (w_dtype == BSQ_BF16)
+            hipLaunchKernelGGL(colscore_kernel<uint16_t>, grid, dim3(256), 0, st,
+                               static_cast<const uint16_t *>(W), d_out, d_in, g, ws.keys, ws.absmax);
+        else
+            hipLaunchKernelGGL(colscore_kernel<float>, grid, dim3(256), 0, st,
+                               static_cast<const float *>(W), d_out, d_in, g, ws.keys, ws.absmax);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(ws.words) * 4, st,
+                           ws.keys, ws.absmax, d_in, k, ws.words, out.prot_idx, out.prot_scale, ws.colmap,
+                           ws.bitmap);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    EncodeArgs a{};
+    a.W = W;
+    a.d_out = d_out;
+    a.d_in = d_in;
+    a.pitch = out.pitch;
+    a.C = d_in / cfg.d;
+    a.k = k;
+    a.words = ws.words;
+    a.total = n_mats * d_out * out.pitch;
+    const char *cb = static_cast<const char *>(codec);
+    for (int s = 0; s < cfg.stages; ++s) {
+        a.codes[s] = out.codes[s];
+        a.gains[s] = out.gains[s];
+        a.tab32[s] = reinterpret_cast<const float *>(cb + codec_tab32_offset(cfg, s));
+    }
+    a.q8 = out.prot_q8;
+    a.scale = out.prot_scale;
+    a.colmap = ws.colmap;
+    a.bitmap = (k > 0) ? ws.bitmap : nullptr;
+    a.err = err;
+    if (a.total == 0) return hipSuccess;
+    if (cfg.d == 8)
+        return (w_dtype == BSQ_BF16) ? launch_encode_chunks<8, uint16_t>(cfg.stages, a, st)
+                                     : launch_encode_chunks<8, float>(cfg.stages, a, st);
+    return (w_dtype == BSQ_BF16) ? launch_encode_chunks<16, uint16_t>(cfg.stages, a, st)
+                                 : launch_encode_chunks<16, float>(cfg.stages, a, st);
+}
+
+}  // namespace bsq

@@ -1,0 +1,218 @@
+"""The C ABI without a GPU: the library loads, exports every entry point that
+include/bsq.h declares, sizes its buffers consistently with the oracle's
+storage accounting (eq. real_size), and rejects invalid arguments on the host
+before launching anything (fake, never-dereferenced device pointers)."""
+import ctypes as ct
+import os
+import re
+
+import pytest
+
+import oracle
+import paper_2607_08643_amd as bsq
+from paper_2607_08643_amd import _binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x7F0000000000  # 256-aligned, never dereferenced: every call below fails validation first
+
+
+def header_functions():
+    with open(os.path.join(ROOT, "include", "bsq.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"^[a-z0-9_ ]*?\*?\s*(bsq_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = bsq.lib()
+    names = header_functions()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(L, name), name
+    assert set(names) == set(B.EXPORTS)
+    assert bsq.bsq_version() == 1
+    for s in range(0, 9):
+        assert bsq.status_str(s) != "unknown status"
+    assert bsq.status_str(99) == "unknown status"
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(d=12), bsq.BSQ_ERR_UNSUPPORTED),
+    (dict(d=0), bsq.BSQ_ERR_ARG),
+    (dict(d=17), bsq.BSQ_ERR_ARG),
+    (dict(stages=0), bsq.BSQ_ERR_ARG),
+    (dict(stages=5), bsq.BSQ_ERR_ARG),
+    (dict(kind=3), bsq.BSQ_ERR_ARG),
+    (dict(hidden=0), bsq.BSQ_ERR_ARG),
+    (dict(hidden=65), bsq.BSQ_ERR_ARG),
+    (dict(protect_num=2, protect_den=1), bsq.BSQ_ERR_ARG),
+    (dict(protect_num=-1), bsq.BSQ_ERR_ARG),
+    (dict(protect_den=0), bsq.BSQ_ERR_ARG),
+    (dict(), bsq.BSQ_OK),
+    (dict(d=16, hidden=16), bsq.BSQ_OK),
+    (dict(kind=bsq.DEC_IDENTITY, hidden=0), bsq.BSQ_OK),
+])
+def test_config_validation(kw, status):
+    assert bsq.bsq_config_check(bsq.Config(**kw)) == status
+
+
+def test_code_bits_must_equal_chunk_length():
+    c = bsq.Config().c()
+    c.b = 16
+    assert bsq.lib().bsq_config_check(ct.byref(c)) == bsq.BSQ_ERR_UNSUPPORTED
+
+
+@pytest.mark.parametrize("d", [8, 16])
+@pytest.mark.parametrize("shape", [(4096, 4096), (1024, 4096), (4096, 12288), (25600, 5120), (333, 296), (0, 256)])
+@pytest.mark.parametrize("rank", [0, 16])
+def test_sizes_match_oracle_accounting(d, shape, rank):
+    d_out, d_in = shape
+    if d_in % d:
+        pytest.skip("not chunkable")
+    cfg = bsq.Config(d=d, hidden=d)
+    got = bsq.bsq_layer_sizes(cfg, d_out, d_in, rank)
+    ref = oracle.sizes(oracle.Config(d=d, b=d, stages=2, kind=oracle.KIND_MLP, hidden=d), d_out, d_in, rank)
+    for key in ("S_code", "S_dec", "S_8bit", "S_LoRA", "S_meta", "S_tot", "bpw_nominal"):
+        assert got[key] == pytest.approx(ref[key], rel=0, abs=1e-9), key
+    if d_out:
+        assert got["bpw_real"] == pytest.approx(ref["bpw_real"], rel=1e-12)
+    assert got["pitch"] == oracle.pitch(d_in, d) and got["k"] == ref["k"]
+    assert got["code_plane_bytes"] == d_out * got["pitch"] * (1 if d == 8 else 2)
+
+
+def test_shape_validation():
+    cfg = bsq.Config()
+    with pytest.raises(bsq.BsqError) as e:
+        bsq.bsq_layer_sizes(cfg, 16, 100)  # 100 is not a multiple of 8
+    assert e.value.status == bsq.BSQ_ERR_SHAPE
+    with pytest.raises(bsq.BsqError) as e:
+        bsq.bsq_layer_sizes(cfg, 16, 0)
+    assert e.value.status == bsq.BSQ_ERR_SHAPE
+    with pytest.raises(bsq.BsqError) as e:
+        bsq.bsq_layer_sizes(cfg, -1, 64)
+    assert e.value.status == bsq.BSQ_ERR_SHAPE
+    with pytest.raises(bsq.BsqError) as e:
+        bsq.bsq_layer_sizes(cfg, 16, 64, lora_rank=17)
+    assert e.value.status == bsq.BSQ_ERR_ARG
+
+
+def _fake_layer(cfg, d_out, d_in, n_mats=1, misalign=False):
+    L = B.bsq_layer()
+    for s in range(cfg.stages):
+        L.codes[s] = FAKE + 0x1000 * s + (1 if misalign else 0)
+        L.gains[s] = FAKE + 0x100000 + 0x1000 * s
+    L.prot_idx, L.prot_q8, L.prot_scale = FAKE + 0x200000, FAKE + 0x300000, FAKE + 0x400000
+    L.d_out, L.d_in, L.pitch, L.k, L.n_mats = d_out, d_in, cfg.pitch(d_in), cfg.k(d_in), n_mats
+    return L
+
+
+def _encode(cfg, L, *, W=FAKE, dtype=bsq.BSQ_BF16, n_mats=1, d_out=64, d_in=256, ws_bytes=1 << 30, err=FAKE,
+            ws=FAKE, codec=FAKE):
+    c = cfg.c()
+    return bsq.lib().bsq_encode(ct.byref(c), codec and ct.c_void_p(codec), W and ct.c_void_p(W), dtype, n_mats,
+                                d_out, d_in, None, ct.byref(L) if L is not None else None,
+                                err and ct.c_void_p(err), ws and ct.c_void_p(ws), ws_bytes, None)
+
+
+def test_encode_rejects_before_launch():
+    cfg = bsq.Config()
+    L = _fake_layer(cfg, 64, 256)
+    assert _encode(cfg, L, W=0) == bsq.BSQ_ERR_ARG
+    assert _encode(cfg, None) == bsq.BSQ_ERR_ARG
+    assert _encode(cfg, L, err=0) == bsq.BSQ_ERR_ARG
+    assert _encode(cfg, L, dtype=7) == bsq.BSQ_ERR_DTYPE
+    assert _encode(cfg, L, d_in=250) == bsq.BSQ_ERR_SHAPE
+    assert _encode(cfg, L, d_out=65) == bsq.BSQ_ERR_ARG          # layer shape mismatch
+    assert _encode(cfg, L, n_mats=2) == bsq.BSQ_ERR_ARG
+    assert _encode(cfg, L, W=FAKE + 8) == bsq.BSQ_ERR_ALIGN
+    assert _encode(cfg, L, ws=FAKE + 64) == bsq.BSQ_ERR_ALIGN
+    assert _encode(cfg, _fake_layer(cfg, 64, 256, misalign=True)) == bsq.BSQ_ERR_ALIGN
+    assert _encode(cfg, L, ws_bytes=16) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    bad = _fake_layer(cfg, 64, 256)
+    bad.pitch = 33
+    assert _encode(cfg, bad) == bsq.BSQ_ERR_ARG
+    bad = _fake_layer(cfg, 64, 256)
+    bad.prot_idx = 0
+    assert _encode(cfg, bad) == bsq.BSQ_ERR_ARG
+    bad = _fake_layer(cfg, 64, 256)
+    bad.k = 1
+    assert _encode(cfg, bad) == bsq.BSQ_ERR_ARG
+
+
+def test_decode_gemv_gemm_reject_before_launch():
+    cfg = bsq.Config()
+    c = cfg.c()
+    Lib = bsq.lib()
+    L = _fake_layer(cfg, 64, 256)
+    assert Lib.bsq_decode(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), ct.c_void_p(FAKE), 5, None) == bsq.BSQ_ERR_DTYPE
+    assert Lib.bsq_decode(ct.byref(c), None, ct.byref(L), ct.c_void_p(FAKE), 0, None) == bsq.BSQ_ERR_ARG
+    assert Lib.bsq_decode(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), ct.c_void_p(FAKE + 4), 0, None) == bsq.BSQ_ERR_ALIGN
+    codecs = (ct.c_void_p * 1)(FAKE)
+    layers = (B.bsq_layer * 1)(L)
+    ys = (ct.c_void_p * 1)(FAKE)
+
+    def gemv(n=1, x=FAKE, xd=1, yd=1, ws=FAKE, ws_bytes=1 << 30, loras=None, lay=layers):
+        return Lib.bsq_gemv(ct.byref(c), n, codecs, lay, loras, x and ct.c_void_p(x), xd, ys, yd,
+                            ws and ct.c_void_p(ws), ws_bytes, None)
+    assert gemv(n=0) == bsq.BSQ_ERR_ARG
+    assert gemv(n=9) == bsq.BSQ_ERR_ARG
+    assert gemv(x=0) == bsq.BSQ_ERR_ARG
+    assert gemv(xd=3) == bsq.BSQ_ERR_DTYPE
+    assert gemv(yd=3) == bsq.BSQ_ERR_DTYPE
+    assert gemv(ws_bytes=8) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    assert gemv(ws=FAKE + 16) == bsq.BSQ_ERR_ALIGN
+    assert gemv(loras=(B.bsq_lora * 1)(B.bsq_lora(FAKE, FAKE, 17))) == bsq.BSQ_ERR_ARG
+    assert gemv(loras=(B.bsq_lora * 1)(B.bsq_lora(0, FAKE, 4))) == bsq.BSQ_ERR_ARG
+    stacked = (B.bsq_layer * 1)(_fake_layer(cfg, 64, 256, n_mats=2))
+    assert gemv(lay=stacked) == bsq.BSQ_ERR_ARG
+
+    def gemm(M=16, ldx=256, ldy=64, xd=1, X=FAKE, ws_bytes=1 << 30, lora=None):
+        lo = B.bsq_lora(0, 0, 0) if lora is None else lora
+        return Lib.bsq_gemm(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), ct.byref(lo), X and ct.c_void_p(X), xd, M,
+                            ldx, ct.c_void_p(FAKE), 1, ldy, ct.c_void_p(FAKE), ws_bytes, None)
+    assert gemm(xd=0) == bsq.BSQ_ERR_DTYPE               # X must be bf16
+    assert gemm(M=-1) == bsq.BSQ_ERR_SHAPE
+    assert gemm(ldx=128) == bsq.BSQ_ERR_SHAPE
+    assert gemm(ldx=260) == bsq.BSQ_ERR_SHAPE            # not a multiple of 8
+    assert gemm(ldy=32) == bsq.BSQ_ERR_SHAPE
+    assert gemm(X=FAKE + 2) == bsq.BSQ_ERR_ALIGN
+    assert gemm(ws_bytes=4) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    assert gemm(lora=B.bsq_lora(FAKE, FAKE, 0x7fffffff)) == bsq.BSQ_ERR_ARG
+
+
+def test_codec_prepare_rejects_before_launch():
+    cfg = bsq.Config()
+    c = cfg.c()
+    Lib = bsq.lib()
+    need = bsq.bsq_codec_bytes(cfg)
+    assert need == 2 * 256 * 8 * 6
+    assert bsq.bsq_codec_bytes(bsq.Config(d=16, hidden=16)) == 2 * 65536 * 16 * 6
+    decs = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE)] * 4)
+    assert Lib.bsq_codec_prepare(ct.byref(c), decs, ct.c_void_p(FAKE), need - 1, None) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    assert Lib.bsq_codec_prepare(ct.byref(c), decs, ct.c_void_p(FAKE + 128), need, None) == bsq.BSQ_ERR_ALIGN
+    assert Lib.bsq_codec_prepare(ct.byref(c), None, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
+    nob2 = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, 0)] * 4)
+    assert Lib.bsq_codec_prepare(ct.byref(c), nob2, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
+
+
+def test_workspace_sizes_are_positive_and_grow():
+    cfg = bsq.Config()
+    e1 = bsq.bsq_workspace_bytes(cfg, bsq.OP_ENCODE, 1, 4096, 4096)
+    e8 = bsq.bsq_workspace_bytes(cfg, bsq.OP_ENCODE, 8, 4096, 4096)
+    assert 0 < e1 < e8
+    g1 = bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 1, 4096, 4096)
+    g3 = bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 3, 4096, 4096)
+    assert 0 < g1 < g3
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 4096, 4096, 256) >= 256 * 16 * 4
+    with pytest.raises(bsq.BsqError):
+        bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 9, 4096, 4096)
+    with pytest.raises(bsq.BsqError):
+        bsq.bsq_workspace_bytes(cfg, 7, 1, 4096, 4096)
+
+
+def test_product_path_has_no_cpu_fallback():
+    """The binding imports neither the oracle nor any CPU implementation."""
+    import inspect
+    src = inspect.getsource(B)
+    assert "import oracle" not in src and "from oracle" not in src
+    with open(os.path.join(ROOT, "paper_2607_08643_amd", "__init__.py")) as f:
+        assert "oracle" not in f.read()

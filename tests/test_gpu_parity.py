@@ -1,0 +1,340 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Bar: codes, gains, protected indices, int8 payload and scales bit-exact;
+fp32 decode bit-exact (bf16 decode = the oracle's fp32 value rounded to
+nearest even); products within 2e-2 relative per output for bf16 activations
+and 1e-4 for fp32 activations, each with a floor of 1e-2 * rms(y) for outputs
+that cancel to about zero (the fraction of outputs on the floor is reported).
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_08643_amd as bsq
+import synth
+
+pytestmark = pytest.mark.gpu
+
+OKIND = {bsq.DEC_IDENTITY: oracle.KIND_IDENTITY, bsq.DEC_LINEAR: oracle.KIND_LINEAR, bsq.DEC_MLP: oracle.KIND_MLP}
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def ocfg(cfg: bsq.Config) -> oracle.Config:
+    return oracle.Config(d=cfg.d, b=cfg.d, stages=cfg.stages, kind=OKIND[cfg.kind], hidden=cfg.hidden,
+                         protect_num=cfg.protect_num, protect_den=cfg.protect_den)
+
+
+def np_codes(t):
+    a = t.cpu().numpy()
+    return a.view(np.uint16) if a.dtype == np.int16 else a
+
+
+def np_gains(t):
+    return t.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+def decoders(cfg, seed=7):
+    return synth.decoder_params(cfg.kind, cfg.d, cfg.d, cfg.hidden, cfg.stages, seed=seed)
+
+
+def assert_layer_equal(layer, enc, cfg, m=None):
+    L = layer.mat(m) if m is not None else layer
+    for s in range(cfg.stages):
+        np.testing.assert_array_equal(np_codes(L.codes[s]), enc.codes[s], err_msg=f"codes stage {s}")
+        np.testing.assert_array_equal(np_gains(L.gains[s]), enc.gains[s], err_msg=f"gains stage {s}")
+    if cfg.k(L.d_in):
+        np.testing.assert_array_equal(L.idx.cpu().numpy(), enc.idx, err_msg="protected indices")
+        np.testing.assert_array_equal(L.q8.cpu().numpy(), enc.q8, err_msg="int8 payload")
+        np.testing.assert_array_equal(L.scale.cpu().numpy().view(np.uint32), enc.scale.view(np.uint32),
+                                      err_msg="scales")
+
+
+def check_close(y, y_ref, rel, what):
+    y = np.asarray(y, dtype=np.float64)
+    floor = 1e-2 * np.sqrt(np.mean(y_ref ** 2)) if y_ref.size else 0.0
+    den = np.maximum(np.abs(y_ref), floor)
+    bad = np.abs(y - y_ref) > rel * den
+    on_floor = float(np.mean(np.abs(y_ref) < floor)) if y_ref.size else 0.0
+    worst = float(np.max(np.abs(y - y_ref) / np.maximum(den, 1e-300))) if y_ref.size else 0.0
+    say(f"  {what}: max err/tol-denominator {worst:.2e} (bar {rel:g}), {on_floor:.2%} of outputs on the floor")
+    assert not bad.any(), f"{what}: {int(bad.sum())} outputs outside {rel} (worst {worst:.3e})"
+
+
+# (name, d_out, d_in, cfg kwargs, dtype, n_mats, with_g)
+SMALL = [
+    ("tiny-256x256-fp32-d8", 256, 256, dict(d=8, hidden=8, protect_num=0), torch.float32, 1, False),
+    ("ragged-333x296-d8", 333, 296, dict(d=8, hidden=8), torch.bfloat16, 1, False),
+    ("ragged-77x592-d16", 77, 592, dict(d=16, hidden=16, protect_num=1, protect_den=50), torch.bfloat16, 1, False),
+    ("identity-128x512-d8", 128, 512, dict(d=8, kind=bsq.DEC_IDENTITY, hidden=0), torch.bfloat16, 1, False),
+    ("linear-64x512-d16-3stage", 64, 512, dict(d=16, kind=bsq.DEC_LINEAR, stages=3), torch.float32, 1, False),
+    ("mlp-1stage-200x384-d8", 200, 384, dict(d=8, stages=1, hidden=8), torch.bfloat16, 1, False),
+    ("mlp-4stage-50x1024-d8-h16", 50, 1024, dict(d=8, stages=4, hidden=16), torch.bfloat16, 1, False),
+    ("mlp-h5-96x320-d16", 96, 320, dict(d=16, hidden=5), torch.bfloat16, 1, False),
+    ("stack3-96x1024-d8", 96, 1024, dict(d=8, hidden=8), torch.bfloat16, 3, False),
+    ("stack2-40x640-d16-fp32", 40, 640, dict(d=16, hidden=16), torch.float32, 2, False),
+    ("g-128x640-d8", 128, 640, dict(d=8, hidden=8), torch.bfloat16, 1, True),
+    ("rho25-64x256-d8", 64, 256, dict(d=8, hidden=8, protect_num=1, protect_den=4), torch.bfloat16, 1, False),
+]
+
+
+def _make(name, d_out, d_in, kw, dtype, n_mats, with_g, gpu, seed=11):
+    cfg = bsq.Config(**kw)
+    decs = decoders(cfg, seed)
+    k = cfg.k(d_in)
+    W, _ = synth.weight(d_out, d_in, seed, k_outliers=k, dtype=dtype, device="cpu", n_mats=n_mats)
+    g = None
+    if with_g:
+        g = torch.rand((n_mats, d_in) if n_mats > 1 else (d_in,), generator=torch.Generator().manual_seed(seed)) + 0.5
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W.to(gpu), g=None if g is None else g.to(gpu))
+    torch.cuda.synchronize()
+    Wf = oracle.to_f32(W)
+    oc = ocfg(cfg)
+    tabs = oracle.decoder_table(oc, decs)
+    encs = []
+    for m in range(n_mats):
+        Wm = Wf[m] if n_mats > 1 else Wf
+        gm = None if g is None else (g[m] if n_mats > 1 else g).numpy()
+        encs.append(oracle.encode(oc, decs, Wm, g=gm, tables=tabs))
+    return cfg, decs, codec, layer, W, encs, tabs
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_encode_decode_bit_exact(case, gpu):
+    say(f"case {case[0]}")
+    cfg, decs, codec, layer, W, encs, tabs = _make(*case, gpu)
+    oc = ocfg(cfg)
+    n_mats = case[5]
+    for m, enc in enumerate(encs):
+        assert_layer_equal(layer, enc, cfg, m if n_mats > 1 else None)
+    w32 = bsq.bsq_decode(cfg, codec, layer, dtype=torch.float32)
+    w16 = bsq.bsq_decode(cfg, codec, layer, dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    for m, enc in enumerate(encs):
+        ref = oracle.decode(oc, decs, enc, tables=tabs)
+        got = (w32[m] if n_mats > 1 else w32).cpu().numpy()
+        np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+        got16 = (w16[m] if n_mats > 1 else w16).cpu()
+        ref16 = torch.from_numpy(ref).to(torch.bfloat16)
+        assert torch.equal(got16.view(torch.int16), ref16.view(torch.int16))
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+@pytest.mark.parametrize("with_lora", [False, True], ids=["nolora", "lora"])
+def test_gemv_matches_oracle(case, with_lora, gpu):
+    say(f"case {case[0]} lora={with_lora}")
+    cfg, decs, codec, layer, W, encs, tabs = _make(*case, gpu)
+    oc = ocfg(cfg)
+    name, d_out, d_in, _, dtype, n_mats, _ = case
+    x = synth.activation(d_in, seed=5, dtype=dtype)
+    for m, enc in enumerate(encs):
+        lora = synth.lora(d_out, d_in, 16 if m % 2 == 0 else 3, seed=9 + m) if with_lora else None
+        lora_dev = None if lora is None else (lora[0].to(gpu), lora[1].to(gpu))
+        for ydt in (torch.float32, torch.bfloat16):
+            y = bsq.bsq_gemv(cfg, codec, layer.mat(m), x.to(gpu), loras=lora_dev, y_dtype=ydt)
+            torch.cuda.synchronize()
+            lref = None if lora is None else (oracle.to_f32(lora[0]), oracle.to_f32(lora[1]))
+            y_ref = oracle.gemv(oc, decs, enc, oracle.to_f32(x), lora=lref)
+            rel = 1e-4 if (dtype == torch.float32 and ydt == torch.float32) else 2e-2
+            check_close(y.float().cpu().numpy(), y_ref, rel, f"gemv m={m} y={ydt}")
+
+
+@pytest.mark.parametrize("case", [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11]],
+                         ids=[c[0] for c in (SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11])])
+@pytest.mark.parametrize("M", [1, 5, 16, 64, 100, 256])
+def test_gemm_matches_oracle(case, M, gpu):
+    say(f"case {case[0]} M={M}")
+    cfg, decs, codec, layer, W, encs, tabs = _make(*case, gpu)
+    oc = ocfg(cfg)
+    name, d_out, d_in, _, dtype, n_mats, _ = case
+    X = synth.activation(d_in, seed=6, dtype=torch.bfloat16, batch=M)
+    lora = synth.lora(d_out, d_in, 16, seed=3)
+    Y = bsq.bsq_gemm(cfg, codec, layer, X.to(gpu), lora=(lora[0].to(gpu), lora[1].to(gpu)), y_dtype=torch.float32)
+    Yb = bsq.bsq_gemm(cfg, codec, layer, X.to(gpu), y_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    Xf = oracle.to_f32(X)
+    Y_ref = oracle.gemm(oc, decs, encs[0], Xf, lora=(oracle.to_f32(lora[0]), oracle.to_f32(lora[1])))
+    check_close(Y.cpu().numpy(), Y_ref, 2e-2, "gemm fp32 out")
+    Yb_ref = oracle.gemm(oc, decs, encs[0], Xf)
+    check_close(Yb.float().cpu().numpy(), Yb_ref, 2e-2, "gemm bf16 out")
+
+
+def test_grouped_gemv_three_categories(gpu):
+    """q/k/v-like group: one x, three matrices of different heights, three codecs."""
+    say("grouped qkv-like 320/96/96 x 1024")
+    d_in = 1024
+    outs = [320, 96, 96]
+    cfg = bsq.Config(d=8, hidden=8)
+    oc = ocfg(cfg)
+    x = synth.activation(d_in, seed=1)
+    codecs, layers, encs, decs_all, loras = [], [], [], [], []
+    for i, d_out in enumerate(outs):
+        decs = decoders(cfg, seed=100 + i)
+        W, _ = synth.weight(d_out, d_in, seed=200 + i, k_outliers=cfg.k(d_in))
+        codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+        codecs.append(codec)
+        layers.append(bsq.bsq_encode(cfg, codec, W.to(gpu)))
+        encs.append(oracle.encode(oc, decs, oracle.to_f32(W)))
+        decs_all.append(decs)
+        loras.append(synth.lora(d_out, d_in, 16, seed=300 + i))
+    ys = bsq.bsq_gemv(cfg, codecs, layers, x.to(gpu), loras=[(a.to(gpu), b.to(gpu)) for a, b in loras],
+                      y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    for i in range(3):
+        assert_layer_equal(layers[i], encs[i], cfg)
+        y_ref = oracle.gemv(oc, decs_all[i], encs[i], oracle.to_f32(x),
+                            lora=(oracle.to_f32(loras[i][0]), oracle.to_f32(loras[i][1])))
+        check_close(ys[i].cpu().numpy(), y_ref, 2e-2, f"group member {i}")
+
+
+# ---------------------------------------------------------------- edge cases
+def _encode_both(cfg, W_cpu, gpu, seed=3):
+    decs = decoders(cfg, seed)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W_cpu.to(gpu))
+    torch.cuda.synchronize()
+    enc = oracle.encode(ocfg(cfg), decs, oracle.to_f32(W_cpu))
+    return decs, codec, layer, enc
+
+
+@pytest.mark.parametrize("d", [8, 16])
+def test_edge_values(d, gpu):
+    """All-zero rows, constant blocks, -0.0, fp32 subnormals, huge values that
+    saturate the fp16 gain, tiny values that underflow it, tied columns."""
+    say(f"edge values d={d}")
+    cfg = bsq.Config(d=d, hidden=d, protect_num=1, protect_den=16)
+    r = np.random.default_rng(1)
+    W = r.normal(0, 0.02, (48, 16 * d)).astype(np.float32)
+    W[0] = 0.0
+    W[1] = -0.0
+    W[2] = 0.5
+    W[3, : d] = -0.0
+    W[4] = np.float32(1e-41) * np.sign(r.normal(size=16 * d))          # subnormal
+    W[5] = np.float32(3e38) * np.sign(r.normal(size=16 * d))           # near fp32 max
+    W[6] = np.float32(1e6)                                             # gain saturates at 65504
+    W[7] = np.float32(1e-9) * r.normal(size=16 * d)                    # gain underflows fp16
+    W[:, 5] = W[:, 9]                                                  # tied columns
+    W[:, 17] = 0.0
+    Wt = torch.from_numpy(W)
+    decs, codec, layer, enc = _encode_both(cfg, Wt, gpu)
+    assert_layer_equal(layer, enc, cfg)
+    w32 = bsq.bsq_decode(cfg, codec, layer, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ref = oracle.decode(ocfg(cfg), decs, enc)
+    np.testing.assert_array_equal(w32.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
+def test_all_zero_and_constant_matrices(gpu):
+    say("all-zero and constant matrices")
+    cfg = bsq.Config(d=8, hidden=8)
+    for W in (torch.zeros(64, 512), torch.full((64, 512), 0.25)):
+        decs, codec, layer, enc = _encode_both(cfg, W.to(torch.bfloat16), gpu)
+        assert_layer_equal(layer, enc, cfg)
+        np.testing.assert_array_equal(enc.idx, np.arange(cfg.k(512)))     # ties -> lowest columns
+
+
+def test_empty_matrix_and_empty_batch(gpu):
+    say("d_out = 0 and M = 0")
+    cfg = bsq.Config(d=8, hidden=8)
+    decs, codec, layer, enc = _encode_both(cfg, torch.zeros(0, 512, dtype=torch.bfloat16), gpu)
+    np.testing.assert_array_equal(layer.idx.cpu().numpy(), enc.idx)
+    np.testing.assert_array_equal(layer.scale.cpu().numpy(), enc.scale)
+    y = bsq.bsq_gemv(cfg, codec, layer, synth.activation(512, 1).to(gpu))
+    Y = bsq.bsq_gemm(cfg, codec, layer, torch.zeros(0, 512, dtype=torch.bfloat16, device=gpu))
+    torch.cuda.synchronize()
+    assert y.numel() == 0 and Y.shape == (0, 0)
+    W, _ = synth.weight(32, 512, 2, k_outliers=6)
+    codec2 = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer2 = bsq.bsq_encode(cfg, codec2, W.to(gpu))
+    Y = bsq.bsq_gemm(cfg, codec2, layer2, torch.zeros(0, 512, dtype=torch.bfloat16, device=gpu))
+    torch.cuda.synchronize()
+    assert Y.shape == (0, 32)
+
+
+@pytest.mark.parametrize("bad", [float("nan"), float("inf"), float("-inf")])
+def test_nonfinite_input_sets_error_word(bad, gpu):
+    say(f"non-finite input {bad}")
+    cfg = bsq.Config(d=8, hidden=8)
+    W = torch.randn(16, 256) * 0.02
+    W[3, 77] = bad
+    codec = bsq.bsq_codec_prepare(cfg, decoders(cfg), device=gpu)
+    with pytest.raises(bsq.BsqError) as e:
+        bsq.bsq_encode(cfg, codec, W.to(torch.bfloat16).to(gpu))
+    assert e.value.status == bsq.BSQ_ERR_NONFINITE
+
+
+# ---------------------------------------------------------------- full sizes
+FULL = [
+    ("qwen3-8b-q-4096x4096-d8", 4096, 4096, 8),
+    ("qwen3-8b-q-4096x4096-d16", 4096, 4096, 16),
+    ("qwen3-8b-down-4096x12288-d8", 4096, 12288, 8),
+    ("qwen3-8b-gate-12288x4096-d16", 12288, 4096, 16),
+    ("qwen3-32b-down-5120x25600-d8", 5120, 25600, 8),
+    ("qwen3-32b-gate-25600x5120-d16", 25600, 5120, 16),
+]
+
+
+@pytest.mark.parametrize("case", FULL, ids=[c[0] for c in FULL])
+def test_full_size_encode_and_gemv(case, gpu):
+    """A whole projection at its real shape: every code, gain, index and int8
+    value bit-exact; GEMV (with LoRA) within tolerance on every output."""
+    name, d_out, d_in, d = case
+    say(f"case {name}")
+    cfg = bsq.Config(d=d, hidden=d)
+    oc = ocfg(cfg)
+    decs = decoders(cfg, seed=d)
+    W, cols = synth.weight(d_out, d_in, seed=d_out + d_in, k_outliers=cfg.k(d_in), device=gpu)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W)
+    x = synth.activation(d_in, seed=4, device=gpu)
+    A, Bm = synth.lora(d_out, d_in, 16, seed=5, device=gpu)
+    y = bsq.bsq_gemv(cfg, codec, layer, x, loras=(A, Bm), y_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    Wf = oracle.to_f32(W)
+    enc = oracle.encode(oc, decs, Wf, nthreads=0)
+    np.testing.assert_array_equal(enc.idx, np.asarray(cols))
+    assert_layer_equal(layer, enc, cfg)
+    y_ref = oracle.gemv(oc, decs, enc, oracle.to_f32(x), lora=(oracle.to_f32(A), oracle.to_f32(Bm)))
+    check_close(y.float().cpu().numpy(), y_ref, 2e-2, name)
+
+
+@pytest.mark.parametrize("d", [8, 16])
+def test_full_size_gemm_m256(d, gpu):
+    say(f"qwen3-8b o_proj 4096x4096 gemm M=256 d={d}")
+    cfg = bsq.Config(d=d, hidden=d)
+    oc = ocfg(cfg)
+    decs = decoders(cfg, seed=d)
+    W, _ = synth.weight(4096, 4096, seed=77, k_outliers=cfg.k(4096), device=gpu)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W)
+    X = synth.activation(4096, seed=8, device=gpu, batch=256)
+    A, Bm = synth.lora(4096, 4096, 16, seed=9, device=gpu)
+    Y = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    enc = oracle.encode(oc, decs, oracle.to_f32(W))
+    assert_layer_equal(layer, enc, cfg)
+    Y_ref = oracle.gemm(oc, decs, enc, oracle.to_f32(X), lora=(oracle.to_f32(A), oracle.to_f32(Bm)))
+    check_close(Y.float().cpu().numpy(), Y_ref, 2e-2, "gemm M=256")
+
+
+def test_category_batched_stack_encode(gpu):
+    """Eight k_proj-shaped layers (1024 x 4096) of one category in one encode."""
+    say("stack of 8 x 1024x4096, d=8")
+    cfg = bsq.Config(d=8, hidden=8)
+    oc = ocfg(cfg)
+    decs = decoders(cfg, seed=3)
+    W, _ = synth.weight(1024, 4096, seed=5, k_outliers=cfg.k(4096), device=gpu, n_mats=8)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W)
+    torch.cuda.synchronize()
+    Wf = oracle.to_f32(W)
+    tabs = oracle.decoder_table(oc, decs)
+    for m in range(8):
+        assert_layer_equal(layer, oracle.encode(oc, decs, Wf[m], tables=tabs), cfg, m)
