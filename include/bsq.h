@@ -201,19 +201,42 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
  * example q/k/v or gate/up), batch 1, without forming W_hat:
  *   y_g = W_hat_g x + B_g (A_g x)    for g = 0 .. n-1
  * computed as sum_c sum_s gain * <D_s(code), x~_c> + sum_p q8_p s_p x_{idx_p}
- * + B (A x), where x~ is x with the protected positions zeroed.
+ * + B (A x), where x~ is x with the protected positions zeroed (Section V
+ * names this direct computation from the codes as future work; the stage sum
+ * is eq. parallel_stage_decode, the protected term eq. protected_8bit_scatter,
+ * the LoRA term Section III-F).
  *   codecs  host array [n] of prepared codec device pointers (one per category)
  *   layers  host array [n]; all share d_in (and cfg); n_mats must be 1
  *   loras   host array [n] or NULL; an entry with rank 0 means no LoRA
- *   x       device [d_in], bf16 or fp32
+ *   x       device [d_in], bf16 (16-byte aligned) or fp32 (x_dtype)
  *   y       host array [n] of device outputs [d_out_g], y_dtype (bf16 or fp32)
- *   ws      device workspace of bsq_workspace_bytes(GEMV, n, max d_out, d_in)
+ *   ws      device workspace of bsq_workspace_bytes(GEMV, n, max d_out, d_in),
+ *           256-byte aligned (holds the LoRA vectors A_g x)
  * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
- * fp32 decoder table and fp32 arithmetic throughout. */
+ * fp32 decoder table and fp32 arithmetic throughout.
+ * bsq_gemv = bsq_gemv_prepare followed by bsq_gemv_run on the same stream. */
 bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
                     const bsq_layer *layers, const bsq_lora *loras,
                     const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
                     void *ws, size_t ws_bytes, void *stream);
+
+/* Activation preparation of the GEMV that needs a reduction over all of x:
+ * writes the LoRA vectors t_g = A_g x (fp32, 16 per member) into `ws`.
+ * Launches nothing when no member has a LoRA adapter. Arguments as for
+ * bsq_gemv. (Masking x and scaling the protected activations happen inside
+ * bsq_gemv_run.) */
+bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const bsq_layer *layers,
+                            const bsq_lora *loras, const void *x, int32_t x_dtype,
+                            void *ws, size_t ws_bytes, void *stream);
+
+/* The streaming product of the GEMV, alone: reads x, the code and gain
+ * planes, the int8 payload and LoRA B once, and the LoRA vectors that a
+ * preceding bsq_gemv_prepare (same group, same x) left in `ws` on the same
+ * stream. Limits of the bf16 path: d_in <= 65536 and k <= 4096. */
+bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs,
+                        const bsq_layer *layers, const bsq_lora *loras, const void *x,
+                        int32_t x_dtype, void *const *y, int32_t y_dtype, void *ws,
+                        size_t ws_bytes, void *stream);
 
 /* Fused decode-GEMM for M tokens (decode one weight tile to bf16 in LDS,
  * then MFMA), Y = X W_hat^T + (X A^T) B^T:

@@ -67,7 +67,8 @@ class bsq_sizes(ct.Structure):
 
 
 EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes", "bsq_workspace_bytes",
-           "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemm")
+           "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemv_prepare",
+           "bsq_gemv_run", "bsq_gemm")
 
 _lib = None
 
@@ -93,6 +94,8 @@ def lib():
     L.bsq_encode.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
     L.bsq_decode.argtypes = [P, P, P, P, I32, P]
     L.bsq_gemv.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
+    L.bsq_gemv_prepare.argtypes = [P, I32, P, P, P, I32, P, SZ, P]
+    L.bsq_gemv_run.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
     L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P]
     for f in EXPORTS[2:]:
         getattr(L, f).restype = I32
@@ -369,6 +372,19 @@ class GemvPlan:
         _check(lib().bsq_gemv(ct.byref(self._c), self.n, self._codecs, self._layers, self._loras, _ptr(self.x),
                               self._xd, self._y, self._yd, _ptr(self.ws), self.ws.numel(), _stream(stream)),
                "bsq_gemv")
+        return self.out
+
+    def prepare(self, stream=None):
+        """bsq_gemv_prepare: the LoRA vectors A x (no launch without LoRA)."""
+        _check(lib().bsq_gemv_prepare(ct.byref(self._c), self.n, self._layers, self._loras, _ptr(self.x),
+                                      self._xd, _ptr(self.ws), self.ws.numel(), _stream(stream)),
+               "bsq_gemv_prepare")
+
+    def run(self, stream=None):
+        """bsq_gemv_run: the streaming product over the prepared workspace."""
+        _check(lib().bsq_gemv_run(ct.byref(self._c), self.n, self._codecs, self._layers, self._loras,
+                                  _ptr(self.x), self._xd, self._y, self._yd, _ptr(self.ws), self.ws.numel(),
+                                  _stream(stream)), "bsq_gemv_run")
         return self.out
 
 

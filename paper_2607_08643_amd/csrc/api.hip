@@ -219,29 +219,73 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
     return from_hip(launch_decode(*cfg, codec, *layer, W_hat, out_dtype, static_cast<hipStream_t>(stream)));
 }
 
-bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
-                    const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
-                    void *ws, size_t ws_bytes, void *stream)
+namespace {
+
+bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                      const bsq_lora *loras, int32_t x_dtype, void *const *y, int32_t y_dtype, void *ws,
+                      size_t ws_bytes)
 {
     bsq_status s = check_cfg(cfg);
     if (s != BSQ_OK) return s;
     if (n < 1 || n > BSQ_MAX_GROUP) return BSQ_ERR_ARG;
-    if (!codecs || !layers || !x || !y || !ws) return BSQ_ERR_ARG;
+    if (!layers || !ws) return BSQ_ERR_ARG;
     if (x_dtype != BSQ_F32 && x_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
-    if (y_dtype != BSQ_F32 && y_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if (y && y_dtype != BSQ_F32 && y_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     for (int m = 0; m < n; ++m) {
-        if ((s = check_layer(*cfg, &layers[m], true)) != BSQ_OK) return s;
+        if ((s = check_layer(*cfg, &layers[m], codecs != nullptr)) != BSQ_OK) return s;
         if (layers[m].n_mats != 1 || layers[m].d_in != layers[0].d_in) return BSQ_ERR_ARG;
-        if (!codecs[m] || (!y[m] && layers[m].d_out > 0)) return BSQ_ERR_ARG;
-        if (!aligned(codecs[m], 256)) return BSQ_ERR_ALIGN;
-        if (!aligned(y[m], y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+        if (codecs) {
+            if (!codecs[m]) return BSQ_ERR_ARG;
+            if (!aligned(codecs[m], 256)) return BSQ_ERR_ALIGN;
+        }
+        if (y) {
+            if (!y[m] && layers[m].d_out > 0) return BSQ_ERR_ARG;
+            if (!aligned(y[m], y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+        }
         if (loras && (s = check_lora(&loras[m])) != BSQ_OK) return s;
     }
-    if (!aligned(ws, 256) || !aligned(x, x_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+    if (!aligned(ws, 256)) return BSQ_ERR_ALIGN;
     if (x_dtype == BSQ_BF16 && layers[0].pitch * cfg->d / 128 > 512) return BSQ_ERR_UNSUPPORTED;
+    if (x_dtype == BSQ_BF16 && layers[0].k > 4096) return BSQ_ERR_UNSUPPORTED;
     if (ws_bytes < gemv_ws_bytes(*cfg, n, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
-    return from_hip(launch_gemv(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws,
-                                static_cast<hipStream_t>(stream)));
+    return BSQ_OK;
+}
+
+}  // namespace
+
+bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const bsq_layer *layers, const bsq_lora *loras,
+                            const void *x, int32_t x_dtype, void *ws, size_t ws_bytes, void *stream)
+{
+    bsq_status s = check_gemv(cfg, n, nullptr, layers, loras, x_dtype, nullptr, BSQ_F32, ws, ws_bytes);
+    if (s != BSQ_OK) return s;
+    if (!x) return BSQ_ERR_ARG;
+    if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+    return from_hip(launch_gemv_prep(*cfg, n, layers, loras, x, x_dtype, ws, static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                        const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                        void *ws, size_t ws_bytes, void *stream)
+{
+    if (!codecs || !y || !x) return BSQ_ERR_ARG;
+    bsq_status s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, y, y_dtype, ws, ws_bytes);
+    if (s != BSQ_OK) return s;
+    if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
+    return from_hip(launch_gemv_run(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                    const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                    void *ws, size_t ws_bytes, void *stream)
+{
+    if (!codecs || !y || !x) return BSQ_ERR_ARG;
+    bsq_status s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, y, y_dtype, ws, ws_bytes);
+    if (s != BSQ_OK) return s;
+    if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((s = from_hip(launch_gemv_prep(*cfg, n, layers, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
+    return from_hip(launch_gemv_run(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws, st));
 }
 
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer, const bsq_lora *lora,

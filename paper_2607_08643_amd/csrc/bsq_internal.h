@@ -77,9 +77,11 @@ hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_lay
                          void *w_hat, int out_dtype, hipStream_t st);
 
 size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t d_in);
-hipError_t launch_gemv(const bsq_config &cfg, int n, const void *const *codecs,
-                       const bsq_layer *layers, const bsq_lora *loras, const void *x, int x_dtype,
-                       void *const *y, int y_dtype, void *ws, hipStream_t st);
+hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const bsq_layer *layers, const bsq_lora *loras,
+                            const void *x, int x_dtype, void *ws, hipStream_t st);
+hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
+                           const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
+                           void *ws, hipStream_t st);
 
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_in, int64_t M);
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &layer,

@@ -201,7 +201,7 @@ def test_workspace_sizes_are_positive_and_grow():
     assert 0 < e1 < e8
     g1 = bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 1, 4096, 4096)
     g3 = bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 3, 4096, 4096)
-    assert 0 < g1 < g3
+    assert 0 < g1 <= g3 and g3 >= 3 * 16 * 4
     assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 4096, 4096, 256) >= 256 * 16 * 4
     with pytest.raises(bsq.BsqError):
         bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 9, 4096, 4096)
