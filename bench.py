@@ -337,9 +337,11 @@ def cpu_baseline(blk, torch):
                        protect_num=cfg.protect_num, protect_den=cfg.protect_den)
     ci = [p.name for p in blk.projs].index("q")
     decs = synth.decoder_params(synth.DEC_MLP, cfg.d, cfg.d, cfg.d, 2, seed=synth.BASE_SEED, category=ci)
-    codes = [c.cpu().numpy().view(np.uint16) if c.dtype == torch.int16 else c.cpu().numpy() for c in L.codes]
-    gains = [g.cpu().view(torch.int16).numpy().view(np.uint16) for g in L.gains]
-    enc = oracle.Encoded(codes, gains, L.idx.cpu().numpy(), L.q8.cpu().numpy(), L.scale.cpu().numpy(),
+    codes = [L.rowmajor(c).contiguous().cpu().numpy() for c in L.codes]
+    codes = [c.view(np.uint16) if c.dtype == np.int16 else c for c in codes]
+    gains = [L.rowmajor(g).contiguous().cpu().view(torch.int16).numpy().view(np.uint16) for g in L.gains]
+    enc = oracle.Encoded(codes, gains, L.idx.cpu().numpy(), np.ascontiguousarray(L.q8.cpu().numpy()[:, :L.k]),
+                         L.scale.cpu().numpy(),
                          L.pitch, L.d_out, L.d_in)
     x = np.random.default_rng(0).normal(size=L.d_in).astype(np.float32)
     tabs = oracle.decoder_table(oc, decs)

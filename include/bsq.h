@@ -20,16 +20,28 @@
  *
  * Data layout of an encoded matrix W [d_out][d_in] (row-major)
  * ------------------------------------------------------------
- * chunk (i, c) = W[i, c*d : (c+1)*d], C = d_in / d chunks per row, and every
- * row is padded to `pitch` = roundup(C, 16) chunks (padding: code 0, gain +0).
- *   codes[s]   uint8 (d = 8) or uint16 little-endian (d = 16), [d_out][pitch]:
+ * chunk (i, c) = W[i, c*d : (c+1)*d], C = d_in / d chunks per row, every
+ * row is padded to `pitch` = roundup(C, 16) chunks and the rows to a
+ * multiple of 64 (padding: code 0, gain +0). The code and gain planes are
+ * stored in 64-row x 16-chunk tiles:
+ *   element (i, c) is at ((i/64 * pitch/16 + c/16) * 64 + i%64) * 16 + c%16
+ * i.e. [ceil(d_out/64)][pitch/16][64][16], so that 64 rows x 16 chunks are one
+ * contiguous 1 KiB (d = 8) or 2 KiB (d = 16) code tile and 2 KiB gain tile.
+ *   codes[s]   uint8 (d = 8) or uint16 little-endian (d = 16), tiled:
  *              bit j of a code is 1 iff element j of the stage target is >= 0
  *              (+0 and -0 give 1), element j -> bit j (LSB first);
- *   gains[s]   fp16 bits, [d_out][pitch]: per-chunk least-squares gain of
+ *   gains[s]   fp16 bits, tiled: per-chunk least-squares gain of
  *              stage s (round to nearest even, finite overflow saturated);
  *   prot_idx   int32 [k], the protected input columns in ascending order;
- *   prot_q8    int8  [d_out][k], symmetric int8 codes of those columns;
- *   prot_scale fp32  [k], one scale per protected column.
+ *   prot_q8    int8  [d_out][kp], kp = roundup(k, 16), 16-byte aligned:
+ *              row i holds the symmetric int8 codes of row i's k protected
+ *              entries, then kp - k zero bytes;
+ *   prot_scale fp32  [k], one scale per protected column;
+ *   prot_bits  uint32 [pitch * d / 32], bit j%32 of word j/32 set iff input
+ *              column j is protected (the same set as prot_idx, as a bitmap
+ *              over the padded columns; padding bits 0). Derived metadata
+ *              written by bsq_encode so that the products can mask the
+ *              activations with one scalar load per 128 columns.
  * A stack of n_mats matrices of one shape stores these arrays back to back,
  * matrix-major ([n_mats][...]).
  */
@@ -43,7 +55,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 1
+#define BSQ_ABI_VERSION 2
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -93,13 +105,15 @@ typedef struct {
 } bsq_decoder;
 
 /* One encoded matrix (or a stack of n_mats of one shape), device pointers.
- * prot_* may be NULL when k == 0. */
+ * prot_* may be NULL when k == 0; bsq_decode and bsq_gemm do not read
+ * prot_bits (they may receive NULL there). */
 typedef struct {
     void *codes[BSQ_MAX_STAGES];
     uint16_t *gains[BSQ_MAX_STAGES];
     int32_t *prot_idx;
     int8_t *prot_q8;
     float *prot_scale;
+    uint32_t *prot_bits;
     int64_t d_out;
     int64_t d_in;
     int64_t pitch;   /* chunks per row including padding: roundup(d_in/d, 16) */
@@ -125,7 +139,8 @@ typedef struct {
     int64_t chunks;             /* d_out * d_in / d */
     int64_t code_plane_bytes;   /* one stage's code buffer, padded */
     int64_t gain_plane_bytes;   /* one stage's gain buffer, padded */
-    int64_t idx_bytes, q8_bytes, scale_bytes;
+    int64_t idx_bytes, q8_bytes, scale_bytes;  /* q8_bytes = d_out * roundup(k, 16) */
+    int64_t bits_bytes;         /* prot_bits (0 when k == 0); not part of S_tot */
     double S_code, S_dec, S_8bit, S_LoRA, S_meta, S_tot;
     double bpw_nominal;         /* S * b / d (Section III-A) */
     double bpw_real;            /* 8 * S_tot / (d_out * d_in) */
@@ -211,7 +226,10 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
  *   x       device [d_in], bf16 (16-byte aligned) or fp32 (x_dtype)
  *   y       host array [n] of device outputs [d_out_g], y_dtype (bf16 or fp32)
  *   ws      device workspace of bsq_workspace_bytes(GEMV, n, max d_out, d_in),
- *           256-byte aligned (holds the LoRA vectors A_g x)
+ *           256-byte aligned, ZERO-FILLED before its first use: it holds the
+ *           LoRA vectors A_g x and flagged per-row partial sums that every
+ *           call leaves at zero again. Calls that share a workspace must
+ *           not overlap.
  * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
  * fp32 decoder table and fp32 arithmetic throughout.
  * bsq_gemv = bsq_gemv_prepare followed by bsq_gemv_run on the same stream. */

@@ -49,6 +49,7 @@ class bsq_decoder(ct.Structure):
 class bsq_layer(ct.Structure):
     _fields_ = [("codes", ct.c_void_p * MAX_STAGES), ("gains", ct.c_void_p * MAX_STAGES),
                 ("prot_idx", ct.c_void_p), ("prot_q8", ct.c_void_p), ("prot_scale", ct.c_void_p),
+                ("prot_bits", ct.c_void_p),
                 ("d_out", ct.c_int64), ("d_in", ct.c_int64), ("pitch", ct.c_int64), ("k", ct.c_int64),
                 ("n_mats", ct.c_int64)]
 
@@ -61,6 +62,7 @@ class bsq_sizes(ct.Structure):
     _fields_ = [("pitch", ct.c_int64), ("k", ct.c_int64), ("chunks", ct.c_int64),
                 ("code_plane_bytes", ct.c_int64), ("gain_plane_bytes", ct.c_int64),
                 ("idx_bytes", ct.c_int64), ("q8_bytes", ct.c_int64), ("scale_bytes", ct.c_int64),
+                ("bits_bytes", ct.c_int64),
                 ("S_code", ct.c_double), ("S_dec", ct.c_double), ("S_8bit", ct.c_double),
                 ("S_LoRA", ct.c_double), ("S_meta", ct.c_double), ("S_tot", ct.c_double),
                 ("bpw_nominal", ct.c_double), ("bpw_real", ct.c_double)]
@@ -69,6 +71,9 @@ class bsq_sizes(ct.Structure):
 EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes", "bsq_workspace_bytes",
            "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemv_prepare",
            "bsq_gemv_run", "bsq_gemm")
+
+# struct layouts above follow this version of include/bsq.h
+ABI_VERSION = 2
 
 _lib = None
 
@@ -99,6 +104,9 @@ def lib():
     L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P]
     for f in EXPORTS[2:]:
         getattr(L, f).restype = I32
+    if L.bsq_version() != ABI_VERSION:
+        raise ImportError(f"{LIB_PATH} implements ABI version {L.bsq_version()}, these bindings expect "
+                          f"{ABI_VERSION}: rebuild the library")
     _lib = L
     return L
 
@@ -201,9 +209,9 @@ class Codec:
         return self.buf.data_ptr()
 
 
-def _empty_aligned(nbytes: int, device, align: int = 256) -> torch.Tensor:
+def _empty_aligned(nbytes: int, device, align: int = 256, zero: bool = False) -> torch.Tensor:
     """A uint8 device buffer whose data pointer is `align`-byte aligned."""
-    t = torch.empty(nbytes + align, dtype=torch.uint8, device=device)
+    t = (torch.zeros if zero else torch.empty)(nbytes + align, dtype=torch.uint8, device=device)
     off = (-t.data_ptr()) % align
     return t[off:off + nbytes]
 
@@ -245,6 +253,7 @@ class Layer:
     d_out: int
     d_in: int
     n_mats: int = 1
+    bits: torch.Tensor | None = None  # protected-column bitmap, int32 [.., pitch * d / 32]
 
     @property
     def pitch(self) -> int:
@@ -263,8 +272,21 @@ class Layer:
             L.prot_idx = self.idx.data_ptr()
             L.prot_q8 = self.q8.data_ptr()
             L.prot_scale = self.scale.data_ptr()
+            if self.bits is not None:
+                L.prot_bits = self.bits.data_ptr()
         L.d_out, L.d_in, L.pitch, L.k, L.n_mats = self.d_out, self.d_in, self.pitch, self.k, self.n_mats
         return L
+
+    @property
+    def row_groups(self) -> int:
+        return (self.d_out + 63) // 64
+
+    def rowmajor(self, plane):
+        """A tiled plane [.., RG, pitch/16, 64, 16] as row-major [.., d_out, pitch]
+        (a view change for comparisons and host tools; no arithmetic)."""
+        lead = plane.shape[:-4]
+        t = plane.transpose(-3, -2).reshape(*lead, self.row_groups * 64, self.pitch)
+        return t[..., :self.d_out, :]
 
     def mat(self, m: int) -> "Layer":
         """Matrix m of a stack, as a single-matrix layer (views, no copy)."""
@@ -273,30 +295,38 @@ class Layer:
         k = self.k
         return Layer(self.cfg, [c[m] for c in self.codes], [g[m] for g in self.gains],
                      None if k == 0 else self.idx[m], None if k == 0 else self.q8[m],
-                     None if k == 0 else self.scale[m], self.d_out, self.d_in, 1)
+                     None if k == 0 else self.scale[m], self.d_out, self.d_in, 1,
+                     None if (k == 0 or self.bits is None) else self.bits[m])
 
     def nbytes_streamed(self) -> int:
-        """Bytes a product reads from this layer's planes (padded planes, int8
-        payload, scales and indices)."""
-        n = sum(t.numel() * t.element_size() for t in self.codes + self.gains)
+        """Bytes a product reads from this layer: the code and gain planes of
+        the d_out real rows, the int8 payload, scales, indices and bitmap."""
+        per_row = self.pitch * (self.codes[0].element_size() + 2) * self.cfg.stages
+        n = per_row * self.d_out
         if self.k:
-            n += self.q8.numel() + self.scale.numel() * 4 + self.idx.numel() * 4
+            n += self.d_out * self.k + self.scale.numel() * 4 + self.idx.numel() * 4
+            if self.bits is not None:
+                n += self.bits.numel() * 4
         return n
 
 
 def layer_empty(cfg: Config, d_out: int, d_in: int, n_mats: int = 1, device="cuda") -> Layer:
+    """Planes in the tiled layout [n_mats][ceil(d_out/64)][pitch/16][64][16];
+    the int8 payload as [n_mats][d_out][roundup(k, 16)]."""
     P, k = cfg.pitch(d_in), cfg.k(d_in)
     ct_ = torch.uint8 if cfg.d <= 8 else torch.int16
-    shape = (n_mats, d_out, P) if n_mats > 1 else (d_out, P)
+    tiles = ((d_out + 63) // 64, P // 16, 64, 16)
+    shape = ((n_mats,) + tiles) if n_mats > 1 else tiles
     codes = [torch.empty(shape, dtype=ct_, device=device) for _ in range(cfg.stages)]
     gains = [torch.empty(shape, dtype=torch.float16, device=device) for _ in range(cfg.stages)]
-    idx = q8 = scale = None
+    idx = q8 = scale = bits = None
     if k > 0:
         lead = (n_mats,) if n_mats > 1 else ()
         idx = torch.empty(lead + (k,), dtype=torch.int32, device=device)
-        q8 = torch.empty(lead + (d_out, k), dtype=torch.int8, device=device)
+        q8 = torch.empty(lead + (d_out, (k + 15) // 16 * 16), dtype=torch.int8, device=device)
         scale = torch.empty(lead + (k,), dtype=torch.float32, device=device)
-    return Layer(cfg, codes, gains, idx, q8, scale, d_out, d_in, n_mats)
+        bits = torch.empty(lead + (P * cfg.d // 32,), dtype=torch.int32, device=device)
+    return Layer(cfg, codes, gains, idx, q8, scale, d_out, d_in, n_mats, bits)
 
 
 def bsq_encode(cfg: Config, codec: Codec, W: torch.Tensor, g: torch.Tensor | None = None,
@@ -359,7 +389,8 @@ class GemvPlan:
         self.layers, self.codecs, self.loras = layers, codecs, loras
         self.out = out if out is not None else [torch.empty(L.d_out, dtype=y_dtype, device=dev) for L in layers]
         need = bsq_workspace_bytes(cfg, OP_GEMV, n, max(L.d_out for L in layers), layers[0].d_in)
-        self.ws = ws if ws is not None else _empty_aligned(need, dev)
+        # zero-filled once: the kernels leave their arrival counters at zero
+        self.ws = ws if ws is not None else _empty_aligned(need, dev, zero=True)
         self._c = cfg.c()
         self._codecs = (ct.c_void_p * n)(*[cd.ptr() for cd in codecs])
         self._layers = (bsq_layer * n)(*[L.c() for L in layers])

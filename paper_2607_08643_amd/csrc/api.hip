@@ -43,7 +43,7 @@ bsq_status check_shape(const bsq_config &c, int64_t d_out, int64_t d_in)
     return BSQ_OK;
 }
 
-bsq_status check_layer(const bsq_config &c, const bsq_layer *L, bool need_planes)
+bsq_status check_layer(const bsq_config &c, const bsq_layer *L, bool need_planes, bool need_bits)
 {
     if (!L) return BSQ_ERR_ARG;
     bsq_status s = check_shape(c, L->d_out, L->d_in);
@@ -60,7 +60,10 @@ bsq_status check_layer(const bsq_config &c, const bsq_layer *L, bool need_planes
     if (L->k > 0 && (!L->prot_idx || !L->prot_scale)) return BSQ_ERR_ARG;
     if (L->k > 0 && L->d_out > 0 && !L->prot_q8) return BSQ_ERR_ARG;
     if (L->k > 0 && !aligned(L->prot_idx, 4)) return BSQ_ERR_ALIGN;
+    if (L->k > 0 && L->d_out > 0 && !aligned(L->prot_q8, 16)) return BSQ_ERR_ALIGN;
     if (L->k > 0 && !aligned(L->prot_scale, 4)) return BSQ_ERR_ALIGN;
+    if (need_bits && L->k > 0 && !L->prot_bits) return BSQ_ERR_ARG;
+    if (need_bits && L->k > 0 && !aligned(L->prot_bits, 16)) return BSQ_ERR_ALIGN;
     return BSQ_OK;
 }
 
@@ -112,11 +115,12 @@ bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, i
     out->pitch = P;
     out->k = k;
     out->chunks = d_out * C;
-    out->code_plane_bytes = d_out * P * code_bytes;
-    out->gain_plane_bytes = d_out * P * 2;
+    out->code_plane_bytes = plane_elems(d_out, P) * code_bytes;
+    out->gain_plane_bytes = plane_elems(d_out, P) * 2;
     out->idx_bytes = k * 4;
-    out->q8_bytes = d_out * k;
+    out->q8_bytes = d_out * q8_pitch(k);
     out->scale_bytes = k * 4;
+    out->bits_bytes = (k > 0) ? prot_words(P, c.d) * 4 : 0;
     int64_t dec_params = 0;
     if (c.dec_kind == BSQ_DEC_MLP) dec_params = int64_t(c.hidden) * c.b + c.hidden + int64_t(c.d) * c.hidden + c.d;
     else if (c.dec_kind == BSQ_DEC_LINEAR) dec_params = int64_t(c.d) * c.b + c.d;
@@ -143,7 +147,7 @@ bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats
     case BSQ_OP_ENCODE: *bytes = encode_ws_layout(*cfg, n_mats, d_in, nullptr, nullptr); return BSQ_OK;
     case BSQ_OP_GEMV:
         if (n_mats > BSQ_MAX_GROUP) return BSQ_ERR_ARG;
-        *bytes = gemv_ws_bytes(*cfg, n_mats, d_in);
+        *bytes = gemv_ws_bytes(*cfg, n_mats, d_out, d_in);
         return BSQ_OK;
     case BSQ_OP_GEMM:
         if (M < 0) return BSQ_ERR_ARG;
@@ -193,7 +197,7 @@ bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, i
     if (w_dtype != BSQ_F32 && w_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     if ((s = check_shape(c, d_out, d_in)) != BSQ_OK) return s;
     if (n_mats < 1) return BSQ_ERR_ARG;
-    if ((s = check_layer(c, out, true)) != BSQ_OK) return s;
+    if ((s = check_layer(c, out, true, true)) != BSQ_OK) return s;
     if (out->d_out != d_out || out->d_in != d_in || out->n_mats != n_mats) return BSQ_ERR_ARG;
     if (!aligned(W, 16) || !aligned(codec, 256) || !aligned(ws, 256) || !aligned(err, 4)) return BSQ_ERR_ALIGN;
     if (out->k > 0 && d_in > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
@@ -214,7 +218,7 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
     if (!codec || !layer) return BSQ_ERR_ARG;
     if (!W_hat && layer->d_out > 0) return BSQ_ERR_ARG;
     if (out_dtype != BSQ_F32 && out_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
-    if ((s = check_layer(*cfg, layer, true)) != BSQ_OK) return s;
+    if ((s = check_layer(*cfg, layer, true, false)) != BSQ_OK) return s;
     if (!aligned(W_hat, 16) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
     return from_hip(launch_decode(*cfg, codec, *layer, W_hat, out_dtype, static_cast<hipStream_t>(stream)));
 }
@@ -232,7 +236,7 @@ bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codec
     if (x_dtype != BSQ_F32 && x_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     if (y && y_dtype != BSQ_F32 && y_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     for (int m = 0; m < n; ++m) {
-        if ((s = check_layer(*cfg, &layers[m], codecs != nullptr)) != BSQ_OK) return s;
+        if ((s = check_layer(*cfg, &layers[m], codecs != nullptr, codecs != nullptr)) != BSQ_OK) return s;
         if (layers[m].n_mats != 1 || layers[m].d_in != layers[0].d_in) return BSQ_ERR_ARG;
         if (codecs) {
             if (!codecs[m]) return BSQ_ERR_ARG;
@@ -245,9 +249,11 @@ bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codec
         if (loras && (s = check_lora(&loras[m])) != BSQ_OK) return s;
     }
     if (!aligned(ws, 256)) return BSQ_ERR_ALIGN;
-    if (x_dtype == BSQ_BF16 && layers[0].pitch * cfg->d / 128 > 512) return BSQ_ERR_UNSUPPORTED;
+    if (x_dtype == BSQ_BF16 && cfg->d == 16 && layers[0].pitch * cfg->d / 128 > 512) return BSQ_ERR_UNSUPPORTED;
     if (x_dtype == BSQ_BF16 && layers[0].k > 4096) return BSQ_ERR_UNSUPPORTED;
-    if (ws_bytes < gemv_ws_bytes(*cfg, n, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    int64_t max_d_out = 0;
+    for (int m = 0; m < n; ++m) max_d_out = layers[m].d_out > max_d_out ? layers[m].d_out : max_d_out;
+    if (ws_bytes < gemv_ws_bytes(*cfg, n, max_d_out, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
     return BSQ_OK;
 }
 
@@ -298,7 +304,7 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     if (M > 0 && (!X || (!Y && layer->d_out > 0))) return BSQ_ERR_ARG;
     if (x_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     if (y_dtype != BSQ_F32 && y_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
-    if ((s = check_layer(*cfg, layer, true)) != BSQ_OK) return s;
+    if ((s = check_layer(*cfg, layer, true, false)) != BSQ_OK) return s;
     if (layer->n_mats != 1) return BSQ_ERR_ARG;
     if ((s = check_lora(lora)) != BSQ_OK) return s;
     if (M < 0 || ldx < layer->d_in || ldy < layer->d_out || ldx % 8 != 0) return BSQ_ERR_SHAPE;

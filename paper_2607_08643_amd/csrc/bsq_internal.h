@@ -25,6 +25,19 @@ inline size_t codec_total_bytes(const bsq_config &c) { return size_t(c.stages) *
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // ---------------------------------------------------------------------------
+// Tiled plane layout of the code and gain planes: 64-row x 16-chunk tiles,
+// [n_mats][ceil(d_out / 64)][pitch / 16][64][16]. A wave that owns 64 rows
+// and one 16-chunk block reads one contiguous tile with one 16-byte load per
+// lane per code plane (d = 8); a 64-row x 128-input weight tile of the GEMM
+// (d = 8) is exactly one tile.
+// ---------------------------------------------------------------------------
+__host__ __device__ inline int64_t tile_index(int64_t row, int64_t chunk, int64_t pitch)
+{
+    return ((((row >> 6) * (pitch >> 4)) + (chunk >> 4)) << 10) + ((row & 63) << 4) + (chunk & 15);
+}
+__host__ __device__ inline int64_t plane_elems(int64_t d_out, int64_t pitch) { return ((d_out + 63) >> 6) * 64 * pitch; }
+
+// ---------------------------------------------------------------------------
 // Device helpers.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
@@ -65,9 +78,14 @@ struct EncodeWs {
     double *keys;       // [n_mats][d_in]
     float *absmax;      // [n_mats][d_in]
     int32_t *colmap;    // [n_mats][d_in]: protected column -> its position p
-    uint32_t *bitmap;   // [n_mats][words]: bit j set iff column j is protected
-    int64_t words;      // ceil(d_in / 32)
 };
+
+// int8 payload row length: k protected columns padded to a multiple of 16
+// (zero bytes), so that one row is read with 16-byte loads
+__host__ __device__ inline int64_t q8_pitch(int64_t k) { return (k + 15) & ~int64_t(15); }
+
+// 32-bit words of a layer's protected-column bitmap: one bit per padded column
+__host__ __device__ inline int64_t prot_words(int64_t pitch, int d) { return pitch * d / 32; }
 size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, char *base, EncodeWs *ws);
 hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W, int w_dtype,
                          int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
@@ -76,7 +94,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
 hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
                          void *w_hat, int out_dtype, hipStream_t st);
 
-size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t d_in);
+size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in);
 hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const bsq_layer *layers, const bsq_lora *loras,
                             const void *x, int x_dtype, void *ws, hipStream_t st);
 hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,

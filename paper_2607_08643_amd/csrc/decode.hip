@@ -61,7 +61,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     if (gid >= a.d_out * a.C) return;
     const int64_t i = gid / a.C;
     const int64_t c = gid - i * a.C;
-    const int64_t plane = (m * a.d_out + i) * a.pitch + c;
+    const int64_t plane = m * plane_elems(a.d_out, a.pitch) + tile_index(i, c, a.pitch);
 
     float v[D];
 #pragma unroll
@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
             for (int j = 0; j < D; ++j) {
                 if (!((pm >> j) & 1u)) continue;
                 const int p = find_pos(idx, a.k, int32_t(col0 + j));
-                v[j] = float(a.q8[(m * a.d_out + i) * a.k + p]) * a.scale[m * a.k + p];
+                v[j] = float(a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p]) * a.scale[m * a.k + p];
             }
         }
     }

@@ -113,7 +113,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__rest
                                                             int32_t *__restrict__ colmap_all,
                                                             uint32_t *__restrict__ bitmap_all)
 {
-    extern __shared__ uint32_t s_bits[];  // [words]
+    extern __shared__ uint32_t s_bits[];  // [words], the padded columns of one matrix
     __shared__ uint32_t hist[256];
     __shared__ unsigned long long s_prefix;
     __shared__ long long s_remaining;
@@ -230,16 +230,20 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
         }
         __syncthreads();
     }
+    // one thread per element of the tiled planes (padding rows and chunks
+    // included), so consecutive threads write consecutive code and gain words
     const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (gid >= a.total) return;
-    const int64_t per_mat = a.d_out * a.pitch;
+    const int64_t per_mat = plane_elems(a.d_out, a.pitch);
     const int64_t m = gid / per_mat;
-    const int64_t rem = gid - m * per_mat;
-    const int64_t i = rem / a.pitch;
-    const int64_t c = rem - i * a.pitch;
+    const int64_t e = gid - m * per_mat;
+    const int64_t tile = e >> 10;
+    const int64_t nb = a.pitch >> 4;
+    const int64_t i = (tile / nb) * 64 + ((e >> 4) & 63);
+    const int64_t c = (tile % nb) * 16 + (e & 15);
     using code_t = typename std::conditional<D == 8, uint8_t, uint16_t>::type;
 
-    if (c >= a.C) {
+    if (c >= a.C || i >= a.d_out) {
 #pragma unroll
         for (int s = 0; s < S; ++s) {
             static_cast<code_t *>(a.codes[s])[gid] = 0;
@@ -269,6 +273,10 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
     for (int j = 0; j < D; ++j) finite &= __builtin_isfinite(w[j]);
     if (!finite) atomicOr(a.err, 1);
 
+    // zero padding of the row's int8 payload
+    if (c == 0) {
+        for (int64_t p = a.k; p < q8_pitch(a.k); ++p) a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p] = 0;
+    }
     // protected positions of this chunk: Q8 payload, then masked out of BSQ
     uint32_t pm = 0;
     if (a.bitmap) {
@@ -287,7 +295,7 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
                     if (tq < -127.0f) tq = -127.0f;
                     q = int8_t(tq);
                 }
-                a.q8[(m * a.d_out + i) * a.k + p] = q;
+                a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p] = q;
             }
         }
     }
@@ -355,7 +363,6 @@ hipError_t launch_encode_chunks(int stages, const EncodeArgs &a, hipStream_t st)
 size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, char *base, EncodeWs *ws)
 {
     (void)cfg;
-    const int64_t words = (d_in + 31) / 32;
     size_t off = 0;
     const size_t o_keys = off;
     off = align256(off + size_t(n_mats) * d_in * 8);
@@ -363,14 +370,10 @@ size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, cha
     off = align256(off + size_t(n_mats) * d_in * 4);
     const size_t o_map = off;
     off = align256(off + size_t(n_mats) * d_in * 4);
-    const size_t o_bits = off;
-    off = align256(off + size_t(n_mats) * words * 4);
     if (ws) {
         ws->keys = reinterpret_cast<double *>(base + o_keys);
         ws->absmax = reinterpret_cast<float *>(base + o_abs);
         ws->colmap = reinterpret_cast<int32_t *>(base + o_map);
-        ws->bitmap = reinterpret_cast<uint32_t *>(base + o_bits);
-        ws->words = words;
     }
     return off;
 }
@@ -390,9 +393,10 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
             hipLaunchKernelGGL(colscore_kernel<float>, grid, dim3(256), 0, st,
                                static_cast<const float *>(W), d_out, d_in, g, ws.keys, ws.absmax);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(ws.words) * 4, st,
-                           ws.keys, ws.absmax, d_in, k, ws.words, out.prot_idx, out.prot_scale, ws.colmap,
-                           ws.bitmap);
+        const int64_t words = prot_words(out.pitch, cfg.d);
+        hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st,
+                           ws.keys, ws.absmax, d_in, k, words, out.prot_idx, out.prot_scale, ws.colmap,
+                           out.prot_bits);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     EncodeArgs a{};
@@ -402,8 +406,8 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
     a.pitch = out.pitch;
     a.C = d_in / cfg.d;
     a.k = k;
-    a.words = ws.words;
-    a.total = n_mats * d_out * out.pitch;
+    a.words = prot_words(out.pitch, cfg.d);
+    a.total = n_mats * plane_elems(d_out, out.pitch);
     const char *cb = static_cast<const char *>(codec);
     for (int s = 0; s < cfg.stages; ++s) {
         a.codes[s] = out.codes[s];
@@ -413,7 +417,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
     a.q8 = out.prot_q8;
     a.scale = out.prot_scale;
     a.colmap = ws.colmap;
-    a.bitmap = (k > 0) ? ws.bitmap : nullptr;
+    a.bitmap = (k > 0) ? out.prot_bits : nullptr;
     a.err = err;
     if (a.total == 0) return hipSuccess;
     if (cfg.d == 8)

@@ -125,7 +125,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
 #pragma unroll
             for (int j = 0; j < D; ++j) v[j] = 0.0f;
             if (row < a.d_out && c < a.C) {
-                const int64_t off = row * a.pitch + c;
+                const int64_t off = tile_index(row, c, a.pitch);
 #pragma unroll
                 for (int s = 0; s < S; ++s) {
                     const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[off])
@@ -150,7 +150,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
                         for (int j = 0; j < D; ++j) {
                             if (!((pm >> j) & 1u)) continue;
                             const int p = find_pos(a.idx, a.k, int32_t(col0 + j));
-                            v[j] = float(a.q8[row * a.k + p]) * a.scale[p];
+                            v[j] = float(a.q8[row * q8_pitch(a.k) + p]) * a.scale[p];
                         }
                     }
                 }

@@ -23,6 +23,11 @@
 namespace bsq {
 namespace {
 
+// row-lane kernel: polls of a row group's last slice for the other slices'
+// partial sums before it gives up and writes NaN (seconds; never expected)
+constexpr int LANE_SPIN_LIMIT = 1 << 22;
+
+
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c)
@@ -56,8 +61,10 @@ struct GemvMat {
     const uint16_t *A;  // LoRA A [rank][d_in], bf16
     const uint16_t *B;  // LoRA B [d_out][rank], bf16
     int rank;
+    const uint32_t *bits;  // protected-column bitmap [pitch * d / 32]
     int64_t d_out;
-    int64_t block_begin;  // first block of this member in the streaming grid
+    int64_t block_begin;  // first block of this member in the grid
+    int64_t rg_begin;     // row-lane kernel: first 64-row group of this member (partial-sum slots)
     float *t;             // workspace: A x, [16]
     void *y;
 };
@@ -66,6 +73,8 @@ struct GemvArgs {
     GemvMat mat[BSQ_MAX_GROUP];
     int n;
     int64_t d_in, pitch, k, nseg, rs, rpb;
+    int64_t nblk, q;   // row-lane kernel: 16-chunk blocks per row, slices per 64-row group
+    uint64_t *slots;   // row-lane kernel: {flag, partial} [row groups][q - 1][64], zero between calls
     const void *x;
     int x_bf16, y_bf16;
 };
@@ -184,8 +193,29 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
     const GemvMat &M = a.mat[m];
     const int64_t row_begin = (int64_t(blockIdx.x) - M.block_begin) * rpb;
     const int nrows = int((M.d_out - row_begin < rpb) ? (M.d_out - row_begin) : rpb);
+    const int slot = t / nseg, seg = t - slot * nseg;
+    const bool active = slot < rs;
+    constexpr int SEGC = 128 / D;
 
-    // block setup: decoder table, protected bitmap, scaled protected activations
+    // issue this thread's first HBM loads before the block setup: its x
+    // segment and its first two rows (rows i = slot, slot + rs, ...)
+    uint4 xv[16];
+    RowData<D, S> r0, r1;
+    const int64_t j0 = int64_t(seg) * 128;
+    const int nmine = (active && nrows > slot) ? (nrows - slot + rs - 1) / rs : 0;
+    static_assert(SEGC == 8, "the streaming kernel reads one 8-chunk tile block per segment");
+    const int64_t row0 = row_begin + slot;
+    const int64_t base = tile_index(row0, int64_t(seg) * SEGC, a.pitch);
+    if (active) {
+        const uint4 *xp = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(a.x) + j0);
+#pragma unroll
+        for (int q = 0; q < 16; ++q) xv[q] = (j0 + 8 * q < a.d_in) ? xp[q] : make_uint4(0, 0, 0, 0);
+        if (nmine > 0) load_row<D, S>(r0, M, base);
+        if (nmine > 1) load_row<D, S>(r1, M, tile_index(row0 + rs, int64_t(seg) * SEGC, a.pitch));
+    }
+
+    // block setup while the loads are in flight: decoder table, protected
+    // bitmap, scaled protected activations
     if constexpr (D == 8) {
         for (int e = t; e < S * 256; e += NT) s_tab[e] = reinterpret_cast<const uint4 *>(M.tab16[e >> 8])[e & 255];
     }
@@ -204,14 +234,7 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
     }
     __syncthreads();
 
-    const int slot = t / nseg, seg = t - slot * nseg;
-    if (slot < rs) {
-        // x~ segment: 128 bf16 inputs starting at seg * 128, protected positions zeroed
-        uint4 xv[16];
-        const int64_t j0 = int64_t(seg) * 128;
-        const uint4 *xp = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(a.x) + j0);
-#pragma unroll
-        for (int q = 0; q < 16; ++q) xv[q] = (j0 + 8 * q < a.d_in) ? xp[q] : make_uint4(0, 0, 0, 0);
+    if (active) {
         if (a.k > 0) {
 #pragma unroll
             for (int wq = 0; wq < 4; ++wq) {
@@ -231,18 +254,13 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
                 }
             }
         }
-        constexpr int SEGC = 128 / D;
-        const int nmine = (nrows > slot) ? (nrows - slot + rs - 1) / rs : 0;
-        const int64_t base = (row_begin + slot) * a.pitch + int64_t(seg) * SEGC;
-        const int64_t step = int64_t(rs) * a.pitch;
-        RowData<D, S> r0, r1;
-        if (nmine > 0) load_row<D, S>(r0, M, base);
+        // two rows in flight: compute one while the next but one loads
         int i = 0;
         for (; i + 1 < nmine; i += 2) {
-            load_row<D, S>(r1, M, base + int64_t(i + 1) * step);
             s_red[(slot + i * rs) * nseg + seg] = row_dot<D, S>(r0, xv, s_tab, M);
-            if (i + 2 < nmine) load_row<D, S>(r0, M, base + int64_t(i + 2) * step);
+            if (i + 2 < nmine) load_row<D, S>(r0, M, tile_index(row0 + int64_t(i + 2) * rs, int64_t(seg) * SEGC, a.pitch));
             s_red[(slot + (i + 1) * rs) * nseg + seg] = row_dot<D, S>(r1, xv, s_tab, M);
+            if (i + 3 < nmine) load_row<D, S>(r1, M, tile_index(row0 + int64_t(i + 3) * rs, int64_t(seg) * SEGC, a.pitch));
         }
         if (i < nmine) s_red[(slot + i * rs) * nseg + seg] = row_dot<D, S>(r0, xv, s_tab, M);
     }
@@ -257,8 +275,7 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
         float v = 0.0f;
         const float *rp = s_red + r * nseg;
         for (int q = g; q < nseg; q += G) v += rp[q];
-        const int8_t *q8r = M.q8 + row * a.k;
-        for (int64_t p = g; p < a.k; p += G) v = __builtin_fmaf(float(q8r[p]), s_xs[p], v);
+        for (int64_t p = g; p < a.k; p += G) v = __builtin_fmaf(float(M.q8[row * q8_pitch(a.k) + p]), s_xs[p], v);
         for (int q = g; q < M.rank; q += G) v = __builtin_fmaf(bf16_to_f32(M.B[row * M.rank + q]), M.t[q], v);
         for (int o = G >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
         if (g == 0) {
@@ -266,6 +283,310 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
             else static_cast<float *>(M.y)[row] = v;
         }
     }
+}
+
+// ---------------------------------------------------------------------------
+// Row-lane kernel (d = 8, bf16 activations).
+//
+// Tile = 64 rows x 16 chunks (128 inputs), stored contiguously (1 KiB of codes
+// and 2 KiB of gains per stage); the tiles of a 64-row group follow each other
+// in memory. A lane owns one row, so the 128-input activation block of a tile
+// is wave-uniform: it is read with scalar loads, masked in scalar registers
+// with the layer's protected-column bitmap, and is the scalar operand of
+// v_dot2_f32_bf16. Table lookups come from LDS.
+//
+// The grid is many short workgroups rather than a persistent one: a workgroup
+// of four waves owns one slice of 4 * TPW consecutive tiles of one row group,
+// each wave streams its TPW tiles two at a time, and the four wave sums of a
+// row are added in LDS in wave order. Short workgroups let the hardware
+// dispatcher balance the load over the CUs as they free up.
+//
+// The Q slices of a row group are consecutive workgroups. Slices 0 .. Q-2
+// each publish their 64 partial sums together with a ready flag (one 64-bit
+// agent-scope atomic store per lane, so data and flag are seen together) and
+// are done; the last slice polls those slots, adds them in slice order, then
+// its own sum, clears the slots and applies the int8 and LoRA epilogue.
+// Workgroups are dispatched in index order, so the slices it waits for are
+// running or done; a bounded poll turns a never-expected stall into NaN
+// outputs instead of a hang. No counter, no cache-wide writeback or
+// invalidate, and no contributor waits.
+//
+// The tile loop is branch-free around its loads: a conditional load makes
+// the compiler wait for it at once, which would leave one tile in flight.
+// ---------------------------------------------------------------------------
+template <int S>
+struct LaneBlk {
+    uint4 c[S];     // 16 codes of the lane's row
+    uint4 g[S][2];  // 16 fp16 gains
+};
+
+template <int S>
+__device__ __forceinline__ void lane_load(LaneBlk<S> &b, const GemvMat &M, int64_t off)
+{
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        b.c[s] = *reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(M.codes[s]) + off);
+        const uint4 *gp = reinterpret_cast<const uint4 *>(M.gains[s] + off);
+        b.g[s][0] = gp[0];
+        b.g[s][1] = gp[1];
+    }
+}
+
+template <int S>
+__device__ __forceinline__ float lane_block(const LaneBlk<S> &b, const uint32_t (&xm)[64], const uint4 *s_tab,
+                                            float acc)
+{
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const uint32_t cw[4] = {b.c[s].x, b.c[s].y, b.c[s].z, b.c[s].w};
+        const uint32_t gw[8] = {b.g[s][0].x, b.g[s][0].y, b.g[s][0].z, b.g[s][0].w,
+                                b.g[s][1].x, b.g[s][1].y, b.g[s][1].z, b.g[s][1].w};
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) {
+            const uint32_t code = (cw[kk >> 2] >> (8 * (kk & 3))) & 0xffu;
+            const uint4 e = s_tab[s * 256 + code];
+            float dsum = dot2_bf16(e.x, xm[4 * kk + 0], 0.0f);
+            dsum = dot2_bf16(e.y, xm[4 * kk + 1], dsum);
+            dsum = dot2_bf16(e.z, xm[4 * kk + 2], dsum);
+            dsum = dot2_bf16(e.w, xm[4 * kk + 3], dsum);
+            const float g = (kk & 1) ? half_hi(gw[kk >> 1]) : half_lo(gw[kk >> 1]);
+            acc = __builtin_fmaf(g, dsum, acc);
+        }
+    }
+    return acc;
+}
+
+// Zero the protected columns of a 128-input activation block (bits: the
+// layer's bitmap, four words per block), in scalar registers.
+__device__ __forceinline__ void mask_block(uint32_t (&xm)[64], const uint32_t *bits, int64_t b)
+{
+    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+    typedef const u32x4 __attribute__((address_space(4))) *cx4_ptr;
+    const u32x4 bw = ((cx4_ptr)(bits))[b];
+    if (bw[0] | bw[1] | bw[2] | bw[3]) {
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) {
+            const uint32_t cb = (bw[kk >> 2] >> (8 * (kk & 3))) & 0xffu;
+            if (cb) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t b2 = cb >> (2 * q);
+                    xm[4 * kk + q] &= ((b2 & 1u) ? 0u : 0x0000ffffu) | ((b2 & 2u) ? 0u : 0xffff0000u);
+                }
+            }
+        }
+    }
+}
+
+// int8 protected columns, the LoRA term, and the store of one output row.
+// A lane reads its row's int8 codes (padded to 16) with up to eight 16-byte
+// loads issued together, and its LoRA row likewise, so the epilogue costs
+// about one memory round trip per 128 protected columns.
+__device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M, const float *s_xs, int64_t row,
+                                            float acc)
+{
+    if (row >= M.d_out) return;
+    const uint4 *qr = reinterpret_cast<const uint4 *>(M.q8 + row * q8_pitch(a.k));
+    for (int64_t p0 = 0; p0 < a.k; p0 += 128) {
+        uint4 qv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (p0 + 16 * u < a.k) qv[u] = qr[p0 / 16 + u];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            if (p0 + 16 * u >= a.k) break;
+            const uint32_t qw[4] = {qv[u].x, qv[u].y, qv[u].z, qv[u].w};
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int64_t p = p0 + 16 * u + e;
+                if (p < a.k) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), s_xs[p], acc);
+            }
+        }
+    }
+    if (M.rank > 0) {
+        const uint16_t *br = M.B + row * M.rank;
+        uint16_t bq[BSQ_MAX_LORA_RANK];
+#pragma unroll
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bq[q] = (q < M.rank) ? br[q] : uint16_t(0);
+#pragma unroll
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q)
+            if (q < M.rank) acc = __builtin_fmaf(bf16_to_f32(bq[q]), M.t[q], acc);
+    }
+    if (a.y_bf16) static_cast<uint16_t *>(M.y)[row] = f32_to_bf16(acc);
+    else static_cast<float *>(M.y)[row] = acc;
+}
+
+typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef const u32x16 __attribute__((address_space(4))) *cx16_ptr;
+
+// One full tile: its 128 activations by scalar loads, masked, then decoded
+// and dotted.
+template <int S>
+__device__ __forceinline__ float lane_tile(const LaneBlk<S> &t, cx16_ptr xv, const uint32_t *bits, int64_t k,
+                                           int64_t b, const uint4 *s_tab, float acc)
+{
+    uint32_t xm[64];
+#pragma unroll
+    for (int z = 0; z < 4; ++z) {
+        const u32x16 v = xv[4 * b + z];
+#pragma unroll
+        for (int w = 0; w < 16; ++w) xm[16 * z + w] = v[w];
+    }
+    if (k > 0) mask_block(xm, bits, b);
+    return lane_block<S>(t, xm, s_tab, acc);
+}
+
+template <int S, int TPW>
+__global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
+{
+    constexpr int WV = 4, NT = 256;      // waves per workgroup, threads
+    constexpr int PF = TPW < 2 ? TPW : 2;  // tiles in flight per wave
+    extern __shared__ uint4 s_mem[];
+    uint4 *s_tab = s_mem;                                      // [S][256] entries of 8 bf16
+    float *s_red = reinterpret_cast<float *>(s_mem + S * 256);  // [WV][64] wave sums
+    float *s_xs = s_red + WV * 64;                             // [k] scale_p * x_{idx_p}
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+
+    int m = 0;
+    while (m + 1 < a.n && int64_t(blockIdx.x) >= a.mat[m + 1].block_begin) ++m;
+    const GemvMat &M = a.mat[m];
+    const int64_t nblk = a.nblk, Q = a.q;
+    const int64_t unit = int64_t(blockIdx.x) - M.block_begin;  // row group * Q + slice
+    const int64_t rg = unit / Q, q = unit - rg * Q;
+    const int64_t tbase = ((rg * nblk) << 10) + (int64_t(lane) << 4);
+    // this wave's tiles [b0, b1); those whose 128 columns are all real go
+    // through the pipelined loop, a ragged last tile of the row (d_in not a
+    // multiple of 128) is handled after it
+    const int64_t full_blocks = (a.d_in / 8) / 16;
+    const int64_t b0 = (q * WV + wave) * TPW;
+    const int64_t b1 = (b0 + TPW < nblk) ? b0 + TPW : nblk;
+    const int64_t nt = ((b1 < full_blocks) ? b1 : full_blocks) - b0;  // may be <= 0
+    const bool ragged = b0 <= full_blocks && full_blocks < b1;
+
+    // Prologue in a fixed issue order (vector-memory completions are counted
+    // in order): the decoder table straight to LDS by DMA
+    // (global_load_lds_dwordx4, 64 entries per wave instruction), then the
+    // first tiles, so that the wait before the barrier covers the table but
+    // not the tiles. Tile indices are clamped so every load is in bounds and
+    // unconditional (a wave without tiles reloads its row group's first tile).
+    static_assert((S * 256) % NT == 0, "table chunks are shared out evenly");
+#pragma unroll
+    for (int r = 0; r < S * 256 / NT; ++r) {
+        const int c = r * WV + wave;  // 64-entry chunk of the [S][256] table
+        const uint4 *src = reinterpret_cast<const uint4 *>(M.tab16[c >> 2]) + (c & 3) * 64 + lane;
+        __builtin_amdgcn_global_load_lds(src, s_tab + c * 64, 16, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    const int64_t blast = (nt > 0) ? b0 + nt - 1 : 0;
+    LaneBlk<S> buf[PF];
+#pragma unroll
+    for (int u = 0; u < PF; ++u) lane_load<S>(buf[u], M, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
+    __builtin_amdgcn_sched_barrier(0);
+    // protected index and scale of this thread's column, used at the end
+    int32_t pj = -1;
+    float psc = 0.0f;
+    if (a.k > 0) {
+        const int64_t pt = (t < a.k) ? t : a.k - 1;
+        pj = M.idx[pt];
+        psc = M.scale[pt];
+    }
+    // the table is in LDS once at most the tile (and index) loads are
+    // pending; a plain s_barrier (no release fence) lets those stay in flight
+    constexpr int NTILE = PF * 3 * S;
+    constexpr int NIDX = NTILE + 2;
+    if (a.k > 0) __builtin_amdgcn_s_waitcnt((NIDX & 15) | ((NIDX >> 4) << 14) | (7 << 4) | (15 << 8));
+    else __builtin_amdgcn_s_waitcnt((NTILE & 15) | ((NTILE >> 4) << 14) | (7 << 4) | (15 << 8));
+    asm volatile("s_barrier" ::: "memory");
+
+    const cx16_ptr xv = (cx16_ptr)(a.x);
+    float acc = 0.0f;
+    int64_t i = 0;
+    for (; i + 2 * PF <= nt; i += PF) {
+#pragma unroll
+        for (int u = 0; u < PF; ++u) {
+            const int64_t b = b0 + i + u;
+            acc = lane_tile<S>(buf[u], xv, M.bits, a.k, b, s_tab, acc);
+            lane_load<S>(buf[u], M, tbase + ((b + PF) << 10));
+        }
+    }
+    // tail: PF .. 2 PF - 1 tiles left (or fewer than PF if nt < PF)
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+        if (i + u < nt) {
+            const int64_t b = b0 + i + u;
+            acc = lane_tile<S>(buf[u], xv, M.bits, a.k, b, s_tab, acc);
+            if (i + u + PF < nt) lane_load<S>(buf[u], M, tbase + ((b + PF) << 10));
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+        if (i + PF + u < nt) acc = lane_tile<S>(buf[u], xv, M.bits, a.k, b0 + i + PF + u, s_tab, acc);
+    }
+    if (ragged) {
+        const int64_t b = full_blocks;
+        lane_load<S>(buf[0], M, tbase + (b << 10));
+        typedef const uint32_t __attribute__((address_space(4))) *cu32_ptr;
+        const cu32_ptr xw = (cu32_ptr)(a.x);
+        uint32_t xm[64];
+#pragma unroll
+        for (int z = 0; z < 64; ++z) xm[z] = (b * 128 + 2 * z < a.d_in) ? xw[b * 64 + z] : 0u;
+        if (a.k > 0) mask_block(xm, M.bits, b);
+        acc = lane_block<S>(buf[0], xm, s_tab, acc);
+    }
+
+    // scaled protected activations for the epilogue (indices loaded above)
+    if (t < a.k) s_xs[t] = (pj >= 0 && pj < a.d_in) ? psc * load_x(a.x, pj, 1) : 0.0f;
+    for (int64_t p = NT + t; p < a.k; p += NT) {  // more protected columns than threads
+        const int32_t j = M.idx[p];
+        s_xs[p] = (j >= 0 && j < a.d_in) ? M.scale[p] * load_x(a.x, j, 1) : 0.0f;
+    }
+    // the four wave sums of each row, in wave order
+    s_red[wave * 64 + lane] = acc;
+    __syncthreads();
+    if (wave != 0) return;
+    float v = s_red[lane];
+#pragma unroll
+    for (int w = 1; w < WV; ++w) v += s_red[w * 64 + lane];
+    const int64_t row = rg * 64 + lane;
+    if (Q == 1) {
+        lane_finish(a, M, s_xs, row, v);
+        return;
+    }
+    uint64_t *slots = a.slots + (M.rg_begin + rg) * (Q - 1) * 64 + lane;
+    if (q < Q - 1) {
+        __hip_atomic_store(slots + q * 64, (uint64_t(1) << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    float tot = 0.0f;
+    bool timed_out = false;
+    for (int64_t q0 = 0; q0 < Q - 1; q0 += 16) {
+        uint64_t pw[16];
+        for (int spin = 0;; ++spin) {
+            bool ready = true;
+#pragma unroll
+            for (int u = 0; u < 16; ++u) {
+                if (q0 + u < Q - 1) {
+                    pw[u] = __hip_atomic_load(slots + (q0 + u) * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    ready &= (pw[u] >> 32) != 0;
+                }
+            }
+            if (__all(ready)) break;
+            if (spin == LANE_SPIN_LIMIT) {  // never expected: report NaN rather than hang
+                timed_out = true;
+                break;
+            }
+            __builtin_amdgcn_s_sleep(2);
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u)
+            if (q0 + u < Q - 1) tot += __uint_as_float(uint32_t(pw[u]));
+    }
+    tot += v;
+    for (int64_t q0 = 0; q0 < Q - 1; ++q0)
+        __hip_atomic_store(slots + q0 * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    lane_finish(a, M, s_xs, row, timed_out ? __builtin_nanf("") : tot);
 }
 
 // ---------------------------------------------------------------------------
@@ -295,7 +616,7 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
             const int64_t col = c * D + j;
             xv[j] = (a.k > 0 && is_protected(M.idx, a.k, col)) ? 0.0f : x[col];
         }
-        const int64_t off = row * a.pitch + c;
+        const int64_t off = tile_index(row, c, a.pitch);
 #pragma unroll
         for (int s = 0; s < S; ++s) {
             const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(M.codes[s])[off])
@@ -309,7 +630,7 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
         }
     }
     for (int64_t p = lane; p < a.k; p += 64)
-        acc = __builtin_fmaf(float(M.q8[row * a.k + p]), M.scale[p] * x[M.idx[p]], acc);
+        acc = __builtin_fmaf(float(M.q8[row * q8_pitch(a.k) + p]), M.scale[p] * x[M.idx[p]], acc);
     for (int q = lane; q < M.rank; q += 64) acc = __builtin_fmaf(bf16_to_f32(M.B[row * M.rank + q]), M.t[q], acc);
     for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
     if (lane == 0) {
@@ -355,6 +676,8 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
     a.x_bf16 = (x_dtype == BSQ_BF16);
     a.y_bf16 = (y_dtype == BSQ_BF16);
     float *wt = static_cast<float *>(ws);
+    char *wb = static_cast<char *>(ws);
+    a.slots = reinterpret_cast<uint64_t *>(wb + align256(size_t(n) * BSQ_MAX_LORA_RANK * 4));
     for (int m = 0; m < n; ++m) {
         GemvMat &M = a.mat[m];
         const bsq_layer &L = layers[m];
@@ -370,6 +693,7 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
         M.idx = L.prot_idx;
         M.q8 = L.prot_q8;
         M.scale = L.prot_scale;
+        M.bits = L.prot_bits;
         M.rank = 0;
         if (loras && loras[m].rank > 0) {
             M.A = loras[m].A;
@@ -385,11 +709,18 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
 
 }  // namespace
 
-size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t d_in)
+// Row-lane kernel: tiles per wave; a workgroup (4 waves) covers 4 * LANE_TPW
+// tiles, Q = ceil(nblk / (4 * LANE_TPW)) slices per 64-row group.
+constexpr int LANE_TPW = 4;
+
+int64_t lane_slices(int64_t nblk) { return (nblk + 4 * LANE_TPW - 1) / (4 * LANE_TPW); }
+
+size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in)
 {
-    (void)cfg;
-    (void)d_in;
-    return align256(size_t(n) * BSQ_MAX_LORA_RANK * 4);
+    const int64_t rg = n * ((max_d_out + 63) / 64);
+    const int64_t nblk = (d_in / cfg.d + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN;
+    // LoRA vectors, then {flag, partial} slots for all but the last slice
+    return align256(size_t(n) * BSQ_MAX_LORA_RANK * 4) + size_t(rg) * size_t(lane_slices(nblk) - 1) * 64 * 8;
 }
 
 size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_rpb)
@@ -423,6 +754,27 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
     if (x_dtype != BSQ_BF16)
         return (D == 8) ? launch_f32<8>(S, a, rows_total, st) : launch_f32<16>(S, a, rows_total, st);
 
+    if (D == 8) {
+        // row-lane kernel: one workgroup per (64-row group, slice of tiles)
+        a.nblk = a.pitch / 16;
+        a.q = lane_slices(a.nblk);
+        int64_t blocks = 0, rgs = 0;
+        for (int m = 0; m < n; ++m) {
+            const int64_t nrg = (layers[m].d_out + 63) / 64;
+            a.mat[m].block_begin = blocks;
+            a.mat[m].rg_begin = rgs;
+            blocks += nrg * a.q;
+            rgs += nrg;
+        }
+        const size_t shm = size_t(S) * 256 * 16 + 4 * 64 * 4 + size_t(a.k) * 4;
+        switch (S) {
+        case 1: hipLaunchKernelGGL((gemv_lane_kernel<1, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
+        case 2: hipLaunchKernelGGL((gemv_lane_kernel<2, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
+        case 3: hipLaunchKernelGGL((gemv_lane_kernel<3, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
+        default: hipLaunchKernelGGL((gemv_lane_kernel<4, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
+        }
+        return hipGetLastError();
+    }
     const int64_t nseg = a.pitch / (128 / D);
     // block size: the multiple of 64 up to 512 that leaves the fewest idle threads
     int nt = 256;
@@ -452,8 +804,7 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
         blocks += (layers[m].d_out + a.rpb - 1) / a.rpb;
     }
     const size_t shm = gemv_stream_lds_bytes(cfg, a.d_in, a.rpb * nseg);
-    return (D == 8) ? launch_stream<8>(S, a, nt, int(blocks), shm, st)
-                    : launch_stream<16>(S, a, nt, int(blocks), shm, st);
+    return launch_stream<16>(S, a, nt, int(blocks), shm, st);
 }
 
 }  // namespace bsq

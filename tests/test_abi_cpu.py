@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 1
+    assert bsq.bsq_version() == 2
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -76,7 +76,11 @@ def test_sizes_match_oracle_accounting(d, shape, rank):
     if d_out:
         assert got["bpw_real"] == pytest.approx(ref["bpw_real"], rel=1e-12)
     assert got["pitch"] == oracle.pitch(d_in, d) and got["k"] == ref["k"]
-    assert got["code_plane_bytes"] == d_out * got["pitch"] * (1 if d == 8 else 2)
+    rows = (d_out + 63) // 64 * 64   # tiled planes pad the rows to 64
+    assert got["code_plane_bytes"] == rows * got["pitch"] * (1 if d == 8 else 2)
+    assert got["gain_plane_bytes"] == rows * got["pitch"] * 2
+    # one bit per padded input column when there are protected columns
+    assert got["bits_bytes"] == (got["pitch"] * d // 8 if got["k"] else 0)
 
 
 def test_shape_validation():
@@ -101,6 +105,7 @@ def _fake_layer(cfg, d_out, d_in, n_mats=1, misalign=False):
         L.codes[s] = FAKE + 0x1000 * s + (1 if misalign else 0)
         L.gains[s] = FAKE + 0x100000 + 0x1000 * s
     L.prot_idx, L.prot_q8, L.prot_scale = FAKE + 0x200000, FAKE + 0x300000, FAKE + 0x400000
+    L.prot_bits = FAKE + 0x500000
     L.d_out, L.d_in, L.pitch, L.k, L.n_mats = d_out, d_in, cfg.pitch(d_in), cfg.k(d_in), n_mats
     return L
 
@@ -136,6 +141,15 @@ def test_encode_rejects_before_launch():
     bad = _fake_layer(cfg, 64, 256)
     bad.k = 1
     assert _encode(cfg, bad) == bsq.BSQ_ERR_ARG
+    bad = _fake_layer(cfg, 64, 256)
+    bad.prot_bits = 0                                          # the encoder writes the bitmap
+    assert _encode(cfg, bad) == bsq.BSQ_ERR_ARG
+    bad = _fake_layer(cfg, 64, 256)
+    bad.prot_bits = FAKE + 0x500004
+    assert _encode(cfg, bad) == bsq.BSQ_ERR_ALIGN
+    bad = _fake_layer(cfg, 64, 256)
+    bad.prot_q8 = FAKE + 0x300008                              # rows are read with 16-byte loads
+    assert _encode(cfg, bad) == bsq.BSQ_ERR_ALIGN
 
 
 def test_decode_gemv_gemm_reject_before_launch():
@@ -164,6 +178,9 @@ def test_decode_gemv_gemm_reject_before_launch():
     assert gemv(loras=(B.bsq_lora * 1)(B.bsq_lora(0, FAKE, 4))) == bsq.BSQ_ERR_ARG
     stacked = (B.bsq_layer * 1)(_fake_layer(cfg, 64, 256, n_mats=2))
     assert gemv(lay=stacked) == bsq.BSQ_ERR_ARG
+    nobits = _fake_layer(cfg, 64, 256)
+    nobits.prot_bits = 0                                       # the product masks with the bitmap
+    assert gemv(lay=(B.bsq_layer * 1)(nobits)) == bsq.BSQ_ERR_ARG
 
     def gemm(M=16, ldx=256, ldy=64, xd=1, X=FAKE, ws_bytes=1 << 30, lora=None):
         lo = B.bsq_lora(0, 0, 0) if lora is None else lora

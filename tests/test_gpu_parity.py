@@ -40,13 +40,13 @@ def ocfg(cfg: bsq.Config) -> oracle.Config:
                          protect_num=cfg.protect_num, protect_den=cfg.protect_den)
 
 
-def np_codes(t):
-    a = t.cpu().numpy()
+def np_codes(L, t):
+    a = L.rowmajor(t).contiguous().cpu().numpy()
     return a.view(np.uint16) if a.dtype == np.int16 else a
 
 
-def np_gains(t):
-    return t.cpu().view(torch.int16).numpy().view(np.uint16)
+def np_gains(L, t):
+    return L.rowmajor(t).contiguous().cpu().view(torch.int16).numpy().view(np.uint16)
 
 
 def decoders(cfg, seed=7):
@@ -56,13 +56,25 @@ def decoders(cfg, seed=7):
 def assert_layer_equal(layer, enc, cfg, m=None):
     L = layer.mat(m) if m is not None else layer
     for s in range(cfg.stages):
-        np.testing.assert_array_equal(np_codes(L.codes[s]), enc.codes[s], err_msg=f"codes stage {s}")
-        np.testing.assert_array_equal(np_gains(L.gains[s]), enc.gains[s], err_msg=f"gains stage {s}")
+        np.testing.assert_array_equal(np_codes(L, L.codes[s]), enc.codes[s], err_msg=f"codes stage {s}")
+        np.testing.assert_array_equal(np_gains(L, L.gains[s]), enc.gains[s], err_msg=f"gains stage {s}")
+        # padding rows of the last 64-row group hold code 0 and gain +0
+        pad = L.row_groups * 64 - L.d_out
+        if pad:
+            full = L.codes[s].transpose(-3, -2).reshape(L.row_groups * 64, L.pitch)
+            assert int(full[L.d_out:].abs().sum()) == 0
     if cfg.k(L.d_in):
         np.testing.assert_array_equal(L.idx.cpu().numpy(), enc.idx, err_msg="protected indices")
-        np.testing.assert_array_equal(L.q8.cpu().numpy(), enc.q8, err_msg="int8 payload")
+        q8 = L.q8.cpu().numpy()
+        np.testing.assert_array_equal(q8[:, :enc.q8.shape[1]], enc.q8, err_msg="int8 payload")
+        assert not q8[:, enc.q8.shape[1]:].any(), "int8 payload padding"
         np.testing.assert_array_equal(L.scale.cpu().numpy().view(np.uint32), enc.scale.view(np.uint32),
                                       err_msg="scales")
+        # bitmap over the padded columns: exactly the oracle's protected set
+        want = np.zeros(L.pitch * cfg.d, dtype=np.uint8)
+        want[enc.idx] = 1
+        want = np.packbits(want, bitorder="little").view(np.uint32)
+        np.testing.assert_array_equal(L.bits.cpu().numpy().view(np.uint32), want, err_msg="protected bitmap")
 
 
 BF16_U = 2.0 ** -8
