@@ -26,6 +26,9 @@ namespace {
 // row-lane kernel: polls of a row group's last slice for the other slices'
 // partial sums before it gives up and writes NaN (seconds; never expected)
 constexpr int LANE_SPIN_LIMIT = 1 << 22;
+// row-lane kernel: largest padded int8 row that a finishing slice brings to
+// LDS (64 rows x 256 B = 16 KiB); longer rows are read from global memory
+constexpr int64_t LANE_Q8_LDS_MAX = 256;
 
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
@@ -378,6 +381,22 @@ __device__ __forceinline__ void mask_block(uint32_t (&xm)[64], const uint32_t *b
     }
 }
 
+// The LoRA term and the store of one output row (row < d_out).
+__device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMat &M, int64_t row, float acc)
+{
+    if (M.rank > 0) {
+        const uint16_t *br = M.B + row * M.rank;
+        uint16_t bq[BSQ_MAX_LORA_RANK];
+#pragma unroll
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bq[q] = (q < M.rank) ? br[q] : uint16_t(0);
+#pragma unroll
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q)
+            if (q < M.rank) acc = __builtin_fmaf(bf16_to_f32(bq[q]), M.t[q], acc);
+    }
+    if (a.y_bf16) static_cast<uint16_t *>(M.y)[row] = f32_to_bf16(acc);
+    else static_cast<float *>(M.y)[row] = acc;
+}
+
 // int8 protected columns, the LoRA term, and the store of one output row.
 // A lane reads its row's int8 codes (padded to 16) with up to eight 16-byte
 // loads issued together, and its LoRA row likewise, so the epilogue costs
@@ -403,17 +422,31 @@ __device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M,
             }
         }
     }
-    if (M.rank > 0) {
-        const uint16_t *br = M.B + row * M.rank;
-        uint16_t bq[BSQ_MAX_LORA_RANK];
-#pragma unroll
-        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bq[q] = (q < M.rank) ? br[q] : uint16_t(0);
-#pragma unroll
-        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q)
-            if (q < M.rank) acc = __builtin_fmaf(bf16_to_f32(bq[q]), M.t[q], acc);
+    lane_finish_lora(a, M, row, acc);
+}
+
+// The epilogue with the int8 rows already in LDS (s_q8 [64][kp], this lane's
+// row at lane * kp), else from global memory.
+__device__ __forceinline__ void lane_finish_lds(const GemvArgs &a, const GemvMat &M, const float *s_xs,
+                                                const int8_t *s_q8, bool q8_lds, int64_t row, float acc)
+{
+    if (row >= M.d_out) return;
+    if (!q8_lds || a.k == 0) {
+        lane_finish(a, M, s_xs, row, acc);
+        return;
     }
-    if (a.y_bf16) static_cast<uint16_t *>(M.y)[row] = f32_to_bf16(acc);
-    else static_cast<float *>(M.y)[row] = acc;
+    const int64_t kp = q8_pitch(a.k);
+    const uint4 *qr = reinterpret_cast<const uint4 *>(s_q8 + (row & 63) * kp);
+    for (int64_t p0 = 0; p0 < a.k; p0 += 16) {
+        const uint4 qv = qr[p0 / 16];
+        const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+            const int64_t p = p0 + e;
+            if (p < a.k) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), s_xs[p], acc);
+        }
+    }
+    lane_finish_lora(a, M, row, acc);
 }
 
 typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
@@ -444,7 +477,10 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
     extern __shared__ uint4 s_mem[];
     uint4 *s_tab = s_mem;                                      // [S][256] entries of 8 bf16
     float *s_red = reinterpret_cast<float *>(s_mem + S * 256);  // [WV][64] wave sums
-    float *s_xs = s_red + WV * 64;                             // [k] scale_p * x_{idx_p}
+    float *s_xs = s_red + WV * 64;                             // [kp] scale_p * x_{idx_p}
+    const int64_t kp = q8_pitch(a.k);
+    int8_t *s_q8 = reinterpret_cast<int8_t *>(s_xs + kp);      // [64][kp] int8 rows (finishing slice)
+    const bool q8_lds = kp <= LANE_Q8_LDS_MAX;
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
 
@@ -463,6 +499,7 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
     const int64_t b1 = (b0 + TPW < nblk) ? b0 + TPW : nblk;
     const int64_t nt = ((b1 < full_blocks) ? b1 : full_blocks) - b0;  // may be <= 0
     const bool ragged = b0 <= full_blocks && full_blocks < b1;
+    const bool fin = q == Q - 1;  // this slice finishes the row group
 
     // Prologue in a fixed issue order (vector-memory completions are counted
     // in order): the decoder table straight to LDS by DMA
@@ -476,6 +513,17 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
         const int c = r * WV + wave;  // 64-entry chunk of the [S][256] table
         const uint4 *src = reinterpret_cast<const uint4 *>(M.tab16[c >> 2]) + (c & 3) * 64 + lane;
         __builtin_amdgcn_global_load_lds(src, s_tab + c * 64, 16, 0, 0);
+    }
+    // the finishing slice brings its row group's int8 rows to LDS the same way
+    // (rows past d_out get clamped copies and are never read)
+    if (fin && a.k > 0 && q8_lds) {
+        const int8_t *src = M.q8 + rg * 64 * kp;
+        const int64_t avail = ((M.d_out - rg * 64 < 64) ? M.d_out - rg * 64 : 64) * kp;
+        for (int64_t o = int64_t(wave) * 1024; o < 64 * kp; o += WV * 1024) {
+            const int64_t e = o + lane * 16;
+            const int64_t es = (e < avail) ? e : avail - 16;
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4 *>(src + es), s_q8 + o, 16, 0, 0);
+        }
     }
     __builtin_amdgcn_sched_barrier(0);
     const int64_t blast = (nt > 0) ? b0 + nt - 1 : 0;
@@ -535,11 +583,14 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
         acc = lane_block<S>(buf[0], xm, s_tab, acc);
     }
 
-    // scaled protected activations for the epilogue (indices loaded above)
-    if (t < a.k) s_xs[t] = (pj >= 0 && pj < a.d_in) ? psc * load_x(a.x, pj, 1) : 0.0f;
-    for (int64_t p = NT + t; p < a.k; p += NT) {  // more protected columns than threads
-        const int32_t j = M.idx[p];
-        s_xs[p] = (j >= 0 && j < a.d_in) ? M.scale[p] * load_x(a.x, j, 1) : 0.0f;
+    // scaled protected activations for the epilogue (indices loaded above),
+    // only in the finishing slice
+    if (fin) {
+        if (t < a.k) s_xs[t] = (pj >= 0 && pj < a.d_in) ? psc * load_x(a.x, pj, 1) : 0.0f;
+        for (int64_t p = NT + t; p < a.k; p += NT) {  // more protected columns than threads
+            const int32_t j = M.idx[p];
+            s_xs[p] = (j >= 0 && j < a.d_in) ? M.scale[p] * load_x(a.x, j, 1) : 0.0f;
+        }
     }
     // the four wave sums of each row, in wave order
     s_red[wave * 64 + lane] = acc;
@@ -550,11 +601,11 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
     for (int w = 1; w < WV; ++w) v += s_red[w * 64 + lane];
     const int64_t row = rg * 64 + lane;
     if (Q == 1) {
-        lane_finish(a, M, s_xs, row, v);
+        lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, v);
         return;
     }
     uint64_t *slots = a.slots + (M.rg_begin + rg) * (Q - 1) * 64 + lane;
-    if (q < Q - 1) {
+    if (!fin) {
         __hip_atomic_store(slots + q * 64, (uint64_t(1) << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
         return;
@@ -586,7 +637,7 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
     tot += v;
     for (int64_t q0 = 0; q0 < Q - 1; ++q0)
         __hip_atomic_store(slots + q0 * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    lane_finish(a, M, s_xs, row, timed_out ? __builtin_nanf("") : tot);
+    lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, timed_out ? __builtin_nanf("") : tot);
 }
 
 // ---------------------------------------------------------------------------
@@ -766,7 +817,9 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
             blocks += nrg * a.q;
             rgs += nrg;
         }
-        const size_t shm = size_t(S) * 256 * 16 + 4 * 64 * 4 + size_t(a.k) * 4;
+        const int64_t kp = q8_pitch(a.k);
+        const size_t shm = size_t(S) * 256 * 16 + 4 * 64 * 4 + size_t(kp) * 4 +
+                           ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
         switch (S) {
         case 1: hipLaunchKernelGGL((gemv_lane_kernel<1, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
         case 2: hipLaunchKernelGGL((gemv_lane_kernel<2, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
