@@ -32,6 +32,11 @@ __device__ __forceinline__ int find_pos(const int32_t *idx, int64_t k, int32_t j
     return int(lo);
 }
 
+// A block walks the tiles of one matrix (grid-stride, so the decoder tables
+// and the protected bitmap are set up once per block). Thread t handles the
+// tile elements t, t + 256, t + 512, t + 768: element e is row e / 16, chunk
+// e % 16 of the tile, so the code and gain reads follow the tile layout and
+// 16 consecutive threads write one contiguous row segment of W_hat.
 template <int D, int S, bool BF16OUT>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
@@ -40,81 +45,96 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     uint32_t *s_bits = s_mem;
     float *s_tab = reinterpret_cast<float *>(s_mem + ((a.words + 3) & ~int64_t(3)));
     const int64_t m = blockIdx.y;
+    const int t = threadIdx.x;
     const int32_t *idx = a.idx ? a.idx + m * a.k : nullptr;
     if (a.k > 0) {
-        for (int64_t w = threadIdx.x; w < a.words; w += blockDim.x) s_bits[w] = 0u;
+        for (int64_t w = t; w < a.words; w += blockDim.x) s_bits[w] = 0u;
         __syncthreads();
-        for (int64_t p = threadIdx.x; p < a.k; p += blockDim.x) {
+        for (int64_t p = t; p < a.k; p += blockDim.x) {
             const int32_t j = idx[p];
             if (j >= 0 && j < a.d_in) atomicOr(&s_bits[j >> 5], 1u << (j & 31));
         }
     }
     if constexpr (D == 8) {
-        for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
+        for (int e = t; e < S * 256 * 8; e += blockDim.x) {
             int s = e / (256 * 8), r = e - s * 256 * 8;
             s_tab[e] = a.tab32[s][r];
         }
     }
     __syncthreads();
 
-    const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (gid >= a.d_out * a.C) return;
-    const int64_t i = gid / a.C;
-    const int64_t c = gid - i * a.C;
-    const int64_t plane = m * plane_elems(a.d_out, a.pitch) + tile_index(i, c, a.pitch);
+    const int64_t nb = a.pitch / 16;                 // tiles per 64-row group
+    const int64_t tiles = (a.d_out + 63) / 64 * nb;  // tiles of this matrix
+    const int64_t kp = q8_pitch(a.k);
+    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        const int64_t rg = tile / nb, cb = tile - rg * nb;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int e = t + 256 * u;
+            const int64_t i = rg * 64 + (e >> 4);
+            const int64_t c = cb * 16 + (e & 15);
+            if (i >= a.d_out || c >= a.C) continue;
+            const int64_t plane = m * plane_elems(a.d_out, a.pitch) + tile * 1024 + e;
 
-    float v[D];
+            float v[D];
 #pragma unroll
-    for (int j = 0; j < D; ++j) v[j] = 0.0f;
+            for (int j = 0; j < D; ++j) v[j] = 0.0f;
 #pragma unroll
-    for (int s = 0; s < S; ++s) {
-        const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[plane])
-                                       : uint32_t(static_cast<const uint16_t *>(a.codes[s])[plane]);
-        const float g = f16_bits_to_f32(a.gains[s][plane]);
-        const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
-        const float4 *y4 = reinterpret_cast<const float4 *>(y);
+            for (int s = 0; s < S; ++s) {
+                const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[plane])
+                                               : uint32_t(static_cast<const uint16_t *>(a.codes[s])[plane]);
+                const float g = f16_bits_to_f32(a.gains[s][plane]);
+                const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
+                const float4 *y4 = reinterpret_cast<const float4 *>(y);
 #pragma unroll
-        for (int q = 0; q < D / 4; ++q) {
-            float4 t = y4[q];
-            v[4 * q + 0] = __builtin_fmaf(g, t.x, v[4 * q + 0]);
-            v[4 * q + 1] = __builtin_fmaf(g, t.y, v[4 * q + 1]);
-            v[4 * q + 2] = __builtin_fmaf(g, t.z, v[4 * q + 2]);
-            v[4 * q + 3] = __builtin_fmaf(g, t.w, v[4 * q + 3]);
-        }
-    }
-    if (a.k > 0) {
-        const int64_t col0 = c * D;
-        const uint32_t pm = (s_bits[col0 >> 5] >> (col0 & 31)) & ((1u << D) - 1u);
-        if (pm) {
+                for (int q = 0; q < D / 4; ++q) {
+                    float4 tv = y4[q];
+                    v[4 * q + 0] = __builtin_fmaf(g, tv.x, v[4 * q + 0]);
+                    v[4 * q + 1] = __builtin_fmaf(g, tv.y, v[4 * q + 1]);
+                    v[4 * q + 2] = __builtin_fmaf(g, tv.z, v[4 * q + 2]);
+                    v[4 * q + 3] = __builtin_fmaf(g, tv.w, v[4 * q + 3]);
+                }
+            }
+            if (a.k > 0) {
+                const int64_t col0 = c * D;
+                const uint32_t pm = (s_bits[col0 >> 5] >> (col0 & 31)) & ((1u << D) - 1u);
+                if (pm) {
 #pragma unroll
-            for (int j = 0; j < D; ++j) {
-                if (!((pm >> j) & 1u)) continue;
-                const int p = find_pos(idx, a.k, int32_t(col0 + j));
-                v[j] = float(a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p]) * a.scale[m * a.k + p];
+                    for (int j = 0; j < D; ++j) {
+                        if (!((pm >> j) & 1u)) continue;
+                        const int p = find_pos(idx, a.k, int32_t(col0 + j));
+                        v[j] = float(a.q8[(m * a.d_out + i) * kp + p]) * a.scale[m * a.k + p];
+                    }
+                }
+            }
+            const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
+            if constexpr (BF16OUT) {
+                uint16_t h[D];
+#pragma unroll
+                for (int j = 0; j < D; ++j) h[j] = f32_to_bf16(v[j]);
+                uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + o);
+#pragma unroll
+                for (int q = 0; q < D / 8; ++q) dst[q] = reinterpret_cast<const uint4 *>(h)[q];
+            } else {
+                float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + o);
+#pragma unroll
+                for (int q = 0; q < D / 4; ++q)
+                    dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
             }
         }
-    }
-    const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
-    if constexpr (BF16OUT) {
-        uint16_t h[D];
-#pragma unroll
-        for (int j = 0; j < D; ++j) h[j] = f32_to_bf16(v[j]);
-        uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + o);
-#pragma unroll
-        for (int q = 0; q < D / 8; ++q) dst[q] = reinterpret_cast<const uint4 *>(h)[q];
-    } else {
-        float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + o);
-#pragma unroll
-        for (int q = 0; q < D / 4; ++q) dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
     }
 }
 
 template <int D, bool BF16OUT>
 hipError_t launch_decode_t(int stages, const DecodeArgs &a, int64_t n_mats, hipStream_t st)
 {
-    const int64_t n = a.d_out * a.C;
-    if (n == 0 || n_mats == 0) return hipSuccess;
-    const dim3 grid(unsigned((n + 255) / 256), unsigned(n_mats));
+    const int64_t tiles = (a.d_out + 63) / 64 * (a.pitch / 16);
+    if (tiles == 0 || n_mats == 0) return hipSuccess;
+    // about eight blocks per CU in all, each walking its share of the tiles
+    int64_t gx = (2048 + n_mats - 1) / n_mats;
+    if (gx > tiles) gx = tiles;
+    if (gx < 1) gx = 1;
+    const dim3 grid = dim3(unsigned(gx), unsigned(n_mats));
     const size_t shm = size_t((a.words + 3) & ~int64_t(3)) * 4 + ((D == 8) ? size_t(stages) * 256 * 8 * 4 : 0);
     switch (stages) {
     case 1: hipLaunchKernelGGL((decode_kernel<D, 1, BF16OUT>), grid, dim3(256), shm, st, a); break;

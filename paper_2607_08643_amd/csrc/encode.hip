@@ -219,21 +219,11 @@ struct EncodeArgs {
     int32_t *err;
 };
 
+// one element of the tiled planes (padding rows and chunks included):
+// consecutive elements are consecutive code and gain words
 template <int D, int S, typename T>
-__global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
+__device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, int64_t gid)
 {
-    extern __shared__ float s_tab[];  // D == 8: [S][256][8]
-    if constexpr (D == 8) {
-        for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
-            int s = e / (256 * 8), r = e - s * 256 * 8;
-            s_tab[e] = a.tab32[s][r];
-        }
-        __syncthreads();
-    }
-    // one thread per element of the tiled planes (padding rows and chunks
-    // included), so consecutive threads write consecutive code and gain words
-    const int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (gid >= a.total) return;
     const int64_t per_mat = plane_elems(a.d_out, a.pitch);
     const int64_t m = gid / per_mat;
     const int64_t e = gid - m * per_mat;
@@ -344,10 +334,31 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
     }
 }
 
+// The element loop is grid-stride, so the decoder tables (d = 8) are staged in
+// LDS once per block rather than once per 256 chunks.
+template <int D, int S, typename T>
+__global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
+{
+    extern __shared__ float s_tab[];  // D == 8: [S][256][8]
+    if constexpr (D == 8) {
+        for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
+            int s = e / (256 * 8), r = e - s * 256 * 8;
+            s_tab[e] = a.tab32[s][r];
+        }
+        __syncthreads();
+    }
+    for (int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; gid < a.total;
+         gid += int64_t(gridDim.x) * blockDim.x)
+        encode_element<D, S, T>(a, s_tab, gid);
+}
+
 template <int D, typename T>
 hipError_t launch_encode_chunks(int stages, const EncodeArgs &a, hipStream_t st)
 {
-    const dim3 grid(unsigned((a.total + 255) / 256));
+    // at most about 16 blocks per CU; each walks its share of the elements
+    int64_t blocks = (a.total + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
+    const dim3 grid = dim3(unsigned(blocks));
     const size_t shm = (D == 8) ? size_t(stages) * 256 * 8 * 4 : 0;
     switch (stages) {
     case 1: hipLaunchKernelGGL((encode_kernel<D, 1, T>), grid, dim3(256), shm, st, a); break;
