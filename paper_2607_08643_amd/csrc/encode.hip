@@ -40,25 +40,40 @@ __global__ __launch_bounds__(256) void colscore_kernel(const T *__restrict__ W, 
     const T *p = W + m * d_out * d_in + col;
     double s = 0.0;
     float mx = 0.0f;
-    int64_t i = 0;
-    constexpr int U = 16;
-    for (; i + U <= d_out; i += U) {
-        float v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = load_elem<T>(p + (i + u) * d_in);
+    // rows in order, U at a time, the next U already in flight (two register
+    // buffers, branch-free steady state so the loads are not waited on early)
+    constexpr int U = 32;
+    float va[U], vb[U];
+    auto take = [&](const float (&v)[U]) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            double dv = double(v[u]);
+            const double dv = double(v[u]);
             s = s + dv * dv;
-            float a = __builtin_fabsf(v[u]);
+            const float a = __builtin_fabsf(v[u]);
             if (a > mx) mx = a;
         }
+    };
+    int64_t i = 0;
+    if (d_out >= 2 * U) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) va[u] = load_elem<T>(p + int64_t(u) * d_in);
+        for (; i + 3 * U <= d_out; i += 2 * U) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) vb[u] = load_elem<T>(p + (i + U + u) * d_in);
+            take(va);
+#pragma unroll
+            for (int u = 0; u < U; ++u) va[u] = load_elem<T>(p + (i + 2 * U + u) * d_in);
+            take(vb);
+        }
+        // rows [i, i + U) are in va; the rest is done one by one below
+        take(va);
+        i += U;
     }
     for (; i < d_out; ++i) {
-        float v = load_elem<T>(p + i * d_in);
-        double dv = double(v);
+        const float v = load_elem<T>(p + i * d_in);
+        const double dv = double(v);
         s = s + dv * dv;
-        float a = __builtin_fabsf(v);
+        const float a = __builtin_fabsf(v);
         if (a > mx) mx = a;
     }
     if (g) {
