@@ -16,11 +16,10 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
-constexpr int BN = 64;       // weight rows per block
-constexpr int BK = 64;       // inputs per K step
+constexpr int BN = 64;       // weight rows per block (one 64-row group)
+constexpr int BK = 128;      // inputs per K step
 constexpr int LDS_PAD = 8;   // bf16 padding per LDS row (breaks bank aliasing)
 constexpr int LDK = BK + LDS_PAD;
-constexpr int MAX_BM = 128;  // tokens per block
 
 struct GemmArgs {
     const void *codes[BSQ_MAX_STAGES];
@@ -70,23 +69,109 @@ __global__ __launch_bounds__(256) void gemm_lora_prep(const uint16_t *X, int64_t
     if (t == 0) T[m * BSQ_MAX_LORA_RANK + r] = (r < rank) ? red[0] : 0.0f;
 }
 
-template <int D, int S, int MT>
+// Decode of one K step of the weight tile: rows [0, 64) of the 64-row group,
+// the tile's chunks [cbeg, cbeg + CPS) (d = 8: all 16; d = 16: half), as
+// bf16 into s_w. Thread t owns row t / 4 and CPT = CPS / 4 consecutive
+// chunks; its code and gain words come from the prefetch registers.
+template <int D, int S>
+struct DecodeRegs {
+    static constexpr int CPT = (D == 8) ? 4 : 2;     // chunks per thread per K step
+    uint32_t code[S][(D == 8) ? 1 : 1];              // CPT codes: 4 bytes (d = 8) or 2 x uint16 (d = 16)
+    uint32_t gain[S][CPT / 2];                        // CPT fp16 gains
+};
+
+template <int D, int S>
+__device__ __forceinline__ void gemm_prefetch(DecodeRegs<D, S> &r, const GemmArgs &a, int64_t tile, int cbeg, int t)
+{
+    constexpr int CPT = DecodeRegs<D, S>::CPT;
+    const int64_t e = (tile << 10) + ((t >> 2) << 4) + cbeg + (t & 3) * CPT;  // first element
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        if constexpr (D == 8) r.code[s][0] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
+        else r.code[s][0] = *reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(a.codes[s]) + e);
+        if constexpr (CPT == 4) {
+            const uint2 g = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
+            r.gain[s][0] = g.x;
+            r.gain[s][1] = g.y;
+        } else {
+            r.gain[s][0] = *reinterpret_cast<const uint32_t *>(a.gains[s] + e);
+        }
+    }
+}
+
+template <int D, int S>
+__device__ __forceinline__ void gemm_decode(const DecodeRegs<D, S> &r, const GemmArgs &a, const float *s_tab,
+                                            const uint32_t *s_bits, uint16_t *s_w, int64_t rg, int64_t c0, int t)
+{
+    constexpr int CPT = DecodeRegs<D, S>::CPT;
+    const int rr = t >> 2;
+    const int64_t row = rg * 64 + rr;
+#pragma unroll
+    for (int u = 0; u < CPT; ++u) {
+        const int64_t c = c0 + (t & 3) * CPT + u;  // chunk index in the row
+        float v[D];
+#pragma unroll
+        for (int j = 0; j < D; ++j) v[j] = 0.0f;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            const uint32_t code = (D == 8) ? ((r.code[s][0] >> (8 * u)) & 0xffu) : ((r.code[s][0] >> (16 * u)) & 0xffffu);
+            const uint32_t gw = r.gain[s][u >> 1];
+            const float g = f16_bits_to_f32(uint16_t((u & 1) ? (gw >> 16) : (gw & 0xffffu)));
+            const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
+            const float4 *y4 = reinterpret_cast<const float4 *>(y);
+#pragma unroll
+            for (int q = 0; q < D / 4; ++q) {
+                const float4 yy = y4[q];
+                v[4 * q + 0] = __builtin_fmaf(g, yy.x, v[4 * q + 0]);
+                v[4 * q + 1] = __builtin_fmaf(g, yy.y, v[4 * q + 1]);
+                v[4 * q + 2] = __builtin_fmaf(g, yy.z, v[4 * q + 2]);
+                v[4 * q + 3] = __builtin_fmaf(g, yy.w, v[4 * q + 3]);
+            }
+        }
+        if (a.k > 0 && row < a.d_out && c < a.C) {
+            const int64_t col0 = c * D;
+            const uint32_t pm = (s_bits[col0 >> 5] >> (col0 & 31)) & ((1u << D) - 1u);
+            if (pm) {
+#pragma unroll
+                for (int j = 0; j < D; ++j) {
+                    if (!((pm >> j) & 1u)) continue;
+                    const int p = find_pos(a.idx, a.k, int32_t(col0 + j));
+                    v[j] = float(a.q8[row * q8_pitch(a.k) + p]) * a.scale[p];
+                }
+            }
+        }
+        uint16_t h[D];
+#pragma unroll
+        for (int j = 0; j < D; ++j) h[j] = f32_to_bf16(v[j]);
+        uint16_t *dst = s_w + rr * LDK + ((t & 3) * CPT + u) * D;
+#pragma unroll
+        for (int q = 0; q < D / 8; ++q) reinterpret_cast<uint4 *>(dst)[q] = reinterpret_cast<const uint4 *>(h)[q];
+    }
+}
+
+// One workgroup: the 64 rows of one row group x BM = WM * MT * 16 tokens.
+// Waves are WM (token) x WN (row) with WM * WN = 4; a wave owns MT token
+// groups and NT = 4 / WN row groups of 16. K steps of BK = 128 inputs.
+template <int D, int S, int WM, int MT>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
 {
-    constexpr int BM = 16 * MT;
-    constexpr int CPR = BK / D;             // chunks per tile row per K step
-    constexpr int NCH = BN * CPR;           // chunks per tile
+    constexpr int WN = 4 / WM, NT = 4 / WN, BM = WM * MT * 16;
+    constexpr int CPS = BK / D;  // chunks per K step
     __shared__ __attribute__((aligned(16))) uint16_t s_w[BN * LDK];
-    __shared__ __attribute__((aligned(16))) uint16_t s_x[BM * LDK];
-    extern __shared__ uint32_t s_dyn[];     // protected bitmap [words], then fp32 tables (D == 8)
+    extern __shared__ uint32_t s_dyn[];  // protected bitmap [words], then fp32 tables (D == 8)
     uint32_t *s_bits = s_dyn;
     float *s_tab = reinterpret_cast<float *>(s_dyn + ((a.words + 3) & ~int64_t(3)));
 
-    const int t = threadIdx.x;
-    const int lane = t & 63, wave = t >> 6;
-    const int64_t n0 = int64_t(blockIdx.x) * BN;
-    const int64_t m0 = int64_t(blockIdx.y) * BM;
+    const int t = threadIdx.x, lane = t & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int wm = wave % WM, wn = wave / WM;
+    const int64_t rg = blockIdx.x;                        // row group
+    const int64_t m0 = int64_t(blockIdx.y) * BM + wm * MT * 16;  // this wave's first token
+    const int64_t nb = a.pitch / 16;                      // tiles per row group
+    const int64_t ksteps = (a.C + CPS - 1) / CPS;         // K steps over the real chunks
 
+    DecodeRegs<D, S> pre;
+    gemm_prefetch<D, S>(pre, a, rg * nb, 0, t);
     if (a.k > 0) {
         for (int64_t w = t; w < a.words; w += 256) s_bits[w] = 0u;
         __syncthreads();
@@ -103,104 +188,86 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
     }
     __syncthreads();
 
-    f32x4_t acc[MT];
+    f32x4_t acc[MT][NT];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) acc[i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-    for (int64_t k0 = 0; k0 < a.d_in; k0 += BK) {
-        // X tile: BM x BK bf16, 8 elements per 16-byte load
-        for (int e = t; e < BM * (BK / 8); e += 256) {
-            const int r = e / (BK / 8), c8 = (e - r * (BK / 8)) * 8;
-            const int64_t row = m0 + r, col = k0 + c8;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (row < a.M && col < a.d_in) v = *reinterpret_cast<const uint4 *>(a.X + row * a.ldx + col);
-            *reinterpret_cast<uint4 *>(s_x + r * LDK + c8) = v;
-        }
-        // weight tile: decode BN rows x CPR chunks
-        for (int e = t; e < NCH; e += 256) {
-            const int r = e / CPR, cc = e - r * CPR;
-            const int64_t row = n0 + r;
-            const int64_t c = k0 / D + cc;
-            float v[D];
+    // X fragments of a K step: token 16 i + lane % 16 of this wave, inputs
+    // k0 + 32 kk4 + 8 (lane / 16) .. + 8. Loads are unconditional with the
+    // token and input clamped into X (a clamped token's outputs are never
+    // stored; a clamped input meets a zero weight), so they are not waited on
+    // until the MFMAs need them, one K step later.
+    uint4 xf[MT][BK / 32], xn[MT][BK / 32];
+    auto load_x = [&](uint4 (&dst)[MT][BK / 32], int64_t k0) {
 #pragma unroll
-            for (int j = 0; j < D; ++j) v[j] = 0.0f;
-            if (row < a.d_out && c < a.C) {
-                const int64_t off = tile_index(row, c, a.pitch);
+        for (int i = 0; i < MT; ++i) {
+            int64_t tok = m0 + 16 * i + (lane & 15);
+            tok = tok < a.M ? tok : a.M - 1;
 #pragma unroll
-                for (int s = 0; s < S; ++s) {
-                    const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[off])
-                                                   : uint32_t(static_cast<const uint16_t *>(a.codes[s])[off]);
-                    const float g = f16_bits_to_f32(a.gains[s][off]);
-                    const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
-                    const float4 *y4 = reinterpret_cast<const float4 *>(y);
-#pragma unroll
-                    for (int q = 0; q < D / 4; ++q) {
-                        const float4 yy = y4[q];
-                        v[4 * q + 0] = __builtin_fmaf(g, yy.x, v[4 * q + 0]);
-                        v[4 * q + 1] = __builtin_fmaf(g, yy.y, v[4 * q + 1]);
-                        v[4 * q + 2] = __builtin_fmaf(g, yy.z, v[4 * q + 2]);
-                        v[4 * q + 3] = __builtin_fmaf(g, yy.w, v[4 * q + 3]);
-                    }
-                }
-                if (a.k > 0) {
-                    const int64_t col0 = c * D;
-                    const uint32_t pm = (s_bits[col0 >> 5] >> (col0 & 31)) & ((1u << D) - 1u);
-                    if (pm) {
-#pragma unroll
-                        for (int j = 0; j < D; ++j) {
-                            if (!((pm >> j) & 1u)) continue;
-                            const int p = find_pos(a.idx, a.k, int32_t(col0 + j));
-                            v[j] = float(a.q8[row * q8_pitch(a.k) + p]) * a.scale[p];
-                        }
-                    }
-                }
+            for (int q = 0; q < BK / 32; ++q) {
+                int64_t kq = k0 + 32 * q + 8 * (lane >> 4);
+                kq = kq < a.d_in ? kq : a.d_in - 8;
+                dst[i][q] = *reinterpret_cast<const uint4 *>(a.X + tok * a.ldx + kq);
             }
-            uint16_t h[D];
-#pragma unroll
-            for (int j = 0; j < D; ++j) h[j] = f32_to_bf16(v[j]);
-            uint16_t *dst = s_w + r * LDK + cc * D;
-#pragma unroll
-            for (int q = 0; q < D / 8; ++q) reinterpret_cast<uint4 *>(dst)[q] = reinterpret_cast<const uint4 *>(h)[q];
         }
+    };
+    load_x(xf, 0);
+
+    for (int64_t ks = 0; ks < ksteps; ++ks) {
+        const int64_t c0 = ks * CPS;  // first chunk of this step
+        gemm_decode<D, S>(pre, a, s_tab, s_bits, s_w, rg, c0, t);
+        const int64_t c1 = (ks + 1 < ksteps) ? c0 + CPS : c0;  // the last step reloads its own words
+        gemm_prefetch<D, S>(pre, a, rg * nb + c1 / 16, int(c1 % 16), t);
+        load_x(xn, c1 * D);
         __syncthreads();
-        // MFMA: wave w owns weight rows [16w, 16w + 16) of the tile, all BM tokens.
-        // A = X (16 tokens x 32 inputs), B = W_hat^T (32 inputs x 16 weight rows);
-        // both operands take inputs [8*(lane/16), +8) of the 32, so any fixed
-        // ordering of the K lanes inside the instruction cancels out.
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 32) {
-            const int kq = kk + 8 * (lane >> 4);
-            const uint4 bw = *reinterpret_cast<const uint4 *>(s_w + (16 * wave + (lane & 15)) * LDK + kq);
-            const bf16x8_t bop = __builtin_bit_cast(bf16x8_t, bw);
+        for (int q = 0; q < BK / 32; ++q) {
+            bf16x8_t bop[NT];
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                const uint4 bw = *reinterpret_cast<const uint4 *>(s_w + (16 * (wn * NT + j) + (lane & 15)) * LDK +
+                                                                 32 * q + 8 * (lane >> 4));
+                bop[j] = __builtin_bit_cast(bf16x8_t, bw);
+            }
 #pragma unroll
             for (int i = 0; i < MT; ++i) {
-                const uint4 ax = *reinterpret_cast<const uint4 *>(s_x + (16 * i + (lane & 15)) * LDK + kq);
-                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, ax), bop, acc[i], 0, 0, 0);
+                const bf16x8_t aop = __builtin_bit_cast(bf16x8_t, xf[i][q]);
+#pragma unroll
+                for (int j = 0; j < NT; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, bop[j], acc[i][j], 0, 0, 0);
             }
         }
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int q = 0; q < BK / 32; ++q) xf[i][q] = xn[i][q];
         __syncthreads();
     }
 
-    // epilogue: D[i][j] with token i = 4*(lane/16) + r, weight row j = lane % 16
-    const int64_t n = n0 + 16 * wave + (lane & 15);
-    if (n >= a.d_out) return;
-    float bl[BSQ_MAX_LORA_RANK];
+    // epilogue: acc[i][j] element r is token 16 i + 4 (lane / 16) + r, row 16 j + lane % 16
 #pragma unroll
-    for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bl[q] = (q < a.rank) ? bf16_to_f32(a.B[n * a.rank + q]) : 0.0f;
+    for (int j = 0; j < NT; ++j) {
+        const int64_t n = rg * 64 + 16 * (wn * NT + j) + (lane & 15);
+        if (n >= a.d_out) continue;
+        float bl[BSQ_MAX_LORA_RANK];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bl[q] = (q < a.rank) ? bf16_to_f32(a.B[n * a.rank + q]) : 0.0f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t m = m0 + 16 * i + 4 * (lane >> 4) + r;
-            if (m >= a.M) continue;
-            float v = acc[i][r];
-            if (a.rank > 0) {
-                const float *Tm = a.T + m * BSQ_MAX_LORA_RANK;
+        for (int i = 0; i < MT; ++i) {
 #pragma unroll
-                for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) v = __builtin_fmaf(bl[q], Tm[q], v);
+            for (int r = 0; r < 4; ++r) {
+                const int64_t m = m0 + 16 * i + 4 * (lane >> 4) + r;
+                if (m >= a.M) continue;
+                float v = acc[i][j][r];
+                if (a.rank > 0) {
+                    const float *Tm = a.T + m * BSQ_MAX_LORA_RANK;
+#pragma unroll
+                    for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) v = __builtin_fmaf(bl[q], Tm[q], v);
+                }
+                if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n] = f32_to_bf16(v);
+                else static_cast<float *>(a.Y)[m * a.ldy + n] = v;
             }
-            if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n] = f32_to_bf16(v);
-            else static_cast<float *>(a.Y)[m * a.ldy + n] = v;
         }
     }
 }
@@ -208,15 +275,17 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
 template <int D, int S>
 hipError_t launch_gemm_t(const GemmArgs &a, hipStream_t st)
 {
-    const int64_t nb = (a.d_out + BN - 1) / BN;
+    const int64_t nrg = (a.d_out + 63) / 64;
     const size_t shm = size_t((a.words + 3) & ~int64_t(3)) * 4 + ((D == 8) ? size_t(S) * 256 * 8 * 4 : 0);
+    const dim3 block = dim3(256);
     if (a.M <= 16) {
-        hipLaunchKernelGGL((gemm_kernel<D, S, 1>), dim3(unsigned(nb), unsigned((a.M + 15) / 16)), dim3(256), shm, st, a);
+        hipLaunchKernelGGL((gemm_kernel<D, S, 1, 1>), dim3(unsigned(nrg), unsigned((a.M + 15) / 16)), block, shm, st, a);
     } else if (a.M <= 64) {
-        hipLaunchKernelGGL((gemm_kernel<D, S, 4>), dim3(unsigned(nb), unsigned((a.M + 63) / 64)), dim3(256), shm, st, a);
+        hipLaunchKernelGGL((gemm_kernel<D, S, 4, 1>), dim3(unsigned(nrg), unsigned((a.M + 63) / 64)), block, shm, st, a);
+    } else if (a.M <= 128) {
+        hipLaunchKernelGGL((gemm_kernel<D, S, 4, 2>), dim3(unsigned(nrg), unsigned((a.M + 127) / 128)), block, shm, st, a);
     } else {
-        hipLaunchKernelGGL((gemm_kernel<D, S, 8>), dim3(unsigned(nb), unsigned((a.M + MAX_BM - 1) / MAX_BM)), dim3(256),
-                           shm, st, a);
+        hipLaunchKernelGGL((gemm_kernel<D, S, 4, 4>), dim3(unsigned(nrg), unsigned((a.M + 255) / 256)), block, shm, st, a);
     }
     return hipGetLastError();
 }
