@@ -248,7 +248,7 @@ def main():
                     for pname in ("q", "gate", "up"):
                         Lp = blk.layers[pname].mat(0)
                         Y = torch.empty((M, Lp.d_out), dtype=torch.bfloat16, device=dev)
-                        ws = torch.empty(bsq.bsq_workspace_bytes(blk.cfg, bsq.OP_GEMM, 1, Lp.d_out, 4096, M) + 256,
+                        ws = torch.zeros(bsq.bsq_workspace_bytes(blk.cfg, bsq.OP_GEMM, 1, Lp.d_out, 4096, M) + 256,
                                          dtype=torch.uint8, device=dev)
                         ws = ws[(-ws.data_ptr()) % 256:]
                         for r in range(2):

@@ -175,9 +175,10 @@ bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats
 /* A prepared codec: the stage decoders evaluated on all 2^b codes
  * (Section III-G, batched parallel residual decoding needs only D_s(code)).
  * The buffer holds, per stage, an fp32 table [2^b][d] filled in the same fp32
- * operation order as the encoder's definition (so encode and decode are exact)
- * and a bf16 copy [2^b][d] for the products. One codec per (category, stage
- * set) serves every layer of that category.
+ * operation order as the encoder's definition (so encode and decode are
+ * exact), then a bf16 copy [2^b][d] for the GEMV's products and an fp16 copy
+ * [2^b][d] for the GEMM's decode (both rounded to nearest even). One codec
+ * per (category, stage set) serves every layer of that category.
  * bsq_codec_bytes: required size (host only).
  * bsq_codec_prepare: `dec` is a host array of `stages` bsq_decoder structs
  * whose tensors are device pointers; `codec` is a device buffer of at least
@@ -260,7 +261,15 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  * then MFMA), Y = X W_hat^T + (X A^T) B^T:
  *   X  device bf16 [M][ldx] (ldx >= d_in, multiple of 8)
  *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
- *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M) */
+ *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M),
+ *      256-byte aligned, ZERO-FILLED before its first use: its first 16 KiB
+ *      are per-tile arrival counters of the split-K reduction that every call
+ *      leaves at zero again (the rest is scratch: X A^T and fp32 partial
+ *      tiles). One workspace serves GEMM calls of any shape; it must not be
+ *      shared with a GEMV workspace, and calls that share it must not
+ *      overlap.
+ * The K steps of a tile may be split over several blocks; their fp32
+ * partials are summed in a fixed order, so results are deterministic. */
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
                     const bsq_lora *lora, const void *X, int32_t x_dtype, int64_t M,
                     int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,

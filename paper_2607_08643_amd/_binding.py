@@ -440,7 +440,7 @@ def bsq_gemm(cfg: Config, codec: Codec, layer: Layer, X: torch.Tensor, lora=None
     dev = X.device
     out = out if out is not None else torch.empty((M, layer.d_out), dtype=y_dtype, device=dev)
     need = bsq_workspace_bytes(cfg, OP_GEMM, 1, layer.d_out, d_in, M)
-    ws = ws if ws is not None else _empty_aligned(need, dev)
+    ws = ws if ws is not None else _empty_aligned(need, dev, zero=True)
     c, L = cfg.c(), layer.c()
     lo = _lora_struct(lora)
     _check(lib().bsq_gemm(ct.byref(c), ct.c_void_p(codec.ptr()), ct.byref(L), ct.byref(lo), _ptr(X),

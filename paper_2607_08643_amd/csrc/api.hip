@@ -151,7 +151,7 @@ bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats
         return BSQ_OK;
     case BSQ_OP_GEMM:
         if (M < 0) return BSQ_ERR_ARG;
-        *bytes = gemm_ws_bytes(*cfg, d_in, M);
+        *bytes = gemm_ws_bytes(*cfg, d_out, d_in, M);
         return BSQ_OK;
     default: return BSQ_ERR_ARG;
     }
@@ -310,7 +310,7 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     if (M < 0 || ldx < layer->d_in || ldy < layer->d_out || ldx % 8 != 0) return BSQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(ws, 256) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
     if (!aligned(Y, y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
-    if (ws_bytes < gemm_ws_bytes(*cfg, layer->d_in, M)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    if (ws_bytes < gemm_ws_bytes(*cfg, layer->d_out, layer->d_in, M)) return BSQ_ERR_BUFFER_TOO_SMALL;
     if (layer->k > 4096) return BSQ_ERR_UNSUPPORTED;
     return from_hip(launch_gemm(*cfg, codec, *layer, lora, X, M, ldx, Y, y_dtype, ldy, ws,
                                 static_cast<hipStream_t>(stream)));

@@ -12,7 +12,9 @@ namespace bsq {
 // ---------------------------------------------------------------------------
 // Codec buffer: for each stage an fp32 table [2^b][d] (exact decoder values),
 // then for each stage a bf16 table [2^b][d] (the same values rounded to
-// nearest even, consumed by the products).
+// nearest even, consumed by the GEMV's bf16 products), then for each stage an
+// fp16 table [2^b][d] (rounded to nearest even, consumed by the GEMM's decode
+// through mixed-precision fma).
 // ---------------------------------------------------------------------------
 inline size_t codec_entries(const bsq_config &c) { return (size_t(1) << c.b) * size_t(c.d); }
 inline size_t codec_tab32_offset(const bsq_config &c, int s) { return size_t(s) * codec_entries(c) * 4; }
@@ -20,7 +22,11 @@ inline size_t codec_tab16_offset(const bsq_config &c, int s)
 {
     return size_t(c.stages) * codec_entries(c) * 4 + size_t(s) * codec_entries(c) * 2;
 }
-inline size_t codec_total_bytes(const bsq_config &c) { return size_t(c.stages) * codec_entries(c) * 6; }
+inline size_t codec_tabh_offset(const bsq_config &c, int s)
+{
+    return size_t(c.stages) * codec_entries(c) * 6 + size_t(s) * codec_entries(c) * 2;
+}
+inline size_t codec_total_bytes(const bsq_config &c) { return size_t(c.stages) * codec_entries(c) * 8; }
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -49,6 +55,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f)
     if ((u & 0x7f800000u) == 0x7f800000u) return uint16_t((u >> 16) | ((u & 0xffffu) ? 0x40u : 0u));
     u += 0x7fffu + ((u >> 16) & 1u);
     return uint16_t(u >> 16);
+}
+
+// Two fp32 values rounded to bf16 (nearest even, as f32_to_bf16 for every
+// non-NaN input) in one v_cvt_pk_bf16_f32; lo in the low half.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi)
+{
+    typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+    typedef float f32x2_v __attribute__((ext_vector_type(2)));
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_v{lo, hi}, bf16x2_v));
 }
 
 __device__ __forceinline__ float f16_bits_to_f32(uint16_t h)
@@ -101,7 +116,7 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
                            const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
                            void *ws, hipStream_t st);
 
-size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_in, int64_t M);
+size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M);
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
                        const bsq_lora *lora, const void *X, int64_t M, int64_t ldx, void *Y,
                        int y_dtype, int64_t ldy, void *ws, hipStream_t st);

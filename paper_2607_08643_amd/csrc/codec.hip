@@ -3,7 +3,8 @@
 // compact symmetric decoder with one hidden ReLU layer). The fp32 table is
 // filled with the same fmaf chains, in the same element order, as the
 // definition of the encoder, so that encode and decode are exact; the bf16
-// table (round to nearest even) feeds the products.
+// table (round to nearest even) feeds the GEMV's products, the fp16 table
+// (round to nearest even) the GEMM's decode.
 #include "bsq_internal.h"
 
 namespace bsq {
@@ -16,6 +17,7 @@ struct TableArgs {
     const float *b2[BSQ_MAX_STAGES];
     float *t32[BSQ_MAX_STAGES];
     uint16_t *t16[BSQ_MAX_STAGES];
+    uint16_t *th[BSQ_MAX_STAGES];
     float cscale;  // (float)(1 / sqrt(b)), rounded once from double
     int kind;
     int hidden;
@@ -65,10 +67,12 @@ __global__ __launch_bounds__(256) void codec_table_kernel(TableArgs a)
     }
     float *o32 = a.t32[s] + size_t(code) * D;
     uint16_t *o16 = a.t16[s] + size_t(code) * D;
+    uint16_t *oh = a.th[s] + size_t(code) * D;
 #pragma unroll
     for (int m = 0; m < D; ++m) {
         o32[m] = y[m];
         o16[m] = f32_to_bf16(y[m]);
+        oh[m] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(y[m]));
     }
 }
 
@@ -85,6 +89,7 @@ hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, vo
         a.b2[s] = dec[s].b2;
         a.t32[s] = reinterpret_cast<float *>(base + codec_tab32_offset(cfg, s));
         a.t16[s] = reinterpret_cast<uint16_t *>(base + codec_tab16_offset(cfg, s));
+        a.th[s] = reinterpret_cast<uint16_t *>(base + codec_tabh_offset(cfg, s));
     }
     a.cscale = float(1.0 / __builtin_sqrt(double(cfg.b)));
     a.kind = cfg.dec_kind;

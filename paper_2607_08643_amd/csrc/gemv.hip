@@ -23,6 +23,12 @@
 namespace bsq {
 namespace {
 
+// Workspace: the LoRA vectors of up to BSQ_MAX_GROUP members, then the
+// flagged partial slots. The slots start at the same offset for every group
+// size, so a workspace shared by groups of different sizes keeps its slots
+// at zero between calls.
+constexpr size_t gemv_t_bytes() { return (size_t(BSQ_MAX_GROUP) * BSQ_MAX_LORA_RANK * 4 + 255) & ~size_t(255); }
+
 // row-lane kernel: polls of a row group's last slice for the other slices'
 // partial sums before it gives up and writes NaN (seconds; never expected)
 constexpr int LANE_SPIN_LIMIT = 1 << 22;
@@ -728,7 +734,7 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
     a.y_bf16 = (y_dtype == BSQ_BF16);
     float *wt = static_cast<float *>(ws);
     char *wb = static_cast<char *>(ws);
-    a.slots = reinterpret_cast<uint64_t *>(wb + align256(size_t(n) * BSQ_MAX_LORA_RANK * 4));
+    a.slots = reinterpret_cast<uint64_t *>(wb + gemv_t_bytes());
     for (int m = 0; m < n; ++m) {
         GemvMat &M = a.mat[m];
         const bsq_layer &L = layers[m];
@@ -771,7 +777,7 @@ size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_
     const int64_t rg = n * ((max_d_out + 63) / 64);
     const int64_t nblk = (d_in / cfg.d + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN;
     // LoRA vectors, then {flag, partial} slots for all but the last slice
-    return align256(size_t(n) * BSQ_MAX_LORA_RANK * 4) + size_t(rg) * size_t(lane_slices(nblk) - 1) * 64 * 8;
+    return gemv_t_bytes() + size_t(rg) * size_t(lane_slices(nblk) - 1) * 64 * 8;
 }
 
 size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_rpb)

@@ -201,8 +201,8 @@ def test_codec_prepare_rejects_before_launch():
     c = cfg.c()
     Lib = bsq.lib()
     need = bsq.bsq_codec_bytes(cfg)
-    assert need == 2 * 256 * 8 * 6
-    assert bsq.bsq_codec_bytes(bsq.Config(d=16, hidden=16)) == 2 * 65536 * 16 * 6
+    assert need == 2 * 256 * 8 * 8
+    assert bsq.bsq_codec_bytes(bsq.Config(d=16, hidden=16)) == 2 * 65536 * 16 * 8
     decs = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE)] * 4)
     assert Lib.bsq_codec_prepare(ct.byref(c), decs, ct.c_void_p(FAKE), need - 1, None) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
     assert Lib.bsq_codec_prepare(ct.byref(c), decs, ct.c_void_p(FAKE + 128), need, None) == bsq.BSQ_ERR_ALIGN

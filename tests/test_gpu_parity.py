@@ -195,8 +195,16 @@ def test_gemv_matches_oracle(case, with_lora, gpu):
                             rss=rss_terms(w_hat, xf, lref))
 
 
-@pytest.mark.parametrize("case", [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11]],
-                         ids=[c[0] for c in (SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11])])
+# Long rows: the K steps of a tile are split over several blocks (ragged
+# split sizes, a partial last step) and reduced by the last block to arrive.
+SPLITK = [
+    ("splitk-200x2600-d8", 200, 2600, dict(d=8, hidden=8), torch.bfloat16, 1, False),
+    ("splitk-130x2608-d16", 130, 2608, dict(d=16, hidden=16), torch.bfloat16, 1, False),
+]
+GEMM_CASES = [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11]] + SPLITK
+
+
+@pytest.mark.parametrize("case", GEMM_CASES, ids=[c[0] for c in GEMM_CASES])
 @pytest.mark.parametrize("M", [1, 5, 16, 64, 100, 256])
 def test_gemm_matches_oracle(case, M, gpu):
     say(f"case {case[0]} M={M}")
@@ -215,6 +223,32 @@ def test_gemm_matches_oracle(case, M, gpu):
     check_close(Y.cpu().numpy(), Y_ref, 2e-2, "gemm fp32 out", rss=rss_terms(w_hat, Xf, lref))
     Yb_ref = oracle.dense_product(w_hat, Xf)
     check_close(Yb.float().cpu().numpy(), Yb_ref, 2e-2, "gemm bf16 out", rss=rss_terms(w_hat, Xf))
+
+
+@pytest.mark.parametrize("d", [8, 16])
+def test_gemm_workspace_reuse(d, gpu):
+    """One zero-filled workspace for calls of different token counts: each
+    result equals the one from a fresh workspace, and the arrival counters
+    are back at zero after every call."""
+    say(f"gemm workspace reuse d={d}")
+    cfg = bsq.Config(d=d, hidden=d)
+    decs = decoders(cfg, seed=d + 3)
+    d_out, d_in = 1000, 2048
+    W, _ = synth.weight(d_out, d_in, seed=31, k_outliers=cfg.k(d_in), device=gpu)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W)
+    Ms = [16, 256, 5, 100, 16, 64, 256]
+    need = max(bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, d_out, d_in, M) for M in Ms)
+    raw = torch.zeros(need + 256, dtype=torch.uint8, device=gpu)
+    ws = raw[(-raw.data_ptr()) % 256:][:need]
+    A, Bm = synth.lora(d_out, d_in, 16, seed=4, device=gpu)
+    for i, M in enumerate(Ms):
+        X = synth.activation(d_in, seed=40 + i, device=gpu, batch=M)
+        Y = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.float32, ws=ws)
+        Y_fresh = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.float32)
+        torch.cuda.synchronize()
+        assert torch.equal(Y, Y_fresh), f"M={M}: shared-workspace result differs"
+        assert int(ws[:16384].view(torch.int32).abs().sum()) == 0, f"M={M}: counters not reset"
 
 
 def test_grouped_gemv_three_categories(gpu):
