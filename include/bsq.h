@@ -262,12 +262,12 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  *   X  device bf16 [M][ldx] (ldx >= d_in, multiple of 8)
  *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
  *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M),
- *      256-byte aligned, ZERO-FILLED before its first use: its first 16 KiB
- *      are per-tile arrival counters of the split-K reduction that every call
- *      leaves at zero again (the rest is scratch: X A^T and fp32 partial
- *      tiles). One workspace serves GEMM calls of any shape; it must not be
- *      shared with a GEMV workspace, and calls that share it must not
- *      overlap.
+ *      256-byte aligned, ZERO-FILLED before its first use: its first 8 MiB
+ *      hold the flagged fp32 partial tiles of the split-K reduction, which
+ *      every call leaves at zero again; the rest is scratch (X with the
+ *      protected columns zeroed, the gathered protected activations, X A^T).
+ *      One workspace serves GEMM calls of any shape; it must not be shared
+ *      with a GEMV workspace, and calls that share it must not overlap.
  * The K steps of a tile may be split over several blocks; their fp32
  * partials are summed in a fixed order, so results are deterministic. */
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer,

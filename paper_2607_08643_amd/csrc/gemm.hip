@@ -22,11 +22,12 @@
 // its activation as bf16 exactly once.
 //
 // Split K: when weight blocks x token tiles alone would leave the chip mostly
-// idle, the K steps are divided over ksplit blocks per tile (grid z). Each
-// writes its fp32 partial tile to the workspace with device-coherent stores
-// and bumps the tile's counter; the last to arrive sums the partials in split
-// order (so the result does not depend on arrival order), runs the epilogue
-// and sets the counter back to zero.
+// idle, the K steps are divided over ksplit blocks per tile (grid z). Splits
+// z < ksplit - 1 store their fp32 partial tile as flagged 64-bit slots
+// {1, value} (device-coherent stores, no fence) and exit; the last split,
+// dispatched after all the others, polls the slots, sums the partials in
+// split order (so the result does not depend on timing), clears the slots,
+// and runs the epilogue.
 #include <algorithm>
 #include <type_traits>
 
@@ -41,11 +42,14 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 128;    // inputs per K step
 
-// The arrival counters sit at a fixed place, the first GEMM_CNT_MAX words of
-// the workspace, whatever the shape: every call leaves them at zero, and no
-// other data of any GEMM call is ever written there, so one workspace serves
-// calls of different shapes.
-constexpr int64_t GEMM_CNT_MAX = 4096;
+// The flagged partial slots sit at a fixed place, the first GEMM_SLOT_BYTES
+// of the workspace, whatever the shape: every call leaves them at zero, and
+// no other data of any GEMM call is ever written there, so one workspace
+// serves calls of different shapes. The K split is capped to fit.
+constexpr int64_t GEMM_SLOT_BYTES = int64_t(8) << 20;
+// polls of the finishing split for the other splits' slots before it gives
+// up and writes NaN (seconds; never expected)
+constexpr int GEMM_SPIN_LIMIT = 1 << 22;
 
 struct GemmArgs {
     const void *codes[BSQ_MAX_STAGES];
@@ -61,9 +65,8 @@ struct GemmArgs {
     int64_t M, d_out, pitch, ksteps, Kp, k, kp32, ldy;
     void *Y;
     int y_bf16;
-    int ksplit;      // blocks per tile along K (grid z)
-    uint32_t *cnt;   // [tiles] arrival counters, zero between calls
-    float *part;     // [tiles][ksplit][BM * BN] fp32 partial tiles (ksplit > 1)
+    int ksplit;        // blocks per tile along K (grid z)
+    uint64_t *slots;   // [tiles][ksplit - 1][BM * BN] flagged partials, zero between calls
 };
 
 // ---------------------------------------------------------------------------
@@ -379,67 +382,65 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
         }
     }
 
+    bool timed_out = false;
     if (a.ksplit > 1) {
-        // partial tile in MFMA fragment order: float4 (wave, i, j) of each
-        // lane, stored and loaded as fp32 atomics (device scope)
-        __shared__ int s_last;
+        // partial tile in MFMA fragment order: slot ((wave MT + i) NT + j) 256
+        // + 64 r + lane of the split's [BM * BN] range
         const int64_t tile = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-        float *tp = a.part + tile * int64_t(a.ksplit) * (BM * BN);
-        auto frag = [&](int zz, int i, int j) { return tp + int64_t(zz) * (BM * BN) + int64_t(((wave * MT + i) * NT + j) * 64 + lane) * 4; };
+        uint64_t *tp = a.slots + tile * int64_t(a.ksplit - 1) * (BM * BN) + lane;
+        auto slot = [&](int zz, int i, int j, int r) { return tp + int64_t(zz) * (BM * BN) + ((wave * MT + i) * NT + j) * 256 + 64 * r; };
+        if (z < a.ksplit - 1) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
+            for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int j = 0; j < NT; ++j)
+                for (int j = 0; j < NT; ++j)
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    __hip_atomic_store(frag(z, i, j) + r, float(acc[i][j][r]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        // every wave's stores complete before the barrier (a workgroup
-        // barrier alone does not wait for them), so the counter release of
-        // thread 0 orders all of them
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
-        if (t == 0) {
-            const uint32_t prev = __hip_atomic_fetch_add(a.cnt + tile, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-            s_last = (prev == uint32_t(a.ksplit - 1));
+                    for (int r = 0; r < 4; ++r)
+                        __hip_atomic_store(slot(z, i, j, r), (uint64_t(1) << 32) | __float_as_uint(acc[i][j][r]),
+                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
         }
-        __syncthreads();
-        if (!s_last) return;
-        // Last block of the tile: every partial, its own included, is in
-        // device memory (each block's stores were ordered before its counter
-        // release); read with device-coherent loads, U splits in flight at a
-        // time, and summed in split order.
-        constexpr int U = (MT * NT >= 8) ? 1 : 8 / (MT * NT);
+        // the finishing split: partials of splits 0 .. ksplit - 2 in order,
+        // then its own
         f32x4_t sum[MT][NT];
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
             for (int j = 0; j < NT; ++j) sum[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        for (int zz = 0; zz < a.ksplit; zz += U) {
-            f32x4_t v[U][MT][NT];
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int zs = (zz + u < a.ksplit) ? zz + u : a.ksplit - 1;  // tail: harmless reload
+        for (int zz = 0; zz < a.ksplit - 1; ++zz) {
+            uint64_t pw[MT][NT][4];
+            for (int spin = 0;; ++spin) {
+                bool ready = true;
 #pragma unroll
                 for (int i = 0; i < MT; ++i)
 #pragma unroll
                     for (int j = 0; j < NT; ++j)
 #pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            v[u][i][j][r] = __hip_atomic_load(frag(zs, i, j) + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        for (int r = 0; r < 4; ++r) {
+                            pw[i][j][r] = __hip_atomic_load(slot(zz, i, j, r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            ready &= (pw[i][j][r] >> 32) != 0;
+                        }
+                if (__all(ready)) break;
+                if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
+                    timed_out = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(2);
             }
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (zz + u < a.ksplit)
+            for (int i = 0; i < MT; ++i)
 #pragma unroll
-                    for (int i = 0; i < MT; ++i)
+                for (int j = 0; j < NT; ++j)
 #pragma unroll
-                        for (int j = 0; j < NT; ++j) sum[i][j] += v[u][i][j];
+                    for (int r = 0; r < 4; ++r) {
+                        sum[i][j][r] += __uint_as_float(uint32_t(pw[i][j][r]));
+                        __hip_atomic_store(slot(zz, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    }
         }
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int j = 0; j < NT; ++j) acc[i][j] = sum[i][j];
-        if (t == 0) __hip_atomic_store(a.cnt + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int j = 0; j < NT; ++j) acc[i][j] = sum[i][j] + acc[i][j];
     }
 
     // epilogue: LoRA, then Y
@@ -456,7 +457,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
             for (int r = 0; r < 4; ++r) {
                 const int64_t m = m0 + 16 * i + 4 * g + r;
                 if (m >= a.M) continue;
-                float v = acc[i][j][r];
+                float v = timed_out ? __builtin_nanf("") : acc[i][j][r];
                 if (a.rank > 0) {
                     const float *Tm = a.T + m * BSQ_MAX_LORA_RANK;
 #pragma unroll
@@ -474,7 +475,7 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
 struct GemmPlan {
     int mt, nt;  // token groups and 64-row groups per block
     int64_t bm, bn, mtiles, nblk, ksteps, ksplit, Mp, Kp, kp32;
-    size_t t_off, xt_off, xp_off, part_off, total;
+    size_t t_off, xt_off, xp_off, total;
 };
 
 GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
@@ -494,19 +495,16 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     p.kp32 = (k + 31) & ~int64_t(31);
     const int64_t tiles = p.nblk * p.mtiles;
     // about two rounds of blocks over 256 CUs, at least 4 K steps per block,
-    // at most GEMM_PART_MAX bytes of partial tiles
-    constexpr int64_t GEMM_PART_MAX = int64_t(64) << 20;
+    // the flagged partials within GEMM_SLOT_BYTES
     int64_t ks = (2 * 256 * occ + tiles - 1) / (tiles > 0 ? tiles : 1);
     ks = std::min<int64_t>(ks, p.ksteps / 4);
-    ks = std::min<int64_t>(ks, GEMM_PART_MAX / std::max<int64_t>(1, tiles * p.bm * p.bn * 4));
+    ks = std::min<int64_t>(ks, 1 + GEMM_SLOT_BYTES / std::max<int64_t>(1, tiles * p.bm * p.bn * 8));
     ks = std::min<int64_t>(ks, 64);
-    if (tiles > GEMM_CNT_MAX) ks = 1;
     p.ksplit = std::max<int64_t>(ks, 1);
-    p.t_off = size_t(GEMM_CNT_MAX) * 4;
+    p.t_off = size_t(GEMM_SLOT_BYTES);
     p.xt_off = p.t_off + align256(size_t(p.Mp) * BSQ_MAX_LORA_RANK * 4);
     p.xp_off = p.xt_off + align256(size_t(p.Mp) * size_t(p.Kp) * 2);
-    p.part_off = p.xp_off + align256(size_t(p.Mp) * size_t(std::max<int64_t>(p.kp32, 32)) * 2);
-    p.total = p.part_off + (p.ksplit > 1 ? size_t(tiles) * size_t(p.ksplit) * size_t(p.bm * p.bn) * 4 : 0);
+    p.total = p.xp_off + align256(size_t(p.Mp) * size_t(std::max<int64_t>(p.kp32, 32)) * 2);
     return p;
 }
 
@@ -565,8 +563,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     a.y_bf16 = (y_dtype == BSQ_BF16);
     a.rank = 0;
     a.ksplit = int(p.ksplit);
-    a.cnt = static_cast<uint32_t *>(ws);
-    a.part = reinterpret_cast<float *>(wb + p.part_off);
+    a.slots = static_cast<uint64_t *>(ws);
 
     PrepArgs pa{};
     pa.X = static_cast<const uint16_t *>(X);
