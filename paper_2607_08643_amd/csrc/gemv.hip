@@ -341,91 +341,59 @@ __device__ __forceinline__ void lane_load(LaneBlk<S> &b, const GemvMat &M, int64
     }
 }
 
-template <int S>
-__device__ __forceinline__ float lane_block(const LaneBlk<S> &b, const uint32_t (&xm)[64], const uint4 *s_tab,
-                                            float acc)
-{
-#pragma unroll
-    for (int s = 0; s < S; ++s) {
-        const uint32_t cw[4] = {b.c[s].x, b.c[s].y, b.c[s].z, b.c[s].w};
-        const uint32_t gw[8] = {b.g[s][0].x, b.g[s][0].y, b.g[s][0].z, b.g[s][0].w,
-                                b.g[s][1].x, b.g[s][1].y, b.g[s][1].z, b.g[s][1].w};
-#pragma unroll
-        for (int kk = 0; kk < 16; ++kk) {
-            const uint32_t code = (cw[kk >> 2] >> (8 * (kk & 3))) & 0xffu;
-            const uint4 e = s_tab[s * 256 + code];
-            float dsum = dot2_bf16(e.x, xm[4 * kk + 0], 0.0f);
-            dsum = dot2_bf16(e.y, xm[4 * kk + 1], dsum);
-            dsum = dot2_bf16(e.z, xm[4 * kk + 2], dsum);
-            dsum = dot2_bf16(e.w, xm[4 * kk + 3], dsum);
-            const float g = (kk & 1) ? half_hi(gw[kk >> 1]) : half_lo(gw[kk >> 1]);
-            acc = __builtin_fmaf(g, dsum, acc);
-        }
-    }
-    return acc;
-}
-
-// Zero the protected columns of a 128-input activation block (bits: the
-// layer's bitmap, four words per block), in scalar registers.
-__device__ __forceinline__ void mask_block(uint32_t (&xm)[64], const uint32_t *bits, int64_t b)
-{
-    typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-    typedef const u32x4 __attribute__((address_space(4))) *cx4_ptr;
-    const u32x4 bw = ((cx4_ptr)(bits))[b];
-    if (bw[0] | bw[1] | bw[2] | bw[3]) {
-#pragma unroll
-        for (int kk = 0; kk < 16; ++kk) {
-            const uint32_t cb = (bw[kk >> 2] >> (8 * (kk & 3))) & 0xffu;
-            if (cb) {
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t b2 = cb >> (2 * q);
-                    xm[4 * kk + q] &= ((b2 & 1u) ? 0u : 0x0000ffffu) | ((b2 & 2u) ? 0u : 0xffff0000u);
-                }
-            }
-        }
-    }
-}
-
-// The LoRA term and the store of one output row (row < d_out).
+// The LoRA term and the store of one output row (row < d_out). The rank-16
+// row of B is loaded unconditionally (indices clamped to the rank) so that
+// its loads are in flight together.
 __device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMat &M, int64_t row, float acc)
 {
     if (M.rank > 0) {
         const uint16_t *br = M.B + row * M.rank;
         uint16_t bq[BSQ_MAX_LORA_RANK];
 #pragma unroll
-        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bq[q] = (q < M.rank) ? br[q] : uint16_t(0);
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bq[q] = br[(q < M.rank) ? q : M.rank - 1];
 #pragma unroll
-        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q)
-            if (q < M.rank) acc = __builtin_fmaf(bf16_to_f32(bq[q]), M.t[q], acc);
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) {
+            const float f = __builtin_fmaf(bf16_to_f32(bq[q]), M.t[q], acc);
+            acc = (q < M.rank) ? f : acc;
+        }
     }
     if (a.y_bf16) static_cast<uint16_t *>(M.y)[row] = f32_to_bf16(acc);
     else static_cast<float *>(M.y)[row] = acc;
 }
 
-// int8 protected columns, the LoRA term, and the store of one output row.
-// A lane reads its row's int8 codes (padded to 16) with up to eight 16-byte
-// loads issued together, and its LoRA row likewise, so the epilogue costs
-// about one memory round trip per 128 protected columns.
+// Sixteen protected columns of one row: int8 codes (one 16-byte word) against
+// the scaled activations xs[0 .. 15] (LDS, 16-byte aligned, zero past k).
+__device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc)
+{
+    const float4 *x4 = reinterpret_cast<const float4 *>(xs);
+    const float4 xa = x4[0], xb = x4[1], xc = x4[2], xd = x4[3];
+    const float xv[16] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w,
+                          xc.x, xc.y, xc.z, xc.w, xd.x, xd.y, xd.z, xd.w};
+    const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), xv[e], acc);
+    return acc;
+}
+
+// int8 protected columns, the LoRA term, and the store of one output row,
+// with the row's int8 codes read from global memory: four 16-byte words at a
+// time, all issued before any is used (indices clamped to the padded row,
+// words past it zeroed), then one word after the other.
 __device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M, const float *s_xs, int64_t row,
                                             float acc)
 {
     if (row >= M.d_out) return;
+    const int64_t nw = q8_pitch(a.k) / 16;  // 16-byte words per row
     const uint4 *qr = reinterpret_cast<const uint4 *>(M.q8 + row * q8_pitch(a.k));
-    for (int64_t p0 = 0; p0 < a.k; p0 += 128) {
-        uint4 qv[8];
+    for (int64_t w0 = 0; w0 < nw; w0 += 4) {
+        uint4 qv[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
-            if (p0 + 16 * u < a.k) qv[u] = qr[p0 / 16 + u];
+        for (int u = 0; u < 4; ++u) qv[u] = qr[(w0 + u < nw) ? w0 + u : nw - 1];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            if (p0 + 16 * u >= a.k) break;
-            const uint32_t qw[4] = {qv[u].x, qv[u].y, qv[u].z, qv[u].w};
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int64_t p = p0 + 16 * u + e;
-                if (p < a.k) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), s_xs[p], acc);
-            }
+        for (int u = 0; u < 4; ++u) {
+            const uint4 q = (w0 + u < nw) ? qv[u] : make_uint4(0, 0, 0, 0);
+            acc = q8_block(q, s_xs + 16 * ((w0 + u < nw) ? w0 + u : nw - 1), acc);
+            asm volatile("" : "+v"(acc));  // one word's activations live at a time
         }
     }
     lane_finish_lora(a, M, row, acc);
@@ -438,45 +406,120 @@ __device__ __forceinline__ void lane_finish_lds(const GemvArgs &a, const GemvMat
 {
     if (row >= M.d_out) return;
     if (!q8_lds || a.k == 0) {
-        lane_finish(a, M, s_xs, row, acc);
+        if (a.k > 0) lane_finish(a, M, s_xs, row, acc);
+        else lane_finish_lora(a, M, row, acc);
         return;
     }
-    const int64_t kp = q8_pitch(a.k);
-    const uint4 *qr = reinterpret_cast<const uint4 *>(s_q8 + (row & 63) * kp);
-    for (int64_t p0 = 0; p0 < a.k; p0 += 16) {
-        const uint4 qv = qr[p0 / 16];
-        const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-            const int64_t p = p0 + e;
-            if (p < a.k) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), s_xs[p], acc);
-        }
+    const int64_t nw = q8_pitch(a.k) / 16;
+    const uint4 *qr = reinterpret_cast<const uint4 *>(s_q8 + (row & 63) * q8_pitch(a.k));
+    int64_t w = 0;
+    for (; w + 2 <= nw; w += 2) {  // two words per step, their LDS reads together
+        const uint4 q0 = qr[w], q1 = qr[w + 1];
+        acc = q8_block(q0, s_xs + 16 * w, acc);
+        acc = q8_block(q1, s_xs + 16 * (w + 1), acc);
     }
+    if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc);
     lane_finish_lora(a, M, row, acc);
 }
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x16 __attribute__((ext_vector_type(16)));
+typedef const u32x4 __attribute__((address_space(4))) *cx4_ptr;
 typedef const u32x16 __attribute__((address_space(4))) *cx16_ptr;
 
-// One full tile: its 128 activations by scalar loads, masked, then decoded
-// and dotted.
+// Zero the protected inputs of one 32-input group held in scalar registers
+// (16 bf16 pairs); `bw` is the group's bitmap word, bit 2w (2w + 1) for the
+// low (high) half of word w. Straight-line scalar code under one uniform
+// branch: most groups hold no protected input.
+__device__ __forceinline__ u32x16 mask_group(u32x16 v, uint32_t bw)
+{
+    if (bw) {
+#pragma unroll
+        for (int w = 0; w < 16; ++w) {
+            const uint32_t lo = uint32_t(int32_t(bw << (31 - 2 * w)) >> 31);   // 0 or ~0
+            const uint32_t hi = uint32_t(int32_t(bw << (30 - 2 * w)) >> 31);
+            v[w] &= ~((lo & 0x0000ffffu) | (hi & 0xffff0000u));
+        }
+    }
+    return v;
+}
+
+// One 32-input group (chunks 4z .. 4z+3 of a tile) of the lane's row, all
+// stages: table entries from LDS, dotted with the wave-uniform activations.
 template <int S>
-__device__ __forceinline__ float lane_tile(const LaneBlk<S> &t, cx16_ptr xv, const uint32_t *bits, int64_t k,
+__device__ __forceinline__ float lane_group(const LaneBlk<S> &b, int z, const u32x16 &xz, const uint4 *s_tab,
+                                            float acc)
+{
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        const uint32_t cw = (z == 0) ? b.c[s].x : (z == 1) ? b.c[s].y : (z == 2) ? b.c[s].z : b.c[s].w;
+        const uint4 gq = b.g[s][z >> 1];
+        const uint32_t g0 = (z & 1) ? gq.z : gq.x;
+        const uint32_t g1 = (z & 1) ? gq.w : gq.y;
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+            const uint32_t code = (cw >> (8 * kk)) & 0xffu;
+            const uint4 e = s_tab[s * 256 + code];
+            float dsum = dot2_bf16(e.x, xz[4 * kk + 0], 0.0f);
+            dsum = dot2_bf16(e.y, xz[4 * kk + 1], dsum);
+            dsum = dot2_bf16(e.z, xz[4 * kk + 2], dsum);
+            dsum = dot2_bf16(e.w, xz[4 * kk + 3], dsum);
+            const uint32_t gw = (kk < 2) ? g0 : g1;
+            const float g = (kk & 1) ? half_hi(gw) : half_lo(gw);
+            acc = __builtin_fmaf(g, dsum, acc);
+        }
+    }
+    return acc;
+}
+
+// One full tile (128 inputs of block b): four groups of 32 activations, each
+// read with one scalar load and masked with its bitmap word. `bsrc` is the
+// bitmap (or, with no protected columns, any readable array of at least
+// 4 words per block, and kmask = 0).
+template <int S>
+__device__ __forceinline__ float lane_tile(const LaneBlk<S> &t, cx16_ptr xv, cx4_ptr bsrc, uint32_t kmask,
                                            int64_t b, const uint4 *s_tab, float acc)
 {
-    uint32_t xm[64];
+    const u32x4 bw = bsrc[b];
 #pragma unroll
     for (int z = 0; z < 4; ++z) {
-        const u32x16 v = xv[4 * b + z];
-#pragma unroll
-        for (int w = 0; w < 16; ++w) xm[16 * z + w] = v[w];
+        const u32x16 xz = mask_group(xv[4 * b + z], bw[z] & kmask);
+        acc = lane_group<S>(t, z, xz, s_tab, acc);
+        // finish each group before the next one (the compiler would otherwise
+        // defer the products past the masking branches and keep every group's
+        // table entries live)
+        asm volatile("" : "+v"(acc));
     }
-    if (k > 0) mask_block(xm, bits, b);
-    return lane_block<S>(t, xm, s_tab, acc);
+    return acc;
+}
+
+// The ragged last block of a row (d_in not a multiple of 128): activations
+// past d_in read as zero.
+template <int S>
+__device__ __forceinline__ float lane_tile_ragged(const LaneBlk<S> &t, const uint32_t *x32, int64_t d_in,
+                                                  cx4_ptr bsrc, uint32_t kmask, int64_t b, const uint4 *s_tab,
+                                                  float acc)
+{
+    typedef const uint32_t __attribute__((address_space(4))) *cu32_ptr;
+    const cu32_ptr xw = (cu32_ptr)(x32);
+    const u32x4 bw = bsrc[b];
+#pragma unroll
+    for (int z = 0; z < 4; ++z) {
+        u32x16 xz;
+#pragma unroll
+        for (int w = 0; w < 16; ++w) {
+            const int64_t col = b * 128 + 32 * z + 2 * w;
+            xz[w] = (col < d_in) ? xw[b * 64 + 16 * z + w] : 0u;
+        }
+        xz = mask_group(xz, bw[z] & kmask);
+        acc = lane_group<S>(t, z, xz, s_tab, acc);
+    }
+    return acc;
 }
 
 template <int S, int TPW>
-__global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 : 2))) void gemv_lane_kernel(
+    const GemvArgs a)
 {
     constexpr int WV = 4, NT = 256;      // waves per workgroup, threads
     constexpr int PF = TPW < 2 ? TPW : 2;  // tiles in flight per wave
@@ -538,63 +581,48 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
     for (int u = 0; u < PF; ++u) lane_load<S>(buf[u], M, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
     __builtin_amdgcn_sched_barrier(0);
     // protected index and scale of this thread's column, used at the end
-    int32_t pj = -1;
-    float psc = 0.0f;
-    if (a.k > 0) {
-        const int64_t pt = (t < a.k) ? t : a.k - 1;
-        pj = M.idx[pt];
-        psc = M.scale[pt];
-    }
-    // the table is in LDS once at most the tile (and index) loads are
+    // (unconditional loads, so that every path has the same loads in flight;
+    // with no protected columns they read x and are ignored)
+    const int64_t pt = (a.k > 0) ? ((t < a.k) ? t : a.k - 1) : 0;
+    const int32_t pj_raw = ((a.k > 0) ? M.idx : static_cast<const int32_t *>(a.x))[pt];
+    const float psc = ((a.k > 0) ? M.scale : static_cast<const float *>(a.x))[pt];
+    const int32_t pj = (a.k > 0) ? pj_raw : -1;
+    // the table is in LDS once at most the tile and index loads are
     // pending; a plain s_barrier (no release fence) lets those stay in flight
-    constexpr int NTILE = PF * 3 * S;
-    constexpr int NIDX = NTILE + 2;
-    if (a.k > 0) __builtin_amdgcn_s_waitcnt((NIDX & 15) | ((NIDX >> 4) << 14) | (7 << 4) | (15 << 8));
-    else __builtin_amdgcn_s_waitcnt((NTILE & 15) | ((NTILE >> 4) << 14) | (7 << 4) | (15 << 8));
+    constexpr int NIDX = PF * 3 * S + 2;
+    __builtin_amdgcn_s_waitcnt((NIDX & 15) | ((NIDX >> 4) << 14) | (7 << 4) | (15 << 8));
     asm volatile("s_barrier" ::: "memory");
 
     const cx16_ptr xv = (cx16_ptr)(a.x);
+    // the bitmap, or (no protected columns) x itself read under a zero mask,
+    // so that the per-tile bitmap load is unconditional
+    const cx4_ptr bsrc = (a.k > 0) ? (cx4_ptr)(M.bits) : (cx4_ptr)(a.x);
+    const uint32_t kmask = (a.k > 0) ? ~0u : 0u;
+    // the wave's TPW tiles as straight-line code with PF tiles in flight (no
+    // loop, so the waits before each tile count exactly the loads issued
+    // after it); tile indices are clamped to the wave's last full tile so
+    // every load is unconditional, and the sums of tiles past nt are dropped
     float acc = 0.0f;
-    int64_t i = 0;
-    for (; i + 2 * PF <= nt; i += PF) {
 #pragma unroll
-        for (int u = 0; u < PF; ++u) {
-            const int64_t b = b0 + i + u;
-            acc = lane_tile<S>(buf[u], xv, M.bits, a.k, b, s_tab, acc);
-            lane_load<S>(buf[u], M, tbase + ((b + PF) << 10));
-        }
-    }
-    // tail: PF .. 2 PF - 1 tiles left (or fewer than PF if nt < PF)
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-        if (i + u < nt) {
-            const int64_t b = b0 + i + u;
-            acc = lane_tile<S>(buf[u], xv, M.bits, a.k, b, s_tab, acc);
-            if (i + u + PF < nt) lane_load<S>(buf[u], M, tbase + ((b + PF) << 10));
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-        if (i + PF + u < nt) acc = lane_tile<S>(buf[u], xv, M.bits, a.k, b0 + i + PF + u, s_tab, acc);
+    for (int u = 0; u < TPW; ++u) {
+        const int64_t b = (b0 + u < blast) ? b0 + u : blast;
+        const float ts = lane_tile<S>(buf[u % PF], xv, bsrc, kmask, b, s_tab, 0.0f);
+        acc += (u < nt) ? ts : 0.0f;
+        if (u + PF < TPW)
+            lane_load<S>(buf[u % PF], M, tbase + (((b0 + u + PF < blast) ? b0 + u + PF : blast) << 10));
     }
     if (ragged) {
         const int64_t b = full_blocks;
         lane_load<S>(buf[0], M, tbase + (b << 10));
-        typedef const uint32_t __attribute__((address_space(4))) *cu32_ptr;
-        const cu32_ptr xw = (cu32_ptr)(a.x);
-        uint32_t xm[64];
-#pragma unroll
-        for (int z = 0; z < 64; ++z) xm[z] = (b * 128 + 2 * z < a.d_in) ? xw[b * 64 + z] : 0u;
-        if (a.k > 0) mask_block(xm, M.bits, b);
-        acc = lane_block<S>(buf[0], xm, s_tab, acc);
+        acc = lane_tile_ragged<S>(buf[0], static_cast<const uint32_t *>(a.x), a.d_in, bsrc, kmask, b, s_tab, acc);
     }
 
     // scaled protected activations for the epilogue (indices loaded above),
     // only in the finishing slice
     if (fin) {
-        if (t < a.k) s_xs[t] = (pj >= 0 && pj < a.d_in) ? psc * load_x(a.x, pj, 1) : 0.0f;
-        for (int64_t p = NT + t; p < a.k; p += NT) {  // more protected columns than threads
-            const int32_t j = M.idx[p];
+        if (t < kp) s_xs[t] = (t < a.k && pj >= 0 && pj < a.d_in) ? psc * load_x(a.x, pj, 1) : 0.0f;
+        for (int64_t p = NT + t; p < kp; p += NT) {  // more protected columns than threads
+            const int32_t j = (p < a.k) ? M.idx[p] : -1;
             s_xs[p] = (j >= 0 && j < a.d_in) ? M.scale[p] * load_x(a.x, j, 1) : 0.0f;
         }
     }
@@ -618,27 +646,28 @@ __global__ __launch_bounds__(256) void gemv_lane_kernel(const GemvArgs a)
     }
     float tot = 0.0f;
     bool timed_out = false;
-    for (int64_t q0 = 0; q0 < Q - 1; q0 += 16) {
-        uint64_t pw[16];
+    // the other slices' slots, eight at a time, all eight loads in flight
+    // together (slot indices clamped to the last one, extra copies unused)
+    constexpr int PW = 8;
+    for (int64_t q0 = 0; q0 < Q - 1; q0 += PW) {
+        uint64_t pw[PW];
         for (int spin = 0;; ++spin) {
+#pragma unroll
+            for (int u = 0; u < PW; ++u)
+                pw[u] = __hip_atomic_load(slots + ((q0 + u < Q - 1) ? q0 + u : Q - 2) * 64, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
             bool ready = true;
 #pragma unroll
-            for (int u = 0; u < 16; ++u) {
-                if (q0 + u < Q - 1) {
-                    pw[u] = __hip_atomic_load(slots + (q0 + u) * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    ready &= (pw[u] >> 32) != 0;
-                }
-            }
+            for (int u = 0; u < PW; ++u) ready &= (pw[u] >> 32) != 0;
             if (__all(ready)) break;
             if (spin == LANE_SPIN_LIMIT) {  // never expected: report NaN rather than hang
                 timed_out = true;
                 break;
             }
-            __builtin_amdgcn_s_sleep(2);
+            __builtin_amdgcn_s_sleep(1);
         }
 #pragma unroll
-        for (int u = 0; u < 16; ++u)
-            if (q0 + u < Q - 1) tot += __uint_as_float(uint32_t(pw[u]));
+        for (int u = 0; u < PW; ++u) tot += (q0 + u < Q - 1) ? __uint_as_float(uint32_t(pw[u])) : 0.0f;
     }
     tot += v;
     for (int64_t q0 = 0; q0 < Q - 1; ++q0)
@@ -721,6 +750,18 @@ hipError_t launch_stream(int stages, const GemvArgs &a, int nt, int grid, size_t
     return hipGetLastError();
 }
 
+template <int TPW>
+void launch_lane(int stages, const GemvArgs &a, int64_t blocks, size_t shm, hipStream_t st)
+{
+    const dim3 grid{unsigned(blocks)}, blk{256u};
+    switch (stages) {
+    case 1: hipLaunchKernelGGL((gemv_lane_kernel<1, TPW>), grid, blk, shm, st, a); break;
+    case 2: hipLaunchKernelGGL((gemv_lane_kernel<2, TPW>), grid, blk, shm, st, a); break;
+    case 3: hipLaunchKernelGGL((gemv_lane_kernel<3, TPW>), grid, blk, shm, st, a); break;
+    default: hipLaunchKernelGGL((gemv_lane_kernel<4, TPW>), grid, blk, shm, st, a); break;
+    }
+}
+
 GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                    const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype, void *ws)
 {
@@ -766,18 +807,29 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
 
 }  // namespace
 
-// Row-lane kernel: tiles per wave; a workgroup (4 waves) covers 4 * LANE_TPW
-// tiles, Q = ceil(nblk / (4 * LANE_TPW)) slices per 64-row group.
-constexpr int LANE_TPW = 4;
+// Row-lane kernel: a workgroup (4 waves) covers 4 * TPW consecutive tiles of
+// one 64-row group, so a row group has Q = ceil(nblk / (4 TPW)) slices. TPW is
+// the largest of 4, 2, 1 whose grid still holds LANE_MIN_WAVES waves (half of
+// the 4096 wave slots of 256 compute units at four waves per SIMD): fewer,
+// longer waves where the matrix is large, more slices where it is small.
+constexpr int64_t LANE_MIN_WAVES = 2048;
 
-int64_t lane_slices(int64_t nblk) { return (nblk + 4 * LANE_TPW - 1) / (4 * LANE_TPW); }
+int64_t lane_slices(int64_t nblk, int tpw) { return (nblk + 4 * tpw - 1) / (4 * tpw); }
+
+int lane_tpw(int64_t row_groups, int64_t nblk)
+{
+    for (int tpw = 4; tpw > 1; tpw >>= 1)
+        if (row_groups * lane_slices(nblk, tpw) * 4 >= LANE_MIN_WAVES) return tpw;
+    return 1;
+}
 
 size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in)
 {
     const int64_t rg = n * ((max_d_out + 63) / 64);
     const int64_t nblk = (d_in / cfg.d + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN;
     // LoRA vectors, then {flag, partial} slots for all but the last slice
-    return gemv_t_bytes() + size_t(rg) * size_t(lane_slices(nblk) - 1) * 64 * 8;
+    // (as many slices as the smallest TPW makes)
+    return gemv_t_bytes() + size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8;
 }
 
 size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_rpb)
@@ -814,8 +866,12 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
     if (D == 8) {
         // row-lane kernel: one workgroup per (64-row group, slice of tiles)
         a.nblk = a.pitch / 16;
-        a.q = lane_slices(a.nblk);
-        int64_t blocks = 0, rgs = 0;
+        int64_t rgs = 0;
+        for (int m = 0; m < n; ++m) rgs += (layers[m].d_out + 63) / 64;
+        const int tpw = lane_tpw(rgs, a.nblk);
+        a.q = lane_slices(a.nblk, tpw);
+        int64_t blocks = 0;
+        rgs = 0;
         for (int m = 0; m < n; ++m) {
             const int64_t nrg = (layers[m].d_out + 63) / 64;
             a.mat[m].block_begin = blocks;
@@ -826,11 +882,10 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
         const int64_t kp = q8_pitch(a.k);
         const size_t shm = size_t(S) * 256 * 16 + 4 * 64 * 4 + size_t(kp) * 4 +
                            ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
-        switch (S) {
-        case 1: hipLaunchKernelGGL((gemv_lane_kernel<1, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
-        case 2: hipLaunchKernelGGL((gemv_lane_kernel<2, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
-        case 3: hipLaunchKernelGGL((gemv_lane_kernel<3, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
-        default: hipLaunchKernelGGL((gemv_lane_kernel<4, LANE_TPW>), dim3(unsigned(blocks)), dim3(256), shm, st, a); break;
+        switch (tpw) {
+        case 4: launch_lane<4>(S, a, blocks, shm, st); break;
+        case 2: launch_lane<2>(S, a, blocks, shm, st); break;
+        default: launch_lane<1>(S, a, blocks, shm, st); break;
         }
         return hipGetLastError();
     }
