@@ -10,11 +10,12 @@ activations. The block is encoded R times from independent weights (8 copies,
 copies and the 256 MB last-level cache cannot hold the working set.
 
 A step is one decode token through the block: four grouped fused GEMVs
-(q/k/v, o, gate/up, down), each an activation prep and a streaming kernel,
-replayed from a HIP graph. `value` is the compressed bytes the step must move
-(code planes, gain planes, int8 payload, scales, indices, x, y) divided by the
-step time. Encode throughput (Mchunks/s), decode GB/s and the fused GEMM's
-TFLOP/s at M = 16/64/256 are measured in the same run on the same weights.
+(q/k/v, o, gate/up, down), each an activation prep and a streaming kernel.
+Steps are replayed from a HIP graph holding one pass over the copies. `value`
+is the compressed bytes the step must move (code planes, gain planes, int8
+payload, scales, indices, x, y) divided by the step time. Encode throughput
+(Mchunks/s), decode GB/s and the fused GEMM's TFLOP/s at M = 16/64/256 are
+measured in the same run on the same weights.
 
 `roofline` covers the dominant kernel (the streaming GEMV of the gate/up
 group): algorithmic bytes per launch / its mean launch time from HIP events
@@ -163,6 +164,9 @@ def main():
                 if r == 0:
                     step_bytes += algorithmic_bytes(layers, ps[0].d_in, sum(p.d_out for p in ps))
             plans.append(pr)
+        # one graph per copy (one step each) and one graph of a whole pass
+        # over the copies (R consecutive steps, so that a replay's launch cost
+        # is paid once per R steps, as a decode loop captured once would)
         s = torch.cuda.Stream()
         graphs = []
         with torch.cuda.stream(s):
@@ -176,16 +180,27 @@ def main():
                     for pl in plans[r]:
                         pl()
                 graphs.append(g)
+            g_pass = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_pass, stream=s):
+                for r in range(args.copies):
+                    for pl in plans[r]:
+                        pl()
         torch.cuda.synchronize()
         log(f"[bench] d={d}: {step_bytes / 1e6:.1f} MB per step; warmup {args.warmup}, timed {args.steps}")
-        for i in range(args.warmup):
-            graphs[i % args.copies].replay()
+
+        def run_steps(k):
+            # exactly k steps: whole passes, then single steps
+            for _ in range(k // args.copies):
+                g_pass.replay()
+            for i in range(k % args.copies):
+                graphs[i].replay()
+
+        run_steps(args.warmup)
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record()
-        for i in range(args.steps):
-            graphs[i % args.copies].replay()
+        run_steps(args.steps)
         t1.record()
         torch.cuda.synchronize()
         ms = t0.elapsed_time(t1) / args.steps
@@ -270,7 +285,7 @@ def main():
         if head is None:
             head = (blk, plans)
         else:
-            del blk, plans, graphs
+            del blk, plans, graphs, g_pass
         torch.cuda.synchronize()
 
     # same-box copy reference (and the calibration kernel for the byte

@@ -55,7 +55,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 2
+#define BSQ_ABI_VERSION 3
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -177,8 +177,12 @@ bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats
  * The buffer holds, per stage, an fp32 table [2^b][d] filled in the same fp32
  * operation order as the encoder's definition (so encode and decode are
  * exact), then a bf16 copy [2^b][d] for the GEMV's products and an fp16 copy
- * [2^b][d] for the GEMM's decode (both rounded to nearest even). One codec
- * per (category, stage set) serves every layer of that category.
+ * [2^b][d] for the GEMM's decode (both rounded to nearest even). For the
+ * symmetric decoder at d = 16 it also holds, per stage, the hidden
+ * pre-activation W1 q + b1 split by code byte (two fp16 tables [256][h] whose
+ * entries add up to it) and copies of W2 and b2, from which the GEMV
+ * evaluates that decoder. One codec per (category, stage set) serves every
+ * layer of that category.
  * bsq_codec_bytes: required size (host only).
  * bsq_codec_prepare: `dec` is a host array of `stages` bsq_decoder structs
  * whose tensors are device pointers; `codec` is a device buffer of at least
@@ -228,8 +232,11 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
  *   y       host array [n] of device outputs [d_out_g], y_dtype (bf16 or fp32)
  *   ws      device workspace of bsq_workspace_bytes(GEMV, n, max d_out, d_in),
  *           256-byte aligned, ZERO-FILLED before its first use: it holds the
- *           LoRA vectors A_g x and flagged per-row partial sums that every
- *           call leaves at zero again. Calls that share a workspace must
+ *           LoRA vectors A_g x, the folded activations of the d = 16
+ *           symmetric decoder (see bsq_gemv_prepare) and flagged per-row
+ *           partial sums that every call leaves at zero again. A workspace
+ *           serves calls of one configuration and one d_in (any group size
+ *           and d_out it was sized for); calls that share a workspace must
  *           not overlap.
  * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
  * fp32 decoder table and fp32 arithmetic throughout.
@@ -239,14 +246,21 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
                     const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
                     void *ws, size_t ws_bytes, void *stream);
 
-/* Activation preparation of the GEMV that needs a reduction over all of x:
- * writes the LoRA vectors t_g = A_g x (fp32, 16 per member) into `ws`.
- * Launches nothing when no member has a LoRA adapter. Arguments as for
- * bsq_gemv. (Masking x and scaling the protected activations happen inside
+/* Activation preparation of the GEMV: work that needs a reduction over all
+ * of x, written into `ws` (one launch):
+ *  - the LoRA vectors t_g = A_g x (fp32, 16 per member);
+ *  - for the symmetric decoder at d = 16 with hidden width 16 and bf16 x, the
+ *    decoder's output layer folded into the masked activations: per member,
+ *    stage and chunk c, u = W2^T x~_c and b2 . x~_c (so that
+ *    <D(code), x~_c> = <relu(W1 q + b1), u> + b2 . x~_c), u stored in fp16
+ *    with a power-of-two scale.
+ * Launches nothing when neither applies. Arguments as for bsq_gemv; `codecs`
+ * may be NULL unless the folded activations are needed. (Masking x for the
+ * other configurations and scaling the protected activations happen inside
  * bsq_gemv_run.) */
-bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const bsq_layer *layers,
-                            const bsq_lora *loras, const void *x, int32_t x_dtype,
-                            void *ws, size_t ws_bytes, void *stream);
+bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const *codecs,
+                            const bsq_layer *layers, const bsq_lora *loras, const void *x,
+                            int32_t x_dtype, void *ws, size_t ws_bytes, void *stream);
 
 /* The streaming product of the GEMV, alone: reads x, the code and gain
  * planes, the int8 payload and LoRA B once, and the LoRA vectors that a

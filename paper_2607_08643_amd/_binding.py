@@ -73,7 +73,7 @@ EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes
            "bsq_gemv_run", "bsq_gemm")
 
 # struct layouts above follow this version of include/bsq.h
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 _lib = None
 
@@ -99,7 +99,7 @@ def lib():
     L.bsq_encode.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
     L.bsq_decode.argtypes = [P, P, P, P, I32, P]
     L.bsq_gemv.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
-    L.bsq_gemv_prepare.argtypes = [P, I32, P, P, P, I32, P, SZ, P]
+    L.bsq_gemv_prepare.argtypes = [P, I32, P, P, P, P, I32, P, SZ, P]
     L.bsq_gemv_run.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
     L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P]
     for f in EXPORTS[2:]:
@@ -406,9 +406,10 @@ class GemvPlan:
         return self.out
 
     def prepare(self, stream=None):
-        """bsq_gemv_prepare: the LoRA vectors A x (no launch without LoRA)."""
-        _check(lib().bsq_gemv_prepare(ct.byref(self._c), self.n, self._layers, self._loras, _ptr(self.x),
-                                      self._xd, _ptr(self.ws), self.ws.numel(), _stream(stream)),
+        """bsq_gemv_prepare: the LoRA vectors A x and, for the d = 16 symmetric
+        decoder, the folded activations (no launch when neither applies)."""
+        _check(lib().bsq_gemv_prepare(ct.byref(self._c), self.n, self._codecs, self._layers, self._loras,
+                                      _ptr(self.x), self._xd, _ptr(self.ws), self.ws.numel(), _stream(stream)),
                "bsq_gemv_prepare")
 
     def run(self, stream=None):

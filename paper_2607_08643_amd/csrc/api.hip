@@ -249,7 +249,11 @@ bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codec
         if (loras && (s = check_lora(&loras[m])) != BSQ_OK) return s;
     }
     if (!aligned(ws, 256)) return BSQ_ERR_ALIGN;
-    if (x_dtype == BSQ_BF16 && cfg->d == 16 && layers[0].pitch * cfg->d / 128 > 512) return BSQ_ERR_UNSUPPORTED;
+    // the d = 16 streaming kernel (decoders other than the width-16 symmetric
+    // one) holds one 128-input segment per thread of a 512-thread block
+    const bool split16 = codec_has_split(*cfg) && cfg->hidden == 16;
+    if (x_dtype == BSQ_BF16 && cfg->d == 16 && !split16 && layers[0].pitch * cfg->d / 128 > 512)
+        return BSQ_ERR_UNSUPPORTED;
     if (x_dtype == BSQ_BF16 && layers[0].k > 4096) return BSQ_ERR_UNSUPPORTED;
     int64_t max_d_out = 0;
     for (int m = 0; m < n; ++m) max_d_out = layers[m].d_out > max_d_out ? layers[m].d_out : max_d_out;
@@ -259,14 +263,18 @@ bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codec
 
 }  // namespace
 
-bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const bsq_layer *layers, const bsq_lora *loras,
-                            const void *x, int32_t x_dtype, void *ws, size_t ws_bytes, void *stream)
+bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                            const bsq_lora *loras, const void *x, int32_t x_dtype, void *ws, size_t ws_bytes,
+                            void *stream)
 {
-    bsq_status s = check_gemv(cfg, n, nullptr, layers, loras, x_dtype, nullptr, BSQ_F32, ws, ws_bytes);
+    bsq_status s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, nullptr, BSQ_F32, ws, ws_bytes);
     if (s != BSQ_OK) return s;
     if (!x) return BSQ_ERR_ARG;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
-    return from_hip(launch_gemv_prep(*cfg, n, layers, loras, x, x_dtype, ws, static_cast<hipStream_t>(stream)));
+    // the d = 16 symmetric decoder folds its output layer into x here
+    if (!codecs && codec_has_split(*cfg) && x_dtype == BSQ_BF16) return BSQ_ERR_ARG;
+    return from_hip(
+        launch_gemv_prep(*cfg, n, codecs, layers, loras, x, x_dtype, ws, static_cast<hipStream_t>(stream)));
 }
 
 bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
@@ -290,7 +298,7 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
     if (s != BSQ_OK) return s;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((s = from_hip(launch_gemv_prep(*cfg, n, layers, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
+    if ((s = from_hip(launch_gemv_prep(*cfg, n, codecs, layers, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
     return from_hip(launch_gemv_run(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws, st));
 }
 

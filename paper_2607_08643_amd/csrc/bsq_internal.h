@@ -15,6 +15,14 @@ namespace bsq {
 // nearest even, consumed by the GEMV's bf16 products), then for each stage an
 // fp16 table [2^b][d] (rounded to nearest even, consumed by the GEMM's decode
 // through mixed-precision fma).
+//
+// The symmetric decoder at d = b = 16 also gets, per stage, its hidden
+// pre-activation split by code byte: fp16 [2][h/8][256][8], half 0 holding
+// b1 + W1[:, 0:8] q(v) and half 1 W1[:, 8:16] q(v) for every byte v (so the
+// pre-activation of a code is the sum of one entry of each half; each entry
+// is stored as h/8 groups of eight units, 16 bytes each), followed by fp32
+// copies of W2 [d][h] and b2 [d]. The GEMV folds W2 and b2 into the
+// activations and evaluates the decoder from these halves.
 // ---------------------------------------------------------------------------
 inline size_t codec_entries(const bsq_config &c) { return (size_t(1) << c.b) * size_t(c.d); }
 inline size_t codec_tab32_offset(const bsq_config &c, int s) { return size_t(s) * codec_entries(c) * 4; }
@@ -26,7 +34,25 @@ inline size_t codec_tabh_offset(const bsq_config &c, int s)
 {
     return size_t(c.stages) * codec_entries(c) * 6 + size_t(s) * codec_entries(c) * 2;
 }
-inline size_t codec_total_bytes(const bsq_config &c) { return size_t(c.stages) * codec_entries(c) * 8; }
+inline bool codec_has_split(const bsq_config &c) { return c.dec_kind == BSQ_DEC_MLP && c.d == 16 && c.b == 16; }
+// one stage's split tables and decoder copies
+inline size_t codec_split_stage_bytes(const bsq_config &c)
+{
+    return codec_has_split(c) ? size_t(2) * 256 * c.hidden * 2 + size_t(c.d) * c.hidden * 4 + size_t(c.d) * 4 : 0;
+}
+inline size_t codec_split_offset(const bsq_config &c, int s)
+{
+    return size_t(c.stages) * codec_entries(c) * 8 + size_t(s) * codec_split_stage_bytes(c);
+}
+inline size_t codec_w2_offset(const bsq_config &c, int s)
+{
+    return codec_split_offset(c, s) + size_t(2) * 256 * c.hidden * 2;
+}
+inline size_t codec_b2_offset(const bsq_config &c, int s) { return codec_w2_offset(c, s) + size_t(c.d) * c.hidden * 4; }
+inline size_t codec_total_bytes(const bsq_config &c)
+{
+    return size_t(c.stages) * codec_entries(c) * 8 + size_t(c.stages) * codec_split_stage_bytes(c);
+}
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -110,8 +136,8 @@ hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_lay
                          void *w_hat, int out_dtype, hipStream_t st);
 
 size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in);
-hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const bsq_layer *layers, const bsq_lora *loras,
-                            const void *x, int x_dtype, void *ws, hipStream_t st);
+hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
+                            const bsq_lora *loras, const void *x, int x_dtype, void *ws, hipStream_t st);
 hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                            const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
                            void *ws, hipStream_t st);

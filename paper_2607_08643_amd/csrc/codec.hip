@@ -4,7 +4,9 @@
 // filled with the same fmaf chains, in the same element order, as the
 // definition of the encoder, so that encode and decode are exact; the bf16
 // table (round to nearest even) feeds the GEMV's products, the fp16 table
-// (round to nearest even) the GEMM's decode.
+// (round to nearest even) the GEMM's decode. For the symmetric decoder at
+// d = 16 the hidden pre-activation is also tabulated per code byte (two
+// halves whose entries add up to it), the form the d = 16 GEMV evaluates.
 #include "bsq_internal.h"
 
 namespace bsq {
@@ -76,6 +78,47 @@ __global__ __launch_bounds__(256) void codec_table_kernel(TableArgs a)
     }
 }
 
+struct SplitArgs {
+    const float *W1[BSQ_MAX_STAGES];
+    const float *b1[BSQ_MAX_STAGES];
+    const float *W2[BSQ_MAX_STAGES];
+    const float *b2[BSQ_MAX_STAGES];
+    uint16_t *split[BSQ_MAX_STAGES];  // fp16 [2][256][h]
+    float *w2[BSQ_MAX_STAGES];        // fp32 [16][h]
+    float *b2c[BSQ_MAX_STAGES];       // fp32 [16]
+    float cscale;
+    int hidden;
+};
+
+// One block per stage, one thread per byte v: half 0 of the hidden
+// pre-activation is the fmaf chain b1_k + sum_{j<8} W1[k][j] q_j(v), half 1
+// the chain 0 + sum_{j<8} W1[k][8 + j] q_j(v) (q_j(v) = +c if bit j of v is
+// set, else -c), both rounded to fp16 (nearest even). Stored as
+// [half][k / 8][v][k % 8]: the 16-byte groups of eight hidden units of all
+// bytes v are contiguous, so that a lookup's 16-byte reads spread over every
+// LDS bank.
+__global__ __launch_bounds__(256) void codec_split_kernel(SplitArgs a)
+{
+    const int s = blockIdx.x;
+    const uint32_t v = threadIdx.x;
+    const int h = a.hidden;
+    const float *W1 = a.W1[s];
+    float q[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) q[j] = ((v >> j) & 1u) ? a.cscale : -a.cscale;
+    for (int half = 0; half < 2; ++half) {
+        for (int k = 0; k < h; ++k) {
+            float acc = half ? 0.0f : a.b1[s][k];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) acc = __builtin_fmaf(W1[k * 16 + 8 * half + j], q[j], acc);
+            a.split[s][((size_t(half) * ((h + 7) / 8) + k / 8) * 256 + v) * 8 + k % 8] =
+                __builtin_bit_cast(uint16_t, static_cast<_Float16>(acc));
+        }
+    }
+    for (int e = int(v); e < 16 * h; e += 256) a.w2[s][e] = a.W2[s][e];
+    if (v < 16) a.b2c[s][v] = a.b2[s][v];
+}
+
 }  // namespace
 
 hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, void *codec, hipStream_t st)
@@ -100,6 +143,21 @@ hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, vo
         hipLaunchKernelGGL(codec_table_kernel<8>, grid, dim3(256), 0, st, a);
     else
         hipLaunchKernelGGL(codec_table_kernel<16>, grid, dim3(256), 0, st, a);
+    if (codec_has_split(cfg)) {
+        SplitArgs sa{};
+        for (int s = 0; s < cfg.stages; ++s) {
+            sa.W1[s] = dec[s].W1;
+            sa.b1[s] = dec[s].b1;
+            sa.W2[s] = dec[s].W2;
+            sa.b2[s] = dec[s].b2;
+            sa.split[s] = reinterpret_cast<uint16_t *>(base + codec_split_offset(cfg, s));
+            sa.w2[s] = reinterpret_cast<float *>(base + codec_w2_offset(cfg, s));
+            sa.b2c[s] = reinterpret_cast<float *>(base + codec_b2_offset(cfg, s));
+        }
+        sa.cscale = a.cscale;
+        sa.hidden = cfg.hidden;
+        hipLaunchKernelGGL(codec_split_kernel, dim3(unsigned(cfg.stages)), dim3(256), 0, st, sa);
+    }
     return hipGetLastError();
 }
 

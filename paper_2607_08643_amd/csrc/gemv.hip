@@ -29,6 +29,18 @@ namespace {
 // at zero between calls.
 constexpr size_t gemv_t_bytes() { return (size_t(BSQ_MAX_GROUP) * BSQ_MAX_LORA_RANK * 4 + 255) & ~size_t(255); }
 
+// The d = 16 symmetric decoder path (hidden width 16) evaluates the decoder
+// from split pre-activation tables and folded activations.
+inline bool gemv_split16(const bsq_config &cfg) { return codec_has_split(cfg) && cfg.hidden == 16; }
+
+// Workspace of that path: a 64-byte folded-activation record per (member,
+// stage, chunk), for BSQ_MAX_GROUP members so that the slots behind it start
+// at the same offset for every group size of one configuration and d_in.
+inline size_t gemv_xp_bytes(const bsq_config &cfg, int64_t pitch)
+{
+    return gemv_split16(cfg) ? size_t(BSQ_MAX_GROUP) * cfg.stages * size_t(pitch) * 64 : 0;
+}
+
 // row-lane kernel: polls of a row group's last slice for the other slices'
 // partial sums before it gives up and writes NaN (seconds; never expected)
 constexpr int LANE_SPIN_LIMIT = 1 << 22;
@@ -71,6 +83,12 @@ struct GemvMat {
     const uint16_t *B;  // LoRA B [d_out][rank], bf16
     int rank;
     const uint32_t *bits;  // protected-column bitmap [pitch * d / 32]
+    // d = 16 symmetric decoder: split pre-activation tables (fp16 [2][2][256][8])
+    // and the fp32 W2 [16][16], b2 [16] of each stage
+    const uint16_t *split[BSQ_MAX_STAGES];
+    const float *w2[BSQ_MAX_STAGES];
+    const float *b2[BSQ_MAX_STAGES];
+    uint32_t *xp;  // workspace: folded activation records [S][pitch][16] (d = 16 decoder path)
     int64_t d_out;
     int64_t block_begin;  // first block of this member in the grid
     int64_t rg_begin;     // row-lane kernel: first 64-row group of this member (partial-sum slots)
@@ -80,7 +98,7 @@ struct GemvMat {
 
 struct GemvArgs {
     GemvMat mat[BSQ_MAX_GROUP];
-    int n;
+    int n, stages;
     int64_t d_in, pitch, k, nseg, rs, rpb;
     int64_t nblk, q;   // row-lane kernel: 16-chunk blocks per row, slices per 64-row group
     uint64_t *slots;   // row-lane kernel: {flag, partial} [row groups][q - 1][64], zero between calls
@@ -94,26 +112,83 @@ __device__ __forceinline__ float load_x(const void *x, int64_t j, int bf)
 }
 
 // ---------------------------------------------------------------------------
-// LoRA prep: t[m][r] = sum_j A[r][j] x_j (unmasked x), one block per (m, r).
+// Activation prep, one launch:
+//  * blocks [0, n * 16): the LoRA vectors t[m][r] = sum_j A[r][j] x_j
+//    (unmasked x), one block per (member, rank index);
+//  * the rest (d = 16 symmetric decoder only): one block per (member,
+//    stage, 16 chunks), sixteen threads per chunk c, fold the decoder's
+//    output layer into the masked activations of the chunk:
+//    u_k = sum_i W2[i][k] x~_{16c+i} and beta = sum_i b2[i] x~_{16c+i}, so
+//    that <D(code), x~_c> = <relu(a), u> + beta with a the hidden
+//    pre-activation of the code. The record is u in fp16 scaled by 2^-e (e
+//    puts max |u| in [2^13, 2^14), so no u overflows or loses range), then
+//    beta 2^-e and 2^e as fp32, in a 64-byte slot. Chunks past the row
+//    (pitch padding) get zeros.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void gemv_lora_prep_kernel(const GemvArgs a)
+__global__ __launch_bounds__(256) void gemv_prep_kernel(const GemvArgs a, int lora_blocks)
 {
     __shared__ float red[256];
-    const int m = blockIdx.x / BSQ_MAX_LORA_RANK;
-    const int r = blockIdx.x % BSQ_MAX_LORA_RANK;
     const int t = threadIdx.x;
-    const GemvMat &M = a.mat[m];
-    if (r >= M.rank) return;
-    float acc = 0.0f;
-    for (int64_t j = t; j < a.d_in; j += 256)
-        acc = __builtin_fmaf(bf16_to_f32(M.A[int64_t(r) * a.d_in + j]), load_x(a.x, j, a.x_bf16), acc);
-    red[t] = acc;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-        if (t < o) red[t] += red[t + o];
+    if (int(blockIdx.x) < lora_blocks) {
+        const int m = blockIdx.x / BSQ_MAX_LORA_RANK;
+        const int r = blockIdx.x % BSQ_MAX_LORA_RANK;
+        const GemvMat &M = a.mat[m];
+        if (r >= M.rank) return;
+        float acc = 0.0f;
+        for (int64_t j = t; j < a.d_in; j += 256)
+            acc = __builtin_fmaf(bf16_to_f32(M.A[int64_t(r) * a.d_in + j]), load_x(a.x, j, a.x_bf16), acc);
+        red[t] = acc;
         __syncthreads();
+        for (int o = 128; o > 0; o >>= 1) {
+            if (t < o) red[t] += red[t + o];
+            __syncthreads();
+        }
+        if (t == 0) M.t[r] = red[0];
+        return;
     }
-    if (t == 0) M.t[r] = red[0];
+    // folded activations: one block per (member, stage, 16-chunk block),
+    // thread t = 16 (chunk in the block) + hidden unit k
+    __shared__ float s_w2[256], s_b2[16], s_x[16][17];
+    const int64_t bid = int64_t(blockIdx.x) - lora_blocks;
+    const int64_t nblk = a.pitch / 16;
+    const int m = int(bid / (int64_t(a.stages) * nblk));
+    if (m >= a.n) return;
+    const int s = int((bid / nblk) % a.stages);
+    const int64_t c = (bid % nblk) * 16 + t / 16;
+    const int k = t & 15;
+    const GemvMat &M = a.mat[m];
+    s_w2[t] = M.w2[s][t];  // W2 [i][k], i the output element
+    if (t < 16) s_b2[t] = M.b2[s][t];
+    {
+        const int64_t col = 16 * c + k;  // this thread's element of the chunk
+        float v = (col < a.d_in) ? load_x(a.x, col, a.x_bf16) : 0.0f;
+        if (a.k > 0 && col < a.d_in && ((M.bits[col >> 5] >> (col & 31)) & 1u)) v = 0.0f;
+        s_x[t / 16][k] = v;
+    }
+    __syncthreads();
+    const float *xc = s_x[t / 16];
+    float u = 0.0f, beta = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        u = __builtin_fmaf(s_w2[i * 16 + k], xc[i], u);
+        beta = __builtin_fmaf(s_b2[i], xc[i], beta);
+    }
+    float amax = __builtin_fabsf(u);
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) amax = __builtin_fmaxf(amax, __shfl_xor(amax, o, 16));
+    int e = 0;
+    if (amax > 0.0f && amax <= 3.0e38f) {
+        int ex;
+        __builtin_frexpf(amax, &ex);  // amax = f 2^ex, f in [0.5, 1)
+        e = ex - 14;
+        e = (e < -110) ? -110 : (e > 110 ? 110 : e);
+    }
+    uint32_t *rec = M.xp + (int64_t(s) * a.pitch + c) * 16;
+    reinterpret_cast<uint16_t *>(rec)[k] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(__builtin_ldexpf(u, -e)));
+    if (k == 0) {
+        rec[8] = __float_as_uint(__builtin_ldexpf(beta, -e));
+        rec[9] = __float_as_uint(__builtin_ldexpf(1.0f, e));
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -323,18 +398,20 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
 // The tile loop is branch-free around its loads: a conditional load makes
 // the compiler wait for it at once, which would leave one tile in flight.
 // ---------------------------------------------------------------------------
-template <int S>
+template <int D, int S>
 struct LaneBlk {
-    uint4 c[S];     // 16 codes of the lane's row
-    uint4 g[S][2];  // 16 fp16 gains
+    uint4 c[S][D / 8];  // 16 codes of the lane's row (one byte each at d = 8, two at d = 16)
+    uint4 g[S][2];      // 16 fp16 gains
 };
 
-template <int S>
-__device__ __forceinline__ void lane_load(LaneBlk<S> &b, const GemvMat &M, int64_t off)
+template <int D, int S>
+__device__ __forceinline__ void lane_load(LaneBlk<D, S> &b, const GemvMat &M, int64_t off)
 {
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-        b.c[s] = *reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(M.codes[s]) + off);
+        const uint4 *cp = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(M.codes[s]) + off * (D / 8));
+#pragma unroll
+        for (int h = 0; h < D / 8; ++h) b.c[s][h] = cp[h];
         const uint4 *gp = reinterpret_cast<const uint4 *>(M.gains[s] + off);
         b.g[s][0] = gp[0];
         b.g[s][1] = gp[1];
@@ -447,12 +524,12 @@ __device__ __forceinline__ u32x16 mask_group(u32x16 v, uint32_t bw)
 // One 32-input group (chunks 4z .. 4z+3 of a tile) of the lane's row, all
 // stages: table entries from LDS, dotted with the wave-uniform activations.
 template <int S>
-__device__ __forceinline__ float lane_group(const LaneBlk<S> &b, int z, const u32x16 &xz, const uint4 *s_tab,
+__device__ __forceinline__ float lane_group(const LaneBlk<8, S> &b, int z, const u32x16 &xz, const uint4 *s_tab,
                                             float acc)
 {
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-        const uint32_t cw = (z == 0) ? b.c[s].x : (z == 1) ? b.c[s].y : (z == 2) ? b.c[s].z : b.c[s].w;
+        const uint32_t cw = (z == 0) ? b.c[s][0].x : (z == 1) ? b.c[s][0].y : (z == 2) ? b.c[s][0].z : b.c[s][0].w;
         const uint4 gq = b.g[s][z >> 1];
         const uint32_t g0 = (z & 1) ? gq.z : gq.x;
         const uint32_t g1 = (z & 1) ? gq.w : gq.y;
@@ -473,17 +550,17 @@ __device__ __forceinline__ float lane_group(const LaneBlk<S> &b, int z, const u3
 }
 
 // One full tile (128 inputs of block b): four groups of 32 activations, each
-// read with one scalar load and masked with its bitmap word. `bsrc` is the
-// bitmap (or, with no protected columns, any readable array of at least
-// 4 words per block, and kmask = 0).
+// read with one scalar load (xb: the tile's activations, 4 groups) and
+// masked with its bitmap word. `bsrc` is the bitmap (or, with no protected
+// columns, any readable array of at least 4 words per block, and kmask = 0).
 template <int S>
-__device__ __forceinline__ float lane_tile(const LaneBlk<S> &t, cx16_ptr xv, cx4_ptr bsrc, uint32_t kmask,
+__device__ __forceinline__ float lane_tile(const LaneBlk<8, S> &t, cx16_ptr xb, cx4_ptr bsrc, uint32_t kmask,
                                            int64_t b, const uint4 *s_tab, float acc)
 {
     const u32x4 bw = bsrc[b];
 #pragma unroll
     for (int z = 0; z < 4; ++z) {
-        const u32x16 xz = mask_group(xv[4 * b + z], bw[z] & kmask);
+        const u32x16 xz = mask_group(xb[z], bw[z] & kmask);
         acc = lane_group<S>(t, z, xz, s_tab, acc);
         // finish each group before the next one (the compiler would otherwise
         // defer the products past the masking branches and keep every group's
@@ -496,7 +573,7 @@ __device__ __forceinline__ float lane_tile(const LaneBlk<S> &t, cx16_ptr xv, cx4
 // The ragged last block of a row (d_in not a multiple of 128): activations
 // past d_in read as zero.
 template <int S>
-__device__ __forceinline__ float lane_tile_ragged(const LaneBlk<S> &t, const uint32_t *x32, int64_t d_in,
+__device__ __forceinline__ float lane_tile_ragged(const LaneBlk<8, S> &t, const uint32_t *x32, int64_t d_in,
                                                   cx4_ptr bsrc, uint32_t kmask, int64_t b, const uint4 *s_tab,
                                                   float acc)
 {
@@ -517,15 +594,81 @@ __device__ __forceinline__ float lane_tile_ragged(const LaneBlk<S> &t, const uin
     return acc;
 }
 
-template <int S, int TPW>
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+// c + <relu(lo + hi), u> over one pair of fp16 lanes (packed add and max,
+// then v_dot2_f32_f16 with fp32 accumulation)
+__device__ __forceinline__ float relu_dot2_f16(uint32_t lo, uint32_t hi, uint32_t u, float c)
+{
+    const half2_t pre = __builtin_bit_cast(half2_t, lo) + __builtin_bit_cast(half2_t, hi);
+    const half2_t act = __builtin_elementwise_max(pre, half2_t{0, 0});
+    return __builtin_amdgcn_fdot2(act, __builtin_bit_cast(half2_t, u), c, false);
+}
+
+// One tile of the d = 16 symmetric decoder (16 chunks of the lane's row, all
+// stages). Per chunk and stage: the code's hidden pre-activation is the sum
+// of the two split-table entries of its bytes (fp16, from LDS), the ReLU is
+// taken in fp16, and the dot with the chunk's folded activation record (u in
+// fp16, beta and the scale 2^e; staged in LDS for the workgroup's columns)
+// is accumulated in fp32. `bl` is the tile's column block within the slice,
+// `rch` the slice's chunks per stage.
+template <int S>
+__device__ __forceinline__ float lane_tile16(const LaneBlk<16, S> &t, const uint4 *s_rec, int rch, int bl,
+                                             const uint4 *s_split, float acc)
+{
+#pragma unroll
+    for (int kk = 0; kk < 16; ++kk) {
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            const uint4 cq = t.c[s][kk >> 3];
+            const uint32_t cwd = ((kk & 7) >> 1) == 0 ? cq.x : ((kk & 7) >> 1) == 1 ? cq.y : ((kk & 7) >> 1) == 2 ? cq.z : cq.w;
+            const uint32_t code = (kk & 1) ? (cwd >> 16) : (cwd & 0xffffu);
+            // the chunk's record (LDS, wave-uniform address): u, then beta, 2^e
+            const uint4 *rp = s_rec + (s * rch + bl * 16 + kk) * 4;
+            const uint4 r0 = rp[0], r1 = rp[1];
+            const uint2 r2 = *reinterpret_cast<const uint2 *>(rp + 2);
+            // split tables [S][half][2][256] x 16 B: hidden units 0-7 and
+            // 8-15 of a byte's entry are 4 KiB apart
+            const uint4 *pl = s_split + (s * 4 + 0) * 256 + (code & 0xffu);
+            const uint4 *ph = s_split + (s * 4 + 2) * 256 + (code >> 8);
+            const uint4 l0 = pl[0], l1 = pl[256], h0 = ph[0], h1 = ph[256];
+            const uint32_t lw[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+            const uint32_t hw[8] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
+            // (the words are bit-cast inside a helper: bit-casting elements of a
+            // scalar-loaded vector in place was once compiled to read element 0
+            // for every pair)
+            const uint32_t rw[10] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w, r2.x, r2.y};
+            float dsum = __uint_as_float(rw[8]);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) dsum = relu_dot2_f16(lw[i], hw[i], rw[i], dsum);
+            dsum *= __uint_as_float(rw[9]);
+            const uint4 gq = t.g[s][kk >> 3];
+            const uint32_t gw = ((kk & 7) >> 1) == 0 ? gq.x : ((kk & 7) >> 1) == 1 ? gq.y : ((kk & 7) >> 1) == 2 ? gq.z : gq.w;
+            const float gv = (kk & 1) ? half_hi(gw) : half_lo(gw);
+            acc = __builtin_fmaf(gv, dsum, acc);
+        }
+        asm volatile("" : "+v"(acc));  // one chunk's entries and record live at a time
+    }
+    return acc;
+}
+
+template <int D, int S, int TPW>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 : 2))) void gemv_lane_kernel(
     const GemvArgs a)
 {
     constexpr int WV = 4, NT = 256;      // waves per workgroup, threads
     constexpr int PF = TPW < 2 ? TPW : 2;  // tiles in flight per wave
+    // LDS table: d = 8, [S][256] bf16 decoder entries (16 B); d = 16, the
+    // split pre-activation tables [S][2][2][256] (16 B groups)
+    constexpr int TAB = (D == 8) ? S * 256 : S * 1024;  // uint4 units
+    // d = 16: the folded activation records of the slice's columns,
+    // [S][RCH chunks] 64-byte slots
+    constexpr int RCH = WV * TPW * 16;
+    constexpr int REC = (D == 8) ? 0 : S * RCH * 4;  // uint4 units
     extern __shared__ uint4 s_mem[];
-    uint4 *s_tab = s_mem;                                      // [S][256] entries of 8 bf16
-    float *s_red = reinterpret_cast<float *>(s_mem + S * 256);  // [WV][64] wave sums
+    uint4 *s_tab = s_mem;
+    uint4 *s_rec = s_mem + TAB;
+    float *s_red = reinterpret_cast<float *>(s_mem + TAB + REC);  // [WV][64] wave sums
     float *s_xs = s_red + WV * 64;                             // [kp] scale_p * x_{idx_p}
     const int64_t kp = q8_pitch(a.k);
     int8_t *s_q8 = reinterpret_cast<int8_t *>(s_xs + kp);      // [64][kp] int8 rows (finishing slice)
@@ -543,7 +686,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // this wave's tiles [b0, b1); those whose 128 columns are all real go
     // through the pipelined loop, a ragged last tile of the row (d_in not a
     // multiple of 128) is handled after it
-    const int64_t full_blocks = (a.d_in / 8) / 16;
+    const int64_t full_blocks = (D == 8) ? (a.d_in / 8) / 16 : nblk;  // d = 16: padding chunks read zeros
     const int64_t b0 = (q * WV + wave) * TPW;
     const int64_t b1 = (b0 + TPW < nblk) ? b0 + TPW : nblk;
     const int64_t nt = ((b1 < full_blocks) ? b1 : full_blocks) - b0;  // may be <= 0
@@ -556,12 +699,28 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // first tiles, so that the wait before the barrier covers the table but
     // not the tiles. Tile indices are clamped so every load is in bounds and
     // unconditional (a wave without tiles reloads its row group's first tile).
-    static_assert((S * 256) % NT == 0, "table chunks are shared out evenly");
+    static_assert(TAB % NT == 0, "table chunks are shared out evenly");
 #pragma unroll
-    for (int r = 0; r < S * 256 / NT; ++r) {
-        const int c = r * WV + wave;  // 64-entry chunk of the [S][256] table
-        const uint4 *src = reinterpret_cast<const uint4 *>(M.tab16[c >> 2]) + (c & 3) * 64 + lane;
+    for (int r = 0; r < TAB / NT; ++r) {
+        const int c = r * WV + wave;  // 1 KiB chunk of the table: 64 lanes x 16 B
+        const uint4 *src = (D == 8) ? reinterpret_cast<const uint4 *>(M.tab16[c >> 2]) + (c & 3) * 64 + lane
+                                    : reinterpret_cast<const uint4 *>(M.split[c >> 4]) + (c & 15) * 64 + lane;
         __builtin_amdgcn_global_load_lds(src, s_tab + c * 64, 16, 0, 0);
+    }
+    if constexpr (D == 16) {
+        // the slice's records, 16 per wave instruction (four lanes per 64-byte
+        // slot); chunks past the row's padded end read the last slot (unused)
+        static_assert((S * RCH / 16) % WV == 0, "record chunks are shared out evenly");
+        const int64_t c0 = q * RCH;  // the slice's first chunk
+#pragma unroll
+        for (int r = 0; r < S * RCH / 16 / WV; ++r) {
+            const int e = r * WV + wave;
+            const int s = e / (RCH / 16);
+            const int64_t cc = c0 + (e % (RCH / 16)) * 16 + lane / 4;
+            const uint4 *src = reinterpret_cast<const uint4 *>(
+                M.xp + (int64_t(s) * a.pitch + ((cc < a.pitch) ? cc : a.pitch - 1)) * 16) + (lane & 3);
+            __builtin_amdgcn_global_load_lds(src, s_rec + e * 64, 16, 0, 0);
+        }
     }
     // the finishing slice brings its row group's int8 rows to LDS the same way
     // (rows past d_out get clamped copies and are never read)
@@ -575,10 +734,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
         }
     }
     __builtin_amdgcn_sched_barrier(0);
-    const int64_t blast = (nt > 0) ? b0 + nt - 1 : 0;
-    LaneBlk<S> buf[PF];
+    // a wave without a full tile works on the slice's first block (always a
+    // real block) and drops the result
+    const int64_t blast = (nt > 0) ? b0 + nt - 1 : q * WV * TPW;
+    LaneBlk<D, S> buf[PF];
 #pragma unroll
-    for (int u = 0; u < PF; ++u) lane_load<S>(buf[u], M, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
+    for (int u = 0; u < PF; ++u) lane_load<D, S>(buf[u], M, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
     __builtin_amdgcn_sched_barrier(0);
     // protected index and scale of this thread's column, used at the end
     // (unconditional loads, so that every path has the same loads in flight;
@@ -589,7 +750,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     const int32_t pj = (a.k > 0) ? pj_raw : -1;
     // the table is in LDS once at most the tile and index loads are
     // pending; a plain s_barrier (no release fence) lets those stay in flight
-    constexpr int NIDX = PF * 3 * S + 2;
+    constexpr int NIDX = PF * (D / 8 + 2) * S + 2;
     __builtin_amdgcn_s_waitcnt((NIDX & 15) | ((NIDX >> 4) << 14) | (7 << 4) | (15 << 8));
     asm volatile("s_barrier" ::: "memory");
 
@@ -606,15 +767,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
         const int64_t b = (b0 + u < blast) ? b0 + u : blast;
-        const float ts = lane_tile<S>(buf[u % PF], xv, bsrc, kmask, b, s_tab, 0.0f);
+        float ts;
+        // (a dropped tile reads its activations from the decoder table, which
+        // is at least 4 KiB, so that no read goes past a short row's x)
+        if constexpr (D == 8)
+            ts = lane_tile<S>(buf[u % PF], (u < nt) ? xv + 4 * b : (cx16_ptr)(M.tab16[0]), bsrc, kmask, b, s_tab,
+                              0.0f);
+        else ts = lane_tile16<S>(buf[u % PF], s_rec, RCH, int(b - q * WV * TPW), s_tab, 0.0f);
         acc += (u < nt) ? ts : 0.0f;
         if (u + PF < TPW)
-            lane_load<S>(buf[u % PF], M, tbase + (((b0 + u + PF < blast) ? b0 + u + PF : blast) << 10));
+            lane_load<D, S>(buf[u % PF], M, tbase + (((b0 + u + PF < blast) ? b0 + u + PF : blast) << 10));
     }
-    if (ragged) {
-        const int64_t b = full_blocks;
-        lane_load<S>(buf[0], M, tbase + (b << 10));
-        acc = lane_tile_ragged<S>(buf[0], static_cast<const uint32_t *>(a.x), a.d_in, bsrc, kmask, b, s_tab, acc);
+    if constexpr (D == 8) {
+        if (ragged) {
+            const int64_t b = full_blocks;
+            lane_load<D, S>(buf[0], M, tbase + (b << 10));
+            acc = lane_tile_ragged<S>(buf[0], static_cast<const uint32_t *>(a.x), a.d_in, bsrc, kmask, b, s_tab,
+                                      acc);
+        }
     }
 
     // scaled protected activations for the epilogue (indices loaded above),
@@ -750,15 +920,15 @@ hipError_t launch_stream(int stages, const GemvArgs &a, int nt, int grid, size_t
     return hipGetLastError();
 }
 
-template <int TPW>
+template <int D, int TPW>
 void launch_lane(int stages, const GemvArgs &a, int64_t blocks, size_t shm, hipStream_t st)
 {
     const dim3 grid{unsigned(blocks)}, blk{256u};
     switch (stages) {
-    case 1: hipLaunchKernelGGL((gemv_lane_kernel<1, TPW>), grid, blk, shm, st, a); break;
-    case 2: hipLaunchKernelGGL((gemv_lane_kernel<2, TPW>), grid, blk, shm, st, a); break;
-    case 3: hipLaunchKernelGGL((gemv_lane_kernel<3, TPW>), grid, blk, shm, st, a); break;
-    default: hipLaunchKernelGGL((gemv_lane_kernel<4, TPW>), grid, blk, shm, st, a); break;
+    case 1: hipLaunchKernelGGL((gemv_lane_kernel<D, 1, TPW>), grid, blk, shm, st, a); break;
+    case 2: hipLaunchKernelGGL((gemv_lane_kernel<D, 2, TPW>), grid, blk, shm, st, a); break;
+    case 3: hipLaunchKernelGGL((gemv_lane_kernel<D, 3, TPW>), grid, blk, shm, st, a); break;
+    default: hipLaunchKernelGGL((gemv_lane_kernel<D, 4, TPW>), grid, blk, shm, st, a); break;
     }
 }
 
@@ -773,9 +943,10 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
     a.x = x;
     a.x_bf16 = (x_dtype == BSQ_BF16);
     a.y_bf16 = (y_dtype == BSQ_BF16);
+    a.stages = cfg.stages;
     float *wt = static_cast<float *>(ws);
     char *wb = static_cast<char *>(ws);
-    a.slots = reinterpret_cast<uint64_t *>(wb + gemv_t_bytes());
+    a.slots = reinterpret_cast<uint64_t *>(wb + gemv_t_bytes() + gemv_xp_bytes(cfg, a.pitch));
     for (int m = 0; m < n; ++m) {
         GemvMat &M = a.mat[m];
         const bsq_layer &L = layers[m];
@@ -786,8 +957,14 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
             if (cb) {
                 M.tab16[s] = reinterpret_cast<const uint16_t *>(cb + codec_tab16_offset(cfg, s));
                 M.tab32[s] = reinterpret_cast<const float *>(cb + codec_tab32_offset(cfg, s));
+                if (codec_has_split(cfg)) {
+                    M.split[s] = reinterpret_cast<const uint16_t *>(cb + codec_split_offset(cfg, s));
+                    M.w2[s] = reinterpret_cast<const float *>(cb + codec_w2_offset(cfg, s));
+                    M.b2[s] = reinterpret_cast<const float *>(cb + codec_b2_offset(cfg, s));
+                }
             }
         }
+        M.xp = reinterpret_cast<uint32_t *>(wb + gemv_t_bytes()) + int64_t(m) * cfg.stages * a.pitch * 16;
         M.idx = L.prot_idx;
         M.q8 = L.prot_q8;
         M.scale = L.prot_scale;
@@ -827,9 +1004,11 @@ size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_
 {
     const int64_t rg = n * ((max_d_out + 63) / 64);
     const int64_t nblk = (d_in / cfg.d + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN;
-    // LoRA vectors, then {flag, partial} slots for all but the last slice
-    // (as many slices as the smallest TPW makes)
-    return gemv_t_bytes() + size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8;
+    // LoRA vectors, folded activation records (d = 16 decoder path), then
+    // {flag, partial} slots for all but the last slice (as many slices as the
+    // smallest TPW makes)
+    return gemv_t_bytes() + gemv_xp_bytes(cfg, nblk * BSQ_PITCH_ALIGN) +
+           size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8;
 }
 
 size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_rpb)
@@ -840,14 +1019,17 @@ size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_r
            size_t((words + 3) & ~int64_t(3)) * 4 + size_t(k) * 4;
 }
 
-hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const bsq_layer *layers, const bsq_lora *loras,
-                            const void *x, int x_dtype, void *ws, hipStream_t st)
+hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
+                            const bsq_lora *loras, const void *x, int x_dtype, void *ws, hipStream_t st)
 {
     bool any = false;
     for (int m = 0; m < n && loras; ++m) any |= (loras[m].rank > 0);
-    if (!any) return hipSuccess;
-    const GemvArgs a = make_args(cfg, n, nullptr, layers, loras, x, x_dtype, nullptr, BSQ_F32, ws);
-    hipLaunchKernelGGL(gemv_lora_prep_kernel, dim3(unsigned(n * BSQ_MAX_LORA_RANK)), dim3(256), 0, st, a);
+    const bool fold = gemv_split16(cfg) && x_dtype == BSQ_BF16;
+    if (!any && !fold) return hipSuccess;
+    const GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, nullptr, BSQ_F32, ws);
+    const int lora_blocks = any ? n * BSQ_MAX_LORA_RANK : 0;
+    const int64_t fold_blocks = fold ? int64_t(n) * cfg.stages * (a.pitch / 16) : 0;
+    hipLaunchKernelGGL(gemv_prep_kernel, dim3(unsigned(lora_blocks + fold_blocks)), dim3(256), 0, st, a, lora_blocks);
     return hipGetLastError();
 }
 
@@ -863,7 +1045,7 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
     if (x_dtype != BSQ_BF16)
         return (D == 8) ? launch_f32<8>(S, a, rows_total, st) : launch_f32<16>(S, a, rows_total, st);
 
-    if (D == 8) {
+    if (D == 8 || gemv_split16(cfg)) {
         // row-lane kernel: one workgroup per (64-row group, slice of tiles)
         a.nblk = a.pitch / 16;
         int64_t rgs = 0;
@@ -880,12 +1062,20 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
             rgs += nrg;
         }
         const int64_t kp = q8_pitch(a.k);
-        const size_t shm = size_t(S) * 256 * 16 + 4 * 64 * 4 + size_t(kp) * 4 +
-                           ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
-        switch (tpw) {
-        case 4: launch_lane<4>(S, a, blocks, shm, st); break;
-        case 2: launch_lane<2>(S, a, blocks, shm, st); break;
-        default: launch_lane<1>(S, a, blocks, shm, st); break;
+        const size_t tab = (D == 8) ? size_t(S) * 256 * 16 : size_t(S) * 1024 * 16 + size_t(S) * 4 * tpw * 16 * 64;
+        const size_t shm = tab + 4 * 64 * 4 + size_t(kp) * 4 + ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
+        if (D == 8) {
+            switch (tpw) {
+            case 4: launch_lane<8, 4>(S, a, blocks, shm, st); break;
+            case 2: launch_lane<8, 2>(S, a, blocks, shm, st); break;
+            default: launch_lane<8, 1>(S, a, blocks, shm, st); break;
+            }
+        } else {
+            switch (tpw) {
+            case 4: launch_lane<16, 4>(S, a, blocks, shm, st); break;
+            case 2: launch_lane<16, 2>(S, a, blocks, shm, st); break;
+            default: launch_lane<16, 1>(S, a, blocks, shm, st); break;
+            }
         }
         return hipGetLastError();
     }

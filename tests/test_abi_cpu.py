@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 2
+    assert bsq.bsq_version() == 3
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -202,7 +202,11 @@ def test_codec_prepare_rejects_before_launch():
     Lib = bsq.lib()
     need = bsq.bsq_codec_bytes(cfg)
     assert need == 2 * 256 * 8 * 8
-    assert bsq.bsq_codec_bytes(bsq.Config(d=16, hidden=16)) == 2 * 65536 * 16 * 8
+    # d = 16 symmetric decoder: the four tables, then per stage the byte-split
+    # pre-activation halves (fp16 [2][256][h]) and fp32 copies of W2 and b2
+    split = 2 * 256 * 16 * 2 + 16 * 16 * 4 + 16 * 4
+    assert bsq.bsq_codec_bytes(bsq.Config(d=16, hidden=16)) == 2 * 65536 * 16 * 8 + 2 * split
+    assert bsq.bsq_codec_bytes(bsq.Config(d=16, kind=bsq.DEC_LINEAR)) == 2 * 65536 * 16 * 8
     decs = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE)] * 4)
     assert Lib.bsq_codec_prepare(ct.byref(c), decs, ct.c_void_p(FAKE), need - 1, None) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
     assert Lib.bsq_codec_prepare(ct.byref(c), decs, ct.c_void_p(FAKE + 128), need, None) == bsq.BSQ_ERR_ALIGN

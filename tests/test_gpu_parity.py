@@ -125,6 +125,8 @@ SMALL = [
     ("stack2-40x640-d16-fp32", 40, 640, dict(d=16, hidden=16), torch.float32, 2, False),
     ("g-128x640-d8", 128, 640, dict(d=8, hidden=8), torch.bfloat16, 1, True),
     ("rho25-64x256-d8", 64, 256, dict(d=8, hidden=8, protect_num=1, protect_den=4), torch.bfloat16, 1, False),
+    ("mlp-3stage-100x768-d16", 100, 768, dict(d=16, hidden=16, stages=3), torch.bfloat16, 1, False),
+    ("stack2-130x1056-d16", 130, 1056, dict(d=16, hidden=16), torch.bfloat16, 2, False),
 ]
 
 
@@ -195,6 +197,24 @@ def test_gemv_matches_oracle(case, with_lora, gpu):
                             rss=rss_terms(w_hat, xf, lref))
 
 
+@pytest.mark.parametrize("scale", [2.0 ** 24, 2.0 ** -24], ids=["huge", "tiny"])
+def test_gemv_d16_activation_range(scale, gpu):
+    """The d = 16 decoder path folds W2 into x and keeps the result in fp16
+    with a power-of-two scale per chunk: activations far outside fp16's range
+    must still give the oracle's product within tolerance."""
+    case = ("range-192x1024-d16", 192, 1024, dict(d=16, hidden=16), torch.bfloat16, 1, False)
+    say(f"case {case[0]} x scale {scale}")
+    cfg, decs, codec, layer, W, encs, tabs = _make(*case, gpu)
+    oc = ocfg(cfg)
+    x = (synth.activation(1024, seed=5, dtype=torch.float32) * scale).to(torch.bfloat16)
+    y = bsq.bsq_gemv(cfg, codec, layer, x.to(gpu), y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    xf = oracle.to_f32(x)
+    w_hat = oracle.decode(oc, decs, encs[0], tables=tabs)
+    y_ref = oracle.dense_product(w_hat, xf, None)
+    check_close(y.float().cpu().numpy(), y_ref, 2e-2, f"gemv x*{scale}", rss=rss_terms(w_hat, xf, None))
+
+
 # Long rows: the K steps of a tile are split over several blocks (ragged
 # split sizes, a partial last step) and reduced by the last block to arrive.
 SPLITK = [
@@ -251,12 +271,13 @@ def test_gemm_workspace_reuse(d, gpu):
         assert int(torch.count_nonzero(ws[:8 << 20])) == 0, f"M={M}: split-K slots not cleared"
 
 
-def test_grouped_gemv_three_categories(gpu):
+@pytest.mark.parametrize("d", [8, 16])
+def test_grouped_gemv_three_categories(d, gpu):
     """q/k/v-like group: one x, three matrices of different heights, three codecs."""
-    say("grouped qkv-like 320/96/96 x 1024")
+    say(f"grouped qkv-like 320/96/96 x 1024 d={d}")
     d_in = 1024
     outs = [320, 96, 96]
-    cfg = bsq.Config(d=8, hidden=8)
+    cfg = bsq.Config(d=d, hidden=d)
     oc = ocfg(cfg)
     x = synth.activation(d_in, seed=1)
     codecs, layers, encs, decs_all, loras = [], [], [], [], []
