@@ -131,7 +131,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__rest
     extern __shared__ uint32_t s_bits[];  // [words], the padded columns of one matrix
     __shared__ uint32_t hist[256];
     __shared__ unsigned long long s_prefix;
-    __shared__ long long s_remaining;
+    __shared__ long long s_remaining, s_next_remaining;
     __shared__ int s_wave[TOPK_THREADS / 64 + 1];
 
     const int64_t m = blockIdx.x;
@@ -158,18 +158,33 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__rest
             if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255ull], 1u);
         }
         __syncthreads();
-        if (t == 0) {
-            long long rem = s_remaining, cum = 0;
-            for (int dgt = 255; dgt >= 0; --dgt) {
-                long long h = hist[dgt];
-                if (cum + h >= rem) {
-                    s_prefix = prefix | (static_cast<unsigned long long>(dgt) << shift);
-                    s_remaining = rem - cum;
-                    break;
-                }
-                cum += h;
+        // the digit holding the rem-th largest key: with cum(dgt) the count of
+        // keys in digits above dgt, the unique dgt with cum < rem <= cum + h.
+        // Threads 0..255 (whole waves) own digit 255 - t; an inclusive scan
+        // over those four waves gives cum + h of every digit.
+        unsigned h = 0, incl = 0;
+        if (t < 256) {
+            h = hist[255 - t];
+            incl = h;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const unsigned y = __shfl_up(incl, o, 64);
+                if ((t & 63) >= o) incl += y;
+            }
+            if ((t & 63) == 63) s_wave[t >> 6] = int(incl);
+        }
+        __syncthreads();
+        if (t < 256) {
+            for (int w = 0; w < (t >> 6); ++w) incl += unsigned(s_wave[w]);
+            const long long rem = s_remaining;
+            const long long cum = (long long)(incl - h);
+            if (cum < rem && rem <= (long long)incl) {
+                s_prefix = prefix | (static_cast<unsigned long long>(255 - t) << shift);
+                s_next_remaining = rem - cum;
             }
         }
+        __syncthreads();
+        if (t == 0) s_remaining = s_next_remaining;
         mask |= 255ull << shift;
         __syncthreads();
     }
@@ -235,17 +250,11 @@ struct EncodeArgs {
 };
 
 // one element of the tiled planes (padding rows and chunks included):
-// consecutive elements are consecutive code and gain words
+// matrix m, row i, chunk c, at plane position gid
 template <int D, int S, typename T>
-__device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, int64_t gid)
+__device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, int64_t m, int64_t i,
+                                               int64_t c, int64_t gid)
 {
-    const int64_t per_mat = plane_elems(a.d_out, a.pitch);
-    const int64_t m = gid / per_mat;
-    const int64_t e = gid - m * per_mat;
-    const int64_t tile = e >> 10;
-    const int64_t nb = a.pitch >> 4;
-    const int64_t i = (tile / nb) * 64 + ((e >> 4) & 63);
-    const int64_t c = (tile % nb) * 16 + (e & 15);
     using code_t = typename std::conditional<D == 8, uint8_t, uint16_t>::type;
 
     if (c >= a.C || i >= a.d_out) {
@@ -349,8 +358,11 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
     }
 }
 
-// The element loop is grid-stride, so the decoder tables (d = 8) are staged in
-// LDS once per block rather than once per 256 chunks.
+// A block walks whole 64-row x 16-chunk tiles (grid-stride), so the decoder
+// tables (d = 8) are staged in LDS once per block, and a tile's matrix, row
+// group and column block come from one scalar division per tile. Thread t
+// takes elements t, t + 256, ... of the tile: a wave covers four rows of 16
+// consecutive chunks, so its row reads are contiguous.
 template <int D, int S, typename T>
 __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
 {
@@ -362,16 +374,26 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
         }
         __syncthreads();
     }
-    for (int64_t gid = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; gid < a.total;
-         gid += int64_t(gridDim.x) * blockDim.x)
-        encode_element<D, S, T>(a, s_tab, gid);
+    const int64_t nb = a.pitch >> 4;
+    const int64_t tiles_per_mat = ((a.d_out + 63) >> 6) * nb;
+    const int64_t ntiles = a.total >> 10;
+    for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+        const int64_t m = tile / tiles_per_mat;
+        const int64_t rem = tile - m * tiles_per_mat;
+        const int64_t rg = rem / nb, blk = rem - rg * nb;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = q * 256 + int(threadIdx.x);
+            encode_element<D, S, T>(a, s_tab, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), (tile << 10) + e);
+        }
+    }
 }
 
 template <int D, typename T>
 hipError_t launch_encode_chunks(int stages, const EncodeArgs &a, hipStream_t st)
 {
-    // at most about 16 blocks per CU; each walks its share of the elements
-    int64_t blocks = (a.total + 255) / 256;
+    // at most about 16 blocks per CU; each walks its share of the tiles
+    int64_t blocks = a.total >> 10;
     if (blocks > 4096) blocks = 4096;
     const dim3 grid = dim3(unsigned(blocks));
     const size_t shm = (D == 8) ? size_t(stages) * 256 * 8 * 4 : 0;
