@@ -56,6 +56,8 @@ def parse():
     p.add_argument("--no-gemm", action="store_true")
     p.add_argument("--profile-gemv-only", action="store_true",
                    help="only run the GEMV steps (for rocprofv3 counter passes)")
+    p.add_argument("--no-stacks", action="store_true",
+                   help="skip the 36-layer Qwen3-8B (+LoRA) and 64-layer Qwen3-32B stack figures")
     return p.parse_args()
 
 
@@ -308,6 +310,14 @@ def main():
     cpu = None
     if not args.no_cpu and not args.profile_gemv_only:
         cpu = cpu_baseline(head[0], torch)
+    stacks = {}
+    if not args.no_stacks and not args.profile_gemv_only:
+        del head
+        torch.cuda.empty_cache()
+        stacks["qwen3_8b_36_layers_lora16"] = stack_bench(bsq, synth, torch, np, synth.qwen3_8b_block(), 36, args.d,
+                                                          16, dev, "Qwen3-8B 36-layer stack + LoRA")
+        stacks["qwen3_32b_64_layers"] = stack_bench(bsq, synth, torch, np, synth.qwen3_32b_block(), 64, args.d, 0,
+                                                    dev, "Qwen3-32B 64-layer stack")
     traffic = read_traffic()
     line = {
         "metric": METRIC,
@@ -347,6 +357,7 @@ def main():
             "mean_launch_us": round(hd["kernel_us"], 2),
         },
         "cpu_baseline": cpu,
+        "stacks": stacks or None,
     }
     other = [d for d in results if d != args.d]
     if other:
@@ -357,6 +368,88 @@ def main():
                            "kernel_gbs": round(o["kernel_gbs"], 1), "gemm": o.get("gemm"),
                            "decode_gbs": round(o.get("decode_gbs", 0.0), 1)}
     print(json.dumps(line), flush=True)
+
+
+def stack_bench(bsq, synth, torch, np, projs, n_layers, d, lora_rank, dev, tag):
+    """A whole stack of layers: every projection of every layer encoded in one
+    launch per category (timed), then one decode token through all layers,
+    captured in one HIP graph: per layer the four grouped GEMVs (with their
+    LoRA prep when adapters are present). Returns encode G chunks/s and the
+    token's compressed-byte rate."""
+    cfg = bsq.Config(d=d, stages=2, kind=bsq.DEC_MLP, hidden=d, protect_num=1, protect_den=100)
+    codecs, layers, loras = {}, {}, {}
+    enc_s, chunks = 0.0, 0
+    for ci, p in enumerate(projs):
+        decs = synth.decoder_params(synth.DEC_MLP, d, d, d, 2, seed=synth.BASE_SEED, category=ci)
+        codecs[p.name] = bsq.bsq_codec_prepare(cfg, decs, device=dev)
+        W, _ = synth.weight(p.d_out, p.d_in, seed=7000 + 100 * ci + d, k_outliers=cfg.k(p.d_in), device=dev,
+                            n_mats=n_layers)
+        if n_layers == 1:
+            W = W.unsqueeze(0)
+        out = bsq.layer_empty(cfg, p.d_out, p.d_in, n_layers, dev)
+        ws = torch.empty(bsq.bsq_workspace_bytes(cfg, bsq.OP_ENCODE, n_layers, p.d_out, p.d_in) + 256,
+                         dtype=torch.uint8, device=dev)
+        ws = ws[(-ws.data_ptr()) % 256:]
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        bsq.bsq_encode(cfg, codecs[p.name], W, out=out, ws=ws, err=err, check=False)
+        e1.record()
+        torch.cuda.synchronize()
+        if int(err.item()):
+            raise RuntimeError(f"{tag}: non-finite weights")
+        enc_s += e0.elapsed_time(e1) / 1e3
+        chunks += n_layers * p.d_out * p.d_in // d
+        layers[p.name] = out
+        del W, ws
+        if lora_rank:
+            loras[p.name] = [synth.lora(p.d_out, p.d_in, lora_rank, seed=9000 + 100 * ci + li, device=dev)
+                             for li in range(n_layers)]
+    groups = {}
+    for p in projs:
+        groups.setdefault(p.group, []).append(p)
+    xs = {g: synth.activation(ps[0].d_in, seed=300 + i, device=dev) for i, (g, ps) in enumerate(groups.items())}
+    plans, nbytes = [], 0
+    for li in range(n_layers):
+        for g, ps in groups.items():
+            Ls = [layers[p.name].mat(li) for p in ps]
+            lr = [loras[p.name][li] for p in ps] if lora_rank else None
+            plans.append(bsq.GemvPlan(cfg, [codecs[p.name] for p in ps], Ls, xs[g], loras=lr,
+                                      y_dtype=torch.bfloat16))
+            nbytes += algorithmic_bytes(Ls, ps[0].d_in, sum(p.d_out for p in ps))
+            if lora_rank:
+                nbytes += sum(2 * lora_rank * (p.d_in + p.d_out) * 2 for p in ps)
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for pl in plans:
+            pl()
+        torch.cuda.synchronize()
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr, stream=s):
+            for pl in plans:
+                pl()
+        gr.replay()
+        torch.cuda.synchronize()
+        reps = max(3, int(0.3 / max(1e-6, nbytes / 2.5e12)))
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(s)
+        for _ in range(reps):
+            gr.replay()
+        t1.record(s)
+        torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    gbs = nbytes / (ms / 1e3) / 1e9
+    res = {"d": d, "layers": n_layers, "lora_rank": lora_rank, "encode_gchunks_per_s": round(chunks / enc_s / 1e9, 2),
+           "encode_chunks": chunks, "gemv_ms_per_token": round(ms, 4), "gemv_bytes_per_token": nbytes,
+           "gemv_gbs": round(gbs, 1), "gemv_pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+           "launches_per_token": len(plans) * (2 if lora_rank else 1)}
+    log(f"[bench] {tag}: encode {res['encode_gchunks_per_s']} G chunks/s; decode token {ms:.3f} ms, "
+        f"{gbs:.0f} GB/s ({gbs / HBM_PEAK_GBS:.1%} of 8 TB/s)")
+    del plans, gr, layers, codecs, loras
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(blk, torch):

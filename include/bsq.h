@@ -248,7 +248,9 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
 
 /* Activation preparation of the GEMV: work that needs a reduction over all
  * of x, written into `ws` (one launch):
- *  - the LoRA vectors t_g = A_g x (fp32, 16 per member);
+ *  - the LoRA vectors t_g = A_g x (fp32, 16 per member), for the paths that
+ *    do not compute them inside bsq_gemv_run (that is, fp32 x, and d = 16
+ *    with a decoder other than the width-16 symmetric one);
  *  - for the symmetric decoder at d = 16 with hidden width 16 and bf16 x, the
  *    decoder's output layer folded into the masked activations: per member,
  *    stage and chunk c, u = W2^T x~_c and b2 . x~_c (so that
@@ -263,9 +265,11 @@ bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const 
                             int32_t x_dtype, void *ws, size_t ws_bytes, void *stream);
 
 /* The streaming product of the GEMV, alone: reads x, the code and gain
- * planes, the int8 payload and LoRA B once, and the LoRA vectors that a
- * preceding bsq_gemv_prepare (same group, same x) left in `ws` on the same
- * stream. Limits of the bf16 path: d_in <= 65536 and k <= 4096. */
+ * planes, the int8 payload and LoRA A and B once, and whatever a preceding
+ * bsq_gemv_prepare (same group, same x) left in `ws` on the same stream.
+ * With bf16 x at d = 8 (and d = 16 with the width-16 symmetric decoder) the
+ * LoRA vectors are computed inside this launch. Limits of the bf16 path:
+ * d_in <= 65536 and k <= 4096. */
 bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs,
                         const bsq_layer *layers, const bsq_lora *loras, const void *x,
                         int32_t x_dtype, void *const *y, int32_t y_dtype, void *ws,

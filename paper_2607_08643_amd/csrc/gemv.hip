@@ -36,6 +36,11 @@ inline bool gemv_split16(const bsq_config &cfg) { return codec_has_split(cfg) &&
 // Workspace of that path: a 64-byte folded-activation record per (member,
 // stage, chunk), for BSQ_MAX_GROUP members so that the slots behind it start
 // at the same offset for every group size of one configuration and d_in.
+inline bool gemv_lane_path(const bsq_config &cfg, int x_dtype)
+{
+    return x_dtype == BSQ_BF16 && (cfg.d == 8 || gemv_split16(cfg));
+}
+
 inline size_t gemv_xp_bytes(const bsq_config &cfg, int64_t pitch)
 {
     return gemv_split16(cfg) ? size_t(BSQ_MAX_GROUP) * cfg.stages * size_t(pitch) * 64 : 0;
@@ -92,6 +97,7 @@ struct GemvMat {
     int64_t d_out;
     int64_t block_begin;  // first block of this member in the grid
     int64_t rg_begin;     // row-lane kernel: first 64-row group of this member (partial-sum slots)
+    int64_t lora_begin;   // row-lane kernel: first LoRA workgroup of this member (one per rank index)
     float *t;             // workspace: A x, [16]
     void *y;
 };
@@ -102,6 +108,8 @@ struct GemvArgs {
     int64_t d_in, pitch, k, nseg, rs, rpb;
     int64_t nblk, q;   // row-lane kernel: 16-chunk blocks per row, slices per 64-row group
     uint64_t *slots;   // row-lane kernel: {flag, partial} [row groups][q - 1][64], zero between calls
+    uint64_t *tslots;  // row-lane kernel: {flag, (A x)_r} [row groups][16], zero between calls
+    int64_t lora_blocks;  // row-lane kernel: LoRA workgroups ahead of the tiles' workgroups
     const void *x;
     int x_bf16, y_bf16;
 };
@@ -418,10 +426,11 @@ __device__ __forceinline__ void lane_load(LaneBlk<D, S> &b, const GemvMat &M, in
     }
 }
 
-// The LoRA term and the store of one output row (row < d_out). The rank-16
-// row of B is loaded unconditionally (indices clamped to the rank) so that
-// its loads are in flight together.
-__device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMat &M, int64_t row, float acc)
+// The LoRA term (tv = A x) and the store of one output row (row < d_out).
+// The rank-16 row of B is loaded unconditionally (indices clamped to the
+// rank) so that its loads are in flight together.
+__device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMat &M, int64_t row, float acc,
+                                                 const float (&tv)[BSQ_MAX_LORA_RANK])
 {
     if (M.rank > 0) {
         const uint16_t *br = M.B + row * M.rank;
@@ -430,7 +439,7 @@ __device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMa
         for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bq[q] = br[(q < M.rank) ? q : M.rank - 1];
 #pragma unroll
         for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) {
-            const float f = __builtin_fmaf(bf16_to_f32(bq[q]), M.t[q], acc);
+            const float f = __builtin_fmaf(bf16_to_f32(bq[q]), tv[q], acc);
             acc = (q < M.rank) ? f : acc;
         }
     }
@@ -457,7 +466,7 @@ __device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc)
 // time, all issued before any is used (indices clamped to the padded row,
 // words past it zeroed), then one word after the other.
 __device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M, const float *s_xs, int64_t row,
-                                            float acc)
+                                            float acc, const float (&tv)[BSQ_MAX_LORA_RANK])
 {
     if (row >= M.d_out) return;
     const int64_t nw = q8_pitch(a.k) / 16;  // 16-byte words per row
@@ -473,18 +482,19 @@ __device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M,
             asm volatile("" : "+v"(acc));  // one word's activations live at a time
         }
     }
-    lane_finish_lora(a, M, row, acc);
+    lane_finish_lora(a, M, row, acc, tv);
 }
 
 // The epilogue with the int8 rows already in LDS (s_q8 [64][kp], this lane's
 // row at lane * kp), else from global memory.
 __device__ __forceinline__ void lane_finish_lds(const GemvArgs &a, const GemvMat &M, const float *s_xs,
-                                                const int8_t *s_q8, bool q8_lds, int64_t row, float acc)
+                                                const int8_t *s_q8, bool q8_lds, int64_t row, float acc,
+                                                const float (&tv)[BSQ_MAX_LORA_RANK])
 {
     if (row >= M.d_out) return;
     if (!q8_lds || a.k == 0) {
-        if (a.k > 0) lane_finish(a, M, s_xs, row, acc);
-        else lane_finish_lora(a, M, row, acc);
+        if (a.k > 0) lane_finish(a, M, s_xs, row, acc, tv);
+        else lane_finish_lora(a, M, row, acc, tv);
         return;
     }
     const int64_t nw = q8_pitch(a.k) / 16;
@@ -496,7 +506,7 @@ __device__ __forceinline__ void lane_finish_lds(const GemvArgs &a, const GemvMat
         acc = q8_block(q1, s_xs + 16 * (w + 1), acc);
     }
     if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc);
-    lane_finish_lora(a, M, row, acc);
+    lane_finish_lora(a, M, row, acc, tv);
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -594,6 +604,91 @@ __device__ __forceinline__ float lane_tile_ragged(const LaneBlk<8, S> &t, const 
     return acc;
 }
 
+// LoRA workgroup of the row-lane kernel: t_r = sum_j A[r][j] x_j (unmasked x)
+// for one (member, rank index r), published into slot r of every row group
+// of the member as a flagged 64-bit word for the group's finishing workgroup,
+// which reads and clears it.
+__device__ __forceinline__ void lane_lora_block(const GemvArgs &a, float *s_red)
+{
+    const int t = threadIdx.x;
+    int m = 0;
+    while (m + 1 < a.n && int64_t(blockIdx.x) >= a.mat[m + 1].lora_begin) ++m;
+    const GemvMat &M = a.mat[m];
+    const int r = int(int64_t(blockIdx.x) - M.lora_begin);
+    // eight inputs per 16-byte load (x is 16-byte aligned; the row of A is
+    // read in 16-byte pieces where it is, element by element where not),
+    // four pieces per thread in flight
+    const uint16_t *ar = M.A + int64_t(r) * a.d_in;
+    const uint16_t *xr = static_cast<const uint16_t *>(a.x);
+    const bool vec = ((reinterpret_cast<uintptr_t>(ar) & 15) == 0);
+    const int64_t n8 = vec ? a.d_in / 8 : 0;
+    float acc = 0.0f;
+    for (int64_t p0 = t; p0 < n8; p0 += 4 * 256) {
+        uint4 av[4], xv[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t p = (p0 + u * 256 < n8) ? p0 + u * 256 : n8 - 1;
+            av[u] = reinterpret_cast<const uint4 *>(ar)[p];
+            xv[u] = reinterpret_cast<const uint4 *>(xr)[p];
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (p0 + u * 256 >= n8) break;
+            const uint32_t aw[4] = {av[u].x, av[u].y, av[u].z, av[u].w};
+            const uint32_t xw[4] = {xv[u].x, xv[u].y, xv[u].z, xv[u].w};
+#pragma unroll
+            for (int h = 0; h < 4; ++h) {
+                acc = __builtin_fmaf(__uint_as_float(aw[h] << 16), __uint_as_float(xw[h] << 16), acc);
+                acc = __builtin_fmaf(__uint_as_float(aw[h] & 0xffff0000u), __uint_as_float(xw[h] & 0xffff0000u), acc);
+            }
+        }
+    }
+    for (int64_t j = n8 * 8 + t; j < a.d_in; j += 256)  // the rest, element by element
+        acc = __builtin_fmaf(bf16_to_f32(ar[j]), bf16_to_f32(xr[j]), acc);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if ((t & 63) == 0) s_red[t >> 6] = acc;
+    __syncthreads();
+    const float tr = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
+    const int64_t nrg = (M.d_out + 63) / 64;
+    for (int64_t rg = t; rg < nrg; rg += 256)
+        __hip_atomic_store(a.tslots + (M.rg_begin + rg) * BSQ_MAX_LORA_RANK + r,
+                           (uint64_t(1) << 32) | __float_as_uint(tr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The finishing workgroup's LoRA vector of row group rg: the LoRA
+// workgroups' flagged slots (all loads in flight together, indices clamped
+// to the rank), then cleared. Zeros when the member has no adapter.
+__device__ __forceinline__ bool lane_lora_vector(const GemvArgs &a, const GemvMat &M, int64_t rg,
+                                                 float (&tv)[BSQ_MAX_LORA_RANK])
+{
+#pragma unroll
+    for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) tv[q] = 0.0f;
+    if (M.rank == 0) return true;
+    uint64_t *ts = a.tslots + (M.rg_begin + rg) * BSQ_MAX_LORA_RANK;
+    uint64_t pw[BSQ_MAX_LORA_RANK];
+    bool ok = true;
+    for (int spin = 0;; ++spin) {
+#pragma unroll
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q)
+            pw[q] = __hip_atomic_load(ts + ((q < M.rank) ? q : M.rank - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        bool ready = true;
+#pragma unroll
+        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) ready &= (pw[q] >> 32) != 0;
+        if (__all(ready)) break;
+        if (spin == LANE_SPIN_LIMIT) {  // never expected: report NaN rather than hang
+            ok = false;
+            break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+#pragma unroll
+    for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) tv[q] = (q < M.rank) ? __uint_as_float(uint32_t(pw[q])) : 0.0f;
+    const int lane = threadIdx.x & 63;
+    if (lane < M.rank) __hip_atomic_store(ts + lane, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return ok;
+}
+
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 // c + <relu(lo + hi), u> over one pair of fp16 lanes (packed add and max,
@@ -676,11 +771,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
 
+    if (int64_t(blockIdx.x) < a.lora_blocks) {  // the LoRA vectors, ahead of every tile
+        lane_lora_block(a, reinterpret_cast<float *>(s_mem));
+        return;
+    }
+    const int64_t bid = int64_t(blockIdx.x) - a.lora_blocks;
     int m = 0;
-    while (m + 1 < a.n && int64_t(blockIdx.x) >= a.mat[m + 1].block_begin) ++m;
+    while (m + 1 < a.n && bid >= a.mat[m + 1].block_begin) ++m;
     const GemvMat &M = a.mat[m];
     const int64_t nblk = a.nblk, Q = a.q;
-    const int64_t unit = int64_t(blockIdx.x) - M.block_begin;  // row group * Q + slice
+    const int64_t unit = bid - M.block_begin;  // row group * Q + slice
     const int64_t rg = unit / Q, q = unit - rg * Q;
     const int64_t tbase = ((rg * nblk) << 10) + (int64_t(lane) << 4);
     // this wave's tiles [b0, b1); those whose 128 columns are all real go
@@ -804,8 +904,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
 #pragma unroll
     for (int w = 1; w < WV; ++w) v += s_red[w * 64 + lane];
     const int64_t row = rg * 64 + lane;
+    float tv[BSQ_MAX_LORA_RANK];
     if (Q == 1) {
-        lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, v);
+        const bool ok = lane_lora_vector(a, M, rg, tv);
+        lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, ok ? v : __builtin_nanf(""), tv);
         return;
     }
     uint64_t *slots = a.slots + (M.rg_begin + rg) * (Q - 1) * 64 + lane;
@@ -842,7 +944,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     tot += v;
     for (int64_t q0 = 0; q0 < Q - 1; ++q0)
         __hip_atomic_store(slots + q0 * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, timed_out ? __builtin_nanf("") : tot);
+    const bool ok = lane_lora_vector(a, M, rg, tv);
+    lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, (timed_out || !ok) ? __builtin_nanf("") : tot, tv);
 }
 
 // ---------------------------------------------------------------------------
@@ -1006,9 +1109,10 @@ size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_
     const int64_t nblk = (d_in / cfg.d + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN;
     // LoRA vectors, folded activation records (d = 16 decoder path), then
     // {flag, partial} slots for all but the last slice (as many slices as the
-    // smallest TPW makes)
+    // smallest TPW makes), then the flagged LoRA vector slots of every row
+    // group
     return gemv_t_bytes() + gemv_xp_bytes(cfg, nblk * BSQ_PITCH_ALIGN) +
-           size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8;
+           size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8 + size_t(rg) * BSQ_MAX_LORA_RANK * 8;
 }
 
 size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_rpb)
@@ -1024,6 +1128,8 @@ hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *cod
 {
     bool any = false;
     for (int m = 0; m < n && loras; ++m) any |= (loras[m].rank > 0);
+    // the row-lane kernel computes its LoRA vectors itself
+    if (gemv_lane_path(cfg, x_dtype)) any = false;
     const bool fold = gemv_split16(cfg) && x_dtype == BSQ_BF16;
     if (!any && !fold) return hipSuccess;
     const GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, nullptr, BSQ_F32, ws);
@@ -1052,15 +1158,22 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
         for (int m = 0; m < n; ++m) rgs += (layers[m].d_out + 63) / 64;
         const int tpw = lane_tpw(rgs, a.nblk);
         a.q = lane_slices(a.nblk, tpw);
-        int64_t blocks = 0;
+        // LoRA workgroups first (one per member and rank index), then the
+        // tiles' workgroups; the LoRA vector slots follow the partial slots
+        a.tslots = a.slots + rgs * (lane_slices(a.nblk, 1) - 1) * 64;
+        int64_t blocks = 0, lora_blocks = 0;
         rgs = 0;
         for (int m = 0; m < n; ++m) {
             const int64_t nrg = (layers[m].d_out + 63) / 64;
             a.mat[m].block_begin = blocks;
             a.mat[m].rg_begin = rgs;
+            a.mat[m].lora_begin = lora_blocks;
             blocks += nrg * a.q;
             rgs += nrg;
+            lora_blocks += a.mat[m].rank;
         }
+        a.lora_blocks = lora_blocks;
+        blocks += lora_blocks;
         const int64_t kp = q8_pitch(a.k);
         const size_t tab = (D == 8) ? size_t(S) * 256 * 16 : size_t(S) * 1024 * 16 + size_t(S) * 4 * tpw * 16 * 64;
         const size_t shm = tab + 4 * 64 * 4 + size_t(kp) * 4 + ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
