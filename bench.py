@@ -346,7 +346,7 @@ def main():
         "decode_gbs": round(hd.get("decode_gbs", 0.0), 1),
         "gemm": hd.get("gemm"),
         "roofline": {
-            "kernel": f"gemv_lane_kernel<2,4> (gate/up group, bsq_gemv_run, d={args.d})",
+            "kernel": f"gemv_lane_kernel<{args.d}, 2, TPW> (gate/up launch of bsq_gemv_run, d={args.d})",
             "bound": "hbm",
             "achieved": round(hd["kernel_gbs"], 1),
             "peak": HBM_PEAK_GBS,

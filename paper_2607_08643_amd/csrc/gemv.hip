@@ -6,18 +6,19 @@
 // from the int8 path, eq. protected_8bit_scatter) and the stage sum is the
 // parallel residual decoding of eq. parallel_stage_decode.
 //
-// Streaming kernel (bf16 activations). Each block owns a contiguous range of
-// rows of one group member. At start it stages in LDS the member's bf16
-// decoder table (d = 8), the protected-column bitmap and the scaled protected
-// activations scale_p * x_{idx_p}. A thread owns one 128-input segment of x~
-// (16 chunks at d = 8, 8 chunks at d = 16), masked and held in registers,
-// and walks down its rows two at a time: the next row's code and gain words
-// (128-bit loads, read once from HBM) are in flight while the current row is
-// decoded by table lookup and dotted with x~ by v_dot2_f32_bf16 in fp32.
-// Segment partials go to LDS and are reduced once per block, where the
-// epilogue adds the int8 and LoRA terms. The only other kernel is the LoRA
-// prep (t = A x, one fp32 16-vector per member), launched only when a member
-// has an adapter.
+// Kernels:
+//  * gemv_prep_kernel (bsq_gemv_prepare): the d = 16 symmetric decoder's
+//    folded activation records (the output layer folded into x~ per chunk),
+//    and the LoRA vectors A x for the kernels that do not compute them.
+//  * gemv_lane_kernel (bf16 activations, d = 8, and d = 16 with the
+//    symmetric decoder of hidden width 16): a lane owns a row of a 64-row
+//    tile, the tile's activations are wave-uniform scalar operands, the
+//    decoder comes from LDS tables; extra workgroups ahead of the tiles
+//    compute the LoRA vectors A x. The headline kernel.
+//  * gemv_stream_kernel (bf16 activations, other d = 16 decoders): a thread
+//    owns a 128-input segment of x~ and walks down rows, table lookups from
+//    global memory.
+//  * gemv_f32_kernel (fp32 activations): one wave per row, fp32 tables.
 #include "bsq_internal.h"
 
 namespace bsq {
