@@ -4,6 +4,8 @@
 // stages decode in parallel rather than one after the other); the protected
 // columns are then taken from the int8 payload. The stage sum is the fmaf
 // chain of the definition, so the fp32 output is bit-identical to it.
+#include <type_traits>
+
 #include "bsq_internal.h"
 
 namespace bsq {
@@ -20,30 +22,31 @@ struct DecodeArgs {
     void *out;
 };
 
-// Position p of column j in the ascending protected list (j is known to be in it).
-__device__ __forceinline__ int find_pos(const int32_t *idx, int64_t k, int32_t j)
-{
-    int64_t lo = 0, hi = k - 1;
-    while (lo < hi) {
-        int64_t mid = (lo + hi) >> 1;
-        if (idx[mid] < j) lo = mid + 1;
-        else hi = mid;
-    }
-    return int(lo);
-}
-
 // A block walks the tiles of one matrix (grid-stride, so the decoder tables
-// and the protected bitmap are set up once per block). Thread t handles the
-// tile elements t, t + 256, t + 512, t + 768: element e is row e / 16, chunk
-// e % 16 of the tile, so the code and gain reads follow the tile layout and
-// 16 consecutive threads write one contiguous row segment of W_hat.
+// and the protected-column metadata are set up once per block). Thread t
+// handles the four consecutive chunks 4 (t % 4) .. + 3 of row t / 4 of the
+// tile: one 4- or 8-byte code load and one 8-byte gain load per stage, and a
+// 64-byte (bf16, d = 8) run of W_hat per thread, 256 contiguous bytes per row
+// and wave. Tiles always lie inside the padded planes, so the loads of the
+// next tile are issued unconditionally while the current one is assembled;
+// only the stores check the row and chunk bounds.
+//
+// Protected columns: the position p of column j in the ascending index list
+// is the number of protected columns before it, i.e. the rank of the first
+// protected column of j's 32-column word plus the set bits of that word
+// below j (both kept in LDS), so no search over the list is needed.
 template <int D, int S, bool BF16OUT>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
+    typedef typename std::conditional<D == 8, uint32_t, uint2>::type CodeWord;
     extern __shared__ uint32_t s_mem[];
-    // [words] protected bitmap of this matrix, then (D == 8) the fp32 tables
+    // [words4] protected bitmap, [words4] rank of each word's first protected
+    // column, [k4] scales, then (D == 8) the fp32 tables
+    const int64_t words4 = (a.words + 3) & ~int64_t(3), k4 = (a.k + 3) & ~int64_t(3);
     uint32_t *s_bits = s_mem;
-    float *s_tab = reinterpret_cast<float *>(s_mem + ((a.words + 3) & ~int64_t(3)));
+    int32_t *s_rank = reinterpret_cast<int32_t *>(s_mem + words4);
+    float *s_scale = reinterpret_cast<float *>(s_mem + 2 * words4);
+    float *s_tab = reinterpret_cast<float *>(s_mem + 2 * words4 + k4);
     const int64_t m = blockIdx.y;
     const int t = threadIdx.x;
     const int32_t *idx = a.idx ? a.idx + m * a.k : nullptr;
@@ -52,7 +55,12 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         __syncthreads();
         for (int64_t p = t; p < a.k; p += blockDim.x) {
             const int32_t j = idx[p];
-            if (j >= 0 && j < a.d_in) atomicOr(&s_bits[j >> 5], 1u << (j & 31));
+            s_scale[p] = a.scale[m * a.k + p];
+            if (j >= 0 && j < a.d_in) {
+                atomicOr(&s_bits[j >> 5], 1u << (j & 31));
+                const int32_t jp = (p > 0) ? idx[p - 1] : -1;
+                if (jp < 0 || (jp >> 5) != (j >> 5)) s_rank[j >> 5] = int32_t(p);
+            }
         }
     }
     if constexpr (D == 8) {
@@ -66,25 +74,37 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     const int64_t nb = a.pitch / 16;                 // tiles per 64-row group
     const int64_t tiles = (a.d_out + 63) / 64 * nb;  // tiles of this matrix
     const int64_t kp = q8_pitch(a.k);
-    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+    const int64_t pbase = m * plane_elems(a.d_out, a.pitch) + 4 * t;
+    const int r = t >> 2, cc0 = 4 * (t & 3);  // row and first chunk within the tile
+
+    CodeWord code[2][S];
+    uint2 gain[2][S];
+    auto load = [&](int P, int64_t tile) {
+        const int64_t e = pbase + tile * 1024;
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            if constexpr (D == 8) code[P][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
+            else code[P][s] = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(a.codes[s]) + e);
+            gain[P][s] = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
+        }
+    };
+    auto body = [&](int P, int64_t tile) {
         const int64_t rg = tile / nb, cb = tile - rg * nb;
+        const int64_t i = rg * 64 + r;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int e = t + 256 * u;
-            const int64_t i = rg * 64 + (e >> 4);
-            const int64_t c = cb * 16 + (e & 15);
-            if (i >= a.d_out || c >= a.C) continue;
-            const int64_t plane = m * plane_elems(a.d_out, a.pitch) + tile * 1024 + e;
-
+            const int64_t c = cb * 16 + cc0 + u;
             float v[D];
 #pragma unroll
             for (int j = 0; j < D; ++j) v[j] = 0.0f;
 #pragma unroll
             for (int s = 0; s < S; ++s) {
-                const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[plane])
-                                               : uint32_t(static_cast<const uint16_t *>(a.codes[s])[plane]);
-                const float g = f16_bits_to_f32(a.gains[s][plane]);
-                const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
+                uint32_t cw;
+                if constexpr (D == 8) cw = (code[P][s] >> (8 * u)) & 0xffu;
+                else cw = ((u < 2 ? code[P][s].x : code[P][s].y) >> (16 * (u & 1))) & 0xffffu;
+                const uint32_t gw = (u < 2) ? gain[P][s].x : gain[P][s].y;
+                const float g = f16_bits_to_f32(uint16_t(gw >> (16 * (u & 1))));
+                const float *y = (D == 8) ? (s_tab + (s * 256 + cw) * 8) : (a.tab32[s] + size_t(cw) * D);
                 const float4 *y4 = reinterpret_cast<const float4 *>(y);
 #pragma unroll
                 for (int q = 0; q < D / 4; ++q) {
@@ -95,26 +115,30 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
                     v[4 * q + 3] = __builtin_fmaf(g, tv.w, v[4 * q + 3]);
                 }
             }
+            if (i >= a.d_out || c >= a.C) continue;
             if (a.k > 0) {
                 const int64_t col0 = c * D;
-                const uint32_t pm = (s_bits[col0 >> 5] >> (col0 & 31)) & ((1u << D) - 1u);
+                const uint32_t word = s_bits[col0 >> 5];
+                const uint32_t pm = (word >> (col0 & 31)) & ((1u << D) - 1u);
                 if (pm) {
 #pragma unroll
                     for (int j = 0; j < D; ++j) {
                         if (!((pm >> j) & 1u)) continue;
-                        const int p = find_pos(idx, a.k, int32_t(col0 + j));
-                        v[j] = float(a.q8[(m * a.d_out + i) * kp + p]) * a.scale[m * a.k + p];
+                        const int b = int((col0 + j) & 31);
+                        int64_t p = s_rank[col0 >> 5] + __builtin_popcount(word & ((1u << b) - 1u));
+                        p = (p < 0) ? 0 : (p < a.k) ? p : a.k - 1;  // an index list that is not ascending stays in bounds
+                        v[j] = float(a.q8[(m * a.d_out + i) * kp + p]) * s_scale[p];
                     }
                 }
             }
             const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
             if constexpr (BF16OUT) {
-                uint16_t h[D];
+                uint32_t h[D / 2];
 #pragma unroll
-                for (int j = 0; j < D; ++j) h[j] = f32_to_bf16(v[j]);
+                for (int j = 0; j < D / 2; ++j) h[j] = uint32_t(f32_to_bf16(v[2 * j])) | (uint32_t(f32_to_bf16(v[2 * j + 1])) << 16);
                 uint4 *dst = reinterpret_cast<uint4 *>(static_cast<uint16_t *>(a.out) + o);
 #pragma unroll
-                for (int q = 0; q < D / 8; ++q) dst[q] = reinterpret_cast<const uint4 *>(h)[q];
+                for (int q = 0; q < D / 8; ++q) dst[q] = make_uint4(h[4 * q], h[4 * q + 1], h[4 * q + 2], h[4 * q + 3]);
             } else {
                 float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.out) + o);
 #pragma unroll
@@ -122,6 +146,20 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
                     dst[q] = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
             }
         }
+    };
+    int64_t tile = blockIdx.x;
+    if (tile >= tiles) return;
+    load(0, tile);
+    for (;;) {
+        const int64_t t1 = tile + gridDim.x;
+        load(1, (t1 < tiles) ? t1 : tile);
+        body(0, tile);
+        if (t1 >= tiles) break;
+        const int64_t t2 = t1 + gridDim.x;
+        load(0, (t2 < tiles) ? t2 : t1);
+        body(1, t1);
+        if (t2 >= tiles) break;
+        tile = t2;
     }
 }
 
@@ -135,7 +173,8 @@ hipError_t launch_decode_t(int stages, const DecodeArgs &a, int64_t n_mats, hipS
     if (gx > tiles) gx = tiles;
     if (gx < 1) gx = 1;
     const dim3 grid = dim3(unsigned(gx), unsigned(n_mats));
-    const size_t shm = size_t((a.words + 3) & ~int64_t(3)) * 4 + ((D == 8) ? size_t(stages) * 256 * 8 * 4 : 0);
+    const size_t shm = size_t((a.words + 3) & ~int64_t(3)) * 8 + size_t((a.k + 3) & ~int64_t(3)) * 4 +
+                       ((D == 8) ? size_t(stages) * 256 * 8 * 4 : 0);
     switch (stages) {
     case 1: hipLaunchKernelGGL((decode_kernel<D, 1, BF16OUT>), grid, dim3(256), shm, st, a); break;
     case 2: hipLaunchKernelGGL((decode_kernel<D, 2, BF16OUT>), grid, dim3(256), shm, st, a); break;

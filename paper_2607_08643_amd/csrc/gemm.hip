@@ -65,6 +65,7 @@ struct GemmArgs {
     int64_t M, d_out, pitch, ksteps, Kp, k, kp32, ldy;
     void *Y;
     int y_bf16;
+    int y_vec;         // Y 16-byte aligned with 16-byte row pitch: vector stores
     int ksplit;        // blocks per tile along K (grid z)
     uint64_t *slots;   // [tiles][ksplit - 1][BM * BN] flagged partials, zero between calls
 };
@@ -164,119 +165,149 @@ __device__ __forceinline__ void lds_barrier()
     asm volatile("s_barrier" ::: "memory");
 }
 
-// One K step's code and gain words of a lane, for each of its NT row groups:
-// d = 8: chunks 4 g .. 4 g + 3 of the step (one code word, two gain words);
-// d = 16: chunks 2 g, 2 g + 1 (one word of two codes, one gain word).
-template <int D, int S, int NT>
-struct WRegs {
-    uint32_t code[NT][S];
-    uint32_t gain[NT][S][D == 8 ? 2 : 1];
+// Wait until at most N vector-memory operations of this wave are in flight.
+template <int N>
+__device__ __forceinline__ void wait_vm()
+{
+    static_assert(N >= 0 && N <= 63, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// LDS of one workgroup (gfx950: 160 KiB per compute unit).
+constexpr int GEMM_LDS_BYTES = 160 * 1024;
+
+// Shape of the main kernel. A workgroup of 8 waves owns BN = 64 NT weight
+// rows and BM = 16 MT tokens. Wave w owns the row set rs = w % 4 (NT groups of
+// 16 rows: block rows 16 (NT rs + j) + lane % 16) and the half kh = w / 4 of
+// every K step (MFMA k-slices 2 kh and 2 kh + 1); the two halves of a row
+// set add their tiles at the end. Per K step, the X~ tile and the code and
+// gain words of the block's NT 64-row plane tiles reach LDS by DMA
+// (global_load_lds_dwordx4, 64 16-byte units per wave instruction) into a
+// ring of NS slots, NS - 1 steps ahead.
+template <int D, int S, int MT, int NT>
+struct GemmShape {
+    static constexpr int BM = 16 * MT, BN = 64 * NT;
+    // 16-byte units of one (64-row tile, stage) per step: d = 8, the tile's
+    // 1 KiB of codes and 2 KiB of gains; d = 16, half a tile (the step's 8
+    // chunks): 16 bytes of codes and 16 of gains per row
+    static constexpr int WU = (D == 8) ? 192 : 128;
+    static constexpr int XSLOT = BM * 256;            // bytes: [BM][128] bf16
+    static constexpr int WSLOT = NT * S * WU * 16;    // bytes: [NT][S][codes | gains]
+    static constexpr int TAB = (D == 8) ? S * 4096 : 0;  // fp16 decoder tables [S][256][8]
+    static constexpr int NS_FIT = (GEMM_LDS_BYTES - TAB) / (XSLOT + WSLOT);
+    static constexpr int NS = NS_FIT < 8 ? NS_FIT : 8;
+    static constexpr int NXI = BM / 4;              // X~ DMA wave instructions per step
+    static constexpr int NWI = NT * S * WU / 64;    // weight DMA wave instructions per step
+    static constexpr int NI = NXI + NWI;            // wave w issues instructions w, w + 8, ... < NI
+    static constexpr int PMAX = (NI + 7) / 8, PMIN = NI / 8;  // DMA instructions per wave and step
+    static constexpr size_t LDS = size_t(NS) * (XSLOT + WSLOT) + TAB;
+    static_assert(NS >= 2, "two pipeline stages fit in LDS");
+    static_assert(MT * NT * 4096 <= NS * XSLOT, "the exchange of the two K halves fits in the X~ ring");
+    static_assert((NS - 2) * PMAX <= 63, "wait count fits vmcnt");
+    static_assert(WU % 64 == 0, "a DMA instruction stays within one (tile, stage)");
 };
 
-// Number of vector-memory instructions w_load issues (for the wait counts).
-template <int D, int S, int NT>
-constexpr int w_loads() { return NT * S * 2; }
-
-template <int D, int S, int NT>
-__device__ __forceinline__ void w_load(WRegs<D, S, NT> &w, const GemmArgs &a, const int64_t (&ebase)[NT], int64_t ks)
-{
-    constexpr int CPS = BK / D;
-    const int64_t c0 = ks * CPS;
-    const int64_t off = ((c0 >> 4) << 10) + (c0 & 15);
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int64_t e = ebase[j] + off;
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-            if constexpr (D == 8) {
-                w.code[j][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
-                const uint2 g = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
-                w.gain[j][s][0] = g.x;
-                w.gain[j][s][1] = g.y;
-            } else {
-                w.code[j][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(a.codes[s]) + e);
-                w.gain[j][s][0] = *reinterpret_cast<const uint32_t *>(a.gains[s] + e);
-            }
-        }
-    }
-}
-
-// B fragments of one row group: bq[q] = the 8 bf16 weights of inputs
-// 32 g + 8 q .. + 8 of the step (d = 8: chunk 4 g + q; d = 16: half q % 2 of
-// chunk 2 g + q / 2), each sum_s gain_s * D_s(code_s)[j] as an fp32 fmaf
-// chain over fp16 gains and fp16 table values (v_fma_mix_f32), rounded to
-// bf16. d = 8 reads the tables from LDS, d = 16 from global memory.
-template <int D, int S, int NT>
-__device__ __forceinline__ void w_decode(const WRegs<D, S, NT> &w, int j, const GemmArgs &a, const uint16_t *s_tab,
-                                         u32x4_t (&bq)[4])
-{
-    typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
-    constexpr int CPL = (D == 8) ? 4 : 2;  // chunks per lane
-#pragma unroll
-    for (int u = 0; u < CPL; ++u) {
-        float v[D];
-#pragma unroll
-        for (int e = 0; e < D; ++e) v[e] = 0.0f;
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-            const uint32_t code = (D == 8) ? ((w.code[j][s] >> (8 * u)) & 0xffu) : ((w.code[j][s] >> (16 * u)) & 0xffffu);
-            const uint32_t gw = (D == 8) ? w.gain[j][s][u >> 1] : w.gain[j][s][0];
-            const float g = f16_bits_to_f32(uint16_t((u & 1) ? (gw >> 16) : (gw & 0xffffu)));
-            const uint16_t *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tabh[s] + size_t(code) * D);
-#pragma unroll
-            for (int q = 0; q < D / 8; ++q) {
-                const f16x8_t yy = *reinterpret_cast<const f16x8_t *>(y + 8 * q);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) v[8 * q + e] = __builtin_fmaf(g, float(yy[e]), v[8 * q + e]);
-            }
-        }
-#pragma unroll
-        for (int h = 0; h < D / 8; ++h)
-            bq[(D == 8) ? u : 2 * u + h] = u32x4_t{pack_bf16x2(v[8 * h + 0], v[8 * h + 1]), pack_bf16x2(v[8 * h + 2], v[8 * h + 3]),
-                                                   pack_bf16x2(v[8 * h + 4], v[8 * h + 5]), pack_bf16x2(v[8 * h + 6], v[8 * h + 7])};
-    }
-}
-
-// One block: BN = 64 NT rows x BM = 16 MT tokens x the K steps [kb, ke) of
-// split z. Wave w owns rows 16 (NT w + j) + lane % 16 of the block, j < NT,
-// and all BM tokens: acc[i][j] element r is token 16 i + 4 (lane / 16) + r.
+// One block: BN rows x BM tokens x the K steps [kb, ke) of split z.
+// acc[i][j] element r is token 16 i + 4 (lane / 16) + r of row group j.
+//
+// K step ks (slot ks % NS of both rings): wait until only the DMAs of the
+// next NS - 2 steps may be in flight, barrier (every wave's DMAs of step ks
+// have landed, and every wave is done with step ks - 1), DMA step
+// ks + NS - 1 into the slot step ks - 1 used (clamped to the last step: a
+// harmless reload into a free slot), decode this wave's B fragments from the
+// slot's code and gain words and the LDS tables, MFMAs against the X~ slot.
+// The inputs of a step are permuted identically on both operands so that a
+// lane's fragment is a whole chunk (d = 8) or half a chunk (d = 16): MFMA
+// input group g = lane / 16 of k-slice q covers inputs 32 g + 8 q .. + 8.
 template <int D, int S, int MT, int NT>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
+__global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
 {
-    constexpr int BM = MT * 16, BN = 64 * NT;
-    constexpr int XSLOT = BM * BK;   // bf16 elements per X~ slot
-    constexpr int NXL = BM / 16;     // X~ loads (16 B) per lane per step
-    constexpr int NW = w_loads<D, S, NT>();
-    static_assert(NW <= 63, "wait count fits vmcnt");
-    // LDS: two X~ slots [BM][128] bf16 (the 16-byte segment s of row r
-    // stored at position s ^ (r % 16): conflict-free fragment reads), and the
-    // fp32 tables (D == 8)
-    __shared__ __attribute__((aligned(16))) uint16_t s_x[2][XSLOT];
-    __shared__ __attribute__((aligned(16))) uint16_t s_tab[(D == 8) ? S * 2048 : 8];
+    using G = GemmShape<D, S, MT, NT>;
+    typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+    extern __shared__ __attribute__((aligned(16))) uint4 s_mem4[];
+    uint8_t *s_mem = reinterpret_cast<uint8_t *>(s_mem4);
+    uint8_t *s_xr = s_mem;                          // X~ ring, 16-byte segment s of row r at s ^ (r % 16)
+    uint8_t *s_wr = s_mem + G::NS * G::XSLOT;       // weight ring
+    uint4 *s_tab4 = reinterpret_cast<uint4 *>(s_wr + G::NS * G::WSLOT);  // d = 8 tables
+    const uint16_t *s_tab = reinterpret_cast<const uint16_t *>(s_tab4);
 
-    const int t = threadIdx.x, lane = t & 63, g = lane >> 4;
+    const int t = threadIdx.x, lane = t & 63, g = lane >> 4, r16 = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-    const int64_t n0 = int64_t(blockIdx.x) * BN;          // first row of the block
-    const int64_t m0 = int64_t(blockIdx.y) * BM;          // first token of the block
+    const int rs = wave & 3, kh = wave >> 2;
+    const int64_t n0 = int64_t(blockIdx.x) * G::BN;  // first row of the block
+    const int64_t m0 = int64_t(blockIdx.y) * G::BM;  // first token of the block
     const int z = blockIdx.z;
     const int64_t kb = a.ksteps * z / a.ksplit, ke = a.ksteps * (z + 1) / a.ksplit;
-    const int64_t nb = a.pitch / 16;
-    int64_t ebase[NT];  // tile element of the lane's row, chunk group g, step 0
-#pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int64_t row = n0 + 16 * (NT * wave + j) + (lane & 15);
-        ebase[j] = (((row >> 6) * nb) << 10) + ((row & 63) << 4) + (BK / D / 4) * g;
-    }
+    const int64_t nb = a.pitch / 16;                 // 16-chunk blocks per row
+    const int64_t rbmax = (a.d_out + 63) / 64 - 1;   // last 64-row tile of the planes
 
-    // fp16 tables (D == 8): S x 2048 values, one 16-byte piece per thread
-    // per stage, all loads issued before the first store
-    if constexpr (D == 8) {
-        u32x4_t tv[S];
+    // DMA instructions of this wave, r-th: joint instruction v = wave + 8 r
+    // of the step (v < NXI: 64 units of X~, unit u = row u / 16, LDS segment
+    // u % 16; else 64 units of the code and gain words of (64-row tile jt,
+    // stage s), tiles past the planes clamped to the last one, whose rows are
+    // never stored). Source of step ks = base + (ks / 2) A + (ks % 2) B bytes;
+    // destination = ring + slot * slot bytes + offset.
+    const uint8_t *dsrc[G::PMAX];
+    int64_t dA[G::PMAX], dB[G::PMAX];
+    int doff[G::PMAX], dslot[G::PMAX];
+    bool dx[G::PMAX];
 #pragma unroll
-        for (int s = 0; s < S; ++s) tv[s] = reinterpret_cast<const u32x4_t *>(a.tabh[s])[t];
-#pragma unroll
-        for (int s = 0; s < S; ++s) reinterpret_cast<u32x4_t *>(s_tab + s * 2048)[t] = tv[s];
+    for (int r = 0; r < G::PMAX; ++r) {
+        const int v0 = wave + 8 * r;
+        const int v = (v0 < G::NI) ? v0 : G::NI - 1;  // (r-th instruction absent when v0 >= NI)
+        if (v < G::NXI) {
+            const int u = 64 * v + lane, row = u >> 4, sp = u & 15;
+            dsrc[r] = reinterpret_cast<const uint8_t *>(a.Xt + (m0 + row) * a.Kp + 8 * (sp ^ (row & 15)));
+            dA[r] = 2 * 2 * BK;
+            dB[r] = 2 * BK;
+            dx[r] = true;
+            doff[r] = 1024 * v;
+            dslot[r] = G::XSLOT;
+        } else {
+            const int vw = v - G::NXI;
+            const int pair = (64 * vw) / G::WU;        // jt * S + s (uniform over the wave)
+            const int w0 = 64 * vw - pair * G::WU;     // first unit within the (tile, stage)
+            const int jt = pair / S, st = pair - jt * S;
+            const int64_t rb = ((n0 >> 6) + jt < rbmax) ? (n0 >> 6) + jt : rbmax;
+            const int w = w0 + lane;
+            const int64_t tb = (rb * nb) << 10;        // element of the row block's first tile
+            if constexpr (D == 8) {
+                dsrc[r] = (w0 < 64) ? static_cast<const uint8_t *>(a.codes[st]) + tb + 16 * w
+                                    : reinterpret_cast<const uint8_t *>(a.gains[st] + tb) + 16 * (w - 64);
+                dA[r] = (w0 < 64) ? 2048 : 4096;
+                dB[r] = (w0 < 64) ? 1024 : 2048;
+            } else {
+                dsrc[r] = (w0 < 64) ? reinterpret_cast<const uint8_t *>(static_cast<const uint16_t *>(a.codes[st]) + tb) + 32 * (w & 63)
+                                    : reinterpret_cast<const uint8_t *>(a.gains[st] + tb) + 32 * (w & 63);
+                dA[r] = 2048;
+                dB[r] = 16;
+            }
+            dx[r] = false;
+            doff[r] = 1024 * vw;
+            dslot[r] = G::WSLOT;
+        }
     }
+    const int pw = (wave < G::NI % 8) ? G::PMAX : G::PMIN;  // this wave's DMA instructions per step
+    auto dma_step = [&](int64_t ks, int sl) {
+#pragma unroll
+        for (int r = 0; r < G::PMAX; ++r) {
+            if (r >= G::PMIN && wave + 8 * r >= G::NI) continue;
+            const uint4 *src = reinterpret_cast<const uint4 *>(dsrc[r] + (ks >> 1) * dA[r] + (ks & 1) * dB[r]);
+            uint8_t *dst = (dx[r] ? s_xr : s_wr) + sl * dslot[r] + doff[r];
+            __builtin_amdgcn_global_load_lds(src, reinterpret_cast<uint4 *>(dst), 16, 0, 0);
+        }
+    };
+
+    // prologue: the decoder tables (d = 8; older than every step's DMA, so
+    // the first step's wait covers them), then steps kb .. kb + NS - 2
+    if constexpr (D == 8) {
+        for (int v = wave; v < S * 4; v += 8) {  // 1 KiB of stage v / 4
+            const uint4 *src = reinterpret_cast<const uint4 *>(a.tabh[v >> 2]) + (v & 3) * 64 + lane;
+            __builtin_amdgcn_global_load_lds(src, s_tab4 + 64 * v, 16, 0, 0);
+        }
+    }
+#pragma unroll
+    for (int p = 0; p < G::NS - 1; ++p) dma_step((kb + p < ke) ? kb + p : ke - 1, p);
 
     f32x4_t acc[MT][NT];
 #pragma unroll
@@ -284,187 +315,278 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmArgs a)
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
 
-    // X~ tile of step ks through registers: pass n of thread t carries the
-    // 16-byte segment e = 256 n + t, row e / 16, segment e % 16
-    auto x_load = [&](u32x4_t (&xr)[NXL], int64_t ks) {
-#pragma unroll
-        for (int n = 0; n < NXL; ++n) {
-            const int e = 256 * n + t;
-            xr[n] = *reinterpret_cast<const u32x4_t *>(a.Xt + (m0 + (e >> 4)) * a.Kp + ks * BK + 8 * (e & 15));
-        }
-    };
-    auto x_store = [&](const u32x4_t (&xr)[NXL], uint16_t *slot) {
-#pragma unroll
-        for (int n = 0; n < NXL; ++n) {
-            const int e = 256 * n + t, r = e >> 4;
-            *reinterpret_cast<u32x4_t *>(slot + r * BK + 8 * ((e & 15) ^ (r & 15))) = xr[n];
-        }
-    };
-
-    // One K step ks at parity P: wait until only the code and gain loads of
-    // step ks + 1 may be in flight (issue order per step: X~ of step ks + 2,
-    // then code and gain words of step ks + 2), barrier, store X~ of step
-    // ks + 1 to the other slot (read last in step ks - 1, before this
-    // barrier), issue the loads of step ks + 2 (clamped to the last step: a
-    // harmless reload), decode this step's weights, MFMAs on this step's slot.
-    WRegs<D, S, NT> w[2];
-    u32x4_t xr[2][NXL];
-    auto step = [&](auto pc, int64_t ks) {
-        constexpr int P = decltype(pc)::value;
-        __builtin_amdgcn_s_waitcnt((NW & 15) | ((NW >> 4) << 14) | (7 << 4) | (15 << 8));
+    int sl = 0;  // slot of step ks
+    for (int64_t ks = kb; ks < ke; ++ks) {
+        if (pw == G::PMAX) wait_vm<(G::NS - 2) * G::PMAX>();
+        else wait_vm<(G::NS - 2) * G::PMIN>();
         lds_barrier();
-        x_store(xr[P ^ 1], s_x[P ^ 1]);
-        const int64_t kn = (ks + 2 < ke) ? ks + 2 : ke - 1;
-        x_load(xr[P], kn);
-        // keep the issue order (X~ loads, decode, code and gain loads): the
-        // wait at the top of the next step relies on it
-        __builtin_amdgcn_sched_barrier(0);
-        u32x4_t bq[NT][4];
+        const uint8_t *ws = s_wr + sl * G::WSLOT;
+        const uint8_t *xs = s_xr + sl * G::XSLOT;
+        // code and gain words of this wave's chunks: d = 8, chunks 4 g + 2 kh
+        // and + 1 (two codes, two gains); d = 16, chunk 2 g + kh
+        uint32_t cw[NT][S], gw[NT][S];
 #pragma unroll
-        for (int j = 0; j < NT; ++j) w_decode<D, S, NT>(w[P], j, a, s_tab, bq[j]);
-        __builtin_amdgcn_sched_barrier(0);
-        w_load<D, S, NT>(w[P], a, ebase, kn);
-        __builtin_amdgcn_sched_barrier(0);
-        const uint16_t *xs = s_x[P];
+        for (int j = 0; j < NT; ++j) {
+            const int grp = NT * rs + j, jt = grp >> 2, rit = 16 * (grp & 3) + r16;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-#pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                const int rr = 16 * i + (lane & 15);
-                const u32x4_t av = *reinterpret_cast<const u32x4_t *>(xs + rr * BK + 8 * ((4 * g + q) ^ (lane & 15)));
-                const bf16x8_t aop = __builtin_bit_cast(bf16x8_t, av);
-#pragma unroll
-                for (int j = 0; j < NT; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(aop, __builtin_bit_cast(bf16x8_t, bq[j][q]), acc[i][j], 0, 0, 0);
+            for (int s = 0; s < S; ++s) {
+                const uint8_t *base = ws + (jt * S + s) * (G::WU * 16);
+                if constexpr (D == 8) {
+                    cw[j][s] = *reinterpret_cast<const uint16_t *>(base + rit * 16 + 4 * g + 2 * kh);
+                    gw[j][s] = *reinterpret_cast<const uint32_t *>(base + 1024 + rit * 32 + 8 * g + 4 * kh);
+                } else {
+                    cw[j][s] = *reinterpret_cast<const uint16_t *>(base + rit * 16 + 4 * g + 2 * kh);
+                    gw[j][s] = *reinterpret_cast<const uint16_t *>(base + 1024 + rit * 16 + 4 * g + 2 * kh);
+                }
             }
         }
-    };
-    // prologue: X~ of step kb in its slot, step kb + 1 in registers, code and
-    // gain words of kb and kb + 1 in flight (kb + 1 clamped)
-    const int64_t k1 = (kb + 1 < ke) ? kb + 1 : ke - 1;
-    x_load(xr[0], kb);
-    w_load<D, S, NT>(w[0], a, ebase, kb);
-    x_load(xr[1], k1);
-    w_load<D, S, NT>(w[1], a, ebase, k1);
-    x_store(xr[0], s_x[0]);
-    for (int64_t ks = kb; ks < ke; ks += 2) {
-        step(std::integral_constant<int, 0>(), ks);
-        if (ks + 1 < ke) step(std::integral_constant<int, 1>(), ks + 1);
-    }
-    __builtin_amdgcn_s_waitcnt(0);  // loads past the last step land before the block ends
-
-    // protected term (split 0 only): X[:, idx] (bf16) times bf16(q8 s), the
-    // weights of lane row 16 (NT w + j) + lane % 16 at positions 32 qq + 8 g + e
-    if (z == 0 && a.k > 0) {
-        const int64_t kp = q8_pitch(a.k);
-        for (int64_t qq = 0; qq < a.kp32 / 32; ++qq) {
-            const int64_t p0 = 32 * qq + 8 * g;
-            u32x4_t bp[NT];
+        // X~ fragments of k-slices 2 kh and 2 kh + 1
+        u32x4_t av[2][MT];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+                av[u][i] = *reinterpret_cast<const u32x4_t *>(xs + (16 * i + r16) * 256 + 16 * ((4 * g + 2 * kh + u) ^ r16));
+        // decoder entries of both k-slices: tv[j][u][s] (d = 16: the two
+        // halves of the chunk's entry are u = 0, 1); for d = 16 they are
+        // global loads, issued before this step's DMA so that waiting for
+        // them does not wait for it
+        f16x8_t tv[NT][2][S];
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                if constexpr (D == 8) {
+#pragma unroll
+                    for (int u = 0; u < 2; ++u)
+                        tv[j][u][s] = *reinterpret_cast<const f16x8_t *>(s_tab + (s * 256 + ((cw[j][s] >> (8 * u)) & 0xffu)) * 8);
+                } else {
+                    const f16x8_t *y = reinterpret_cast<const f16x8_t *>(a.tabh[s] + size_t(cw[j][s] & 0xffffu) * 16);
+                    tv[j][0][s] = y[0];
+                    tv[j][1][s] = y[1];
+                }
+            }
+        {
+            const int sn = (sl == 0) ? G::NS - 1 : sl - 1;
+            const int64_t kn = ks + G::NS - 1;
+            dma_step((kn < ke) ? kn : ke - 1, sn);
+        }
+        // per k-slice u: the B fragments (the 8 bf16 weights of the lane's
+        // inputs, each sum_s gain_s * D_s(code_s)[e] as an fp32 fma chain over
+        // fp16 gains and fp16 table values, rounded to bf16), then the MFMAs;
+        // slice 1's decode can run while slice 0's MFMAs execute
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            u32x4_t bq[NT];
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
-                const int64_t row = n0 + 16 * (NT * wave + j) + (lane & 15);
                 float v[8];
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int64_t p = p0 + e;
-                    v[e] = (row < a.d_out && p < a.k) ? float(a.q8[row * kp + p]) * a.scale[p] : 0.0f;
+                for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    const float gs = f16_bits_to_f32(uint16_t((D == 8) ? (gw[j][s] >> (16 * u)) : gw[j][s]));
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) v[e] = __builtin_fmaf(gs, float(tv[j][u][s][e]), v[e]);
                 }
-                bp[j] = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+                bq[j] = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
             }
-#pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                const u32x4_t av = *reinterpret_cast<const u32x4_t *>(a.Xp + (m0 + 16 * i + (lane & 15)) * a.kp32 + p0);
-#pragma unroll
-                for (int j = 0; j < NT; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                                         __builtin_bit_cast(bf16x8_t, bp[j]), acc[i][j], 0, 0, 0);
-            }
-        }
-    }
-
-    bool timed_out = false;
-    if (a.ksplit > 1) {
-        // partial tile in MFMA fragment order: slot ((wave MT + i) NT + j) 256
-        // + 64 r + lane of the split's [BM * BN] range
-        const int64_t tile = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-        uint64_t *tp = a.slots + tile * int64_t(a.ksplit - 1) * (BM * BN) + lane;
-        auto slot = [&](int zz, int i, int j, int r) { return tp + int64_t(zz) * (BM * BN) + ((wave * MT + i) * NT + j) * 256 + 64 * r; };
-        if (z < a.ksplit - 1) {
 #pragma unroll
             for (int i = 0; i < MT; ++i)
 #pragma unroll
                 for (int j = 0; j < NT; ++j)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r)
-                        __hip_atomic_store(slot(z, i, j, r), (uint64_t(1) << 32) | __float_as_uint(acc[i][j][r]),
-                                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            return;
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av[u][i]),
+                                                                         __builtin_bit_cast(bf16x8_t, bq[j]), acc[i][j], 0, 0, 0);
         }
-        // the finishing split: partials of splits 0 .. ksplit - 2 in order,
-        // then its own
-        f32x4_t sum[MT][NT];
+        sl = (sl + 1 == G::NS) ? 0 : sl + 1;
+    }
+    // the clamped DMAs past the last step land before the ring is reused
+    wait_vm<0>();
+    lds_barrier();
+
+    // protected term (split 0, by the kh = 1 waves): X[:, idx] (bf16) times
+    // bf16(q8 s), the weights of lane row 16 (NT rs + j) + lane % 16 at
+    // positions 32 qq + 8 g + e; two slices of 32 positions per round, all
+    // their loads issued together (int8 codes as one 8-byte word per row;
+    // positions past k read as zero)
+    if (kh == 1 && z == 0 && a.k > 0) {
+        const int64_t kp = q8_pitch(a.k), nq = a.kp32 / 32;
+        for (int64_t q0 = 0; q0 < nq; q0 += 2) {
+            uint2 qv[2][NT];
+            float sc[2][8];
+            u32x4_t xv[2][MT];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const bool live = q0 + h < nq;
+                const int64_t p0 = 32 * (q0 + h) + 8 * g;
+#pragma unroll
+                for (int j = 0; j < NT; ++j) {
+                    const int64_t row = n0 + 16 * (NT * rs + j) + r16;
+                    qv[h][j] = (live && row < a.d_out && p0 < kp) ? *reinterpret_cast<const uint2 *>(a.q8 + row * kp + p0)
+                                                                  : make_uint2(0u, 0u);
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) sc[h][e] = (live && p0 + e < a.k) ? a.scale[p0 + e] : 0.0f;
+#pragma unroll
+                for (int i = 0; i < MT; ++i)
+                    xv[h][i] = live ? *reinterpret_cast<const u32x4_t *>(a.Xp + (m0 + 16 * i + r16) * a.kp32 + p0)
+                                    : u32x4_t{0u, 0u, 0u, 0u};
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+#pragma unroll
+                for (int j = 0; j < NT; ++j) {
+                    float v[8];
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const uint32_t w = (e < 4) ? qv[h][j].x : qv[h][j].y;
+                        v[e] = float(int8_t(uint8_t(w >> (8 * (e & 3))))) * sc[h][e];
+                    }
+                    const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                               pack_bf16x2(v[6], v[7])};
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv[h][i]),
+                                                                             __builtin_bit_cast(bf16x8_t, bp), acc[i][j], 0, 0, 0);
+                }
+            }
+        }
+    }
+
+    // the kh = 1 half of every row set hands its tile to the kh = 0 half
+    // through LDS (the X~ ring, free now); the sum is kh 0 + kh 1
+    f32x4_t *s_red = reinterpret_cast<f32x4_t *>(s_mem);
+    if (kh == 1) {
 #pragma unroll
         for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int j = 0; j < NT; ++j) sum[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        for (int zz = 0; zz < a.ksplit - 1; ++zz) {
-            uint64_t pw[MT][NT][4];
-            for (int spin = 0;; ++spin) {
-                bool ready = true;
+            for (int j = 0; j < NT; ++j) s_red[((rs * MT + i) * NT + j) * 64 + lane] = acc[i][j];
+    }
+    lds_barrier();
+    if (kh == 0) {
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int j = 0; j < NT; ++j) acc[i][j] = acc[i][j] + s_red[((rs * MT + i) * NT + j) * 64 + lane];
+    }
+    lds_barrier();  // the exchange area is free again
+
+    bool timed_out = false;
+    if (a.ksplit > 1) {
+        // partial tile in MFMA fragment order: slot ((rs MT + i) NT + j) 256
+        // + 64 r + lane of the split's [BM * BN] range
+        const int64_t tile = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+        uint64_t *tp = a.slots + tile * int64_t(a.ksplit - 1) * (G::BM * G::BN) + lane;
+        auto slot = [&](int zz, int i, int j, int r) { return tp + int64_t(zz) * (G::BM * G::BN) + ((rs * MT + i) * NT + j) * 256 + 64 * r; };
+        if (z < a.ksplit - 1) {  // (uniform over the workgroup)
+            if (kh == 0) {
 #pragma unroll
                 for (int i = 0; i < MT; ++i)
 #pragma unroll
                     for (int j = 0; j < NT; ++j)
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            pw[i][j][r] = __hip_atomic_load(slot(zz, i, j, r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                            ready &= (pw[i][j][r] >> 32) != 0;
-                        }
-                if (__all(ready)) break;
-                if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
-                    timed_out = true;
-                    break;
-                }
-                __builtin_amdgcn_s_sleep(2);
+                        for (int r = 0; r < 4; ++r)
+                            __hip_atomic_store(slot(z, i, j, r), (uint64_t(1) << 32) | __float_as_uint(acc[i][j][r]),
+                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             }
-#pragma unroll
-            for (int i = 0; i < MT; ++i)
-#pragma unroll
-                for (int j = 0; j < NT; ++j)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        sum[i][j][r] += __uint_as_float(uint32_t(pw[i][j][r]));
-                        __hip_atomic_store(slot(zz, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    }
+            return;
         }
+        // the finishing split (kh = 0 waves): per token group, the partials
+        // of splits 0 .. ksplit - 2 in order, then its own
+        if (kh == 0) {
 #pragma unroll
-        for (int i = 0; i < MT; ++i)
+            for (int i = 0; i < MT; ++i) {
+                f32x4_t sum[NT];
 #pragma unroll
-            for (int j = 0; j < NT; ++j) acc[i][j] = sum[i][j] + acc[i][j];
+                for (int j = 0; j < NT; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+                for (int zz = 0; zz < a.ksplit - 1; ++zz) {
+                    uint64_t pw[NT][4];
+                    for (int spin = 0;; ++spin) {
+                        bool ready = true;
+#pragma unroll
+                        for (int j = 0; j < NT; ++j)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                pw[j][r] = __hip_atomic_load(slot(zz, i, j, r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                ready &= (pw[j][r] >> 32) != 0;
+                            }
+                        if (__all(ready)) break;
+                        if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
+                            timed_out = true;
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+#pragma unroll
+                    for (int j = 0; j < NT; ++j)
+#pragma unroll
+                        for (int r = 0; r < 4; ++r) {
+                            sum[j][r] += __uint_as_float(uint32_t(pw[j][r]));
+                            __hip_atomic_store(slot(zz, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        }
+                }
+#pragma unroll
+                for (int j = 0; j < NT; ++j) acc[i][j] = sum[j] + acc[i][j];
+            }
+        }
     }
 
-    // epilogue: LoRA, then Y
+    // epilogue (all of LDS is free now): the kh = 0 waves add LoRA and put
+    // the tile in LDS as fp32 [BM][BN + 4]; then every thread stores
+    // 8-output segments of the tile's rows (one 16-byte store per bf16
+    // segment, two per fp32 segment, when Y allows; element stores at a
+    // ragged edge)
+    constexpr int OS = G::BN + 4;  // row stride of the staged tile (floats)
+    static_assert(size_t(G::BM) * OS * 4 <= G::LDS, "the output tile fits in LDS");
+    float *s_out = reinterpret_cast<float *>(s_mem);
+    if (kh == 0) {
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-        const int64_t n = n0 + 16 * (NT * wave + j) + (lane & 15);
-        if (n >= a.d_out) continue;
-        float bl[BSQ_MAX_LORA_RANK];
+        for (int j = 0; j < NT; ++j) {
+            const int nl = 16 * (NT * rs + j) + r16;
+            const int64_t n = n0 + nl;
+            const int64_t nc = (n < a.d_out) ? n : a.d_out - 1;
+            float bl[BSQ_MAX_LORA_RANK];
 #pragma unroll
-        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bl[q] = (q < a.rank) ? bf16_to_f32(a.B[n * a.rank + q]) : 0.0f;
+            for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bl[q] = (q < a.rank) ? bf16_to_f32(a.B[nc * a.rank + q]) : 0.0f;
 #pragma unroll
-        for (int i = 0; i < MT; ++i) {
+            for (int i = 0; i < MT; ++i) {
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int64_t m = m0 + 16 * i + 4 * g + r;
-                if (m >= a.M) continue;
-                float v = timed_out ? __builtin_nanf("") : acc[i][j][r];
-                if (a.rank > 0) {
-                    const float *Tm = a.T + m * BSQ_MAX_LORA_RANK;
+                for (int r = 0; r < 4; ++r) {
+                    const int ml = 16 * i + 4 * g + r;
+                    float v = timed_out ? __builtin_nanf("") : acc[i][j][r];
+                    if (a.rank > 0) {
+                        const float *Tm = a.T + (m0 + ml) * BSQ_MAX_LORA_RANK;
 #pragma unroll
-                    for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) v = __builtin_fmaf(bl[q], Tm[q], v);
+                        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) v = __builtin_fmaf(bl[q], Tm[q], v);
+                    }
+                    s_out[ml * OS + nl] = v;
                 }
-                if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n] = f32_to_bf16(v);
-                else static_cast<float *>(a.Y)[m * a.ldy + n] = v;
+            }
+        }
+    }
+    lds_barrier();
+    for (int e = t; e < G::BM * (G::BN / 8); e += 512) {
+        const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
+        const int64_t m = m0 + ml, n = n0 + nl;
+        if (m >= a.M || n >= a.d_out) continue;
+        const float4 lo = *reinterpret_cast<const float4 *>(s_out + ml * OS + nl);
+        const float4 hi = *reinterpret_cast<const float4 *>(s_out + ml * OS + nl + 4);
+        const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if (a.y_vec && n + 8 <= a.d_out) {
+            if (a.y_bf16) {
+                *reinterpret_cast<u32x4_t *>(static_cast<uint16_t *>(a.Y) + m * a.ldy + n) =
+                    u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+            } else {
+                float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.Y) + m * a.ldy + n);
+                dst[0] = lo;
+                dst[1] = hi;
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                if (n + c >= a.d_out) break;
+                if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n + c] = f32_to_bf16(v[c]);
+                else static_cast<float *>(a.Y)[m * a.ldy + n + c] = v[c];
             }
         }
     }
@@ -481,10 +603,8 @@ struct GemmPlan {
 GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
 {
     GemmPlan p{};
-    int occ;  // blocks per CU the variant reaches (LDS)
-    if (M <= 16) p.mt = 1, p.nt = 1, occ = 4;
-    else if (M <= 64) p.mt = 4, p.nt = 2, occ = 2;
-    else p.mt = 8, p.nt = 2, occ = 1;
+    p.mt = (M <= 16) ? 1 : (M <= 64) ? 4 : 8;
+    p.nt = 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -494,10 +614,12 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     p.Kp = p.ksteps * BK;
     p.kp32 = (k + 31) & ~int64_t(31);
     const int64_t tiles = p.nblk * p.mtiles;
-    // about two rounds of blocks over 256 CUs, at least 4 K steps per block,
-    // the flagged partials within GEMM_SLOT_BYTES
-    int64_t ks = (2 * 256 * occ + tiles - 1) / (tiles > 0 ? tiles : 1);
-    ks = std::min<int64_t>(ks, p.ksteps / 4);
+    // one workgroup per compute unit (the LDS rings take most of its LDS):
+    // split K as far as one round of workgroups over the 256 compute units
+    // allows (a second, partial round would double the time), keeping at least
+    // 2 K steps per split and the flagged partials within GEMM_SLOT_BYTES
+    int64_t ks = 256 / (tiles > 0 ? tiles : 1);
+    ks = std::min<int64_t>(ks, p.ksteps / 2);
     ks = std::min<int64_t>(ks, 1 + GEMM_SLOT_BYTES / std::max<int64_t>(1, tiles * p.bm * p.bn * 8));
     ks = std::min<int64_t>(ks, 64);
     p.ksplit = std::max<int64_t>(ks, 1);
@@ -511,15 +633,23 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
 template <int D, int S, int MT, int NT>
 hipError_t launch_main(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 {
+    using G = GemmShape<D, S, MT, NT>;
+    static bool lds_set = false;  // the LDS rings exceed the default dynamic LDS limit
+    if (!lds_set) {
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(&gemm_kernel<D, S, MT, NT>),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, int(G::LDS));
+        if (e != hipSuccess) return e;
+        lds_set = true;
+    }
     const dim3 grid = dim3(unsigned(p.nblk), unsigned(p.mtiles), unsigned(p.ksplit));
-    hipLaunchKernelGGL((gemm_kernel<D, S, MT, NT>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((gemm_kernel<D, S, MT, NT>), grid, dim3(512), G::LDS, st, a);
     return hipGetLastError();
 }
 
 template <int D, int S>
 hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 {
-    if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
+    if (p.mt == 1) return launch_main<D, S, 1, 2>(a, p, st);
     if (p.mt == 4) return launch_main<D, S, 4, 2>(a, p, st);
     return launch_main<D, S, 8, 2>(a, p, st);
 }
@@ -561,6 +691,10 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     a.ldy = ldy;
     a.Y = Y;
     a.y_bf16 = (y_dtype == BSQ_BF16);
+    {
+        const int64_t es = a.y_bf16 ? 2 : 4;
+        a.y_vec = (reinterpret_cast<uintptr_t>(Y) % 16 == 0) && ((ldy * es) % 16 == 0);
+    }
     a.rank = 0;
     a.ksplit = int(p.ksplit);
     a.slots = static_cast<uint64_t *>(ws);
