@@ -71,8 +71,11 @@ struct GemmArgs {
 };
 
 // ---------------------------------------------------------------------------
-// Prep: one block per padded token row m < Mp.
+// Prep: one workgroup per (padded token row m < Mp, block of PREP_COLS X~
+// columns); the first column block of a row also writes its protected
+// activations and T.
 // ---------------------------------------------------------------------------
+constexpr int PREP_COLS = 2048;  // X~ columns per prep workgroup (256 threads x 8)
 struct PrepArgs {
     const uint16_t *X;
     int64_t ldx, M, d_in, Kp, k, kp32;
@@ -86,38 +89,41 @@ struct PrepArgs {
 
 __global__ __launch_bounds__(256) void gemm_prep(const PrepArgs a)
 {
-    extern __shared__ uint32_t s_bits[];  // [Kp / 32] protected bitmap
+    // workgroup (m, cb): token row m < Mp, X~ columns [2048 cb, 2048 cb + 2048)
+    __shared__ uint32_t s_bits[PREP_COLS / 32];  // protected bitmap of the column block
     __shared__ float s_red[BSQ_MAX_LORA_RANK][4];
     const int t = threadIdx.x;
-    const int64_t m = blockIdx.x;
+    const int64_t m = blockIdx.x, c0 = int64_t(blockIdx.y) * PREP_COLS;
     const bool live = m < a.M;
-    const int64_t words = a.Kp / 32;
-    for (int64_t w = t; w < words; w += 256) s_bits[w] = 0u;
+    if (t < PREP_COLS / 32) s_bits[t] = 0u;
     __syncthreads();
     for (int64_t p = t; p < a.k; p += 256) {
         const int32_t j = a.idx[p];
-        if (j >= 0 && j < a.d_in) atomicOr(&s_bits[j >> 5], 1u << (j & 31));
+        if (j >= 0 && j < a.d_in && j >= c0 && j < c0 + PREP_COLS) atomicOr(&s_bits[(j - c0) >> 5], 1u << (j & 31));
     }
     __syncthreads();
     const uint16_t *xr = a.X + m * a.ldx;
-    // X~: 8-input segments; protected inputs, inputs past d_in and rows past
-    // M are zero
-    for (int64_t sg = t; sg < a.Kp / 8; sg += 256) {
-        const int64_t j0 = sg * 8;
-        u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
-        if (live && j0 < a.d_in) {
-            v = *reinterpret_cast<const u32x4_t *>(xr + j0);
-            const uint32_t pm = (s_bits[j0 >> 5] >> (j0 & 31)) & 0xffu;
-            if (pm) {
+    // X~: one 8-input segment per thread; protected inputs, inputs past d_in
+    // and rows past M are zero
+    {
+        const int64_t j0 = c0 + 8 * t;
+        if (j0 < a.Kp) {
+            u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
+            if (live && j0 < a.d_in) {
+                v = *reinterpret_cast<const u32x4_t *>(xr + j0);
+                const uint32_t pm = (s_bits[(8 * t) >> 5] >> ((8 * t) & 31)) & 0xffu;
+                if (pm) {
 #pragma unroll
-                for (int h = 0; h < 4; ++h) {
-                    const uint32_t keep = (((pm >> (2 * h)) & 1u) ? 0u : 0xffffu) | (((pm >> (2 * h + 1)) & 1u) ? 0u : 0xffff0000u);
-                    v[h] &= keep;
+                    for (int h = 0; h < 4; ++h) {
+                        const uint32_t keep = (((pm >> (2 * h)) & 1u) ? 0u : 0xffffu) | (((pm >> (2 * h + 1)) & 1u) ? 0u : 0xffff0000u);
+                        v[h] &= keep;
+                    }
                 }
             }
+            *reinterpret_cast<u32x4_t *>(a.Xt + m * a.Kp + j0) = v;
         }
-        *reinterpret_cast<u32x4_t *>(a.Xt + m * a.Kp + j0) = v;
     }
+    if (blockIdx.y != 0) return;
     // gathered protected activations, zero past k
     for (int64_t p = t; p < a.kp32; p += 256) {
         uint16_t v = 0;
@@ -193,7 +199,11 @@ struct GemmShape {
     static constexpr int WU = (D == 8) ? 192 : 128;
     static constexpr int XSLOT = BM * 256;            // bytes: [BM][128] bf16
     static constexpr int WSLOT = NT * S * WU * 16;    // bytes: [NT][S][codes | gains]
-    static constexpr int TAB = (D == 8) ? S * 4096 : 0;  // fp16 decoder tables [S][256][8]
+    // fp16 decoder tables (d = 8) [S][256 codes][TC copies][8]: lane l reads
+    // copy l % TC, which spreads the random lookups of a wave over the LDS
+    // banks; 8 copies where three ring slots still fit, else one
+    static constexpr int TC = (D == 8 && (GEMM_LDS_BYTES - S * 4096 * 8) / (XSLOT + WSLOT) >= 3) ? 8 : 1;
+    static constexpr int TAB = (D == 8) ? S * 4096 * TC : 0;
     static constexpr int NS_FIT = (GEMM_LDS_BYTES - TAB) / (XSLOT + WSLOT);
     static constexpr int NS = NS_FIT < 8 ? NS_FIT : 8;
     static constexpr int NXI = BM / 4;              // X~ DMA wave instructions per step
@@ -203,7 +213,7 @@ struct GemmShape {
     static constexpr size_t LDS = size_t(NS) * (XSLOT + WSLOT) + TAB;
     static_assert(NS >= 2, "two pipeline stages fit in LDS");
     static_assert(MT * NT * 4096 <= NS * XSLOT, "the exchange of the two K halves fits in the X~ ring");
-    static_assert((NS - 2) * PMAX <= 63, "wait count fits vmcnt");
+    static_assert((NS - 1) * PMAX <= 63, "wait count fits vmcnt");
     static_assert(WU % 64 == 0, "a DMA instruction stays within one (tile, stage)");
 };
 
@@ -226,7 +236,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
     typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
     extern __shared__ __attribute__((aligned(16))) uint4 s_mem4[];
     uint8_t *s_mem = reinterpret_cast<uint8_t *>(s_mem4);
-    uint8_t *s_xr = s_mem;                          // X~ ring, 16-byte segment s of row r at s ^ (r % 16)
+    uint8_t *s_xr = s_mem;                          // X~ ring (MFMA fragment order)
     uint8_t *s_wr = s_mem + G::NS * G::XSLOT;       // weight ring
     uint4 *s_tab4 = reinterpret_cast<uint4 *>(s_wr + G::NS * G::WSLOT);  // d = 8 tables
     const uint16_t *s_tab = reinterpret_cast<const uint16_t *>(s_tab4);
@@ -256,8 +266,10 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
         const int v0 = wave + 8 * r;
         const int v = (v0 < G::NI) ? v0 : G::NI - 1;  // (r-th instruction absent when v0 >= NI)
         if (v < G::NXI) {
-            const int u = 64 * v + lane, row = u >> 4, sp = u & 15;
-            dsrc[r] = reinterpret_cast<const uint8_t *>(a.Xt + (m0 + row) * a.Kp + 8 * (sp ^ (row & 15)));
+            // X~ slot in MFMA fragment order: unit (q MT + i) 64 + l holds the
+            // 8 inputs 32 (l / 16) + 8 q of token 16 i + l % 16 (k-slice q)
+            const int q = v / MT, i = v - q * MT;
+            dsrc[r] = reinterpret_cast<const uint8_t *>(a.Xt + (m0 + 16 * i + r16) * a.Kp + 32 * g + 8 * q);
             dA[r] = 2 * 2 * BK;
             dB[r] = 2 * BK;
             dx[r] = true;
@@ -288,43 +300,46 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
         }
     }
     const int pw = (wave < G::NI % 8) ? G::PMAX : G::PMIN;  // this wave's DMA instructions per step
-    auto dma_step = [&](int64_t ks, int sl) {
+    // issue group: X~ of step kx into X~ slot slx and the weights of step kw
+    // into weight slot slw (w_only: the weights alone)
+    auto dma_group = [&](int64_t kx, int slx, int64_t kw, int slw, bool w_only) {
 #pragma unroll
         for (int r = 0; r < G::PMAX; ++r) {
             if (r >= G::PMIN && wave + 8 * r >= G::NI) continue;
-            const uint4 *src = reinterpret_cast<const uint4 *>(dsrc[r] + (ks >> 1) * dA[r] + (ks & 1) * dB[r]);
-            uint8_t *dst = (dx[r] ? s_xr : s_wr) + sl * dslot[r] + doff[r];
+            if (w_only && dx[r]) continue;
+            const int64_t k = dx[r] ? kx : kw;
+            const uint4 *src = reinterpret_cast<const uint4 *>(dsrc[r] + (k >> 1) * dA[r] + (k & 1) * dB[r]);
+            uint8_t *dst = dx[r] ? s_xr + slx * G::XSLOT + doff[r] : s_wr + slw * G::WSLOT + doff[r];
             __builtin_amdgcn_global_load_lds(src, reinterpret_cast<uint4 *>(dst), 16, 0, 0);
         }
     };
+    auto clampk = [&](int64_t k) { return (k < ke) ? k : ke - 1; };
 
-    // prologue: the decoder tables (d = 8; older than every step's DMA, so
-    // the first step's wait covers them), then steps kb .. kb + NS - 2
+    // Software pipeline over the K steps. Group c (c >= 0) carries the X~ of
+    // step kb + c (X~ slot c % NS) and the weights of step kb + c + 1 (weight
+    // slot (c + 1) % NS); group -1 the weights of step kb. Iteration c runs
+    // the MFMAs of step kb + c with B fragments decoded in iteration c - 1
+    // while it decodes step kb + c + 1, so the matrix cores and the decode
+    // arithmetic overlap. Steps past ke - 1 are clamped (harmless reloads
+    // into slots no later iteration reads before they are refilled).
     if constexpr (D == 8) {
-        for (int v = wave; v < S * 4; v += 8) {  // 1 KiB of stage v / 4
-            const uint4 *src = reinterpret_cast<const uint4 *>(a.tabh[v >> 2]) + (v & 3) * 64 + lane;
+        // decoder tables: wave instruction v fills LDS units 64 v .. + 63, unit
+        // (s 256 + e) TC + c = copy c of entry e of stage s
+        for (int v = wave; v < S * 4 * G::TC; v += 8) {
+            const int u = 64 * v + lane, se = u / G::TC;
+            const uint4 *src = reinterpret_cast<const uint4 *>(a.tabh[se >> 8]) + (se & 255);
             __builtin_amdgcn_global_load_lds(src, s_tab4 + 64 * v, 16, 0, 0);
         }
     }
+    dma_group(0, 0, kb, 0, true);
 #pragma unroll
-    for (int p = 0; p < G::NS - 1; ++p) dma_step((kb + p < ke) ? kb + p : ke - 1, p);
+    for (int c = 0; c < G::NS - 1; ++c) dma_group(clampk(kb + c), c, clampk(kb + c + 1), (c + 1) % G::NS, false);
 
-    f32x4_t acc[MT][NT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-
-    int sl = 0;  // slot of step ks
-    for (int64_t ks = kb; ks < ke; ++ks) {
-        if (pw == G::PMAX) wait_vm<(G::NS - 2) * G::PMAX>();
-        else wait_vm<(G::NS - 2) * G::PMIN>();
-        lds_barrier();
-        const uint8_t *ws = s_wr + sl * G::WSLOT;
-        const uint8_t *xs = s_xr + sl * G::XSLOT;
-        // code and gain words of this wave's chunks: d = 8, chunks 4 g + 2 kh
-        // and + 1 (two codes, two gains); d = 16, chunk 2 g + kh
-        uint32_t cw[NT][S], gw[NT][S];
+    // code and gain words of this wave's chunks in weight slot sw: d = 8,
+    // chunks 4 g + 2 kh and + 1 (two codes, two gains); d = 16, chunk 2 g + kh
+    uint32_t cw[NT][S], gw[NT][S];
+    auto load_words = [&](int sw) {
+        const uint8_t *ws = s_wr + sw * G::WSLOT;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
             const int grp = NT * rs + j, jt = grp >> 2, rit = 16 * (grp & 3) + r16;
@@ -340,18 +355,11 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
                 }
             }
         }
-        // X~ fragments of k-slices 2 kh and 2 kh + 1
-        u32x4_t av[2][MT];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-            for (int i = 0; i < MT; ++i)
-                av[u][i] = *reinterpret_cast<const u32x4_t *>(xs + (16 * i + r16) * 256 + 16 * ((4 * g + 2 * kh + u) ^ r16));
-        // decoder entries of both k-slices: tv[j][u][s] (d = 16: the two
-        // halves of the chunk's entry are u = 0, 1); for d = 16 they are
-        // global loads, issued before this step's DMA so that waiting for
-        // them does not wait for it
-        f16x8_t tv[NT][2][S];
+    };
+    // decoder entries of both k-slices: tv[j][u][s] (d = 16: the two halves
+    // of the chunk's entry are u = 0, 1; global loads)
+    f16x8_t tv[NT][2][S];
+    auto load_tables = [&]() {
 #pragma unroll
         for (int j = 0; j < NT; ++j)
 #pragma unroll
@@ -359,25 +367,21 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
                 if constexpr (D == 8) {
 #pragma unroll
                     for (int u = 0; u < 2; ++u)
-                        tv[j][u][s] = *reinterpret_cast<const f16x8_t *>(s_tab + (s * 256 + ((cw[j][s] >> (8 * u)) & 0xffu)) * 8);
+                        tv[j][u][s] = *reinterpret_cast<const f16x8_t *>(
+                            s_tab + ((s * 256 + ((cw[j][s] >> (8 * u)) & 0xffu)) * G::TC + (lane & (G::TC - 1))) * 8);
                 } else {
                     const f16x8_t *y = reinterpret_cast<const f16x8_t *>(a.tabh[s] + size_t(cw[j][s] & 0xffffu) * 16);
                     tv[j][0][s] = y[0];
                     tv[j][1][s] = y[1];
                 }
             }
-        {
-            const int sn = (sl == 0) ? G::NS - 1 : sl - 1;
-            const int64_t kn = ks + G::NS - 1;
-            dma_step((kn < ke) ? kn : ke - 1, sn);
-        }
-        // per k-slice u: the B fragments (the 8 bf16 weights of the lane's
-        // inputs, each sum_s gain_s * D_s(code_s)[e] as an fp32 fma chain over
-        // fp16 gains and fp16 table values, rounded to bf16), then the MFMAs;
-        // slice 1's decode can run while slice 0's MFMAs execute
+    };
+    // B fragments: bq[j][u] = the 8 bf16 weights of the lane's inputs in
+    // k-slice 2 kh + u, each sum_s gain_s * D_s(code_s)[e] as an fp32 fma
+    // chain over fp16 gains and fp16 table values, rounded to bf16
+    auto decode = [&](u32x4_t (&bq)[NT][2]) {
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            u32x4_t bq[NT];
+        for (int u = 0; u < 2; ++u)
 #pragma unroll
             for (int j = 0; j < NT; ++j) {
                 float v[8];
@@ -389,16 +393,57 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
 #pragma unroll
                     for (int e = 0; e < 8; ++e) v[e] = __builtin_fmaf(gs, float(tv[j][u][s][e]), v[e]);
                 }
-                bq[j] = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+                bq[j][u] = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
             }
+    };
+
+    u32x4_t bq[NT][2];
+    // group -1 has landed (the NS - 1 younger groups may still be in flight)
+    if (pw == G::PMAX) wait_vm<(G::NS - 1) * G::PMAX>();
+    else wait_vm<(G::NS - 1) * G::PMIN>();
+    lds_barrier();
+    load_words(0);
+    load_tables();
+    decode(bq);
+
+    f32x4_t acc[MT][NT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    int sx = 0;                      // X~ slot of step ks (c % NS)
+    int swn = (G::NS > 1) ? 1 : 0;   // weight slot of step ks + 1 ((c + 1) % NS)
+    for (int64_t ks = kb; ks < ke; ++ks) {
+        if (pw == G::PMAX) wait_vm<(G::NS - 2) * G::PMAX>();
+        else wait_vm<(G::NS - 2) * G::PMIN>();
+        lds_barrier();
+        load_words(swn);
+        if constexpr (D == 16) load_tables();  // global: issued before this iteration's DMA
+        {
+            // group c + NS - 1: X~ slot (c - 1) % NS, weight slot c % NS
+            const int slx = (sx == 0) ? G::NS - 1 : sx - 1;
+            const int slw = (swn == 0) ? G::NS - 1 : swn - 1;
+            dma_group(clampk(ks + G::NS - 1), slx, clampk(ks + G::NS), slw, false);
+        }
+        if constexpr (D == 8) load_tables();
+        const uint8_t *xs = s_xr + sx * G::XSLOT;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+            u32x4_t av[MT];
+#pragma unroll
+            for (int i = 0; i < MT; ++i)
+                av[i] = reinterpret_cast<const u32x4_t *>(xs)[((2 * kh + u) * MT + i) * 64 + lane];
 #pragma unroll
             for (int i = 0; i < MT; ++i)
 #pragma unroll
                 for (int j = 0; j < NT; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av[u][i]),
-                                                                         __builtin_bit_cast(bf16x8_t, bq[j]), acc[i][j], 0, 0, 0);
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av[i]),
+                                                                         __builtin_bit_cast(bf16x8_t, bq[j][u]), acc[i][j], 0, 0, 0);
         }
-        sl = (sl + 1 == G::NS) ? 0 : sl + 1;
+        decode(bq);  // step ks + 1
+        sx = (sx + 1 == G::NS) ? 0 : sx + 1;
+        swn = (swn + 1 == G::NS) ? 0 : swn + 1;
     }
     // the clamped DMAs past the last step land before the ring is reused
     wait_vm<0>();
@@ -492,24 +537,30 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
             return;
         }
         // the finishing split (kh = 0 waves): per token group, the partials
-        // of splits 0 .. ksplit - 2 in order, then its own
+        // of splits 0 .. ksplit - 2 (polled SPL splits at a time, their loads
+        // in flight together), added in split order, then its own
         if (kh == 0) {
+            constexpr int SPL = (MT <= 2) ? 4 : 1;
 #pragma unroll
             for (int i = 0; i < MT; ++i) {
                 f32x4_t sum[NT];
 #pragma unroll
                 for (int j = 0; j < NT; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-                for (int zz = 0; zz < a.ksplit - 1; ++zz) {
-                    uint64_t pw[NT][4];
+                for (int z0 = 0; z0 < a.ksplit - 1; z0 += SPL) {
+                    uint64_t pw[SPL][NT][4];
                     for (int spin = 0;; ++spin) {
                         bool ready = true;
 #pragma unroll
-                        for (int j = 0; j < NT; ++j)
+                        for (int zi = 0; zi < SPL; ++zi) {
+                            const int zz = (z0 + zi < a.ksplit - 1) ? z0 + zi : a.ksplit - 2;  // (clamped: a re-read)
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) {
-                                pw[j][r] = __hip_atomic_load(slot(zz, i, j, r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                                ready &= (pw[j][r] >> 32) != 0;
-                            }
+                            for (int j = 0; j < NT; ++j)
+#pragma unroll
+                                for (int r = 0; r < 4; ++r) {
+                                    pw[zi][j][r] = __hip_atomic_load(slot(zz, i, j, r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                    ready &= (pw[zi][j][r] >> 32) != 0;
+                                }
+                        }
                         if (__all(ready)) break;
                         if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
                             timed_out = true;
@@ -518,12 +569,16 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
                         __builtin_amdgcn_s_sleep(2);
                     }
 #pragma unroll
-                    for (int j = 0; j < NT; ++j)
+                    for (int zi = 0; zi < SPL; ++zi) {
+                        if (z0 + zi >= a.ksplit - 1) break;
 #pragma unroll
-                        for (int r = 0; r < 4; ++r) {
-                            sum[j][r] += __uint_as_float(uint32_t(pw[j][r]));
-                            __hip_atomic_store(slot(zz, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                        }
+                        for (int j = 0; j < NT; ++j)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) {
+                                sum[j][r] += __uint_as_float(uint32_t(pw[zi][j][r]));
+                                __hip_atomic_store(slot(z0 + zi, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            }
+                    }
                 }
 #pragma unroll
                 for (int j = 0; j < NT; ++j) acc[i][j] = sum[j] + acc[i][j];
@@ -717,7 +772,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
         pa.A = lora->A;
         pa.rank = lora->rank;
     }
-    hipLaunchKernelGGL(gemm_prep, dim3(unsigned(p.Mp)), dim3(256), size_t(p.Kp / 32) * 4, st, pa);
+    hipLaunchKernelGGL(gemm_prep, dim3(unsigned(p.Mp), unsigned((p.Kp + PREP_COLS - 1) / PREP_COLS)), dim3(256), 0, st, pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 
