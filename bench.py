@@ -15,7 +15,9 @@ Steps are replayed from a HIP graph holding one pass over the copies. `value`
 is the compressed bytes the step must move (code planes, gain planes, int8
 payload, scales, indices, x, y) divided by the step time. Encode throughput
 (Mchunks/s), decode GB/s and the fused GEMM's TFLOP/s at M = 16/64/256 are
-measured in the same run on the same weights.
+measured in the same run on the same weights, as is `comparator`: on the gate
+projection, the unfused path (bsq_decode to bf16, then the library product)
+and the library product on a stored W_hat, beside the fused kernels.
 
 `roofline` covers the dominant kernel (the streaming GEMV of the gate/up
 group): algorithmic bytes per launch / its mean launch time from HIP events
@@ -227,7 +229,7 @@ def main():
         with torch.cuda.stream(s):
             kg.replay()
             torch.cuda.synchronize()
-            for _ in range(5):
+            for _ in range(20):
                 a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 a0.record(s)
                 kg.replay()
@@ -235,12 +237,14 @@ def main():
                 torch.cuda.synchronize()
                 k_times.append(a0.elapsed_time(a1) / n_k)
         k_ms = float(np.median(k_times))
+        k_p10, k_p90 = float(np.percentile(k_times, 10)), float(np.percentile(k_times, 90))
         gu = [blk.layers[p.name].mat(0) for p in blk.groups()["gateup"]]
         k_bytes = algorithmic_bytes(gu, 4096, 2 * 12288)
         k_gbs = k_bytes / (k_ms / 1e3) / 1e9
         log(f"[bench] d={d}: gate/up streaming GEMV {k_ms * 1e3:.1f} us/launch, {k_gbs:.0f} GB/s")
         res = dict(ms_per_step=ms, gbs=gbs, step_bytes=step_bytes, encode_mchunks=blk.chunks / blk.encode_s / 1e6,
-                   kernel_us=k_ms * 1e3, kernel_bytes=k_bytes, kernel_gbs=k_gbs)
+                   kernel_us=k_ms * 1e3, kernel_bytes=k_bytes, kernel_gbs=k_gbs,
+                   kernel_us_p10=k_p10 * 1e3, kernel_us_p90=k_p90 * 1e3)
 
         if not args.profile_gemv_only:
             # decode GB/s (reads the planes, writes bf16 W_hat) on the largest projection
@@ -295,6 +299,7 @@ def main():
                     gem[str(M)] = dict(tflops=round(tf, 1), pct_bf16_mfma_peak=round(100 * tf / BF16_MFMA_PEAK_TFLOPS, 2))
                     log(f"[bench] d={d}: gemm M={M}: {tf:.1f} TFLOP/s")
                 res["gemm"] = gem
+                res["comparator"] = comparator(blk, bsq, synth, torch, dev, args.copies)
         results[d] = res
         if head is None:
             head = (blk, plans)
@@ -357,6 +362,7 @@ def main():
         "encode_mchunks_per_s": round(hd["encode_mchunks"], 1),
         "decode_gbs": round(hd.get("decode_gbs", 0.0), 1),
         "gemm": hd.get("gemm"),
+        "comparator": hd.get("comparator"),
         "roofline": {
             "kernel": f"gemv_lane_kernel<{args.d}, 2, TPW> (gate/up launch of bsq_gemv_run, d={args.d})",
             "bound": "hbm",
@@ -367,6 +373,7 @@ def main():
             "traffic": traffic,
             "algorithmic_bytes_per_launch": hd["kernel_bytes"],
             "mean_launch_us": round(hd["kernel_us"], 2),
+            "launch_us_p10_p90": [round(hd["kernel_us_p10"], 2), round(hd["kernel_us_p90"], 2)],
         },
         "cpu_baseline": cpu,
         "stacks": stacks or None,
@@ -464,6 +471,69 @@ def stack_bench(bsq, synth, torch, np, projs, n_layers, d, lora_rank, dev, tag):
     return res
 
 
+def graph_us(torch, fns, reps=4):
+    """Mean time per call of fns (a list of callables issued in order),
+    captured in one HIP graph on a side stream and replayed."""
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        for f in fns:
+            f()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for f in fns:
+                f()
+        g.replay()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        for _ in range(reps):
+            g.replay()
+        b.record(s)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e3 / (reps * len(fns))
+
+
+def comparator(blk, bsq, synth, torch, dev, copies):
+    """The paper's own inference path as an unfused comparator on the gate
+    projection: bsq_decode to bf16 W_hat, then the library product
+    (torch.nn.functional.linear, i.e. hipBLASLt), per call; and the library
+    product alone (W_hat decoded once and kept, 2 B per weight). Against the
+    fused bsq_gemv (M = 1) and bsq_gemm (M = 16, 64, 256), all timed by graph
+    replay over the encoded copies."""
+    import torch.nn.functional as F
+    name = "gate"
+    Ls = [blk.layers[name].mat(r) for r in range(copies)]
+    codec = blk.codecs[name]
+    d_out, d_in = Ls[0].d_out, Ls[0].d_in
+    W_hat = torch.empty((d_out, d_in), dtype=torch.bfloat16, device=dev)
+    out = {}
+    for M in (1, 16, 64, 256):
+        X = synth.activation(d_in, seed=900 + M, device=dev, batch=M) if M > 1 else synth.activation(d_in, seed=901, device=dev)
+        Y = torch.empty((M, d_out) if M > 1 else (d_out,), dtype=torch.bfloat16, device=dev)
+        Xm = X if M > 1 else X.view(1, d_in)
+        if M == 1:
+            plans = [bsq.GemvPlan(blk.cfg, [codec], [L], X) for L in Ls]
+            fused = graph_us(torch, [(lambda pl=pl: pl()) for pl in plans])
+        else:
+            ws = torch.zeros(bsq.bsq_workspace_bytes(blk.cfg, bsq.OP_GEMM, 1, d_out, d_in, M) + 256,
+                             dtype=torch.uint8, device=dev)
+            ws = ws[(-ws.data_ptr()) % 256:]
+            fused = graph_us(torch, [(lambda L=L: bsq.bsq_gemm(blk.cfg, codec, L, X, out=Y, ws=ws)) for L in Ls])
+            del ws
+        unfused = graph_us(torch, [(lambda L=L: (bsq.bsq_decode(blk.cfg, codec, L, out=W_hat),
+                                                 torch.matmul(Xm, W_hat.t(), out=Y.view(Xm.shape[0], d_out))))
+                                   for L in Ls])
+        library = graph_us(torch, [(lambda: torch.matmul(Xm, W_hat.t(), out=Y.view(Xm.shape[0], d_out)))] * copies)
+        out[str(M)] = {"fused_us": round(fused, 1), "decode_then_library_us": round(unfused, 1),
+                       "library_on_stored_w_hat_us": round(library, 1)}
+        log(f"[bench] comparator M={M}: fused {fused:.1f} us, decode+library {unfused:.1f} us, "
+            f"library on stored W_hat {library:.1f} us")
+    del W_hat
+    return {"projection": f"gate {d_out}x{d_in}, d={blk.cfg.d}", "library": "torch.matmul (hipBLASLt), bf16",
+            "per_M": out}
+
+
 def cpu_baseline(blk, torch):
     """The oracle's fused GEMV route (plain C, fp64, OpenMP rows) on the host
     cores over copy 0 of the q projection, repeated to about 10 s of CPU time."""
@@ -497,9 +567,29 @@ def cpu_baseline(blk, torch):
             break
     gbs = reps * nbytes / el / 1e9
     log(f"[bench] cpu oracle: {gbs:.3f} GB/s on {cores} threads ({reps} reps)")
+    # the same route on one thread (bit-identical: rows are independent)
+    reps1, t1 = 0, time.perf_counter()
+    while True:
+        oracle.gemv_fused(oc, decs, enc, x, tables=tabs, nthreads=1)
+        reps1 += 1
+        el1 = time.perf_counter() - t1
+        if el1 > 3.0:
+            break
+    gbs1 = reps1 * nbytes / el1 / 1e9
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": cores, "kind": "oracle",
             "sample": f"fused fp64 GEMV route of the oracle over copy 0 of the q projection "
-                      f"(4096x4096, d={cfg.d}), {reps} repetitions, {el:.1f} s"}
+                      f"(4096x4096, d={cfg.d}), {reps} repetitions, {el:.1f} s",
+            "single_thread_value": round(gbs1, 4), "cpu_model": model,
+            "affinity_cores": len(os.sched_getaffinity(0))}
 
 
 if __name__ == "__main__":
