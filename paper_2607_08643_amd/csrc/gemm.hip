@@ -647,6 +647,348 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Small-M kernel (d = 8, M <= 16): the streaming organisation of the batch-1
+// GEMV with MFMA products. A workgroup of four waves owns a slice of 4 TPW
+// consecutive 64-row x 128-input plane tiles of one 64-row group; a wave
+// takes TPW of them, two in flight, loading each lane's code and gain words
+// straight from the tile (row 16 j + lane % 16, chunks 4 g .. 4 g + 3,
+// g = lane / 16) and its X~ fragments from the prepared activations. Per
+// tile and k-slice q the lane decodes chunk 4 g + q of its four rows into B
+// fragments (fp32 fma chain over fp16 gains and LDS fp16 table entries,
+// rounded to bf16) for v_mfma_f32_16x16x32_bf16 against the 16 tokens. The
+// four wave tiles are added in wave order in LDS; the slices of a row group
+// hand their partials to the last one through flagged 64-bit slots (in-order
+// dispatch makes the wait safe), which adds them in slice order and applies
+// the protected term, LoRA and the store. No barrier inside the tile loop.
+// ---------------------------------------------------------------------------
+// largest padded protected row (bytes) the small-M kernel's finishing
+// workgroup stages in LDS; longer rows are read from global memory
+constexpr int LANE_GEMM_PROT_MAX = 256;
+
+struct LaneGemmArgs {
+    GemmArgs g;
+    int64_t nblk;   // 128-input tiles per row (K steps)
+    int64_t q;      // slices per 64-row group
+    int64_t rgs;    // 64-row groups
+};
+
+template <int S>
+struct LaneTile {
+    uint32_t code[4][S];  // chunks 4 g .. + 3 of row 16 j + lane % 16
+    uint2 gain[4][S];
+    u32x4_t x[4];         // X~ fragments of k-slices 0 .. 3
+};
+
+template <int S>
+__device__ __forceinline__ void lane_gemm_load(LaneTile<S> &T, const GemmArgs &a, int64_t e0, const uint16_t *xrow)
+{
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            const int64_t e = e0 + 256 * j;
+            T.code[j][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
+            T.gain[j][s] = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
+        }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) T.x[q] = *reinterpret_cast<const u32x4_t *>(xrow + 8 * q);
+}
+
+template <int S>
+__device__ __forceinline__ void lane_gemm_tile(const LaneTile<S> &T, const uint16_t *s_tab, f32x4_t (&acc)[4])
+{
+    typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            f16x8_t tv[S];
+#pragma unroll
+            for (int s = 0; s < S; ++s)
+                tv[s] = *reinterpret_cast<const f16x8_t *>(s_tab + (s * 256 + ((T.code[j][s] >> (8 * q)) & 0xffu)) * 8);
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = 0.0f;
+#pragma unroll
+            for (int s = 0; s < S; ++s) {
+                const uint32_t gw = (q < 2) ? T.gain[j][s].x : T.gain[j][s].y;
+                const float gs = f16_bits_to_f32(uint16_t(gw >> (16 * (q & 1))));
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = __builtin_fmaf(gs, float(tv[s][e]), v[e]);
+            }
+            const u32x4_t bq = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                       pack_bf16x2(v[6], v[7])};
+            acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, T.x[q]),
+                                                             __builtin_bit_cast(bf16x8_t, bq), acc[j], 0, 0, 0);
+        }
+    }
+}
+
+template <int S, int TPW>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void gemm_lane_kernel(const LaneGemmArgs la)
+{
+    constexpr int WV = 4, PF = TPW < 2 ? TPW : 2;
+    const GemmArgs &a = la.g;
+    __shared__ __attribute__((aligned(16))) uint4 s_tab_mem[S * 256];  // fp16 tables [S][256][8]
+    __shared__ f32x4_t s_red[WV][4][64];                               // wave tiles; then the output tile
+    // finishing workgroup: its rows' int8 codes [64][kp], the scales [k] and
+    // the protected activations [16][kp32], when kp <= LANE_GEMM_PROT_MAX
+    __shared__ __attribute__((aligned(16))) uint4 s_prot_mem[(64 * LANE_GEMM_PROT_MAX + 4 * LANE_GEMM_PROT_MAX + 32 * LANE_GEMM_PROT_MAX) / 16];
+    uint4 *s_tab4 = s_tab_mem;  // (plain pointers: the LDS DMA builtin takes one)
+    uint4 *s_prot4 = s_prot_mem;
+    const uint16_t *s_tab = reinterpret_cast<const uint16_t *>(s_tab4);
+    const int t = threadIdx.x, lane = t & 63, g = lane >> 4, r16 = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+    const int64_t unit = blockIdx.x, Q = la.q;
+    const int64_t rg = unit / Q, q = unit - rg * Q;
+    const int64_t nb = a.pitch / 16;
+    const int64_t b0 = (q * WV + wave) * TPW;
+    const int64_t nt = ((b0 + TPW < la.nblk) ? b0 + TPW : la.nblk) - b0;  // this wave's tiles (may be <= 0)
+    const int64_t blast = (nt > 0) ? b0 + nt - 1 : 0;                   // a wave without tiles reloads tile 0
+    const bool fin = q == Q - 1;
+
+    // tables by DMA, then the first tiles (unconditional, clamped)
+    for (int v = wave; v < S * 4; v += WV) {
+        const uint4 *src = reinterpret_cast<const uint4 *>(a.tabh[v >> 2]) + (v & 3) * 64 + lane;
+        __builtin_amdgcn_global_load_lds(src, s_tab4 + 64 * v, 16, 0, 0);
+    }
+    // the finishing workgroup's protected-column data: int8 rows and
+    // activations by DMA (rows past d_out clamped: those bytes are never
+    // read), the scales by plain loads once the tiles are requested
+    const int64_t kp = q8_pitch(a.k);
+    const bool prot_lds = fin && a.k > 0 && kp <= LANE_GEMM_PROT_MAX;
+    int8_t *s_q8 = reinterpret_cast<int8_t *>(s_prot4);
+    float *s_sc = reinterpret_cast<float *>(s_prot4 + 4 * LANE_GEMM_PROT_MAX);
+    uint16_t *s_xp = reinterpret_cast<uint16_t *>(s_prot4 + 4 * LANE_GEMM_PROT_MAX + LANE_GEMM_PROT_MAX / 4);
+    if (prot_lds) {
+        const int64_t n0p = rg * 64;
+        const int64_t avail = ((a.d_out - n0p < 64) ? a.d_out - n0p : 64) * kp;  // bytes of real rows
+        const int nq8 = int((64 * kp) / 1024 + ((64 * kp) % 1024 != 0));
+        for (int v = wave; v < nq8; v += WV) {
+            const int64_t e = int64_t(v) * 1024 + 16 * lane;
+            const int64_t es = (e + 16 <= avail) ? e : avail - 16;
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4 *>(a.q8 + n0p * kp + es), s_prot4 + 64 * v, 16, 0, 0);
+        }
+        const int nxp = int((32 * a.kp32) / 1024);  // 16 rows x kp32 bf16, whole KiB (kp32 % 32 == 0)
+        for (int v = wave; v < nxp; v += WV)
+            __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4 *>(a.Xp) + 64 * v + lane,
+                                             s_prot4 + 4 * LANE_GEMM_PROT_MAX + LANE_GEMM_PROT_MAX / 4 + 64 * v, 16, 0, 0);
+    }
+    const int64_t ebase = ((rg * nb) << 10) + (int64_t(r16) << 4) + 4 * g;  // row r16 of the group, chunk 4 g of tile 0
+    const uint16_t *xbase = a.Xt + int64_t(r16) * a.Kp + 32 * g;
+    LaneTile<S> buf[PF];
+    // the scales (one per thread, k <= 256) into a register, stored to LDS
+    // after the tiles; then the first PF tiles. The load of the scale is
+    // unconditional (a valid dummy address where it is not needed) so that
+    // nothing waits for it here. The wait before the barrier leaves all but
+    // the first tile's loads in flight (issue order: DMAs, scale, tiles; LPT
+    // vector loads per tile).
+    constexpr int LPT = 8 * S + 4;
+    const float *scp = prot_lds ? a.scale + ((t < a.k) ? t : a.k - 1) : reinterpret_cast<const float *>(a.Xt);
+    const float scv = *scp;
+#pragma unroll
+    for (int u = 0; u < PF; ++u) {
+        const int64_t b = (b0 + u < blast) ? b0 + u : blast;
+        lane_gemm_load<S>(buf[u], a, ebase + (b << 10), xbase + b * BK);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    wait_vm<(PF - 1) * LPT>();
+    lds_barrier();
+
+    f32x4_t acc[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+        if (u < nt) lane_gemm_tile<S>(buf[u % PF], s_tab, acc);
+        if (u + PF < TPW) {
+            const int64_t b = (b0 + u + PF < blast) ? b0 + u + PF : blast;
+            lane_gemm_load<S>(buf[u % PF], a, ebase + (b << 10), xbase + b * BK);
+        }
+    }
+
+    // the four wave tiles, added in wave order by wave 0
+    if (prot_lds && t < a.k) s_sc[t] = scv;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) s_red[wave][j][lane] = acc[j];
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        acc[j] = s_red[0][j][lane];
+#pragma unroll
+        for (int w = 1; w < WV; ++w) acc[j] = acc[j] + s_red[w][j][lane];
+    }
+
+    bool timed_out = false;
+    if (Q > 1) {
+        uint64_t *slots = a.slots + (rg * (Q - 1)) * 1024 + lane;
+        if (!fin) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    __hip_atomic_store(slots + q * 1024 + (4 * j + r) * 64, (uint64_t(1) << 32) | __float_as_uint(acc[j][r]),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return;
+        }
+        f32x4_t sum[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        // two slices per round trip (the second clamped to the last slice:
+        // a re-read), added in slice order
+        for (int64_t q0 = 0; q0 < Q - 1; q0 += 2) {
+            uint64_t pw[2][16];
+            const int64_t qs[2] = {q0, (q0 + 1 < Q - 1) ? q0 + 1 : Q - 2};
+            for (int spin = 0;; ++spin) {
+                bool ready = true;
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) {
+                        pw[h][e] = __hip_atomic_load(slots + qs[h] * 1024 + e * 64, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        ready &= (pw[h][e] >> 32) != 0;
+                    }
+                if (__all(ready)) break;
+                if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
+                    timed_out = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                if (q0 + h >= Q - 1) break;
+#pragma unroll
+                for (int e = 0; e < 16; ++e) {
+                    sum[e >> 2][e & 3] += __uint_as_float(uint32_t(pw[h][e]));
+                    __hip_atomic_store(slots + (q0 + h) * 1024 + e * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[j] = sum[j] + acc[j];
+    }
+
+    const int64_t n0 = rg * 64;
+    // protected term: X[:, idx] (bf16) times bf16(q8 s), from LDS when staged
+    if (a.k > 0) {
+        for (int64_t qq = 0; qq < a.kp32 / 32; ++qq) {
+            const int64_t p0 = 32 * qq + 8 * g;
+            float sc[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) sc[e] = (p0 + e < a.k) ? (prot_lds ? s_sc[p0 + e] : a.scale[p0 + e]) : 0.0f;
+            const u32x4_t xv = prot_lds ? *reinterpret_cast<const u32x4_t *>(s_xp + int64_t(r16) * a.kp32 + p0)
+                                        : *reinterpret_cast<const u32x4_t *>(a.Xp + int64_t(r16) * a.kp32 + p0);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int64_t row = n0 + 16 * j + r16;
+                uint2 qv = make_uint2(0u, 0u);
+                if (row < a.d_out && p0 < kp)
+                    qv = prot_lds ? *reinterpret_cast<const uint2 *>(s_q8 + (16 * j + r16) * kp + p0)
+                                  : *reinterpret_cast<const uint2 *>(a.q8 + row * kp + p0);
+                float v[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const uint32_t w = (e < 4) ? qv.x : qv.y;
+                    v[e] = float(int8_t(uint8_t(w >> (8 * (e & 3))))) * sc[e];
+                }
+                const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                                           pack_bf16x2(v[6], v[7])};
+                acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv),
+                                                                 __builtin_bit_cast(bf16x8_t, bp), acc[j], 0, 0, 0);
+            }
+        }
+    }
+    // LoRA into the tile (element r of acc[j] is token 4 g + r, row
+    // n0 + 16 j + lane % 16), staged in LDS as fp32 [16][64 + 4], then Y in
+    // 8-output segments (16-byte stores when Y allows)
+    float *s_out = reinterpret_cast<float *>(&s_red[0][0][0]);
+    constexpr int OS = 68;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int64_t n = n0 + 16 * j + r16;
+        const int64_t nc = (n < a.d_out) ? n : a.d_out - 1;
+        float bl[BSQ_MAX_LORA_RANK];
+#pragma unroll
+        for (int qr = 0; qr < BSQ_MAX_LORA_RANK; ++qr) bl[qr] = (qr < a.rank) ? bf16_to_f32(a.B[nc * a.rank + qr]) : 0.0f;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int64_t m = 4 * g + r;
+            float v = timed_out ? __builtin_nanf("") : acc[j][r];
+            if (a.rank > 0) {
+                const float *Tm = a.T + m * BSQ_MAX_LORA_RANK;
+#pragma unroll
+                for (int qr = 0; qr < BSQ_MAX_LORA_RANK; ++qr) v = __builtin_fmaf(bl[qr], Tm[qr], v);
+            }
+            s_out[m * OS + 16 * j + r16] = v;
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // this wave's LDS writes (only wave 0 is left)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int e = h * 64 + lane, m = e >> 3, nl = 8 * (e & 7);  // 16 tokens x 8 segments
+        const int64_t n = n0 + nl;
+        if (m >= a.M || n >= a.d_out) continue;
+        const float4 lo = *reinterpret_cast<const float4 *>(s_out + m * OS + nl);
+        const float4 hi = *reinterpret_cast<const float4 *>(s_out + m * OS + nl + 4);
+        const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        if (a.y_vec && n + 8 <= a.d_out) {
+            if (a.y_bf16) {
+                *reinterpret_cast<u32x4_t *>(static_cast<uint16_t *>(a.Y) + m * a.ldy + n) =
+                    u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+            } else {
+                float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.Y) + m * a.ldy + n);
+                dst[0] = lo;
+                dst[1] = hi;
+            }
+        } else {
+#pragma unroll
+            for (int c = 0; c < 8; ++c) {
+                if (n + c >= a.d_out) break;
+                if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n + c] = f32_to_bf16(v[c]);
+                else static_cast<float *>(a.Y)[m * a.ldy + n + c] = v[c];
+            }
+        }
+    }
+}
+
+// Tiles per wave of the small-M kernel: the largest of 4, 2, 1 whose grid
+// still holds 2048 waves, raised while the slices' partials would not fit in
+// GEMM_SLOT_BYTES (1024 flagged values per slice but the last).
+int lane_gemm_tpw(int64_t rgs, int64_t nblk)
+{
+    auto slices = [&](int tpw) { return (nblk + 4 * tpw - 1) / (4 * tpw); };
+    int tpw = 1;
+    for (int c = 4; c > 1; c >>= 1)
+        if (rgs * slices(c) * 4 >= 2048) {
+            tpw = c;
+            break;
+        }
+    while (tpw < 16 && (slices(tpw) - 1) * rgs * 1024 * 8 > GEMM_SLOT_BYTES) tpw *= 2;
+    return ((slices(tpw) - 1) * rgs * 1024 * 8 > GEMM_SLOT_BYTES) ? 0 : tpw;  // 0: does not fit
+}
+
+template <int S, int TPW>
+hipError_t launch_lane_t(const LaneGemmArgs &la, hipStream_t st)
+{
+    hipLaunchKernelGGL((gemm_lane_kernel<S, TPW>), dim3(unsigned(la.rgs * la.q)), dim3(256), 0, st, la);
+    return hipGetLastError();
+}
+
+template <int S>
+hipError_t launch_lane(const LaneGemmArgs &la, int tpw, hipStream_t st)
+{
+    switch (tpw) {
+    case 1: return launch_lane_t<S, 1>(la, st);
+    case 2: return launch_lane_t<S, 2>(la, st);
+    case 4: return launch_lane_t<S, 4>(la, st);
+    case 8: return launch_lane_t<S, 8>(la, st);
+    default: return launch_lane_t<S, 16>(la, st);
+    }
+}
+
 // Launch shape: token tile and rows per block by M, then the K split, then
 // the workspace layout.
 struct GemmPlan {
@@ -777,6 +1119,23 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     if (e != hipSuccess) return e;
 
     const int S = cfg.stages;
+    if (cfg.d == 8 && M <= 16) {
+        // small M: the streaming kernel, when its slices' partials fit
+        LaneGemmArgs la{};
+        la.g = a;
+        la.nblk = p.ksteps;
+        la.rgs = (L.d_out + 63) / 64;
+        const int tpw = lane_gemm_tpw(la.rgs, la.nblk);
+        if (tpw > 0) {
+            la.q = (la.nblk + 4 * tpw - 1) / (4 * tpw);
+            switch (S) {
+            case 1: return launch_lane<1>(la, tpw, st);
+            case 2: return launch_lane<2>(la, tpw, st);
+            case 3: return launch_lane<3>(la, tpw, st);
+            default: return launch_lane<4>(la, tpw, st);
+            }
+        }
+    }
     if (cfg.d == 8) {
         switch (S) {
         case 1: return launch_gemm_t<8, 1>(a, p, st);

@@ -416,16 +416,19 @@ def test_full_size_encode_and_gemv(case, gpu):
     check_close(y.float().cpu().numpy(), y_ref, 2e-2, name, rss=rss_terms(w_hat, xf, lref))
 
 
+@pytest.mark.parametrize("M", [16, 256])
 @pytest.mark.parametrize("d", [8, 16])
-def test_full_size_gemm_m256(d, gpu):
-    say(f"qwen3-8b o_proj 4096x4096 gemm M=256 d={d}")
+def test_full_size_gemm(d, M, gpu):
+    """Qwen3-8B o_proj shape at the batched sizes of the workload (M = 16 runs
+    the streaming small-M kernel at d = 8, M = 256 the tiled one)."""
+    say(f"qwen3-8b o_proj 4096x4096 gemm M={M} d={d}")
     cfg = bsq.Config(d=d, hidden=d)
     oc = ocfg(cfg)
     decs = decoders(cfg, seed=d)
     W, _ = synth.weight(4096, 4096, seed=77, k_outliers=cfg.k(4096), device=gpu)
     codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
     layer = bsq.bsq_encode(cfg, codec, W)
-    X = synth.activation(4096, seed=8, device=gpu, batch=256)
+    X = synth.activation(4096, seed=8, device=gpu, batch=M)
     A, Bm = synth.lora(4096, 4096, 16, seed=9, device=gpu)
     Y = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.bfloat16)
     torch.cuda.synchronize()
@@ -435,7 +438,7 @@ def test_full_size_gemm_m256(d, gpu):
     w_hat = oracle.decode(oc, decs, enc)
     Xf = oracle.to_f32(X)
     Y_ref = oracle.dense_product(w_hat, Xf, lref)
-    check_close(Y.float().cpu().numpy(), Y_ref, 2e-2, "gemm M=256", rss=rss_terms(w_hat, Xf, lref))
+    check_close(Y.float().cpu().numpy(), Y_ref, 2e-2, f"gemm M={M}", rss=rss_terms(w_hat, Xf, lref))
 
 
 def test_category_batched_stack_encode(gpu):
