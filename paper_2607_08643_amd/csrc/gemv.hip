@@ -397,8 +397,10 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
 // The Q slices of a row group are consecutive workgroups. Slices 0 .. Q-2
 // each publish their 64 partial sums together with a ready flag (one 64-bit
 // agent-scope atomic store per lane, so data and flag are seen together) and
-// are done; the last slice polls those slots, adds them in slice order, then
-// its own sum, clears the slots and applies the int8 and LoRA epilogue.
+// are done; the last slice adds the int8 and LoRA terms to its own sum
+// (work that does not depend on the others, so it overlaps the wait), then
+// polls those slots, adds them in slice order, then its own sum, clears the
+// slots and stores.
 // Workgroups are dispatched in index order, so the slices it waits for are
 // running or done; a bounded poll turns a never-expected stall into NaN
 // outputs instead of a hang. No counter, no cache-wide writeback or
@@ -427,11 +429,11 @@ __device__ __forceinline__ void lane_load(LaneBlk<D, S> &b, const GemvMat &M, in
     }
 }
 
-// The LoRA term (tv = A x) and the store of one output row (row < d_out).
+// The LoRA term (tv = A x) of one output row (row < d_out), added to acc.
 // The rank-16 row of B is loaded unconditionally (indices clamped to the
 // rank) so that its loads are in flight together.
-__device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMat &M, int64_t row, float acc,
-                                                 const float (&tv)[BSQ_MAX_LORA_RANK])
+__device__ __forceinline__ float lane_lora_term(const GemvMat &M, int64_t row, float acc,
+                                                const float (&tv)[BSQ_MAX_LORA_RANK])
 {
     if (M.rank > 0) {
         const uint16_t *br = M.B + row * M.rank;
@@ -444,8 +446,13 @@ __device__ __forceinline__ void lane_finish_lora(const GemvArgs &a, const GemvMa
             acc = (q < M.rank) ? f : acc;
         }
     }
-    if (a.y_bf16) static_cast<uint16_t *>(M.y)[row] = f32_to_bf16(acc);
-    else static_cast<float *>(M.y)[row] = acc;
+    return acc;
+}
+
+__device__ __forceinline__ void lane_store(const GemvArgs &a, const GemvMat &M, int64_t row, float v)
+{
+    if (a.y_bf16) static_cast<uint16_t *>(M.y)[row] = f32_to_bf16(v);
+    else static_cast<float *>(M.y)[row] = v;
 }
 
 // Sixteen protected columns of one row: int8 codes (one 16-byte word) against
@@ -462,14 +469,13 @@ __device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc)
     return acc;
 }
 
-// int8 protected columns, the LoRA term, and the store of one output row,
-// with the row's int8 codes read from global memory: four 16-byte words at a
-// time, all issued before any is used (indices clamped to the padded row,
-// words past it zeroed), then one word after the other.
-__device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M, const float *s_xs, int64_t row,
-                                            float acc, const float (&tv)[BSQ_MAX_LORA_RANK])
+// The int8 protected columns of one row (row < d_out) added to acc, the
+// row's int8 codes read from global memory: four 16-byte words at a time,
+// all issued before any is used (indices clamped to the padded row, words
+// past it zeroed), then one word after the other.
+__device__ __forceinline__ float lane_q8_global(const GemvArgs &a, const GemvMat &M, const float *s_xs, int64_t row,
+                                                float acc)
 {
-    if (row >= M.d_out) return;
     const int64_t nw = q8_pitch(a.k) / 16;  // 16-byte words per row
     const uint4 *qr = reinterpret_cast<const uint4 *>(M.q8 + row * q8_pitch(a.k));
     for (int64_t w0 = 0; w0 < nw; w0 += 4) {
@@ -483,31 +489,33 @@ __device__ __forceinline__ void lane_finish(const GemvArgs &a, const GemvMat &M,
             asm volatile("" : "+v"(acc));  // one word's activations live at a time
         }
     }
-    lane_finish_lora(a, M, row, acc, tv);
+    return acc;
 }
 
-// The epilogue with the int8 rows already in LDS (s_q8 [64][kp], this lane's
-// row at lane * kp), else from global memory.
-__device__ __forceinline__ void lane_finish_lds(const GemvArgs &a, const GemvMat &M, const float *s_xs,
-                                                const int8_t *s_q8, bool q8_lds, int64_t row, float acc,
-                                                const float (&tv)[BSQ_MAX_LORA_RANK])
+// The terms of one row (row < d_out) that do not come from the codes: the
+// int8 protected columns, with the row's codes in LDS (s_q8 [64][kp], this
+// lane's row at lane * kp) or else in global memory, then the LoRA term;
+// added to acc in that order.
+__device__ __forceinline__ float lane_extras(const GemvArgs &a, const GemvMat &M, const float *s_xs,
+                                             const int8_t *s_q8, bool q8_lds, int64_t row, float acc,
+                                             const float (&tv)[BSQ_MAX_LORA_RANK])
 {
-    if (row >= M.d_out) return;
-    if (!q8_lds || a.k == 0) {
-        if (a.k > 0) lane_finish(a, M, s_xs, row, acc, tv);
-        else lane_finish_lora(a, M, row, acc, tv);
-        return;
+    if (a.k > 0) {
+        if (q8_lds) {
+            const int64_t nw = q8_pitch(a.k) / 16;
+            const uint4 *qr = reinterpret_cast<const uint4 *>(s_q8 + (row & 63) * q8_pitch(a.k));
+            int64_t w = 0;
+            for (; w + 2 <= nw; w += 2) {  // two words per step, their LDS reads together
+                const uint4 q0 = qr[w], q1 = qr[w + 1];
+                acc = q8_block(q0, s_xs + 16 * w, acc);
+                acc = q8_block(q1, s_xs + 16 * (w + 1), acc);
+            }
+            if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc);
+        } else {
+            acc = lane_q8_global(a, M, s_xs, row, acc);
+        }
     }
-    const int64_t nw = q8_pitch(a.k) / 16;
-    const uint4 *qr = reinterpret_cast<const uint4 *>(s_q8 + (row & 63) * q8_pitch(a.k));
-    int64_t w = 0;
-    for (; w + 2 <= nw; w += 2) {  // two words per step, their LDS reads together
-        const uint4 q0 = qr[w], q1 = qr[w + 1];
-        acc = q8_block(q0, s_xs + 16 * w, acc);
-        acc = q8_block(q1, s_xs + 16 * (w + 1), acc);
-    }
-    if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc);
-    lane_finish_lora(a, M, row, acc, tv);
+    return lane_lora_term(M, row, acc, tv);
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -905,16 +913,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
 #pragma unroll
     for (int w = 1; w < WV; ++w) v += s_red[w * 64 + lane];
     const int64_t row = rg * 64 + lane;
-    float tv[BSQ_MAX_LORA_RANK];
-    if (Q == 1) {
-        const bool ok = lane_lora_vector(a, M, rg, tv);
-        lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, ok ? v : __builtin_nanf(""), tv);
-        return;
-    }
     uint64_t *slots = a.slots + (M.rg_begin + rg) * (Q - 1) * 64 + lane;
     if (!fin) {
         __hip_atomic_store(slots + q * 64, (uint64_t(1) << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
+        return;
+    }
+    // the finishing slice adds the protected and LoRA terms to its own sum
+    // first: they do not depend on the other slices, so this work overlaps
+    // the wait for them
+    float tv[BSQ_MAX_LORA_RANK];
+    const bool ok = lane_lora_vector(a, M, rg, tv);
+    if (row < M.d_out) v = lane_extras(a, M, s_xs, s_q8, q8_lds, row, v, tv);
+    if (Q == 1) {
+        if (row < M.d_out) lane_store(a, M, row, ok ? v : __builtin_nanf(""));
         return;
     }
     float tot = 0.0f;
@@ -945,8 +957,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     tot += v;
     for (int64_t q0 = 0; q0 < Q - 1; ++q0)
         __hip_atomic_store(slots + q0 * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const bool ok = lane_lora_vector(a, M, rg, tv);
-    lane_finish_lds(a, M, s_xs, s_q8, q8_lds, row, (timed_out || !ok) ? __builtin_nanf("") : tot, tv);
+    if (row < M.d_out) lane_store(a, M, row, (timed_out || !ok) ? __builtin_nanf("") : tot);
 }
 
 // ---------------------------------------------------------------------------
