@@ -15,8 +15,12 @@ rule by brute force, pack/unpack round trip, residual non-increase, closed form
 of the identity decoder, least-squares gains against numpy lstsq, MLP special
 cases that reduce to known maps, Q8 bounds, TopK on planted outliers, binary16
 rounding against numpy, the paper's rate arithmetic, and agreement of the two
-product routes. Trained-codec quality (PPL, accuracy) is parity unpinned: the
-paper publishes no decoder weights.
+product routes. Output-row and coupled MLP protection
+(tests/test_oracle_protection_axes.py): the coupled score on rows and columns
+with exact integer norms, ties, reductions to the single-matrix selections,
+row keys and row Q8 as the column versions of the transpose, and bit-identity
+of the coded rows with the unprotected encoding. Trained-codec quality (PPL,
+accuracy) is parity unpinned: the paper publishes no decoder weights.
 """
 from __future__ import annotations
 
@@ -79,9 +83,15 @@ def lib():
         L.orc_decode.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, P, I32]
         L.orc_gemv_fused.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64,
                                      P, I32, P, P, P, I32]
+        L.orc_topk.argtypes = [P, I64, I64, P]
+        L.orc_row_keys.argtypes = [P, I64, I64, P, P]
+        L.orc_coupled_select.argtypes = [P, P, P, I64, I64, P, P, P, I64, P, P]
+        L.orc_q8_rows.argtypes = [P, I64, I64, P, I64, P, P]
+        L.orc_encode_set.argtypes = [I32, I32, P, P, I64, I64, I32, P, I64, I64, P, P, P, P, I32]
         L.orc_max_threads.restype = I32
         for f in ("orc_decoder_eval", "orc_decoder_table", "orc_protect_select",
-                  "orc_encode", "orc_decode", "orc_gemv_fused"):
+                  "orc_encode", "orc_decode", "orc_gemv_fused", "orc_topk", "orc_coupled_select",
+                  "orc_encode_set"):
             getattr(L, f).restype = I32
         _lib = L
     return _lib
@@ -112,12 +122,18 @@ class Config:
     hidden: int = 8
     protect_num: int = 1
     protect_den: int = 100
+    protect_axis: int = 0   # 0: input columns, 1: output rows
 
     def k(self, d_in: int) -> int:
-        """k = ceil(rho * d_in), rho = num/den, in integer arithmetic."""
+        """k = ceil(rho * n), rho = num/den, in integer arithmetic, for n
+        channels on the protected axis."""
         if self.protect_num == 0:
             return 0
         return (d_in * self.protect_num + self.protect_den - 1) // self.protect_den
+
+    def k_for(self, d_out: int, d_in: int) -> int:
+        """Protected slices of a d_out x d_in matrix on this config's axis."""
+        return self.k(d_out if self.protect_axis == 1 else d_in)
 
 
 def pitch(d_in: int, d: int) -> int:
@@ -130,11 +146,12 @@ class Encoded:
     codes: list          # per stage: uint8/uint16 [d_out, pitch]
     gains: list          # per stage: uint16 (fp16 bits) [d_out, pitch]
     idx: np.ndarray      # int32 [k]
-    q8: np.ndarray       # int8 [d_out, k]
+    q8: np.ndarray       # int8 [d_out, k] (axis 0) or [k, d_in] (axis 1)
     scale: np.ndarray    # fp32 [k]
     pitch: int = 0
     d_out: int = 0
     d_in: int = 0
+    axis: int = 0        # 0: protected input columns, 1: protected output rows
 
 
 def _f32(a) -> np.ndarray:
@@ -180,6 +197,48 @@ def protect_select(w: np.ndarray, k: int, g=None) -> np.ndarray:
     return idx[:k].copy()
 
 
+def topk(key: np.ndarray, k: int) -> np.ndarray:
+    key = np.ascontiguousarray(key, dtype=np.float64)
+    idx = np.zeros(max(k, 1), dtype=np.int32)
+    _check(lib().orc_topk(_p(key), len(key), k, _p(idx)), "topk")
+    return idx[:k].copy()
+
+
+def row_keys(w: np.ndarray, g=None) -> np.ndarray:
+    w = _f32(w)
+    d_out, d_in = w.shape
+    key = np.zeros(d_out, dtype=np.float64)
+    g = None if g is None else _f32(g)
+    lib().orc_row_keys(_p(w), d_out, d_in, _p(g), _p(key))
+    return key
+
+
+def coupled_select(w_gate, w_up, w_down, k: int, g_gate=None, g_up=None, g_down=None):
+    """Coupled MLP intermediate-channel set (eq. mlp_coupled_protection):
+    (idx ascending [k], score fp64 [d_ffn])."""
+    wg, wu, wd = _f32(w_gate), _f32(w_up), _f32(w_down)
+    d_ffn, d_model = wg.shape
+    if wu.shape != (d_ffn, d_model) or wd.shape != (d_model, d_ffn):
+        raise OracleError("coupled_select: shapes")
+    idx = np.zeros(max(k, 1), dtype=np.int32)
+    score = np.zeros(max(d_ffn, 1), dtype=np.float64)
+    gs = [None if v is None else _f32(v) for v in (g_gate, g_up, g_down)]
+    _check(lib().orc_coupled_select(_p(wg), _p(wu), _p(wd), d_model, d_ffn, _p(gs[0]), _p(gs[1]),
+                                    _p(gs[2]), k, _p(idx), _p(score)), "coupled_select")
+    return idx[:k].copy(), score[:d_ffn].copy()
+
+
+def q8_rows(w: np.ndarray, idx: np.ndarray):
+    w = _f32(w)
+    d_out, d_in = w.shape
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    k = len(idx)
+    q = np.zeros((max(k, 1), d_in), dtype=np.int8)
+    s = np.zeros(max(k, 1), dtype=np.float32)
+    lib().orc_q8_rows(_p(w), d_out, d_in, _p(idx), k, _p(q), _p(s))
+    return q[:k].copy(), s[:k].copy()
+
+
 def q8(w: np.ndarray, idx: np.ndarray):
     w = _f32(w)
     d_out, d_in = w.shape
@@ -193,11 +252,16 @@ def q8(w: np.ndarray, idx: np.ndarray):
 
 def encode(cfg: Config, decs, w: np.ndarray, g=None, nthreads: int = 0,
            tables=None) -> Encoded:
-    """Encode one fp32 matrix w [d_out, d_in] (bf16 inputs: convert exactly first)."""
+    """Encode one fp32 matrix w [d_out, d_in] (bf16 inputs: convert exactly first).
+    With protect_axis = 1 the protected slices are the output rows of largest
+    energy (row_keys, g per output row), encoded by encode_set."""
     w = _f32(w)
     d_out, d_in = w.shape
     if d_in % cfg.d:
         raise OracleError("d_in must be a multiple of d")
+    if cfg.protect_axis == 1:
+        idx = topk(row_keys(w, g), cfg.k(d_out))
+        return encode_set(cfg, decs, w, idx, nthreads=nthreads, tables=tables)
     P = pitch(d_in, cfg.d)
     k = cfg.k(d_in)
     tables = tables or decoder_table(cfg, decs)
@@ -215,9 +279,46 @@ def encode(cfg: Config, decs, w: np.ndarray, g=None, nthreads: int = 0,
                    P, d_out, d_in)
 
 
+def encode_set(cfg: Config, decs, w: np.ndarray, idx, nthreads: int = 0, tables=None) -> Encoded:
+    """Encode with a given protected set on cfg.protect_axis (orc_encode_set)."""
+    w = _f32(w)
+    d_out, d_in = w.shape
+    if d_in % cfg.d:
+        raise OracleError("d_in must be a multiple of d")
+    axis = cfg.protect_axis
+    P = pitch(d_in, cfg.d)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    k = len(idx)
+    tables = tables or decoder_table(cfg, decs)
+    ctype = np.uint8 if cfg.d <= 8 else np.uint16
+    codes = [np.zeros((d_out, P), dtype=ctype) for _ in range(cfg.stages)]
+    gains = [np.zeros((d_out, P), dtype=np.uint16) for _ in range(cfg.stages)]
+    qshape = (max(k, 1), d_in) if axis == 1 else (d_out, max(k, 1))
+    q = np.zeros(qshape, dtype=np.int8)
+    s = np.zeros(max(k, 1), dtype=np.float32)
+    idx_arg = idx if k else np.zeros(1, np.int32)
+    rc = lib().orc_encode_set(cfg.d, cfg.stages, _ptr_array(tables), _p(w), d_out, d_in, axis,
+                              _p(idx_arg), k, P, _ptr_array(codes), _ptr_array(gains), _p(q), _p(s),
+                              nthreads)
+    _check(rc, "encode_set")
+    q = q[:k] if axis == 1 else q[:, :k]
+    return Encoded(codes, gains, idx.copy(), np.ascontiguousarray(q), s[:k].copy(), P, d_out, d_in, axis)
+
+
 def decode(cfg: Config, decs, enc: Encoded, nthreads: int = 0, tables=None) -> np.ndarray:
+    """W_hat (eq. parallel_stage_decode, eq. protected_8bit_scatter). Row
+    protection: the stage sum of the coded rows, then each protected row is
+    q8[p, :] * scale_p (fp32 products)."""
     tables = tables or decoder_table(cfg, decs)
     w_hat = np.zeros((enc.d_out, enc.d_in), dtype=np.float32)
+    if enc.axis == 1:
+        rc = lib().orc_decode(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
+                              _ptr_array(enc.codes), _ptr_array(enc.gains), None, None, None, 0,
+                              _p(w_hat), nthreads)
+        _check(rc, "decode")
+        for p, i in enumerate(enc.idx):
+            w_hat[i, :] = enc.q8[p].astype(np.float32) * np.float32(enc.scale[p])
+        return w_hat
     k = len(enc.idx)
     idx = enc.idx if k else np.zeros(1, np.int32)
     q = enc.q8 if k else np.zeros((enc.d_out, 1), np.int8)
@@ -231,9 +332,23 @@ def decode(cfg: Config, decs, enc: Encoded, nthreads: int = 0, tables=None) -> n
 
 def gemv_fused(cfg: Config, decs, enc: Encoded, x, lora=None, nthreads: int = 0,
                tables=None) -> np.ndarray:
-    """Fused route in fp64 (never forms W_hat)."""
+    """Fused route in fp64 (never forms W_hat). Row protection: the coded
+    rows by the C route with no protected column, then each protected row as
+    scale_p * <q8[p, :], x> + B (A x)."""
     tables = tables or decoder_table(cfg, decs)
     x64 = np.ascontiguousarray(x, dtype=np.float64)
+    if enc.axis == 1:
+        plain = Encoded(enc.codes, enc.gains, np.zeros(0, np.int32), np.zeros((enc.d_out, 0), np.int8),
+                        np.zeros(0, np.float32), enc.pitch, enc.d_out, enc.d_in, 0)
+        y = gemv_fused(cfg, decs, plain, x64, lora, nthreads, tables)
+        for p, i in enumerate(enc.idx):
+            acc = float(enc.scale[p]) * float(np.dot(enc.q8[p].astype(np.float64), x64))
+            if lora is not None:
+                A64 = np.asarray(lora[0], dtype=np.float64)
+                B64 = np.asarray(lora[1], dtype=np.float64)
+                acc += float(B64[i] @ (A64 @ x64))
+            y[i] = acc
+        return y
     y = np.zeros(enc.d_out, dtype=np.float64)
     k = len(enc.idx)
     idx = enc.idx if k else np.zeros(1, np.int32)
@@ -288,12 +403,16 @@ def sizes(cfg: Config, d_out: int, d_in: int, lora_rank: int = 0) -> dict:
     a model counts them once per category, since every layer of a category
     shares its decoders)."""
     C = d_in // cfg.d
-    k = cfg.k(d_in)
-    s_code = cfg.stages * d_out * C * cfg.b / 8
+    k = cfg.k_for(d_out, d_in)
+    # row protection: the protected rows carry no BSQ codes or gains (their
+    # all-zero rows in the planes are layout, not payload), and each holds
+    # d_in int8 values
+    coded_rows = d_out - k if cfg.protect_axis == 1 else d_out
+    s_code = cfg.stages * coded_rows * C * cfg.b / 8
     s_dec = cfg.stages * decoder_param_count(cfg) * 4
-    s_8bit = d_out * k
+    s_8bit = k * d_in if cfg.protect_axis == 1 else d_out * k
     s_lora = 2 * lora_rank * (d_in + d_out)
-    s_meta = cfg.stages * d_out * C * 2 + 4 * k + 4 * k
+    s_meta = cfg.stages * coded_rows * C * 2 + 4 * k + 4 * k
     tot = s_code + s_dec + s_8bit + s_lora + s_meta
     return dict(S_code=s_code, S_dec=s_dec, S_8bit=s_8bit, S_LoRA=s_lora, S_meta=s_meta,
                 S_tot=tot, chunks=d_out * C, k=k,

@@ -195,25 +195,89 @@ static int cmp_i32_asc(const void *pa, const void *pb)
     return (a > b) - (a < b);
 }
 
-/* P = TopK_j(key, k): the k largest keys, equal keys -> lower column first;
- * returned in ascending column order. Not thread-safe (qsort comparator
- * state); the oracle calls it from one thread. */
+/* TopK over given keys: the k largest of key[0 .. n-1], equal keys -> lower
+ * index first; returned in ascending index order. Not thread-safe (qsort
+ * comparator state); the oracle calls it from one thread. */
+int orc_topk(const double *key, int64_t n, int64_t k, int32_t *idx)
+{
+    if (k < 0 || k > n) return ORC_ERR_ARG;
+    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!order) return ORC_ERR_ARG;
+    for (int64_t j = 0; j < n; ++j) order[j] = j;
+    g_sort_keys = key;
+    qsort(order, (size_t)n, sizeof(int64_t), cmp_key_desc_index_asc);
+    for (int64_t p = 0; p < k; ++p) idx[p] = (int32_t)order[p];
+    qsort(idx, (size_t)k, sizeof(int32_t), cmp_i32_asc);
+    free(order);
+    return ORC_OK;
+}
+
+/* P = TopK_j(key, k) over the column keys. */
 int orc_protect_select(const float *w, int64_t d_out, int64_t d_in, const float *g,
                        int64_t k, int32_t *idx, double *key_out)
 {
     if (k < 0 || k > d_in) return ORC_ERR_ARG;
-    double *key = key_out ? key_out : (double *)malloc(sizeof(double) * (size_t)d_in);
-    int64_t *order = (int64_t *)malloc(sizeof(int64_t) * (size_t)(d_in > 0 ? d_in : 1));
-    if (!key || !order) return ORC_ERR_ARG;
+    double *key = key_out ? key_out : (double *)malloc(sizeof(double) * (size_t)(d_in > 0 ? d_in : 1));
+    if (!key) return ORC_ERR_ARG;
     orc_column_keys(w, d_out, d_in, g, key);
-    for (int64_t j = 0; j < d_in; ++j) order[j] = j;
-    g_sort_keys = key;
-    qsort(order, (size_t)d_in, sizeof(int64_t), cmp_key_desc_index_asc);
-    for (int64_t p = 0; p < k; ++p) idx[p] = (int32_t)order[p];
-    qsort(idx, (size_t)k, sizeof(int32_t), cmp_i32_asc);
-    free(order);
+    int rc = orc_topk(key, d_in, k, idx);
     if (!key_out) free(key);
-    return ORC_OK;
+    return rc;
+}
+
+/* Output-channel energy key_i = g_i^2 * sum_j w_ij^2 in fp64, columns summed
+ * in order j = 0 .. d_in-1; g (one value per output row) defaults to 1. This
+ * is the score of eq. protected_channel_selection applied to rows, the
+ * output-channel axis of the protection-axis ablation (Section IV-D). */
+void orc_row_keys(const float *w, int64_t d_out, int64_t d_in, const float *g, double *key)
+{
+    for (int64_t i = 0; i < d_out; ++i) {
+        double s = 0.0;
+        for (int64_t j = 0; j < d_in; ++j) {
+            double v = (double)w[i * d_in + j];
+            s = s + v * v;
+        }
+        if (g) {
+            double gi = (double)g[i];
+            s = (gi * gi) * s;
+        }
+        key[i] = s;
+    }
+}
+
+/* Coupled MLP intermediate-channel score (eq. mlp_coupled_protection). For
+ * gate and up ([d_ffn][d_model]) channel j is output row j; for down
+ * ([d_model][d_ffn]) it is input column j:
+ *   S_j = |g^gate_j| ||W_gate[j, :]|| + |g^up_j| ||W_up[j, :]|| + |g^down_j| ||W_down[:, j]||
+ * Each squared norm is an fp64 sum in element order, the norm its correctly
+ * rounded fp64 square root, and the three terms are added left to right. The
+ * statistics g are magnitudes (absolute value taken); NULL means ones.
+ * P = TopK_j(S, k) as orc_topk. score (may be NULL) receives S. */
+int orc_coupled_select(const float *wg, const float *wu, const float *wd, int64_t d_model, int64_t d_ffn,
+                       const float *gg, const float *gu, const float *gd, int64_t k, int32_t *idx,
+                       double *score_out)
+{
+    if (k < 0 || k > d_ffn || d_model < 0) return ORC_ERR_ARG;
+    size_t n = (size_t)(d_ffn > 0 ? d_ffn : 1);
+    double *sg = (double *)malloc(sizeof(double) * n), *su = (double *)malloc(sizeof(double) * n);
+    double *sd = (double *)malloc(sizeof(double) * n);
+    double *score = score_out ? score_out : (double *)malloc(sizeof(double) * n);
+    if (!sg || !su || !sd || !score) return ORC_ERR_ARG;
+    orc_row_keys(wg, d_ffn, d_model, NULL, sg);
+    orc_row_keys(wu, d_ffn, d_model, NULL, su);
+    orc_column_keys(wd, d_model, d_ffn, NULL, sd);
+    for (int64_t j = 0; j < d_ffn; ++j) {
+        double a = gg ? fabs((double)gg[j]) : 1.0;
+        double b = gu ? fabs((double)gu[j]) : 1.0;
+        double c = gd ? fabs((double)gd[j]) : 1.0;
+        score[j] = (a * sqrt(sg[j]) + b * sqrt(su[j])) + c * sqrt(sd[j]);
+    }
+    int rc = orc_topk(score, d_ffn, k, idx);
+    free(sg);
+    free(su);
+    free(sd);
+    if (!score_out) free(score);
+    return rc;
 }
 
 /* Q8 of the protected columns (eq. protected_8bit_scatter; reading: symmetric
@@ -246,6 +310,37 @@ void orc_q8(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int
     }
 }
 
+/* Q8 of protected output rows (eq. protected_8bit_scatter with row slices;
+ * reading: symmetric int8, one fp32 scale per protected row):
+ *   m_p = max_j |w[idx_p][j]|;  s_p = m_p / 127;
+ *   q8[p * d_in + j] = clamp(round_half_even(w[idx_p][j] / s_p), -127, 127),
+ *   and q = 0 when s_p = 0. */
+void orc_q8_rows(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int64_t k,
+                 int8_t *q8, float *scale)
+{
+    (void)d_out;
+    for (int64_t p = 0; p < k; ++p) {
+        const float *row = w + (int64_t)idx[p] * d_in;
+        float m = 0.0f;
+        for (int64_t j = 0; j < d_in; ++j) {
+            float a = fabsf(row[j]);
+            if (a > m) m = a;
+        }
+        float s = m / 127.0f;
+        scale[p] = s;
+        for (int64_t j = 0; j < d_in; ++j) {
+            int8_t q = 0;
+            if (s != 0.0f) {
+                float t = nearbyintf(row[j] / s);
+                if (t > 127.0f) t = 127.0f;
+                if (t < -127.0f) t = -127.0f;
+                q = (int8_t)t;
+            }
+            q8[p * d_in + j] = q;
+        }
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Encoder: sphere map + sign code + residual stage (Sections III-C, III-D). */
 /* ------------------------------------------------------------------------ */
@@ -273,37 +368,24 @@ void orc_q8(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int
  *   idx[k] ascending protected columns, q8[d_out][k], scale[k].
  *
  * tables[s] is the decoder table of stage s (orc_decoder_table). */
-int orc_encode(int d, int stages, const float *const *tables,
-               const float *w, int64_t d_out, int64_t d_in, const float *g,
-               int64_t k, int64_t pitch,
-               void *const *codes, uint16_t *const *gains,
-               int32_t *idx, int8_t *q8, float *scale, int nthreads)
+/* The per-chunk stages of every row i with skip[i] == 0 (skip may be NULL);
+ * positions j with prot[j] != 0 are masked out of BSQ. Rows with skip[i] set
+ * and padding chunks get code 0 and gain +0. */
+static void encode_rows(int d, int stages, const float *const *tables, const float *w, int64_t d_out,
+                        int64_t d_in, int64_t pitch, const unsigned char *prot, const unsigned char *skip,
+                        void *const *codes, uint16_t *const *gains, int nthreads)
 {
-    if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
-    if (d_in % d != 0 || k < 0 || k > d_in) return ORC_ERR_ARG;
     int64_t C = d_in / d;
-    if (pitch < C) return ORC_ERR_ARG;
-    for (int64_t t = 0; t < d_out * d_in; ++t)
-        if (!isfinite(w[t])) return ORC_ERR_NONFINITE;
-
-    /* protected set, Q8 payload and the complement mask */
-    unsigned char *prot = (unsigned char *)calloc((size_t)(d_in > 0 ? d_in : 1), 1);
-    if (!prot) return ORC_ERR_ARG;
-    if (k > 0) {
-        int rc = orc_protect_select(w, d_out, d_in, g, k, idx, NULL);
-        if (rc) { free(prot); return rc; }
-        orc_q8(w, d_out, d_in, idx, k, q8, scale);
-        for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
-    }
-
 #ifdef _OPENMP
     if (nthreads > 0) omp_set_num_threads(nthreads);
 #pragma omp parallel for schedule(dynamic, 16)
+#else
+    (void)nthreads;
 #endif
     for (int64_t i = 0; i < d_out; ++i) {
         float r[MAX_CODE_BITS];
         for (int64_t c = 0; c < pitch; ++c) {
-            if (c >= C) {
+            if (c >= C || (skip && skip[i])) {
                 for (int s = 0; s < stages; ++s) {
                     if (d <= 8) ((uint8_t *)codes[s])[i * pitch + c] = 0;
                     else ((uint16_t *)codes[s])[i * pitch + c] = 0;
@@ -340,7 +422,74 @@ int orc_encode(int d, int stages, const float *const *tables,
             }
         }
     }
+}
+
+int orc_encode(int d, int stages, const float *const *tables,
+               const float *w, int64_t d_out, int64_t d_in, const float *g,
+               int64_t k, int64_t pitch,
+               void *const *codes, uint16_t *const *gains,
+               int32_t *idx, int8_t *q8, float *scale, int nthreads)
+{
+    if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    if (d_in % d != 0 || k < 0 || k > d_in) return ORC_ERR_ARG;
+    int64_t C = d_in / d;
+    if (pitch < C) return ORC_ERR_ARG;
+    for (int64_t t = 0; t < d_out * d_in; ++t)
+        if (!isfinite(w[t])) return ORC_ERR_NONFINITE;
+
+    /* protected set, Q8 payload and the complement mask */
+    unsigned char *prot = (unsigned char *)calloc((size_t)(d_in > 0 ? d_in : 1), 1);
+    if (!prot) return ORC_ERR_ARG;
+    if (k > 0) {
+        int rc = orc_protect_select(w, d_out, d_in, g, k, idx, NULL);
+        if (rc) { free(prot); return rc; }
+        orc_q8(w, d_out, d_in, idx, k, q8, scale);
+        for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
+    }
+    encode_rows(d, stages, tables, w, d_out, d_in, pitch, prot, NULL, codes, gains, nthreads);
     free(prot);
+    return ORC_OK;
+}
+
+/* Encode with a given protected set idx[k] (strictly ascending, in range;
+ * ORC_ERR_ARG otherwise):
+ *   axis 0 (input columns): Q8 of those columns (orc_q8, q8 [d_out][k]) and
+ *          BSQ on the rest of every row, exactly as orc_encode does after its
+ *          own selection;
+ *   axis 1 (output rows): Q8 of those rows (orc_q8_rows, q8 [k][d_in]); BSQ
+ *          on every other row with no position masked (the complement of a
+ *          row slice is whole rows); the protected rows are not BSQ-coded and
+ *          keep code 0 and gain +0 in the planes.
+ * This is how the coupled MLP set of eq. mlp_coupled_protection reaches the
+ * three matrices: rows of gate and up, columns of down. */
+int orc_encode_set(int d, int stages, const float *const *tables,
+                   const float *w, int64_t d_out, int64_t d_in, int axis,
+                   const int32_t *idx, int64_t k, int64_t pitch,
+                   void *const *codes, uint16_t *const *gains,
+                   int8_t *q8, float *scale, int nthreads)
+{
+    if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    if (axis != 0 && axis != 1) return ORC_ERR_ARG;
+    int64_t n = axis ? d_out : d_in;
+    if (d_in % d != 0 || k < 0 || k > n) return ORC_ERR_ARG;
+    if (pitch < d_in / d) return ORC_ERR_ARG;
+    for (int64_t p = 0; p < k; ++p)
+        if (idx[p] < 0 || idx[p] >= n || (p > 0 && idx[p] <= idx[p - 1])) return ORC_ERR_ARG;
+    for (int64_t t = 0; t < d_out * d_in; ++t)
+        if (!isfinite(w[t])) return ORC_ERR_NONFINITE;
+    unsigned char *prot = (unsigned char *)calloc((size_t)(d_in > 0 ? d_in : 1), 1);
+    unsigned char *skip = (unsigned char *)calloc((size_t)(d_out > 0 ? d_out : 1), 1);
+    if (!prot || !skip) { free(prot); free(skip); return ORC_ERR_ARG; }
+    if (axis == 0) {
+        orc_q8(w, d_out, d_in, idx, k, q8, scale);
+        for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
+    } else {
+        orc_q8_rows(w, d_out, d_in, idx, k, q8, scale);
+        for (int64_t p = 0; p < k; ++p) skip[idx[p]] = 1;
+    }
+    encode_rows(d, stages, tables, w, d_out, d_in, pitch, prot, skip, codes, gains, nthreads);
+    free(prot);
+    free(skip);
     return ORC_OK;
 }
 
