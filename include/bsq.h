@@ -44,6 +44,18 @@
  *              activations with one scalar load per 128 columns.
  * A stack of n_mats matrices of one shape stores these arrays back to back,
  * matrix-major ([n_mats][...]).
+ *
+ * With protect_axis = 1 (protected output rows, the output-channel axis of
+ * the protection-axis ablation in Section IV-D, and the gate/up side of
+ * eq. mlp_coupled_protection) the protected slices are k whole rows:
+ *   prot_idx   int32 [k], the protected rows in ascending order;
+ *   prot_q8    int8  [k][q8_pitch(d_in)], q8_pitch(n) = roundup(n, 16):
+ *              row p holds the symmetric int8 codes of row prot_idx[p], then
+ *              zero bytes;
+ *   prot_scale fp32  [k], one scale per protected row;
+ *   prot_bits  unused (may be NULL);
+ * and the protected rows are not BSQ-coded: their code and gain planes hold
+ * code 0 and gain +0. k = ceil(rho * d_out) for this axis.
  */
 #ifndef BSQ_H
 #define BSQ_H
@@ -55,7 +67,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 3
+#define BSQ_ABI_VERSION 4
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -88,7 +100,9 @@ typedef struct {
     int32_t dec_kind;    /* bsq_dec_kind */
     int32_t hidden;      /* MLP hidden width h, 1..64; ignored for other kinds */
     int32_t protect_num; /* protected-channel ratio rho = num/den (eq. protected_channel_selection); */
-    int32_t protect_den; /*   num = 0 disables the protected path; k = ceil(d_in*num/den) */
+    int32_t protect_den; /*   num = 0 disables the protected path; k = ceil(n*num/den) for the n */
+                         /*   channels of the protected axis (d_in for columns, d_out for rows) */
+    int32_t protect_axis; /* 0: protected input columns; 1: protected output rows */
 } bsq_config;
 
 /* Parameters of one stage's decoder, fp32, row-major, device pointers.
@@ -146,8 +160,9 @@ typedef struct {
     double bpw_real;            /* 8 * S_tot / (d_out * d_in) */
 } bsq_sizes;
 
-/* Operations for bsq_workspace_bytes. */
-typedef enum { BSQ_OP_ENCODE = 0, BSQ_OP_GEMV = 1, BSQ_OP_GEMM = 2 } bsq_op;
+/* Operations for bsq_workspace_bytes. BSQ_OP_SELECT is bsq_coupled_select,
+ * with d_out = d_ffn and d_in = d_model. */
+typedef enum { BSQ_OP_ENCODE = 0, BSQ_OP_GEMV = 1, BSQ_OP_GEMM = 2, BSQ_OP_SELECT = 3 } bsq_op;
 
 /* ---------------------------------------------------------------------- */
 
@@ -199,6 +214,9 @@ bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec,
  * order). The outputs are bit-identical to the definition.
  *   W      device, bf16 or fp32, [n_mats][d_out][d_in] row-major, 16-byte aligned
  *   g      device fp32 [n_mats][d_in] activation statistic, or NULL for ones
+ *          (protect_axis = 1: the rows are scored instead, key_i = g_i^2
+ *          sum_j W_ij^2 with columns in order and g [n_mats][d_out]; the
+ *          protected rows are then encoded as by bsq_encode_with_set)
  *   out    host struct of device output buffers sized by bsq_layer_sizes
  *          (times n_mats); out->d_out/d_in/pitch/k/n_mats must match
  *   err    device int32 error word; the caller zeroes it before the call; the
@@ -209,9 +227,50 @@ bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, i
                       const bsq_layer *out, int32_t *err, void *ws, size_t ws_bytes,
                       void *stream);
 
+/* Encode with a given protected set (no selection): as bsq_encode, except that
+ * the k slices on cfg->protect_axis are idx (device int32 [n_mats][k], each
+ * matrix's entries strictly ascending and in [0, n) for the axis length n;
+ * it may alias out->prot_idx). Column axis: int8 quantisation of those
+ * columns and BSQ on the rest of every row. Row axis: int8 quantisation of
+ * those rows (one scale per row, the absmax over the row / 127); BSQ on the
+ * other rows with no position masked; the protected rows get code 0 and gain
+ * +0. An invalid set ORs 2 into *err (and the outputs are unspecified); NaN
+ * or Inf in W ORs 1. This is how the coupled set of bsq_coupled_select is
+ * applied to the gate and up rows (axis 1) and the down columns (axis 0).
+ * `g` is not used. Other arguments as for bsq_encode. */
+bsq_status bsq_encode_with_set(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype,
+                               int64_t n_mats, int64_t d_out, int64_t d_in, const int32_t *idx,
+                               const bsq_layer *out, int32_t *err, void *ws, size_t ws_bytes,
+                               void *stream);
+
+/* Coupled MLP intermediate-channel selection (eq. mlp_coupled_protection):
+ * for channel j < d_ffn,
+ *   S_j = |g_gate_j| ||W_gate[j, :]|| + |g_up_j| ||W_up[j, :]|| + |g_down_j| ||W_down[:, j]||
+ * with each squared norm an fp64 sum in element order (columns for the gate
+ * and up rows, rows for the down column), the norm its correctly rounded fp64
+ * square root and the three terms added left to right; then the k =
+ * ceil(rho * d_ffn) largest, ties to the lower channel, ascending. Results
+ * are bit-identical to that definition.
+ *   W_gate, W_up  device [d_ffn][d_model], W_down device [d_model][d_ffn],
+ *                 all bf16 or all fp32 (w_dtype), 16-byte aligned
+ *   g_*           device fp32 [d_ffn] activation statistics, or NULL for ones
+ *                 (taken by magnitude)
+ *   idx           device int32 [k] output
+ *   scores        device fp64 [d_ffn] output of S, or NULL
+ *   err           device int32 error word (caller zeroes it); ORs 1 on NaN
+ *                 or Inf in a weight
+ *   ws            device workspace of bsq_workspace_bytes(SELECT, 1, d_ffn,
+ *                 d_model) bytes, 256-byte aligned
+ * protect_axis is ignored. */
+bsq_status bsq_coupled_select(const bsq_config *cfg, const void *W_gate, const void *W_up, const void *W_down,
+                              int32_t w_dtype, int64_t d_model, int64_t d_ffn, const float *g_gate,
+                              const float *g_up, const float *g_down, int32_t *idx, double *scores,
+                              int32_t *err, void *ws, size_t ws_bytes, void *stream);
+
 /* Decode (eq. parallel_stage_decode, eq. protected_8bit_scatter):
  * W_hat[i][j] = sum_s gain_s * D_s(code_s)[j] as an fmaf chain over the stages
- * in fp32, then W_hat[:, idx_p] = q8[:, p] * scale_p. Bit-identical to the
+ * in fp32, then W_hat[:, idx_p] = q8[:, p] * scale_p (protect_axis = 1:
+ * W_hat[idx_p, :] = q8[p, :] * scale_p). Bit-identical to the
  * definition for BSQ_F32 output; BSQ_BF16 rounds that value to nearest even.
  *   W_hat  device [n_mats][d_out][d_in] of out_dtype, 16-byte aligned */
 bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
@@ -239,7 +298,10 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
  *           and d_out it was sized for); calls that share a workspace must
  *           not overlap.
  * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
- * fp32 decoder table and fp32 arithmetic throughout.
+ * fp32 decoder table and fp32 arithmetic throughout. With protect_axis = 1
+ * the coded rows come from the streaming kernels and each protected row is
+ * written afterwards as scale_p <q8[p, :], x> + B[row] (A x), one wave per
+ * row (same stream).
  * bsq_gemv = bsq_gemv_prepare followed by bsq_gemv_run on the same stream. */
 bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
                     const bsq_layer *layers, const bsq_lora *loras,
@@ -287,7 +349,9 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  *      One workspace serves GEMM calls of any shape; it must not be shared
  *      with a GEMV workspace, and calls that share it must not overlap.
  * The K steps of a tile may be split over several blocks; their fp32
- * partials are summed in a fixed order, so results are deterministic. */
+ * partials are summed in a fixed order, so results are deterministic. With
+ * protect_axis = 1 each protected row's column of Y is written afterwards as
+ * scale_p X q8[p, :]^T + (X A^T) B[row]^T (same stream). */
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
                     const bsq_lora *lora, const void *X, int32_t x_dtype, int64_t M,
                     int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,

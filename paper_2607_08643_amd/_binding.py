@@ -27,7 +27,7 @@ BSQ_OK, BSQ_ERR_ARG, BSQ_ERR_SHAPE, BSQ_ERR_DTYPE, BSQ_ERR_ALIGN = 0, 1, 2, 3, 4
 BSQ_ERR_BUFFER_TOO_SMALL, BSQ_ERR_NONFINITE, BSQ_ERR_DEVICE, BSQ_ERR_UNSUPPORTED = 5, 6, 7, 8
 BSQ_F32, BSQ_BF16 = 0, 1
 DEC_IDENTITY, DEC_LINEAR, DEC_MLP = 0, 1, 2
-OP_ENCODE, OP_GEMV, OP_GEMM = 0, 1, 2
+OP_ENCODE, OP_GEMV, OP_GEMM, OP_SELECT = 0, 1, 2, 3
 
 
 class BsqError(RuntimeError):
@@ -39,7 +39,8 @@ class BsqError(RuntimeError):
 # ---------------------------------------------------------------- C structs
 class bsq_config(ct.Structure):
     _fields_ = [("d", ct.c_int32), ("b", ct.c_int32), ("stages", ct.c_int32), ("dec_kind", ct.c_int32),
-                ("hidden", ct.c_int32), ("protect_num", ct.c_int32), ("protect_den", ct.c_int32)]
+                ("hidden", ct.c_int32), ("protect_num", ct.c_int32), ("protect_den", ct.c_int32),
+                ("protect_axis", ct.c_int32)]
 
 
 class bsq_decoder(ct.Structure):
@@ -70,10 +71,10 @@ class bsq_sizes(ct.Structure):
 
 EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes", "bsq_workspace_bytes",
            "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemv_prepare",
-           "bsq_gemv_run", "bsq_gemm")
+           "bsq_gemv_run", "bsq_gemm", "bsq_encode_with_set", "bsq_coupled_select")
 
 # struct layouts above follow this version of include/bsq.h
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 _lib = None
 
@@ -102,6 +103,8 @@ def lib():
     L.bsq_gemv_prepare.argtypes = [P, I32, P, P, P, P, I32, P, SZ, P]
     L.bsq_gemv_run.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
     L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P]
+    L.bsq_encode_with_set.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
+    L.bsq_coupled_select.argtypes = [P, P, P, P, I32, I64, I64, P, P, P, P, P, P, P, SZ, P]
     for f in EXPORTS[2:]:
         getattr(L, f).restype = I32
     if L.bsq_version() != ABI_VERSION:
@@ -149,6 +152,7 @@ class Config:
     hidden: int = 8
     protect_num: int = 1
     protect_den: int = 100
+    protect_axis: int = 0   # 0: protected input columns, 1: protected output rows
 
     @property
     def b(self) -> int:
@@ -156,12 +160,17 @@ class Config:
 
     def c(self) -> bsq_config:
         return bsq_config(self.d, self.b, self.stages, self.kind, self.hidden, self.protect_num,
-                          self.protect_den)
+                          self.protect_den, self.protect_axis)
 
-    def k(self, d_in: int) -> int:
+    def k(self, n: int) -> int:
+        """ceil(rho * n): protected channels among n."""
         if self.protect_num == 0:
             return 0
-        return (d_in * self.protect_num + self.protect_den - 1) // self.protect_den
+        return (n * self.protect_num + self.protect_den - 1) // self.protect_den
+
+    def k_for(self, d_out: int, d_in: int) -> int:
+        """Protected slices of a d_out x d_in matrix on this config's axis."""
+        return self.k(d_out if self.protect_axis == 1 else d_in)
 
     def pitch(self, d_in: int) -> int:
         C = d_in // self.d
@@ -261,7 +270,7 @@ class Layer:
 
     @property
     def k(self) -> int:
-        return self.cfg.k(self.d_in)
+        return self.cfg.k_for(self.d_out, self.d_in)
 
     def c(self) -> bsq_layer:
         L = bsq_layer()
@@ -303,7 +312,9 @@ class Layer:
         the d_out real rows, the int8 payload, scales, indices and bitmap."""
         per_row = self.pitch * (self.codes[0].element_size() + 2) * self.cfg.stages
         n = per_row * self.d_out
-        if self.k:
+        if self.k and self.cfg.protect_axis == 1:
+            n += self.q8.numel() + self.scale.numel() * 4 + self.idx.numel() * 4
+        elif self.k:
             n += self.d_out * self.k + self.scale.numel() * 4 + self.idx.numel() * 4
             if self.bits is not None:
                 n += self.bits.numel() * 4
@@ -312,8 +323,9 @@ class Layer:
 
 def layer_empty(cfg: Config, d_out: int, d_in: int, n_mats: int = 1, device="cuda") -> Layer:
     """Planes in the tiled layout [n_mats][ceil(d_out/64)][pitch/16][64][16];
-    the int8 payload as [n_mats][d_out][roundup(k, 16)]."""
-    P, k = cfg.pitch(d_in), cfg.k(d_in)
+    the int8 payload as [n_mats][d_out][roundup(k, 16)] (protected rows:
+    [n_mats][k][roundup(d_in, 16)], and no bitmap)."""
+    P, k = cfg.pitch(d_in), cfg.k_for(d_out, d_in)
     ct_ = torch.uint8 if cfg.d <= 8 else torch.int16
     tiles = ((d_out + 63) // 64, P // 16, 64, 16)
     shape = ((n_mats,) + tiles) if n_mats > 1 else tiles
@@ -323,9 +335,12 @@ def layer_empty(cfg: Config, d_out: int, d_in: int, n_mats: int = 1, device="cud
     if k > 0:
         lead = (n_mats,) if n_mats > 1 else ()
         idx = torch.empty(lead + (k,), dtype=torch.int32, device=device)
-        q8 = torch.empty(lead + (d_out, (k + 15) // 16 * 16), dtype=torch.int8, device=device)
         scale = torch.empty(lead + (k,), dtype=torch.float32, device=device)
-        bits = torch.empty(lead + (P * cfg.d // 32,), dtype=torch.int32, device=device)
+        if cfg.protect_axis == 1:
+            q8 = torch.empty(lead + (k, (d_in + 15) // 16 * 16), dtype=torch.int8, device=device)
+        else:
+            q8 = torch.empty(lead + (d_out, (k + 15) // 16 * 16), dtype=torch.int8, device=device)
+            bits = torch.empty(lead + (P * cfg.d // 32,), dtype=torch.int32, device=device)
     return Layer(cfg, codes, gains, idx, q8, scale, d_out, d_in, n_mats, bits)
 
 
@@ -355,6 +370,68 @@ def bsq_encode(cfg: Config, codec: Codec, W: torch.Tensor, g: torch.Tensor | Non
         if int(err.item()) & 1:
             raise BsqError(BSQ_ERR_NONFINITE, "bsq_encode")
     return out
+
+
+def bsq_encode_with_set(cfg: Config, codec: Codec, W: torch.Tensor, idx: torch.Tensor, out: Layer | None = None,
+                        ws: torch.Tensor | None = None, err: torch.Tensor | None = None, check: bool = True,
+                        stream=None) -> Layer:
+    """Encode W with a given protected set idx (int32 [k] or [n_mats, k], ascending)
+    on cfg.protect_axis: columns (axis 0) or rows (axis 1)."""
+    if W.dim() == 2:
+        n_mats, (d_out, d_in) = 1, W.shape
+    elif W.dim() == 3:
+        n_mats, d_out, d_in = W.shape
+    else:
+        raise ValueError("W must be 2-D or 3-D")
+    W = W.contiguous()
+    dev = W.device
+    out = out or layer_empty(cfg, d_out, d_in, n_mats, dev)
+    need = bsq_workspace_bytes(cfg, OP_ENCODE, n_mats, d_out, d_in)
+    ws = ws if ws is not None else _empty_aligned(need, dev)
+    own_err = err is None
+    err = err if err is not None else torch.zeros(1, dtype=torch.int32, device=dev)
+    idx = idx.to(device=dev, dtype=torch.int32).contiguous()
+    if idx.numel() != n_mats * out.k:
+        raise ValueError(f"idx holds {idx.numel()} entries, the layout needs {n_mats} x {out.k}")
+    c, L = cfg.c(), out.c()
+    _check(lib().bsq_encode_with_set(ct.byref(c), ct.c_void_p(codec.ptr()), _ptr(W), _dtype_code(W.dtype), n_mats,
+                                     d_out, d_in, _ptr(idx) if idx.numel() else None, ct.byref(L), _ptr(err),
+                                     _ptr(ws), ws.numel(), _stream(stream)), "bsq_encode_with_set")
+    if check and own_err:
+        e = int(err.item())
+        if e & 1:
+            raise BsqError(BSQ_ERR_NONFINITE, "bsq_encode_with_set")
+        if e & 2:
+            raise BsqError(BSQ_ERR_ARG, "bsq_encode_with_set (protected set not ascending or out of range)")
+    return out
+
+
+def bsq_coupled_select(cfg: Config, W_gate: torch.Tensor, W_up: torch.Tensor, W_down: torch.Tensor,
+                       g_gate=None, g_up=None, g_down=None, with_scores: bool = False, check: bool = True,
+                       stream=None):
+    """Coupled MLP intermediate-channel set (eq. mlp_coupled_protection): int32
+    [ceil(rho d_ffn)] ascending, and with_scores the fp64 scores [d_ffn]."""
+    d_ffn, d_model = W_gate.shape
+    if tuple(W_up.shape) != (d_ffn, d_model) or tuple(W_down.shape) != (d_model, d_ffn):
+        raise ValueError("W_gate, W_up must be [d_ffn, d_model] and W_down [d_model, d_ffn]")
+    if not (W_gate.dtype == W_up.dtype == W_down.dtype):
+        raise TypeError("the three matrices must share one dtype")
+    dev = W_gate.device
+    Wg, Wu, Wd = (t.contiguous() for t in (W_gate, W_up, W_down))
+    k = cfg.k(d_ffn)
+    idx = torch.empty(max(k, 1), dtype=torch.int32, device=dev)
+    scores = torch.empty(d_ffn, dtype=torch.float64, device=dev) if with_scores else None
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws = _empty_aligned(bsq_workspace_bytes(cfg, OP_SELECT, 1, d_ffn, d_model), dev)
+    gs = [None if g is None else g.to(device=dev, dtype=torch.float32).contiguous() for g in (g_gate, g_up, g_down)]
+    c = cfg.c()
+    _check(lib().bsq_coupled_select(ct.byref(c), _ptr(Wg), _ptr(Wu), _ptr(Wd), _dtype_code(Wg.dtype), d_model,
+                                    d_ffn, *[_ptr(g) for g in gs], _ptr(idx), _ptr(scores), _ptr(err), _ptr(ws),
+                                    ws.numel(), _stream(stream)), "bsq_coupled_select")
+    if check and int(err.item()) & 1:
+        raise BsqError(BSQ_ERR_NONFINITE, "bsq_coupled_select")
+    idx = idx[:k]
+    return (idx, scores) if with_scores else idx
 
 
 def bsq_decode(cfg: Config, codec: Codec, layer: Layer, dtype=torch.float32, out: torch.Tensor | None = None,

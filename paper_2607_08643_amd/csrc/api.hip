@@ -10,10 +10,37 @@ namespace {
 
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-int64_t k_of(const bsq_config &c, int64_t d_in)
+// protected slices of a d_out x d_in matrix on the config's axis
+int64_t k_of(const bsq_config &c, int64_t d_out, int64_t d_in)
 {
     if (c.protect_num == 0) return 0;
-    return (d_in * c.protect_num + c.protect_den - 1) / c.protect_den;
+    const int64_t n = (c.protect_axis == 1) ? d_out : d_in;
+    return (n * c.protect_num + c.protect_den - 1) / c.protect_den;
+}
+
+bool row_axis(const bsq_config &c) { return c.protect_axis == 1 && c.protect_num > 0; }
+
+// The configuration and layer the streaming kernels see: with protected rows
+// they code every row with no column masked (the protected rows' code 0 and
+// gain +0 contribute nothing), and the rows kernels write the protected rows.
+bsq_config coded_cfg(const bsq_config &c)
+{
+    bsq_config r = c;
+    if (row_axis(c)) r.protect_num = 0;
+    return r;
+}
+
+bsq_layer coded_layer(const bsq_config &c, const bsq_layer &L)
+{
+    bsq_layer r = L;
+    if (row_axis(c)) {
+        r.k = 0;
+        r.prot_idx = nullptr;
+        r.prot_q8 = nullptr;
+        r.prot_scale = nullptr;
+        r.prot_bits = nullptr;
+    }
+    return r;
 }
 
 int64_t pitch_of(const bsq_config &c, int64_t d_in)
@@ -30,6 +57,7 @@ bsq_status check_cfg(const bsq_config *c)
     if (c->dec_kind < BSQ_DEC_IDENTITY || c->dec_kind > BSQ_DEC_MLP) return BSQ_ERR_ARG;
     if (c->dec_kind == BSQ_DEC_MLP && (c->hidden < 1 || c->hidden > BSQ_MAX_HIDDEN)) return BSQ_ERR_ARG;
     if (c->protect_num < 0 || c->protect_den < 1 || c->protect_num > c->protect_den) return BSQ_ERR_ARG;
+    if (c->protect_axis != 0 && c->protect_axis != 1) return BSQ_ERR_ARG;
     if (c->d != 8 && c->d != 16) return BSQ_ERR_UNSUPPORTED;
     if (c->b != c->d) return BSQ_ERR_UNSUPPORTED;
     return BSQ_OK;
@@ -50,12 +78,20 @@ bsq_status check_layer(const bsq_config &c, const bsq_layer *L, bool need_planes
     if (s != BSQ_OK) return s;
     if (L->n_mats < 1) return BSQ_ERR_ARG;
     if (L->pitch != pitch_of(c, L->d_in)) return BSQ_ERR_ARG;
-    if (L->k != k_of(c, L->d_in)) return BSQ_ERR_ARG;
+    if (L->k != k_of(c, L->d_out, L->d_in)) return BSQ_ERR_ARG;
     if (need_planes && L->d_out > 0) {
         for (int i = 0; i < c.stages; ++i) {
             if (!L->codes[i] || !L->gains[i]) return BSQ_ERR_ARG;
             if (!aligned(L->codes[i], 16) || !aligned(L->gains[i], 16)) return BSQ_ERR_ALIGN;
         }
+    }
+    if (row_axis(c)) {
+        // protected rows: indices, scales and the [k][q8_pitch(d_in)] payload
+        if (L->k > 0 && (!L->prot_idx || !L->prot_scale || !L->prot_q8)) return BSQ_ERR_ARG;
+        if (L->k > 0 && (!aligned(L->prot_idx, 4) || !aligned(L->prot_scale, 4) || !aligned(L->prot_q8, 16)))
+            return BSQ_ERR_ALIGN;
+        if (L->k > 0 && L->d_in > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
+        return BSQ_OK;
     }
     if (L->k > 0 && (!L->prot_idx || !L->prot_scale)) return BSQ_ERR_ARG;
     if (L->k > 0 && L->d_out > 0 && !L->prot_q8) return BSQ_ERR_ARG;
@@ -110,7 +146,11 @@ bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, i
     if ((s = check_shape(*cfg, d_out, d_in)) != BSQ_OK) return s;
     if (lora_rank < 0 || lora_rank > BSQ_MAX_LORA_RANK) return BSQ_ERR_ARG;
     const bsq_config &c = *cfg;
-    const int64_t C = d_in / c.d, k = k_of(c, d_in), P = pitch_of(c, d_in);
+    const int64_t C = d_in / c.d, k = k_of(c, d_out, d_in), P = pitch_of(c, d_in);
+    const bool rows = row_axis(c);
+    // protected rows are not BSQ-coded: their all-zero plane rows are layout,
+    // not payload
+    const int64_t coded_rows = rows ? d_out - k : d_out;
     const int64_t code_bytes = (c.d <= 8) ? 1 : 2;
     out->pitch = P;
     out->k = k;
@@ -118,17 +158,17 @@ bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, i
     out->code_plane_bytes = plane_elems(d_out, P) * code_bytes;
     out->gain_plane_bytes = plane_elems(d_out, P) * 2;
     out->idx_bytes = k * 4;
-    out->q8_bytes = d_out * q8_pitch(k);
+    out->q8_bytes = rows ? k * q8_pitch(d_in) : d_out * q8_pitch(k);
     out->scale_bytes = k * 4;
-    out->bits_bytes = (k > 0) ? prot_words(P, c.d) * 4 : 0;
+    out->bits_bytes = (k > 0 && !rows) ? prot_words(P, c.d) * 4 : 0;
     int64_t dec_params = 0;
     if (c.dec_kind == BSQ_DEC_MLP) dec_params = int64_t(c.hidden) * c.b + c.hidden + int64_t(c.d) * c.hidden + c.d;
     else if (c.dec_kind == BSQ_DEC_LINEAR) dec_params = int64_t(c.d) * c.b + c.d;
-    out->S_code = double(c.stages) * double(d_out) * double(C) * double(c.b) / 8.0;
+    out->S_code = double(c.stages) * double(coded_rows) * double(C) * double(c.b) / 8.0;
     out->S_dec = double(c.stages) * double(dec_params) * 4.0;
-    out->S_8bit = double(d_out) * double(k);
+    out->S_8bit = rows ? double(k) * double(d_in) : double(d_out) * double(k);
     out->S_LoRA = 2.0 * double(lora_rank) * double(d_in + d_out);
-    out->S_meta = double(c.stages) * double(d_out) * double(C) * 2.0 + 8.0 * double(k);
+    out->S_meta = double(c.stages) * double(coded_rows) * double(C) * 2.0 + 8.0 * double(k);
     out->S_tot = out->S_code + out->S_dec + out->S_8bit + out->S_LoRA + out->S_meta;
     out->bpw_nominal = double(c.stages) * double(c.b) / double(c.d);
     out->bpw_real = (d_out > 0) ? 8.0 * out->S_tot / (double(d_out) * double(d_in)) : 0.0;
@@ -144,14 +184,18 @@ bsq_status bsq_workspace_bytes(const bsq_config *cfg, int32_t op, int64_t n_mats
     if ((s = check_shape(*cfg, d_out, d_in)) != BSQ_OK) return s;
     if (n_mats < 1) return BSQ_ERR_ARG;
     switch (op) {
-    case BSQ_OP_ENCODE: *bytes = encode_ws_layout(*cfg, n_mats, d_in, nullptr, nullptr); return BSQ_OK;
+    case BSQ_OP_ENCODE: *bytes = encode_ws_layout(*cfg, n_mats, d_out, d_in, nullptr, nullptr); return BSQ_OK;
     case BSQ_OP_GEMV:
         if (n_mats > BSQ_MAX_GROUP) return BSQ_ERR_ARG;
-        *bytes = gemv_ws_bytes(*cfg, n_mats, d_out, d_in);
+        *bytes = gemv_ws_bytes(coded_cfg(*cfg), n_mats, d_out, d_in);
         return BSQ_OK;
     case BSQ_OP_GEMM:
         if (M < 0) return BSQ_ERR_ARG;
-        *bytes = gemm_ws_bytes(*cfg, d_out, d_in, M);
+        *bytes = gemm_ws_bytes(coded_cfg(*cfg), d_out, d_in, M);
+        return BSQ_OK;
+    case BSQ_OP_SELECT:
+        if (n_mats != 1) return BSQ_ERR_ARG;
+        *bytes = select_ws_layout(d_out, nullptr, nullptr);
         return BSQ_OK;
     default: return BSQ_ERR_ARG;
     }
@@ -185,9 +229,11 @@ bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec, void
     return from_hip(launch_codec_tables(*cfg, dec ? dec : none, codec, static_cast<hipStream_t>(stream)));
 }
 
-bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype, int64_t n_mats,
-                      int64_t d_out, int64_t d_in, const float *g, const bsq_layer *out, int32_t *err, void *ws,
-                      size_t ws_bytes, void *stream)
+namespace {
+
+bsq_status encode_common(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype, int64_t n_mats,
+                         int64_t d_out, int64_t d_in, const float *g, const int32_t *given, const bsq_layer *out,
+                         int32_t *err, void *ws, size_t ws_bytes, void *stream)
 {
     bsq_status s = check_cfg(cfg);
     if (s != BSQ_OK) return s;
@@ -197,17 +243,66 @@ bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, i
     if (w_dtype != BSQ_F32 && w_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     if ((s = check_shape(c, d_out, d_in)) != BSQ_OK) return s;
     if (n_mats < 1) return BSQ_ERR_ARG;
-    if ((s = check_layer(c, out, true, true)) != BSQ_OK) return s;
+    if ((s = check_layer(c, out, true, !row_axis(c))) != BSQ_OK) return s;
     if (out->d_out != d_out || out->d_in != d_in || out->n_mats != n_mats) return BSQ_ERR_ARG;
     if (!aligned(W, 16) || !aligned(codec, 256) || !aligned(ws, 256) || !aligned(err, 4)) return BSQ_ERR_ALIGN;
     if (out->k > 0 && d_in > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
+    // the TopK (and the set check) keeps one bit per channel of the axis in LDS
+    if (out->k > 0 && row_axis(c) && d_out > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
+    if (out->k > 0 && row_axis(c) && (out->k > 65535 || n_mats > 65535)) return BSQ_ERR_UNSUPPORTED;
     if (g && !aligned(g, 4)) return BSQ_ERR_ALIGN;
-    const size_t need = encode_ws_layout(c, n_mats, d_in, nullptr, nullptr);
+    if (given && out->k > 0 && !aligned(given, 4)) return BSQ_ERR_ALIGN;
+    const size_t need = encode_ws_layout(c, n_mats, d_out, d_in, nullptr, nullptr);
     if (ws_bytes < need) return BSQ_ERR_BUFFER_TOO_SMALL;
     EncodeWs w{};
-    encode_ws_layout(c, n_mats, d_in, static_cast<char *>(ws), &w);
-    return from_hip(launch_encode(c, codec, W, w_dtype, n_mats, d_out, d_in, g, *out, err, w,
+    encode_ws_layout(c, n_mats, d_out, d_in, static_cast<char *>(ws), &w);
+    return from_hip(launch_encode(c, codec, W, w_dtype, n_mats, d_out, d_in, g, given, *out, err, w,
                                   static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype, int64_t n_mats,
+                      int64_t d_out, int64_t d_in, const float *g, const bsq_layer *out, int32_t *err, void *ws,
+                      size_t ws_bytes, void *stream)
+{
+    return encode_common(cfg, codec, W, w_dtype, n_mats, d_out, d_in, g, nullptr, out, err, ws, ws_bytes, stream);
+}
+
+bsq_status bsq_encode_with_set(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype,
+                               int64_t n_mats, int64_t d_out, int64_t d_in, const int32_t *idx, const bsq_layer *out,
+                               int32_t *err, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!cfg) return BSQ_ERR_ARG;
+    if (cfg->protect_num > 0 && !idx && k_of(*cfg, d_out, d_in) > 0) return BSQ_ERR_ARG;
+    return encode_common(cfg, codec, W, w_dtype, n_mats, d_out, d_in, nullptr, idx, out, err, ws, ws_bytes,
+                         stream);
+}
+
+bsq_status bsq_coupled_select(const bsq_config *cfg, const void *W_gate, const void *W_up, const void *W_down,
+                              int32_t w_dtype, int64_t d_model, int64_t d_ffn, const float *g_gate,
+                              const float *g_up, const float *g_down, int32_t *idx, double *scores, int32_t *err,
+                              void *ws, size_t ws_bytes, void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (w_dtype != BSQ_F32 && w_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if (d_model < 1 || d_ffn < 1) return BSQ_ERR_SHAPE;
+    // fp64 partial norms of whole columns/rows, one lane each; the TopK bitmap in LDS
+    if (d_ffn > (int64_t(1) << 18) || d_model > (int64_t(1) << 31)) return BSQ_ERR_UNSUPPORTED;
+    if (!W_gate || !W_up || !W_down || !err || !ws) return BSQ_ERR_ARG;
+    const int64_t k = (cfg->protect_num == 0) ? 0 : (d_ffn * cfg->protect_num + cfg->protect_den - 1) / cfg->protect_den;
+    if (k > 0 && !idx) return BSQ_ERR_ARG;
+    if (!aligned(W_gate, 16) || !aligned(W_up, 16) || !aligned(W_down, 16) || !aligned(err, 4) || !aligned(ws, 256))
+        return BSQ_ERR_ALIGN;
+    if ((g_gate && !aligned(g_gate, 4)) || (g_up && !aligned(g_up, 4)) || (g_down && !aligned(g_down, 4)))
+        return BSQ_ERR_ALIGN;
+    if ((idx && !aligned(idx, 4)) || (scores && !aligned(scores, 8))) return BSQ_ERR_ALIGN;
+    if (ws_bytes < select_ws_layout(d_ffn, nullptr, nullptr)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    SelectWs w{};
+    select_ws_layout(d_ffn, static_cast<char *>(ws), &w);
+    return from_hip(launch_coupled_select(W_gate, W_up, W_down, w_dtype, d_model, d_ffn, g_gate, g_up, g_down, k, idx,
+                                          scores, err, w, static_cast<hipStream_t>(stream)));
 }
 
 bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer *layer, void *W_hat,
@@ -220,7 +315,11 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
     if (out_dtype != BSQ_F32 && out_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
     if ((s = check_layer(*cfg, layer, true, false)) != BSQ_OK) return s;
     if (!aligned(W_hat, 16) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
-    return from_hip(launch_decode(*cfg, codec, *layer, W_hat, out_dtype, static_cast<hipStream_t>(stream)));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bsq_layer coded = coded_layer(*cfg, *layer);
+    if ((s = from_hip(launch_decode(coded_cfg(*cfg), codec, coded, W_hat, out_dtype, st))) != BSQ_OK) return s;
+    if (!row_axis(*cfg)) return BSQ_OK;
+    return from_hip(launch_decode_rows(*layer, W_hat, out_dtype, st));
 }
 
 namespace {
@@ -254,12 +353,21 @@ bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codec
     const bool split16 = codec_has_split(*cfg) && cfg->hidden == 16;
     if (x_dtype == BSQ_BF16 && cfg->d == 16 && !split16 && layers[0].pitch * cfg->d / 128 > 512)
         return BSQ_ERR_UNSUPPORTED;
-    if (x_dtype == BSQ_BF16 && layers[0].k > 4096) return BSQ_ERR_UNSUPPORTED;
+    if (x_dtype == BSQ_BF16 && !row_axis(*cfg) && layers[0].k > 4096) return BSQ_ERR_UNSUPPORTED;
     int64_t max_d_out = 0;
     for (int m = 0; m < n; ++m) max_d_out = layers[m].d_out > max_d_out ? layers[m].d_out : max_d_out;
-    if (ws_bytes < gemv_ws_bytes(*cfg, n, max_d_out, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    if (ws_bytes < gemv_ws_bytes(coded_cfg(*cfg), n, max_d_out, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
     return BSQ_OK;
 }
+
+// the layers as the streaming kernels see them (coded_layer of each)
+struct CodedGroup {
+    bsq_layer L[BSQ_MAX_GROUP];
+    CodedGroup(const bsq_config &c, int n, const bsq_layer *layers)
+    {
+        for (int m = 0; m < n; ++m) L[m] = coded_layer(c, layers[m]);
+    }
+};
 
 }  // namespace
 
@@ -273,8 +381,9 @@ bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const 
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
     // the d = 16 symmetric decoder folds its output layer into x here
     if (!codecs && codec_has_split(*cfg) && x_dtype == BSQ_BF16) return BSQ_ERR_ARG;
-    return from_hip(
-        launch_gemv_prep(*cfg, n, codecs, layers, loras, x, x_dtype, ws, static_cast<hipStream_t>(stream)));
+    const CodedGroup g(*cfg, n, layers);
+    return from_hip(launch_gemv_prep(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, ws,
+                                     static_cast<hipStream_t>(stream)));
 }
 
 bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
@@ -285,8 +394,13 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
     bsq_status s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, y, y_dtype, ws, ws_bytes);
     if (s != BSQ_OK) return s;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
-    return from_hip(launch_gemv_run(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws,
-                                    static_cast<hipStream_t>(stream)));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const CodedGroup g(*cfg, n, layers);
+    if ((s = from_hip(launch_gemv_run(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, st))) !=
+        BSQ_OK)
+        return s;
+    if (!row_axis(*cfg)) return BSQ_OK;
+    return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
 }
 
 bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
@@ -298,8 +412,13 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
     if (s != BSQ_OK) return s;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((s = from_hip(launch_gemv_prep(*cfg, n, codecs, layers, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
-    return from_hip(launch_gemv_run(*cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws, st));
+    const bsq_config cc = coded_cfg(*cfg);
+    const CodedGroup g(*cfg, n, layers);
+    if ((s = from_hip(launch_gemv_prep(cc, n, codecs, g.L, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
+    if ((s = from_hip(launch_gemv_run(cc, n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, st))) != BSQ_OK)
+        return s;
+    if (!row_axis(*cfg)) return BSQ_OK;
+    return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
 }
 
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer, const bsq_lora *lora,
@@ -318,10 +437,17 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     if (M < 0 || ldx < layer->d_in || ldy < layer->d_out || ldx % 8 != 0) return BSQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(ws, 256) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
     if (!aligned(Y, y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
-    if (ws_bytes < gemm_ws_bytes(*cfg, layer->d_out, layer->d_in, M)) return BSQ_ERR_BUFFER_TOO_SMALL;
-    if (layer->k > 4096) return BSQ_ERR_UNSUPPORTED;
-    return from_hip(launch_gemm(*cfg, codec, *layer, lora, X, M, ldx, Y, y_dtype, ldy, ws,
-                                static_cast<hipStream_t>(stream)));
+    const bsq_config cc = coded_cfg(*cfg);
+    if (ws_bytes < gemm_ws_bytes(cc, layer->d_out, layer->d_in, M)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    const bool rows = row_axis(*cfg);
+    if (!rows && layer->k > 4096) return BSQ_ERR_UNSUPPORTED;
+    // the protected-row launch takes four tokens per block along grid y
+    if (rows && (M + 3) / 4 > 65535) return BSQ_ERR_UNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bsq_layer coded = coded_layer(*cfg, *layer);
+    if ((s = from_hip(launch_gemm(cc, codec, coded, lora, X, M, ldx, Y, y_dtype, ldy, ws, st))) != BSQ_OK) return s;
+    if (!rows) return BSQ_OK;
+    return from_hip(launch_gemm_rows(*layer, lora, X, M, ldx, Y, y_dtype, ldy, gemm_lora_t(ws), st));
 }
 
 }  // extern "C"

@@ -116,9 +116,17 @@ __device__ __forceinline__ uint16_t gain_to_f16(float a)
 hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, void *codec, hipStream_t st);
 
 struct EncodeWs {
-    double *keys;       // [n_mats][d_in]
-    float *absmax;      // [n_mats][d_in]
-    int32_t *colmap;    // [n_mats][d_in]: protected column -> its position p
+    double *keys;       // [n_mats][n], n = d_in (column axis) or d_out (row axis)
+    float *absmax;      // [n_mats][n]
+    int32_t *colmap;    // [n_mats][n]: protected column -> its position p
+    uint32_t *bits;     // row axis: the row selection's bitmap (unused)
+};
+
+struct SelectWs {       // coupled MLP selection, all [d_ffn]
+    double *sg, *su, *sd, *keys;
+    float *absmax, *scale;
+    int32_t *colmap;
+    uint32_t *bits;
 };
 
 // int8 payload row length: k protected columns padded to a multiple of 16
@@ -127,10 +135,24 @@ __host__ __device__ inline int64_t q8_pitch(int64_t k) { return (k + 15) & ~int6
 
 // 32-bit words of a layer's protected-column bitmap: one bit per padded column
 __host__ __device__ inline int64_t prot_words(int64_t pitch, int d) { return pitch * d / 32; }
-size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, char *base, EncodeWs *ws);
+size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_out, int64_t d_in, char *base,
+                        EncodeWs *ws);
+size_t select_ws_layout(int64_t d_ffn, char *base, SelectWs *ws);
+// `given`: a caller's protected set (device int32 [n_mats][k]), or nullptr to select one
 hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W, int w_dtype,
-                         int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
+                         int64_t n_mats, int64_t d_out, int64_t d_in, const float *g, const int32_t *given,
                          const bsq_layer &out, int32_t *err, const EncodeWs &ws, hipStream_t st);
+hipError_t launch_coupled_select(const void *Wg, const void *Wu, const void *Wd, int w_dtype, int64_t d_model,
+                                 int64_t d_ffn, const float *gg, const float *gu, const float *gd, int64_t k,
+                                 int32_t *idx, double *scores, int32_t *err, const SelectWs &ws, hipStream_t st);
+// protected output rows of the products (run after the streaming kernels, same stream)
+hipError_t launch_decode_rows(const bsq_layer &layer, void *w_hat, int out_dtype, hipStream_t st);
+hipError_t launch_gemv_rows(int n, const bsq_layer *layers, const bsq_lora *loras, const void *x, int x_dtype,
+                            void *const *y, int y_dtype, hipStream_t st);
+hipError_t launch_gemm_rows(const bsq_layer &layer, const bsq_lora *lora, const void *X, int64_t M, int64_t ldx,
+                            void *Y, int y_dtype, int64_t ldy, const float *T, hipStream_t st);
+// X A^T (fp32 [Mp][BSQ_MAX_LORA_RANK]) as left in a GEMM workspace by launch_gemm
+const float *gemm_lora_t(const void *ws);
 
 hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
                          void *w_hat, int out_dtype, hipStream_t st);

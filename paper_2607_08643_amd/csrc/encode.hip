@@ -32,7 +32,7 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p) { return
 template <typename T>
 __global__ __launch_bounds__(256) void colscore_kernel(const T *__restrict__ W, int64_t d_out, int64_t d_in,
                                                        const float *__restrict__ g, double *__restrict__ keys,
-                                                       float *__restrict__ absmax)
+                                                       float *__restrict__ absmax, int32_t *err)
 {
     const int64_t m = blockIdx.y;
     const int64_t col = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -82,6 +82,85 @@ __global__ __launch_bounds__(256) void colscore_kernel(const T *__restrict__ W, 
     }
     keys[m * d_in + col] = s;
     absmax[m * d_in + col] = mx;
+    // a NaN or Inf makes the fp64 sum non-finite (squares of finite fp32
+    // values cannot overflow it)
+    if (err && !__builtin_isfinite(s)) atomicOr(err, 1);
+}
+
+// ---------------------------------------------------------------------------
+// Row energy key_i = g_i^2 * sum_j w_ij^2 (fp64, columns in order) and the
+// row absmax: the output-channel score, and the gate/up terms of the coupled
+// MLP score. One lane per row, walking its row in 16-byte pieces (a lane
+// reuses each cache line over its next loads).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void rowscore_kernel(const T *__restrict__ W, int64_t n_rows, int64_t n_cols,
+                                                       const float *__restrict__ g, double *__restrict__ keys,
+                                                       float *__restrict__ absmax, int32_t *err)
+{
+    const int64_t m = blockIdx.y;
+    const int64_t row = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (row >= n_rows) return;
+    const T *p = W + (m * n_rows + row) * n_cols;
+    double s = 0.0;
+    float mx = 0.0f;
+    auto take = [&](float v) {
+        const double dv = double(v);
+        s = s + dv * dv;
+        const float a = __builtin_fabsf(v);
+        if (a > mx) mx = a;
+    };
+    constexpr int V = 16 / int(sizeof(T));
+    const int64_t nv = n_cols / V;  // whole 16-byte pieces (rows are 16-byte aligned when n_cols % V == 0)
+    if (n_cols % V == 0) {
+        for (int64_t v = 0; v < nv; ++v) {
+            const uint4 raw = reinterpret_cast<const uint4 *>(p)[v];
+            if constexpr (sizeof(T) == 4) {
+                take(__uint_as_float(raw.x));
+                take(__uint_as_float(raw.y));
+                take(__uint_as_float(raw.z));
+                take(__uint_as_float(raw.w));
+            } else {
+                const uint32_t w4[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    take(bf16_to_f32(uint16_t(w4[e] & 0xffffu)));
+                    take(bf16_to_f32(uint16_t(w4[e] >> 16)));
+                }
+            }
+        }
+    } else {
+        for (int64_t j = 0; j < n_cols; ++j) take(load_elem<T>(p + j));
+    }
+    if (g) {
+        const double gi = double(g[m * n_rows + row]);
+        s = (gi * gi) * s;
+    }
+    keys[m * n_rows + row] = s;
+    absmax[m * n_rows + row] = mx;
+    if (err && !__builtin_isfinite(s)) atomicOr(err, 1);
+}
+
+// Coupled MLP score of channel j (eq. mlp_coupled_protection) from the three
+// fp64 squared norms: |g_gate| sqrt(sg) + |g_up| sqrt(su) + |g_down| sqrt(sd),
+// added left to right (correctly rounded fp64 square roots; no contraction).
+__global__ __launch_bounds__(256) void coupled_score_kernel(const double *__restrict__ sg,
+                                                            const double *__restrict__ su,
+                                                            const double *__restrict__ sd, const float *gg,
+                                                            const float *gu, const float *gd, int64_t n,
+                                                            double *__restrict__ keys, double *scores)
+{
+    const int64_t j = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (j >= n) return;
+    const double a = gg ? __builtin_fabs(double(gg[j])) : 1.0;
+    const double b = gu ? __builtin_fabs(double(gu[j])) : 1.0;
+    const double c = gd ? __builtin_fabs(double(gd[j])) : 1.0;
+    const double ta = a * __builtin_sqrt(sg[j]);
+    const double tb = b * __builtin_sqrt(su[j]);
+    const double tc = c * __builtin_sqrt(sd[j]);
+    const double v = (ta + tb) + tc;
+    keys[j] = v;
+    if (scores) scores[j] = v;
 }
 
 // Exclusive prefix sum over a 1024-thread block; returns the block total.
@@ -230,6 +309,118 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__rest
     }
     __syncthreads();
     for (int64_t w = t; w < words; w += TOPK_THREADS) bitmap[w] = s_bits[w];
+}
+
+// ---------------------------------------------------------------------------
+// A given protected column set: checks it (strictly ascending, in range),
+// then writes what topk_kernel writes for a selected one: the indices, the
+// scales absmax / 127, the column -> p map and the bitmap. One block per
+// matrix. An invalid entry ORs 2 into *err and is left out.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(TOPK_THREADS) void colset_kernel(const int32_t *__restrict__ idx_in,
+                                                              const float *__restrict__ absmax_all, int64_t d_in,
+                                                              int64_t k, int64_t words, int32_t *idx_out,
+                                                              float *__restrict__ scale_all,
+                                                              int32_t *__restrict__ colmap_all,
+                                                              uint32_t *__restrict__ bitmap_all, int32_t *err)
+{
+    extern __shared__ uint32_t s_bits[];
+    const int64_t m = blockIdx.x;
+    const int t = threadIdx.x;
+    for (int64_t j = t; j < d_in; j += TOPK_THREADS) colmap_all[m * d_in + j] = -1;
+    for (int64_t w = t; w < words; w += TOPK_THREADS) s_bits[w] = 0u;
+    __syncthreads();
+    for (int64_t p = t; p < k; p += TOPK_THREADS) {
+        const int32_t j = idx_in[m * k + p];
+        const bool ok = j >= 0 && j < d_in && (p == 0 || idx_in[m * k + p - 1] < j);
+        if (!ok) {
+            atomicOr(err, 2);
+            continue;
+        }
+        colmap_all[m * d_in + j] = int32_t(p);
+        atomicOr(&s_bits[j >> 5], 1u << (j & 31));
+        scale_all[m * k + p] = absmax_all[m * d_in + j] / 127.0f;
+        idx_out[m * k + p] = j;
+    }
+    __syncthreads();
+    for (int64_t w = t; w < words; w += TOPK_THREADS) bitmap_all[m * words + w] = s_bits[w];
+}
+
+// ---------------------------------------------------------------------------
+// Protected output rows (eq. protected_8bit_scatter with row slices): one
+// block per (protected row p, matrix). Checks the set, then the row's absmax
+// (exact in any order), scale = absmax / 127, the int8 row (round half even,
+// clamped to +-127, zero past d_in and when the scale is 0), and clears the
+// row's codes and gains in every stage plane (the row is not BSQ-coded). Runs
+// after the per-chunk encoder on the same stream.
+// ---------------------------------------------------------------------------
+struct RowProtArgs {
+    const void *W;
+    int64_t d_out, d_in, pitch, k;
+    const int32_t *idx_in;
+    int32_t *idx_out;
+    int8_t *q8;       // [n_mats][k][q8_pitch(d_in)]
+    float *scale;     // [n_mats][k]
+    void *codes[BSQ_MAX_STAGES];
+    uint16_t *gains[BSQ_MAX_STAGES];
+    int stages, code_bytes;
+    int32_t *err;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void rowprot_kernel(const RowProtArgs a)
+{
+    __shared__ float s_max[4];
+    const int64_t p = blockIdx.x, m = blockIdx.y;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int32_t i = a.idx_in[m * a.k + p];
+    const bool ok = i >= 0 && i < a.d_out && (p == 0 || a.idx_in[m * a.k + p - 1] < i);
+    if (!ok) {
+        if (t == 0) atomicOr(a.err, 2);
+        return;
+    }
+    const T *row = static_cast<const T *>(a.W) + (m * a.d_out + i) * a.d_in;
+    float mx = 0.0f;
+    for (int64_t j = t; j < a.d_in; j += 256) {
+        const float v = __builtin_fabsf(load_elem<T>(row + j));
+        if (v > mx) mx = v;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float y = __shfl_xor(mx, o, 64);
+        mx = (y > mx) ? y : mx;
+    }
+    if (lane == 0) s_max[wave] = mx;
+    __syncthreads();
+    float am = s_max[0];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) am = (s_max[w] > am) ? s_max[w] : am;
+    const float sc = am / 127.0f;
+    if (t == 0) {
+        a.scale[m * a.k + p] = sc;
+        a.idx_out[m * a.k + p] = i;
+    }
+    const int64_t qp = q8_pitch(a.d_in);
+    int8_t *qrow = a.q8 + (m * a.k + p) * qp;
+    for (int64_t j = t; j < qp; j += 256) {
+        int8_t q = 0;
+        if (j < a.d_in && sc != 0.0f) {
+            float tq = __builtin_rintf(load_elem<T>(row + j) / sc);
+            if (tq > 127.0f) tq = 127.0f;
+            if (tq < -127.0f) tq = -127.0f;
+            q = int8_t(tq);
+        }
+        qrow[j] = q;
+    }
+    const int64_t base = m * plane_elems(a.d_out, a.pitch);
+    for (int64_t c = t; c < a.pitch; c += 256) {
+        const int64_t gid = base + tile_index(i, c, a.pitch);
+        for (int s = 0; s < a.stages; ++s) {
+            if (a.code_bytes == 1) static_cast<uint8_t *>(a.codes[s])[gid] = 0;
+            else static_cast<uint16_t *>(a.codes[s])[gid] = 0;
+            a.gains[s][gid] = 0;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -408,43 +599,116 @@ hipError_t launch_encode_chunks(int stages, const EncodeArgs &a, hipStream_t st)
 
 }  // namespace
 
-size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_in, char *base, EncodeWs *ws)
+size_t encode_ws_layout(const bsq_config &cfg, int64_t n_mats, int64_t d_out, int64_t d_in, char *base,
+                        EncodeWs *ws)
 {
-    (void)cfg;
+    // scores, absmax and the channel map over the protected axis, and (row
+    // axis) the selection's bitmap, which nothing reads
+    const int64_t n = (cfg.protect_axis == 1) ? d_out : d_in;
     size_t off = 0;
     const size_t o_keys = off;
-    off = align256(off + size_t(n_mats) * d_in * 8);
+    off = align256(off + size_t(n_mats) * n * 8);
     const size_t o_abs = off;
-    off = align256(off + size_t(n_mats) * d_in * 4);
+    off = align256(off + size_t(n_mats) * n * 4);
     const size_t o_map = off;
-    off = align256(off + size_t(n_mats) * d_in * 4);
+    off = align256(off + size_t(n_mats) * n * 4);
+    const size_t o_bits = off;
+    if (cfg.protect_axis == 1) off = align256(off + size_t(n_mats) * ((n + 31) / 32) * 4);
     if (ws) {
         ws->keys = reinterpret_cast<double *>(base + o_keys);
         ws->absmax = reinterpret_cast<float *>(base + o_abs);
         ws->colmap = reinterpret_cast<int32_t *>(base + o_map);
+        ws->bits = reinterpret_cast<uint32_t *>(base + o_bits);
     }
     return off;
 }
 
+size_t select_ws_layout(int64_t d_ffn, char *base, SelectWs *ws)
+{
+    const int64_t n = d_ffn;
+    size_t off = 0, o[8];
+    for (int e = 0; e < 4; ++e) {  // sg, su, sd, keys (fp64)
+        o[e] = off;
+        off = align256(off + size_t(n) * 8);
+    }
+    for (int e = 4; e < 7; ++e) {  // absmax, scale, colmap (4 bytes each; unused results of the TopK)
+        o[e] = off;
+        off = align256(off + size_t(n) * 4);
+    }
+    o[7] = off;  // bitmap
+    off = align256(off + size_t((n + 31) / 32) * 4);
+    if (ws) {
+        ws->sg = reinterpret_cast<double *>(base + o[0]);
+        ws->su = reinterpret_cast<double *>(base + o[1]);
+        ws->sd = reinterpret_cast<double *>(base + o[2]);
+        ws->keys = reinterpret_cast<double *>(base + o[3]);
+        ws->absmax = reinterpret_cast<float *>(base + o[4]);
+        ws->scale = reinterpret_cast<float *>(base + o[5]);
+        ws->colmap = reinterpret_cast<int32_t *>(base + o[6]);
+        ws->bits = reinterpret_cast<uint32_t *>(base + o[7]);
+    }
+    return off;
+}
+
+namespace {
+
+template <typename T>
+hipError_t launch_colscore(const void *W, int64_t n_mats, int64_t d_out, int64_t d_in, const float *g, double *keys,
+                           float *absmax, int32_t *err, hipStream_t st)
+{
+    dim3 grid(unsigned((d_in + 255) / 256), unsigned(n_mats));
+    hipLaunchKernelGGL(colscore_kernel<T>, grid, dim3(256), 0, st, static_cast<const T *>(W), d_out, d_in, g, keys,
+                       absmax, err);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_rowscore(const void *W, int64_t n_mats, int64_t n_rows, int64_t n_cols, const float *g,
+                           double *keys, float *absmax, int32_t *err, hipStream_t st)
+{
+    dim3 grid(unsigned((n_rows + 255) / 256), unsigned(n_mats));
+    hipLaunchKernelGGL(rowscore_kernel<T>, grid, dim3(256), 0, st, static_cast<const T *>(W), n_rows, n_cols, g,
+                       keys, absmax, err);
+    return hipGetLastError();
+}
+
+}  // namespace
+
 hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W, int w_dtype,
-                         int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
+                         int64_t n_mats, int64_t d_out, int64_t d_in, const float *g, const int32_t *given,
                          const bsq_layer &out, int32_t *err, const EncodeWs &ws, hipStream_t st)
 {
     const int64_t k = out.k;
+    const bool rows = cfg.protect_axis == 1;
+    const bool bf = w_dtype == BSQ_BF16;
     hipError_t e = hipSuccess;
-    if (k > 0) {
-        dim3 grid(unsigned((d_in + 255) / 256), unsigned(n_mats));
-        if (w_dtype == BSQ_BF16)
-            hipLaunchKernelGGL(colscore_kernel<uint16_t>, grid, dim3(256), 0, st,
-                               static_cast<const uint16_t *>(W), d_out, d_in, g, ws.keys, ws.absmax);
-        else
-            hipLaunchKernelGGL(colscore_kernel<float>, grid, dim3(256), 0, st,
-                               static_cast<const float *>(W), d_out, d_in, g, ws.keys, ws.absmax);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (k > 0 && !rows) {
+        // column scores (or, for a given set, only the column absmax)
+        e = bf ? launch_colscore<uint16_t>(W, n_mats, d_out, d_in, given ? nullptr : g, ws.keys, ws.absmax,
+                                           nullptr, st)
+               : launch_colscore<float>(W, n_mats, d_out, d_in, given ? nullptr : g, ws.keys, ws.absmax, nullptr,
+                                        st);
+        if (e != hipSuccess) return e;
         const int64_t words = prot_words(out.pitch, cfg.d);
-        hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st,
-                           ws.keys, ws.absmax, d_in, k, words, out.prot_idx, out.prot_scale, ws.colmap,
-                           out.prot_bits);
+        if (given)
+            hipLaunchKernelGGL(colset_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st,
+                               given, ws.absmax, d_in, k, words, out.prot_idx, out.prot_scale, ws.colmap,
+                               out.prot_bits, err);
+        else
+            hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st,
+                               ws.keys, ws.absmax, d_in, k, words, out.prot_idx, out.prot_scale, ws.colmap,
+                               out.prot_bits);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (k > 0 && rows && !given) {
+        // output-row scores and their TopK (indices to the layer; the scale,
+        // map and bitmap the TopK also writes are recomputed or unused)
+        e = bf ? launch_rowscore<uint16_t>(W, n_mats, d_out, d_in, g, ws.keys, ws.absmax, nullptr, st)
+               : launch_rowscore<float>(W, n_mats, d_out, d_in, g, ws.keys, ws.absmax, nullptr, st);
+        if (e != hipSuccess) return e;
+        const int64_t words = (d_out + 31) / 32;
+        hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st, ws.keys,
+                           ws.absmax, d_out, k, words, out.prot_idx, out.prot_scale, ws.colmap, ws.bits);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     EncodeArgs a{};
@@ -453,7 +717,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
     a.d_in = d_in;
     a.pitch = out.pitch;
     a.C = d_in / cfg.d;
-    a.k = k;
+    a.k = rows ? 0 : k;  // the per-chunk encoder masks protected columns only
     a.words = prot_words(out.pitch, cfg.d);
     a.total = n_mats * plane_elems(d_out, out.pitch);
     const char *cb = static_cast<const char *>(codec);
@@ -462,17 +726,70 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
         a.gains[s] = out.gains[s];
         a.tab32[s] = reinterpret_cast<const float *>(cb + codec_tab32_offset(cfg, s));
     }
-    a.q8 = out.prot_q8;
+    a.q8 = rows ? nullptr : out.prot_q8;
     a.scale = out.prot_scale;
     a.colmap = ws.colmap;
-    a.bitmap = (k > 0) ? out.prot_bits : nullptr;
+    a.bitmap = (k > 0 && !rows) ? out.prot_bits : nullptr;
     a.err = err;
-    if (a.total == 0) return hipSuccess;
-    if (cfg.d == 8)
-        return (w_dtype == BSQ_BF16) ? launch_encode_chunks<8, uint16_t>(cfg.stages, a, st)
-                                     : launch_encode_chunks<8, float>(cfg.stages, a, st);
-    return (w_dtype == BSQ_BF16) ? launch_encode_chunks<16, uint16_t>(cfg.stages, a, st)
-                                 : launch_encode_chunks<16, float>(cfg.stages, a, st);
+    if (a.total > 0) {
+        if (cfg.d == 8)
+            e = bf ? launch_encode_chunks<8, uint16_t>(cfg.stages, a, st)
+                   : launch_encode_chunks<8, float>(cfg.stages, a, st);
+        else
+            e = bf ? launch_encode_chunks<16, uint16_t>(cfg.stages, a, st)
+                   : launch_encode_chunks<16, float>(cfg.stages, a, st);
+        if (e != hipSuccess) return e;
+    }
+    if (k > 0 && rows && d_in > 0) {
+        RowProtArgs r{};
+        r.W = W;
+        r.d_out = d_out;
+        r.d_in = d_in;
+        r.pitch = out.pitch;
+        r.k = k;
+        r.idx_in = given ? given : out.prot_idx;
+        r.idx_out = out.prot_idx;
+        r.q8 = out.prot_q8;
+        r.scale = out.prot_scale;
+        for (int s = 0; s < cfg.stages; ++s) {
+            r.codes[s] = out.codes[s];
+            r.gains[s] = out.gains[s];
+        }
+        r.stages = cfg.stages;
+        r.code_bytes = (cfg.d <= 8) ? 1 : 2;
+        r.err = err;
+        const dim3 grid{unsigned(k), unsigned(n_mats)};
+        if (bf) hipLaunchKernelGGL(rowprot_kernel<uint16_t>, grid, dim3(256), 0, st, r);
+        else hipLaunchKernelGGL(rowprot_kernel<float>, grid, dim3(256), 0, st, r);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_coupled_select(const void *Wg, const void *Wu, const void *Wd, int w_dtype, int64_t d_model,
+                                 int64_t d_ffn, const float *gg, const float *gu, const float *gd, int64_t k,
+                                 int32_t *idx, double *scores, int32_t *err, const SelectWs &ws, hipStream_t st)
+{
+    const bool bf = w_dtype == BSQ_BF16;
+    hipError_t e;
+    // squared norms: gate and up rows (over d_model), down columns (over d_model rows)
+    e = bf ? launch_rowscore<uint16_t>(Wg, 1, d_ffn, d_model, nullptr, ws.sg, ws.absmax, err, st)
+           : launch_rowscore<float>(Wg, 1, d_ffn, d_model, nullptr, ws.sg, ws.absmax, err, st);
+    if (e != hipSuccess) return e;
+    e = bf ? launch_rowscore<uint16_t>(Wu, 1, d_ffn, d_model, nullptr, ws.su, ws.absmax, err, st)
+           : launch_rowscore<float>(Wu, 1, d_ffn, d_model, nullptr, ws.su, ws.absmax, err, st);
+    if (e != hipSuccess) return e;
+    e = bf ? launch_colscore<uint16_t>(Wd, 1, d_model, d_ffn, nullptr, ws.sd, ws.absmax, err, st)
+           : launch_colscore<float>(Wd, 1, d_model, d_ffn, nullptr, ws.sd, ws.absmax, err, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(coupled_score_kernel, dim3(unsigned((d_ffn + 255) / 256)), dim3(256), 0, st, ws.sg, ws.su,
+                       ws.sd, gg, gu, gd, d_ffn, ws.keys, scores);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (k == 0) return hipSuccess;
+    const int64_t words = (d_ffn + 31) / 32;
+    hipLaunchKernelGGL(topk_kernel, dim3(1u), dim3(TOPK_THREADS), size_t(words) * 4, st, ws.keys, ws.absmax, d_ffn, k,
+                       words, idx, ws.scale, ws.colmap, ws.bits);
+    return hipGetLastError();
 }
 
 }  // namespace bsq

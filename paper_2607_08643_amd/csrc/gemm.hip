@@ -1053,6 +1053,11 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 
 }  // namespace
 
+const float *gemm_lora_t(const void *ws)
+{
+    return reinterpret_cast<const float *>(static_cast<const char *>(ws) + GEMM_SLOT_BYTES);
+}
+
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M)
 {
     const int64_t k = cfg.protect_num ? (d_in * cfg.protect_num + cfg.protect_den - 1) / cfg.protect_den : 0;

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 3
+    assert bsq.bsq_version() == 4
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -64,13 +64,15 @@ def test_code_bits_must_equal_chunk_length():
 @pytest.mark.parametrize("d", [8, 16])
 @pytest.mark.parametrize("shape", [(4096, 4096), (1024, 4096), (4096, 12288), (25600, 5120), (333, 296), (0, 256)])
 @pytest.mark.parametrize("rank", [0, 16])
-def test_sizes_match_oracle_accounting(d, shape, rank):
+@pytest.mark.parametrize("axis", [0, 1], ids=["cols", "rows"])
+def test_sizes_match_oracle_accounting(d, shape, rank, axis):
     d_out, d_in = shape
     if d_in % d:
         pytest.skip("not chunkable")
-    cfg = bsq.Config(d=d, hidden=d)
+    cfg = bsq.Config(d=d, hidden=d, protect_axis=axis)
     got = bsq.bsq_layer_sizes(cfg, d_out, d_in, rank)
-    ref = oracle.sizes(oracle.Config(d=d, b=d, stages=2, kind=oracle.KIND_MLP, hidden=d), d_out, d_in, rank)
+    ref = oracle.sizes(oracle.Config(d=d, b=d, stages=2, kind=oracle.KIND_MLP, hidden=d, protect_axis=axis),
+                       d_out, d_in, rank)
     for key in ("S_code", "S_dec", "S_8bit", "S_LoRA", "S_meta", "S_tot", "bpw_nominal"):
         assert got[key] == pytest.approx(ref[key], rel=0, abs=1e-9), key
     if d_out:
@@ -79,6 +81,11 @@ def test_sizes_match_oracle_accounting(d, shape, rank):
     rows = (d_out + 63) // 64 * 64   # tiled planes pad the rows to 64
     assert got["code_plane_bytes"] == rows * got["pitch"] * (1 if d == 8 else 2)
     assert got["gain_plane_bytes"] == rows * got["pitch"] * 2
+    if axis == 1:
+        # protected rows: [k][roundup(d_in, 16)] int8 payload and no bitmap
+        assert got["k"] == cfg.k(d_out) and got["bits_bytes"] == 0
+        assert got["q8_bytes"] == got["k"] * ((d_in + 15) // 16 * 16)
+        return
     # one bit per padded input column when there are protected columns
     assert got["bits_bytes"] == (got["pitch"] * d // 8 if got["k"] else 0)
 
@@ -237,3 +244,49 @@ def test_product_path_has_no_cpu_fallback():
     assert "import oracle" not in src and "from oracle" not in src
     with open(os.path.join(ROOT, "paper_2607_08643_amd", "__init__.py")) as f:
         assert "oracle" not in f.read()
+
+
+def test_row_axis_and_select_reject_before_launch():
+    """Protected rows (protect_axis = 1), bsq_encode_with_set and
+    bsq_coupled_select validate on the host and return before any launch."""
+    c = bsq.Config(protect_axis=2).c()
+    assert bsq.lib().bsq_config_check(ct.byref(c)) == bsq.BSQ_ERR_ARG
+    cfg = bsq.Config(protect_axis=1)
+    L = _fake_layer(cfg, 300, 256)
+    L.k = cfg.k(300)                                           # k counts rows on this axis
+    L.prot_bits = 0                                            # no bitmap for protected rows
+    assert L.k == 3
+    ws_rows = bsq.bsq_workspace_bytes(cfg, bsq.OP_ENCODE, 1, 300, 256)
+    ws_cols = bsq.bsq_workspace_bytes(bsq.Config(), bsq.OP_ENCODE, 1, 300, 256)
+    assert ws_rows != ws_cols                                  # scores over rows, not columns
+    bad = _fake_layer(cfg, 300, 256)
+    bad.k = cfg.k(600)                                         # not ceil(rho * d_out)
+    assert _encode(cfg, bad, d_out=300) == bsq.BSQ_ERR_ARG
+    L.prot_q8 = FAKE + 0x300008
+    assert _encode(cfg, L, d_out=300) == bsq.BSQ_ERR_ALIGN
+    L.prot_q8 = 0
+    assert _encode(cfg, L, d_out=300) == bsq.BSQ_ERR_ARG
+    L.prot_q8 = FAKE + 0x300000
+    cc = cfg.c()
+    lib = bsq.lib()
+    # a protected set is required when k > 0
+    assert lib.bsq_encode_with_set(ct.byref(cc), ct.c_void_p(FAKE), ct.c_void_p(FAKE), bsq.BSQ_BF16, 1, 300, 256,
+                                   None, ct.byref(L), ct.c_void_p(FAKE), ct.c_void_p(FAKE), 1 << 30,
+                                   None) == bsq.BSQ_ERR_ARG
+    assert lib.bsq_encode_with_set(ct.byref(cc), ct.c_void_p(FAKE), ct.c_void_p(FAKE), bsq.BSQ_BF16, 1, 300, 256,
+                                   ct.c_void_p(FAKE + 2), ct.byref(L), ct.c_void_p(FAKE), ct.c_void_p(FAKE),
+                                   1 << 30, None) == bsq.BSQ_ERR_ALIGN
+
+    def sel(d_model=256, d_ffn=1000, dtype=bsq.BSQ_BF16, ws_bytes=1 << 30, Wg=FAKE, idx=FAKE, ws=FAKE):
+        return lib.bsq_coupled_select(ct.byref(cc), Wg and ct.c_void_p(Wg), ct.c_void_p(FAKE), ct.c_void_p(FAKE),
+                                      dtype, d_model, d_ffn, None, None, None, idx and ct.c_void_p(idx), None,
+                                      ct.c_void_p(FAKE), ws and ct.c_void_p(ws), ws_bytes, None)
+    assert sel(Wg=0) == bsq.BSQ_ERR_ARG
+    assert sel(idx=0) == bsq.BSQ_ERR_ARG
+    assert sel(ws=0) == bsq.BSQ_ERR_ARG
+    assert sel(dtype=9) == bsq.BSQ_ERR_DTYPE
+    assert sel(d_ffn=0) == bsq.BSQ_ERR_SHAPE
+    assert sel(d_ffn=(1 << 18) + 1) == bsq.BSQ_ERR_UNSUPPORTED
+    assert sel(Wg=FAKE + 4) == bsq.BSQ_ERR_ALIGN
+    assert sel(ws_bytes=64) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_SELECT, 1, 25600, 5120) > 25600 * 8 * 4
