@@ -56,6 +56,8 @@ def parse():
     p.add_argument("--no-d16", action="store_true", help="skip the d = 16 figures")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     p.add_argument("--no-gemm", action="store_true")
+    p.add_argument("--profile-gemm-only", action="store_true",
+                   help="d = 8 GEMV step and the fused GEMM at M = 16/64/256 only (for counter runs)")
     p.add_argument("--profile-gemv-only", action="store_true",
                    help="only run the GEMV steps (for rocprofv3 counter passes)")
     p.add_argument("--no-stacks", action="store_true",
@@ -149,7 +151,8 @@ def main():
     torch.cuda.set_device(dev)
     bsq.lib()
     results = {}
-    d_list = [args.d] + ([] if (args.no_d16 or args.profile_gemv_only) else [16 if args.d == 8 else 8])
+    only = args.profile_gemv_only or args.profile_gemm_only
+    d_list = [args.d] + ([] if (args.no_d16 or only) else [16 if args.d == 8 else 8])
     head = None
     for d in d_list:
         log(f"[bench] encoding {args.copies} copies of the Qwen3-8B block at d={d}")
@@ -246,7 +249,7 @@ def main():
                    kernel_us=k_ms * 1e3, kernel_bytes=k_bytes, kernel_gbs=k_gbs,
                    kernel_us_p10=k_p10 * 1e3, kernel_us_p90=k_p90 * 1e3)
 
-        if not args.profile_gemv_only:
+        if not args.profile_gemv_only and not args.profile_gemm_only:
             # decode GB/s (reads the planes, writes bf16 W_hat) on the largest projection
             L = blk.layers["gate"].mat(0)
             out = torch.empty((L.d_out, L.d_in), dtype=torch.bfloat16, device=dev)
@@ -261,6 +264,8 @@ def main():
             dms = a.elapsed_time(b) / 10
             res["decode_gbs"] = (L.nbytes_streamed() + out.numel() * 2) / (dms / 1e3) / 1e9
             del out
+        if not args.profile_gemv_only:
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             if not args.no_gemm:
                 gem = {}
                 for M in (16, 64, 256):
@@ -299,7 +304,8 @@ def main():
                     gem[str(M)] = dict(tflops=round(tf, 1), pct_bf16_mfma_peak=round(100 * tf / BF16_MFMA_PEAK_TFLOPS, 2))
                     log(f"[bench] d={d}: gemm M={M}: {tf:.1f} TFLOP/s")
                 res["gemm"] = gem
-                res["comparator"] = comparator(blk, bsq, synth, torch, dev, args.copies)
+                if not args.profile_gemm_only:
+                    res["comparator"] = comparator(blk, bsq, synth, torch, dev, args.copies)
         results[d] = res
         if head is None:
             head = (blk, plans)
@@ -325,10 +331,10 @@ def main():
     del src, dst
     hd = results[args.d]
     cpu = None
-    if not args.no_cpu and not args.profile_gemv_only:
+    if not args.no_cpu and not only:
         cpu = cpu_baseline(head[0], torch)
     stacks = {}
-    if not args.no_stacks and not args.profile_gemv_only:
+    if not args.no_stacks and not only:
         del head
         torch.cuda.empty_cache()
         stacks["qwen3_8b_36_layers_lora16"] = stack_bench(bsq, synth, torch, np, synth.qwen3_8b_block(), 36, args.d,
