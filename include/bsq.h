@@ -237,7 +237,9 @@ bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, i
  * +0. An invalid set ORs 2 into *err (and the outputs are unspecified); NaN
  * or Inf in W ORs 1. This is how the coupled set of bsq_coupled_select is
  * applied to the gate and up rows (axis 1) and the down columns (axis 0).
- * `g` is not used. Other arguments as for bsq_encode. */
+ * `g` is not used. Other arguments as for bsq_encode. With protect_axis = 1
+ * and k > 0: d_out <= 2^18 and n_mats <= 65535 (BSQ_ERR_UNSUPPORTED beyond;
+ * the same holds for bsq_encode on that axis). */
 bsq_status bsq_encode_with_set(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype,
                                int64_t n_mats, int64_t d_out, int64_t d_in, const int32_t *idx,
                                const bsq_layer *out, int32_t *err, void *ws, size_t ws_bytes,
@@ -351,7 +353,8 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  * The K steps of a tile may be split over several blocks; their fp32
  * partials are summed in a fixed order, so results are deterministic. With
  * protect_axis = 1 each protected row's column of Y is written afterwards as
- * scale_p X q8[p, :]^T + (X A^T) B[row]^T (same stream). */
+ * scale_p X q8[p, :]^T + (X A^T) B[row]^T (same stream); that pass takes four
+ * tokens per block, so M <= 262140 there (BSQ_ERR_UNSUPPORTED beyond). */
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
                     const bsq_lora *lora, const void *X, int32_t x_dtype, int64_t M,
                     int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,

@@ -249,7 +249,8 @@ bsq_status encode_common(const bsq_config *cfg, const void *codec, const void *W
     if (out->k > 0 && d_in > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
     // the TopK (and the set check) keeps one bit per channel of the axis in LDS
     if (out->k > 0 && row_axis(c) && d_out > (int64_t(1) << 18)) return BSQ_ERR_UNSUPPORTED;
-    if (out->k > 0 && row_axis(c) && (out->k > 65535 || n_mats > 65535)) return BSQ_ERR_UNSUPPORTED;
+    // the protected-row pass runs one block per (row, matrix), matrices along grid y
+    if (out->k > 0 && row_axis(c) && n_mats > 65535) return BSQ_ERR_UNSUPPORTED;
     if (g && !aligned(g, 4)) return BSQ_ERR_ALIGN;
     if (given && out->k > 0 && !aligned(given, 4)) return BSQ_ERR_ALIGN;
     const size_t need = encode_ws_layout(c, n_mats, d_out, d_in, nullptr, nullptr);
