@@ -290,3 +290,40 @@ def test_coupled_mlp_protection_end_to_end(gpu):
         vf = oracle.to_f32(v)
         check_close(y.cpu().numpy(), oracle.dense_product(w_hat, vf), 2e-2, f"axis {oc_axis} product",
                     rss=rss_terms(w_hat, vf))
+
+
+@pytest.mark.parametrize("d", [8, 16])
+def test_row_axis_degenerate_cases(d, gpu):
+    """Row axis with no protected rows (rho = 0, and a matrix too small for
+    k > 0 is impossible: k = ceil(rho d_out) >= 1 for d_out >= 1), an empty
+    batch, and every row protected (rho = 1: no row is BSQ-coded)."""
+    decs = None
+    for num, den in ((0, 1), (1, 1)):
+        cfg = bsq.Config(d=d, hidden=d, protect_axis=1, protect_num=num, protect_den=den)
+        decs = decoders(cfg, 2)
+        oc = ocfg(cfg)
+        W, _ = synth.weight(70, 256, 17)
+        codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+        layer = bsq.bsq_encode(cfg, codec, W.to(gpu))
+        enc = oracle.encode(oc, decs, oracle.to_f32(W))
+        torch.cuda.synchronize()
+        assert_rows_layer_equal(layer, enc, cfg)
+        w_hat = oracle.decode(oc, decs, enc)
+        got = bsq.bsq_decode(cfg, codec, layer)
+        x = synth.activation(256, seed=3)
+        y = bsq.bsq_gemv(cfg, codec, layer, x.to(gpu), y_dtype=torch.float32)
+        X = synth.activation(256, seed=4, batch=7)
+        Y = bsq.bsq_gemm(cfg, codec, layer, X.to(gpu), y_dtype=torch.float32)
+        Y0 = bsq.bsq_gemm(cfg, codec, layer, X[:0].to(gpu), y_dtype=torch.float32)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(got.cpu().numpy().view(np.uint32), w_hat.view(np.uint32))
+        xf, Xf = oracle.to_f32(x), oracle.to_f32(X)
+        check_close(y.cpu().numpy(), oracle.dense_product(w_hat, xf), 2e-2, f"gemv rho={num}/{den}",
+                    rss=rss_terms(w_hat, xf))
+        check_close(Y.cpu().numpy(), oracle.dense_product(w_hat, Xf), 2e-2, f"gemm rho={num}/{den}",
+                    rss=rss_terms(w_hat, Xf))
+        assert Y0.shape == (0, 70)
+        if num == den:
+            # every row protected: the planes hold only zeros
+            for s in range(cfg.stages):
+                assert int(layer.codes[s].abs().sum()) == 0 and int(layer.gains[s].abs().sum()) == 0
