@@ -455,3 +455,44 @@ def test_category_batched_stack_encode(gpu):
     tabs = oracle.decoder_table(oc, decs)
     for m in range(8):
         assert_layer_equal(layer, oracle.encode(oc, decs, Wf[m], tables=tabs), cfg, m)
+
+
+@pytest.mark.parametrize("d", [8, 16])
+def test_full_block_grouped_gemv(d, gpu):
+    """The bench's step at full size and in its launch configuration: the
+    Qwen3-8B-shaped block's four grouped GEMVs (q/k/v sharing x, o, gate/up
+    sharing x, down), one codec per projection category, rank-16 LoRA on the
+    q/k/v group; every output of every projection against the oracle's own
+    encoding of the same weights."""
+    cfg = bsq.Config(d=d, hidden=d)
+    oc = ocfg(cfg)
+    projs = synth.qwen3_8b_block()
+    groups = {}
+    for p in projs:
+        groups.setdefault(p.group, []).append(p)
+    for gi, (gname, ps) in enumerate(groups.items()):
+        say(f"block group {gname} d={d}")
+        x = synth.activation(ps[0].d_in, seed=90 + gi, device=gpu)
+        xf = oracle.to_f32(x)
+        codecs, layers, encs, decs_l, loras = [], [], [], [], []
+        for p in ps:
+            decs = decoders(cfg, seed=100 + projs.index(p))
+            W, _ = synth.weight(p.d_out, p.d_in, seed=200 + projs.index(p), k_outliers=cfg.k(p.d_in), device=gpu)
+            codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+            codecs.append(codec)
+            layers.append(bsq.bsq_encode(cfg, codec, W))
+            encs.append(oracle.encode(oc, decs, oracle.to_f32(W)))
+            decs_l.append(decs)
+            loras.append(synth.lora(p.d_out, p.d_in, 16, seed=300 + projs.index(p), device=gpu)
+                         if gname == "qkv" else None)
+            del W
+        lora_arg = loras if gname == "qkv" else None
+        ys = bsq.bsq_gemv(cfg, codecs, layers, x, loras=lora_arg, y_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        for i, p in enumerate(ps):
+            lref = None if loras[i] is None else (oracle.to_f32(loras[i][0]), oracle.to_f32(loras[i][1]))
+            w_hat = oracle.decode(oc, decs_l[i], encs[i])
+            y_ref = oracle.dense_product(w_hat, xf, lref)
+            check_close(ys[i].float().cpu().numpy(), y_ref, 2e-2, f"{p.name} d={d}",
+                        rss=rss_terms(w_hat, xf, lref))
+            del w_hat
