@@ -238,6 +238,119 @@ def test_linear_special_cases():
     np.testing.assert_array_equal(tab, ident[:, perm])
 
 
+def _all_codes_q(b):
+    """q for every b-bit code, [2^b, b]: q_j = +-1/sqrt(b) by bit j (LSB first),
+    built here from the definition of the sphere map (Section III-C)."""
+    codes = np.arange(1 << b, dtype=np.int64)
+    bits = (codes[:, None] >> np.arange(b)[None, :]) & 1
+    return np.where(bits == 1, 1.0, -1.0) / math.sqrt(b)
+
+
+def _fma_chain_bound(n_terms, *mags):
+    """Bound on |fp32 fmaf chain - exact| for a sum of n_terms products
+    started from a bias: each step rounds once (relative 2^-24), so the
+    error is at most (n + 1) 2^-24 times the sum of the magnitudes."""
+    return (n_terms + 1) * 2.0 ** -24 * sum(mags)
+
+
+@pytest.mark.parametrize("d,b", [(8, 8), (16, 16), (8, 12), (12, 8)])
+def test_linear_decoder_with_bias_against_numpy(d, b):
+    """Linear decoder y = beta + M q (M is d x b, beta nonzero), every code,
+    against an fp64 numpy evaluation written from the definition: a dropped or
+    mis-indexed beta, a transposed M or a row stride of d instead of b fails."""
+    cfg = Config(d=d, b=b, stages=1, kind=KIND_LINEAR, protect_num=0)
+    r = _rng(300 + d + b)
+    M = r.uniform(-0.5, 0.5, (d, b)).astype(np.float32)
+    beta = r.uniform(-1.0, 1.0, d).astype(np.float32)
+    tab = oracle.decoder_table(cfg, [synth.StageDecoder(W1=M, b1=beta)])[0]
+    q = _all_codes_q(b)
+    qf = q.astype(np.float32).astype(np.float64)   # the oracle's fp32 code values
+    want = beta.astype(np.float64)[None, :] + qf @ M.astype(np.float64).T
+    bound = _fma_chain_bound(b, np.abs(beta)[None, :], np.abs(qf) @ np.abs(M.astype(np.float64)).T)
+    assert np.all(np.abs(tab - want) <= bound)
+    # the bias alone (M = 0) comes back exactly, for every code
+    tab0 = oracle.decoder_table(cfg, [synth.StageDecoder(W1=np.zeros((d, b), np.float32), b1=beta)])[0]
+    np.testing.assert_array_equal(tab0, np.broadcast_to(beta, tab0.shape))
+
+
+def test_linear_permutation_plus_bias_is_one_rounding():
+    """M a permutation and beta nonzero: each output is beta_m + q_perm(m)
+    rounded once to fp32 (the chain adds exact zeros and one product), so the
+    table equals numpy's fp32 sum bit for bit."""
+    d = 8
+    cfg = Config(d=d, b=d, stages=1, kind=KIND_LINEAR, protect_num=0)
+    perm = np.array([3, 0, 7, 1, 6, 2, 5, 4])
+    P = np.eye(d, dtype=np.float32)[perm]
+    beta = (np.arange(d, dtype=np.float32) - 3.25) * np.float32(0.37)
+    tab = oracle.decoder_table(cfg, [synth.StageDecoder(W1=P, b1=beta)])[0]
+    c = np.float32(oracle.lib().orc_code_scale(d))
+    q32 = np.where(_all_codes_q(d) > 0, c, -c).astype(np.float32)
+    want = beta[None, :] + q32[:, perm]
+    np.testing.assert_array_equal(tab.view(np.uint32), want.astype(np.float32).view(np.uint32))
+
+
+@pytest.mark.parametrize("d,b,h", [(8, 8, 5), (8, 8, 16), (16, 16, 5), (8, 12, 16), (12, 8, 3)])
+def test_mlp_decoder_hidden_width_against_numpy(d, b, h):
+    """Symmetric decoder at hidden widths other than d: every code against an
+    fp64 numpy evaluation of W2 relu(W1 q + b1) + b2. The bound propagates the
+    fp32 rounding of each hidden unit through relu (1-Lipschitz) and W2, so a
+    W2 stride of d instead of h, a hidden loop bound of d, or a W1 stride of d
+    instead of b fails."""
+    cfg = Config(d=d, b=b, stages=1, kind=KIND_MLP, hidden=h, protect_num=0)
+    decs = synth.decoder_params(KIND_MLP, d, b, h, 1, seed=400 + h)
+    dec = decs[0]
+    tab = oracle.decoder_table(cfg, decs)[0]
+    q = _all_codes_q(b).astype(np.float32).astype(np.float64)
+    W1, b1, W2, b2 = (v.astype(np.float64) for v in (dec.W1, dec.b1, dec.W2, dec.b2))
+    pre = q @ W1.T + b1[None, :]
+    a = np.maximum(pre, 0.0)
+    want = a @ W2.T + b2[None, :]
+    ea = _fma_chain_bound(b, np.abs(b1)[None, :], np.abs(q) @ np.abs(W1).T)
+    bound = ea @ np.abs(W2).T + _fma_chain_bound(h, np.abs(b2)[None, :], (np.abs(a) + ea) @ np.abs(W2).T)
+    assert np.all(np.abs(tab - want) <= bound)
+    assert np.abs(want).max() > 10 * bound.max()   # the bound is far below the values it guards
+
+
+def test_mlp_decoder_selector_closed_form():
+    """h = 16 > d = 8 with one-hot W1 and W2: hidden unit k is b1_k + q_(k mod b)
+    (one fp32 rounding), and output m reads only hidden unit 15 - m, all of
+    them past index d. So y_m = relu(fp32(b1_(15-m) + q_((15-m) mod 8))) bit
+    for bit; a loop over d hidden units or a W2 stride of d gives b2 = 0 or
+    the wrong unit."""
+    d, b, h = 8, 8, 16
+    cfg = Config(d=d, b=b, stages=1, kind=KIND_MLP, hidden=h, protect_num=0)
+    W1 = np.zeros((h, b), np.float32)
+    W1[np.arange(h), np.arange(h) % b] = 1.0
+    b1 = np.array([0.5, -0.5, 0.25, -1.0, 0.125, -0.25, 0.75, -0.125,
+                   0.3, -0.3, 0.1, -0.6, 0.45, -0.05, 0.2, -0.4], np.float32)
+    sel = h - 1 - np.arange(d)
+    W2 = np.zeros((d, h), np.float32)
+    W2[np.arange(d), sel] = 1.0
+    b2 = np.zeros(d, np.float32)
+    tab = oracle.decoder_table(cfg, [synth.StageDecoder(W1=W1, b1=b1, W2=W2, b2=b2)])[0]
+    c = np.float32(oracle.lib().orc_code_scale(b))
+    q32 = np.where(_all_codes_q(b) > 0, c, -c).astype(np.float32)
+    pre = b1[sel][None, :] + q32[:, sel % b]                 # fp32 sums, one rounding each
+    want = np.where(pre > 0, pre, np.float32(0.0)).astype(np.float32)
+    np.testing.assert_array_equal(tab.view(np.uint32), want.view(np.uint32))
+    assert (want > 0).mean() > 0.3 and (want == 0).mean() > 0.3
+
+
+def test_mlp_relu_gives_positive_zero():
+    """relu(a) is +0 for a <= 0, including a = -0: with W1 = 0 and b1 = -0 the
+    pre-activation of code 0 is -0 (every product is -0), with b1 = -1 it is
+    negative; W2 = 1 and b2 = -0 then give y = +0 only if relu returned +0
+    (-0 + -0 would stay -0). The sign bit is checked on every code."""
+    d = 8
+    cfg = Config(d=d, b=d, stages=1, kind=KIND_MLP, hidden=d, protect_num=0)
+    for b1v in (-0.0, -1.0):
+        dec = synth.StageDecoder(W1=np.zeros((d, d), np.float32), b1=np.full(d, b1v, np.float32),
+                                 W2=np.ones((d, d), np.float32), b2=np.full(d, -0.0, np.float32))
+        tab = oracle.decoder_table(cfg, [dec])[0]
+        assert np.all(tab == 0.0)
+        assert not np.signbit(tab).any(), f"b1 = {b1v}: relu returned -0"
+
+
 # ---------------------------------------------------------------- protected path
 def test_q8_bounds_and_symmetry():
     r = _rng(50)
