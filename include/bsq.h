@@ -11,9 +11,10 @@
  * - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *   Every entry point that launches work is asynchronous on that stream.
  * - Arguments are validated on the host before anything is launched; a
- *   non-BSQ_OK return means nothing was enqueued. Device-side conditions
- *   (non-finite input) are reported through a device error word that the
- *   caller reads after synchronising.
+ *   non-BSQ_OK return means nothing was enqueued. Device-side conditions are
+ *   reported through a device error word (int32, caller-owned, zeroed by the
+ *   caller) into which the kernels OR the BSQ_DEVERR_* bits below; the caller
+ *   reads it after synchronising.
  * - No C++ exception crosses this boundary.
  * - Calls are re-entrant; two calls that share an output or workspace buffer
  *   on different streams race.
@@ -67,7 +68,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 4
+#define BSQ_ABI_VERSION 5
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -85,6 +86,25 @@ typedef enum {
     BSQ_ERR_DEVICE = 7,           /* a HIP launch or runtime call failed */
     BSQ_ERR_UNSUPPORTED = 8       /* valid configuration that this build does not implement */
 } bsq_status;
+
+/* Bits of a device error word.
+ *   NONFINITE  the weights hold NaN or Inf (bsq_encode, bsq_encode_with_set,
+ *              bsq_coupled_select);
+ *   BAD_SET    a given protected set is not strictly ascending or out of
+ *              range (bsq_encode_with_set);
+ *   TIMEOUT    a product's finishing workgroup gave up waiting for another
+ *              workgroup's partial result (never expected: workgroups run in
+ *              dispatch order, and the wait is bounded only so that a fault
+ *              elsewhere cannot hang the queue). The affected outputs are NaN
+ *              and the workspace is left POISONED;
+ *   POISONED   the workspace was marked by an earlier call that timed out: a
+ *              late partial may still sit in it, so nothing in it was used
+ *              and the outputs of this call are NaN. Zero-fill the workspace
+ *              (after synchronising) to use it again. */
+#define BSQ_DEVERR_NONFINITE 1
+#define BSQ_DEVERR_BAD_SET 2
+#define BSQ_DEVERR_TIMEOUT 4
+#define BSQ_DEVERR_POISONED 8
 
 typedef enum { BSQ_F32 = 0, BSQ_BF16 = 1 } bsq_dtype;
 
@@ -169,6 +189,15 @@ typedef enum { BSQ_OP_ENCODE = 0, BSQ_OP_GEMV = 1, BSQ_OP_GEMM = 2, BSQ_OP_SELEC
 /* Library ABI version (BSQ_ABI_VERSION). */
 int32_t bsq_version(void);
 
+/* Testing aid: the number of polls a product's finishing workgroup makes for
+ * another workgroup's partial result before it gives up (BSQ_DEVERR_TIMEOUT).
+ * 0 makes every such wait give up at once, so that the timeout and poison
+ * handling can be exercised with every kernel still exiting normally; a
+ * negative value restores the default (about a second of polling). Applies
+ * to calls issued afterwards (a captured graph keeps the value it was
+ * captured with); process-wide, host only. Returns the previous value. */
+int32_t bsq_debug_set_wait_limit(int32_t polls);
+
 /* Static description of a status code; never NULL. */
 const char *bsq_status_str(int32_t status);
 
@@ -220,7 +249,7 @@ bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec,
  *   out    host struct of device output buffers sized by bsq_layer_sizes
  *          (times n_mats); out->d_out/d_in/pitch/k/n_mats must match
  *   err    device int32 error word; the caller zeroes it before the call; the
- *          library ORs 1 into it when W holds NaN or Inf (BSQ_ERR_NONFINITE)
+ *          library ORs BSQ_DEVERR_NONFINITE into it when W holds NaN or Inf
  *   ws     device workspace of bsq_workspace_bytes(ENCODE) bytes, 256-aligned */
 bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, int32_t w_dtype,
                       int64_t n_mats, int64_t d_out, int64_t d_in, const float *g,
@@ -234,8 +263,8 @@ bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, i
  * columns and BSQ on the rest of every row. Row axis: int8 quantisation of
  * those rows (one scale per row, the absmax over the row / 127); BSQ on the
  * other rows with no position masked; the protected rows get code 0 and gain
- * +0. An invalid set ORs 2 into *err (and the outputs are unspecified); NaN
- * or Inf in W ORs 1. This is how the coupled set of bsq_coupled_select is
+ * +0. An invalid set ORs BSQ_DEVERR_BAD_SET into *err (and the outputs are
+ * unspecified); NaN or Inf in W ORs BSQ_DEVERR_NONFINITE. This is how the coupled set of bsq_coupled_select is
  * applied to the gate and up rows (axis 1) and the down columns (axis 0).
  * `g` is not used. Other arguments as for bsq_encode. With protect_axis = 1
  * and k > 0: d_out <= 2^18 and n_mats <= 65535 (BSQ_ERR_UNSUPPORTED beyond;
@@ -259,7 +288,7 @@ bsq_status bsq_encode_with_set(const bsq_config *cfg, const void *codec, const v
  *                 (taken by magnitude)
  *   idx           device int32 [k] output
  *   scores        device fp64 [d_ffn] output of S, or NULL
- *   err           device int32 error word (caller zeroes it); ORs 1 on NaN
+ *   err           device int32 error word (caller zeroes it); ORs BSQ_DEVERR_NONFINITE on NaN
  *                 or Inf in a weight
  *   ws            device workspace of bsq_workspace_bytes(SELECT, 1, d_ffn,
  *                 d_model) bytes, 256-byte aligned
@@ -278,6 +307,19 @@ bsq_status bsq_coupled_select(const bsq_config *cfg, const void *W_gate, const v
 bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
                       void *W_hat, int32_t out_dtype, void *stream);
 
+/* One residual stage of a sequential decode, fp32 output (the stage-by-stage
+ * form that eq. parallel_stage_decode replaces with one stage-parallel pass;
+ * Section III-G compares the two as engineering cost):
+ *   W_hat[i][j] = fmaf(gain_s, D_s(code_s)[j], accumulate ? W_hat[i][j] : 0)
+ * over the unprotected positions of stage `stage` (0 <= stage < stages); the
+ * call for the last stage then writes the protected columns (or rows) from
+ * the int8 payload. Calling it for stage = 0 .. stages-1, with accumulate = 0
+ * then 1, leaves in W_hat the bits bsq_decode writes with BSQ_F32 output, at
+ * the cost of one launch and one fp32 read-modify-write of W_hat per stage.
+ *   W_hat  device fp32 [n_mats][d_out][d_in], 16-byte aligned */
+bsq_status bsq_decode_stage(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
+                            int32_t stage, int32_t accumulate, void *W_hat, void *stream);
+
 /* Fused decode-GEMV for a group of n matrices that read the same x (for
  * example q/k/v or gate/up), batch 1, without forming W_hat:
  *   y_g = W_hat_g x + B_g (A_g x)    for g = 0 .. n-1
@@ -292,13 +334,16 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
  *   x       device [d_in], bf16 (16-byte aligned) or fp32 (x_dtype)
  *   y       host array [n] of device outputs [d_out_g], y_dtype (bf16 or fp32)
  *   ws      device workspace of bsq_workspace_bytes(GEMV, n, max d_out, d_in),
- *           256-byte aligned, ZERO-FILLED before its first use: it holds the
- *           LoRA vectors A_g x, the folded activations of the d = 16
- *           symmetric decoder (see bsq_gemv_prepare) and flagged per-row
- *           partial sums that every call leaves at zero again. A workspace
- *           serves calls of one configuration and one d_in (any group size
- *           and d_out it was sized for); calls that share a workspace must
- *           not overlap.
+ *           256-byte aligned, ZERO-FILLED before its first use: a 256-byte
+ *           header (its first word is the poison word), the LoRA vectors
+ *           A_g x, the folded activations of the d = 16 symmetric decoder
+ *           (see bsq_gemv_prepare) and flagged per-row partial sums that
+ *           every call leaves at zero again. A workspace serves calls of one
+ *           configuration and one d_in (any group size and d_out it was sized
+ *           for); calls that share a workspace must not overlap.
+ *   err     device int32 error word or NULL: TIMEOUT and POISONED (see
+ *           BSQ_DEVERR_*) are ORed into it; without it those conditions
+ *           still give NaN outputs and a poisoned workspace
  * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
  * fp32 decoder table and fp32 arithmetic throughout. With protect_axis = 1
  * the coded rows come from the streaming kernels and each protected row is
@@ -308,7 +353,7 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
 bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
                     const bsq_layer *layers, const bsq_lora *loras,
                     const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
-                    void *ws, size_t ws_bytes, void *stream);
+                    void *ws, size_t ws_bytes, int32_t *err, void *stream);
 
 /* Activation preparation of the GEMV: work that needs a reduction over all
  * of x, written into `ws` (one launch):
@@ -333,23 +378,30 @@ bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const 
  * bsq_gemv_prepare (same group, same x) left in `ws` on the same stream.
  * With bf16 x at d = 8 (and d = 16 with the width-16 symmetric decoder) the
  * LoRA vectors are computed inside this launch. Limits of the bf16 path:
- * d_in <= 65536 and k <= 4096. */
+ * d_in <= 65536 and k <= 4096. `err` as for bsq_gemv. */
 bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs,
                         const bsq_layer *layers, const bsq_lora *loras, const void *x,
                         int32_t x_dtype, void *const *y, int32_t y_dtype, void *ws,
-                        size_t ws_bytes, void *stream);
+                        size_t ws_bytes, int32_t *err, void *stream);
 
-/* Fused decode-GEMM for M tokens (decode one weight tile to bf16 in LDS,
- * then MFMA), Y = X W_hat^T + (X A^T) B^T:
+/* Fused decode-GEMM for M tokens, Y = X W_hat^T + (X A^T) B^T: the batched
+ * form of the product bsq_gemv computes (the direct computation from the
+ * binary codes that Section V names as future work; stage sum of
+ * eq. parallel_stage_decode, protected term of eq. protected_8bit_scatter,
+ * LoRA term of Section III-F). Each lane decodes its weight fragments from
+ * the code and gain planes straight into bf16 MFMA operands (fp16 decoder
+ * tables in LDS, fp32 fma over the stages), so W_hat is never formed:
  *   X  device bf16 [M][ldx] (ldx >= d_in, multiple of 8)
  *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
  *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M),
- *      256-byte aligned, ZERO-FILLED before its first use: its first 8 MiB
- *      hold the flagged fp32 partial tiles of the split-K reduction, which
- *      every call leaves at zero again; the rest is scratch (X with the
- *      protected columns zeroed, the gathered protected activations, X A^T).
- *      One workspace serves GEMM calls of any shape; it must not be shared
- *      with a GEMV workspace, and calls that share it must not overlap.
+ *      256-byte aligned, ZERO-FILLED before its first use: a 256-byte header
+ *      (its first word is the poison word), then 8 MiB of flagged fp32
+ *      partial tiles of the split-K reduction, which every call leaves at
+ *      zero again; the rest is scratch (X with the protected columns zeroed,
+ *      the gathered protected activations, X A^T). One workspace serves GEMM
+ *      calls of any shape; it must not be shared with a GEMV workspace, and
+ *      calls that share it must not overlap.
+ *   err device int32 error word or NULL, as for bsq_gemv.
  * The K steps of a tile may be split over several blocks; their fp32
  * partials are summed in a fixed order, so results are deterministic. With
  * protect_axis = 1 each protected row's column of Y is written afterwards as
@@ -358,7 +410,7 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer,
                     const bsq_lora *lora, const void *X, int32_t x_dtype, int64_t M,
                     int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,
-                    void *ws, size_t ws_bytes, void *stream);
+                    void *ws, size_t ws_bytes, int32_t *err, void *stream);
 
 #ifdef __cplusplus
 }

@@ -28,6 +28,7 @@ BSQ_ERR_BUFFER_TOO_SMALL, BSQ_ERR_NONFINITE, BSQ_ERR_DEVICE, BSQ_ERR_UNSUPPORTED
 BSQ_F32, BSQ_BF16 = 0, 1
 DEC_IDENTITY, DEC_LINEAR, DEC_MLP = 0, 1, 2
 OP_ENCODE, OP_GEMV, OP_GEMM, OP_SELECT = 0, 1, 2, 3
+DEVERR_NONFINITE, DEVERR_BAD_SET, DEVERR_TIMEOUT, DEVERR_POISONED = 1, 2, 4, 8
 
 
 class BsqError(RuntimeError):
@@ -71,10 +72,11 @@ class bsq_sizes(ct.Structure):
 
 EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes", "bsq_workspace_bytes",
            "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemv_prepare",
-           "bsq_gemv_run", "bsq_gemm", "bsq_encode_with_set", "bsq_coupled_select")
+           "bsq_gemv_run", "bsq_gemm", "bsq_encode_with_set", "bsq_coupled_select",
+           "bsq_debug_set_wait_limit", "bsq_decode_stage")
 
 # struct layouts above follow this version of include/bsq.h
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 _lib = None
 
@@ -99,10 +101,12 @@ def lib():
     L.bsq_codec_prepare.argtypes = [P, P, P, SZ, P]
     L.bsq_encode.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
     L.bsq_decode.argtypes = [P, P, P, P, I32, P]
-    L.bsq_gemv.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
+    L.bsq_gemv.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P, P]
     L.bsq_gemv_prepare.argtypes = [P, I32, P, P, P, P, I32, P, SZ, P]
-    L.bsq_gemv_run.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P]
-    L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P]
+    L.bsq_gemv_run.argtypes = [P, I32, P, P, P, P, I32, P, I32, P, SZ, P, P]
+    L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P, P]
+    L.bsq_debug_set_wait_limit.argtypes = [I32]
+    L.bsq_decode_stage.argtypes = [P, P, P, I32, I32, P, P]
     L.bsq_encode_with_set.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
     L.bsq_coupled_select.argtypes = [P, P, P, P, I32, I64, I64, P, P, P, P, P, P, P, SZ, P]
     for f in EXPORTS[2:]:
@@ -445,6 +449,17 @@ def bsq_decode(cfg: Config, codec: Codec, layer: Layer, dtype=torch.float32, out
     return out
 
 
+def bsq_decode_stage(cfg: Config, codec: Codec, layer: Layer, stage: int, accumulate: bool, out: torch.Tensor,
+                     stream=None) -> torch.Tensor:
+    """One residual stage of a sequential decode into the fp32 `out`
+    (bsq_decode_stage); stages 0 .. S-1, accumulating from stage 1, give the
+    bits of bsq_decode."""
+    c, L = cfg.c(), layer.c()
+    _check(lib().bsq_decode_stage(ct.byref(c), ct.c_void_p(codec.ptr()), ct.byref(L), int(stage), int(accumulate),
+                                  _ptr(out), _stream(stream)), "bsq_decode_stage")
+    return out
+
+
 def _lora_struct(lora) -> bsq_lora:
     if lora is None:
         return bsq_lora(None, None, 0)
@@ -457,7 +472,7 @@ class GemvPlan:
     calls (and inside a HIP-graph capture) with the same buffers."""
 
     def __init__(self, cfg: Config, codecs, layers, x: torch.Tensor, loras=None, y_dtype=torch.bfloat16,
-                 out=None, ws=None):
+                 out=None, ws=None, err=None):
         n = len(layers)
         if not (1 <= n <= MAX_GROUP) or len(codecs) != n:
             raise ValueError("group size must be 1..8 with one codec per layer")
@@ -466,8 +481,9 @@ class GemvPlan:
         self.layers, self.codecs, self.loras = layers, codecs, loras
         self.out = out if out is not None else [torch.empty(L.d_out, dtype=y_dtype, device=dev) for L in layers]
         need = bsq_workspace_bytes(cfg, OP_GEMV, n, max(L.d_out for L in layers), layers[0].d_in)
-        # zero-filled once: the kernels leave their arrival counters at zero
+        # zero-filled once: the kernels leave their flagged slots at zero
         self.ws = ws if ws is not None else _empty_aligned(need, dev, zero=True)
+        self.err = err  # device int32 error word (TIMEOUT / POISONED bits), or None
         self._c = cfg.c()
         self._codecs = (ct.c_void_p * n)(*[cd.ptr() for cd in codecs])
         self._layers = (bsq_layer * n)(*[L.c() for L in layers])
@@ -478,8 +494,8 @@ class GemvPlan:
 
     def __call__(self, stream=None):
         _check(lib().bsq_gemv(ct.byref(self._c), self.n, self._codecs, self._layers, self._loras, _ptr(self.x),
-                              self._xd, self._y, self._yd, _ptr(self.ws), self.ws.numel(), _stream(stream)),
-               "bsq_gemv")
+                              self._xd, self._y, self._yd, _ptr(self.ws), self.ws.numel(), _ptr(self.err),
+                              _stream(stream)), "bsq_gemv")
         return self.out
 
     def prepare(self, stream=None):
@@ -493,12 +509,12 @@ class GemvPlan:
         """bsq_gemv_run: the streaming product over the prepared workspace."""
         _check(lib().bsq_gemv_run(ct.byref(self._c), self.n, self._codecs, self._layers, self._loras,
                                   _ptr(self.x), self._xd, self._y, self._yd, _ptr(self.ws), self.ws.numel(),
-                                  _stream(stream)), "bsq_gemv_run")
+                                  _ptr(self.err), _stream(stream)), "bsq_gemv_run")
         return self.out
 
 
 def bsq_gemv(cfg: Config, codecs, layers, x: torch.Tensor, loras=None, y_dtype=torch.bfloat16, out=None,
-             ws=None, stream=None):
+             ws=None, stream=None, err=None):
     """Grouped fused decode-GEMV: returns [W_hat_g x + B_g A_g x for each layer g]."""
     if isinstance(layers, Layer):
         layers, codecs = [layers], [codecs]
@@ -506,13 +522,13 @@ def bsq_gemv(cfg: Config, codecs, layers, x: torch.Tensor, loras=None, y_dtype=t
         single = True
     else:
         single = False
-    plan = GemvPlan(cfg, codecs, layers, x.contiguous(), loras, y_dtype, out, ws)
+    plan = GemvPlan(cfg, codecs, layers, x.contiguous(), loras, y_dtype, out, ws, err)
     ys = plan(stream)
     return ys[0] if single else ys
 
 
 def bsq_gemm(cfg: Config, codec: Codec, layer: Layer, X: torch.Tensor, lora=None, y_dtype=torch.bfloat16,
-             out=None, ws=None, stream=None) -> torch.Tensor:
+             out=None, ws=None, stream=None, err=None) -> torch.Tensor:
     """Fused decode-GEMM: Y = X W_hat^T + (X A^T) B^T for X [M, d_in] bf16."""
     M, d_in = X.shape
     dev = X.device
@@ -523,5 +539,12 @@ def bsq_gemm(cfg: Config, codec: Codec, layer: Layer, X: torch.Tensor, lora=None
     lo = _lora_struct(lora)
     _check(lib().bsq_gemm(ct.byref(c), ct.c_void_p(codec.ptr()), ct.byref(L), ct.byref(lo), _ptr(X),
                           _dtype_code(X.dtype), M, X.stride(0), _ptr(out), _dtype_code(out.dtype), out.stride(0),
-                          _ptr(ws), ws.numel(), _stream(stream)), "bsq_gemm")
+                          _ptr(ws), ws.numel(), _ptr(err), _stream(stream)), "bsq_gemm")
     return out
+
+
+def bsq_debug_set_wait_limit(polls: int) -> int:
+    """Testing aid (bsq_debug_set_wait_limit): polls before a product's
+    finishing workgroup gives up waiting; 0 forces every such wait to give
+    up, a negative value restores the default. Returns the previous value."""
+    return int(lib().bsq_debug_set_wait_limit(int(polls)))

@@ -114,11 +114,28 @@ bsq_status check_lora(const bsq_lora *l)
 
 bsq_status from_hip(hipError_t e) { return e == hipSuccess ? BSQ_OK : BSQ_ERR_DEVICE; }
 
+// polls before a finishing workgroup's wait gives up: about a second of
+// s_sleep polling by default (never expected to be reached, since workgroups
+// run in dispatch order); bsq_debug_set_wait_limit changes it
+constexpr int32_t DEFAULT_WAIT_LIMIT = 1 << 22;
+int32_t g_wait_limit = DEFAULT_WAIT_LIMIT;
+
 }  // namespace
+
+namespace bsq {
+int wait_limit() { return __atomic_load_n(&g_wait_limit, __ATOMIC_RELAXED); }
+}  // namespace bsq
 
 extern "C" {
 
 int32_t bsq_version(void) { return BSQ_ABI_VERSION; }
+
+int32_t bsq_debug_set_wait_limit(int32_t polls)
+{
+    const int32_t prev = __atomic_load_n(&g_wait_limit, __ATOMIC_RELAXED);
+    __atomic_store_n(&g_wait_limit, polls < 0 ? DEFAULT_WAIT_LIMIT : polls, __ATOMIC_RELAXED);
+    return prev;
+}
 
 const char *bsq_status_str(int32_t s)
 {
@@ -323,6 +340,24 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
     return from_hip(launch_decode_rows(*layer, W_hat, out_dtype, st));
 }
 
+bsq_status bsq_decode_stage(const bsq_config *cfg, const void *codec, const bsq_layer *layer, int32_t stage,
+                            int32_t accumulate, void *W_hat, void *stream)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!codec || !layer) return BSQ_ERR_ARG;
+    if (!W_hat && layer->d_out > 0) return BSQ_ERR_ARG;
+    if (stage < 0 || stage >= cfg->stages || (accumulate != 0 && accumulate != 1)) return BSQ_ERR_ARG;
+    if ((s = check_layer(*cfg, layer, true, false)) != BSQ_OK) return s;
+    if (!aligned(W_hat, 16) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bsq_layer coded = coded_layer(*cfg, *layer);
+    if ((s = from_hip(launch_decode_stage(coded_cfg(*cfg), codec, coded, stage, accumulate, W_hat, st))) != BSQ_OK)
+        return s;
+    if (!row_axis(*cfg) || stage != cfg->stages - 1) return BSQ_OK;
+    return from_hip(launch_decode_rows(*layer, W_hat, BSQ_F32, st));
+}
+
 namespace {
 
 bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
@@ -389,16 +424,17 @@ bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const 
 
 bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
                         const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
-                        void *ws, size_t ws_bytes, void *stream)
+                        void *ws, size_t ws_bytes, int32_t *err, void *stream)
 {
     if (!codecs || !y || !x) return BSQ_ERR_ARG;
     bsq_status s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, y, y_dtype, ws, ws_bytes);
     if (s != BSQ_OK) return s;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
+    if (err && !aligned(err, 4)) return BSQ_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const CodedGroup g(*cfg, n, layers);
-    if ((s = from_hip(launch_gemv_run(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, st))) !=
-        BSQ_OK)
+    if ((s = from_hip(launch_gemv_run(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, err,
+                                      st))) != BSQ_OK)
         return s;
     if (!row_axis(*cfg)) return BSQ_OK;
     return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
@@ -406,17 +442,18 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
 
 bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
                     const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
-                    void *ws, size_t ws_bytes, void *stream)
+                    void *ws, size_t ws_bytes, int32_t *err, void *stream)
 {
     if (!codecs || !y || !x) return BSQ_ERR_ARG;
     bsq_status s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, y, y_dtype, ws, ws_bytes);
     if (s != BSQ_OK) return s;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
+    if (err && !aligned(err, 4)) return BSQ_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bsq_config cc = coded_cfg(*cfg);
     const CodedGroup g(*cfg, n, layers);
     if ((s = from_hip(launch_gemv_prep(cc, n, codecs, g.L, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
-    if ((s = from_hip(launch_gemv_run(cc, n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, st))) != BSQ_OK)
+    if ((s = from_hip(launch_gemv_run(cc, n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, err, st))) != BSQ_OK)
         return s;
     if (!row_axis(*cfg)) return BSQ_OK;
     return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
@@ -424,7 +461,7 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
 
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer, const bsq_lora *lora,
                     const void *X, int32_t x_dtype, int64_t M, int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,
-                    void *ws, size_t ws_bytes, void *stream)
+                    void *ws, size_t ws_bytes, int32_t *err, void *stream)
 {
     bsq_status s = check_cfg(cfg);
     if (s != BSQ_OK) return s;
@@ -438,6 +475,7 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     if (M < 0 || ldx < layer->d_in || ldy < layer->d_out || ldx % 8 != 0) return BSQ_ERR_SHAPE;
     if (!aligned(X, 16) || !aligned(ws, 256) || !aligned(codec, 256)) return BSQ_ERR_ALIGN;
     if (!aligned(Y, y_dtype == BSQ_F32 ? 4 : 2)) return BSQ_ERR_ALIGN;
+    if (err && !aligned(err, 4)) return BSQ_ERR_ALIGN;
     const bsq_config cc = coded_cfg(*cfg);
     if (ws_bytes < gemm_ws_bytes(cc, layer->d_out, layer->d_in, M)) return BSQ_ERR_BUFFER_TOO_SMALL;
     const bool rows = row_axis(*cfg);
@@ -446,7 +484,8 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     if (rows && (M + 3) / 4 > 65535) return BSQ_ERR_UNSUPPORTED;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const bsq_layer coded = coded_layer(*cfg, *layer);
-    if ((s = from_hip(launch_gemm(cc, codec, coded, lora, X, M, ldx, Y, y_dtype, ldy, ws, st))) != BSQ_OK) return s;
+    if ((s = from_hip(launch_gemm(cc, codec, coded, lora, X, M, ldx, Y, y_dtype, ldy, ws, err, st))) != BSQ_OK)
+        return s;
     if (!rows) return BSQ_OK;
     return from_hip(launch_gemm_rows(*layer, lora, X, M, ldx, Y, y_dtype, ldy, gemm_lora_t(ws), st));
 }

@@ -156,17 +156,25 @@ const float *gemm_lora_t(const void *ws);
 
 hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
                          void *w_hat, int out_dtype, hipStream_t st);
+hipError_t launch_decode_stage(const bsq_config &cfg, const void *codec, const bsq_layer &layer, int stage,
+                               int accumulate, void *w_hat, hipStream_t st);
 
 size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in);
 hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                             const bsq_lora *loras, const void *x, int x_dtype, void *ws, hipStream_t st);
 hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                            const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
-                           void *ws, hipStream_t st);
+                           void *ws, int32_t *err, hipStream_t st);
 
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M);
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &layer,
                        const bsq_lora *lora, const void *X, int64_t M, int64_t ldx, void *Y,
-                       int y_dtype, int64_t ldy, void *ws, hipStream_t st);
+                       int y_dtype, int64_t ldy, void *ws, int32_t *err, hipStream_t st);
+
+// Polls a finishing workgroup makes for another workgroup's partial result
+// before it gives up (reports BSQ_DEVERR_TIMEOUT and poisons the workspace).
+// Workgroups run in dispatch order, so the wait is never expected to give
+// up; bsq_debug_set_wait_limit lowers the bound so that tests can force it.
+int wait_limit();
 
 }  // namespace bsq

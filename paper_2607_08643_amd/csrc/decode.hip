@@ -20,6 +20,8 @@ struct DecodeArgs {
     const int8_t *q8;
     const float *scale;
     void *out;
+    int accumulate;  // start each element from the fp32 value already in out (sequential stages)
+    int scatter;     // write the protected columns (the last stage of a sequential decode)
 };
 
 // A block walks the tiles of one matrix (grid-stride, so the decoder tables
@@ -94,9 +96,24 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int64_t c = cb * 16 + cc0 + u;
+            const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
+            const bool live = i < a.d_out && c < a.C;
             float v[D];
 #pragma unroll
             for (int j = 0; j < D; ++j) v[j] = 0.0f;
+            if constexpr (!BF16OUT) {
+                if (a.accumulate && live) {  // the running stage sum of the earlier launches
+                    const float4 *src = reinterpret_cast<const float4 *>(static_cast<const float *>(a.out) + o);
+#pragma unroll
+                    for (int q = 0; q < D / 4; ++q) {
+                        const float4 w4 = src[q];
+                        v[4 * q + 0] = w4.x;
+                        v[4 * q + 1] = w4.y;
+                        v[4 * q + 2] = w4.z;
+                        v[4 * q + 3] = w4.w;
+                    }
+                }
+            }
 #pragma unroll
             for (int s = 0; s < S; ++s) {
                 uint32_t cw;
@@ -115,8 +132,8 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
                     v[4 * q + 3] = __builtin_fmaf(g, tv.w, v[4 * q + 3]);
                 }
             }
-            if (i >= a.d_out || c >= a.C) continue;
-            if (a.k > 0) {
+            if (!live) continue;
+            if (a.k > 0 && a.scatter) {
                 const int64_t col0 = c * D;
                 const uint32_t word = s_bits[col0 >> 5];
                 const uint32_t pm = (word >> (col0 & 31)) & ((1u << D) - 1u);
@@ -131,7 +148,6 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
                     }
                 }
             }
-            const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
             if constexpr (BF16OUT) {
                 uint32_t h[D / 2];
 #pragma unroll
@@ -206,12 +222,41 @@ hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_lay
     a.q8 = L.prot_q8;
     a.scale = L.prot_scale;
     a.out = w_hat;
+    a.scatter = 1;
     const bool bf = (out_dtype == BSQ_BF16);
     if (cfg.d == 8)
         return bf ? launch_decode_t<8, true>(cfg.stages, a, L.n_mats, st)
                   : launch_decode_t<8, false>(cfg.stages, a, L.n_mats, st);
     return bf ? launch_decode_t<16, true>(cfg.stages, a, L.n_mats, st)
               : launch_decode_t<16, false>(cfg.stages, a, L.n_mats, st);
+}
+
+// One residual stage of a sequential decode: W_hat = fmaf(gain, D_s(code),
+// W_hat or 0) over the stage's plane, the protected columns written with the
+// last stage. Called for s = 0 .. S-1 (accumulating from s = 1) it gives the
+// bits of the stage-parallel decode, one launch and one fp32 round trip of
+// W_hat per stage.
+hipError_t launch_decode_stage(const bsq_config &cfg, const void *codec, const bsq_layer &L, int stage,
+                               int accumulate, void *w_hat, hipStream_t st)
+{
+    DecodeArgs a{};
+    a.d_out = L.d_out;
+    a.d_in = L.d_in;
+    a.pitch = L.pitch;
+    a.C = L.d_in / cfg.d;
+    a.k = L.k;
+    a.words = (L.k > 0) ? (L.d_in + 31) / 32 : 0;
+    const char *cb = static_cast<const char *>(codec);
+    a.codes[0] = L.codes[stage];
+    a.gains[0] = L.gains[stage];
+    a.tab32[0] = reinterpret_cast<const float *>(cb + codec_tab32_offset(cfg, stage));
+    a.idx = L.prot_idx;
+    a.q8 = L.prot_q8;
+    a.scale = L.prot_scale;
+    a.out = w_hat;
+    a.accumulate = accumulate;
+    a.scatter = (stage == cfg.stages - 1);
+    return (cfg.d == 8) ? launch_decode_t<8, false>(1, a, L.n_mats, st) : launch_decode_t<16, false>(1, a, L.n_mats, st);
 }
 
 }  // namespace bsq

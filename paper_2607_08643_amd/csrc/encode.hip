@@ -84,7 +84,7 @@ __global__ __launch_bounds__(256) void colscore_kernel(const T *__restrict__ W, 
     absmax[m * d_in + col] = mx;
     // a NaN or Inf makes the fp64 sum non-finite (squares of finite fp32
     // values cannot overflow it)
-    if (err && !__builtin_isfinite(s)) atomicOr(err, 1);
+    if (err && !__builtin_isfinite(s)) atomicOr(err, int32_t(BSQ_DEVERR_NONFINITE));
 }
 
 // ---------------------------------------------------------------------------
@@ -138,7 +138,7 @@ __global__ __launch_bounds__(256) void rowscore_kernel(const T *__restrict__ W, 
     }
     keys[m * n_rows + row] = s;
     absmax[m * n_rows + row] = mx;
-    if (err && !__builtin_isfinite(s)) atomicOr(err, 1);
+    if (err && !__builtin_isfinite(s)) atomicOr(err, int32_t(BSQ_DEVERR_NONFINITE));
 }
 
 // Coupled MLP score of channel j (eq. mlp_coupled_protection) from the three
@@ -334,7 +334,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void colset_kernel(const int32_t *__r
         const int32_t j = idx_in[m * k + p];
         const bool ok = j >= 0 && j < d_in && (p == 0 || idx_in[m * k + p - 1] < j);
         if (!ok) {
-            atomicOr(err, 2);
+            atomicOr(err, int32_t(BSQ_DEVERR_BAD_SET));
             continue;
         }
         colmap_all[m * d_in + j] = int32_t(p);
@@ -376,7 +376,7 @@ __global__ __launch_bounds__(256) void rowprot_kernel(const RowProtArgs a)
     const int32_t i = a.idx_in[m * a.k + p];
     const bool ok = i >= 0 && i < a.d_out && (p == 0 || a.idx_in[m * a.k + p - 1] < i);
     if (!ok) {
-        if (t == 0) atomicOr(a.err, 2);
+        if (t == 0) atomicOr(a.err, int32_t(BSQ_DEVERR_BAD_SET));
         return;
     }
     const T *row = static_cast<const T *>(a.W) + (m * a.d_out + i) * a.d_in;
@@ -476,7 +476,7 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
     bool finite = true;
 #pragma unroll
     for (int j = 0; j < D; ++j) finite &= __builtin_isfinite(w[j]);
-    if (!finite) atomicOr(a.err, 1);
+    if (!finite) atomicOr(a.err, int32_t(BSQ_DEVERR_NONFINITE));
 
     // zero padding of the row's int8 payload
     if (c == 0) {

@@ -42,14 +42,15 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 128;    // inputs per K step
 
-// The flagged partial slots sit at a fixed place, the first GEMM_SLOT_BYTES
-// of the workspace, whatever the shape: every call leaves them at zero, and
-// no other data of any GEMM call is ever written there, so one workspace
-// serves calls of different shapes. The K split is capped to fit.
+// The workspace starts with a 256-byte header whose first word is the
+// poison word (nonzero once a call gave up waiting for a partial tile and
+// left flagged slots behind). The flagged partial slots follow at a fixed
+// place, GEMM_SLOT_BYTES from offset GEMM_HDR, whatever the shape: every
+// call leaves them at zero, and no other data of any GEMM call is ever
+// written there, so one workspace serves calls of different shapes. The K
+// split is capped to fit.
+constexpr int64_t GEMM_HDR = 256;
 constexpr int64_t GEMM_SLOT_BYTES = int64_t(8) << 20;
-// polls of the finishing split for the other splits' slots before it gives
-// up and writes NaN (seconds; never expected)
-constexpr int GEMM_SPIN_LIMIT = 1 << 22;
 
 struct GemmArgs {
     const void *codes[BSQ_MAX_STAGES];
@@ -68,7 +69,25 @@ struct GemmArgs {
     int y_vec;         // Y 16-byte aligned with 16-byte row pitch: vector stores
     int ksplit;        // blocks per tile along K (grid z)
     uint64_t *slots;   // [tiles][ksplit - 1][BM * BN] flagged partials, zero between calls
+    uint32_t *poison;  // the workspace's poison word
+    int32_t *err;      // caller's device error word, or null
+    int spin_limit;    // polls before a wait gives up (wait_limit())
 };
+
+// The finishing block's outcome when it could not use the other blocks'
+// partials: lane 0 reports it in the caller's error word, and after a
+// give-up marks the workspace so that no later call consumes a flag a late
+// block may still set.
+__device__ __forceinline__ void gemm_report(const GemmArgs &a, bool poisoned, bool timed_out)
+{
+    if ((threadIdx.x & 63) != 0) return;
+    if (poisoned) {
+        if (a.err) atomicOr(a.err, int32_t(BSQ_DEVERR_POISONED));
+    } else if (timed_out) {
+        __hip_atomic_store(a.poison, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (a.err) atomicOr(a.err, int32_t(BSQ_DEVERR_TIMEOUT));
+    }
+}
 
 // ---------------------------------------------------------------------------
 // Prep: one workgroup per (padded token row m < Mp, block of PREP_COLS X~
@@ -89,23 +108,28 @@ struct PrepArgs {
 
 __global__ __launch_bounds__(256) void gemm_prep(const PrepArgs a)
 {
-    // workgroup (m, cb): token row m < Mp, X~ columns [2048 cb, 2048 cb + 2048)
+    // workgroup (m, y): token row m < Mp; y < ncb: X~ columns [2048 y, 2048 y
+    // + 2048); y == ncb: the gathered protected activations (and the zero
+    // LoRA entries past the rank); y = ncb + 1 + r: T[m][r] for rank index r
     __shared__ uint32_t s_bits[PREP_COLS / 32];  // protected bitmap of the column block
-    __shared__ float s_red[BSQ_MAX_LORA_RANK][4];
+    __shared__ float s_red[4];
     const int t = threadIdx.x;
-    const int64_t m = blockIdx.x, c0 = int64_t(blockIdx.y) * PREP_COLS;
+    const int64_t m = blockIdx.x;
+    const int64_t ncb = (a.Kp + PREP_COLS - 1) / PREP_COLS;
+    const int64_t y = blockIdx.y;
     const bool live = m < a.M;
-    if (t < PREP_COLS / 32) s_bits[t] = 0u;
-    __syncthreads();
-    for (int64_t p = t; p < a.k; p += 256) {
-        const int32_t j = a.idx[p];
-        if (j >= 0 && j < a.d_in && j >= c0 && j < c0 + PREP_COLS) atomicOr(&s_bits[(j - c0) >> 5], 1u << (j & 31));
-    }
-    __syncthreads();
     const uint16_t *xr = a.X + m * a.ldx;
-    // X~: one 8-input segment per thread; protected inputs, inputs past d_in
-    // and rows past M are zero
-    {
+    if (y < ncb) {
+        const int64_t c0 = y * PREP_COLS;
+        if (t < PREP_COLS / 32) s_bits[t] = 0u;
+        __syncthreads();
+        for (int64_t p = t; p < a.k; p += 256) {
+            const int32_t j = a.idx[p];
+            if (j >= 0 && j < a.d_in && j >= c0 && j < c0 + PREP_COLS) atomicOr(&s_bits[(j - c0) >> 5], 1u << (j & 31));
+        }
+        __syncthreads();
+        // X~: one 8-input segment per thread; protected inputs, inputs past
+        // d_in and rows past M are zero
         const int64_t j0 = c0 + 8 * t;
         if (j0 < a.Kp) {
             u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
@@ -122,40 +146,57 @@ __global__ __launch_bounds__(256) void gemm_prep(const PrepArgs a)
             }
             *reinterpret_cast<u32x4_t *>(a.Xt + m * a.Kp + j0) = v;
         }
+        return;
     }
-    if (blockIdx.y != 0) return;
-    // gathered protected activations, zero past k
-    for (int64_t p = t; p < a.kp32; p += 256) {
-        uint16_t v = 0;
-        if (live && p < a.k) {
-            const int32_t j = a.idx[p];
-            if (j >= 0 && j < a.d_in) v = xr[j];
-        }
-        a.Xp[m * a.kp32 + p] = v;
-    }
-    // T[m][r] = sum_j X[m][j] A[r][j] (fp32), rows past M zero
-    if (a.rank > 0) {
-        float acc[BSQ_MAX_LORA_RANK];
-#pragma unroll
-        for (int r = 0; r < BSQ_MAX_LORA_RANK; ++r) acc[r] = 0.0f;
-        if (live)
-            for (int64_t j = t; j < a.d_in; j += 256) {
-                const float x = bf16_to_f32(xr[j]);
-#pragma unroll
-                for (int r = 0; r < BSQ_MAX_LORA_RANK; ++r)
-                    if (r < a.rank) acc[r] = __builtin_fmaf(x, bf16_to_f32(a.A[int64_t(r) * a.d_in + j]), acc[r]);
+    if (y == ncb) {
+        // gathered protected activations, zero past k
+        for (int64_t p = t; p < a.kp32; p += 256) {
+            uint16_t v = 0;
+            if (live && p < a.k) {
+                const int32_t j = a.idx[p];
+                if (j >= 0 && j < a.d_in) v = xr[j];
             }
-        const int lane = t & 63, wave = t >> 6;
-#pragma unroll
-        for (int r = 0; r < BSQ_MAX_LORA_RANK; ++r) {
-            float v = acc[r];
-            for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-            if (lane == 0) s_red[r][wave] = v;
+            a.Xp[m * a.kp32 + p] = v;
         }
-        __syncthreads();
-        if (t < BSQ_MAX_LORA_RANK)
-            a.T[m * BSQ_MAX_LORA_RANK + t] = (t < a.rank) ? ((s_red[t][0] + s_red[t][1]) + (s_red[t][2] + s_red[t][3])) : 0.0f;
+        // LoRA entries past the rank (all of them without an adapter) are zero
+        if (t >= a.rank && t < BSQ_MAX_LORA_RANK) a.T[m * BSQ_MAX_LORA_RANK + t] = 0.0f;
+        return;
     }
+    // T[m][r] = sum_j X[m][j] A[r][j] (fp32, exact bf16 products), rows past M
+    // zero: eight inputs per 16-byte load where the row of A is 16-byte
+    // aligned, four loads per thread in flight, element by element elsewhere
+    const int r = int(y - ncb - 1);
+    const uint16_t *ar = a.A + int64_t(r) * a.d_in;
+    float acc = 0.0f;
+    if (live) {
+        const bool vec = (reinterpret_cast<uintptr_t>(ar) & 15) == 0;
+        const int64_t n8 = vec ? a.d_in / 8 : 0;
+        for (int64_t p0 = t; p0 < n8; p0 += 4 * 256) {
+            u32x4_t av[4], xv[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t p = (p0 + u * 256 < n8) ? p0 + u * 256 : n8 - 1;
+                av[u] = reinterpret_cast<const u32x4_t *>(ar)[p];
+                xv[u] = reinterpret_cast<const u32x4_t *>(xr)[p];
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (p0 + u * 256 >= n8) break;
+#pragma unroll
+                for (int h = 0; h < 4; ++h) {
+                    acc = __builtin_fmaf(__uint_as_float(av[u][h] << 16), __uint_as_float(xv[u][h] << 16), acc);
+                    acc = __builtin_fmaf(__uint_as_float(av[u][h] & 0xffff0000u), __uint_as_float(xv[u][h] & 0xffff0000u),
+                                         acc);
+                }
+            }
+        }
+        for (int64_t j = n8 * 8 + t; j < a.d_in; j += 256) acc = __builtin_fmaf(bf16_to_f32(xr[j]), bf16_to_f32(ar[j]), acc);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if ((t & 63) == 0) s_red[t >> 6] = acc;
+    __syncthreads();
+    if (t == 0) a.T[m * BSQ_MAX_LORA_RANK + r] = (s_red[0] + s_red[1]) + (s_red[2] + s_red[3]);
 }
 
 // ---------------------------------------------------------------------------
@@ -541,14 +582,24 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
         // in flight together), added in split order, then its own
         if (kh == 0) {
             constexpr int SPL = (MT <= 2) ? 4 : 1;
+            // a workspace poisoned by an earlier give-up may hold flags of no
+            // block of this call: then the sums are discarded and nothing is
+            // cleared (this call's blocks still set every flag, so the polls
+            // end; the word's load overlaps them)
+            const bool poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
 #pragma unroll
             for (int i = 0; i < MT; ++i) {
+                if (timed_out) break;
                 f32x4_t sum[NT];
 #pragma unroll
                 for (int j = 0; j < NT; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
                 for (int z0 = 0; z0 < a.ksplit - 1; z0 += SPL) {
                     uint64_t pw[SPL][NT][4];
                     for (int spin = 0;; ++spin) {
+                        if (spin >= a.spin_limit) {  // never expected: report, rather than hang
+                            timed_out = true;
+                            break;
+                        }
                         bool ready = true;
 #pragma unroll
                         for (int zi = 0; zi < SPL; ++zi) {
@@ -562,27 +613,35 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
                                 }
                         }
                         if (__all(ready)) break;
-                        if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
-                            timed_out = true;
-                            break;
-                        }
                         __builtin_amdgcn_s_sleep(2);
                     }
+                    if (timed_out) break;
 #pragma unroll
                     for (int zi = 0; zi < SPL; ++zi) {
                         if (z0 + zi >= a.ksplit - 1) break;
 #pragma unroll
                         for (int j = 0; j < NT; ++j)
 #pragma unroll
-                            for (int r = 0; r < 4; ++r) {
-                                sum[j][r] += __uint_as_float(uint32_t(pw[zi][j][r]));
-                                __hip_atomic_store(slot(z0 + zi, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                            }
+                            for (int r = 0; r < 4; ++r) sum[j][r] += __uint_as_float(uint32_t(pw[zi][j][r]));
                     }
                 }
 #pragma unroll
                 for (int j = 0; j < NT; ++j) acc[i][j] = sum[j] + acc[i][j];
             }
+            // every slot consumed: clear them for the next call (after a
+            // give-up they stay, and the workspace is marked)
+            if (!poisoned && !timed_out) {
+                for (int zz = 0; zz < a.ksplit - 1; ++zz)
+#pragma unroll
+                    for (int i = 0; i < MT; ++i)
+#pragma unroll
+                        for (int j = 0; j < NT; ++j)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r)
+                                __hip_atomic_store(slot(zz, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            gemm_report(a, poisoned, timed_out);
+            timed_out = timed_out || poisoned;
         }
     }
 
@@ -836,12 +895,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
         f32x4_t sum[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+        // a workspace poisoned by an earlier give-up may hold flags of no
+        // slice of this call: then the sums are discarded and nothing is
+        // cleared (this call's slices still set every flag, so the polls end;
+        // the word's load overlaps them)
+        const bool poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
         // two slices per round trip (the second clamped to the last slice:
         // a re-read), added in slice order
-        for (int64_t q0 = 0; q0 < Q - 1; q0 += 2) {
+        for (int64_t q0 = 0; q0 < Q - 1 && !timed_out; q0 += 2) {
             uint64_t pw[2][16];
             const int64_t qs[2] = {q0, (q0 + 1 < Q - 1) ? q0 + 1 : Q - 2};
             for (int spin = 0;; ++spin) {
+                if (spin >= a.spin_limit) {  // never expected: report, rather than hang
+                    timed_out = true;
+                    break;
+                }
                 bool ready = true;
 #pragma unroll
                 for (int h = 0; h < 2; ++h)
@@ -851,22 +919,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
                         ready &= (pw[h][e] >> 32) != 0;
                     }
                 if (__all(ready)) break;
-                if (spin == GEMM_SPIN_LIMIT) {  // never expected: report NaN rather than hang
-                    timed_out = true;
-                    break;
-                }
                 __builtin_amdgcn_s_sleep(1);
             }
+            if (timed_out) break;
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 if (q0 + h >= Q - 1) break;
 #pragma unroll
-                for (int e = 0; e < 16; ++e) {
-                    sum[e >> 2][e & 3] += __uint_as_float(uint32_t(pw[h][e]));
-                    __hip_atomic_store(slots + (q0 + h) * 1024 + e * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
+                for (int e = 0; e < 16; ++e) sum[e >> 2][e & 3] += __uint_as_float(uint32_t(pw[h][e]));
             }
         }
+        // every slot consumed: clear them for the next call (after a give-up
+        // they stay, and the workspace is marked)
+        if (!poisoned && !timed_out) {
+            for (int64_t q0 = 0; q0 < Q - 1; ++q0)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    __hip_atomic_store(slots + q0 * 1024 + e * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        gemm_report(a, poisoned, timed_out);
+        timed_out = timed_out || poisoned;
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[j] = sum[j] + acc[j];
     }
@@ -1020,7 +1092,7 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     ks = std::min<int64_t>(ks, 1 + GEMM_SLOT_BYTES / std::max<int64_t>(1, tiles * p.bm * p.bn * 8));
     ks = std::min<int64_t>(ks, 64);
     p.ksplit = std::max<int64_t>(ks, 1);
-    p.t_off = size_t(GEMM_SLOT_BYTES);
+    p.t_off = size_t(GEMM_HDR + GEMM_SLOT_BYTES);
     p.xt_off = p.t_off + align256(size_t(p.Mp) * BSQ_MAX_LORA_RANK * 4);
     p.xp_off = p.xt_off + align256(size_t(p.Mp) * size_t(p.Kp) * 2);
     p.total = p.xp_off + align256(size_t(p.Mp) * size_t(std::max<int64_t>(p.kp32, 32)) * 2);
@@ -1055,7 +1127,7 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 
 const float *gemm_lora_t(const void *ws)
 {
-    return reinterpret_cast<const float *>(static_cast<const char *>(ws) + GEMM_SLOT_BYTES);
+    return reinterpret_cast<const float *>(static_cast<const char *>(ws) + GEMM_HDR + GEMM_SLOT_BYTES);
 }
 
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M)
@@ -1066,7 +1138,7 @@ size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t
 
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &L, const bsq_lora *lora,
                        const void *X, int64_t M, int64_t ldx, void *Y, int y_dtype, int64_t ldy, void *ws,
-                       hipStream_t st)
+                       int32_t *err, hipStream_t st)
 {
     if (M == 0 || L.d_out == 0) return hipSuccess;
     const GemmPlan p = gemm_plan(L.d_out, L.d_in, M, L.k);
@@ -1099,7 +1171,10 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     }
     a.rank = 0;
     a.ksplit = int(p.ksplit);
-    a.slots = static_cast<uint64_t *>(ws);
+    a.slots = reinterpret_cast<uint64_t *>(wb + GEMM_HDR);
+    a.poison = static_cast<uint32_t *>(ws);
+    a.err = err;
+    a.spin_limit = wait_limit();
 
     PrepArgs pa{};
     pa.X = static_cast<const uint16_t *>(X);
@@ -1119,7 +1194,9 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
         pa.A = lora->A;
         pa.rank = lora->rank;
     }
-    hipLaunchKernelGGL(gemm_prep, dim3(unsigned(p.Mp), unsigned((p.Kp + PREP_COLS - 1) / PREP_COLS)), dim3(256), 0, st, pa);
+    // per token row: the X~ column blocks, the gather, then one block per LoRA rank index
+    hipLaunchKernelGGL(gemm_prep, dim3(unsigned(p.Mp), unsigned((p.Kp + PREP_COLS - 1) / PREP_COLS + 1 + pa.rank)),
+                       dim3(256), 0, st, pa);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
 

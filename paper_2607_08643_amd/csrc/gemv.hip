@@ -24,10 +24,13 @@
 namespace bsq {
 namespace {
 
-// Workspace: the LoRA vectors of up to BSQ_MAX_GROUP members, then the
-// flagged partial slots. The slots start at the same offset for every group
-// size, so a workspace shared by groups of different sizes keeps its slots
-// at zero between calls.
+// Workspace: a 256-byte header (its first word is the poison word, nonzero
+// once a call gave up waiting for a partial result and left flagged slots
+// behind), the LoRA vectors of up to BSQ_MAX_GROUP members, then the flagged
+// partial slots. The slots start at the same offset for every group size, so
+// a workspace shared by groups of different sizes keeps its slots at zero
+// between calls.
+constexpr size_t GEMV_HDR = 256;
 constexpr size_t gemv_t_bytes() { return (size_t(BSQ_MAX_GROUP) * BSQ_MAX_LORA_RANK * 4 + 255) & ~size_t(255); }
 
 // The d = 16 symmetric decoder path (hidden width 16) evaluates the decoder
@@ -47,9 +50,6 @@ inline size_t gemv_xp_bytes(const bsq_config &cfg, int64_t pitch)
     return gemv_split16(cfg) ? size_t(BSQ_MAX_GROUP) * cfg.stages * size_t(pitch) * 64 : 0;
 }
 
-// row-lane kernel: polls of a row group's last slice for the other slices'
-// partial sums before it gives up and writes NaN (seconds; never expected)
-constexpr int LANE_SPIN_LIMIT = 1 << 22;
 // row-lane kernel: largest padded int8 row that a finishing slice brings to
 // LDS (64 rows x 256 B = 16 KiB); longer rows are read from global memory
 constexpr int64_t LANE_Q8_LDS_MAX = 256;
@@ -113,6 +113,9 @@ struct GemvArgs {
     int64_t lora_blocks;  // row-lane kernel: LoRA workgroups ahead of the tiles' workgroups
     const void *x;
     int x_bf16, y_bf16;
+    uint32_t *poison;  // row-lane kernel: the workspace's poison word
+    int32_t *err;      // caller's device error word, or null
+    int spin_limit;    // polls before a wait gives up (wait_limit())
 };
 
 __device__ __forceinline__ float load_x(const void *x, int64_t j, int bf)
@@ -678,6 +681,10 @@ __device__ __forceinline__ bool lane_lora_vector(const GemvArgs &a, const GemvMa
     uint64_t pw[BSQ_MAX_LORA_RANK];
     bool ok = true;
     for (int spin = 0;; ++spin) {
+        if (spin >= a.spin_limit) {  // never expected: report, rather than hang
+            ok = false;
+            break;
+        }
 #pragma unroll
         for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q)
             pw[q] = __hip_atomic_load(ts + ((q < M.rank) ? q : M.rank - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -685,16 +692,15 @@ __device__ __forceinline__ bool lane_lora_vector(const GemvArgs &a, const GemvMa
 #pragma unroll
         for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) ready &= (pw[q] >> 32) != 0;
         if (__all(ready)) break;
-        if (spin == LANE_SPIN_LIMIT) {  // never expected: report NaN rather than hang
-            ok = false;
-            break;
-        }
         __builtin_amdgcn_s_sleep(1);
     }
 #pragma unroll
     for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) tv[q] = (q < M.rank) ? __uint_as_float(uint32_t(pw[q])) : 0.0f;
+    // the slots are cleared only when every one was consumed: after a give-up
+    // a late flag may still land, so they stay as they are (the caller sees
+    // the timeout bit and the poisoned workspace)
     const int lane = threadIdx.x & 63;
-    if (lane < M.rank) __hip_atomic_store(ts + lane, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (ok && lane < M.rank) __hip_atomic_store(ts + lane, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return ok;
 }
 
@@ -857,9 +863,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     const int32_t pj_raw = ((a.k > 0) ? M.idx : static_cast<const int32_t *>(a.x))[pt];
     const float psc = ((a.k > 0) ? M.scale : static_cast<const float *>(a.x))[pt];
     const int32_t pj = (a.k > 0) ? pj_raw : -1;
-    // the table is in LDS once at most the tile and index loads are
+    // the workspace's poison word, read by the finishing slice before it
+    // consumes any slot (unconditional, like the loads above)
+    const uint32_t poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // the table is in LDS once at most the tile, index and poison loads are
     // pending; a plain s_barrier (no release fence) lets those stay in flight
-    constexpr int NIDX = PF * (D / 8 + 2) * S + 2;
+    constexpr int NIDX = PF * (D / 8 + 2) * S + 3;
     __builtin_amdgcn_s_waitcnt((NIDX & 15) | ((NIDX >> 4) << 14) | (7 << 4) | (15 << 8));
     asm volatile("s_barrier" ::: "memory");
 
@@ -919,24 +928,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
                            __HIP_MEMORY_SCOPE_AGENT);
         return;
     }
+    // a workspace poisoned by an earlier call that gave up waiting may hold
+    // flags that no slice of this call wrote: consume nothing, write NaN and
+    // report (the caller zero-fills the workspace to recover)
+    if (poisoned != 0u) {
+        if (lane == 0 && a.err) atomicOr(a.err, int32_t(BSQ_DEVERR_POISONED));
+        if (row < M.d_out) lane_store(a, M, row, __builtin_nanf(""));
+        return;
+    }
     // the finishing slice adds the protected and LoRA terms to its own sum
     // first: they do not depend on the other slices, so this work overlaps
     // the wait for them
     float tv[BSQ_MAX_LORA_RANK];
     const bool ok = lane_lora_vector(a, M, rg, tv);
     if (row < M.d_out) v = lane_extras(a, M, s_xs, s_q8, q8_lds, row, v, tv);
-    if (Q == 1) {
-        if (row < M.d_out) lane_store(a, M, row, ok ? v : __builtin_nanf(""));
-        return;
-    }
     float tot = 0.0f;
     bool timed_out = false;
     // the other slices' slots, eight at a time, all eight loads in flight
     // together (slot indices clamped to the last one, extra copies unused)
     constexpr int PW = 8;
-    for (int64_t q0 = 0; q0 < Q - 1; q0 += PW) {
+    for (int64_t q0 = 0; q0 < Q - 1 && !timed_out; q0 += PW) {
         uint64_t pw[PW];
         for (int spin = 0;; ++spin) {
+            if (spin >= a.spin_limit) {  // never expected: report, rather than hang
+                timed_out = true;
+                break;
+            }
 #pragma unroll
             for (int u = 0; u < PW; ++u)
                 pw[u] = __hip_atomic_load(slots + ((q0 + u < Q - 1) ? q0 + u : Q - 2) * 64, __ATOMIC_RELAXED,
@@ -945,19 +962,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
 #pragma unroll
             for (int u = 0; u < PW; ++u) ready &= (pw[u] >> 32) != 0;
             if (__all(ready)) break;
-            if (spin == LANE_SPIN_LIMIT) {  // never expected: report NaN rather than hang
-                timed_out = true;
-                break;
-            }
             __builtin_amdgcn_s_sleep(1);
         }
 #pragma unroll
         for (int u = 0; u < PW; ++u) tot += (q0 + u < Q - 1) ? __uint_as_float(uint32_t(pw[u])) : 0.0f;
     }
     tot += v;
+    if (timed_out || !ok) {
+        // a slice that is late may still set its flag: leave every slot as it
+        // is and mark the workspace, so that no later call takes such a flag
+        // for one of its own
+        if (lane == 0) {
+            __hip_atomic_store(a.poison, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a.err) atomicOr(a.err, int32_t(BSQ_DEVERR_TIMEOUT));
+        }
+        if (row < M.d_out) lane_store(a, M, row, __builtin_nanf(""));
+        return;
+    }
     for (int64_t q0 = 0; q0 < Q - 1; ++q0)
         __hip_atomic_store(slots + q0 * 64, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (row < M.d_out) lane_store(a, M, row, (timed_out || !ok) ? __builtin_nanf("") : tot);
+    if (row < M.d_out) lane_store(a, M, row, tot);
 }
 
 // ---------------------------------------------------------------------------
@@ -1059,8 +1083,10 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
     a.x_bf16 = (x_dtype == BSQ_BF16);
     a.y_bf16 = (y_dtype == BSQ_BF16);
     a.stages = cfg.stages;
-    float *wt = static_cast<float *>(ws);
-    char *wb = static_cast<char *>(ws);
+    char *wb = static_cast<char *>(ws) + GEMV_HDR;
+    float *wt = reinterpret_cast<float *>(wb);
+    a.poison = static_cast<uint32_t *>(ws);
+    a.spin_limit = wait_limit();
     a.slots = reinterpret_cast<uint64_t *>(wb + gemv_t_bytes() + gemv_xp_bytes(cfg, a.pitch));
     for (int m = 0; m < n; ++m) {
         GemvMat &M = a.mat[m];
@@ -1123,7 +1149,7 @@ size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_
     // {flag, partial} slots for all but the last slice (as many slices as the
     // smallest TPW makes), then the flagged LoRA vector slots of every row
     // group
-    return gemv_t_bytes() + gemv_xp_bytes(cfg, nblk * BSQ_PITCH_ALIGN) +
+    return GEMV_HDR + gemv_t_bytes() + gemv_xp_bytes(cfg, nblk * BSQ_PITCH_ALIGN) +
            size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8 + size_t(rg) * BSQ_MAX_LORA_RANK * 8;
 }
 
@@ -1153,10 +1179,11 @@ hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *cod
 
 hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                            const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
-                           void *ws, hipStream_t st)
+                           void *ws, int32_t *err, hipStream_t st)
 {
     const int D = cfg.d, S = cfg.stages;
     GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws);
+    a.err = err;
     int64_t rows_total = 0;
     for (int m = 0; m < n; ++m) rows_total += layers[m].d_out;
     if (rows_total == 0) return hipSuccess;

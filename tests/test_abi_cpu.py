@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 4
+    assert bsq.bsq_version() == 5
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -167,13 +167,23 @@ def test_decode_gemv_gemm_reject_before_launch():
     assert Lib.bsq_decode(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), ct.c_void_p(FAKE), 5, None) == bsq.BSQ_ERR_DTYPE
     assert Lib.bsq_decode(ct.byref(c), None, ct.byref(L), ct.c_void_p(FAKE), 0, None) == bsq.BSQ_ERR_ARG
     assert Lib.bsq_decode(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), ct.c_void_p(FAKE + 4), 0, None) == bsq.BSQ_ERR_ALIGN
+    # sequential stage decode: stage in range, accumulate 0/1, fp32 output aligned
+    def dstage(stage=0, acc=0, out=FAKE):
+        return Lib.bsq_decode_stage(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), stage, acc,
+                                    out and ct.c_void_p(out), None)
+    assert dstage(stage=-1) == bsq.BSQ_ERR_ARG
+    assert dstage(stage=cfg.stages) == bsq.BSQ_ERR_ARG
+    assert dstage(acc=2) == bsq.BSQ_ERR_ARG
+    assert dstage(out=0) == bsq.BSQ_ERR_ARG
+    assert dstage(out=FAKE + 8) == bsq.BSQ_ERR_ALIGN
     codecs = (ct.c_void_p * 1)(FAKE)
     layers = (B.bsq_layer * 1)(L)
     ys = (ct.c_void_p * 1)(FAKE)
 
-    def gemv(n=1, x=FAKE, xd=1, yd=1, ws=FAKE, ws_bytes=1 << 30, loras=None, lay=layers):
-        return Lib.bsq_gemv(ct.byref(c), n, codecs, lay, loras, x and ct.c_void_p(x), xd, ys, yd,
-                            ws and ct.c_void_p(ws), ws_bytes, None)
+    def gemv(n=1, x=FAKE, xd=1, yd=1, ws=FAKE, ws_bytes=1 << 30, loras=None, lay=layers, err=None, run=False):
+        f = Lib.bsq_gemv_run if run else Lib.bsq_gemv
+        return f(ct.byref(c), n, codecs, lay, loras, x and ct.c_void_p(x), xd, ys, yd,
+                 ws and ct.c_void_p(ws), ws_bytes, err and ct.c_void_p(err), None)
     assert gemv(n=0) == bsq.BSQ_ERR_ARG
     assert gemv(n=9) == bsq.BSQ_ERR_ARG
     assert gemv(x=0) == bsq.BSQ_ERR_ARG
@@ -188,11 +198,16 @@ def test_decode_gemv_gemm_reject_before_launch():
     nobits = _fake_layer(cfg, 64, 256)
     nobits.prot_bits = 0                                       # the product masks with the bitmap
     assert gemv(lay=(B.bsq_layer * 1)(nobits)) == bsq.BSQ_ERR_ARG
+    # the optional device error word must be 4-byte aligned (both entry points)
+    assert gemv(err=FAKE + 2) == bsq.BSQ_ERR_ALIGN
+    assert gemv(err=FAKE + 2, run=True) == bsq.BSQ_ERR_ALIGN
+    assert gemv(x=0, run=True) == bsq.BSQ_ERR_ARG
 
-    def gemm(M=16, ldx=256, ldy=64, xd=1, X=FAKE, ws_bytes=1 << 30, lora=None):
+    def gemm(M=16, ldx=256, ldy=64, xd=1, X=FAKE, ws_bytes=1 << 30, lora=None, err=None):
         lo = B.bsq_lora(0, 0, 0) if lora is None else lora
         return Lib.bsq_gemm(ct.byref(c), ct.c_void_p(FAKE), ct.byref(L), ct.byref(lo), X and ct.c_void_p(X), xd, M,
-                            ldx, ct.c_void_p(FAKE), 1, ldy, ct.c_void_p(FAKE), ws_bytes, None)
+                            ldx, ct.c_void_p(FAKE), 1, ldy, ct.c_void_p(FAKE), ws_bytes, err and ct.c_void_p(err),
+                            None)
     assert gemm(xd=0) == bsq.BSQ_ERR_DTYPE               # X must be bf16
     assert gemm(M=-1) == bsq.BSQ_ERR_SHAPE
     assert gemm(ldx=128) == bsq.BSQ_ERR_SHAPE
@@ -201,6 +216,26 @@ def test_decode_gemv_gemm_reject_before_launch():
     assert gemm(X=FAKE + 2) == bsq.BSQ_ERR_ALIGN
     assert gemm(ws_bytes=4) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
     assert gemm(lora=B.bsq_lora(FAKE, FAKE, 0x7fffffff)) == bsq.BSQ_ERR_ARG
+    assert gemm(err=FAKE + 1) == bsq.BSQ_ERR_ALIGN
+
+
+def test_wait_limit_is_settable_and_restorable():
+    """bsq_debug_set_wait_limit returns the previous bound; a negative value
+    restores the default (host state only, no launch)."""
+    default = bsq.bsq_debug_set_wait_limit(-1)
+    assert default > 1000
+    assert bsq.bsq_debug_set_wait_limit(0) == default
+    assert bsq.bsq_debug_set_wait_limit(7) == 0
+    assert bsq.bsq_debug_set_wait_limit(-5) == 7
+    assert bsq.bsq_debug_set_wait_limit(-1) == default
+
+
+def test_product_workspaces_hold_a_header():
+    """GEMV and GEMM workspaces start with a 256-byte header for the poison
+    word, so they exceed their slot and scratch areas by at least that."""
+    cfg = bsq.Config()
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 64, 256, 1) >= 256 + (8 << 20)
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 1, 64, 256) >= 256 + 8 * 16 * 4
 
 
 def test_codec_prepare_rejects_before_launch():

@@ -1,19 +1,15 @@
 """HIP path vs the CPU oracle, element by element, through the C ABI.
 
-Bar: codes, gains, protected indices, int8 payload and scales bit-exact;
-fp32 decode bit-exact (bf16 decode = the oracle's fp32 value rounded to
-nearest even); products within 2e-2 relative per output for bf16
-activations and 1e-4 for fp32 activations.
-
-A relative bar cannot hold for an output that cancels to about zero, so each
-output also gets an absolute floor derived from the arithmetic:
-  * bf16 products round every decoded weight (or decoded table entry) once to
-    bf16, an error of at most u = 2^-8 times |w_ij x_j| per term. Treating the
-    roundings as independent, Hoeffding's inequality bounds the output error
-    by sqrt(2 ln(2/lam)) * u * sqrt(sum_j (w_ij x_j)^2) except with
-    probability lam; lam = 1e-9 per output gives a factor 6.5.
-  * fp32 products use 1e-2 * rms(y).
-The fraction of outputs that needed the floor is printed.
+Bar: codes, gains, protected indices, int8 payload, scales and the bitmap
+bit-exact; fp32 decode bit-exact (bf16 decode = the oracle's fp32 value
+rounded to nearest even); products within 2e-2 relative per output for bf16
+activations and 1e-4 for fp32 activations, with an absolute floor per output
+derived from the rounding the GPU path does (tests/parity_bounds.py: a
+sub-Gaussian bound on the bf16 roundings of the decoded terms, 3.78 u
+sqrt(sum t^2), plus fp32 accumulation). Separate checks take the LoRA term
+and the int8 protected term out of the product (the difference of two calls
+that differ only in that term) and compare each with the oracle's value of
+the term, so that a dropped or partly wrong term cannot hide under the floor.
 """
 import sys
 
@@ -24,15 +20,11 @@ import torch
 import oracle
 import paper_2607_08643_amd as bsq
 import synth
+from parity_bounds import check_close, product_floor, say, term_bar
 
 pytestmark = pytest.mark.gpu
 
 OKIND = {bsq.DEC_IDENTITY: oracle.KIND_IDENTITY, bsq.DEC_LINEAR: oracle.KIND_LINEAR, bsq.DEC_MLP: oracle.KIND_MLP}
-
-
-def say(*a):
-    print(*a, flush=True)
-    sys.stdout.flush()
 
 
 def ocfg(cfg: bsq.Config) -> oracle.Config:
@@ -77,38 +69,18 @@ def assert_layer_equal(layer, enc, cfg, m=None):
         np.testing.assert_array_equal(L.bits.cpu().numpy().view(np.uint32), want, err_msg="protected bitmap")
 
 
-BF16_U = 2.0 ** -8
-HOEFFDING = float(np.sqrt(2.0 * np.log(2.0 / 1e-9)))
+def gemv_kind(x_dtype):
+    """The arithmetic of the GEMV path bsq_gemv takes for this activation
+    dtype: fp32 throughout for fp32 x, else bf16 decoded terms."""
+    return "fp32" if x_dtype == torch.float32 else "gemv"
 
 
-def rss_terms(w_hat, X, lora=None):
-    """sqrt(sum_j (w_ij x_j)^2 [+ sum_r (B_ir t_r)^2]) per output, fp64."""
-    X64 = np.atleast_2d(np.asarray(X, dtype=np.float64))
-    s2 = (X64 ** 2) @ (w_hat.astype(np.float64) ** 2).T
-    if lora is not None:
-        T = X64 @ np.asarray(lora[0], np.float64).T
-        s2 = s2 + (T ** 2) @ (np.asarray(lora[1], np.float64) ** 2).T
-    out = np.sqrt(s2)
-    return out[0] if np.ndim(X) == 1 else out
-
-
-def check_close(y, y_ref, rel, what, rss=None):
-    """|y - y_ref| <= max(rel |y_ref|, floor); floor = the bf16 rounding bound
-    when rss is given, else 1e-2 * rms(y_ref)."""
-    y = np.asarray(y, dtype=np.float64)
-    if not y_ref.size:
-        return
-    if rss is not None:
-        floor = HOEFFDING * BF16_U * np.asarray(rss, dtype=np.float64)
-    else:
-        floor = 1e-2 * np.sqrt(np.mean(y_ref ** 2)) * np.ones_like(y_ref)
-    tol = np.maximum(rel * np.abs(y_ref), floor)
-    err = np.abs(y - y_ref)
-    bad = err > tol
-    on_floor = float(np.mean(floor > rel * np.abs(y_ref)))
-    worst = float(np.max(err / np.maximum(tol, 1e-300)))
-    say(f"  {what}: max err/tol {worst:.2e}, {on_floor:.2%} of outputs on the floor")
-    assert not bad.any(), f"{what}: {int(bad.sum())} outputs outside tolerance (worst err/tol {worst:.3e})"
+def check_product(y, y_ref, kind, cfg, enc, tabs, w_hat, X, lref, what, y_dtype):
+    """The product bar: 1e-4 relative for fp32 activations with fp32 output,
+    else 2e-2, with the derived floor of the path and the output rounding."""
+    rel = 1e-4 if (kind == "fp32" and y_dtype == torch.float32) else 2e-2
+    floor = product_floor(kind, cfg.d, enc, tabs, w_hat, X, lref)
+    check_close(np.asarray(y, dtype=np.float64), y_ref, rel, what, floor, out_bf16=(y_dtype == torch.bfloat16))
 
 
 # (name, d_out, d_in, cfg kwargs, dtype, n_mats, with_g)
@@ -173,6 +145,22 @@ def test_encode_decode_bit_exact(case, gpu):
 
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_sequential_stage_decode_equals_stage_parallel(case, gpu):
+    """Decoding the residual stages one launch after the other
+    (bsq_decode_stage, accumulating in fp32) gives the bits of the
+    stage-parallel decode of eq. parallel_stage_decode (bsq_decode), which
+    the oracle's decode pins."""
+    say(f"case {case[0]} sequential stages")
+    cfg, decs, codec, layer, W, encs, tabs = _make(*case, gpu)
+    par = bsq.bsq_decode(cfg, codec, layer, dtype=torch.float32)
+    seq = torch.full_like(par, float("nan"))
+    for s in range(cfg.stages):
+        bsq.bsq_decode_stage(cfg, codec, layer, s, s > 0, seq)
+    torch.cuda.synchronize()
+    assert torch.equal(seq.view(torch.int32), par.view(torch.int32))
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
 @pytest.mark.parametrize("with_lora", [False, True], ids=["nolora", "lora"])
 def test_gemv_matches_oracle(case, with_lora, gpu):
     say(f"case {case[0]} lora={with_lora}")
@@ -190,11 +178,8 @@ def test_gemv_matches_oracle(case, with_lora, gpu):
             xf = oracle.to_f32(x)
             w_hat = oracle.decode(oc, decs, enc, tables=tabs)
             y_ref = oracle.dense_product(w_hat, xf, lref)
-            if dtype == torch.float32 and ydt == torch.float32:
-                check_close(y.float().cpu().numpy(), y_ref, 1e-4, f"gemv m={m} y={ydt}")
-            else:
-                check_close(y.float().cpu().numpy(), y_ref, 2e-2, f"gemv m={m} y={ydt}",
-                            rss=rss_terms(w_hat, xf, lref))
+            check_product(y.float().cpu().numpy(), y_ref, gemv_kind(dtype), cfg, enc, tabs, w_hat, xf, lref,
+                          f"gemv m={m} y={ydt}", ydt)
 
 
 @pytest.mark.parametrize("scale", [2.0 ** 24, 2.0 ** -24], ids=["huge", "tiny"])
@@ -212,7 +197,8 @@ def test_gemv_d16_activation_range(scale, gpu):
     xf = oracle.to_f32(x)
     w_hat = oracle.decode(oc, decs, encs[0], tables=tabs)
     y_ref = oracle.dense_product(w_hat, xf, None)
-    check_close(y.float().cpu().numpy(), y_ref, 2e-2, f"gemv x*{scale}", rss=rss_terms(w_hat, xf, None))
+    check_product(y.float().cpu().numpy(), y_ref, "gemv", cfg, encs[0], tabs, w_hat, xf, None, f"gemv x*{scale}",
+                  torch.float32)
 
 
 # Long rows: the K steps of a tile are split over several blocks (ragged
@@ -240,16 +226,19 @@ def test_gemm_matches_oracle(case, M, gpu):
     w_hat = oracle.decode(oc, decs, encs[0], tables=tabs)
     lref = (oracle.to_f32(lora[0]), oracle.to_f32(lora[1]))
     Y_ref = oracle.dense_product(w_hat, Xf, lref)
-    check_close(Y.cpu().numpy(), Y_ref, 2e-2, "gemm fp32 out", rss=rss_terms(w_hat, Xf, lref))
+    check_product(Y.cpu().numpy(), Y_ref, "gemm", cfg, encs[0], tabs, w_hat, Xf, lref, "gemm fp32 out",
+                  torch.float32)
     Yb_ref = oracle.dense_product(w_hat, Xf)
-    check_close(Yb.float().cpu().numpy(), Yb_ref, 2e-2, "gemm bf16 out", rss=rss_terms(w_hat, Xf))
+    check_product(Yb.float().cpu().numpy(), Yb_ref, "gemm", cfg, encs[0], tabs, w_hat, Xf, None, "gemm bf16 out",
+                  torch.bfloat16)
 
 
 @pytest.mark.parametrize("d", [8, 16])
 def test_gemm_workspace_reuse(d, gpu):
     """One zero-filled workspace for calls of different token counts: each
-    result equals the one from a fresh workspace, and the split-K slots (the
-    first 8 MiB) are back at zero after every call."""
+    result equals the one from a fresh workspace, and the poison word and the
+    split-K slots (the first 256 B + 8 MiB) are back at zero after every
+    call."""
     say(f"gemm workspace reuse d={d}")
     cfg = bsq.Config(d=d, hidden=d)
     decs = decoders(cfg, seed=d + 3)
@@ -268,7 +257,7 @@ def test_gemm_workspace_reuse(d, gpu):
         Y_fresh = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.float32)
         torch.cuda.synchronize()
         assert torch.equal(Y, Y_fresh), f"M={M}: shared-workspace result differs"
-        assert int(torch.count_nonzero(ws[:8 << 20])) == 0, f"M={M}: split-K slots not cleared"
+        assert int(torch.count_nonzero(ws[:256 + (8 << 20)])) == 0, f"M={M}: poison word or split-K slots not clear"
 
 
 @pytest.mark.parametrize("d", [8, 16])
@@ -296,10 +285,11 @@ def test_grouped_gemv_three_categories(d, gpu):
     for i in range(3):
         assert_layer_equal(layers[i], encs[i], cfg)
         lref = (oracle.to_f32(loras[i][0]), oracle.to_f32(loras[i][1]))
-        w_hat = oracle.decode(oc, decs_all[i], encs[i])
+        tabs = oracle.decoder_table(oc, decs_all[i])
+        w_hat = oracle.decode(oc, decs_all[i], encs[i], tables=tabs)
         y_ref = oracle.dense_product(w_hat, oracle.to_f32(x), lref)
-        check_close(ys[i].cpu().numpy(), y_ref, 2e-2, f"group member {i}",
-                    rss=rss_terms(w_hat, oracle.to_f32(x), lref))
+        check_product(ys[i].cpu().numpy(), y_ref, "gemv", cfg, encs[i], tabs, w_hat, oracle.to_f32(x), lref,
+                      f"group member {i}", torch.float32)
 
 
 # ---------------------------------------------------------------- edge cases
@@ -384,6 +374,10 @@ FULL = [
     ("qwen3-8b-q-4096x4096-d16", 4096, 4096, 16),
     ("qwen3-8b-down-4096x12288-d8", 4096, 12288, 8),
     ("qwen3-8b-gate-12288x4096-d16", 12288, 4096, 16),
+    ("qwen3-32b-q-8192x5120-d8", 8192, 5120, 8),
+    ("qwen3-32b-k-1024x5120-d16", 1024, 5120, 16),
+    ("qwen3-32b-o-5120x8192-d8", 5120, 8192, 8),
+    ("qwen3-32b-o-5120x8192-d16", 5120, 8192, 16),
     ("qwen3-32b-down-5120x25600-d8", 5120, 25600, 8),
     ("qwen3-32b-gate-25600x5120-d16", 25600, 5120, 16),
 ]
@@ -406,21 +400,23 @@ def test_full_size_encode_and_gemv(case, gpu):
     y = bsq.bsq_gemv(cfg, codec, layer, x, loras=(A, Bm), y_dtype=torch.bfloat16)
     torch.cuda.synchronize()
     Wf = oracle.to_f32(W)
-    enc = oracle.encode(oc, decs, Wf, nthreads=0)
+    tabs = oracle.decoder_table(oc, decs)
+    enc = oracle.encode(oc, decs, Wf, nthreads=0, tables=tabs)
     np.testing.assert_array_equal(enc.idx, np.asarray(cols))
     assert_layer_equal(layer, enc, cfg)
     lref = (oracle.to_f32(A), oracle.to_f32(Bm))
-    w_hat = oracle.decode(oc, decs, enc)
+    w_hat = oracle.decode(oc, decs, enc, tables=tabs)
     xf = oracle.to_f32(x)
     y_ref = oracle.dense_product(w_hat, xf, lref)
-    check_close(y.float().cpu().numpy(), y_ref, 2e-2, name, rss=rss_terms(w_hat, xf, lref))
+    check_product(y.float().cpu().numpy(), y_ref, "gemv", cfg, enc, tabs, w_hat, xf, lref, name, torch.bfloat16)
 
 
-@pytest.mark.parametrize("M", [16, 256])
+@pytest.mark.parametrize("M", [16, 64, 256])
 @pytest.mark.parametrize("d", [8, 16])
 def test_full_size_gemm(d, M, gpu):
-    """Qwen3-8B o_proj shape at the batched sizes of the workload (M = 16 runs
-    the streaming small-M kernel at d = 8, M = 256 the tiled one)."""
+    """Qwen3-8B o_proj shape at the batched sizes of the workload, with the
+    rank-16 LoRA (M = 16 runs the streaming small-M kernel at d = 8, the
+    others the tiled one)."""
     say(f"qwen3-8b o_proj 4096x4096 gemm M={M} d={d}")
     cfg = bsq.Config(d=d, hidden=d)
     oc = ocfg(cfg)
@@ -432,67 +428,158 @@ def test_full_size_gemm(d, M, gpu):
     A, Bm = synth.lora(4096, 4096, 16, seed=9, device=gpu)
     Y = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.bfloat16)
     torch.cuda.synchronize()
-    enc = oracle.encode(oc, decs, oracle.to_f32(W))
+    tabs = oracle.decoder_table(oc, decs)
+    enc = oracle.encode(oc, decs, oracle.to_f32(W), tables=tabs)
     assert_layer_equal(layer, enc, cfg)
     lref = (oracle.to_f32(A), oracle.to_f32(Bm))
-    w_hat = oracle.decode(oc, decs, enc)
+    w_hat = oracle.decode(oc, decs, enc, tables=tabs)
     Xf = oracle.to_f32(X)
     Y_ref = oracle.dense_product(w_hat, Xf, lref)
-    check_close(Y.float().cpu().numpy(), Y_ref, 2e-2, f"gemm M={M}", rss=rss_terms(w_hat, Xf, lref))
+    check_product(Y.float().cpu().numpy(), Y_ref, "gemm", cfg, enc, tabs, w_hat, Xf, lref, f"gemm M={M}",
+                  torch.bfloat16)
 
 
-def test_category_batched_stack_encode(gpu):
-    """Eight k_proj-shaped layers (1024 x 4096) of one category in one encode."""
-    say("stack of 8 x 1024x4096, d=8")
+@pytest.mark.parametrize("n_mats,d_out,d_in", [(8, 1024, 4096), (64, 1024, 5120)],
+                         ids=["8x1024x4096", "64x1024x5120"])
+def test_category_batched_stack_encode(n_mats, d_out, d_in, gpu):
+    """Layers of one category in one encode (the k_proj shapes of the
+    Qwen3-8B stack and, at its full depth, of the 64-layer Qwen3-32B stack):
+    every matrix of the stack bit-exact against the oracle's own encoding."""
+    say(f"stack of {n_mats} x {d_out}x{d_in}, d=8")
     cfg = bsq.Config(d=8, hidden=8)
     oc = ocfg(cfg)
     decs = decoders(cfg, seed=3)
-    W, _ = synth.weight(1024, 4096, seed=5, k_outliers=cfg.k(4096), device=gpu, n_mats=8)
+    W, cols = synth.weight(d_out, d_in, seed=5, k_outliers=cfg.k(d_in), device=gpu, n_mats=n_mats)
     codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
     layer = bsq.bsq_encode(cfg, codec, W)
     torch.cuda.synchronize()
-    Wf = oracle.to_f32(W)
     tabs = oracle.decoder_table(oc, decs)
-    for m in range(8):
-        assert_layer_equal(layer, oracle.encode(oc, decs, Wf[m], tables=tabs), cfg, m)
+    for m in range(n_mats):
+        enc = oracle.encode(oc, decs, oracle.to_f32(W[m]), tables=tabs)
+        np.testing.assert_array_equal(enc.idx, np.asarray(cols[m]))
+        assert_layer_equal(layer, enc, cfg, m)
 
 
-@pytest.mark.parametrize("d", [8, 16])
-def test_full_block_grouped_gemv(d, gpu):
-    """The bench's step at full size and in its launch configuration: the
-    Qwen3-8B-shaped block's four grouped GEMVs (q/k/v sharing x, o, gate/up
-    sharing x, down), one codec per projection category, rank-16 LoRA on the
-    q/k/v group; every output of every projection against the oracle's own
-    encoding of the same weights."""
+BLOCK_GROUPS = [(blk, d, grp) for blk in ("qwen3-8b", "qwen3-32b") for d in (8, 16)
+                for grp in ("qkv", "o", "gateup", "down")]
+
+
+@pytest.mark.parametrize("blk,d,grp", BLOCK_GROUPS, ids=[f"{b}-d{d}-{g}" for b, d, g in BLOCK_GROUPS])
+def test_full_block_grouped_gemv(blk, d, grp, gpu):
+    """One decode token through a transformer block's grouped GEMV at full size
+    and in the launch configuration of the layer stacks: the group's members
+    (q/k/v sharing x, o, gate/up sharing x, down) in one call, one codec per
+    projection category, rank-16 LoRA on every member. Every member's
+    encoding bit-exact and every output against the oracle."""
     cfg = bsq.Config(d=d, hidden=d)
     oc = ocfg(cfg)
-    projs = synth.qwen3_8b_block()
-    groups = {}
-    for p in projs:
-        groups.setdefault(p.group, []).append(p)
-    for gi, (gname, ps) in enumerate(groups.items()):
-        say(f"block group {gname} d={d}")
-        x = synth.activation(ps[0].d_in, seed=90 + gi, device=gpu)
-        xf = oracle.to_f32(x)
-        codecs, layers, encs, decs_l, loras = [], [], [], [], []
-        for p in ps:
-            decs = decoders(cfg, seed=100 + projs.index(p))
-            W, _ = synth.weight(p.d_out, p.d_in, seed=200 + projs.index(p), k_outliers=cfg.k(p.d_in), device=gpu)
-            codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
-            codecs.append(codec)
-            layers.append(bsq.bsq_encode(cfg, codec, W))
-            encs.append(oracle.encode(oc, decs, oracle.to_f32(W)))
-            decs_l.append(decs)
-            loras.append(synth.lora(p.d_out, p.d_in, 16, seed=300 + projs.index(p), device=gpu)
-                         if gname == "qkv" else None)
-            del W
-        lora_arg = loras if gname == "qkv" else None
-        ys = bsq.bsq_gemv(cfg, codecs, layers, x, loras=lora_arg, y_dtype=torch.bfloat16)
-        torch.cuda.synchronize()
-        for i, p in enumerate(ps):
-            lref = None if loras[i] is None else (oracle.to_f32(loras[i][0]), oracle.to_f32(loras[i][1]))
-            w_hat = oracle.decode(oc, decs_l[i], encs[i])
-            y_ref = oracle.dense_product(w_hat, xf, lref)
-            check_close(ys[i].float().cpu().numpy(), y_ref, 2e-2, f"{p.name} d={d}",
-                        rss=rss_terms(w_hat, xf, lref))
-            del w_hat
+    projs = synth.qwen3_8b_block() if blk == "qwen3-8b" else synth.qwen3_32b_block()
+    ps = [p for p in projs if p.group == grp]
+    say(f"block {blk} group {grp} d={d}: " + ", ".join(f"{p.name} {p.d_out}x{p.d_in}" for p in ps))
+    x = synth.activation(ps[0].d_in, seed=90 + len(grp), device=gpu)
+    xf = oracle.to_f32(x)
+    codecs, layers, encs, decs_l, loras, Ws = [], [], [], [], [], []
+    for p in ps:
+        pi = projs.index(p)
+        decs = decoders(cfg, seed=100 + pi)
+        W, cols = synth.weight(p.d_out, p.d_in, seed=200 + pi, k_outliers=cfg.k(p.d_in), device=gpu)
+        codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+        codecs.append(codec)
+        layers.append(bsq.bsq_encode(cfg, codec, W))
+        Ws.append(W)
+        decs_l.append(decs)
+        loras.append(synth.lora(p.d_out, p.d_in, 16, seed=300 + pi, device=gpu))
+    ys = bsq.bsq_gemv(cfg, codecs, layers, x, loras=loras, y_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    for i, p in enumerate(ps):
+        tabs = oracle.decoder_table(oc, decs_l[i])
+        enc = oracle.encode(oc, decs_l[i], oracle.to_f32(Ws[i]), tables=tabs)
+        assert_layer_equal(layers[i], enc, cfg)
+        lref = (oracle.to_f32(loras[i][0]), oracle.to_f32(loras[i][1]))
+        w_hat = oracle.decode(oc, decs_l[i], enc, tables=tabs)
+        y_ref = oracle.dense_product(w_hat, xf, lref)
+        check_product(ys[i].float().cpu().numpy(), y_ref, "gemv", cfg, enc, tabs, w_hat, xf, lref,
+                      f"{blk} {p.name} d={d}", torch.bfloat16)
+        del w_hat, enc
+
+
+# ---------------------------------------------------------------- term presence
+TERM_CASES = [
+    ("d8-table-300x1024", 300, 1024, dict(d=8, hidden=8), torch.bfloat16),
+    ("d16-symmetric-200x1024", 200, 1024, dict(d=16, hidden=16), torch.bfloat16),
+    ("d16-linear-130x768", 130, 768, dict(d=16, kind=bsq.DEC_LINEAR), torch.bfloat16),
+    ("d8-fp32x-256x512", 256, 512, dict(d=8, hidden=8), torch.float32),
+    ("d8-4096x4096", 4096, 4096, dict(d=8, hidden=8), torch.bfloat16),
+]
+
+
+def _terms_ref(enc, w_hat, X, lref):
+    """For activations X ([d_in] or [M, d_in]): the oracle's LoRA term
+    B (A x), the int8 protected term sum_p q8[:, p] scale_p x_idx_p and the
+    root sum of squares of its parts, and the sum of |terms| of the whole
+    product, per output (fp64, the shape of the product)."""
+    X64 = np.atleast_2d(np.asarray(X, dtype=np.float64))
+    A64, B64 = (np.asarray(v, dtype=np.float64) for v in lref)
+    q8 = enc.q8.astype(np.float64)
+    lora = (X64 @ A64.T) @ B64.T
+    sx = enc.scale.astype(np.float64)[None, :] * X64[:, enc.idx]
+    q8t = sx @ q8.T
+    q8sq = np.sqrt((sx ** 2) @ (q8 ** 2).T)
+    Xa = np.abs(X64)
+    total = Xa @ np.abs(w_hat.astype(np.float64)).T + (Xa @ np.abs(A64).T) @ np.abs(B64).T
+    out = (lora, q8t, q8sq, total)
+    return tuple(v[0] for v in out) if np.ndim(X) == 1 else out
+
+
+@pytest.mark.parametrize("case", TERM_CASES, ids=[c[0] for c in TERM_CASES])
+def test_gemv_lora_and_protected_terms(case, gpu):
+    """The LoRA term and the int8 protected term of bsq_gemv, each on its own:
+    y(x, with LoRA) - y(x) against the oracle's B (A x), and y(x) - y(x with
+    the protected inputs zeroed) against sum_p q8 scale_p x_idx_p, per output,
+    to within fp32 rounding (both terms are computed in fp32 from exact
+    products on every GEMV path)."""
+    name, d_out, d_in, kw, dtype = case
+    say(f"term presence {name}")
+    cfg, decs, codec, layer, W, encs, tabs = _make(name, d_out, d_in, kw, dtype, 1, False, gpu)
+    enc = encs[0]
+    x = synth.activation(d_in, seed=15, dtype=dtype)
+    A, Bm = synth.lora(d_out, d_in, 16, seed=16)
+    xd = x.to(gpu)
+    y_l = bsq.bsq_gemv(cfg, codec, layer, xd, loras=(A.to(gpu), Bm.to(gpu)), y_dtype=torch.float32)
+    y_0 = bsq.bsq_gemv(cfg, codec, layer, xd, y_dtype=torch.float32)
+    xm = x.clone()
+    xm[torch.as_tensor(enc.idx, dtype=torch.long)] = 0
+    y_m = bsq.bsq_gemv(cfg, codec, layer, xm.to(gpu), y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    xf = oracle.to_f32(x)
+    w_hat = oracle.decode(ocfg(cfg), decs, enc, tables=tabs)
+    lora, q8t, _, total = _terms_ref(enc, w_hat, xf, (oracle.to_f32(A), oracle.to_f32(Bm)))
+    y_l, y_0, y_m = (v.cpu().numpy() for v in (y_l, y_0, y_m))
+    assert term_bar(y_l, y_0, lora, total, 16, "LoRA term") > 100
+    assert term_bar(y_0, y_m, q8t, total, len(enc.idx), "int8 protected term") > 100
+
+
+@pytest.mark.parametrize("d,M", [(8, 16), (8, 64), (16, 16), (16, 256)])
+def test_gemm_lora_and_protected_terms(d, M, gpu):
+    """As for the GEMV, on the fused GEMM: the LoRA term (fp32) to within fp32
+    rounding; the protected term goes through the MFMA as bf16(q8 scale), so
+    its bar adds the sub-Gaussian bound of those roundings."""
+    say(f"gemm term presence d={d} M={M}")
+    cfg, decs, codec, layer, W, encs, tabs = _make("gemm-terms", 320, 2048, dict(d=d, hidden=d), torch.bfloat16,
+                                                   1, False, gpu)
+    enc = encs[0]
+    X = synth.activation(2048, seed=17, dtype=torch.bfloat16, batch=M)
+    A, Bm = synth.lora(320, 2048, 16, seed=18)
+    Xd = X.to(gpu)
+    Y_l = bsq.bsq_gemm(cfg, codec, layer, Xd, lora=(A.to(gpu), Bm.to(gpu)), y_dtype=torch.float32)
+    Y_0 = bsq.bsq_gemm(cfg, codec, layer, Xd, y_dtype=torch.float32)
+    Xm = X.clone()
+    Xm[:, torch.as_tensor(enc.idx, dtype=torch.long)] = 0
+    Y_m = bsq.bsq_gemm(cfg, codec, layer, Xm.to(gpu), y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    Xf = oracle.to_f32(X)
+    w_hat = oracle.decode(ocfg(cfg), decs, enc, tables=tabs)
+    Y_l, Y_0, Y_m = (v.cpu().numpy() for v in (Y_l, Y_0, Y_m))
+    lora, q8t, q8sq, total = _terms_ref(enc, w_hat, Xf, (oracle.to_f32(A), oracle.to_f32(Bm)))
+    assert term_bar(Y_l, Y_0, lora, total, 16, "LoRA term") > 100
+    assert term_bar(Y_0, Y_m, q8t, total, len(enc.idx), "int8 protected term", rounded=q8sq) > 10

@@ -6,7 +6,7 @@ layers).
 Bar as for the column axis: codes, gains, indices, int8 rows and scales
 bit-exact; coupled scores bit-exact (fp64, same order); fp32 decode
 bit-exact; products within 2e-2 relative (bf16 activations) or 1e-4 (fp32)
-with the floors of test_gpu_parity.
+with the derived floors of tests/parity_bounds.py.
 """
 import numpy as np
 import pytest
@@ -15,7 +15,7 @@ import torch
 import oracle
 import paper_2607_08643_amd as bsq
 import synth
-from test_gpu_parity import OKIND, check_close, decoders, np_codes, np_gains, rss_terms, say
+from test_gpu_parity import OKIND, check_product, decoders, gemv_kind, np_codes, np_gains, say
 
 pytestmark = pytest.mark.gpu
 
@@ -132,11 +132,8 @@ def test_row_protected_gemv(case, with_lora, gpu):
         for ydt in (torch.float32, torch.bfloat16):
             y = bsq.bsq_gemv(cfg, codec, layer.mat(m), x.to(gpu), loras=lora_dev, y_dtype=ydt)
             torch.cuda.synchronize()
-            if dtype == torch.float32 and ydt == torch.float32:
-                check_close(y.float().cpu().numpy(), y_ref, 1e-4, f"gemv m={m} y={ydt}")
-            else:
-                check_close(y.float().cpu().numpy(), y_ref, 2e-2, f"gemv m={m} y={ydt}",
-                            rss=rss_terms(w_hat, xf, lref))
+            check_product(y.float().cpu().numpy(), y_ref, gemv_kind(dtype), cfg, enc, tabs, w_hat, xf, lref,
+                          f"gemv m={m} y={ydt}", ydt)
 
 
 @pytest.mark.parametrize("d", [8, 16])
@@ -165,8 +162,8 @@ def test_row_protected_grouped_gemv(d, gpu):
         assert_rows_layer_equal(layers[i], enc, cfg)
         lref = (oracle.to_f32(loras[i][0]), oracle.to_f32(loras[i][1]))
         w_hat = oracle.decode(oc, decs, enc, tables=tabs)
-        check_close(ys[i].cpu().numpy(), oracle.dense_product(w_hat, xf, lref), 2e-2, f"group member {i}",
-                    rss=rss_terms(w_hat, xf, lref))
+        check_product(ys[i].cpu().numpy(), oracle.dense_product(w_hat, xf, lref), "gemv", cfg, enc, tabs, w_hat, xf,
+                      lref, f"group member {i}", torch.float32)
 
 
 @pytest.mark.parametrize("case", [ROWS[0], ROWS[1], ROWS[2]], ids=[c[0] for c in ROWS[:3]])
@@ -184,10 +181,10 @@ def test_row_protected_gemm(case, M, gpu):
     Xf = oracle.to_f32(X)
     w_hat = oracle.decode(oc, decs, encs[0], tables=tabs)
     lref = (oracle.to_f32(lora[0]), oracle.to_f32(lora[1]))
-    check_close(Y.cpu().numpy(), oracle.dense_product(w_hat, Xf, lref), 2e-2, "gemm fp32 out",
-                rss=rss_terms(w_hat, Xf, lref))
-    check_close(Yb.float().cpu().numpy(), oracle.dense_product(w_hat, Xf), 2e-2, "gemm bf16 out",
-                rss=rss_terms(w_hat, Xf))
+    check_product(Y.cpu().numpy(), oracle.dense_product(w_hat, Xf, lref), "gemm", cfg, encs[0], tabs, w_hat, Xf,
+                  lref, "gemm fp32 out", torch.float32)
+    check_product(Yb.float().cpu().numpy(), oracle.dense_product(w_hat, Xf), "gemm", cfg, encs[0], tabs, w_hat, Xf,
+                  None, "gemm bf16 out", torch.bfloat16)
 
 
 @pytest.mark.parametrize("axis", [0, 1], ids=["cols", "rows"])
@@ -286,10 +283,11 @@ def test_coupled_mlp_protection_end_to_end(gpu):
         enc = oracle.encode_set(oc, decs, oracle.to_f32(W), ref_idx)
         if oc_axis == 1:
             assert_rows_layer_equal(L, enc, cfg)
-        w_hat = oracle.decode(oc, decs, enc)
+        tabs = oracle.decoder_table(oc, decs)
+        w_hat = oracle.decode(oc, decs, enc, tables=tabs)
         vf = oracle.to_f32(v)
-        check_close(y.cpu().numpy(), oracle.dense_product(w_hat, vf), 2e-2, f"axis {oc_axis} product",
-                    rss=rss_terms(w_hat, vf))
+        check_product(y.cpu().numpy(), oracle.dense_product(w_hat, vf), "gemv", cfg, enc, tabs, w_hat, vf, None,
+                      f"axis {oc_axis} product", torch.float32)
 
 
 @pytest.mark.parametrize("d", [8, 16])
@@ -305,10 +303,11 @@ def test_row_axis_degenerate_cases(d, gpu):
         W, _ = synth.weight(70, 256, 17)
         codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
         layer = bsq.bsq_encode(cfg, codec, W.to(gpu))
-        enc = oracle.encode(oc, decs, oracle.to_f32(W))
+        tabs = oracle.decoder_table(oc, decs)
+        enc = oracle.encode(oc, decs, oracle.to_f32(W), tables=tabs)
         torch.cuda.synchronize()
         assert_rows_layer_equal(layer, enc, cfg)
-        w_hat = oracle.decode(oc, decs, enc)
+        w_hat = oracle.decode(oc, decs, enc, tables=tabs)
         got = bsq.bsq_decode(cfg, codec, layer)
         x = synth.activation(256, seed=3)
         y = bsq.bsq_gemv(cfg, codec, layer, x.to(gpu), y_dtype=torch.float32)
@@ -318,10 +317,10 @@ def test_row_axis_degenerate_cases(d, gpu):
         torch.cuda.synchronize()
         np.testing.assert_array_equal(got.cpu().numpy().view(np.uint32), w_hat.view(np.uint32))
         xf, Xf = oracle.to_f32(x), oracle.to_f32(X)
-        check_close(y.cpu().numpy(), oracle.dense_product(w_hat, xf), 2e-2, f"gemv rho={num}/{den}",
-                    rss=rss_terms(w_hat, xf))
-        check_close(Y.cpu().numpy(), oracle.dense_product(w_hat, Xf), 2e-2, f"gemm rho={num}/{den}",
-                    rss=rss_terms(w_hat, Xf))
+        check_product(y.cpu().numpy(), oracle.dense_product(w_hat, xf), "gemv", cfg, enc, tabs, w_hat, xf, None,
+                      f"gemv rho={num}/{den}", torch.float32)
+        check_product(Y.cpu().numpy(), oracle.dense_product(w_hat, Xf), "gemm", cfg, enc, tabs, w_hat, Xf, None,
+                      f"gemm rho={num}/{den}", torch.float32)
         assert Y0.shape == (0, 70)
         if num == den:
             # every row protected: the planes hold only zeros
