@@ -74,6 +74,8 @@ extern "C" {
 #define BSQ_MAX_HIDDEN 64
 #define BSQ_MAX_LORA_RANK 16
 #define BSQ_MAX_GROUP 8
+/* size of the library-owned workspace of bsq_gemv_noalloc, per GPU */
+#define BSQ_GEMV_NOALLOC_SCRATCH_BYTES (8u << 20)
 
 typedef enum {
     BSQ_OK = 0,
@@ -354,6 +356,25 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
                     const bsq_layer *layers, const bsq_lora *loras,
                     const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
                     void *ws, size_t ws_bytes, int32_t *err, void *stream);
+
+/* bsq_gemv for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc. The
+ * workspace is not an argument: the library keeps one zero-initialised
+ * device array of BSQ_GEMV_NOALLOC_SCRATCH_BYTES (8 MiB) per GPU, held until
+ * the process ends, and the call allocates nothing (no hipMalloc, hipFree or
+ * allocating library routine). Arguments, results and errors as bsq_gemv.
+ *   clear_scratch  1: zero-fill the array (a kernel on `stream`) before the
+ *                  product; needed only after a call reported
+ *                  BSQ_DEVERR_TIMEOUT or BSQ_DEVERR_POISONED (synchronise
+ *                  first). The first call on a GPU does this by itself.
+ * BSQ_ERR_BUFFER_TOO_SMALL when the group's bsq_workspace_bytes(GEMV, ...)
+ * exceeds the array (e.g. 2 x 25600 x 5120 at d = 8 needs 3.8 MiB). Every call
+ * on a GPU shares that GPU's array, which keeps the last call's contents:
+ * calls that overlap on one GPU (other streams, other host threads) race. */
+bsq_status bsq_gemv_noalloc(const bsq_config *cfg, int32_t n, const void *const *codecs,
+                            const bsq_layer *layers, const bsq_lora *loras,
+                            const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                            int32_t clear_scratch, int32_t *err, void *stream);
 
 /* Activation preparation of the GEMV: work that needs a reduction over all
  * of x, written into `ws` (one launch):

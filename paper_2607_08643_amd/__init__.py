@@ -10,6 +10,6 @@ from ._binding import (  # noqa: F401
     bsq_codec_bytes, bsq_codec_prepare, bsq_config, bsq_config_check, bsq_coupled_select, bsq_debug_set_wait_limit,
     bsq_decode, bsq_decode_stage, bsq_decoder,
     bsq_encode, bsq_encode_with_set,
-    bsq_gemm, bsq_gemv, bsq_layer, bsq_layer_sizes, bsq_lora, bsq_sizes, bsq_version, bsq_workspace_bytes,
+    bsq_gemm, bsq_gemv, bsq_gemv_noalloc, bsq_layer, bsq_layer_sizes, bsq_lora, bsq_sizes, bsq_version, bsq_workspace_bytes,
     layer_empty, lib, status_str,
 )

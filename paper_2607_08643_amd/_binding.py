@@ -22,6 +22,7 @@ MAX_STAGES = 4
 PITCH_ALIGN = 16
 MAX_LORA_RANK = 16
 MAX_GROUP = 8
+GEMV_NOALLOC_SCRATCH_BYTES = 8 << 20
 
 BSQ_OK, BSQ_ERR_ARG, BSQ_ERR_SHAPE, BSQ_ERR_DTYPE, BSQ_ERR_ALIGN = 0, 1, 2, 3, 4
 BSQ_ERR_BUFFER_TOO_SMALL, BSQ_ERR_NONFINITE, BSQ_ERR_DEVICE, BSQ_ERR_UNSUPPORTED = 5, 6, 7, 8
@@ -73,7 +74,7 @@ class bsq_sizes(ct.Structure):
 EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes", "bsq_workspace_bytes",
            "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemv_prepare",
            "bsq_gemv_run", "bsq_gemm", "bsq_encode_with_set", "bsq_coupled_select",
-           "bsq_debug_set_wait_limit", "bsq_decode_stage")
+           "bsq_debug_set_wait_limit", "bsq_decode_stage", "bsq_gemv_noalloc")
 
 # struct layouts above follow this version of include/bsq.h
 ABI_VERSION = 5
@@ -107,6 +108,7 @@ def lib():
     L.bsq_gemm.argtypes = [P, P, P, P, P, I32, I64, I64, P, I32, I64, P, SZ, P, P]
     L.bsq_debug_set_wait_limit.argtypes = [I32]
     L.bsq_decode_stage.argtypes = [P, P, P, I32, I32, P, P]
+    L.bsq_gemv_noalloc.argtypes = [P, I32, P, P, P, P, I32, P, I32, I32, P, P]
     L.bsq_encode_with_set.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
     L.bsq_coupled_select.argtypes = [P, P, P, P, I32, I64, I64, P, P, P, P, P, P, P, SZ, P]
     for f in EXPORTS[2:]:
@@ -525,6 +527,29 @@ def bsq_gemv(cfg: Config, codecs, layers, x: torch.Tensor, loras=None, y_dtype=t
     plan = GemvPlan(cfg, codecs, layers, x.contiguous(), loras, y_dtype, out, ws, err)
     ys = plan(stream)
     return ys[0] if single else ys
+
+
+def bsq_gemv_noalloc(cfg: Config, codecs, layers, x: torch.Tensor, loras=None, y_dtype=torch.bfloat16, out=None,
+                     clear_scratch=False, err=None, stream=None):
+    """bsq_gemv on the library's own scratch array (bsq_gemv_noalloc): no
+    workspace argument, nothing allocated by the call (outputs are allocated
+    here unless `out` is given)."""
+    single = isinstance(layers, Layer)
+    if single:
+        layers, codecs = [layers], [codecs]
+        loras = None if loras is None else [loras]
+    n = len(layers)
+    dev = x.device
+    outs = out if out is not None else [torch.empty(L.d_out, dtype=y_dtype, device=dev) for L in layers]
+    c = cfg.c()
+    cds = (ct.c_void_p * n)(*[cd.ptr() for cd in codecs])
+    lys = (bsq_layer * n)(*[L.c() for L in layers])
+    los = None if loras is None else (bsq_lora * n)(*[_lora_struct(l) for l in loras])
+    ys = (ct.c_void_p * n)(*[t.data_ptr() for t in outs])
+    _check(lib().bsq_gemv_noalloc(ct.byref(c), n, cds, lys, los, _ptr(x), _dtype_code(x.dtype), ys,
+                                  _dtype_code(outs[0].dtype), int(bool(clear_scratch)), _ptr(err), _stream(stream)),
+           "bsq_gemv_noalloc")
+    return outs[0] if single else outs
 
 
 def bsq_gemm(cfg: Config, codec: Codec, layer: Layer, X: torch.Tensor, lora=None, y_dtype=torch.bfloat16,

@@ -418,7 +418,7 @@ bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const 
     // the d = 16 symmetric decoder folds its output layer into x here
     if (!codecs && codec_has_split(*cfg) && x_dtype == BSQ_BF16) return BSQ_ERR_ARG;
     const CodedGroup g(*cfg, n, layers);
-    return from_hip(launch_gemv_prep(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, ws,
+    return from_hip(launch_gemv_prep(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, ws, false,
                                      static_cast<hipStream_t>(stream)));
 }
 
@@ -433,12 +433,34 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
     if (err && !aligned(err, 4)) return BSQ_ERR_ALIGN;
     hipStream_t st = static_cast<hipStream_t>(stream);
     const CodedGroup g(*cfg, n, layers);
-    if ((s = from_hip(launch_gemv_run(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, err,
+    if ((s = from_hip(launch_gemv_run(coded_cfg(*cfg), n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, false,
+                                      err, st))) != BSQ_OK)
+        return s;
+    if (!row_axis(*cfg)) return BSQ_OK;
+    return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
+}
+
+namespace {
+
+// bsq_gemv after validation, on a workspace of one configuration or on the
+// shared scratch array (scratch_layout)
+bsq_status gemv_launch(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                       const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                       void *ws, bool scratch_layout, int32_t *err, hipStream_t st)
+{
+    bsq_status s;
+    const bsq_config cc = coded_cfg(*cfg);
+    const CodedGroup g(*cfg, n, layers);
+    if ((s = from_hip(launch_gemv_prep(cc, n, codecs, g.L, loras, x, x_dtype, ws, scratch_layout, st))) != BSQ_OK)
+        return s;
+    if ((s = from_hip(launch_gemv_run(cc, n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, scratch_layout, err,
                                       st))) != BSQ_OK)
         return s;
     if (!row_axis(*cfg)) return BSQ_OK;
     return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
 }
+
+}  // namespace
 
 bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
                     const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
@@ -449,14 +471,37 @@ bsq_status bsq_gemv(const bsq_config *cfg, int32_t n, const void *const *codecs,
     if (s != BSQ_OK) return s;
     if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
     if (err && !aligned(err, 4)) return BSQ_ERR_ALIGN;
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    const bsq_config cc = coded_cfg(*cfg);
-    const CodedGroup g(*cfg, n, layers);
-    if ((s = from_hip(launch_gemv_prep(cc, n, codecs, g.L, loras, x, x_dtype, ws, st))) != BSQ_OK) return s;
-    if ((s = from_hip(launch_gemv_run(cc, n, codecs, g.L, loras, x, x_dtype, y, y_dtype, ws, err, st))) != BSQ_OK)
+    return gemv_launch(cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws, false, err,
+                       static_cast<hipStream_t>(stream));
+}
+
+bsq_status bsq_gemv_noalloc(const bsq_config *cfg, int32_t n, const void *const *codecs, const bsq_layer *layers,
+                            const bsq_lora *loras, const void *x, int32_t x_dtype, void *const *y, int32_t y_dtype,
+                            int32_t clear_scratch, int32_t *err, void *stream)
+{
+    if (!codecs || !y || !x || !layers) return BSQ_ERR_ARG;
+    if (clear_scratch != 0 && clear_scratch != 1) return BSQ_ERR_ARG;
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (n < 1 || n > BSQ_MAX_GROUP) return BSQ_ERR_ARG;
+    int64_t max_d_out = 0;
+    for (int m = 0; m < n; ++m) {
+        if ((s = check_shape(*cfg, layers[m].d_out, layers[m].d_in)) != BSQ_OK) return s;
+        max_d_out = layers[m].d_out > max_d_out ? layers[m].d_out : max_d_out;
+    }
+    // the group's workspace must fit the library's scratch array
+    if (!gemv_scratch_fits(coded_cfg(*cfg), n, max_d_out, layers[0].d_in)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    // everything bsq_gemv validates, with the array standing in for the
+    // workspace (it is 256-byte aligned and large enough)
+    if ((s = check_gemv(cfg, n, codecs, layers, loras, x_dtype, y, y_dtype, reinterpret_cast<void *>(uintptr_t(256)),
+                        size_t(BSQ_GEMV_NOALLOC_SCRATCH_BYTES))) != BSQ_OK)
         return s;
-    if (!row_axis(*cfg)) return BSQ_OK;
-    return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
+    if (!aligned(x, x_dtype == BSQ_F32 ? 4 : 16)) return BSQ_ERR_ALIGN;
+    if (err && !aligned(err, 4)) return BSQ_ERR_ALIGN;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    void *ws = nullptr;
+    if ((s = from_hip(gemv_scratch(clear_scratch != 0, &ws, st))) != BSQ_OK) return s;
+    return gemv_launch(cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws, true, err, st);
 }
 
 bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *layer, const bsq_lora *lora,

@@ -160,11 +160,20 @@ hipError_t launch_decode_stage(const bsq_config &cfg, const void *codec, const b
                                int accumulate, void *w_hat, hipStream_t st);
 
 size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in);
+// The device address of the current device's bsq_gemv_noalloc scratch array
+// (BSQ_GEMV_NOALLOC_SCRATCH_BYTES, 256-byte aligned); on the first call on a
+// device, or with `clear`, a zero-fill of the array is launched on `st`.
+hipError_t gemv_scratch(bool clear, void **ptr, hipStream_t st);
+// `scratch_layout`: ws is bsq_gemv_noalloc's shared scratch array, whose
+// layout does not depend on the call's shape (see make_args)
 hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
-                            const bsq_lora *loras, const void *x, int x_dtype, void *ws, hipStream_t st);
+                            const bsq_lora *loras, const void *x, int x_dtype, void *ws, bool scratch_layout,
+                            hipStream_t st);
 hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                            const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
-                           void *ws, int32_t *err, hipStream_t st);
+                           void *ws, bool scratch_layout, int32_t *err, hipStream_t st);
+// whether a group's workspace fits the scratch array in its scratch layout
+bool gemv_scratch_fits(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in);
 
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M);
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &layer,

@@ -19,6 +19,8 @@
 //    owns a 128-input segment of x~ and walks down rows, table lookups from
 //    global memory.
 //  * gemv_f32_kernel (fp32 activations): one wave per row, fp32 tables.
+#include <mutex>
+
 #include "bsq_internal.h"
 
 namespace bsq {
@@ -31,6 +33,9 @@ namespace {
 // a workspace shared by groups of different sizes keeps its slots at zero
 // between calls.
 constexpr size_t GEMV_HDR = 256;
+// bsq_gemv_noalloc's scratch array: the folded activation records of the
+// d = 16 symmetric decoder in its last 2 MiB, everything else from the front
+constexpr size_t GEMV_SCRATCH_XP_BYTES = size_t(2) << 20;
 constexpr size_t gemv_t_bytes() { return (size_t(BSQ_MAX_GROUP) * BSQ_MAX_LORA_RANK * 4 + 255) & ~size_t(255); }
 
 // The d = 16 symmetric decoder path (hidden width 16) evaluates the decoder
@@ -1072,7 +1077,8 @@ void launch_lane(int stages, const GemvArgs &a, int64_t blocks, size_t shm, hipS
 }
 
 GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
-                   const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype, void *ws)
+                   const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype, void *ws,
+                   bool scratch_layout)
 {
     GemvArgs a{};
     a.n = n;
@@ -1087,7 +1093,13 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
     float *wt = reinterpret_cast<float *>(wb);
     a.poison = static_cast<uint32_t *>(ws);
     a.spin_limit = wait_limit();
-    a.slots = reinterpret_cast<uint64_t *>(wb + gemv_t_bytes() + gemv_xp_bytes(cfg, a.pitch));
+    // workspace of one configuration: header, LoRA vectors, folded activation
+    // records, slots. The shared scratch array of bsq_gemv_noalloc keeps the
+    // records in its last GEMV_SCRATCH_XP_BYTES instead, so that the slots of
+    // every configuration start at the same offset and never overlap records
+    char *xp_base = scratch_layout ? static_cast<char *>(ws) + (BSQ_GEMV_NOALLOC_SCRATCH_BYTES - GEMV_SCRATCH_XP_BYTES)
+                                   : wb + gemv_t_bytes();
+    a.slots = reinterpret_cast<uint64_t *>(wb + gemv_t_bytes() + (scratch_layout ? 0 : gemv_xp_bytes(cfg, a.pitch)));
     for (int m = 0; m < n; ++m) {
         GemvMat &M = a.mat[m];
         const bsq_layer &L = layers[m];
@@ -1105,7 +1117,7 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
                 }
             }
         }
-        M.xp = reinterpret_cast<uint32_t *>(wb + gemv_t_bytes()) + int64_t(m) * cfg.stages * a.pitch * 16;
+        M.xp = reinterpret_cast<uint32_t *>(xp_base) + int64_t(m) * cfg.stages * a.pitch * 16;
         M.idx = L.prot_idx;
         M.q8 = L.prot_q8;
         M.scale = L.prot_scale;
@@ -1153,6 +1165,14 @@ size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_
            size_t(rg) * size_t(lane_slices(nblk, 1) - 1) * 64 * 8 + size_t(rg) * BSQ_MAX_LORA_RANK * 8;
 }
 
+bool gemv_scratch_fits(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in)
+{
+    const int64_t nblk = (d_in / cfg.d + BSQ_PITCH_ALIGN - 1) / BSQ_PITCH_ALIGN;
+    const size_t xp = gemv_xp_bytes(cfg, nblk * BSQ_PITCH_ALIGN);
+    return xp <= GEMV_SCRATCH_XP_BYTES &&
+           gemv_ws_bytes(cfg, n, max_d_out, d_in) - xp <= BSQ_GEMV_NOALLOC_SCRATCH_BYTES - GEMV_SCRATCH_XP_BYTES;
+}
+
 size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_rpb)
 {
     const int64_t words = (d_in + 31) / 32;
@@ -1162,7 +1182,8 @@ size_t gemv_stream_lds_bytes(const bsq_config &cfg, int64_t d_in, int64_t nseg_r
 }
 
 hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
-                            const bsq_lora *loras, const void *x, int x_dtype, void *ws, hipStream_t st)
+                            const bsq_lora *loras, const void *x, int x_dtype, void *ws, bool scratch_layout,
+                            hipStream_t st)
 {
     bool any = false;
     for (int m = 0; m < n && loras; ++m) any |= (loras[m].rank > 0);
@@ -1170,7 +1191,7 @@ hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *cod
     if (gemv_lane_path(cfg, x_dtype)) any = false;
     const bool fold = gemv_split16(cfg) && x_dtype == BSQ_BF16;
     if (!any && !fold) return hipSuccess;
-    const GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, nullptr, BSQ_F32, ws);
+    const GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, nullptr, BSQ_F32, ws, scratch_layout);
     const int lora_blocks = any ? n * BSQ_MAX_LORA_RANK : 0;
     const int64_t fold_blocks = fold ? int64_t(n) * cfg.stages * (a.pitch / 16) : 0;
     hipLaunchKernelGGL(gemv_prep_kernel, dim3(unsigned(lora_blocks + fold_blocks)), dim3(256), 0, st, a, lora_blocks);
@@ -1179,10 +1200,10 @@ hipError_t launch_gemv_prep(const bsq_config &cfg, int n, const void *const *cod
 
 hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *codecs, const bsq_layer *layers,
                            const bsq_lora *loras, const void *x, int x_dtype, void *const *y, int y_dtype,
-                           void *ws, int32_t *err, hipStream_t st)
+                           void *ws, bool scratch_layout, int32_t *err, hipStream_t st)
 {
     const int D = cfg.d, S = cfg.stages;
-    GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws);
+    GemvArgs a = make_args(cfg, n, codecs, layers, loras, x, x_dtype, y, y_dtype, ws, scratch_layout);
     a.err = err;
     int64_t rows_total = 0;
     for (int m = 0; m < n; ++m) rows_total += layers[m].d_out;
@@ -1261,6 +1282,60 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
     }
     const size_t shm = gemv_stream_lds_bytes(cfg, a.d_in, a.rpb * nseg);
     return launch_stream<16>(S, a, nt, int(blocks), shm, st);
+}
+
+// ---------------------------------------------------------------------------
+// The library-owned GEMV workspace of bsq_gemv_noalloc: one file-scope device
+// array per GPU. In host code `scratch` only names the symbol; the kernels get
+// its device address, taken once per device with hipGetSymbolAddress while
+// that device is current.
+// ---------------------------------------------------------------------------
+namespace {
+
+static __device__ __align__(256) uint8_t scratch[BSQ_GEMV_NOALLOC_SCRATCH_BYTES];
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[SCRATCH_MAX_DEVICES];
+bool g_scratch_cleared[SCRATCH_MAX_DEVICES];
+
+// zero-fill of the scratch array (a kernel, not a memset, so that a call
+// captured into a graph replays it correctly)
+__global__ __launch_bounds__(256) void scratch_clear_kernel(uint4 *p, int64_t n16)
+{
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n16; i += int64_t(gridDim.x) * 256)
+        p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+}  // namespace
+
+hipError_t gemv_scratch(bool clear, void **ptr, hipStream_t st)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return hipErrorInvalidDevice;
+    bool first = false;
+    {
+        std::lock_guard<std::mutex> lock(g_scratch_mutex);
+        if (!g_scratch_ptr[dev]) {
+            void *p = nullptr;
+            e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+            if (e != hipSuccess) return e;
+            if (!p || (reinterpret_cast<uintptr_t>(p) & 255)) return hipErrorInvalidSymbol;
+            g_scratch_ptr[dev] = p;
+        }
+        first = !g_scratch_cleared[dev];
+        g_scratch_cleared[dev] = true;
+        *ptr = g_scratch_ptr[dev];
+    }
+    if (first || clear) {
+        constexpr int64_t n16 = int64_t(BSQ_GEMV_NOALLOC_SCRATCH_BYTES) / 16;
+        hipLaunchKernelGGL(scratch_clear_kernel, dim3(unsigned(n16 / 256 / 16)), dim3(256), 0, st,
+                           static_cast<uint4 *>(*ptr), n16);
+        return hipGetLastError();
+    }
+    return hipSuccess;
 }
 
 }  // namespace bsq

@@ -219,6 +219,31 @@ def test_decode_gemv_gemm_reject_before_launch():
     assert gemm(err=FAKE + 1) == bsq.BSQ_ERR_ALIGN
 
 
+def test_gemv_noalloc_rejects_before_launch():
+    """bsq_gemv_noalloc validates on the host before it touches the device:
+    a group whose workspace exceeds the library's scratch array is refused
+    with BSQ_ERR_BUFFER_TOO_SMALL, bad arguments as bsq_gemv refuses them."""
+    cfg = bsq.Config()
+    c = cfg.c()
+    Lib = bsq.lib()
+    assert B.GEMV_NOALLOC_SCRATCH_BYTES == 8 << 20
+
+    def call(L, n=1, clear=0, x=FAKE, err=None):
+        return Lib.bsq_gemv_noalloc(ct.byref(c), n, (ct.c_void_p * 1)(FAKE), (B.bsq_layer * 1)(L), None,
+                                    x and ct.c_void_p(x), 1, (ct.c_void_p * 1)(FAKE), 1, clear,
+                                    err and ct.c_void_p(err), None)
+    # 32768 rows x 65536 inputs at d = 8: 512 row groups x 127 slices of
+    # flagged partial sums (33 MB), far more than the array holds
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 1, 32768, 65536) > 3 * B.GEMV_NOALLOC_SCRATCH_BYTES
+    assert call(_fake_layer(cfg, 32768, 65536)) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    L = _fake_layer(cfg, 64, 256)
+    assert call(L, clear=2) == bsq.BSQ_ERR_ARG
+    assert call(L, n=0) == bsq.BSQ_ERR_ARG
+    assert call(L, x=0) == bsq.BSQ_ERR_ARG
+    assert call(L, x=FAKE + 2) == bsq.BSQ_ERR_ALIGN
+    assert call(L, err=FAKE + 1) == bsq.BSQ_ERR_ALIGN
+
+
 def test_wait_limit_is_settable_and_restorable():
     """bsq_debug_set_wait_limit returns the previous bound; a negative value
     restores the default (host state only, no launch)."""
