@@ -68,6 +68,7 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c)
                                            false);
 }
 
+
 __device__ __forceinline__ float half_lo(uint32_t w) { return f16_bits_to_f32(uint16_t(w & 0xffffu)); }
 __device__ __forceinline__ float half_hi(uint32_t w) { return f16_bits_to_f32(uint16_t(w >> 16)); }
 
@@ -562,8 +563,10 @@ __device__ __forceinline__ float lane_group(const LaneBlk<8, S> &b, int z, const
         const uint32_t g1 = (z & 1) ? gq.w : gq.y;
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
-            const uint32_t code = (cw >> (8 * kk)) & 0xffu;
-            const uint4 e = s_tab[s * 256 + code];
+            // byte offset of the code's 16-byte entry (one shift of the
+            // selected byte; the stage's base is the instruction's offset)
+            const uint32_t off = ((cw >> (8 * kk)) & 0xffu) << 4;
+            const uint4 e = *reinterpret_cast<const uint4 *>(reinterpret_cast<const char *>(s_tab + s * 256) + off);
             float dsum = dot2_bf16(e.x, xz[4 * kk + 0], 0.0f);
             dsum = dot2_bf16(e.y, xz[4 * kk + 1], dsum);
             dsum = dot2_bf16(e.z, xz[4 * kk + 2], dsum);
@@ -780,10 +783,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // [S][RCH chunks] 64-byte slots
     constexpr int RCH = WV * TPW * 16;
     constexpr int REC = (D == 8) ? 0 : S * RCH * 4;  // uint4 units
+    // the table in static LDS (its address is a constant the compiler folds
+    // into each lookup's offset), the rest in the dynamic allocation
+    __shared__ __attribute__((aligned(16))) uint4 s_tab_mem[TAB];
     extern __shared__ uint4 s_mem[];
-    uint4 *s_tab = s_mem;
-    uint4 *s_rec = s_mem + TAB;
-    float *s_red = reinterpret_cast<float *>(s_mem + TAB + REC);  // [WV][64] wave sums
+    uint4 *s_tab = s_tab_mem;
+    uint4 *s_rec = s_mem;
+    float *s_red = reinterpret_cast<float *>(s_mem + REC);  // [WV][64] wave sums
     float *s_xs = s_red + WV * 64;                             // [kp] scale_p * x_{idx_p}
     const int64_t kp = q8_pitch(a.k);
     int8_t *s_q8 = reinterpret_cast<int8_t *>(s_xs + kp);      // [64][kp] int8 rows (finishing slice)
@@ -807,8 +813,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // through the pipelined loop, a ragged last tile of the row (d_in not a
     // multiple of 128) is handled after it
     const int64_t full_blocks = (D == 8) ? (a.d_in / 8) / 16 : nblk;  // d = 16: padding chunks read zeros
-    const int64_t b0 = (q * WV + wave) * TPW;
-    const int64_t b1 = (b0 + TPW < nblk) ? b0 + TPW : nblk;
+    // the row group's nblk tiles are shared out evenly over its Q * WV waves
+    // (floor or ceil of nblk / (Q WV) each, at most TPW), in order, so no wave
+    // is left idle while another carries a whole extra tile set
+    const int64_t nw = Q * WV, wq = q * WV + wave;
+    const int64_t b0 = (wq * nblk) / nw;
+    const int64_t b1 = ((wq + 1) * nblk) / nw;
+    const int64_t sb0 = (q * nblk) / Q;  // the slice's first block (wave 0's b0)
     const int64_t nt = ((b1 < full_blocks) ? b1 : full_blocks) - b0;  // may be <= 0
     const bool ragged = b0 <= full_blocks && full_blocks < b1;
     const bool fin = q == Q - 1;  // this slice finishes the row group
@@ -831,7 +842,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
         // the slice's records, 16 per wave instruction (four lanes per 64-byte
         // slot); chunks past the row's padded end read the last slot (unused)
         static_assert((S * RCH / 16) % WV == 0, "record chunks are shared out evenly");
-        const int64_t c0 = q * RCH;  // the slice's first chunk
+        const int64_t c0 = sb0 * 16;  // the slice's first chunk (the slice spans at most RCH chunks)
 #pragma unroll
         for (int r = 0; r < S * RCH / 16 / WV; ++r) {
             const int e = r * WV + wave;
@@ -856,7 +867,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     __builtin_amdgcn_sched_barrier(0);
     // a wave without a full tile works on the slice's first block (always a
     // real block) and drops the result
-    const int64_t blast = (nt > 0) ? b0 + nt - 1 : q * WV * TPW;
+    const int64_t blast = (nt > 0) ? b0 + nt - 1 : sb0;
     LaneBlk<D, S> buf[PF];
 #pragma unroll
     for (int u = 0; u < PF; ++u) lane_load<D, S>(buf[u], M, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
@@ -882,22 +893,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // so that the per-tile bitmap load is unconditional
     const cx4_ptr bsrc = (a.k > 0) ? (cx4_ptr)(M.bits) : (cx4_ptr)(a.x);
     const uint32_t kmask = (a.k > 0) ? ~0u : 0u;
-    // the wave's TPW tiles as straight-line code with PF tiles in flight (no
+    // the wave's tiles as straight-line code with PF tiles in flight (no
     // loop, so the waits before each tile count exactly the loads issued
     // after it); tile indices are clamped to the wave's last full tile so
-    // every load is unconditional, and the sums of tiles past nt are dropped
+    // every load is unconditional, and the tiles past nt (a wave with one
+    // tile fewer than TPW, or none) are loaded but not computed
     float acc = 0.0f;
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
         const int64_t b = (b0 + u < blast) ? b0 + u : blast;
-        float ts;
-        // (a dropped tile reads its activations from the decoder table, which
-        // is at least 4 KiB, so that no read goes past a short row's x)
-        if constexpr (D == 8)
-            ts = lane_tile<S>(buf[u % PF], (u < nt) ? xv + 4 * b : (cx16_ptr)(M.tab16[0]), bsrc, kmask, b, s_tab,
-                              0.0f);
-        else ts = lane_tile16<S>(buf[u % PF], s_rec, RCH, int(b - q * WV * TPW), s_tab, 0.0f);
-        acc += (u < nt) ? ts : 0.0f;
+        if (u < nt) {
+            if constexpr (D == 8) acc += lane_tile<S>(buf[u % PF], xv + 4 * b, bsrc, kmask, b, s_tab, 0.0f);
+            else acc += lane_tile16<S>(buf[u % PF], s_rec, RCH, int(b - sb0), s_tab, 0.0f);
+        }
         if (u + PF < TPW)
             lane_load<D, S>(buf[u % PF], M, tbase + (((b0 + u + PF < blast) ? b0 + u + PF : blast) << 10));
     }
@@ -1137,20 +1145,21 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
 
 }  // namespace
 
-// Row-lane kernel: a workgroup (4 waves) covers 4 * TPW consecutive tiles of
-// one 64-row group, so a row group has Q = ceil(nblk / (4 TPW)) slices. TPW is
-// the largest of 4, 2, 1 whose grid still holds LANE_MIN_WAVES waves (half of
-// the 4096 wave slots of 256 compute units at four waves per SIMD): fewer,
-// longer waves where the matrix is large, more slices where it is small.
+// Row-lane kernel: a workgroup (4 waves) covers up to 4 * TPW consecutive
+// tiles of one 64-row group, so a row group has Q = ceil(nblk / (4 TPW))
+// slices, its nblk tiles shared evenly over the Q * 4 waves.
+// LANE_MIN_WAVES is half of the 4096 wave slots of 256 compute units at
+// four waves per SIMD.
 constexpr int64_t LANE_MIN_WAVES = 2048;
 
 int64_t lane_slices(int64_t nblk, int tpw) { return (nblk + 4 * tpw - 1) / (4 * tpw); }
 
 int lane_tpw(int64_t row_groups, int64_t nblk)
 {
-    for (int tpw = 4; tpw > 1; tpw >>= 1)
-        if (row_groups * lane_slices(nblk, tpw) * 4 >= LANE_MIN_WAVES) return tpw;
-    return 1;
+    // two tiles per wave measured fastest on the Qwen3-shaped launches
+    // (1024 to 51200 rows, 4096 to 25600 inputs), with the tiles shared out
+    // evenly; one where two would leave fewer than LANE_MIN_WAVES waves
+    return (row_groups * lane_slices(nblk, 2) * 4 >= LANE_MIN_WAVES) ? 2 : 1;
 }
 
 size_t gemv_ws_bytes(const bsq_config &cfg, int64_t n, int64_t max_d_out, int64_t d_in)
@@ -1235,11 +1244,17 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
         a.lora_blocks = lora_blocks;
         blocks += lora_blocks;
         const int64_t kp = q8_pitch(a.k);
-        const size_t tab = (D == 8) ? size_t(S) * 256 * 16 : size_t(S) * 1024 * 16 + size_t(S) * 4 * tpw * 16 * 64;
-        const size_t shm = tab + 4 * 64 * 4 + size_t(kp) * 4 + ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
+        // dynamic LDS: the d = 16 records, wave sums, scaled protected
+        // activations, the finishing slice's int8 rows (the table is static)
+        const size_t rec = (D == 8) ? 0 : size_t(S) * 4 * tpw * 16 * 64;
+        const size_t shm = rec + 4 * 64 * 4 + size_t(kp) * 4 + ((kp <= LANE_Q8_LDS_MAX) ? size_t(64 * kp) : 0);
         if (D == 8) {
             switch (tpw) {
+            case 8: launch_lane<8, 8>(S, a, blocks, shm, st); break;
+            case 6: launch_lane<8, 6>(S, a, blocks, shm, st); break;
+            case 5: launch_lane<8, 5>(S, a, blocks, shm, st); break;
             case 4: launch_lane<8, 4>(S, a, blocks, shm, st); break;
+            case 3: launch_lane<8, 3>(S, a, blocks, shm, st); break;
             case 2: launch_lane<8, 2>(S, a, blocks, shm, st); break;
             default: launch_lane<8, 1>(S, a, blocks, shm, st); break;
             }
