@@ -64,9 +64,10 @@ def parse():
     p.add_argument("--d", type=int, default=8, help="chunk length of the headline")
     p.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     p.add_argument("--headline-only", action="store_true", help="only the headline stack and its roofline")
-    p.add_argument("--profile", choices=["c5-gateup", "gemm"], default=None,
-                   help="rocprofv3 runs: only the headline's gate/up GEMV launches (c5-gateup) or the batched "
-                        "GEMMs (gemm), plus the 256 MiB calibration copy")
+    p.add_argument("--profile", choices=["c5", "gemm"], default=None,
+                   help="rocprofv3 runs: only the headline stack's encode, its gate/up GEMV launches and a bf16 "
+                        "decode of 8 gate matrices (c5), or the batched GEMMs (gemm), plus the 256 MiB "
+                        "calibration copy")
     return p.parse_args()
 
 
@@ -500,8 +501,14 @@ def main():
     # headline: the 64-layer Qwen3-32B-shaped stack, one decode token per step
     log(f"[bench] encoding the 64-layer Qwen3-32B-shaped stack at d={d}")
     c5 = Stack(bsq, synth, torch, synth.qwen3_32b_block(), 64, d, 0, dev, seed=7000)
-    if args.profile == "c5-gateup":
+    if args.profile == "c5":
         c5.group_launch_us("gateup", s, reps=3)
+        L0 = c5.layers["gate"].mat(0)
+        W_hat = torch.empty((L0.d_out, L0.d_in), dtype=torch.bfloat16, device=dev)
+        for r in range(8):
+            bsq.bsq_decode(c5.cfg, c5.codecs["gate"], c5.layers["gate"].mat(r), out=W_hat)
+        torch.cuda.synchronize()
+        del W_hat
         copy_reference(torch, dev)
         return
     ms = c5.time_tokens(s, args.warmup, args.steps)
