@@ -36,7 +36,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 SRC = os.path.join(HERE, "bsq_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
-KIND_IDENTITY, KIND_LINEAR, KIND_MLP = 0, 1, 2
+KIND_IDENTITY, KIND_LINEAR, KIND_MLP, KIND_MLP_RES1 = 0, 1, 2, 3
+FMT_INT8, FMT_E4M3, FMT_E5M2 = 0, 1, 2   # protected payload formats
 ORC_OK, ORC_ERR_ARG, ORC_ERR_NONFINITE = 0, 1, 6
 PITCH_ALIGN = 16  # rows of the code/gain planes are padded to 16 chunks
 
@@ -74,20 +75,26 @@ def lib():
         L.orc_gain_to_f16.restype = ct.c_uint16
         L.orc_code_scale.argtypes = [I32]
         L.orc_code_scale.restype = ct.c_float
-        L.orc_decoder_eval.argtypes = [I32, I32, I32, I32, P, P, P, P, ct.c_uint32, P]
-        L.orc_decoder_table.argtypes = [I32, I32, I32, I32, P, P, P, P, P]
+        L.orc_decoder_eval.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, ct.c_uint32, P]
+        L.orc_decoder_table.argtypes = [I32, I32, I32, I32, P, P, P, P, P, P, P]
+        L.orc_payload_max.argtypes = [I32]
+        L.orc_payload_max.restype = ct.c_float
+        L.orc_payload_value.argtypes = [ct.c_uint8, I32]
+        L.orc_payload_value.restype = ct.c_float
+        L.orc_payload_quant.argtypes = [ct.c_float, I32]
+        L.orc_payload_quant.restype = ct.c_uint8
         L.orc_column_keys.argtypes = [P, I64, I64, P, P]
         L.orc_protect_select.argtypes = [P, I64, I64, P, I64, P, P]
-        L.orc_q8.argtypes = [P, I64, I64, P, I64, P, P]
-        L.orc_encode.argtypes = [I32, I32, P, P, I64, I64, P, I64, I64, P, P, P, P, P, I32]
-        L.orc_decode.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, P, I32]
-        L.orc_gemv_fused.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64,
+        L.orc_q8.argtypes = [P, I64, I64, P, I64, I32, P, P]
+        L.orc_encode.argtypes = [I32, I32, P, P, I64, I64, P, I64, I64, I32, P, P, P, P, P, I32]
+        L.orc_decode.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, I32, P, I32]
+        L.orc_gemv_fused.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, I32,
                                      P, I32, P, P, P, I32]
         L.orc_topk.argtypes = [P, I64, I64, P]
         L.orc_row_keys.argtypes = [P, I64, I64, P, P]
         L.orc_coupled_select.argtypes = [P, P, P, I64, I64, P, P, P, I64, P, P]
-        L.orc_q8_rows.argtypes = [P, I64, I64, P, I64, P, P]
-        L.orc_encode_set.argtypes = [I32, I32, P, P, I64, I64, I32, P, I64, I64, P, P, P, P, I32]
+        L.orc_q8_rows.argtypes = [P, I64, I64, P, I64, I32, P, P]
+        L.orc_encode_set.argtypes = [I32, I32, P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P, I32]
         L.orc_max_threads.restype = I32
         for f in ("orc_decoder_eval", "orc_decoder_table", "orc_protect_select",
                   "orc_encode", "orc_decode", "orc_gemv_fused", "orc_topk", "orc_coupled_select",
@@ -123,6 +130,7 @@ class Config:
     protect_num: int = 1
     protect_den: int = 100
     protect_axis: int = 0   # 0: input columns, 1: output rows
+    protect_format: int = FMT_INT8  # payload of the protected slices
 
     def k(self, d_in: int) -> int:
         """k = ceil(rho * n), rho = num/den, in integer arithmetic, for n
@@ -146,7 +154,7 @@ class Encoded:
     codes: list          # per stage: uint8/uint16 [d_out, pitch]
     gains: list          # per stage: uint16 (fp16 bits) [d_out, pitch]
     idx: np.ndarray      # int32 [k]
-    q8: np.ndarray       # int8 [d_out, k] (axis 0) or [k, d_in] (axis 1)
+    q8: np.ndarray       # payload bytes (int8 view) [d_out, k] (axis 0) or [k, d_in] (axis 1)
     scale: np.ndarray    # fp32 [k]
     pitch: int = 0
     d_out: int = 0
@@ -158,11 +166,18 @@ def _f32(a) -> np.ndarray:
     return np.ascontiguousarray(a, dtype=np.float32)
 
 
+def _dec_params(dec):
+    """W1, b1, W2, b2, R, c of one stage decoder as fp32 arrays (None where
+    the decoder object has no such tensor; R and c only for the res1 kind)."""
+    vals = (dec.W1, dec.b1, dec.W2, dec.b2, getattr(dec, "R", None), getattr(dec, "c", None))
+    return tuple(None if v is None else _f32(v) for v in vals)
+
+
 def decoder_eval(cfg: Config, dec, code: int) -> np.ndarray:
     y = np.zeros(cfg.d, dtype=np.float32)
-    W1, b1, W2, b2 = (None if v is None else _f32(v) for v in (dec.W1, dec.b1, dec.W2, dec.b2))
+    W1, b1, W2, b2, R, c = _dec_params(dec)
     rc = lib().orc_decoder_eval(cfg.kind, cfg.d, cfg.b, cfg.hidden, _p(W1), _p(b1), _p(W2),
-                                _p(b2), code, _p(y))
+                                _p(b2), _p(R), _p(c), code, _p(y))
     _check(rc, "decoder_eval")
     return y
 
@@ -171,9 +186,9 @@ def decoder_table(cfg: Config, decs) -> list:
     out = []
     for dec in decs[:cfg.stages]:
         t = np.zeros((1 << cfg.b, cfg.d), dtype=np.float32)
-        W1, b1, W2, b2 = (None if v is None else _f32(v) for v in (dec.W1, dec.b1, dec.W2, dec.b2))
+        W1, b1, W2, b2, R, c = _dec_params(dec)
         rc = lib().orc_decoder_table(cfg.kind, cfg.d, cfg.b, cfg.hidden, _p(W1), _p(b1),
-                                     _p(W2), _p(b2), _p(t))
+                                     _p(W2), _p(b2), _p(R), _p(c), _p(t))
         _check(rc, "decoder_table")
         out.append(t)
     return out
@@ -228,25 +243,45 @@ def coupled_select(w_gate, w_up, w_down, k: int, g_gate=None, g_up=None, g_down=
     return idx[:k].copy(), score[:d_ffn].copy()
 
 
-def q8_rows(w: np.ndarray, idx: np.ndarray):
+def payload_max(fmt: int = FMT_INT8) -> float:
+    return float(lib().orc_payload_max(fmt))
+
+
+def payload_value(q: int, fmt: int = FMT_INT8) -> float:
+    """The value of one stored protected byte (0..255) in format fmt."""
+    return float(lib().orc_payload_value(int(q) & 0xFF, fmt))
+
+
+def payload_quant(v: float, fmt: int = FMT_INT8) -> int:
+    """The stored byte (0..255) of the scaled value v in format fmt."""
+    return int(lib().orc_payload_quant(float(v), fmt))
+
+
+def payload_values(q: np.ndarray, fmt: int = FMT_INT8) -> np.ndarray:
+    """fp32 values of an array of stored bytes (any integer dtype of 8 bits)."""
+    table = np.array([payload_value(v, fmt) for v in range(256)], dtype=np.float32)
+    return table[np.asarray(q).view(np.uint8)]
+
+
+def q8_rows(w: np.ndarray, idx: np.ndarray, fmt: int = FMT_INT8):
     w = _f32(w)
     d_out, d_in = w.shape
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     k = len(idx)
     q = np.zeros((max(k, 1), d_in), dtype=np.int8)
     s = np.zeros(max(k, 1), dtype=np.float32)
-    lib().orc_q8_rows(_p(w), d_out, d_in, _p(idx), k, _p(q), _p(s))
+    lib().orc_q8_rows(_p(w), d_out, d_in, _p(idx), k, fmt, _p(q), _p(s))
     return q[:k].copy(), s[:k].copy()
 
 
-def q8(w: np.ndarray, idx: np.ndarray):
+def q8(w: np.ndarray, idx: np.ndarray, fmt: int = FMT_INT8):
     w = _f32(w)
     d_out, d_in = w.shape
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     k = len(idx)
     q = np.zeros((d_out, max(k, 1)), dtype=np.int8)
     s = np.zeros(max(k, 1), dtype=np.float32)
-    lib().orc_q8(_p(w), d_out, d_in, _p(idx), k, _p(q), _p(s))
+    lib().orc_q8(_p(w), d_out, d_in, _p(idx), k, fmt, _p(q), _p(s))
     return q[:, :k].copy(), s[:k].copy()
 
 
@@ -273,7 +308,7 @@ def encode(cfg: Config, decs, w: np.ndarray, g=None, nthreads: int = 0,
     s = np.zeros(max(k, 1), dtype=np.float32)
     g = None if g is None else _f32(g)
     rc = lib().orc_encode(cfg.d, cfg.stages, _ptr_array(tables), _p(w), d_out, d_in, _p(g), k, P,
-                          _ptr_array(codes), _ptr_array(gains), _p(idx), _p(q), _p(s), nthreads)
+                          cfg.protect_format, _ptr_array(codes), _ptr_array(gains), _p(idx), _p(q), _p(s), nthreads)
     _check(rc, "encode")
     return Encoded(codes, gains, idx[:k].copy(), np.ascontiguousarray(q[:, :k]), s[:k].copy(),
                    P, d_out, d_in)
@@ -298,7 +333,7 @@ def encode_set(cfg: Config, decs, w: np.ndarray, idx, nthreads: int = 0, tables=
     s = np.zeros(max(k, 1), dtype=np.float32)
     idx_arg = idx if k else np.zeros(1, np.int32)
     rc = lib().orc_encode_set(cfg.d, cfg.stages, _ptr_array(tables), _p(w), d_out, d_in, axis,
-                              _p(idx_arg), k, P, _ptr_array(codes), _ptr_array(gains), _p(q), _p(s),
+                              _p(idx_arg), k, P, cfg.protect_format, _ptr_array(codes), _ptr_array(gains), _p(q), _p(s),
                               nthreads)
     _check(rc, "encode_set")
     q = q[:k] if axis == 1 else q[:, :k]
@@ -314,10 +349,10 @@ def decode(cfg: Config, decs, enc: Encoded, nthreads: int = 0, tables=None) -> n
     if enc.axis == 1:
         rc = lib().orc_decode(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
                               _ptr_array(enc.codes), _ptr_array(enc.gains), None, None, None, 0,
-                              _p(w_hat), nthreads)
+                              cfg.protect_format, _p(w_hat), nthreads)
         _check(rc, "decode")
         for p, i in enumerate(enc.idx):
-            w_hat[i, :] = enc.q8[p].astype(np.float32) * np.float32(enc.scale[p])
+            w_hat[i, :] = payload_values(enc.q8[p], cfg.protect_format) * np.float32(enc.scale[p])
         return w_hat
     k = len(enc.idx)
     idx = enc.idx if k else np.zeros(1, np.int32)
@@ -325,7 +360,7 @@ def decode(cfg: Config, decs, enc: Encoded, nthreads: int = 0, tables=None) -> n
     s = enc.scale if k else np.zeros(1, np.float32)
     rc = lib().orc_decode(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
                           _ptr_array(enc.codes), _ptr_array(enc.gains), _p(idx),
-                          _p(np.ascontiguousarray(q)), _p(s), k, _p(w_hat), nthreads)
+                          _p(np.ascontiguousarray(q)), _p(s), k, cfg.protect_format, _p(w_hat), nthreads)
     _check(rc, "decode")
     return w_hat
 
@@ -342,7 +377,8 @@ def gemv_fused(cfg: Config, decs, enc: Encoded, x, lora=None, nthreads: int = 0,
                         np.zeros(0, np.float32), enc.pitch, enc.d_out, enc.d_in, 0)
         y = gemv_fused(cfg, decs, plain, x64, lora, nthreads, tables)
         for p, i in enumerate(enc.idx):
-            acc = float(enc.scale[p]) * float(np.dot(enc.q8[p].astype(np.float64), x64))
+            acc = float(enc.scale[p]) * float(np.dot(payload_values(enc.q8[p], cfg.protect_format)
+                                                     .astype(np.float64), x64))
             if lora is not None:
                 A64 = np.asarray(lora[0], dtype=np.float64)
                 B64 = np.asarray(lora[1], dtype=np.float64)
@@ -361,7 +397,7 @@ def gemv_fused(cfg: Config, decs, enc: Encoded, x, lora=None, nthreads: int = 0,
         rank = A64.shape[0]
     rc = lib().orc_gemv_fused(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in,
                               enc.pitch, _ptr_array(enc.codes), _ptr_array(enc.gains), _p(idx),
-                              _p(np.ascontiguousarray(q)), _p(s), k, _p(x64), rank, _p(A64),
+                              _p(np.ascontiguousarray(q)), _p(s), k, cfg.protect_format, _p(x64), rank, _p(A64),
                               _p(B64), _p(y), nthreads)
     _check(rc, "gemv_fused")
     return y
@@ -393,6 +429,8 @@ def gemm(cfg: Config, decs, enc: Encoded, X, lora=None, nthreads: int = 0) -> np
 def decoder_param_count(cfg: Config) -> int:
     if cfg.kind == KIND_MLP:
         return cfg.hidden * cfg.b + cfg.hidden + cfg.d * cfg.hidden + cfg.d
+    if cfg.kind == KIND_MLP_RES1:
+        return cfg.hidden * cfg.b + cfg.hidden + cfg.hidden * cfg.hidden + cfg.hidden + cfg.d * cfg.hidden + cfg.d
     if cfg.kind == KIND_LINEAR:
         return cfg.d * cfg.b + cfg.d
     return 0

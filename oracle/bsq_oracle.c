@@ -35,6 +35,11 @@
 #define KIND_IDENTITY 0
 #define KIND_LINEAR 1
 #define KIND_MLP 2
+#define KIND_MLP_RES1 3
+
+#define FMT_INT8 0
+#define FMT_E4M3 1
+#define FMT_E5M2 2
 
 #define MAX_CODE_BITS 16
 #define MAX_HIDDEN 256
@@ -105,10 +110,17 @@ float orc_code_scale(int b)
  *  linear:   y_m = beta_m + sum_j M[m][j] q_j          (fmaf chain over j)
  *  mlp:      a_k = relu(b1_k + sum_j W1[k][j] q_j)      (fmaf chain over j)
  *            y_m = b2_m + sum_k W2[m][k] a_k            (fmaf chain over k)
+ *  mlp with one residual block (the symmetric decoder's res1 row of the
+ *  codec ablation; reading: the block acts on the hidden layer):
+ *            a_k as above;
+ *            t_k = relu(cr_k + sum_l R[k][l] a_l)       (fmaf chain over l)
+ *            a'_k = a_k + t_k                           (one fp32 add)
+ *            y_m = b2_m + sum_k W2[m][k] a'_k           (fmaf chain over k)
  *  relu(a) = (a > 0) ? a : +0.0f. */
 int orc_decoder_eval(int kind, int d, int b, int h,
                      const float *W1, const float *b1,
                      const float *W2, const float *b2,
+                     const float *R, const float *cr,
                      uint32_t code, float *y)
 {
     if (b < 1 || b > MAX_CODE_BITS || d < 1 || d > MAX_CODE_BITS) return ORC_ERR_ARG;
@@ -124,13 +136,23 @@ int orc_decoder_eval(int kind, int d, int b, int h,
             for (int j = 0; j < b; ++j) acc = fmaf(W1[m * b + j], q[j], acc);
             y[m] = acc;
         }
-    } else if (kind == KIND_MLP) {
+    } else if (kind == KIND_MLP || kind == KIND_MLP_RES1) {
         if (h < 1 || h > MAX_HIDDEN) return ORC_ERR_ARG;
         float a[MAX_HIDDEN];
         for (int k = 0; k < h; ++k) {
             float acc = b1[k];
             for (int j = 0; j < b; ++j) acc = fmaf(W1[k * b + j], q[j], acc);
             a[k] = (acc > 0.0f) ? acc : 0.0f;
+        }
+        if (kind == KIND_MLP_RES1) {
+            if (!R || !cr) return ORC_ERR_ARG;
+            float t[MAX_HIDDEN];
+            for (int k = 0; k < h; ++k) {
+                float acc = cr[k];
+                for (int l = 0; l < h; ++l) acc = fmaf(R[k * h + l], a[l], acc);
+                t[k] = (acc > 0.0f) ? acc : 0.0f;
+            }
+            for (int k = 0; k < h; ++k) a[k] = a[k] + t[k];
         }
         for (int m = 0; m < d; ++m) {
             float acc = b2[m];
@@ -147,11 +169,12 @@ int orc_decoder_eval(int kind, int d, int b, int h,
  * above evaluated for each of the 2^b codes (memoised; same bits). */
 int orc_decoder_table(int kind, int d, int b, int h,
                       const float *W1, const float *b1,
-                      const float *W2, const float *b2, float *table)
+                      const float *W2, const float *b2,
+                      const float *R, const float *c, float *table)
 {
     uint32_t n = 1u << b;
     for (uint32_t code = 0; code < n; ++code) {
-        int rc = orc_decoder_eval(kind, d, b, h, W1, b1, W2, b2, code, table + (size_t)code * d);
+        int rc = orc_decoder_eval(kind, d, b, h, W1, b1, W2, b2, R, c, code, table + (size_t)code * d);
         if (rc) return rc;
     }
     return ORC_OK;
@@ -280,13 +303,83 @@ int orc_coupled_select(const float *wg, const float *wu, const float *wd, int64_
     return rc;
 }
 
-/* Q8 of the protected columns (eq. protected_8bit_scatter; reading: symmetric
- * int8, one fp32 scale per protected column):
- *   m_j = max_i |w_ij|;  s_j = m_j / 127;
- *   q_ij = clamp(round_half_even(w_ij / s_j), -127, 127), and q = 0 when s_j = 0.
+/* ------------------------------------------------------------------------ */
+/* Protected payload formats (Table "BSQ codec components": the protected    */
+/* path stored as INT8, FP8-E4M3 or FP8-E5M2). Each stored element is one    */
+/* byte; its value times the slice's fp32 scale is the weight.               */
+/*   INT8: two's complement, -127..127.                                     */
+/*   E4M3: sign, 4 exponent bits (bias 7), 3 fraction bits; subnormals;      */
+/*         no infinities, S.1111.111 is NaN; largest finite 448.            */
+/*   E5M2: sign, 5 exponent bits (bias 15), 2 fraction bits; subnormals;     */
+/*         S.11111.00 is infinity; largest finite 57344.                    */
+/* (The OCP 8-bit floating point formats; reading: a protected slice is      */
+/* scaled so that its largest magnitude lands on the format's largest        */
+/* finite value, as the int8 path lands it on 127.)                          */
+/* ------------------------------------------------------------------------ */
+
+float orc_payload_max(int fmt)
+{
+    if (fmt == FMT_E4M3) return 448.0f;
+    if (fmt == FMT_E5M2) return 57344.0f;
+    return 127.0f;
+}
+
+/* The value of one stored byte, from the field definitions above. */
+float orc_payload_value(uint8_t q, int fmt)
+{
+    if (fmt == FMT_INT8) return (float)(int8_t)q;
+    int ebits = (fmt == FMT_E4M3) ? 4 : 5, mbits = 7 - ebits;
+    int bias = (1 << (ebits - 1)) - 1;
+    int sign = q >> 7;
+    int ex = (q >> mbits) & ((1 << ebits) - 1);
+    int man = q & ((1 << mbits) - 1);
+    double v;
+    if (fmt == FMT_E4M3 && ex == 15 && man == 7) v = NAN;
+    else if (fmt == FMT_E5M2 && ex == 31) v = man ? NAN : INFINITY;
+    else if (ex == 0) v = ldexp((double)man, 1 - bias - mbits);
+    else v = ldexp((double)((1 << mbits) + man), ex - bias - mbits);
+    return (float)(sign ? -v : v);
+}
+
+/* The stored byte for v (already divided by the scale).
+ *   INT8: clamp(round_half_even(v), -127, 127).
+ *   FP8:  the finite value nearest to v, ties to the even code (fraction
+ *         LSB 0), the sign of v kept (so -0 and negative values that round
+ *         to zero give the negative zero code); |v| above the largest finite
+ *         value saturates to it. Found by trying every finite non-negative
+ *         code, in double precision (every candidate and v are exact there). */
+uint8_t orc_payload_quant(float v, int fmt)
+{
+    if (fmt == FMT_INT8) {
+        float t = nearbyintf(v);
+        if (t > 127.0f) t = 127.0f;
+        if (t < -127.0f) t = -127.0f;
+        return (uint8_t)(int8_t)t;
+    }
+    double a = fabs((double)v);
+    uint8_t sign = signbit(v) ? 0x80u : 0u;
+    uint8_t best = 0;
+    double best_err = INFINITY;
+    for (int code = 0; code < 128; ++code) {
+        double cv = (double)orc_payload_value((uint8_t)code, fmt);
+        if (!isfinite(cv)) continue;
+        double err = fabs(cv - a);
+        if (err < best_err || (err == best_err && (code & 1) == 0)) {
+            best_err = err;
+            best = (uint8_t)code;
+        }
+    }
+    if (a >= (double)orc_payload_max(fmt)) best = (fmt == FMT_E4M3) ? 0x7eu : 0x7bu;
+    return (uint8_t)(sign | best);
+}
+
+/* Q8 of the protected columns (eq. protected_8bit_scatter; reading: symmetric,
+ * one fp32 scale per protected column):
+ *   m_j = max_i |w_ij|;  s_j = m_j / max(fmt)   (127, 448 or 57344);
+ *   q_ij = orc_payload_quant(w_ij / s_j, fmt), and the zero byte when s_j = 0.
  * Layout: q8[i * k + p] for protected column idx[p]. */
 void orc_q8(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int64_t k,
-            int8_t *q8, float *scale)
+            int fmt, uint8_t *q8, float *scale)
 {
     for (int64_t p = 0; p < k; ++p) {
         int64_t j = idx[p];
@@ -295,28 +388,20 @@ void orc_q8(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int
             float a = fabsf(w[i * d_in + j]);
             if (a > m) m = a;
         }
-        float s = m / 127.0f;
+        float s = m / orc_payload_max(fmt);
         scale[p] = s;
-        for (int64_t i = 0; i < d_out; ++i) {
-            int8_t q = 0;
-            if (s != 0.0f) {
-                float t = nearbyintf(w[i * d_in + j] / s);
-                if (t > 127.0f) t = 127.0f;
-                if (t < -127.0f) t = -127.0f;
-                q = (int8_t)t;
-            }
-            q8[i * k + p] = q;
-        }
+        for (int64_t i = 0; i < d_out; ++i)
+            q8[i * k + p] = (s != 0.0f) ? orc_payload_quant(w[i * d_in + j] / s, fmt) : 0u;
     }
 }
 
 /* Q8 of protected output rows (eq. protected_8bit_scatter with row slices;
- * reading: symmetric int8, one fp32 scale per protected row):
- *   m_p = max_j |w[idx_p][j]|;  s_p = m_p / 127;
- *   q8[p * d_in + j] = clamp(round_half_even(w[idx_p][j] / s_p), -127, 127),
- *   and q = 0 when s_p = 0. */
+ * reading: symmetric, one fp32 scale per protected row):
+ *   m_p = max_j |w[idx_p][j]|;  s_p = m_p / max(fmt);
+ *   q8[p * d_in + j] = orc_payload_quant(w[idx_p][j] / s_p, fmt), and the
+ *   zero byte when s_p = 0. */
 void orc_q8_rows(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx, int64_t k,
-                 int8_t *q8, float *scale)
+                 int fmt, uint8_t *q8, float *scale)
 {
     (void)d_out;
     for (int64_t p = 0; p < k; ++p) {
@@ -326,18 +411,10 @@ void orc_q8_rows(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx
             float a = fabsf(row[j]);
             if (a > m) m = a;
         }
-        float s = m / 127.0f;
+        float s = m / orc_payload_max(fmt);
         scale[p] = s;
-        for (int64_t j = 0; j < d_in; ++j) {
-            int8_t q = 0;
-            if (s != 0.0f) {
-                float t = nearbyintf(row[j] / s);
-                if (t > 127.0f) t = 127.0f;
-                if (t < -127.0f) t = -127.0f;
-                q = (int8_t)t;
-            }
-            q8[p * d_in + j] = q;
-        }
+        for (int64_t j = 0; j < d_in; ++j)
+            q8[p * d_in + j] = (s != 0.0f) ? orc_payload_quant(row[j] / s, fmt) : 0u;
     }
 }
 
@@ -426,9 +503,9 @@ static void encode_rows(int d, int stages, const float *const *tables, const flo
 
 int orc_encode(int d, int stages, const float *const *tables,
                const float *w, int64_t d_out, int64_t d_in, const float *g,
-               int64_t k, int64_t pitch,
+               int64_t k, int64_t pitch, int fmt,
                void *const *codes, uint16_t *const *gains,
-               int32_t *idx, int8_t *q8, float *scale, int nthreads)
+               int32_t *idx, uint8_t *q8, float *scale, int nthreads)
 {
     if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
     if (d_in % d != 0 || k < 0 || k > d_in) return ORC_ERR_ARG;
@@ -443,7 +520,7 @@ int orc_encode(int d, int stages, const float *const *tables,
     if (k > 0) {
         int rc = orc_protect_select(w, d_out, d_in, g, k, idx, NULL);
         if (rc) { free(prot); return rc; }
-        orc_q8(w, d_out, d_in, idx, k, q8, scale);
+        orc_q8(w, d_out, d_in, idx, k, fmt, q8, scale);
         for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
     }
     encode_rows(d, stages, tables, w, d_out, d_in, pitch, prot, NULL, codes, gains, nthreads);
@@ -464,9 +541,9 @@ int orc_encode(int d, int stages, const float *const *tables,
  * three matrices: rows of gate and up, columns of down. */
 int orc_encode_set(int d, int stages, const float *const *tables,
                    const float *w, int64_t d_out, int64_t d_in, int axis,
-                   const int32_t *idx, int64_t k, int64_t pitch,
+                   const int32_t *idx, int64_t k, int64_t pitch, int fmt,
                    void *const *codes, uint16_t *const *gains,
-                   int8_t *q8, float *scale, int nthreads)
+                   uint8_t *q8, float *scale, int nthreads)
 {
     if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
     if (axis != 0 && axis != 1) return ORC_ERR_ARG;
@@ -481,10 +558,10 @@ int orc_encode_set(int d, int stages, const float *const *tables,
     unsigned char *skip = (unsigned char *)calloc((size_t)(d_out > 0 ? d_out : 1), 1);
     if (!prot || !skip) { free(prot); free(skip); return ORC_ERR_ARG; }
     if (axis == 0) {
-        orc_q8(w, d_out, d_in, idx, k, q8, scale);
+        orc_q8(w, d_out, d_in, idx, k, fmt, q8, scale);
         for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
     } else {
-        orc_q8_rows(w, d_out, d_in, idx, k, q8, scale);
+        orc_q8_rows(w, d_out, d_in, idx, k, fmt, q8, scale);
         for (int64_t p = 0; p < k; ++p) skip[idx[p]] = 1;
     }
     encode_rows(d, stages, tables, w, d_out, d_in, pitch, prot, skip, codes, gains, nthreads);
@@ -499,11 +576,11 @@ int orc_encode_set(int d, int stages, const float *const *tables,
 
 /* W_hat[i][j] = sum over stages of gain_s * D_s(code_s)[j], as an fmaf chain
  * over s from +0 (each stage decoded independently, then summed); protected
- * columns are then overwritten with q8 * scale. */
+ * columns are then overwritten with value(q8) * scale (fp32 product). */
 int orc_decode(int d, int stages, const float *const *tables,
                int64_t d_out, int64_t d_in, int64_t pitch,
                const void *const *codes, const uint16_t *const *gains,
-               const int32_t *idx, const int8_t *q8, const float *scale, int64_t k,
+               const int32_t *idx, const uint8_t *q8, const float *scale, int64_t k, int fmt,
                float *w_hat, int nthreads)
 {
     if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
@@ -527,20 +604,20 @@ int orc_decode(int d, int stages, const float *const *tables,
             }
         }
         for (int64_t p = 0; p < k; ++p)
-            w_hat[i * d_in + idx[p]] = (float)q8[i * k + p] * scale[p];
+            w_hat[i * d_in + idx[p]] = orc_payload_value(q8[i * k + p], fmt) * scale[p];
     }
     return ORC_OK;
 }
 
 /* ------------------------------------------------------------------------ */
 /* Fused product route, fp64: y_i = sum_c sum_s gain * <D_s(code), x~_c>      */
-/*   + sum_p scale_p q8_ip x_{idx_p} + sum_r B_ir (A x)_r                     */
+/*   + sum_p scale_p value(q8_ip) x_{idx_p} + sum_r B_ir (A x)_r              */
 /* x~ is x with the protected positions zeroed. This route never forms W_hat. */
 /* ------------------------------------------------------------------------ */
 int orc_gemv_fused(int d, int stages, const float *const *tables,
                    int64_t d_out, int64_t d_in, int64_t pitch,
                    const void *const *codes, const uint16_t *const *gains,
-                   const int32_t *idx, const int8_t *q8, const float *scale, int64_t k,
+                   const int32_t *idx, const uint8_t *q8, const float *scale, int64_t k, int fmt,
                    const double *x, int rank, const double *A, const double *B,
                    double *y, int nthreads)
 {
@@ -574,7 +651,7 @@ int orc_gemv_fused(int d, int stages, const float *const *tables,
             }
         }
         for (int64_t p = 0; p < k; ++p)
-            acc += (double)scale[p] * (double)q8[i * k + p] * x[idx[p]];
+            acc += (double)scale[p] * (double)orc_payload_value(q8[i * k + p], fmt) * x[idx[p]];
         for (int r = 0; r < rank; ++r) acc += B[i * rank + r] * t[r];
         y[i] = acc;
     }

@@ -32,6 +32,7 @@ BASE_SEED = 2607_08643
 DEC_IDENTITY = 0
 DEC_LINEAR = 1
 DEC_MLP = 2
+DEC_MLP_RES1 = 3
 
 
 # --------------------------------------------------------------------------
@@ -84,6 +85,7 @@ class StageDecoder:
     """Parameters of one stage's decoder, all fp32, row-major.
 
     MLP:      W1 [h, b], b1 [h], W2 [d, h], b2 [d]
+    MLP_RES1: the MLP's tensors plus the residual block's R [h, h], c [h]
     LINEAR:   W1 = M [d, b], b1 = beta [d]   (W2, b2 unused)
     IDENTITY: no parameters.
     """
@@ -91,6 +93,8 @@ class StageDecoder:
     b1: np.ndarray | None = None
     W2: np.ndarray | None = None
     b2: np.ndarray | None = None
+    R: np.ndarray | None = None
+    c: np.ndarray | None = None
 
 
 def decoder_params(kind: int, d: int, b: int, hidden: int, stages: int,
@@ -105,12 +109,16 @@ def decoder_params(kind: int, d: int, b: int, hidden: int, stages: int,
         elif kind == DEC_LINEAR:
             out.append(StageDecoder(W1=draw(0, d * b, b).reshape(d, b),
                                     b1=draw(1, d, b)))
-        elif kind == DEC_MLP:
+        elif kind in (DEC_MLP, DEC_MLP_RES1):
             h = hidden
-            out.append(StageDecoder(W1=draw(0, h * b, b).reshape(h, b),
-                                    b1=draw(1, h, b),
-                                    W2=draw(2, d * h, h).reshape(d, h),
-                                    b2=draw(3, d, h)))
+            dec = StageDecoder(W1=draw(0, h * b, b).reshape(h, b),
+                               b1=draw(1, h, b),
+                               W2=draw(2, d * h, h).reshape(d, h),
+                               b2=draw(3, d, h))
+            if kind == DEC_MLP_RES1:
+                dec.R = draw(4, h * h, h).reshape(h, h)
+                dec.c = draw(5, h, h)
+            out.append(dec)
         else:
             raise ValueError(f"unknown decoder kind {kind}")
     return out
