@@ -34,9 +34,10 @@
  *   gains[s]   fp16 bits, tiled: per-chunk least-squares gain of
  *              stage s (round to nearest even, finite overflow saturated);
  *   prot_idx   int32 [k], the protected input columns in ascending order;
- *   prot_q8    int8  [d_out][kp], kp = roundup(k, 16), 16-byte aligned:
- *              row i holds the symmetric int8 codes of row i's k protected
- *              entries, then kp - k zero bytes;
+ *   prot_q8    8-bit [d_out][kp], kp = roundup(k, 16), 16-byte aligned:
+ *              row i holds the stored bytes of row i's k protected entries
+ *              (format by protect_format: symmetric int8, or FP8-E4M3 /
+ *              FP8-E5M2), then kp - k zero bytes;
  *   prot_scale fp32  [k], one scale per protected column;
  *   prot_bits  uint32 [pitch * d / 32], bit j%32 of word j/32 set iff input
  *              column j is protected (the same set as prot_idx, as a bitmap
@@ -50,9 +51,9 @@
  * the protection-axis ablation in Section IV-D, and the gate/up side of
  * eq. mlp_coupled_protection) the protected slices are k whole rows:
  *   prot_idx   int32 [k], the protected rows in ascending order;
- *   prot_q8    int8  [k][q8_pitch(d_in)], q8_pitch(n) = roundup(n, 16):
- *              row p holds the symmetric int8 codes of row prot_idx[p], then
- *              zero bytes;
+ *   prot_q8    8-bit [k][q8_pitch(d_in)], q8_pitch(n) = roundup(n, 16):
+ *              row p holds the stored bytes of row prot_idx[p], then zero
+ *              bytes;
  *   prot_scale fp32  [k], one scale per protected row;
  *   prot_bits  unused (may be NULL);
  * and the protected rows are not BSQ-coded: their code and gain planes hold
@@ -68,7 +69,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 5
+#define BSQ_ABI_VERSION 6
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -112,32 +113,60 @@ typedef enum { BSQ_F32 = 0, BSQ_BF16 = 1 } bsq_dtype;
 
 /* Decoder families of the paper's codec ablation (Section IV-D, Table
  * "BSQ codec components"): identity (y = q), linear, and the compact
- * symmetric decoder without residual blocks (one hidden ReLU layer). */
-typedef enum { BSQ_DEC_IDENTITY = 0, BSQ_DEC_LINEAR = 1, BSQ_DEC_MLP = 2 } bsq_dec_kind;
+ * symmetric decoder with no residual block (one hidden ReLU layer) or with
+ * one residual block on its hidden layer. */
+typedef enum {
+    BSQ_DEC_IDENTITY = 0,
+    BSQ_DEC_LINEAR = 1,
+    BSQ_DEC_MLP = 2,
+    BSQ_DEC_MLP_RES1 = 3
+} bsq_dec_kind;
+
+/* Storage format of the protected path (Table "BSQ codec components": INT8,
+ * FP8-E4M3, FP8-E5M2). One byte per protected element and one fp32 scale per
+ * protected slice; the element's weight is value(byte) * scale, and the
+ * scale is the slice's largest magnitude over the format's largest finite
+ * value (127, 448, 57344).
+ *   INT8: two's complement, round half to even, clamped to +-127;
+ *   E4M3: sign, 4 exponent bits (bias 7), 3 fraction bits, subnormals, no
+ *         infinities (S.1111.111 is NaN);
+ *   E5M2: sign, 5 exponent bits (bias 15), 2 fraction bits, subnormals,
+ *         S.11111.00 is infinity.
+ * FP8 rounding: nearest finite value, ties to the even code, sign kept (a
+ * negative value that rounds to zero stores -0), magnitudes past the largest
+ * finite value store it. */
+typedef enum { BSQ_PROT_INT8 = 0, BSQ_PROT_E4M3 = 1, BSQ_PROT_E5M2 = 2 } bsq_prot_format;
 
 typedef struct {
     int32_t d;           /* chunk length: 8 or 16 (Section III-A, codebook_dim) */
     int32_t b;           /* code bits per stage (codebook_bits); must equal d */
     int32_t stages;      /* residual stages S, 1..4 (Section III-D; default 2) */
     int32_t dec_kind;    /* bsq_dec_kind */
-    int32_t hidden;      /* MLP hidden width h, 1..64; ignored for other kinds */
+    int32_t hidden;      /* hidden width h of the symmetric decoders, 1..64; ignored for other kinds */
     int32_t protect_num; /* protected-channel ratio rho = num/den (eq. protected_channel_selection); */
     int32_t protect_den; /*   num = 0 disables the protected path; k = ceil(n*num/den) for the n */
                          /*   channels of the protected axis (d_in for columns, d_out for rows) */
     int32_t protect_axis; /* 0: protected input columns; 1: protected output rows */
+    int32_t protect_format; /* bsq_prot_format of the protected payload */
 } bsq_config;
 
 /* Parameters of one stage's decoder, fp32, row-major, device pointers.
  *   MLP:      W1 [h][b], b1 [h], W2 [d][h], b2 [d];
  *             y = W2 relu(W1 q + b1) + b2, relu(a) = a > 0 ? a : +0
+ *   MLP_RES1: the MLP's tensors and R [h][h], c [h];
+ *             a = relu(W1 q + b1); a' = a + relu(R a + c); y = W2 a' + b2
  *   LINEAR:   W1 = M [d][b], b1 = beta [d]; y = M q + beta   (W2, b2 unused)
  *   IDENTITY: y = q                                           (all unused)
- * with q_j = +-1/sqrt(b) (Section III-C, sphere map and sign binarisation). */
+ * with q_j = +-1/sqrt(b) (Section III-C, sphere map and sign binarisation).
+ * Every dot product is an fp32 fmaf chain from the bias, in index order; R
+ * and c may be NULL for the other kinds. */
 typedef struct {
     const float *W1;
     const float *b1;
     const float *W2;
     const float *b2;
+    const float *R;
+    const float *c;
 } bsq_decoder;
 
 /* One encoded matrix (or a stack of n_mats of one shape), device pointers.
@@ -147,7 +176,7 @@ typedef struct {
     void *codes[BSQ_MAX_STAGES];
     uint16_t *gains[BSQ_MAX_STAGES];
     int32_t *prot_idx;
-    int8_t *prot_q8;
+    int8_t *prot_q8;     /* stored bytes in the config's protect_format */
     float *prot_scale;
     uint32_t *prot_bits;
     int64_t d_out;
@@ -239,7 +268,8 @@ bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec,
 
 /* Encode n_mats matrices of one shape (Sections III-C to III-E):
  * protected-column scores key_j = g_j^2 sum_i W_ij^2 (fp64, rows in order),
- * TopK with ties to the lower column, int8 quantisation of those columns, then
+ * TopK with ties to the lower column, quantisation of those columns in the
+ * protect_format (eq. protected_8bit_scatter; int8 or FP8), then
  * per chunk and stage: sign code, decoded vector D_s(code), least-squares fp16
  * gain over the unprotected positions, residual update (fmaf chains in element
  * order). The outputs are bit-identical to the definition.
@@ -261,9 +291,9 @@ bsq_status bsq_encode(const bsq_config *cfg, const void *codec, const void *W, i
 /* Encode with a given protected set (no selection): as bsq_encode, except that
  * the k slices on cfg->protect_axis are idx (device int32 [n_mats][k], each
  * matrix's entries strictly ascending and in [0, n) for the axis length n;
- * it may alias out->prot_idx). Column axis: int8 quantisation of those
- * columns and BSQ on the rest of every row. Row axis: int8 quantisation of
- * those rows (one scale per row, the absmax over the row / 127); BSQ on the
+ * it may alias out->prot_idx). Column axis: quantisation (protect_format) of those
+ * columns and BSQ on the rest of every row. Row axis: quantisation of
+ * those rows (one scale per row, the absmax over the row / the format max); BSQ on the
  * other rows with no position masked; the protected rows get code 0 and gain
  * +0. An invalid set ORs BSQ_DEVERR_BAD_SET into *err (and the outputs are
  * unspecified); NaN or Inf in W ORs BSQ_DEVERR_NONFINITE. This is how the coupled set of bsq_coupled_select is
@@ -315,7 +345,7 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
  *   W_hat[i][j] = fmaf(gain_s, D_s(code_s)[j], accumulate ? W_hat[i][j] : 0)
  * over the unprotected positions of stage `stage` (0 <= stage < stages); the
  * call for the last stage then writes the protected columns (or rows) from
- * the int8 payload. Calling it for stage = 0 .. stages-1, with accumulate = 0
+ * the protected payload. Calling it for stage = 0 .. stages-1, with accumulate = 0
  * then 1, leaves in W_hat the bits bsq_decode writes with BSQ_F32 output, at
  * the cost of one launch and one fp32 read-modify-write of W_hat per stage.
  *   W_hat  device fp32 [n_mats][d_out][d_in], 16-byte aligned */
@@ -395,7 +425,7 @@ bsq_status bsq_gemv_prepare(const bsq_config *cfg, int32_t n, const void *const 
                             int32_t x_dtype, void *ws, size_t ws_bytes, void *stream);
 
 /* The streaming product of the GEMV, alone: reads x, the code and gain
- * planes, the int8 payload and LoRA A and B once, and whatever a preceding
+ * planes, the protected payload and LoRA A and B once, and whatever a preceding
  * bsq_gemv_prepare (same group, same x) left in `ws` on the same stream.
  * With bf16 x at d = 8 (and d = 16 with the width-16 symmetric decoder) the
  * LoRA vectors are computed inside this launch. Limits of the bf16 path:

@@ -27,7 +27,8 @@ GEMV_NOALLOC_SCRATCH_BYTES = 8 << 20
 BSQ_OK, BSQ_ERR_ARG, BSQ_ERR_SHAPE, BSQ_ERR_DTYPE, BSQ_ERR_ALIGN = 0, 1, 2, 3, 4
 BSQ_ERR_BUFFER_TOO_SMALL, BSQ_ERR_NONFINITE, BSQ_ERR_DEVICE, BSQ_ERR_UNSUPPORTED = 5, 6, 7, 8
 BSQ_F32, BSQ_BF16 = 0, 1
-DEC_IDENTITY, DEC_LINEAR, DEC_MLP = 0, 1, 2
+DEC_IDENTITY, DEC_LINEAR, DEC_MLP, DEC_MLP_RES1 = 0, 1, 2, 3
+PROT_INT8, PROT_E4M3, PROT_E5M2 = 0, 1, 2
 OP_ENCODE, OP_GEMV, OP_GEMM, OP_SELECT = 0, 1, 2, 3
 DEVERR_NONFINITE, DEVERR_BAD_SET, DEVERR_TIMEOUT, DEVERR_POISONED = 1, 2, 4, 8
 
@@ -42,11 +43,12 @@ class BsqError(RuntimeError):
 class bsq_config(ct.Structure):
     _fields_ = [("d", ct.c_int32), ("b", ct.c_int32), ("stages", ct.c_int32), ("dec_kind", ct.c_int32),
                 ("hidden", ct.c_int32), ("protect_num", ct.c_int32), ("protect_den", ct.c_int32),
-                ("protect_axis", ct.c_int32)]
+                ("protect_axis", ct.c_int32), ("protect_format", ct.c_int32)]
 
 
 class bsq_decoder(ct.Structure):
-    _fields_ = [("W1", ct.c_void_p), ("b1", ct.c_void_p), ("W2", ct.c_void_p), ("b2", ct.c_void_p)]
+    _fields_ = [("W1", ct.c_void_p), ("b1", ct.c_void_p), ("W2", ct.c_void_p), ("b2", ct.c_void_p),
+                ("R", ct.c_void_p), ("c", ct.c_void_p)]
 
 
 class bsq_layer(ct.Structure):
@@ -77,7 +79,7 @@ EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes
            "bsq_debug_set_wait_limit", "bsq_decode_stage", "bsq_gemv_noalloc")
 
 # struct layouts above follow this version of include/bsq.h
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 _lib = None
 
@@ -159,6 +161,7 @@ class Config:
     protect_num: int = 1
     protect_den: int = 100
     protect_axis: int = 0   # 0: protected input columns, 1: protected output rows
+    protect_format: int = PROT_INT8   # payload of the protected slices: int8, FP8-E4M3 or FP8-E5M2
 
     @property
     def b(self) -> int:
@@ -166,7 +169,7 @@ class Config:
 
     def c(self) -> bsq_config:
         return bsq_config(self.d, self.b, self.stages, self.kind, self.hidden, self.protect_num,
-                          self.protect_den, self.protect_axis)
+                          self.protect_den, self.protect_axis, self.protect_format)
 
     def k(self, n: int) -> int:
         """ceil(rho * n): protected channels among n."""
@@ -232,14 +235,15 @@ def _empty_aligned(nbytes: int, device, align: int = 256, zero: bool = False) ->
 
 
 def bsq_codec_prepare(cfg: Config, decoders, device="cuda", stream=None) -> Codec:
-    """decoders: per stage an object with W1/b1/W2/b2 (numpy or torch, fp32; None where unused)."""
+    """decoders: per stage an object with W1/b1/W2/b2 and, for the residual-block
+    decoder, R/c (numpy or torch, fp32; None or absent where unused)."""
     dev = torch.device(device)
     params = []
     arr = (bsq_decoder * MAX_STAGES)()
     for s in range(cfg.stages):
         dec = decoders[s] if decoders is not None else None
         ts = []
-        for name in ("W1", "b1", "W2", "b2"):
+        for name in ("W1", "b1", "W2", "b2", "R", "c"):
             v = getattr(dec, name, None) if dec is not None else None
             if v is None:
                 ts.append(None)
@@ -315,7 +319,7 @@ class Layer:
 
     def nbytes_streamed(self) -> int:
         """Bytes a product reads from this layer: the code and gain planes of
-        the d_out real rows, the int8 payload, scales, indices and bitmap."""
+        the d_out real rows, the protected payload, scales, indices and bitmap."""
         per_row = self.pitch * (self.codes[0].element_size() + 2) * self.cfg.stages
         n = per_row * self.d_out
         if self.k and self.cfg.protect_axis == 1:
@@ -329,7 +333,7 @@ class Layer:
 
 def layer_empty(cfg: Config, d_out: int, d_in: int, n_mats: int = 1, device="cuda") -> Layer:
     """Planes in the tiled layout [n_mats][ceil(d_out/64)][pitch/16][64][16];
-    the int8 payload as [n_mats][d_out][roundup(k, 16)] (protected rows:
+    the protected payload (one byte per element) as [n_mats][d_out][roundup(k, 16)] (protected rows:
     [n_mats][k][roundup(d_in, 16)], and no bitmap)."""
     P, k = cfg.pitch(d_in), cfg.k_for(d_out, d_in)
     ct_ = torch.uint8 if cfg.d <= 8 else torch.int16

@@ -54,8 +54,11 @@ bsq_status check_cfg(const bsq_config *c)
     if (!c) return BSQ_ERR_ARG;
     if (c->d < 1 || c->d > 16 || c->b < 1 || c->b > 16) return BSQ_ERR_ARG;
     if (c->stages < 1 || c->stages > BSQ_MAX_STAGES) return BSQ_ERR_ARG;
-    if (c->dec_kind < BSQ_DEC_IDENTITY || c->dec_kind > BSQ_DEC_MLP) return BSQ_ERR_ARG;
-    if (c->dec_kind == BSQ_DEC_MLP && (c->hidden < 1 || c->hidden > BSQ_MAX_HIDDEN)) return BSQ_ERR_ARG;
+    if (c->dec_kind < BSQ_DEC_IDENTITY || c->dec_kind > BSQ_DEC_MLP_RES1) return BSQ_ERR_ARG;
+    if ((c->dec_kind == BSQ_DEC_MLP || c->dec_kind == BSQ_DEC_MLP_RES1) &&
+        (c->hidden < 1 || c->hidden > BSQ_MAX_HIDDEN))
+        return BSQ_ERR_ARG;
+    if (c->protect_format < BSQ_PROT_INT8 || c->protect_format > BSQ_PROT_E5M2) return BSQ_ERR_ARG;
     if (c->protect_num < 0 || c->protect_den < 1 || c->protect_num > c->protect_den) return BSQ_ERR_ARG;
     if (c->protect_axis != 0 && c->protect_axis != 1) return BSQ_ERR_ARG;
     if (c->d != 8 && c->d != 16) return BSQ_ERR_UNSUPPORTED;
@@ -179,7 +182,9 @@ bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, i
     out->scale_bytes = k * 4;
     out->bits_bytes = (k > 0 && !rows) ? prot_words(P, c.d) * 4 : 0;
     int64_t dec_params = 0;
-    if (c.dec_kind == BSQ_DEC_MLP) dec_params = int64_t(c.hidden) * c.b + c.hidden + int64_t(c.d) * c.hidden + c.d;
+    if (c.dec_kind == BSQ_DEC_MLP || c.dec_kind == BSQ_DEC_MLP_RES1)
+        dec_params = int64_t(c.hidden) * c.b + c.hidden + int64_t(c.d) * c.hidden + c.d;
+    if (c.dec_kind == BSQ_DEC_MLP_RES1) dec_params += int64_t(c.hidden) * c.hidden + c.hidden;
     else if (c.dec_kind == BSQ_DEC_LINEAR) dec_params = int64_t(c.d) * c.b + c.d;
     out->S_code = double(c.stages) * double(coded_rows) * double(C) * double(c.b) / 8.0;
     out->S_dec = double(c.stages) * double(dec_params) * 4.0;
@@ -239,7 +244,9 @@ bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec, void
         if (!dec) return BSQ_ERR_ARG;
         for (int i = 0; i < cfg->stages; ++i) {
             if (!dec[i].W1 || !dec[i].b1) return BSQ_ERR_ARG;
-            if (cfg->dec_kind == BSQ_DEC_MLP && (!dec[i].W2 || !dec[i].b2)) return BSQ_ERR_ARG;
+            if ((cfg->dec_kind == BSQ_DEC_MLP || cfg->dec_kind == BSQ_DEC_MLP_RES1) && (!dec[i].W2 || !dec[i].b2))
+                return BSQ_ERR_ARG;
+            if (cfg->dec_kind == BSQ_DEC_MLP_RES1 && (!dec[i].R || !dec[i].c)) return BSQ_ERR_ARG;
         }
     }
     bsq_decoder none[BSQ_MAX_STAGES] = {};
@@ -337,7 +344,7 @@ bsq_status bsq_decode(const bsq_config *cfg, const void *codec, const bsq_layer 
     const bsq_layer coded = coded_layer(*cfg, *layer);
     if ((s = from_hip(launch_decode(coded_cfg(*cfg), codec, coded, W_hat, out_dtype, st))) != BSQ_OK) return s;
     if (!row_axis(*cfg)) return BSQ_OK;
-    return from_hip(launch_decode_rows(*layer, W_hat, out_dtype, st));
+    return from_hip(launch_decode_rows(*layer, cfg->protect_format, W_hat, out_dtype, st));
 }
 
 bsq_status bsq_decode_stage(const bsq_config *cfg, const void *codec, const bsq_layer *layer, int32_t stage,
@@ -355,7 +362,7 @@ bsq_status bsq_decode_stage(const bsq_config *cfg, const void *codec, const bsq_
     if ((s = from_hip(launch_decode_stage(coded_cfg(*cfg), codec, coded, stage, accumulate, W_hat, st))) != BSQ_OK)
         return s;
     if (!row_axis(*cfg) || stage != cfg->stages - 1) return BSQ_OK;
-    return from_hip(launch_decode_rows(*layer, W_hat, BSQ_F32, st));
+    return from_hip(launch_decode_rows(*layer, cfg->protect_format, W_hat, BSQ_F32, st));
 }
 
 namespace {
@@ -437,7 +444,7 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
                                       err, st))) != BSQ_OK)
         return s;
     if (!row_axis(*cfg)) return BSQ_OK;
-    return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
+    return from_hip(launch_gemv_rows(n, layers, cfg->protect_format, loras, x, x_dtype, y, y_dtype, st));
 }
 
 namespace {
@@ -457,7 +464,7 @@ bsq_status gemv_launch(const bsq_config *cfg, int32_t n, const void *const *code
                                       st))) != BSQ_OK)
         return s;
     if (!row_axis(*cfg)) return BSQ_OK;
-    return from_hip(launch_gemv_rows(n, layers, loras, x, x_dtype, y, y_dtype, st));
+    return from_hip(launch_gemv_rows(n, layers, cfg->protect_format, loras, x, x_dtype, y, y_dtype, st));
 }
 
 }  // namespace
@@ -532,7 +539,7 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     if ((s = from_hip(launch_gemm(cc, codec, coded, lora, X, M, ldx, Y, y_dtype, ldy, ws, err, st))) != BSQ_OK)
         return s;
     if (!rows) return BSQ_OK;
-    return from_hip(launch_gemm_rows(*layer, lora, X, M, ldx, Y, y_dtype, ldy, gemm_lora_t(ws), st));
+    return from_hip(launch_gemm_rows(*layer, cfg->protect_format, lora, X, M, ldx, Y, y_dtype, ldy, gemm_lora_t(ws), st));
 }
 
 }  // extern "C"

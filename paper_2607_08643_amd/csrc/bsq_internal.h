@@ -34,6 +34,7 @@ inline size_t codec_tabh_offset(const bsq_config &c, int s)
 {
     return size_t(c.stages) * codec_entries(c) * 6 + size_t(s) * codec_entries(c) * 2;
 }
+// (the residual-block decoder is not split: its block mixes the hidden units)
 inline bool codec_has_split(const bsq_config &c) { return c.dec_kind == BSQ_DEC_MLP && c.d == 16 && c.b == 16; }
 // one stage's split tables and decoder copies
 inline size_t codec_split_stage_bytes(const bsq_config &c)
@@ -111,6 +112,65 @@ __device__ __forceinline__ uint16_t gain_to_f16(float a)
 }
 
 // ---------------------------------------------------------------------------
+// Protected payload formats (bsq_prot_format): one stored byte per protected
+// element; its value times the slice's fp32 scale is the weight, and the
+// scale is the slice's largest magnitude over payload_max.
+// ---------------------------------------------------------------------------
+__host__ __device__ inline float payload_max(int fmt)
+{
+    return fmt == BSQ_PROT_E4M3 ? 448.0f : (fmt == BSQ_PROT_E5M2 ? 57344.0f : 127.0f);
+}
+
+// The value of the stored byte in the low 8 bits of q: int8 two's
+// complement, or the sign / exponent / fraction fields of the FP8 format
+// (E4M3: bias 7, S.1111.111 NaN; E5M2: bias 15, exponent 31 infinity or NaN;
+// exponent 0 subnormal in both). Exact: each value is an fp32 number.
+__device__ __forceinline__ float payload_to_f32(uint32_t q, int fmt)
+{
+    if (fmt == BSQ_PROT_INT8) return float(int8_t(uint8_t(q)));
+    const uint32_t sign = (q & 0x80u) << 24;
+    uint32_t mag;
+    if (fmt == BSQ_PROT_E4M3) {
+        const uint32_t e = (q >> 3) & 15u, m = q & 7u;
+        if (e == 15u && m == 7u) mag = 0x7fc00000u;
+        else if (e) mag = ((e + 120u) << 23) | (m << 20);          // 2^(e - 7) (1 + m / 8)
+        else mag = __float_as_uint(float(m) * 0x1p-9f);            // m 2^-9
+    } else {
+        const uint32_t e = (q >> 2) & 31u, m = q & 3u;
+        if (e == 31u) mag = m ? 0x7fc00000u : 0x7f800000u;
+        else if (e) mag = ((e + 112u) << 23) | (m << 21);          // 2^(e - 15) (1 + m / 4)
+        else mag = __float_as_uint(float(m) * 0x1p-16f);           // m 2^-16
+    }
+    return __uint_as_float(sign | mag);
+}
+
+// The stored byte of v (a weight over its slice's scale). int8: round half
+// to even, clamped to +-127. FP8: the nearest finite value, ties to the even
+// code, sign kept, magnitudes from the largest finite value up stored as it.
+// Below the smallest normal 2^emin the steps are 2^(emin - mb); in the
+// binade [2^e, 2^(e+1)) they are 2^(e - mb), so the scaled magnitude is
+// rounded once to an integer n (exact power-of-two scalings, round to nearest
+// even) and n = 2^(mb+1) carries into the next exponent by itself.
+__device__ __forceinline__ uint32_t payload_from_f32(float v, int fmt)
+{
+    if (fmt == BSQ_PROT_INT8) {
+        float t = __builtin_rintf(v);
+        t = (t > 127.0f) ? 127.0f : t;
+        t = (t < -127.0f) ? -127.0f : t;
+        return uint32_t(uint8_t(int8_t(t)));
+    }
+    const bool e4 = fmt == BSQ_PROT_E4M3;
+    const int mb = e4 ? 3 : 2, bias = e4 ? 7 : 15, emin = 1 - bias;
+    const uint32_t sign = (__float_as_uint(v) >> 24) & 0x80u;
+    const float a = __builtin_fabsf(v);
+    if (a >= payload_max(fmt)) return sign | (e4 ? 0x7eu : 0x7bu);
+    if (a < __builtin_ldexpf(1.0f, emin)) return sign | uint32_t(__builtin_rintf(__builtin_ldexpf(a, mb - emin)));
+    const int e = int((__float_as_uint(a) >> 23) & 0xffu) - 127;
+    const uint32_t n = uint32_t(__builtin_rintf(__builtin_ldexpf(a, mb - e)));
+    return sign | ((uint32_t(e + bias) << mb) + (n - (1u << mb)));
+}
+
+// ---------------------------------------------------------------------------
 // Launchers (defined in the .hip files; all asynchronous on `st`).
 // ---------------------------------------------------------------------------
 hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, void *codec, hipStream_t st);
@@ -129,7 +189,7 @@ struct SelectWs {       // coupled MLP selection, all [d_ffn]
     uint32_t *bits;
 };
 
-// int8 payload row length: k protected columns padded to a multiple of 16
+// protected payload row length: k protected columns padded to a multiple of 16
 // (zero bytes), so that one row is read with 16-byte loads
 __host__ __device__ inline int64_t q8_pitch(int64_t k) { return (k + 15) & ~int64_t(15); }
 
@@ -146,11 +206,12 @@ hipError_t launch_coupled_select(const void *Wg, const void *Wu, const void *Wd,
                                  int64_t d_ffn, const float *gg, const float *gu, const float *gd, int64_t k,
                                  int32_t *idx, double *scores, int32_t *err, const SelectWs &ws, hipStream_t st);
 // protected output rows of the products (run after the streaming kernels, same stream)
-hipError_t launch_decode_rows(const bsq_layer &layer, void *w_hat, int out_dtype, hipStream_t st);
-hipError_t launch_gemv_rows(int n, const bsq_layer *layers, const bsq_lora *loras, const void *x, int x_dtype,
-                            void *const *y, int y_dtype, hipStream_t st);
-hipError_t launch_gemm_rows(const bsq_layer &layer, const bsq_lora *lora, const void *X, int64_t M, int64_t ldx,
-                            void *Y, int y_dtype, int64_t ldy, const float *T, hipStream_t st);
+// (`fmt`: the payload's bsq_prot_format)
+hipError_t launch_decode_rows(const bsq_layer &layer, int fmt, void *w_hat, int out_dtype, hipStream_t st);
+hipError_t launch_gemv_rows(int n, const bsq_layer *layers, int fmt, const bsq_lora *loras, const void *x,
+                            int x_dtype, void *const *y, int y_dtype, hipStream_t st);
+hipError_t launch_gemm_rows(const bsq_layer &layer, int fmt, const bsq_lora *lora, const void *X, int64_t M,
+                            int64_t ldx, void *Y, int y_dtype, int64_t ldy, const float *T, hipStream_t st);
 // X A^T (fp32 [Mp][BSQ_MAX_LORA_RANK]) as left in a GEMM workspace by launch_gemm
 const float *gemm_lora_t(const void *ws);
 

@@ -1,6 +1,7 @@
 // Decoder tables: each stage decoder D_s evaluated on all 2^b spherical codes
 // (Section III-C: q_j = +-1/sqrt(b); Section IV-D: identity, linear and the
-// compact symmetric decoder with one hidden ReLU layer). The fp32 table is
+// compact symmetric decoder with one hidden ReLU layer, without or with one
+// residual block on that layer). The fp32 table is
 // filled with the same fmaf chains, in the same element order, as the
 // definition of the encoder, so that encode and decode are exact; the bf16
 // table (round to nearest even) feeds the GEMV's products, the fp16 table
@@ -17,6 +18,8 @@ struct TableArgs {
     const float *b1[BSQ_MAX_STAGES];
     const float *W2[BSQ_MAX_STAGES];
     const float *b2[BSQ_MAX_STAGES];
+    const float *R[BSQ_MAX_STAGES];   // residual block [h][h], [h] (res1 only)
+    const float *c[BSQ_MAX_STAGES];
     float *t32[BSQ_MAX_STAGES];
     uint16_t *t16[BSQ_MAX_STAGES];
     uint16_t *th[BSQ_MAX_STAGES];
@@ -59,6 +62,17 @@ __global__ __launch_bounds__(256) void codec_table_kernel(TableArgs a)
 #pragma unroll
             for (int j = 0; j < D; ++j) acc = __builtin_fmaf(W1[k * D + j], q[j], acc);
             act[k] = (acc > 0.0f) ? acc : 0.0f;
+        }
+        if (a.kind == BSQ_DEC_MLP_RES1) {
+            // a' = a + relu(c + R a): every t_k from the unmodified a, then the adds
+            const float *R = a.R[s], *c = a.c[s];
+            float t[BSQ_MAX_HIDDEN];
+            for (int k = 0; k < h; ++k) {
+                float acc = c[k];
+                for (int l = 0; l < h; ++l) acc = __builtin_fmaf(R[k * h + l], act[l], acc);
+                t[k] = (acc > 0.0f) ? acc : 0.0f;
+            }
+            for (int k = 0; k < h; ++k) act[k] = act[k] + t[k];
         }
 #pragma unroll
         for (int m = 0; m < D; ++m) {
@@ -130,6 +144,8 @@ hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, vo
         a.b1[s] = dec[s].b1;
         a.W2[s] = dec[s].W2;
         a.b2[s] = dec[s].b2;
+        a.R[s] = dec[s].R;
+        a.c[s] = dec[s].c;
         a.t32[s] = reinterpret_cast<float *>(base + codec_tab32_offset(cfg, s));
         a.t16[s] = reinterpret_cast<uint16_t *>(base + codec_tab16_offset(cfg, s));
         a.th[s] = reinterpret_cast<uint16_t *>(base + codec_tabh_offset(cfg, s));

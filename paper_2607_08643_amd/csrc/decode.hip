@@ -20,6 +20,7 @@ struct DecodeArgs {
     const int8_t *q8;
     const float *scale;
     void *out;
+    int pfmt;        // bsq_prot_format of q8
     int accumulate;  // start each element from the fp32 value already in out (sequential stages)
     int scatter;     // write the protected columns (the last stage of a sequential decode)
 };
@@ -144,7 +145,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
                         const int b = int((col0 + j) & 31);
                         int64_t p = s_rank[col0 >> 5] + __builtin_popcount(word & ((1u << b) - 1u));
                         p = (p < 0) ? 0 : (p < a.k) ? p : a.k - 1;  // an index list that is not ascending stays in bounds
-                        v[j] = float(a.q8[(m * a.d_out + i) * kp + p]) * s_scale[p];
+                        v[j] = payload_to_f32(uint8_t(a.q8[(m * a.d_out + i) * kp + p]), a.pfmt) * s_scale[p];
                     }
                 }
             }
@@ -222,6 +223,7 @@ hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_lay
     a.q8 = L.prot_q8;
     a.scale = L.prot_scale;
     a.out = w_hat;
+    a.pfmt = cfg.protect_format;
     a.scatter = 1;
     const bool bf = (out_dtype == BSQ_BF16);
     if (cfg.d == 8)
@@ -254,6 +256,7 @@ hipError_t launch_decode_stage(const bsq_config &cfg, const void *codec, const b
     a.q8 = L.prot_q8;
     a.scale = L.prot_scale;
     a.out = w_hat;
+    a.pfmt = cfg.protect_format;
     a.accumulate = accumulate;
     a.scatter = (stage == cfg.stages - 1);
     return (cfg.d == 8) ? launch_decode_t<8, false>(1, a, L.n_mats, st) : launch_decode_t<16, false>(1, a, L.n_mats, st);

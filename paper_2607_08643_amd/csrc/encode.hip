@@ -193,7 +193,8 @@ __device__ int block_exclusive_scan(int v, int *s_wave, int &total)
 
 // ---------------------------------------------------------------------------
 // P = TopK(key, k), ties to the lower column, stored ascending; also the
-// per-column scale s_p = absmax / 127, the column -> p map and the bitmap of
+// per-column scale s_p = absmax / pmax (the payload format's largest finite
+// value), the column -> p map and the bitmap of
 // protected columns. One block per matrix: an MSB-first radix select over the
 // 64-bit key patterns (non-negative doubles order like their bit patterns)
 // finds the k-th largest key T; then all keys > T and the lowest-index keys
@@ -201,7 +202,7 @@ __device__ int block_exclusive_scan(int v, int *s_wave, int &total)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__restrict__ keys_all,
                                                             const float *__restrict__ absmax_all,
-                                                            int64_t d_in, int64_t k, int64_t words,
+                                                            int64_t d_in, int64_t k, int64_t words, float pmax,
                                                             int32_t *__restrict__ idx_all,
                                                             float *__restrict__ scale_all,
                                                             int32_t *__restrict__ colmap_all,
@@ -298,7 +299,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__rest
             if (u == T) ++r;
             if (sel) {
                 idx[pos] = int32_t(j);
-                scale[pos] = absmax[j] / 127.0f;
+                scale[pos] = absmax[j] / pmax;
                 colmap[j] = pos;
                 atomicOr(&s_bits[j >> 5], 1u << (j & 31));
                 ++pos;
@@ -314,12 +315,12 @@ __global__ __launch_bounds__(TOPK_THREADS) void topk_kernel(const double *__rest
 // ---------------------------------------------------------------------------
 // A given protected column set: checks it (strictly ascending, in range),
 // then writes what topk_kernel writes for a selected one: the indices, the
-// scales absmax / 127, the column -> p map and the bitmap. One block per
+// scales absmax / pmax, the column -> p map and the bitmap. One block per
 // matrix. An invalid entry ORs 2 into *err and is left out.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(TOPK_THREADS) void colset_kernel(const int32_t *__restrict__ idx_in,
                                                               const float *__restrict__ absmax_all, int64_t d_in,
-                                                              int64_t k, int64_t words, int32_t *idx_out,
+                                                              int64_t k, int64_t words, float pmax, int32_t *idx_out,
                                                               float *__restrict__ scale_all,
                                                               int32_t *__restrict__ colmap_all,
                                                               uint32_t *__restrict__ bitmap_all, int32_t *err)
@@ -339,7 +340,7 @@ __global__ __launch_bounds__(TOPK_THREADS) void colset_kernel(const int32_t *__r
         }
         colmap_all[m * d_in + j] = int32_t(p);
         atomicOr(&s_bits[j >> 5], 1u << (j & 31));
-        scale_all[m * k + p] = absmax_all[m * d_in + j] / 127.0f;
+        scale_all[m * k + p] = absmax_all[m * d_in + j] / pmax;
         idx_out[m * k + p] = j;
     }
     __syncthreads();
@@ -349,8 +350,8 @@ __global__ __launch_bounds__(TOPK_THREADS) void colset_kernel(const int32_t *__r
 // ---------------------------------------------------------------------------
 // Protected output rows (eq. protected_8bit_scatter with row slices): one
 // block per (protected row p, matrix). Checks the set, then the row's absmax
-// (exact in any order), scale = absmax / 127, the int8 row (round half even,
-// clamped to +-127, zero past d_in and when the scale is 0), and clears the
+// (exact in any order), scale = absmax / payload_max, the row's stored bytes
+// (payload_from_f32; zero past d_in and when the scale is 0), and clears the
 // row's codes and gains in every stage plane (the row is not BSQ-coded). Runs
 // after the per-chunk encoder on the same stream.
 // ---------------------------------------------------------------------------
@@ -363,7 +364,7 @@ struct RowProtArgs {
     float *scale;     // [n_mats][k]
     void *codes[BSQ_MAX_STAGES];
     uint16_t *gains[BSQ_MAX_STAGES];
-    int stages, code_bytes;
+    int stages, code_bytes, pfmt;
     int32_t *err;
 };
 
@@ -395,23 +396,15 @@ __global__ __launch_bounds__(256) void rowprot_kernel(const RowProtArgs a)
     float am = s_max[0];
 #pragma unroll
     for (int w = 1; w < 4; ++w) am = (s_max[w] > am) ? s_max[w] : am;
-    const float sc = am / 127.0f;
+    const float sc = am / payload_max(a.pfmt);
     if (t == 0) {
         a.scale[m * a.k + p] = sc;
         a.idx_out[m * a.k + p] = i;
     }
     const int64_t qp = q8_pitch(a.d_in);
     int8_t *qrow = a.q8 + (m * a.k + p) * qp;
-    for (int64_t j = t; j < qp; j += 256) {
-        int8_t q = 0;
-        if (j < a.d_in && sc != 0.0f) {
-            float tq = __builtin_rintf(load_elem<T>(row + j) / sc);
-            if (tq > 127.0f) tq = 127.0f;
-            if (tq < -127.0f) tq = -127.0f;
-            q = int8_t(tq);
-        }
-        qrow[j] = q;
-    }
+    for (int64_t j = t; j < qp; j += 256)
+        qrow[j] = (j < a.d_in && sc != 0.0f) ? int8_t(payload_from_f32(load_elem<T>(row + j) / sc, a.pfmt)) : int8_t(0);
     const int64_t base = m * plane_elems(a.d_out, a.pitch);
     for (int64_t c = t; c < a.pitch; c += 256) {
         const int64_t gid = base + tile_index(i, c, a.pitch);
@@ -438,6 +431,7 @@ struct EncodeArgs {
     const int32_t *colmap;
     const uint32_t *bitmap;
     int32_t *err;
+    int pfmt;  // bsq_prot_format of q8
 };
 
 // one element of the tiled planes (padding rows and chunks included):
@@ -493,14 +487,8 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
                 if (!((pm >> j) & 1u)) continue;
                 const int32_t p = a.colmap[m * a.d_in + col0 + j];
                 const float sc = a.scale[m * a.k + p];
-                int8_t q = 0;
-                if (sc != 0.0f) {
-                    float tq = __builtin_rintf(w[j] / sc);
-                    if (tq > 127.0f) tq = 127.0f;
-                    if (tq < -127.0f) tq = -127.0f;
-                    q = int8_t(tq);
-                }
-                a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p] = q;
+                a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p] =
+                    (sc != 0.0f) ? int8_t(payload_from_f32(w[j] / sc, a.pfmt)) : int8_t(0);
             }
         }
     }
@@ -692,12 +680,12 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
         const int64_t words = prot_words(out.pitch, cfg.d);
         if (given)
             hipLaunchKernelGGL(colset_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st,
-                               given, ws.absmax, d_in, k, words, out.prot_idx, out.prot_scale, ws.colmap,
-                               out.prot_bits, err);
+                               given, ws.absmax, d_in, k, words, payload_max(cfg.protect_format), out.prot_idx,
+                               out.prot_scale, ws.colmap, out.prot_bits, err);
         else
             hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st,
-                               ws.keys, ws.absmax, d_in, k, words, out.prot_idx, out.prot_scale, ws.colmap,
-                               out.prot_bits);
+                               ws.keys, ws.absmax, d_in, k, words, payload_max(cfg.protect_format), out.prot_idx,
+                               out.prot_scale, ws.colmap, out.prot_bits);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (k > 0 && rows && !given) {
@@ -708,7 +696,8 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
         if (e != hipSuccess) return e;
         const int64_t words = (d_out + 31) / 32;
         hipLaunchKernelGGL(topk_kernel, dim3(unsigned(n_mats)), dim3(TOPK_THREADS), size_t(words) * 4, st, ws.keys,
-                           ws.absmax, d_out, k, words, out.prot_idx, out.prot_scale, ws.colmap, ws.bits);
+                           ws.absmax, d_out, k, words, payload_max(cfg.protect_format), out.prot_idx, out.prot_scale,
+                           ws.colmap, ws.bits);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     EncodeArgs a{};
@@ -731,6 +720,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
     a.colmap = ws.colmap;
     a.bitmap = (k > 0 && !rows) ? out.prot_bits : nullptr;
     a.err = err;
+    a.pfmt = cfg.protect_format;
     if (a.total > 0) {
         if (cfg.d == 8)
             e = bf ? launch_encode_chunks<8, uint16_t>(cfg.stages, a, st)
@@ -758,6 +748,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
         r.stages = cfg.stages;
         r.code_bytes = (cfg.d <= 8) ? 1 : 2;
         r.err = err;
+        r.pfmt = cfg.protect_format;
         const dim3 grid{unsigned(k), unsigned(n_mats)};
         if (bf) hipLaunchKernelGGL(rowprot_kernel<uint16_t>, grid, dim3(256), 0, st, r);
         else hipLaunchKernelGGL(rowprot_kernel<float>, grid, dim3(256), 0, st, r);
@@ -788,7 +779,7 @@ hipError_t launch_coupled_select(const void *Wg, const void *Wu, const void *Wd,
     if (k == 0) return hipSuccess;
     const int64_t words = (d_ffn + 31) / 32;
     hipLaunchKernelGGL(topk_kernel, dim3(1u), dim3(TOPK_THREADS), size_t(words) * 4, st, ws.keys, ws.absmax, d_ffn, k,
-                       words, idx, ws.scale, ws.colmap, ws.bits);
+                       words, 127.0f, idx, ws.scale, ws.colmap, ws.bits);
     return hipGetLastError();
 }
 

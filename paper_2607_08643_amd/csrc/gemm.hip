@@ -72,6 +72,7 @@ struct GemmArgs {
     uint32_t *poison;  // the workspace's poison word
     int32_t *err;      // caller's device error word, or null
     int spin_limit;    // polls before a wait gives up (wait_limit())
+    int pfmt;          // bsq_prot_format of q8
 };
 
 // The finishing block's outcome when it could not use the other blocks'
@@ -491,9 +492,9 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
     lds_barrier();
 
     // protected term (split 0, by the kh = 1 waves): X[:, idx] (bf16) times
-    // bf16(q8 s), the weights of lane row 16 (NT rs + j) + lane % 16 at
+    // bf16(value(q8) s), the weights of lane row 16 (NT rs + j) + lane % 16 at
     // positions 32 qq + 8 g + e; two slices of 32 positions per round, all
-    // their loads issued together (int8 codes as one 8-byte word per row;
+    // their loads issued together (stored bytes as one 8-byte word per row;
     // positions past k read as zero)
     if (kh == 1 && z == 0 && a.k > 0) {
         const int64_t kp = q8_pitch(a.k), nq = a.kp32 / 32;
@@ -526,7 +527,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
                         const uint32_t w = (e < 4) ? qv[h][j].x : qv[h][j].y;
-                        v[e] = float(int8_t(uint8_t(w >> (8 * (e & 3))))) * sc[h][e];
+                        v[e] = payload_to_f32(w >> (8 * (e & 3)), a.pfmt) * sc[h][e];
                     }
                     const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                                pack_bf16x2(v[6], v[7])};
@@ -944,7 +945,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
     }
 
     const int64_t n0 = rg * 64;
-    // protected term: X[:, idx] (bf16) times bf16(q8 s), from LDS when staged
+    // protected term: X[:, idx] (bf16) times bf16(value(q8) s), from LDS when staged
     if (a.k > 0) {
         for (int64_t qq = 0; qq < a.kp32 / 32; ++qq) {
             const int64_t p0 = 32 * qq + 8 * g;
@@ -964,7 +965,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
                     const uint32_t w = (e < 4) ? qv.x : qv.y;
-                    v[e] = float(int8_t(uint8_t(w >> (8 * (e & 3))))) * sc[e];
+                    v[e] = payload_to_f32(w >> (8 * (e & 3)), a.pfmt) * sc[e];
                 }
                 const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                            pack_bf16x2(v[6], v[7])};
@@ -1175,6 +1176,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     a.poison = static_cast<uint32_t *>(ws);
     a.err = err;
     a.spin_limit = wait_limit();
+    a.pfmt = cfg.protect_format;
 
     PrepArgs pa{};
     pa.X = static_cast<const uint16_t *>(X);

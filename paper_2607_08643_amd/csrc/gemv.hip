@@ -122,6 +122,7 @@ struct GemvArgs {
     uint32_t *poison;  // row-lane kernel: the workspace's poison word
     int32_t *err;      // caller's device error word, or null
     int spin_limit;    // polls before a wait gives up (wait_limit())
+    int pfmt;          // bsq_prot_format of the protected payload
 };
 
 __device__ __forceinline__ float load_x(const void *x, int64_t j, int bf)
@@ -377,7 +378,8 @@ __global__ __launch_bounds__(512) void gemv_stream_kernel(const GemvArgs a)
         float v = 0.0f;
         const float *rp = s_red + r * nseg;
         for (int q = g; q < nseg; q += G) v += rp[q];
-        for (int64_t p = g; p < a.k; p += G) v = __builtin_fmaf(float(M.q8[row * q8_pitch(a.k) + p]), s_xs[p], v);
+        for (int64_t p = g; p < a.k; p += G)
+            v = __builtin_fmaf(payload_to_f32(uint8_t(M.q8[row * q8_pitch(a.k) + p]), a.pfmt), s_xs[p], v);
         for (int q = g; q < M.rank; q += G) v = __builtin_fmaf(bf16_to_f32(M.B[row * M.rank + q]), M.t[q], v);
         for (int o = G >> 1; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
         if (g == 0) {
@@ -464,17 +466,23 @@ __device__ __forceinline__ void lane_store(const GemvArgs &a, const GemvMat &M, 
     else static_cast<float *>(M.y)[row] = v;
 }
 
-// Sixteen protected columns of one row: int8 codes (one 16-byte word) against
-// the scaled activations xs[0 .. 15] (LDS, 16-byte aligned, zero past k).
-__device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc)
+// Sixteen protected columns of one row: stored bytes (one 16-byte word, in
+// format fmt) against the scaled activations xs[0 .. 15] (LDS, 16-byte
+// aligned, zero past k).
+__device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc, int fmt)
 {
     const float4 *x4 = reinterpret_cast<const float4 *>(xs);
     const float4 xa = x4[0], xb = x4[1], xc = x4[2], xd = x4[3];
     const float xv[16] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w,
                           xc.x, xc.y, xc.z, xc.w, xd.x, xd.y, xd.z, xd.w};
     const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
+    if (fmt == BSQ_PROT_INT8) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), xv[e], acc);
+        for (int e = 0; e < 16; ++e) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), xv[e], acc);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc = __builtin_fmaf(payload_to_f32(qw[e >> 2] >> (8 * (e & 3)), fmt), xv[e], acc);
+    }
     return acc;
 }
 
@@ -494,7 +502,7 @@ __device__ __forceinline__ float lane_q8_global(const GemvArgs &a, const GemvMat
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const uint4 q = (w0 + u < nw) ? qv[u] : make_uint4(0, 0, 0, 0);
-            acc = q8_block(q, s_xs + 16 * ((w0 + u < nw) ? w0 + u : nw - 1), acc);
+            acc = q8_block(q, s_xs + 16 * ((w0 + u < nw) ? w0 + u : nw - 1), acc, a.pfmt);
             asm volatile("" : "+v"(acc));  // one word's activations live at a time
         }
     }
@@ -516,10 +524,10 @@ __device__ __forceinline__ float lane_extras(const GemvArgs &a, const GemvMat &M
             int64_t w = 0;
             for (; w + 2 <= nw; w += 2) {  // two words per step, their LDS reads together
                 const uint4 q0 = qr[w], q1 = qr[w + 1];
-                acc = q8_block(q0, s_xs + 16 * w, acc);
-                acc = q8_block(q1, s_xs + 16 * (w + 1), acc);
+                acc = q8_block(q0, s_xs + 16 * w, acc, a.pfmt);
+                acc = q8_block(q1, s_xs + 16 * (w + 1), acc, a.pfmt);
             }
-            if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc);
+            if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc, a.pfmt);
         } else {
             acc = lane_q8_global(a, M, s_xs, row, acc);
         }
@@ -1038,7 +1046,8 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
         }
     }
     for (int64_t p = lane; p < a.k; p += 64)
-        acc = __builtin_fmaf(float(M.q8[row * q8_pitch(a.k) + p]), M.scale[p] * x[M.idx[p]], acc);
+        acc = __builtin_fmaf(payload_to_f32(uint8_t(M.q8[row * q8_pitch(a.k) + p]), a.pfmt), M.scale[p] * x[M.idx[p]],
+                             acc);
     for (int q = lane; q < M.rank; q += 64) acc = __builtin_fmaf(bf16_to_f32(M.B[row * M.rank + q]), M.t[q], acc);
     for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
     if (lane == 0) {
@@ -1101,6 +1110,7 @@ GemvArgs make_args(const bsq_config &cfg, int n, const void *const *codecs, cons
     float *wt = reinterpret_cast<float *>(wb);
     a.poison = static_cast<uint32_t *>(ws);
     a.spin_limit = wait_limit();
+    a.pfmt = cfg.protect_format;
     // workspace of one configuration: header, LoRA vectors, folded activation
     // records, slots. The shared scratch array of bsq_gemv_noalloc keeps the
     // records in its last GEMV_SCRATCH_XP_BYTES instead, so that the slots of

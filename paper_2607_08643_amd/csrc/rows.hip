@@ -3,10 +3,11 @@
 // the gate/up side of eq. mlp_coupled_protection). The coded rows go through
 // the streaming decode/GEMV/GEMM kernels, where a protected row's code 0 and
 // gain +0 make its BSQ term zero; these kernels then write every protected
-// row of the result from its int8 payload, on the same stream:
-//   decode  W_hat[idx_p, j] = q8[p][j] * scale_p            (fp32 product)
-//   GEMV    y[idx_p]        = scale_p <q8[p], x> + B[idx_p] . (A x)
-//   GEMM    Y[t][idx_p]     = scale_p <q8[p], X[t]> + B[idx_p] . T[t]
+// row of the result from its protected payload (value(q8) per the format,
+// payload_to_f32), on the same stream:
+//   decode  W_hat[idx_p, j] = value(q8[p][j]) * scale_p        (fp32 product)
+//   GEMV    y[idx_p]        = scale_p <value(q8[p]), x> + B[idx_p] . (A x)
+//   GEMM    Y[t][idx_p]     = scale_p <value(q8[p]), X[t]> + B[idx_p] . T[t]
 // (T = X A^T, fp32, left in the GEMM workspace by its activation prep).
 // All three are small side launches: k = ceil(rho * d_out) rows.
 #include "bsq_internal.h"
@@ -19,7 +20,7 @@ template <bool BF16OUT>
 __global__ __launch_bounds__(256) void decode_rows_kernel(const int32_t *__restrict__ idx,
                                                           const int8_t *__restrict__ q8,
                                                           const float *__restrict__ scale, int64_t d_out,
-                                                          int64_t d_in, int64_t k, void *__restrict__ out)
+                                                          int64_t d_in, int64_t k, int fmt, void *__restrict__ out)
 {
     const int64_t p = blockIdx.x, m = blockIdx.y;
     const int64_t row = idx[m * k + p];
@@ -27,7 +28,7 @@ __global__ __launch_bounds__(256) void decode_rows_kernel(const int32_t *__restr
     const int8_t *q = q8 + (m * k + p) * q8_pitch(d_in);
     const int64_t base = (m * d_out + row) * d_in;
     for (int64_t j = threadIdx.x; j < d_in; j += 256) {
-        const float v = float(q[j]) * s;
+        const float v = payload_to_f32(uint8_t(q[j]), fmt) * s;
         if constexpr (BF16OUT) static_cast<uint16_t *>(out)[base + j] = f32_to_bf16(v);
         else static_cast<float *>(out)[base + j] = v;
     }
@@ -51,7 +52,7 @@ struct RowsGemvArgs {
     int rank[BSQ_MAX_GROUP];
     const void *x;
     int64_t d_in;
-    int x_bf16, y_bf16;
+    int x_bf16, y_bf16, pfmt;
 };
 
 // One block per (protected row p, matrix m of the group). Each thread sums
@@ -73,7 +74,7 @@ __global__ __launch_bounds__(256) void gemv_rows_kernel(const RowsGemvArgs a)
     for (int64_t j = t; j < a.d_in; j += 256) {
         const float xv = a.x_bf16 ? bf16_to_f32(static_cast<const uint16_t *>(a.x)[j])
                                   : static_cast<const float *>(a.x)[j];
-        acc += float(q[j]) * xv;
+        acc += payload_to_f32(uint8_t(q[j]), a.pfmt) * xv;
 #pragma unroll
         for (int r = 0; r < BSQ_MAX_LORA_RANK; ++r)
             if (r < rank) tr[r] += bf16_to_f32(A[r * a.d_in + j]) * xv;
@@ -111,7 +112,7 @@ struct RowsGemmArgs {
     const uint16_t *X;  // [M][ldx] bf16
     void *Y;            // [M][ldy]
     int64_t M, ldx, ldy, d_in, k;
-    int rank, y_bf16;
+    int rank, y_bf16, pfmt;
 };
 
 // One block per (protected row p, 4 tokens); wave w takes token 4 by + w and
@@ -125,7 +126,7 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const RowsGemmArgs a)
     const int8_t *q = a.q8 + p * q8_pitch(a.d_in);
     const uint16_t *xr = a.X + tok * a.ldx;
     float acc = 0.0f;
-    for (int64_t j = lane; j < a.d_in; j += 64) acc += float(q[j]) * bf16_to_f32(xr[j]);
+    for (int64_t j = lane; j < a.d_in; j += 64) acc += payload_to_f32(uint8_t(q[j]), a.pfmt) * bf16_to_f32(xr[j]);
     acc = wave_sum(acc);
     if (lane != 0) return;
     const int64_t row = a.idx[p];
@@ -138,21 +139,21 @@ __global__ __launch_bounds__(256) void gemm_rows_kernel(const RowsGemmArgs a)
 
 }  // namespace
 
-hipError_t launch_decode_rows(const bsq_layer &L, void *w_hat, int out_dtype, hipStream_t st)
+hipError_t launch_decode_rows(const bsq_layer &L, int fmt, void *w_hat, int out_dtype, hipStream_t st)
 {
     if (L.k == 0 || L.d_in == 0 || L.n_mats == 0) return hipSuccess;
     const dim3 grid{unsigned(L.k), unsigned(L.n_mats)};
     if (out_dtype == BSQ_BF16)
         hipLaunchKernelGGL(decode_rows_kernel<true>, grid, dim3(256), 0, st, L.prot_idx, L.prot_q8, L.prot_scale,
-                           L.d_out, L.d_in, L.k, w_hat);
+                           L.d_out, L.d_in, L.k, fmt, w_hat);
     else
         hipLaunchKernelGGL(decode_rows_kernel<false>, grid, dim3(256), 0, st, L.prot_idx, L.prot_q8, L.prot_scale,
-                           L.d_out, L.d_in, L.k, w_hat);
+                           L.d_out, L.d_in, L.k, fmt, w_hat);
     return hipGetLastError();
 }
 
-hipError_t launch_gemv_rows(int n, const bsq_layer *layers, const bsq_lora *loras, const void *x, int x_dtype,
-                            void *const *y, int y_dtype, hipStream_t st)
+hipError_t launch_gemv_rows(int n, const bsq_layer *layers, int fmt, const bsq_lora *loras, const void *x,
+                            int x_dtype, void *const *y, int y_dtype, hipStream_t st)
 {
     RowsGemvArgs a{};
     int64_t kmax = 0;
@@ -175,12 +176,13 @@ hipError_t launch_gemv_rows(int n, const bsq_layer *layers, const bsq_lora *lora
     a.d_in = layers[0].d_in;
     a.x_bf16 = (x_dtype == BSQ_BF16);
     a.y_bf16 = (y_dtype == BSQ_BF16);
+    a.pfmt = fmt;
     hipLaunchKernelGGL(gemv_rows_kernel, dim3(unsigned(kmax), unsigned(n)), dim3(256), 0, st, a);
     return hipGetLastError();
 }
 
-hipError_t launch_gemm_rows(const bsq_layer &L, const bsq_lora *lora, const void *X, int64_t M, int64_t ldx,
-                            void *Y, int y_dtype, int64_t ldy, const float *T, hipStream_t st)
+hipError_t launch_gemm_rows(const bsq_layer &L, int fmt, const bsq_lora *lora, const void *X, int64_t M,
+                            int64_t ldx, void *Y, int y_dtype, int64_t ldy, const float *T, hipStream_t st)
 {
     if (L.k == 0 || M == 0) return hipSuccess;
     RowsGemmArgs a{};
@@ -196,6 +198,7 @@ hipError_t launch_gemm_rows(const bsq_layer &L, const bsq_lora *lora, const void
     a.d_in = L.d_in;
     a.k = L.k;
     a.y_bf16 = (y_dtype == BSQ_BF16);
+    a.pfmt = fmt;
     if (lora && lora->rank > 0) {
         a.B = lora->B;
         a.rank = lora->rank;

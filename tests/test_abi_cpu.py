@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 5
+    assert bsq.bsq_version() == 6
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -41,8 +41,12 @@ def test_library_exports_every_declared_symbol():
     (dict(d=17), bsq.BSQ_ERR_ARG),
     (dict(stages=0), bsq.BSQ_ERR_ARG),
     (dict(stages=5), bsq.BSQ_ERR_ARG),
-    (dict(kind=3), bsq.BSQ_ERR_ARG),
+    (dict(kind=4), bsq.BSQ_ERR_ARG),
     (dict(hidden=0), bsq.BSQ_ERR_ARG),
+    (dict(kind=bsq.DEC_MLP_RES1, hidden=0), bsq.BSQ_ERR_ARG),
+    (dict(kind=bsq.DEC_MLP_RES1, hidden=65), bsq.BSQ_ERR_ARG),
+    (dict(protect_format=3), bsq.BSQ_ERR_ARG),
+    (dict(protect_format=-1), bsq.BSQ_ERR_ARG),
     (dict(hidden=65), bsq.BSQ_ERR_ARG),
     (dict(protect_num=2, protect_den=1), bsq.BSQ_ERR_ARG),
     (dict(protect_num=-1), bsq.BSQ_ERR_ARG),
@@ -50,6 +54,10 @@ def test_library_exports_every_declared_symbol():
     (dict(), bsq.BSQ_OK),
     (dict(d=16, hidden=16), bsq.BSQ_OK),
     (dict(kind=bsq.DEC_IDENTITY, hidden=0), bsq.BSQ_OK),
+    (dict(kind=bsq.DEC_MLP_RES1), bsq.BSQ_OK),
+    (dict(d=16, kind=bsq.DEC_MLP_RES1, hidden=5), bsq.BSQ_OK),
+    (dict(protect_format=bsq.PROT_E4M3), bsq.BSQ_OK),
+    (dict(protect_format=bsq.PROT_E5M2, protect_axis=1), bsq.BSQ_OK),
 ])
 def test_config_validation(kw, status):
     assert bsq.bsq_config_check(bsq.Config(**kw)) == status
@@ -65,14 +73,16 @@ def test_code_bits_must_equal_chunk_length():
 @pytest.mark.parametrize("shape", [(4096, 4096), (1024, 4096), (4096, 12288), (25600, 5120), (333, 296), (0, 256)])
 @pytest.mark.parametrize("rank", [0, 16])
 @pytest.mark.parametrize("axis", [0, 1], ids=["cols", "rows"])
-def test_sizes_match_oracle_accounting(d, shape, rank, axis):
+@pytest.mark.parametrize("kind", [bsq.DEC_MLP, bsq.DEC_MLP_RES1], ids=["res0", "res1"])
+def test_sizes_match_oracle_accounting(d, shape, rank, axis, kind):
     d_out, d_in = shape
     if d_in % d:
         pytest.skip("not chunkable")
-    cfg = bsq.Config(d=d, hidden=d, protect_axis=axis)
+    fmt = bsq.PROT_E4M3 if kind == bsq.DEC_MLP_RES1 else bsq.PROT_INT8   # the format does not change a size
+    cfg = bsq.Config(d=d, hidden=d, kind=kind, protect_axis=axis, protect_format=fmt)
     got = bsq.bsq_layer_sizes(cfg, d_out, d_in, rank)
-    ref = oracle.sizes(oracle.Config(d=d, b=d, stages=2, kind=oracle.KIND_MLP, hidden=d, protect_axis=axis),
-                       d_out, d_in, rank)
+    ref = oracle.sizes(oracle.Config(d=d, b=d, stages=2, kind=kind, hidden=d, protect_axis=axis,
+                                     protect_format=fmt), d_out, d_in, rank)
     for key in ("S_code", "S_dec", "S_8bit", "S_LoRA", "S_meta", "S_tot", "bpw_nominal"):
         assert got[key] == pytest.approx(ref[key], rel=0, abs=1e-9), key
     if d_out:
@@ -280,6 +290,15 @@ def test_codec_prepare_rejects_before_launch():
     assert Lib.bsq_codec_prepare(ct.byref(c), None, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
     nob2 = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, 0)] * 4)
     assert Lib.bsq_codec_prepare(ct.byref(c), nob2, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
+    # the residual-block decoder needs R and c as well; it has no split tables at d = 16
+    r1 = bsq.Config(kind=bsq.DEC_MLP_RES1)
+    c1 = r1.c()
+    assert bsq.bsq_codec_bytes(r1) == need
+    assert bsq.bsq_codec_bytes(bsq.Config(d=16, hidden=16, kind=bsq.DEC_MLP_RES1)) == 2 * 65536 * 16 * 8
+    noR = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE, 0, FAKE)] * 4)
+    noc = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE, FAKE, 0)] * 4)
+    for dd in (noR, noc):
+        assert Lib.bsq_codec_prepare(ct.byref(c1), dd, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
 
 
 def test_workspace_sizes_are_positive_and_grow():

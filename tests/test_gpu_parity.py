@@ -24,12 +24,15 @@ from parity_bounds import check_close, product_floor, say, term_bar
 
 pytestmark = pytest.mark.gpu
 
-OKIND = {bsq.DEC_IDENTITY: oracle.KIND_IDENTITY, bsq.DEC_LINEAR: oracle.KIND_LINEAR, bsq.DEC_MLP: oracle.KIND_MLP}
+OKIND = {bsq.DEC_IDENTITY: oracle.KIND_IDENTITY, bsq.DEC_LINEAR: oracle.KIND_LINEAR, bsq.DEC_MLP: oracle.KIND_MLP,
+         bsq.DEC_MLP_RES1: oracle.KIND_MLP_RES1}
+OFMT = {bsq.PROT_INT8: oracle.FMT_INT8, bsq.PROT_E4M3: oracle.FMT_E4M3, bsq.PROT_E5M2: oracle.FMT_E5M2}
 
 
 def ocfg(cfg: bsq.Config) -> oracle.Config:
     return oracle.Config(d=cfg.d, b=cfg.d, stages=cfg.stages, kind=OKIND[cfg.kind], hidden=cfg.hidden,
-                         protect_num=cfg.protect_num, protect_den=cfg.protect_den)
+                         protect_num=cfg.protect_num, protect_den=cfg.protect_den,
+                         protect_format=OFMT[cfg.protect_format])
 
 
 def np_codes(L, t):
@@ -58,8 +61,8 @@ def assert_layer_equal(layer, enc, cfg, m=None):
     if cfg.k(L.d_in):
         np.testing.assert_array_equal(L.idx.cpu().numpy(), enc.idx, err_msg="protected indices")
         q8 = L.q8.cpu().numpy()
-        np.testing.assert_array_equal(q8[:, :enc.q8.shape[1]], enc.q8, err_msg="int8 payload")
-        assert not q8[:, enc.q8.shape[1]:].any(), "int8 payload padding"
+        np.testing.assert_array_equal(q8[:, :enc.q8.shape[1]], enc.q8, err_msg="protected payload")
+        assert not q8[:, enc.q8.shape[1]:].any(), "protected payload padding"
         np.testing.assert_array_equal(L.scale.cpu().numpy().view(np.uint32), enc.scale.view(np.uint32),
                                       err_msg="scales")
         # bitmap over the padded columns: exactly the oracle's protected set
@@ -99,6 +102,15 @@ SMALL = [
     ("rho25-64x256-d8", 64, 256, dict(d=8, hidden=8, protect_num=1, protect_den=4), torch.bfloat16, 1, False),
     ("mlp-3stage-100x768-d16", 100, 768, dict(d=16, hidden=16, stages=3), torch.bfloat16, 1, False),
     ("stack2-130x1056-d16", 130, 1056, dict(d=16, hidden=16), torch.bfloat16, 2, False),
+    # the component ablation's variants: decoder with one residual block, FP8 protected payloads
+    ("res1-160x512-d8", 160, 512, dict(d=8, hidden=8, kind=bsq.DEC_MLP_RES1), torch.bfloat16, 1, False),
+    ("res1-h12-96x640-d16", 96, 640, dict(d=16, hidden=12, kind=bsq.DEC_MLP_RES1), torch.bfloat16, 1, False),
+    ("e4m3-200x512-d8", 200, 512, dict(d=8, hidden=8, protect_format=bsq.PROT_E4M3, protect_num=1, protect_den=32),
+     torch.bfloat16, 1, False),
+    ("e5m2-77x592-d16", 77, 592, dict(d=16, hidden=16, protect_format=bsq.PROT_E5M2, protect_num=1, protect_den=50),
+     torch.bfloat16, 1, False),
+    ("res1-e4m3-fp32-64x256-d8", 64, 256, dict(d=8, hidden=8, kind=bsq.DEC_MLP_RES1, protect_format=bsq.PROT_E4M3),
+     torch.float32, 1, False),
 ]
 
 
@@ -207,7 +219,7 @@ SPLITK = [
     ("splitk-200x2600-d8", 200, 2600, dict(d=8, hidden=8), torch.bfloat16, 1, False),
     ("splitk-130x2608-d16", 130, 2608, dict(d=16, hidden=16), torch.bfloat16, 1, False),
 ]
-GEMM_CASES = [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11]] + SPLITK
+GEMM_CASES = [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11], SMALL[14], SMALL[15], SMALL[16], SMALL[17]] + SPLITK
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[c[0] for c in GEMM_CASES])
@@ -510,17 +522,22 @@ TERM_CASES = [
     ("d16-linear-130x768", 130, 768, dict(d=16, kind=bsq.DEC_LINEAR), torch.bfloat16),
     ("d8-fp32x-256x512", 256, 512, dict(d=8, hidden=8), torch.float32),
     ("d8-4096x4096", 4096, 4096, dict(d=8, hidden=8), torch.bfloat16),
+    ("d8-e4m3-300x1024", 300, 1024, dict(d=8, hidden=8, protect_format=bsq.PROT_E4M3), torch.bfloat16),
+    ("d16-e5m2-200x1024", 200, 1024, dict(d=16, hidden=16, protect_format=bsq.PROT_E5M2), torch.bfloat16),
+    ("d8-res1-e5m2-fp32x-256x512", 256, 512, dict(d=8, hidden=8, kind=bsq.DEC_MLP_RES1,
+                                                   protect_format=bsq.PROT_E5M2), torch.float32),
 ]
 
 
-def _terms_ref(enc, w_hat, X, lref):
+def _terms_ref(enc, w_hat, X, lref, fmt=oracle.FMT_INT8):
     """For activations X ([d_in] or [M, d_in]): the oracle's LoRA term
-    B (A x), the int8 protected term sum_p q8[:, p] scale_p x_idx_p and the
-    root sum of squares of its parts, and the sum of |terms| of the whole
-    product, per output (fp64, the shape of the product)."""
+    B (A x), the protected term sum_p value(q8[:, p]) scale_p x_idx_p (stored
+    bytes read in format fmt) and the root sum of squares of its parts, and
+    the sum of |terms| of the whole product, per output (fp64, the shape of
+    the product)."""
     X64 = np.atleast_2d(np.asarray(X, dtype=np.float64))
     A64, B64 = (np.asarray(v, dtype=np.float64) for v in lref)
-    q8 = enc.q8.astype(np.float64)
+    q8 = oracle.payload_values(enc.q8, fmt).astype(np.float64)
     lora = (X64 @ A64.T) @ B64.T
     sx = enc.scale.astype(np.float64)[None, :] * X64[:, enc.idx]
     q8t = sx @ q8.T
@@ -553,20 +570,22 @@ def test_gemv_lora_and_protected_terms(case, gpu):
     torch.cuda.synchronize()
     xf = oracle.to_f32(x)
     w_hat = oracle.decode(ocfg(cfg), decs, enc, tables=tabs)
-    lora, q8t, _, total = _terms_ref(enc, w_hat, xf, (oracle.to_f32(A), oracle.to_f32(Bm)))
+    lora, q8t, _, total = _terms_ref(enc, w_hat, xf, (oracle.to_f32(A), oracle.to_f32(Bm)),
+                                     OFMT[cfg.protect_format])
     y_l, y_0, y_m = (v.cpu().numpy() for v in (y_l, y_0, y_m))
     assert term_bar(y_l, y_0, lora, total, 16, "LoRA term") > 100
-    assert term_bar(y_0, y_m, q8t, total, len(enc.idx), "int8 protected term") > 100
+    assert term_bar(y_0, y_m, q8t, total, len(enc.idx), "protected term") > 100
 
 
-@pytest.mark.parametrize("d,M", [(8, 16), (8, 64), (16, 16), (16, 256)])
-def test_gemm_lora_and_protected_terms(d, M, gpu):
+@pytest.mark.parametrize("d,M,fmt", [(8, 16, bsq.PROT_INT8), (8, 64, bsq.PROT_INT8), (16, 16, bsq.PROT_INT8),
+                                     (16, 256, bsq.PROT_INT8), (8, 64, bsq.PROT_E4M3), (16, 16, bsq.PROT_E5M2)])
+def test_gemm_lora_and_protected_terms(d, M, fmt, gpu):
     """As for the GEMV, on the fused GEMM: the LoRA term (fp32) to within fp32
     rounding; the protected term goes through the MFMA as bf16(q8 scale), so
     its bar adds the sub-Gaussian bound of those roundings."""
-    say(f"gemm term presence d={d} M={M}")
-    cfg, decs, codec, layer, W, encs, tabs = _make("gemm-terms", 320, 2048, dict(d=d, hidden=d), torch.bfloat16,
-                                                   1, False, gpu)
+    say(f"gemm term presence d={d} M={M} format={fmt}")
+    cfg, decs, codec, layer, W, encs, tabs = _make("gemm-terms", 320, 2048, dict(d=d, hidden=d, protect_format=fmt),
+                                                   torch.bfloat16, 1, False, gpu)
     enc = encs[0]
     X = synth.activation(2048, seed=17, dtype=torch.bfloat16, batch=M)
     A, Bm = synth.lora(320, 2048, 16, seed=18)
@@ -580,6 +599,6 @@ def test_gemm_lora_and_protected_terms(d, M, gpu):
     Xf = oracle.to_f32(X)
     w_hat = oracle.decode(ocfg(cfg), decs, enc, tables=tabs)
     Y_l, Y_0, Y_m = (v.cpu().numpy() for v in (Y_l, Y_0, Y_m))
-    lora, q8t, q8sq, total = _terms_ref(enc, w_hat, Xf, (oracle.to_f32(A), oracle.to_f32(Bm)))
+    lora, q8t, q8sq, total = _terms_ref(enc, w_hat, Xf, (oracle.to_f32(A), oracle.to_f32(Bm)), OFMT[fmt])
     assert term_bar(Y_l, Y_0, lora, total, 16, "LoRA term") > 100
-    assert term_bar(Y_0, Y_m, q8t, total, len(enc.idx), "int8 protected term", rounded=q8sq) > 10
+    assert term_bar(Y_0, Y_m, q8t, total, len(enc.idx), "protected term", rounded=q8sq) > 10

@@ -15,14 +15,15 @@ import torch
 import oracle
 import paper_2607_08643_amd as bsq
 import synth
-from test_gpu_parity import OKIND, check_product, decoders, gemv_kind, np_codes, np_gains, say
+from test_gpu_parity import OFMT, OKIND, check_product, decoders, gemv_kind, np_codes, np_gains, say
 
 pytestmark = pytest.mark.gpu
 
 
 def ocfg(cfg: bsq.Config) -> oracle.Config:
     return oracle.Config(d=cfg.d, b=cfg.d, stages=cfg.stages, kind=OKIND[cfg.kind], hidden=cfg.hidden,
-                         protect_num=cfg.protect_num, protect_den=cfg.protect_den, protect_axis=cfg.protect_axis)
+                         protect_num=cfg.protect_num, protect_den=cfg.protect_den, protect_axis=cfg.protect_axis,
+                         protect_format=OFMT[cfg.protect_format])
 
 
 def planted_rows(d_out, k, seed):
@@ -66,6 +67,9 @@ ROWS = [
     ("rows-stack2-96x640-d16", 96, 640, dict(d=16, hidden=16), torch.bfloat16, 2, False),
     ("rows-64x256-d8-identity", 64, 256, dict(d=8, kind=bsq.DEC_IDENTITY, hidden=0, protect_num=1,
                                                protect_den=8), torch.bfloat16, 1, False),
+    ("rows-e4m3-200x512-d8", 200, 512, dict(d=8, hidden=8, protect_format=bsq.PROT_E4M3), torch.bfloat16, 1, False),
+    ("rows-e5m2-res1-96x640-d16", 96, 640, dict(d=16, hidden=16, kind=bsq.DEC_MLP_RES1,
+                                                 protect_format=bsq.PROT_E5M2), torch.bfloat16, 1, False),
 ]
 
 
@@ -166,7 +170,10 @@ def test_row_protected_grouped_gemv(d, gpu):
                       lref, f"group member {i}", torch.float32)
 
 
-@pytest.mark.parametrize("case", [ROWS[0], ROWS[1], ROWS[2]], ids=[c[0] for c in ROWS[:3]])
+GEMM_ROWS = [ROWS[0], ROWS[1], ROWS[2], ROWS[5], ROWS[6]]
+
+
+@pytest.mark.parametrize("case", GEMM_ROWS, ids=[c[0] for c in GEMM_ROWS])
 @pytest.mark.parametrize("M", [1, 5, 16, 64, 100])
 def test_row_protected_gemm(case, M, gpu):
     say(f"case {case[0]} M={M}")

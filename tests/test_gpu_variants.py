@@ -1,0 +1,98 @@
+"""The FP8 protected payloads on the GPU at the values where a conversion can
+go wrong: a protected slice whose scale is exactly 1 (its largest magnitude is
+the format's largest finite value) and whose entries are every non-negative
+finite value of the format, every midpoint between neighbours (ties to the
+even code), points a quarter step off, values below the smallest subnormal
+and signed zeros, each with both signs. The stored bytes must equal the
+oracle's (found there by trying every code) and torch's own float8 cast, and
+the decoded slice must be torch's reading of those bytes, on the input-column
+axis and on the output-row axis.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2607_08643_amd as bsq
+import synth
+from parity_bounds import say
+from test_gpu_parity import OFMT, OKIND, check_product, decoders, gemv_kind
+
+pytestmark = pytest.mark.gpu
+
+TORCH_FP8 = {bsq.PROT_E4M3: torch.float8_e4m3fn, bsq.PROT_E5M2: torch.float8_e5m2}
+FMAX = {bsq.PROT_E4M3: 448.0, bsq.PROT_E5M2: 57344.0}
+
+
+def crafted_values(fmt):
+    raw = torch.arange(128, dtype=torch.int32).to(torch.uint8)
+    vals = raw.view(TORCH_FP8[fmt]).to(torch.float64).numpy()
+    fin = vals[np.isfinite(vals) & (vals <= FMAX[fmt])]
+    mids = (fin[:-1] + fin[1:]) / 2
+    quarter = fin[:-1] + (fin[1:] - fin[:-1]) / 4
+    tiny = fin[1] * np.array([0.25, 0.5, 0.75])
+    v = np.concatenate([fin, mids, quarter, tiny]).astype(np.float32)
+    v = np.concatenate([v, -v])
+    assert np.abs(v).max() == FMAX[fmt]
+    return v
+
+
+def ocfg(cfg):
+    return oracle.Config(d=cfg.d, b=cfg.d, stages=cfg.stages, kind=OKIND[cfg.kind], hidden=cfg.hidden,
+                         protect_num=cfg.protect_num, protect_den=cfg.protect_den, protect_axis=cfg.protect_axis,
+                         protect_format=OFMT[cfg.protect_format])
+
+
+@pytest.mark.parametrize("fmt", [bsq.PROT_E4M3, bsq.PROT_E5M2], ids=["e4m3", "e5m2"])
+@pytest.mark.parametrize("axis", [0, 1], ids=["cols", "rows"])
+@pytest.mark.parametrize("d", [8, 16])
+def test_fp8_payload_at_every_code_and_tie(fmt, axis, d, gpu):
+    vals = crafted_values(fmt)
+    n = len(vals)
+    slice_len = (n + 63) // 64 * 64
+    r = np.random.default_rng(5 + fmt + 2 * axis)
+    if axis == 0:
+        d_out, d_in, j0 = slice_len, 256, 37
+        W = r.normal(0, 0.02, (d_out, d_in)).astype(np.float32)
+        W[:, j0] = 0.0
+        W[:n, j0] = vals
+    else:
+        d_out, d_in, j0 = 96, slice_len, 41
+        W = r.normal(0, 0.02, (d_out, d_in)).astype(np.float32)
+        W[j0, :] = 0.0
+        W[j0, :n] = vals
+    cfg = bsq.Config(d=d, hidden=d, protect_axis=axis, protect_format=fmt, protect_num=1,
+                     protect_den=(d_in if axis == 0 else d_out))     # k = 1: the planted slice
+    say(f"fp8 crafted slice fmt={fmt} axis={axis} d={d} n={n}")
+    decs = decoders(cfg, seed=13)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, torch.from_numpy(W).to(gpu))
+    w_hat = bsq.bsq_decode(cfg, codec, layer, dtype=torch.float32)
+    torch.cuda.synchronize()
+    oc = ocfg(cfg)
+    enc = oracle.encode(oc, decs, W)
+    assert list(enc.idx) == [j0]
+    assert float(enc.scale[0]) == 1.0
+    got_idx = layer.idx.cpu().numpy()
+    assert list(got_idx) == [j0]
+    assert float(layer.scale.cpu()[0]) == 1.0
+    q = layer.q8.cpu().numpy()
+    stored = (q[:n, 0] if axis == 0 else q[0, :n]).view(np.uint8)
+    want_oracle = (enc.q8[:n, 0] if axis == 0 else enc.q8[0, :n]).view(np.uint8)
+    want_torch = torch.from_numpy(vals).to(TORCH_FP8[fmt]).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(stored, want_oracle, err_msg="bytes vs oracle")
+    np.testing.assert_array_equal(stored, want_torch, err_msg="bytes vs torch")
+    wh = w_hat.cpu().numpy()
+    dec = wh[:n, j0] if axis == 0 else wh[j0, :n]
+    want = torch.from_numpy(stored.copy()).view(TORCH_FP8[fmt]).to(torch.float32).numpy()
+    np.testing.assert_array_equal(dec.view(np.uint32), want.view(np.uint32), err_msg="decoded slice")
+    np.testing.assert_array_equal(wh.view(np.uint32), oracle.decode(oc, decs, enc).view(np.uint32))
+    # the product over the crafted slice
+    x = synth.activation(d_in, seed=8, dtype=torch.bfloat16)
+    y = bsq.bsq_gemv(cfg, codec, layer, x.to(gpu), y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    tabs = oracle.decoder_table(oc, decs)
+    w_ref = oracle.decode(oc, decs, enc, tables=tabs)
+    xf = oracle.to_f32(x)
+    check_product(y.cpu().numpy(), oracle.dense_product(w_ref, xf), gemv_kind(torch.bfloat16), cfg, enc, tabs,
+                  w_ref, xf, None, "gemv over the crafted slice", torch.float32)
