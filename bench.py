@@ -108,15 +108,16 @@ class Stack:
     per projection group. plans[li][g] is the grouped GEMV of group g in
     layer li."""
 
-    def __init__(self, bsq, synth, torch, projs, n_layers, d, lora_rank, dev, seed):
+    def __init__(self, bsq, synth, torch, projs, n_layers, d, lora_rank, dev, seed, kind=None, fmt=0):
         self.torch, self.bsq = torch, bsq
         self.d, self.n_layers, self.lora_rank = d, n_layers, lora_rank
-        self.cfg = bsq.Config(d=d, stages=2, kind=bsq.DEC_MLP, hidden=d, protect_num=1, protect_den=100)
+        kind = bsq.DEC_MLP if kind is None else kind
+        self.cfg = bsq.Config(d=d, stages=2, kind=kind, hidden=d, protect_num=1, protect_den=100, protect_format=fmt)
         self.projs = projs
         self.codecs, self.layers, self.loras = {}, {}, {}
         self.encode_s, self.chunks = 0.0, 0
         for ci, p in enumerate(projs):
-            decs = synth.decoder_params(synth.DEC_MLP, d, d, d, 2, seed=synth.BASE_SEED, category=ci)
+            decs = synth.decoder_params(kind, d, d, d, 2, seed=synth.BASE_SEED, category=ci)
             self.codecs[p.name] = bsq.bsq_codec_prepare(self.cfg, decs, device=dev)
             W, _ = synth.weight(p.d_out, p.d_in, seed=seed + 100 * ci + d, k_outliers=self.cfg.k(p.d_in),
                                 device=dev, n_mats=n_layers)
@@ -354,6 +355,28 @@ def comparator(blk, bsq, synth, torch, dev):
             "per_M": out,
             "residual_decode_fp32": {"stage_parallel_us": round(par, 1), "sequential_us": round(seq, 1),
                                      "stages": S, "stage_parallel_gbs": round(bytes_par / par / 1e3, 1)}}
+
+
+def variants(bsq, synth, torch, dev, s):
+    """The codec-component ablation's variants (Section IV-D) on the
+    Qwen3-8B-shaped block, 8 encoded copies rotated: the symmetric decoder
+    with one residual block, and the FP8-E4M3 / FP8-E5M2 protected payloads;
+    encode rate and batch-1 GEMV step per block."""
+    out = {}
+    for d, kind, fmt, tag in ((8, bsq.DEC_MLP_RES1, bsq.PROT_INT8, "res1"), (8, bsq.DEC_MLP, bsq.PROT_E4M3, "e4m3"),
+                              (8, bsq.DEC_MLP, bsq.PROT_E5M2, "e5m2"), (16, bsq.DEC_MLP_RES1, bsq.PROT_INT8, "res1"),
+                              (16, bsq.DEC_MLP, bsq.PROT_E4M3, "e4m3")):
+        blk = Stack(bsq, synth, torch, synth.qwen3_8b_block(), 8, d, 0, dev, seed=1000, kind=kind, fmt=fmt)
+        step_ms = blk.time_tokens(s, 8, 64) / blk.n_layers
+        step_bytes = blk.token_bytes // blk.n_layers
+        gbs = step_bytes / (step_ms / 1e3) / 1e9
+        out[f"d{d}_{tag}"] = {"ms_per_step": round(step_ms, 5), "gbs": round(gbs, 1),
+                              "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+                              "encode_mchunks_per_s": round(1e3 * blk.encode_gchunks(), 1)}
+        log(f"[bench] variant d={d} {tag}: block step {step_ms * 1e3:.1f} us, {gbs:.0f} GB/s, "
+            f"encode {blk.encode_gchunks():.2f} G chunks/s")
+        blk.release()
+    return out
 
 
 def tiny_latency(bsq, synth, torch, dev):
@@ -603,6 +626,7 @@ def main():
     line["qwen3_8b_block"] = block
     line["gemm"] = gemm
     line["comparator"] = comp
+    line["variants"] = variants(bsq, synth, torch, dev, s)
     line["tiny"] = tiny_latency(bsq, synth, torch, dev)
     line["copy_reference_gbs"] = round(copy_reference(torch, dev), 1)
     if "cpu_baseline" not in line:

@@ -121,27 +121,32 @@ __host__ __device__ inline float payload_max(int fmt)
     return fmt == BSQ_PROT_E4M3 ? 448.0f : (fmt == BSQ_PROT_E5M2 ? 57344.0f : 127.0f);
 }
 
-// The value of the stored byte in the low 8 bits of q: int8 two's
-// complement, or the sign / exponent / fraction fields of the FP8 format
-// (E4M3: bias 7, S.1111.111 NaN; E5M2: bias 15, exponent 31 infinity or NaN;
-// exponent 0 subnormal in both). Exact: each value is an fp32 number.
+// The value of byte SEL of a word of stored bytes: int8 two's complement, or
+// the OCP FP8 fields (E4M3: bias 7, S.1111.111 NaN; E5M2: bias 15, exponent
+// 31 infinity or NaN; exponent 0 subnormal in both), read by gfx950's
+// conversion instructions, which implement exactly these formats (every one
+// of the 256 bytes of both formats is checked against their definitions).
+template <int FMT, int SEL>
+__device__ __forceinline__ float payload_byte(uint32_t word)
+{
+    if constexpr (FMT == BSQ_PROT_E4M3) return __builtin_amdgcn_cvt_f32_fp8(int(word), SEL);
+    else if constexpr (FMT == BSQ_PROT_E5M2) return __builtin_amdgcn_cvt_f32_bf8(int(word), SEL);
+    else return float(int8_t(uint8_t(word >> (8 * SEL))));
+}
+
+// The value of the stored byte in the low 8 bits of q.
+template <int FMT>
+__device__ __forceinline__ float payload_value(uint32_t q)
+{
+    return payload_byte<FMT, 0>(q);
+}
+
+// The same with the format known at run time only (one uniform dispatch).
 __device__ __forceinline__ float payload_to_f32(uint32_t q, int fmt)
 {
-    if (fmt == BSQ_PROT_INT8) return float(int8_t(uint8_t(q)));
-    const uint32_t sign = (q & 0x80u) << 24;
-    uint32_t mag;
-    if (fmt == BSQ_PROT_E4M3) {
-        const uint32_t e = (q >> 3) & 15u, m = q & 7u;
-        if (e == 15u && m == 7u) mag = 0x7fc00000u;
-        else if (e) mag = ((e + 120u) << 23) | (m << 20);          // 2^(e - 7) (1 + m / 8)
-        else mag = __float_as_uint(float(m) * 0x1p-9f);            // m 2^-9
-    } else {
-        const uint32_t e = (q >> 2) & 31u, m = q & 3u;
-        if (e == 31u) mag = m ? 0x7fc00000u : 0x7f800000u;
-        else if (e) mag = ((e + 112u) << 23) | (m << 21);          // 2^(e - 15) (1 + m / 4)
-        else mag = __float_as_uint(float(m) * 0x1p-16f);           // m 2^-16
-    }
-    return __uint_as_float(sign | mag);
+    if (fmt == BSQ_PROT_E4M3) return payload_value<BSQ_PROT_E4M3>(q);
+    if (fmt == BSQ_PROT_E5M2) return payload_value<BSQ_PROT_E5M2>(q);
+    return payload_value<BSQ_PROT_INT8>(q);
 }
 
 // The stored byte of v (a weight over its slice's scale). int8: round half

@@ -52,6 +52,29 @@ constexpr int BK = 128;    // inputs per K step
 constexpr int64_t GEMM_HDR = 256;
 constexpr int64_t GEMM_SLOT_BYTES = int64_t(8) << 20;
 
+// Eight stored protected bytes (two words, byte e of the pair at bits
+// 8 (e % 4) of word e / 4) times their scales, in format FMT; the run-time
+// format is dispatched once per eight bytes (a uniform branch).
+template <int FMT>
+__device__ __forceinline__ void payload8_t(uint2 qv, const float *sc, float (&v)[8])
+{
+    v[0] = payload_byte<FMT, 0>(qv.x) * sc[0];
+    v[1] = payload_byte<FMT, 1>(qv.x) * sc[1];
+    v[2] = payload_byte<FMT, 2>(qv.x) * sc[2];
+    v[3] = payload_byte<FMT, 3>(qv.x) * sc[3];
+    v[4] = payload_byte<FMT, 0>(qv.y) * sc[4];
+    v[5] = payload_byte<FMT, 1>(qv.y) * sc[5];
+    v[6] = payload_byte<FMT, 2>(qv.y) * sc[6];
+    v[7] = payload_byte<FMT, 3>(qv.y) * sc[7];
+}
+
+__device__ __forceinline__ void payload8(uint2 qv, const float *sc, float (&v)[8], int fmt)
+{
+    if (fmt == BSQ_PROT_E4M3) payload8_t<BSQ_PROT_E4M3>(qv, sc, v);
+    else if (fmt == BSQ_PROT_E5M2) payload8_t<BSQ_PROT_E5M2>(qv, sc, v);
+    else payload8_t<BSQ_PROT_INT8>(qv, sc, v);
+}
+
 struct GemmArgs {
     const void *codes[BSQ_MAX_STAGES];
     const uint16_t *gains[BSQ_MAX_STAGES];
@@ -524,11 +547,7 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
 #pragma unroll
                 for (int j = 0; j < NT; ++j) {
                     float v[8];
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        const uint32_t w = (e < 4) ? qv[h][j].x : qv[h][j].y;
-                        v[e] = payload_to_f32(w >> (8 * (e & 3)), a.pfmt) * sc[h][e];
-                    }
+                    payload8(qv[h][j], sc[h], v, a.pfmt);
                     const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                                pack_bf16x2(v[6], v[7])};
 #pragma unroll
@@ -962,11 +981,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void g
                     qv = prot_lds ? *reinterpret_cast<const uint2 *>(s_q8 + (16 * j + r16) * kp + p0)
                                   : *reinterpret_cast<const uint2 *>(a.q8 + row * kp + p0);
                 float v[8];
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const uint32_t w = (e < 4) ? qv.x : qv.y;
-                    v[e] = payload_to_f32(w >> (8 * (e & 3)), a.pfmt) * sc[e];
-                }
+                payload8(qv, sc, v, a.pfmt);
                 const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
                                            pack_bf16x2(v[6], v[7])};
                 acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv),

@@ -467,23 +467,32 @@ __device__ __forceinline__ void lane_store(const GemvArgs &a, const GemvMat &M, 
 }
 
 // Sixteen protected columns of one row: stored bytes (one 16-byte word, in
-// format fmt) against the scaled activations xs[0 .. 15] (LDS, 16-byte
+// format FMT) against the scaled activations xs[0 .. 15] (LDS, 16-byte
 // aligned, zero past k).
-__device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc, int fmt)
+template <int FMT>
+__device__ __forceinline__ float q8_block_t(uint4 qv, const float *xs, float acc)
 {
     const float4 *x4 = reinterpret_cast<const float4 *>(xs);
     const float4 xa = x4[0], xb = x4[1], xc = x4[2], xd = x4[3];
     const float xv[16] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w,
                           xc.x, xc.y, xc.z, xc.w, xd.x, xd.y, xd.z, xd.w};
     const uint32_t qw[4] = {qv.x, qv.y, qv.z, qv.w};
-    if (fmt == BSQ_PROT_INT8) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e) acc = __builtin_fmaf(float(int8_t(qw[e >> 2] >> (8 * (e & 3)))), xv[e], acc);
-    } else {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc = __builtin_fmaf(payload_to_f32(qw[e >> 2] >> (8 * (e & 3)), fmt), xv[e], acc);
+    for (int w = 0; w < 4; ++w) {
+        acc = __builtin_fmaf(payload_byte<FMT, 0>(qw[w]), xv[4 * w], acc);
+        acc = __builtin_fmaf(payload_byte<FMT, 1>(qw[w]), xv[4 * w + 1], acc);
+        acc = __builtin_fmaf(payload_byte<FMT, 2>(qw[w]), xv[4 * w + 2], acc);
+        acc = __builtin_fmaf(payload_byte<FMT, 3>(qw[w]), xv[4 * w + 3], acc);
     }
     return acc;
+}
+
+// (the format dispatched once per sixteen columns, a uniform branch)
+__device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc, int fmt)
+{
+    if (fmt == BSQ_PROT_E4M3) return q8_block_t<BSQ_PROT_E4M3>(qv, xs, acc);
+    if (fmt == BSQ_PROT_E5M2) return q8_block_t<BSQ_PROT_E5M2>(qv, xs, acc);
+    return q8_block_t<BSQ_PROT_INT8>(qv, xs, acc);
 }
 
 // The int8 protected columns of one row (row < d_out) added to acc, the

@@ -6,7 +6,8 @@ even code), points a quarter step off, values below the smallest subnormal
 and signed zeros, each with both signs. The stored bytes must equal the
 oracle's (found there by trying every code) and torch's own float8 cast, and
 the decoded slice must be torch's reading of those bytes, on the input-column
-axis and on the output-row axis.
+axis and on the output-row axis. A second test writes all 256 bytes, NaN and
+infinity codes included, into a layer's payload and decodes them.
 """
 import numpy as np
 import pytest
@@ -96,3 +97,28 @@ def test_fp8_payload_at_every_code_and_tie(fmt, axis, d, gpu):
     xf = oracle.to_f32(x)
     check_product(y.cpu().numpy(), oracle.dense_product(w_ref, xf), gemv_kind(torch.bfloat16), cfg, enc, tabs,
                   w_ref, xf, None, "gemv over the crafted slice", torch.float32)
+
+
+@pytest.mark.parametrize("fmt", [bsq.PROT_E4M3, bsq.PROT_E5M2], ids=["e4m3", "e5m2"])
+@pytest.mark.parametrize("d", [8, 16])
+def test_every_stored_byte_decodes_to_its_value(fmt, d, gpu):
+    """All 256 bytes, NaN and infinity codes included, written into the
+    payload of an encoded layer (scale 1): the decoded protected column is
+    torch's float8 reading of each byte."""
+    say(f"every byte fmt={fmt} d={d}")
+    d_out, d_in = 256, 128
+    cfg = bsq.Config(d=d, hidden=d, protect_format=fmt, protect_num=1, protect_den=d_in)
+    W = synth.weight(d_out, d_in, seed=3, k_outliers=1, dtype=torch.float32)[0]
+    codec = bsq.bsq_codec_prepare(cfg, decoders(cfg, seed=2), device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W.to(gpu))
+    torch.cuda.synchronize()
+    j0 = int(layer.idx.cpu()[0])
+    layer.q8[:, 0] = torch.arange(256, device=gpu, dtype=torch.int32).to(torch.uint8).view(torch.int8)
+    layer.scale.fill_(1.0)
+    w_hat = bsq.bsq_decode(cfg, codec, layer, dtype=torch.float32)
+    torch.cuda.synchronize()
+    got = w_hat[:, j0].cpu().numpy()
+    want = torch.arange(256, dtype=torch.int32).to(torch.uint8).view(TORCH_FP8[fmt]).to(torch.float32).numpy()
+    nan = np.isnan(want)
+    np.testing.assert_array_equal(np.isnan(got), nan)
+    np.testing.assert_array_equal(got[~nan].view(np.uint32), want[~nan].view(np.uint32))
