@@ -38,6 +38,7 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 KIND_IDENTITY, KIND_LINEAR, KIND_MLP, KIND_MLP_RES1 = 0, 1, 2, 3
 FMT_INT8, FMT_E4M3, FMT_E5M2 = 0, 1, 2   # protected payload formats
+ENC_IDENTITY, ENC_LINEAR = 0, 1          # encoder E: z = r (b = d), or z = E r with E [b][d]
 ORC_OK, ORC_ERR_ARG, ORC_ERR_NONFINITE = 0, 1, 6
 PITCH_ALIGN = 16  # rows of the code/gain planes are padded to 16 chunks
 
@@ -86,15 +87,15 @@ def lib():
         L.orc_column_keys.argtypes = [P, I64, I64, P, P]
         L.orc_protect_select.argtypes = [P, I64, I64, P, I64, P, P]
         L.orc_q8.argtypes = [P, I64, I64, P, I64, I32, P, P]
-        L.orc_encode.argtypes = [I32, I32, P, P, I64, I64, P, I64, I64, I32, P, P, P, P, P, I32]
-        L.orc_decode.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, I32, P, I32]
-        L.orc_gemv_fused.argtypes = [I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, I32,
+        L.orc_encode.argtypes = [I32, I32, I32, P, P, P, I64, I64, P, I64, I64, I32, P, P, P, P, P, I32]
+        L.orc_decode.argtypes = [I32, I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, I32, P, I32]
+        L.orc_gemv_fused.argtypes = [I32, I32, I32, P, I64, I64, I64, P, P, P, P, P, I64, I32,
                                      P, I32, P, P, P, I32]
         L.orc_topk.argtypes = [P, I64, I64, P]
         L.orc_row_keys.argtypes = [P, I64, I64, P, P]
         L.orc_coupled_select.argtypes = [P, P, P, I64, I64, P, P, P, I64, P, P]
         L.orc_q8_rows.argtypes = [P, I64, I64, P, I64, I32, P, P]
-        L.orc_encode_set.argtypes = [I32, I32, P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P, I32]
+        L.orc_encode_set.argtypes = [I32, I32, I32, P, P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P, I32]
         L.orc_max_threads.restype = I32
         for f in ("orc_decoder_eval", "orc_decoder_table", "orc_protect_select",
                   "orc_encode", "orc_decode", "orc_gemv_fused", "orc_topk", "orc_coupled_select",
@@ -110,6 +111,20 @@ def _p(a: np.ndarray | None):
 
 def _ptr_array(arrs):
     return (ct.c_void_p * len(arrs))(*[a.ctypes.data for a in arrs])
+
+
+def _encoders(cfg, decs):
+    """With cfg.encoder == ENC_LINEAR: per stage the encoder E [b][d] (fp32,
+    the attribute E of the stage codec object) and the pointer array the C
+    oracle takes; with the identity encoder (b = d): None."""
+    if cfg.encoder == ENC_IDENTITY:
+        if cfg.b != cfg.d:
+            raise OracleError("b != d needs the linear encoder")
+        return None, None
+    es = [None if getattr(dec, "E", None) is None else _f32(dec.E) for dec in decs[:cfg.stages]]
+    if any(e is None or e.shape != (cfg.b, cfg.d) for e in es):
+        raise OracleError("every stage needs an encoder E of shape [b][d]")
+    return es, _ptr_array(es)
 
 
 def _check(rc: int, what: str):
@@ -131,6 +146,7 @@ class Config:
     protect_den: int = 100
     protect_axis: int = 0   # 0: input columns, 1: output rows
     protect_format: int = FMT_INT8  # payload of the protected slices
+    encoder: int = ENC_IDENTITY     # ENC_LINEAR: each stage codec carries E [b][d]
 
     def k(self, d_in: int) -> int:
         """k = ceil(rho * n), rho = num/den, in integer arithmetic, for n
@@ -300,14 +316,15 @@ def encode(cfg: Config, decs, w: np.ndarray, g=None, nthreads: int = 0,
     P = pitch(d_in, cfg.d)
     k = cfg.k(d_in)
     tables = tables or decoder_table(cfg, decs)
-    ctype = np.uint8 if cfg.d <= 8 else np.uint16
+    es, enc_arr = _encoders(cfg, decs)
+    ctype = np.uint8 if cfg.b <= 8 else np.uint16
     codes = [np.zeros((d_out, P), dtype=ctype) for _ in range(cfg.stages)]
     gains = [np.zeros((d_out, P), dtype=np.uint16) for _ in range(cfg.stages)]
     idx = np.zeros(max(k, 1), dtype=np.int32)
     q = np.zeros((d_out, max(k, 1)), dtype=np.int8)
     s = np.zeros(max(k, 1), dtype=np.float32)
     g = None if g is None else _f32(g)
-    rc = lib().orc_encode(cfg.d, cfg.stages, _ptr_array(tables), _p(w), d_out, d_in, _p(g), k, P,
+    rc = lib().orc_encode(cfg.d, cfg.b, cfg.stages, _ptr_array(tables), enc_arr, _p(w), d_out, d_in, _p(g), k, P,
                           cfg.protect_format, _ptr_array(codes), _ptr_array(gains), _p(idx), _p(q), _p(s), nthreads)
     _check(rc, "encode")
     return Encoded(codes, gains, idx[:k].copy(), np.ascontiguousarray(q[:, :k]), s[:k].copy(),
@@ -325,14 +342,15 @@ def encode_set(cfg: Config, decs, w: np.ndarray, idx, nthreads: int = 0, tables=
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     k = len(idx)
     tables = tables or decoder_table(cfg, decs)
-    ctype = np.uint8 if cfg.d <= 8 else np.uint16
+    es, enc_arr = _encoders(cfg, decs)
+    ctype = np.uint8 if cfg.b <= 8 else np.uint16
     codes = [np.zeros((d_out, P), dtype=ctype) for _ in range(cfg.stages)]
     gains = [np.zeros((d_out, P), dtype=np.uint16) for _ in range(cfg.stages)]
     qshape = (max(k, 1), d_in) if axis == 1 else (d_out, max(k, 1))
     q = np.zeros(qshape, dtype=np.int8)
     s = np.zeros(max(k, 1), dtype=np.float32)
     idx_arg = idx if k else np.zeros(1, np.int32)
-    rc = lib().orc_encode_set(cfg.d, cfg.stages, _ptr_array(tables), _p(w), d_out, d_in, axis,
+    rc = lib().orc_encode_set(cfg.d, cfg.b, cfg.stages, _ptr_array(tables), enc_arr, _p(w), d_out, d_in, axis,
                               _p(idx_arg), k, P, cfg.protect_format, _ptr_array(codes), _ptr_array(gains), _p(q), _p(s),
                               nthreads)
     _check(rc, "encode_set")
@@ -347,7 +365,7 @@ def decode(cfg: Config, decs, enc: Encoded, nthreads: int = 0, tables=None) -> n
     tables = tables or decoder_table(cfg, decs)
     w_hat = np.zeros((enc.d_out, enc.d_in), dtype=np.float32)
     if enc.axis == 1:
-        rc = lib().orc_decode(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
+        rc = lib().orc_decode(cfg.d, cfg.b, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
                               _ptr_array(enc.codes), _ptr_array(enc.gains), None, None, None, 0,
                               cfg.protect_format, _p(w_hat), nthreads)
         _check(rc, "decode")
@@ -358,7 +376,7 @@ def decode(cfg: Config, decs, enc: Encoded, nthreads: int = 0, tables=None) -> n
     idx = enc.idx if k else np.zeros(1, np.int32)
     q = enc.q8 if k else np.zeros((enc.d_out, 1), np.int8)
     s = enc.scale if k else np.zeros(1, np.float32)
-    rc = lib().orc_decode(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
+    rc = lib().orc_decode(cfg.d, cfg.b, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in, enc.pitch,
                           _ptr_array(enc.codes), _ptr_array(enc.gains), _p(idx),
                           _p(np.ascontiguousarray(q)), _p(s), k, cfg.protect_format, _p(w_hat), nthreads)
     _check(rc, "decode")
@@ -395,7 +413,7 @@ def gemv_fused(cfg: Config, decs, enc: Encoded, x, lora=None, nthreads: int = 0,
         A64 = np.ascontiguousarray(lora[0], dtype=np.float64)
         B64 = np.ascontiguousarray(lora[1], dtype=np.float64)
         rank = A64.shape[0]
-    rc = lib().orc_gemv_fused(cfg.d, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in,
+    rc = lib().orc_gemv_fused(cfg.d, cfg.b, cfg.stages, _ptr_array(tables), enc.d_out, enc.d_in,
                               enc.pitch, _ptr_array(enc.codes), _ptr_array(enc.gains), _p(idx),
                               _p(np.ascontiguousarray(q)), _p(s), k, cfg.protect_format, _p(x64), rank, _p(A64),
                               _p(B64), _p(y), nthreads)
@@ -427,6 +445,8 @@ def gemm(cfg: Config, decs, enc: Encoded, X, lora=None, nthreads: int = 0) -> np
 # Storage accounting, eq. real_size: S_tot = S_code + S_dec + S_8bit + S_LoRA + S_meta
 # --------------------------------------------------------------------------
 def decoder_param_count(cfg: Config) -> int:
+    """Parameters of one stage decoder (fp32 each); a learned linear encoder
+    adds b * d per stage (counted by sizes())."""
     if cfg.kind == KIND_MLP:
         return cfg.hidden * cfg.b + cfg.hidden + cfg.d * cfg.hidden + cfg.d
     if cfg.kind == KIND_MLP_RES1:
@@ -447,7 +467,7 @@ def sizes(cfg: Config, d_out: int, d_in: int, lora_rank: int = 0) -> dict:
     # d_in int8 values
     coded_rows = d_out - k if cfg.protect_axis == 1 else d_out
     s_code = cfg.stages * coded_rows * C * cfg.b / 8
-    s_dec = cfg.stages * decoder_param_count(cfg) * 4
+    s_dec = cfg.stages * (decoder_param_count(cfg) + (cfg.b * cfg.d if cfg.encoder == ENC_LINEAR else 0)) * 4
     s_8bit = k * d_in if cfg.protect_axis == 1 else d_out * k
     s_lora = 2 * lora_rank * (d_in + d_out)
     s_meta = cfg.stages * coded_rows * C * 2 + 4 * k + 4 * k

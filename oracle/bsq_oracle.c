@@ -425,10 +425,13 @@ void orc_q8_rows(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx
 /* Encode one matrix w [d_out][d_in] (fp32, row-major) into S stages.
  *
  * Chunk (i, c) is w[i, c*d : (c+1)*d] (reading: d consecutive inputs of one
- * output row). With the identity encoder z = r, and for ||z|| > 0 the sign
- * of u = z / ||z|| equals the sign of z, so the code of a chunk is
- *   bit_j = (z_j >= 0)                   (reading: +0 and -0 give 1)
- *   code  = sum_j bit_j << j             (element j -> bit j, LSB first)
+ * output row). The encoder gives z = E(r) in R^b (Section III-C): the
+ * identity (b = d, z = r), or a learned linear map z = E r with E [b][d]
+ * (enc[s] non-NULL; reading: the fmaf chain z_m = sum_j E[m][j] r_j from +0,
+ * j in order). For ||z|| > 0 the sign of u = z / ||z|| equals the sign of z,
+ * so the code of a chunk is
+ *   bit_m = (z_m >= 0)                   (reading: +0 and -0 give 1)
+ *   code  = sum_m bit_m << m             (element m -> bit m, LSB first)
  * Stage s (r^(0) = chunk with protected positions zeroed):
  *   y      = D_s(q)
  *   num    = fmaf chain over unprotected j of r_j * y_j, from +0
@@ -440,7 +443,7 @@ void orc_q8_rows(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx
  * never increases the reconstruction error, whatever its decoder).
  *
  * Outputs, each row padded to `pitch` chunks (padding: code 0, gain +0):
- *   codes[s]  uint8 (d <= 8) or uint16 (d > 8), [d_out][pitch]
+ *   codes[s]  uint8 (b <= 8) or uint16 (b > 8), [d_out][pitch]
  *   gains[s]  fp16 bits,                         [d_out][pitch]
  *   idx[k] ascending protected columns, q8[d_out][k], scale[k].
  *
@@ -448,7 +451,8 @@ void orc_q8_rows(const float *w, int64_t d_out, int64_t d_in, const int32_t *idx
 /* The per-chunk stages of every row i with skip[i] == 0 (skip may be NULL);
  * positions j with prot[j] != 0 are masked out of BSQ. Rows with skip[i] set
  * and padding chunks get code 0 and gain +0. */
-static void encode_rows(int d, int stages, const float *const *tables, const float *w, int64_t d_out,
+static void encode_rows(int d, int b, int stages, const float *const *tables, const float *const *enc,
+                        const float *w, int64_t d_out,
                         int64_t d_in, int64_t pitch, const unsigned char *prot, const unsigned char *skip,
                         void *const *codes, uint16_t *const *gains, int nthreads)
 {
@@ -464,7 +468,7 @@ static void encode_rows(int d, int stages, const float *const *tables, const flo
         for (int64_t c = 0; c < pitch; ++c) {
             if (c >= C || (skip && skip[i])) {
                 for (int s = 0; s < stages; ++s) {
-                    if (d <= 8) ((uint8_t *)codes[s])[i * pitch + c] = 0;
+                    if (b <= 8) ((uint8_t *)codes[s])[i * pitch + c] = 0;
                     else ((uint16_t *)codes[s])[i * pitch + c] = 0;
                     gains[s][i * pitch + c] = 0;
                 }
@@ -476,8 +480,18 @@ static void encode_rows(int d, int stages, const float *const *tables, const flo
             }
             for (int s = 0; s < stages; ++s) {
                 uint32_t code = 0;
-                for (int j = 0; j < d; ++j)
-                    if (r[j] >= 0.0f) code |= 1u << j;
+                if (enc && enc[s]) {
+                    /* learned linear encoder: z_m = sum_j E[m][j] r_j, an
+                     * fmaf chain from +0 in j order; bit m = (z_m >= 0) */
+                    for (int m = 0; m < b; ++m) {
+                        float z = 0.0f;
+                        for (int j = 0; j < d; ++j) z = fmaf(enc[s][m * d + j], r[j], z);
+                        if (z >= 0.0f) code |= 1u << m;
+                    }
+                } else {
+                    for (int j = 0; j < d; ++j)
+                        if (r[j] >= 0.0f) code |= 1u << j;
+                }
                 const float *y = tables[s] + (size_t)code * d;
                 float num = 0.0f, den = 0.0f;
                 for (int j = 0; j < d; ++j) {
@@ -493,7 +507,7 @@ static void encode_rows(int d, int stages, const float *const *tables, const flo
                     if (prot[c * d + j]) continue;
                     r[j] = fmaf(-a, y[j], r[j]);
                 }
-                if (d <= 8) ((uint8_t *)codes[s])[i * pitch + c] = (uint8_t)code;
+                if (b <= 8) ((uint8_t *)codes[s])[i * pitch + c] = (uint8_t)code;
                 else ((uint16_t *)codes[s])[i * pitch + c] = (uint16_t)code;
                 gains[s][i * pitch + c] = gh;
             }
@@ -501,13 +515,14 @@ static void encode_rows(int d, int stages, const float *const *tables, const flo
     }
 }
 
-int orc_encode(int d, int stages, const float *const *tables,
+int orc_encode(int d, int b, int stages, const float *const *tables, const float *const *enc,
                const float *w, int64_t d_out, int64_t d_in, const float *g,
                int64_t k, int64_t pitch, int fmt,
                void *const *codes, uint16_t *const *gains,
                int32_t *idx, uint8_t *q8, float *scale, int nthreads)
 {
     if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    if (b < 1 || b > MAX_CODE_BITS || (b != d && !enc)) return ORC_ERR_ARG;
     if (d_in % d != 0 || k < 0 || k > d_in) return ORC_ERR_ARG;
     int64_t C = d_in / d;
     if (pitch < C) return ORC_ERR_ARG;
@@ -523,7 +538,7 @@ int orc_encode(int d, int stages, const float *const *tables,
         orc_q8(w, d_out, d_in, idx, k, fmt, q8, scale);
         for (int64_t p = 0; p < k; ++p) prot[idx[p]] = 1;
     }
-    encode_rows(d, stages, tables, w, d_out, d_in, pitch, prot, NULL, codes, gains, nthreads);
+    encode_rows(d, b, stages, tables, enc, w, d_out, d_in, pitch, prot, NULL, codes, gains, nthreads);
     free(prot);
     return ORC_OK;
 }
@@ -539,13 +554,14 @@ int orc_encode(int d, int stages, const float *const *tables,
  *          keep code 0 and gain +0 in the planes.
  * This is how the coupled MLP set of eq. mlp_coupled_protection reaches the
  * three matrices: rows of gate and up, columns of down. */
-int orc_encode_set(int d, int stages, const float *const *tables,
+int orc_encode_set(int d, int b, int stages, const float *const *tables, const float *const *enc,
                    const float *w, int64_t d_out, int64_t d_in, int axis,
                    const int32_t *idx, int64_t k, int64_t pitch, int fmt,
                    void *const *codes, uint16_t *const *gains,
                    uint8_t *q8, float *scale, int nthreads)
 {
     if (d < 1 || d > MAX_CODE_BITS || stages < 1 || stages > MAX_STAGES) return ORC_ERR_ARG;
+    if (b < 1 || b > MAX_CODE_BITS || (b != d && !enc)) return ORC_ERR_ARG;
     if (axis != 0 && axis != 1) return ORC_ERR_ARG;
     int64_t n = axis ? d_out : d_in;
     if (d_in % d != 0 || k < 0 || k > n) return ORC_ERR_ARG;
@@ -564,7 +580,7 @@ int orc_encode_set(int d, int stages, const float *const *tables,
         orc_q8_rows(w, d_out, d_in, idx, k, fmt, q8, scale);
         for (int64_t p = 0; p < k; ++p) skip[idx[p]] = 1;
     }
-    encode_rows(d, stages, tables, w, d_out, d_in, pitch, prot, skip, codes, gains, nthreads);
+    encode_rows(d, b, stages, tables, enc, w, d_out, d_in, pitch, prot, skip, codes, gains, nthreads);
     free(prot);
     free(skip);
     return ORC_OK;
@@ -577,7 +593,7 @@ int orc_encode_set(int d, int stages, const float *const *tables,
 /* W_hat[i][j] = sum over stages of gain_s * D_s(code_s)[j], as an fmaf chain
  * over s from +0 (each stage decoded independently, then summed); protected
  * columns are then overwritten with value(q8) * scale (fp32 product). */
-int orc_decode(int d, int stages, const float *const *tables,
+int orc_decode(int d, int b, int stages, const float *const *tables,
                int64_t d_out, int64_t d_in, int64_t pitch,
                const void *const *codes, const uint16_t *const *gains,
                const int32_t *idx, const uint8_t *q8, const float *scale, int64_t k, int fmt,
@@ -595,7 +611,7 @@ int orc_decode(int d, int stages, const float *const *tables,
             for (int j = 0; j < d; ++j) {
                 float v = 0.0f;
                 for (int s = 0; s < stages; ++s) {
-                    uint32_t code = (d <= 8) ? ((const uint8_t *)codes[s])[i * pitch + c]
+                    uint32_t code = (b <= 8) ? ((const uint8_t *)codes[s])[i * pitch + c]
                                              : ((const uint16_t *)codes[s])[i * pitch + c];
                     float a = orc_f16_to_f32(gains[s][i * pitch + c]);
                     v = fmaf(a, tables[s][(size_t)code * d + j], v);
@@ -614,7 +630,7 @@ int orc_decode(int d, int stages, const float *const *tables,
 /*   + sum_p scale_p value(q8_ip) x_{idx_p} + sum_r B_ir (A x)_r              */
 /* x~ is x with the protected positions zeroed. This route never forms W_hat. */
 /* ------------------------------------------------------------------------ */
-int orc_gemv_fused(int d, int stages, const float *const *tables,
+int orc_gemv_fused(int d, int b, int stages, const float *const *tables,
                    int64_t d_out, int64_t d_in, int64_t pitch,
                    const void *const *codes, const uint16_t *const *gains,
                    const int32_t *idx, const uint8_t *q8, const float *scale, int64_t k, int fmt,
@@ -641,7 +657,7 @@ int orc_gemv_fused(int d, int stages, const float *const *tables,
         double acc = 0.0;
         for (int64_t c = 0; c < C; ++c) {
             for (int s = 0; s < stages; ++s) {
-                uint32_t code = (d <= 8) ? ((const uint8_t *)codes[s])[i * pitch + c]
+                uint32_t code = (b <= 8) ? ((const uint8_t *)codes[s])[i * pitch + c]
                                          : ((const uint16_t *)codes[s])[i * pitch + c];
                 double a = (double)orc_f16_to_f32(gains[s][i * pitch + c]);
                 const float *yv = tables[s] + (size_t)code * d;

@@ -88,6 +88,7 @@ class StageDecoder:
     MLP_RES1: the MLP's tensors plus the residual block's R [h, h], c [h]
     LINEAR:   W1 = M [d, b], b1 = beta [d]   (W2, b2 unused)
     IDENTITY: no parameters.
+    E [b, d]: the stage's linear encoder z = E r, when the codec has one.
     """
     W1: np.ndarray | None = None
     b1: np.ndarray | None = None
@@ -95,10 +96,14 @@ class StageDecoder:
     b2: np.ndarray | None = None
     R: np.ndarray | None = None
     c: np.ndarray | None = None
+    E: np.ndarray | None = None
 
 
 def decoder_params(kind: int, d: int, b: int, hidden: int, stages: int,
-                   seed: int = BASE_SEED, category: int = 0) -> list[StageDecoder]:
+                   seed: int = BASE_SEED, category: int = 0, encoder: bool = False) -> list[StageDecoder]:
+    """Seeded stage codecs; with encoder=True each also gets a linear encoder
+    E [b, d] ~ U(-1/sqrt(d), 1/sqrt(d)) (an untrained stand-in for the
+    learned one)."""
     out = []
     for s in range(stages):
         def draw(tensor: int, n: int, fan_in: int) -> np.ndarray:
@@ -121,6 +126,8 @@ def decoder_params(kind: int, d: int, b: int, hidden: int, stages: int,
             out.append(dec)
         else:
             raise ValueError(f"unknown decoder kind {kind}")
+        if encoder:
+            out[-1].E = draw(6, b * d, d).reshape(b, d)
     return out
 
 

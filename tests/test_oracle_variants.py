@@ -1,11 +1,15 @@
 """Pins of the oracle's codec variants from the paper's component ablation
 (Section IV-D, Table "BSQ codec components"): the symmetric decoder with one
-residual block, and the FP8-E4M3 / FP8-E5M2 formats of the protected path.
+residual block, the FP8-E4M3 / FP8-E5M2 formats of the protected path, and a
+linear encoder z = E r (Section III-C's E_phi), which also allows code
+lengths b other than the chunk length d (the b/d settings of Section III-D).
 
 Each pin checks the oracle against something other than itself: torch's own
 float8 conversions (a library routine), closed forms of the two formats,
 special cases of the residual block that reduce to the pinned decoder without
-one, and an fp64 numpy evaluation of the decoder written from its definition.
+one, an fp64 numpy evaluation of the decoder written from its definition,
+encoders whose codes have a closed form (identity, positive scaling,
+permutation, stacked and summed maps), and the signs of E r in fp64.
 """
 from __future__ import annotations
 
@@ -289,3 +293,153 @@ def test_res1_storage_counts_the_block():
     plain = Config(d=8, b=8, stages=2, kind=KIND_MLP, hidden=8)
     assert oracle.decoder_param_count(cfg) == oracle.decoder_param_count(plain) + 8 * 8 + 8
     assert oracle.sizes(cfg, 64, 64)["S_dec"] == 2 * 4 * oracle.decoder_param_count(cfg)
+
+
+# ---------------------------------------------------------------- linear encoder, b != d
+from oracle import ENC_LINEAR, KIND_LINEAR  # noqa: E402
+
+
+def _enc_cfg(d, b, stages=1, kind=KIND_MLP, h=None, **kw):
+    return Config(d=d, b=b, stages=stages, kind=kind, hidden=h or b, encoder=ENC_LINEAR, **kw)
+
+
+def _with_E(decs, Es):
+    out = []
+    for dec, E in zip(decs, Es):
+        nd = synth.StageDecoder(W1=dec.W1, b1=dec.b1, W2=dec.W2, b2=dec.b2)
+        nd.E = np.asarray(E, np.float32)
+        out.append(nd)
+    return out
+
+
+def _bits_of(codes, b):
+    c = np.asarray(codes).astype(np.int64)
+    return (c[..., None] >> np.arange(b)) & 1
+
+
+@pytest.mark.parametrize("d", [8, 16])
+def test_encoder_identity_and_positive_scaling_are_the_plain_encoder(d):
+    """E = I, and E = a positive diagonal (sign(E r) = sign(r)), reproduce the
+    identity-encoder encoding bit for bit: codes, gains, payload, every stage."""
+    plain_cfg = Config(d=d, b=d, stages=2, kind=KIND_MLP, hidden=d)
+    decs = synth.decoder_params(KIND_MLP, d, d, d, 2, seed=31)
+    r = _rng(900 + d)
+    w = r.normal(0, 0.02, (96, 512)).astype(np.float32)
+    w[:, [5, 300]] *= 10
+    want = oracle.encode(plain_cfg, decs, w)
+    scales = r.uniform(0.01, 50.0, d).astype(np.float32)
+    for E in (np.eye(d), np.diag(scales)):
+        got = oracle.encode(_enc_cfg(d, d, stages=2, h=d), _with_E(decs, [E, E]), w)
+        for s in range(2):
+            np.testing.assert_array_equal(got.codes[s], want.codes[s])
+            np.testing.assert_array_equal(got.gains[s], want.gains[s])
+        np.testing.assert_array_equal(got.q8, want.q8)
+
+
+def test_encoder_permutation_permutes_the_code_bits():
+    """E a permutation (b = d = 8, one stage): bit m of the code is bit
+    perm(m) of the identity encoder's code."""
+    d = 8
+    perm = np.array([3, 0, 7, 1, 6, 2, 5, 4])
+    decs = synth.decoder_params(KIND_MLP, d, d, d, 1, seed=32)
+    w = _rng(910).normal(0, 0.02, (64, 256)).astype(np.float32)
+    ident = oracle.encode(Config(d=d, b=d, stages=1, kind=KIND_MLP, hidden=d), decs, w)
+    got = oracle.encode(_enc_cfg(d, d), _with_E(decs, [np.eye(d)[perm]]), w)
+    np.testing.assert_array_equal(_bits_of(got.codes[0], d), _bits_of(ident.codes[0], d)[..., perm])
+
+
+@pytest.mark.parametrize("d,b", [(8, 16), (16, 8)])
+def test_encoder_stacked_and_summed_maps(d, b):
+    """b = 2d with E = [I; -I]: the high byte is the complement of the low
+    one, which is the identity code. b = d/2 with E summing pairs
+    (z_m = r_2m + r_2m+1, one rounding): bit m is the sign of that sum,
+    computed here in fp32 from the definition. No protected columns and no
+    zeros, so every z is nonzero."""
+    decs = synth.decoder_params(KIND_LINEAR, d, b, b, 1, seed=33)
+    w = _rng(920 + d).normal(0, 0.02, (64, 256)).astype(np.float32)
+    C = 256 // d
+    chunks = w.reshape(64, C, d)
+    if b == 2 * d:
+        E = np.vstack([np.eye(d), -np.eye(d)])
+        got = oracle.encode(_enc_cfg(d, b, kind=KIND_LINEAR, protect_num=0), _with_E(decs, [E]), w)
+        lo = (chunks >= 0).astype(np.int64)
+        want = (lo * (1 << np.arange(d))).sum(-1) | (((1 - lo) * (1 << np.arange(d, 2 * d))).sum(-1))
+    else:
+        E = np.zeros((b, d), np.float32)
+        E[np.arange(b), 2 * np.arange(b)] = 1
+        E[np.arange(b), 2 * np.arange(b) + 1] = 1
+        got = oracle.encode(_enc_cfg(d, b, kind=KIND_LINEAR, protect_num=0), _with_E(decs, [E]), w)
+        z = chunks[..., 0::2] + chunks[..., 1::2]          # fp32 sums, one rounding each
+        want = ((z >= 0).astype(np.int64) * (1 << np.arange(b))).sum(-1)
+    np.testing.assert_array_equal(got.codes[0][:, :C].astype(np.int64), want)
+
+
+@pytest.mark.parametrize("d,b", [(8, 16), (16, 8), (8, 8)])
+def test_random_encoder_codes_are_the_signs_of_E_r(d, b):
+    """A random E: every code bit is the sign of z = E r evaluated in fp64
+    wherever |z| exceeds the fmaf chain's rounding bound (the sphere map's
+    sign rule of Section III-C applied to the encoder output), at both
+    stages, with the stage-2 residual recomputed from the stage-1 code and
+    gain by the definition."""
+    cfg = _enc_cfg(d, b, stages=2, h=b, protect_num=0)
+    decs = synth.decoder_params(KIND_MLP, d, b, b, 2, seed=34, encoder=True)
+    w = _rng(930 + d + b).normal(0, 0.02, (48, 128)).astype(np.float32)
+    tabs = oracle.decoder_table(cfg, decs)
+    enc = oracle.encode(cfg, decs, w, tables=tabs)
+    C = 128 // d
+    r = w.reshape(48, C, d).astype(np.float32)
+    checked = 0
+    for s in range(2):
+        E = decs[s].E.astype(np.float64)
+        z = r.astype(np.float64) @ E.T
+        bound = (d + 1) * 2.0 ** -24 * (np.abs(r).astype(np.float64) @ np.abs(E).T)
+        sure = np.abs(z) > bound
+        bits = _bits_of(enc.codes[s][:, :C], b)
+        assert np.all(bits[sure] == (z[sure] >= 0))
+        checked += int(sure.sum())
+        # next stage's target: r - a y with the stage's code and gain (fmaf per element)
+        codes = enc.codes[s][:, :C].astype(np.int64)
+        a = oracle.f16_bits_to_f32(enc.gains[s][:, :C]).astype(np.float32)
+        y = tabs[s][codes]
+        r = (r.astype(np.float64) - a[..., None].astype(np.float64) * y.astype(np.float64)).astype(np.float32)
+    assert checked > 0.99 * 2 * 48 * C * b
+
+
+@pytest.mark.parametrize("d,b", [(8, 16), (16, 8)])
+def test_b_ne_d_routes_agree_and_residual_never_increases(d, b):
+    """b != d: the decode assembly and the two product routes agree, and each
+    stage's least-squares gain keeps the reconstruction error from growing
+    (whatever the encoder picked); code planes are 8-bit for b = 8 and 16-bit
+    for b = 16; sizes count b bits per chunk and stage and the encoder."""
+    cfg = _enc_cfg(d, b, stages=2, h=b, protect_num=1, protect_den=32)
+    decs = synth.decoder_params(KIND_MLP, d, b, b, 2, seed=35, encoder=True)
+    r = _rng(940 + d)
+    w = r.normal(0, 0.02, (80, 512)).astype(np.float32)
+    w[:, [17, 400]] *= 10
+    enc = oracle.encode(cfg, decs, w)
+    assert enc.codes[0].dtype == (np.uint8 if b == 8 else np.uint16)
+    x = r.normal(0, 1, 512).astype(np.float32)
+    y_dense = oracle.gemv(cfg, decs, enc, x)
+    y_fused = oracle.gemv_fused(cfg, decs, enc, x)
+    assert np.max(np.abs(y_dense - y_fused)) <= 1e-6 * np.sqrt(np.mean(y_dense ** 2))
+    one = _enc_cfg(d, b, stages=1, h=b, protect_num=1, protect_den=32)
+    e1 = oracle.encode(one, decs, w)
+    keep = np.ones(512, bool)
+    keep[enc.idx] = False
+    err0 = float(np.sum(w[:, keep].astype(np.float64) ** 2))
+    err1 = float(np.sum((oracle.decode(one, decs, e1) - w)[:, keep].astype(np.float64) ** 2))
+    err2 = float(np.sum((oracle.decode(cfg, decs, enc) - w)[:, keep].astype(np.float64) ** 2))
+    assert err1 <= err0 * (1 + 1e-6) and err2 <= err1 * (1 + 1e-6)
+    sz = oracle.sizes(cfg, 80, 512)
+    assert sz["S_code"] == 2 * 80 * (512 // d) * b / 8
+    assert sz["S_dec"] == 2 * 4 * (oracle.decoder_param_count(cfg) + b * d)
+    assert sz["bpw_nominal"] == 2 * b / d
+
+
+def test_encoder_required_for_b_ne_d():
+    decs = synth.decoder_params(KIND_MLP, 8, 16, 16, 1, seed=36)
+    w = np.ones((8, 64), np.float32)
+    with pytest.raises(oracle.OracleError):
+        oracle.encode(Config(d=8, b=16, stages=1, kind=KIND_MLP, hidden=16), decs, w)
+    with pytest.raises(oracle.OracleError):
+        oracle.encode(_enc_cfg(8, 16), decs, w)       # encoder config but no E
