@@ -108,16 +108,20 @@ class Stack:
     per projection group. plans[li][g] is the grouped GEMV of group g in
     layer li."""
 
-    def __init__(self, bsq, synth, torch, projs, n_layers, d, lora_rank, dev, seed, kind=None, fmt=0):
+    def __init__(self, bsq, synth, torch, projs, n_layers, d, lora_rank, dev, seed, kind=None, fmt=0, b=None):
+        """b: code bits per chunk other than d, with a (seeded, untrained)
+        linear encoder per stage."""
         self.torch, self.bsq = torch, bsq
         self.d, self.n_layers, self.lora_rank = d, n_layers, lora_rank
         kind = bsq.DEC_MLP if kind is None else kind
-        self.cfg = bsq.Config(d=d, stages=2, kind=kind, hidden=d, protect_num=1, protect_den=100, protect_format=fmt)
+        b = b or d
+        self.cfg = bsq.Config(d=d, stages=2, kind=kind, hidden=b, protect_num=1, protect_den=100, protect_format=fmt,
+                              codebook_bits=b, encoder=bsq.ENC_LINEAR if b != d else bsq.ENC_IDENTITY)
         self.projs = projs
         self.codecs, self.layers, self.loras = {}, {}, {}
         self.encode_s, self.chunks = 0.0, 0
         for ci, p in enumerate(projs):
-            decs = synth.decoder_params(kind, d, d, d, 2, seed=synth.BASE_SEED, category=ci)
+            decs = synth.decoder_params(kind, d, b, b, 2, seed=synth.BASE_SEED, category=ci, encoder=(b != d))
             self.codecs[p.name] = bsq.bsq_codec_prepare(self.cfg, decs, device=dev)
             W, _ = synth.weight(p.d_out, p.d_in, seed=seed + 100 * ci + d, k_outliers=self.cfg.k(p.d_in),
                                 device=dev, n_mats=n_layers)
@@ -360,13 +364,19 @@ def comparator(blk, bsq, synth, torch, dev):
 def variants(bsq, synth, torch, dev, s):
     """The codec-component ablation's variants (Section IV-D) on the
     Qwen3-8B-shaped block, 8 encoded copies rotated: the symmetric decoder
-    with one residual block, and the FP8-E4M3 / FP8-E5M2 protected payloads;
-    encode rate and batch-1 GEMV step per block."""
+    with one residual block, the FP8-E4M3 / FP8-E5M2 protected payloads, and
+    code lengths b other than d with a linear encoder (b/d = 2 and 1/2 bits
+    per weight and stage, Section III-D); encode rate and batch-1 GEMV step
+    per block."""
     out = {}
-    for d, kind, fmt, tag in ((8, bsq.DEC_MLP_RES1, bsq.PROT_INT8, "res1"), (8, bsq.DEC_MLP, bsq.PROT_E4M3, "e4m3"),
-                              (8, bsq.DEC_MLP, bsq.PROT_E5M2, "e5m2"), (16, bsq.DEC_MLP_RES1, bsq.PROT_INT8, "res1"),
-                              (16, bsq.DEC_MLP, bsq.PROT_E4M3, "e4m3")):
-        blk = Stack(bsq, synth, torch, synth.qwen3_8b_block(), 8, d, 0, dev, seed=1000, kind=kind, fmt=fmt)
+    for d, kind, fmt, b, tag in ((8, bsq.DEC_MLP_RES1, bsq.PROT_INT8, 8, "res1"),
+                                 (8, bsq.DEC_MLP, bsq.PROT_E4M3, 8, "e4m3"),
+                                 (8, bsq.DEC_MLP, bsq.PROT_E5M2, 8, "e5m2"),
+                                 (16, bsq.DEC_MLP_RES1, bsq.PROT_INT8, 16, "res1"),
+                                 (16, bsq.DEC_MLP, bsq.PROT_E4M3, 16, "e4m3"),
+                                 (8, bsq.DEC_MLP, bsq.PROT_INT8, 16, "b16_linear_encoder"),
+                                 (16, bsq.DEC_MLP, bsq.PROT_INT8, 8, "b8_linear_encoder")):
+        blk = Stack(bsq, synth, torch, synth.qwen3_8b_block(), 8, d, 0, dev, seed=1000, kind=kind, fmt=fmt, b=b)
         step_ms = blk.time_tokens(s, 8, 64) / blk.n_layers
         step_bytes = blk.token_bytes // blk.n_layers
         gbs = step_bytes / (step_ms / 1e3) / 1e9

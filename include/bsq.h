@@ -28,9 +28,10 @@
  *   element (i, c) is at ((i/64 * pitch/16 + c/16) * 64 + i%64) * 16 + c%16
  * i.e. [ceil(d_out/64)][pitch/16][64][16], so that 64 rows x 16 chunks are one
  * contiguous 1 KiB (d = 8) or 2 KiB (d = 16) code tile and 2 KiB gain tile.
- *   codes[s]   uint8 (d = 8) or uint16 little-endian (d = 16), tiled:
- *              bit j of a code is 1 iff element j of the stage target is >= 0
- *              (+0 and -0 give 1), element j -> bit j (LSB first);
+ *   codes[s]   uint8 (b = 8) or uint16 little-endian (b = 16), tiled:
+ *              bit m of a code is 1 iff element m of the encoder output z
+ *              is >= 0 (+0 and -0 give 1), element m -> bit m (LSB first);
+ *              z is the stage target itself with the identity encoder;
  *   gains[s]   fp16 bits, tiled: per-chunk least-squares gain of
  *              stage s (round to nearest even, finite overflow saturated);
  *   prot_idx   int32 [k], the protected input columns in ascending order;
@@ -69,7 +70,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 6
+#define BSQ_ABI_VERSION 7
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -137,9 +138,19 @@ typedef enum {
  * finite value store it. */
 typedef enum { BSQ_PROT_INT8 = 0, BSQ_PROT_E4M3 = 1, BSQ_PROT_E5M2 = 2 } bsq_prot_format;
 
+/* The encoder E_phi of Section III-C, which maps a chunk (or a stage's
+ * residual target) r in R^d to the latent z in R^b whose signs are the code:
+ *   IDENTITY: z = r (requires b = d);
+ *   LINEAR:   z = E r with a learned E [b][d] per stage; z_m is the fp32
+ *             fmaf chain sum_j E[m][j] r_j from +0, j in order.
+ * With the linear encoder b may differ from d (codebook_bits and
+ * codebook_dim of Section III-A, e.g. the b/d = 2 settings of Section
+ * III-D). */
+typedef enum { BSQ_ENC_IDENTITY = 0, BSQ_ENC_LINEAR = 1 } bsq_enc_kind;
+
 typedef struct {
     int32_t d;           /* chunk length: 8 or 16 (Section III-A, codebook_dim) */
-    int32_t b;           /* code bits per stage (codebook_bits); must equal d */
+    int32_t b;           /* code bits per stage: 8 or 16 (codebook_bits); b = d unless the encoder is LINEAR */
     int32_t stages;      /* residual stages S, 1..4 (Section III-D; default 2) */
     int32_t dec_kind;    /* bsq_dec_kind */
     int32_t hidden;      /* hidden width h of the symmetric decoders, 1..64; ignored for other kinds */
@@ -148,9 +159,11 @@ typedef struct {
                          /*   channels of the protected axis (d_in for columns, d_out for rows) */
     int32_t protect_axis; /* 0: protected input columns; 1: protected output rows */
     int32_t protect_format; /* bsq_prot_format of the protected payload */
+    int32_t encoder;        /* bsq_enc_kind */
 } bsq_config;
 
-/* Parameters of one stage's decoder, fp32, row-major, device pointers.
+/* Parameters of one stage's codec, fp32, row-major, device pointers: the
+ * encoder E [b][d] (LINEAR encoder only, else unused) and the decoder.
  *   MLP:      W1 [h][b], b1 [h], W2 [d][h], b2 [d];
  *             y = W2 relu(W1 q + b1) + b2, relu(a) = a > 0 ? a : +0
  *   MLP_RES1: the MLP's tensors and R [h][h], c [h];
@@ -167,6 +180,7 @@ typedef struct {
     const float *b2;
     const float *R;
     const float *c;
+    const float *E;
 } bsq_decoder;
 
 /* One encoded matrix (or a stack of n_mats of one shape), device pointers.
@@ -196,8 +210,10 @@ typedef struct {
 
 /* Storage accounting of eq. real_size for one matrix:
  * S_tot = S_code + S_dec + S_8bit + S_LoRA + S_meta (bytes). S_dec counts the
- * stage decoders once (a model counts them once per category, because every
- * layer of a category shares them). Buffer sizes include the row padding. */
+ * stage decoders (and a linear encoder's b d parameters) once (a model counts
+ * them once per category, because every layer of a category shares them).
+ * Buffer sizes include the row padding; a code plane holds b / 8 bytes per
+ * chunk. */
 typedef struct {
     int64_t pitch;
     int64_t k;
@@ -377,7 +393,10 @@ bsq_status bsq_decode_stage(const bsq_config *cfg, const void *codec, const bsq_
  *           BSQ_DEVERR_*) are ORed into it; without it those conditions
  *           still give NaN outputs and a poisoned workspace
  * bf16 x uses bf16 decoded values with fp32 accumulation; fp32 x uses the
- * fp32 decoder table and fp32 arithmetic throughout. With protect_axis = 1
+ * fp32 decoder table and fp32 arithmetic throughout, and so does every
+ * configuration with b != d (one wave per row over the 2^b-entry fp32
+ * table; bsq_gemm likewise, with fp32 FMA over LDS tiles of decoded
+ * weights instead of MFMA). With protect_axis = 1
  * the coded rows come from the streaming kernels and each protected row is
  * written afterwards as scale_p <q8[p, :], x> + B[row] (A x), one wave per
  * row (same stream).

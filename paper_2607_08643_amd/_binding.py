@@ -29,6 +29,7 @@ BSQ_ERR_BUFFER_TOO_SMALL, BSQ_ERR_NONFINITE, BSQ_ERR_DEVICE, BSQ_ERR_UNSUPPORTED
 BSQ_F32, BSQ_BF16 = 0, 1
 DEC_IDENTITY, DEC_LINEAR, DEC_MLP, DEC_MLP_RES1 = 0, 1, 2, 3
 PROT_INT8, PROT_E4M3, PROT_E5M2 = 0, 1, 2
+ENC_IDENTITY, ENC_LINEAR = 0, 1
 OP_ENCODE, OP_GEMV, OP_GEMM, OP_SELECT = 0, 1, 2, 3
 DEVERR_NONFINITE, DEVERR_BAD_SET, DEVERR_TIMEOUT, DEVERR_POISONED = 1, 2, 4, 8
 
@@ -43,12 +44,12 @@ class BsqError(RuntimeError):
 class bsq_config(ct.Structure):
     _fields_ = [("d", ct.c_int32), ("b", ct.c_int32), ("stages", ct.c_int32), ("dec_kind", ct.c_int32),
                 ("hidden", ct.c_int32), ("protect_num", ct.c_int32), ("protect_den", ct.c_int32),
-                ("protect_axis", ct.c_int32), ("protect_format", ct.c_int32)]
+                ("protect_axis", ct.c_int32), ("protect_format", ct.c_int32), ("encoder", ct.c_int32)]
 
 
 class bsq_decoder(ct.Structure):
     _fields_ = [("W1", ct.c_void_p), ("b1", ct.c_void_p), ("W2", ct.c_void_p), ("b2", ct.c_void_p),
-                ("R", ct.c_void_p), ("c", ct.c_void_p)]
+                ("R", ct.c_void_p), ("c", ct.c_void_p), ("E", ct.c_void_p)]
 
 
 class bsq_layer(ct.Structure):
@@ -79,7 +80,7 @@ EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes
            "bsq_debug_set_wait_limit", "bsq_decode_stage", "bsq_gemv_noalloc")
 
 # struct layouts above follow this version of include/bsq.h
-ABI_VERSION = 6
+ABI_VERSION = 7
 
 _lib = None
 
@@ -162,14 +163,16 @@ class Config:
     protect_den: int = 100
     protect_axis: int = 0   # 0: protected input columns, 1: protected output rows
     protect_format: int = PROT_INT8   # payload of the protected slices: int8, FP8-E4M3 or FP8-E5M2
+    encoder: int = ENC_IDENTITY       # ENC_LINEAR: each stage codec carries E [b, d]
+    codebook_bits: int = 0            # b; 0 means b = d
 
     @property
     def b(self) -> int:
-        return self.d
+        return self.codebook_bits or self.d
 
     def c(self) -> bsq_config:
         return bsq_config(self.d, self.b, self.stages, self.kind, self.hidden, self.protect_num,
-                          self.protect_den, self.protect_axis, self.protect_format)
+                          self.protect_den, self.protect_axis, self.protect_format, self.encoder)
 
     def k(self, n: int) -> int:
         """ceil(rho * n): protected channels among n."""
@@ -243,7 +246,7 @@ def bsq_codec_prepare(cfg: Config, decoders, device="cuda", stream=None) -> Code
     for s in range(cfg.stages):
         dec = decoders[s] if decoders is not None else None
         ts = []
-        for name in ("W1", "b1", "W2", "b2", "R", "c"):
+        for name in ("W1", "b1", "W2", "b2", "R", "c", "E"):
             v = getattr(dec, name, None) if dec is not None else None
             if v is None:
                 ts.append(None)
@@ -336,7 +339,7 @@ def layer_empty(cfg: Config, d_out: int, d_in: int, n_mats: int = 1, device="cud
     the protected payload (one byte per element) as [n_mats][d_out][roundup(k, 16)] (protected rows:
     [n_mats][k][roundup(d_in, 16)], and no bitmap)."""
     P, k = cfg.pitch(d_in), cfg.k_for(d_out, d_in)
-    ct_ = torch.uint8 if cfg.d <= 8 else torch.int16
+    ct_ = torch.uint8 if cfg.b <= 8 else torch.int16
     tiles = ((d_out + 63) // 64, P // 16, 64, 16)
     shape = ((n_mats,) + tiles) if n_mats > 1 else tiles
     codes = [torch.empty(shape, dtype=ct_, device=device) for _ in range(cfg.stages)]

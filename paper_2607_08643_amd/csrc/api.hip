@@ -61,8 +61,11 @@ bsq_status check_cfg(const bsq_config *c)
     if (c->protect_format < BSQ_PROT_INT8 || c->protect_format > BSQ_PROT_E5M2) return BSQ_ERR_ARG;
     if (c->protect_num < 0 || c->protect_den < 1 || c->protect_num > c->protect_den) return BSQ_ERR_ARG;
     if (c->protect_axis != 0 && c->protect_axis != 1) return BSQ_ERR_ARG;
+    if (c->encoder != BSQ_ENC_IDENTITY && c->encoder != BSQ_ENC_LINEAR) return BSQ_ERR_ARG;
     if (c->d != 8 && c->d != 16) return BSQ_ERR_UNSUPPORTED;
-    if (c->b != c->d) return BSQ_ERR_UNSUPPORTED;
+    if (c->b != 8 && c->b != 16) return BSQ_ERR_UNSUPPORTED;
+    // b != d needs an encoder R^d -> R^b; the identity decoder needs b = d
+    if (c->b != c->d && (c->encoder == BSQ_ENC_IDENTITY || c->dec_kind == BSQ_DEC_IDENTITY)) return BSQ_ERR_ARG;
     return BSQ_OK;
 }
 
@@ -171,7 +174,7 @@ bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, i
     // protected rows are not BSQ-coded: their all-zero plane rows are layout,
     // not payload
     const int64_t coded_rows = rows ? d_out - k : d_out;
-    const int64_t code_bytes = (c.d <= 8) ? 1 : 2;
+    const int64_t code_bytes = (c.b <= 8) ? 1 : 2;
     out->pitch = P;
     out->k = k;
     out->chunks = d_out * C;
@@ -184,8 +187,10 @@ bsq_status bsq_layer_sizes(const bsq_config *cfg, int64_t d_out, int64_t d_in, i
     int64_t dec_params = 0;
     if (c.dec_kind == BSQ_DEC_MLP || c.dec_kind == BSQ_DEC_MLP_RES1)
         dec_params = int64_t(c.hidden) * c.b + c.hidden + int64_t(c.d) * c.hidden + c.d;
+    else if (c.dec_kind == BSQ_DEC_LINEAR)
+        dec_params = int64_t(c.d) * c.b + c.d;
     if (c.dec_kind == BSQ_DEC_MLP_RES1) dec_params += int64_t(c.hidden) * c.hidden + c.hidden;
-    else if (c.dec_kind == BSQ_DEC_LINEAR) dec_params = int64_t(c.d) * c.b + c.d;
+    if (c.encoder == BSQ_ENC_LINEAR) dec_params += int64_t(c.b) * c.d;
     out->S_code = double(c.stages) * double(coded_rows) * double(C) * double(c.b) / 8.0;
     out->S_dec = double(c.stages) * double(dec_params) * 4.0;
     out->S_8bit = rows ? double(k) * double(d_in) : double(d_out) * double(k);
@@ -248,6 +253,11 @@ bsq_status bsq_codec_prepare(const bsq_config *cfg, const bsq_decoder *dec, void
                 return BSQ_ERR_ARG;
             if (cfg->dec_kind == BSQ_DEC_MLP_RES1 && (!dec[i].R || !dec[i].c)) return BSQ_ERR_ARG;
         }
+    }
+    if (cfg->encoder == BSQ_ENC_LINEAR) {
+        if (!dec) return BSQ_ERR_ARG;
+        for (int i = 0; i < cfg->stages; ++i)
+            if (!dec[i].E) return BSQ_ERR_ARG;
     }
     bsq_decoder none[BSQ_MAX_STAGES] = {};
     return from_hip(launch_codec_tables(*cfg, dec ? dec : none, codec, static_cast<hipStream_t>(stream)));
@@ -394,7 +404,7 @@ bsq_status check_gemv(const bsq_config *cfg, int32_t n, const void *const *codec
     // the d = 16 streaming kernel (decoders other than the width-16 symmetric
     // one) holds one 128-input segment per thread of a 512-thread block
     const bool split16 = codec_has_split(*cfg) && cfg->hidden == 16;
-    if (x_dtype == BSQ_BF16 && cfg->d == 16 && !split16 && layers[0].pitch * cfg->d / 128 > 512)
+    if (x_dtype == BSQ_BF16 && cfg->d == 16 && cfg->b == 16 && !split16 && layers[0].pitch * cfg->d / 128 > 512)
         return BSQ_ERR_UNSUPPORTED;
     if (x_dtype == BSQ_BF16 && !row_axis(*cfg) && layers[0].k > 4096) return BSQ_ERR_UNSUPPORTED;
     int64_t max_d_out = 0;

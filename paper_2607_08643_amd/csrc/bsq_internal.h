@@ -16,6 +16,7 @@ namespace bsq {
 // fp16 table [2^b][d] (rounded to nearest even, consumed by the GEMM's decode
 // through mixed-precision fma).
 //
+// The table has 2^b entries of d values (b = d with the identity encoder).
 // The symmetric decoder at d = b = 16 also gets, per stage, its hidden
 // pre-activation split by code byte: fp16 [2][h/8][256][8], half 0 holding
 // b1 + W1[:, 0:8] q(v) and half 1 W1[:, 8:16] q(v) for every byte v (so the
@@ -50,9 +51,15 @@ inline size_t codec_w2_offset(const bsq_config &c, int s)
     return codec_split_offset(c, s) + size_t(2) * 256 * c.hidden * 2;
 }
 inline size_t codec_b2_offset(const bsq_config &c, int s) { return codec_w2_offset(c, s) + size_t(c.d) * c.hidden * 4; }
+// then, with a linear encoder, a copy of each stage's E [b][d] (fp32)
+inline size_t codec_enc_offset(const bsq_config &c, int s)
+{
+    return size_t(c.stages) * codec_entries(c) * 8 + size_t(c.stages) * codec_split_stage_bytes(c) +
+           size_t(s) * c.b * c.d * 4;
+}
 inline size_t codec_total_bytes(const bsq_config &c)
 {
-    return size_t(c.stages) * codec_entries(c) * 8 + size_t(c.stages) * codec_split_stage_bytes(c);
+    return codec_enc_offset(c, c.encoder == BSQ_ENC_LINEAR ? c.stages : 0);
 }
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }

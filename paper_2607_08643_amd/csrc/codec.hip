@@ -28,21 +28,22 @@ struct TableArgs {
     int hidden;
 };
 
-template <int D>
+// D outputs per code, B code bits (B = D unless the codec has a linear encoder)
+template <int D, int B>
 __global__ __launch_bounds__(256) void codec_table_kernel(TableArgs a)
 {
     const int s = blockIdx.y;
     const uint32_t code = blockIdx.x * blockDim.x + threadIdx.x;
-    if (code >= (1u << D)) return;
+    if (code >= (1u << B)) return;
 
-    float q[D];
+    float q[B];
 #pragma unroll
-    for (int j = 0; j < D; ++j) q[j] = ((code >> j) & 1u) ? a.cscale : -a.cscale;
+    for (int j = 0; j < B; ++j) q[j] = ((code >> j) & 1u) ? a.cscale : -a.cscale;
 
     float y[D];
-    if (a.kind == BSQ_DEC_IDENTITY) {
+    if (a.kind == BSQ_DEC_IDENTITY) {  // (B = D)
 #pragma unroll
-        for (int j = 0; j < D; ++j) y[j] = q[j];
+        for (int j = 0; j < D; ++j) y[j] = q[j % B];
     } else if (a.kind == BSQ_DEC_LINEAR) {
         const float *M = a.W1[s];
         const float *beta = a.b1[s];
@@ -50,7 +51,7 @@ __global__ __launch_bounds__(256) void codec_table_kernel(TableArgs a)
         for (int m = 0; m < D; ++m) {
             float acc = beta[m];
 #pragma unroll
-            for (int j = 0; j < D; ++j) acc = __builtin_fmaf(M[m * D + j], q[j], acc);
+            for (int j = 0; j < B; ++j) acc = __builtin_fmaf(M[m * B + j], q[j], acc);
             y[m] = acc;
         }
     } else {
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(256) void codec_table_kernel(TableArgs a)
         for (int k = 0; k < h; ++k) {
             float acc = b1[k];
 #pragma unroll
-            for (int j = 0; j < D; ++j) acc = __builtin_fmaf(W1[k * D + j], q[j], acc);
+            for (int j = 0; j < B; ++j) acc = __builtin_fmaf(W1[k * B + j], q[j], acc);
             act[k] = (acc > 0.0f) ? acc : 0.0f;
         }
         if (a.kind == BSQ_DEC_MLP_RES1) {
@@ -155,10 +156,14 @@ hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, vo
     a.hidden = cfg.hidden;
     const uint32_t ncodes = 1u << cfg.b;
     dim3 grid((ncodes + 255) / 256, cfg.stages);
-    if (cfg.d == 8)
-        hipLaunchKernelGGL(codec_table_kernel<8>, grid, dim3(256), 0, st, a);
+    if (cfg.d == 8 && cfg.b == 8)
+        hipLaunchKernelGGL((codec_table_kernel<8, 8>), grid, dim3(256), 0, st, a);
+    else if (cfg.d == 16 && cfg.b == 16)
+        hipLaunchKernelGGL((codec_table_kernel<16, 16>), grid, dim3(256), 0, st, a);
+    else if (cfg.d == 8)
+        hipLaunchKernelGGL((codec_table_kernel<8, 16>), grid, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL(codec_table_kernel<16>, grid, dim3(256), 0, st, a);
+        hipLaunchKernelGGL((codec_table_kernel<16, 8>), grid, dim3(256), 0, st, a);
     if (codec_has_split(cfg)) {
         SplitArgs sa{};
         for (int s = 0; s < cfg.stages; ++s) {
@@ -174,7 +179,15 @@ hipError_t launch_codec_tables(const bsq_config &cfg, const bsq_decoder *dec, vo
         sa.hidden = cfg.hidden;
         hipLaunchKernelGGL(codec_split_kernel, dim3(unsigned(cfg.stages)), dim3(256), 0, st, sa);
     }
-    return hipGetLastError();
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // the encoders travel with the codec, which is all bsq_encode receives
+    for (int s = 0; s < cfg.stages && cfg.encoder == BSQ_ENC_LINEAR; ++s) {
+        e = hipMemcpyAsync(base + codec_enc_offset(cfg, s), dec[s].E, size_t(cfg.b) * cfg.d * 4,
+                           hipMemcpyDeviceToDevice, st);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace bsq

@@ -38,13 +38,16 @@ struct DecodeArgs {
 // is the number of protected columns before it, i.e. the rank of the first
 // protected column of j's 32-column word plus the set bits of that word
 // below j (both kept in LDS), so no search over the list is needed.
-template <int D, int S, bool BF16OUT>
+// D outputs per chunk, B code bits per stage (B = D unless the codec has a
+// linear encoder); the fp32 tables are in LDS for D = B = 8.
+template <int D, int B, int S, bool BF16OUT>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
-    typedef typename std::conditional<D == 8, uint32_t, uint2>::type CodeWord;
+    typedef typename std::conditional<B == 8, uint32_t, uint2>::type CodeWord;
+    constexpr bool TAB_LDS = (D == 8 && B == 8);
     extern __shared__ uint32_t s_mem[];
     // [words4] protected bitmap, [words4] rank of each word's first protected
-    // column, [k4] scales, then (D == 8) the fp32 tables
+    // column, [k4] scales, then (D = B = 8) the fp32 tables
     const int64_t words4 = (a.words + 3) & ~int64_t(3), k4 = (a.k + 3) & ~int64_t(3);
     uint32_t *s_bits = s_mem;
     int32_t *s_rank = reinterpret_cast<int32_t *>(s_mem + words4);
@@ -66,7 +69,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
             }
         }
     }
-    if constexpr (D == 8) {
+    if constexpr (TAB_LDS) {
         for (int e = t; e < S * 256 * 8; e += blockDim.x) {
             int s = e / (256 * 8), r = e - s * 256 * 8;
             s_tab[e] = a.tab32[s][r];
@@ -86,7 +89,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         const int64_t e = pbase + tile * 1024;
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-            if constexpr (D == 8) code[P][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
+            if constexpr (B == 8) code[P][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
             else code[P][s] = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(a.codes[s]) + e);
             gain[P][s] = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
         }
@@ -118,11 +121,11 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 #pragma unroll
             for (int s = 0; s < S; ++s) {
                 uint32_t cw;
-                if constexpr (D == 8) cw = (code[P][s] >> (8 * u)) & 0xffu;
+                if constexpr (B == 8) cw = (code[P][s] >> (8 * u)) & 0xffu;
                 else cw = ((u < 2 ? code[P][s].x : code[P][s].y) >> (16 * (u & 1))) & 0xffffu;
                 const uint32_t gw = (u < 2) ? gain[P][s].x : gain[P][s].y;
                 const float g = f16_bits_to_f32(uint16_t(gw >> (16 * (u & 1))));
-                const float *y = (D == 8) ? (s_tab + (s * 256 + cw) * 8) : (a.tab32[s] + size_t(cw) * D);
+                const float *y = TAB_LDS ? (s_tab + (s * 256 + cw) * 8) : (a.tab32[s] + size_t(cw) * D);
                 const float4 *y4 = reinterpret_cast<const float4 *>(y);
 #pragma unroll
                 for (int q = 0; q < D / 4; ++q) {
@@ -180,7 +183,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     }
 }
 
-template <int D, bool BF16OUT>
+template <int D, int B, bool BF16OUT>
 hipError_t launch_decode_t(int stages, const DecodeArgs &a, int64_t n_mats, hipStream_t st)
 {
     const int64_t tiles = (a.d_out + 63) / 64 * (a.pitch / 16);
@@ -191,14 +194,24 @@ hipError_t launch_decode_t(int stages, const DecodeArgs &a, int64_t n_mats, hipS
     if (gx < 1) gx = 1;
     const dim3 grid = dim3(unsigned(gx), unsigned(n_mats));
     const size_t shm = size_t((a.words + 3) & ~int64_t(3)) * 8 + size_t((a.k + 3) & ~int64_t(3)) * 4 +
-                       ((D == 8) ? size_t(stages) * 256 * 8 * 4 : 0);
+                       ((D == 8 && B == 8) ? size_t(stages) * 256 * 8 * 4 : 0);
     switch (stages) {
-    case 1: hipLaunchKernelGGL((decode_kernel<D, 1, BF16OUT>), grid, dim3(256), shm, st, a); break;
-    case 2: hipLaunchKernelGGL((decode_kernel<D, 2, BF16OUT>), grid, dim3(256), shm, st, a); break;
-    case 3: hipLaunchKernelGGL((decode_kernel<D, 3, BF16OUT>), grid, dim3(256), shm, st, a); break;
-    default: hipLaunchKernelGGL((decode_kernel<D, 4, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    case 1: hipLaunchKernelGGL((decode_kernel<D, B, 1, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    case 2: hipLaunchKernelGGL((decode_kernel<D, B, 2, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    case 3: hipLaunchKernelGGL((decode_kernel<D, B, 3, BF16OUT>), grid, dim3(256), shm, st, a); break;
+    default: hipLaunchKernelGGL((decode_kernel<D, B, 4, BF16OUT>), grid, dim3(256), shm, st, a); break;
     }
     return hipGetLastError();
+}
+
+// the (d, b) instantiation for a configuration
+template <bool BF16OUT>
+hipError_t launch_decode_db(const bsq_config &cfg, int stages, const DecodeArgs &a, int64_t n_mats, hipStream_t st)
+{
+    if (cfg.d == 8) return (cfg.b == 8) ? launch_decode_t<8, 8, BF16OUT>(stages, a, n_mats, st)
+                                        : launch_decode_t<8, 16, BF16OUT>(stages, a, n_mats, st);
+    return (cfg.b == 16) ? launch_decode_t<16, 16, BF16OUT>(stages, a, n_mats, st)
+                         : launch_decode_t<16, 8, BF16OUT>(stages, a, n_mats, st);
 }
 
 }  // namespace
@@ -225,12 +238,8 @@ hipError_t launch_decode(const bsq_config &cfg, const void *codec, const bsq_lay
     a.out = w_hat;
     a.pfmt = cfg.protect_format;
     a.scatter = 1;
-    const bool bf = (out_dtype == BSQ_BF16);
-    if (cfg.d == 8)
-        return bf ? launch_decode_t<8, true>(cfg.stages, a, L.n_mats, st)
-                  : launch_decode_t<8, false>(cfg.stages, a, L.n_mats, st);
-    return bf ? launch_decode_t<16, true>(cfg.stages, a, L.n_mats, st)
-              : launch_decode_t<16, false>(cfg.stages, a, L.n_mats, st);
+    return (out_dtype == BSQ_BF16) ? launch_decode_db<true>(cfg, cfg.stages, a, L.n_mats, st)
+                                   : launch_decode_db<false>(cfg, cfg.stages, a, L.n_mats, st);
 }
 
 // One residual stage of a sequential decode: W_hat = fmaf(gain, D_s(code),
@@ -259,7 +268,7 @@ hipError_t launch_decode_stage(const bsq_config &cfg, const void *codec, const b
     a.pfmt = cfg.protect_format;
     a.accumulate = accumulate;
     a.scatter = (stage == cfg.stages - 1);
-    return (cfg.d == 8) ? launch_decode_t<8, false>(1, a, L.n_mats, st) : launch_decode_t<16, false>(1, a, L.n_mats, st);
+    return launch_decode_db<false>(cfg, 1, a, L.n_mats, st);
 }
 
 }  // namespace bsq

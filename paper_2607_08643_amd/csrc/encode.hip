@@ -432,15 +432,20 @@ struct EncodeArgs {
     const uint32_t *bitmap;
     int32_t *err;
     int pfmt;  // bsq_prot_format of q8
+    const float *enc[BSQ_MAX_STAGES];  // linear encoder E [b][d] per stage, or null (identity)
 };
 
 // one element of the tiled planes (padding rows and chunks included):
-// matrix m, row i, chunk c, at plane position gid
-template <int D, int S, typename T>
-__device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, int64_t m, int64_t i,
-                                               int64_t c, int64_t gid)
+// matrix m, row i, chunk c, at plane position gid. D inputs per chunk, B code
+// bits; ENC: the stage code is the sign pattern of z = E r (E [B][D] in LDS,
+// s_E), else of r itself (B = D). The decoder table is in LDS (s_tab) for
+// D = B = 8, else read from the fp32 table in global memory.
+template <int D, int B, int S, typename T, bool ENC>
+__device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, const float *s_E,
+                                               int64_t m, int64_t i, int64_t c, int64_t gid)
 {
-    using code_t = typename std::conditional<D == 8, uint8_t, uint16_t>::type;
+    using code_t = typename std::conditional<B == 8, uint8_t, uint16_t>::type;
+    constexpr bool TAB_LDS = (D == 8 && B == 8);
 
     if (c >= a.C || i >= a.d_out) {
 #pragma unroll
@@ -499,9 +504,20 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
 #pragma unroll
     for (int s = 0; s < S; ++s) {
         uint32_t code = 0;
+        if constexpr (ENC) {
+            // z_m = sum_j E[m][j] r_j, the fmaf chain from +0 in j order
 #pragma unroll
-        for (int j = 0; j < D; ++j) code |= (r[j] >= 0.0f ? 1u : 0u) << j;
-        const float *y = (D == 8) ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
+            for (int mm = 0; mm < B; ++mm) {
+                float z = 0.0f;
+#pragma unroll
+                for (int j = 0; j < D; ++j) z = __builtin_fmaf(s_E[(s * B + mm) * D + j], r[j], z);
+                code |= (z >= 0.0f ? 1u : 0u) << mm;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < D; ++j) code |= (r[j] >= 0.0f ? 1u : 0u) << j;
+        }
+        const float *y = TAB_LDS ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
         float yv[D];
         if constexpr (D == 8) {
             const float4 *y4 = reinterpret_cast<const float4 *>(y);
@@ -542,17 +558,25 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
 // group and column block come from one scalar division per tile. Thread t
 // takes elements t, t + 256, ... of the tile: a wave covers four rows of 16
 // consecutive chunks, so its row reads are contiguous.
-template <int D, int S, typename T>
+template <int D, int B, int S, typename T, bool ENC>
 __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
 {
-    extern __shared__ float s_tab[];  // D == 8: [S][256][8]
-    if constexpr (D == 8) {
+    extern __shared__ float s_tab[];  // D = B = 8: [S][256][8]; then ENC: [S][B][D]
+    constexpr bool TAB_LDS = (D == 8 && B == 8);
+    float *s_E = s_tab + (TAB_LDS ? S * 256 * 8 : 0);
+    if constexpr (TAB_LDS) {
         for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
             int s = e / (256 * 8), r = e - s * 256 * 8;
             s_tab[e] = a.tab32[s][r];
         }
-        __syncthreads();
     }
+    if constexpr (ENC) {
+        for (int e = threadIdx.x; e < S * B * D; e += blockDim.x) {
+            int s = e / (B * D), r = e - s * B * D;
+            s_E[e] = a.enc[s][r];
+        }
+    }
+    if constexpr (TAB_LDS || ENC) __syncthreads();
     const int64_t nb = a.pitch >> 4;
     const int64_t tiles_per_mat = ((a.d_out + 63) >> 6) * nb;
     const int64_t ntiles = a.total >> 10;
@@ -563,26 +587,38 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = q * 256 + int(threadIdx.x);
-            encode_element<D, S, T>(a, s_tab, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), (tile << 10) + e);
+            encode_element<D, B, S, T, ENC>(a, s_tab, s_E, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), (tile << 10) + e);
         }
     }
 }
 
-template <int D, typename T>
+template <int D, int B, typename T, bool ENC>
 hipError_t launch_encode_chunks(int stages, const EncodeArgs &a, hipStream_t st)
 {
     // at most about 16 blocks per CU; each walks its share of the tiles
     int64_t blocks = a.total >> 10;
     if (blocks > 4096) blocks = 4096;
     const dim3 grid = dim3(unsigned(blocks));
-    const size_t shm = (D == 8) ? size_t(stages) * 256 * 8 * 4 : 0;
+    const size_t shm = ((D == 8 && B == 8) ? size_t(stages) * 256 * 8 * 4 : 0) +
+                       (ENC ? size_t(stages) * B * D * 4 : 0);
     switch (stages) {
-    case 1: hipLaunchKernelGGL((encode_kernel<D, 1, T>), grid, dim3(256), shm, st, a); break;
-    case 2: hipLaunchKernelGGL((encode_kernel<D, 2, T>), grid, dim3(256), shm, st, a); break;
-    case 3: hipLaunchKernelGGL((encode_kernel<D, 3, T>), grid, dim3(256), shm, st, a); break;
-    default: hipLaunchKernelGGL((encode_kernel<D, 4, T>), grid, dim3(256), shm, st, a); break;
+    case 1: hipLaunchKernelGGL((encode_kernel<D, B, 1, T, ENC>), grid, dim3(256), shm, st, a); break;
+    case 2: hipLaunchKernelGGL((encode_kernel<D, B, 2, T, ENC>), grid, dim3(256), shm, st, a); break;
+    case 3: hipLaunchKernelGGL((encode_kernel<D, B, 3, T, ENC>), grid, dim3(256), shm, st, a); break;
+    default: hipLaunchKernelGGL((encode_kernel<D, B, 4, T, ENC>), grid, dim3(256), shm, st, a); break;
     }
     return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_encode_cfg(const bsq_config &cfg, const EncodeArgs &a, hipStream_t st)
+{
+    const int S = cfg.stages;
+    if (cfg.encoder == BSQ_ENC_IDENTITY)
+        return (cfg.d == 8) ? launch_encode_chunks<8, 8, T, false>(S, a, st) : launch_encode_chunks<16, 16, T, false>(S, a, st);
+    if (cfg.d == 8)
+        return (cfg.b == 8) ? launch_encode_chunks<8, 8, T, true>(S, a, st) : launch_encode_chunks<8, 16, T, true>(S, a, st);
+    return (cfg.b == 8) ? launch_encode_chunks<16, 8, T, true>(S, a, st) : launch_encode_chunks<16, 16, T, true>(S, a, st);
 }
 
 }  // namespace
@@ -714,6 +750,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
         a.codes[s] = out.codes[s];
         a.gains[s] = out.gains[s];
         a.tab32[s] = reinterpret_cast<const float *>(cb + codec_tab32_offset(cfg, s));
+        if (cfg.encoder == BSQ_ENC_LINEAR) a.enc[s] = reinterpret_cast<const float *>(cb + codec_enc_offset(cfg, s));
     }
     a.q8 = rows ? nullptr : out.prot_q8;
     a.scale = out.prot_scale;
@@ -722,12 +759,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
     a.err = err;
     a.pfmt = cfg.protect_format;
     if (a.total > 0) {
-        if (cfg.d == 8)
-            e = bf ? launch_encode_chunks<8, uint16_t>(cfg.stages, a, st)
-                   : launch_encode_chunks<8, float>(cfg.stages, a, st);
-        else
-            e = bf ? launch_encode_chunks<16, uint16_t>(cfg.stages, a, st)
-                   : launch_encode_chunks<16, float>(cfg.stages, a, st);
+        e = bf ? launch_encode_cfg<uint16_t>(cfg, a, st) : launch_encode_cfg<float>(cfg, a, st);
         if (e != hipSuccess) return e;
     }
     if (k > 0 && rows && d_in > 0) {
@@ -746,7 +778,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
             r.gains[s] = out.gains[s];
         }
         r.stages = cfg.stages;
-        r.code_bytes = (cfg.d <= 8) ? 1 : 2;
+        r.code_bytes = (cfg.b <= 8) ? 1 : 2;
         r.err = err;
         r.pfmt = cfg.protect_format;
         const dim3 grid{unsigned(k), unsigned(n_mats)};

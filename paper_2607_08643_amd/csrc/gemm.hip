@@ -1077,6 +1077,114 @@ hipError_t launch_lane(const LaneGemmArgs &la, int tpw, hipStream_t st)
     }
 }
 
+// ---------------------------------------------------------------------------
+// Codes of b != d bits per chunk (a codec with a linear encoder): the
+// 2^b-entry decoder table does not suit the MFMA paths' decode, so the
+// product runs in fp32 over LDS tiles of decoded weights. A workgroup of 256
+// threads owns 64 rows x 32 tokens. Per 128-input K step it decodes the
+// 64 x 128 weight tile into LDS (each weight the fmaf chain over the stages
+// from 0, gain times fp32 table entry, as in decode), converts the X~ tile
+// (bf16, protected columns zero, written by gemm_prep) to fp32 in LDS, and
+// each thread accumulates 4 rows x 2 tokens. The protected term uses the
+// gathered activations and the LoRA term T = X A^T, both from gemm_prep.
+// ---------------------------------------------------------------------------
+struct GenericGemmArgs {
+    const void *codes[BSQ_MAX_STAGES];
+    const uint16_t *gains[BSQ_MAX_STAGES];
+    const float *tab32[BSQ_MAX_STAGES];
+    const int8_t *q8;
+    const float *scale;
+    const uint16_t *Xt, *Xp, *B;
+    const float *T;
+    int rank, pfmt, y_bf16;
+    int64_t M, d_out, pitch, C, ksteps, Kp, k, kp32, ldy;
+    void *Y;
+};
+
+template <int D, int B, int S>
+__global__ __launch_bounds__(256) void gemm_generic_kernel(const GenericGemmArgs a)
+{
+    __shared__ float s_w[64][BK + 1];
+    __shared__ float s_x[32][BK + 1];
+    const int t = threadIdx.x;
+    const int64_t n0 = int64_t(blockIdx.x) * 64, m0 = int64_t(blockIdx.y) * 32;
+    const int tr = t >> 4, tc = t & 15;  // rows 4 tr .. + 3, tokens 2 tc, 2 tc + 1
+    constexpr int CPK = BK / D;          // chunks per K step
+    float acc[4][2] = {};
+    for (int64_t ks = 0; ks < a.ksteps; ++ks) {
+        for (int e = t; e < 64 * CPK; e += 256) {
+            const int r = e / CPK, cc = e - r * CPK;
+            const int64_t row = n0 + r, c = ks * CPK + cc;
+            float v[D];
+#pragma unroll
+            for (int j = 0; j < D; ++j) v[j] = 0.0f;
+            if (row < a.d_out && c < a.C) {
+                const int64_t off = tile_index(row, c, a.pitch);
+#pragma unroll
+                for (int s = 0; s < S; ++s) {
+                    const uint32_t code = (B == 8) ? uint32_t(static_cast<const uint8_t *>(a.codes[s])[off])
+                                                   : uint32_t(static_cast<const uint16_t *>(a.codes[s])[off]);
+                    const float g = f16_bits_to_f32(a.gains[s][off]);
+                    const float *y = a.tab32[s] + size_t(code) * D;
+#pragma unroll
+                    for (int j = 0; j < D; ++j) v[j] = __builtin_fmaf(g, y[j], v[j]);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < D; ++j) s_w[r][cc * D + j] = v[j];
+        }
+        for (int e = t; e < 32 * BK; e += 256) {
+            const int tok = e / BK, col = e - tok * BK;
+            const int64_t mt = m0 + tok;
+            s_x[tok][col] = (mt < a.M) ? bf16_to_f32(a.Xt[mt * a.Kp + ks * BK + col]) : 0.0f;
+        }
+        __syncthreads();
+#pragma unroll 4
+        for (int kk = 0; kk < BK; ++kk) {
+            const float x0 = s_x[2 * tc][kk], x1 = s_x[2 * tc + 1][kk];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float w = s_w[4 * tr + i][kk];
+                acc[i][0] = __builtin_fmaf(w, x0, acc[i][0]);
+                acc[i][1] = __builtin_fmaf(w, x1, acc[i][1]);
+            }
+        }
+        __syncthreads();
+    }
+    const int64_t kp = q8_pitch(a.k);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int64_t row = n0 + 4 * tr + i;
+        if (row >= a.d_out) continue;
+#pragma unroll
+        for (int jt = 0; jt < 2; ++jt) {
+            const int64_t tok = m0 + 2 * tc + jt;
+            if (tok >= a.M) continue;
+            float v = acc[i][jt];
+            for (int64_t p = 0; p < a.k; ++p)
+                v = __builtin_fmaf(payload_to_f32(uint8_t(a.q8[row * kp + p]), a.pfmt) * a.scale[p],
+                                   bf16_to_f32(a.Xp[tok * a.kp32 + p]), v);
+            for (int r = 0; r < a.rank; ++r)
+                v = __builtin_fmaf(bf16_to_f32(a.B[row * a.rank + r]), a.T[tok * BSQ_MAX_LORA_RANK + r], v);
+            if (a.y_bf16) static_cast<uint16_t *>(a.Y)[tok * a.ldy + row] = f32_to_bf16(v);
+            else static_cast<float *>(a.Y)[tok * a.ldy + row] = v;
+        }
+    }
+}
+
+template <int D, int B>
+hipError_t launch_generic_t(int stages, const GenericGemmArgs &g, hipStream_t st)
+{
+    const dim3 grid(unsigned((g.d_out + 63) / 64), unsigned((g.M + 31) / 32));
+    switch (stages) {
+    case 1: hipLaunchKernelGGL((gemm_generic_kernel<D, B, 1>), grid, dim3(256), 0, st, g); break;
+    case 2: hipLaunchKernelGGL((gemm_generic_kernel<D, B, 2>), grid, dim3(256), 0, st, g); break;
+    case 3: hipLaunchKernelGGL((gemm_generic_kernel<D, B, 3>), grid, dim3(256), 0, st, g); break;
+    default: hipLaunchKernelGGL((gemm_generic_kernel<D, B, 4>), grid, dim3(256), 0, st, g); break;
+    }
+    return hipGetLastError();
+}
+
 // Launch shape: token tile and rows per block by M, then the K split, then
 // the workspace layout.
 struct GemmPlan {
@@ -1218,6 +1326,35 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     if (e != hipSuccess) return e;
 
     const int S = cfg.stages;
+    if (cfg.b != cfg.d) {
+        GenericGemmArgs g{};
+        const char *cb2 = static_cast<const char *>(codec);
+        for (int s = 0; s < S; ++s) {
+            g.codes[s] = L.codes[s];
+            g.gains[s] = L.gains[s];
+            g.tab32[s] = reinterpret_cast<const float *>(cb2 + codec_tab32_offset(cfg, s));
+        }
+        g.q8 = L.prot_q8;
+        g.scale = L.prot_scale;
+        g.Xt = a.Xt;
+        g.Xp = a.Xp;
+        g.T = a.T;
+        g.B = a.B;
+        g.rank = a.rank;
+        g.pfmt = cfg.protect_format;
+        g.y_bf16 = a.y_bf16;
+        g.M = M;
+        g.d_out = L.d_out;
+        g.pitch = L.pitch;
+        g.C = L.d_in / cfg.d;
+        g.ksteps = p.ksteps;
+        g.Kp = p.Kp;
+        g.k = L.k;
+        g.kp32 = p.kp32;
+        g.ldy = ldy;
+        g.Y = Y;
+        return (cfg.d == 8) ? launch_generic_t<8, 16>(S, g, st) : launch_generic_t<16, 8>(S, g, st);
+    }
     if (cfg.d == 8 && M <= 16) {
         // small M: the streaming kernel, when its slices' partials fit
         LaneGemmArgs la{};

@@ -47,7 +47,7 @@ inline bool gemv_split16(const bsq_config &cfg) { return codec_has_split(cfg) &&
 // at the same offset for every group size of one configuration and d_in.
 inline bool gemv_lane_path(const bsq_config &cfg, int x_dtype)
 {
-    return x_dtype == BSQ_BF16 && (cfg.d == 8 || gemv_split16(cfg));
+    return x_dtype == BSQ_BF16 && cfg.b == cfg.d && (cfg.d == 8 || gemv_split16(cfg));
 }
 
 inline size_t gemv_xp_bytes(const bsq_config &cfg, int64_t pitch)
@@ -1018,7 +1018,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
 // fp32 activations: the fp32 decoder table and fp32 arithmetic throughout.
 // One wave per row, lanes stride over the chunks.
 // ---------------------------------------------------------------------------
-template <int D, int S>
+// fp32 arithmetic throughout (fp32 x, and every configuration with b != d,
+// whatever the dtype of x): one wave per row over the 2^B-entry fp32 table,
+// D inputs per chunk and B code bits per stage; lanes stride the chunks.
+template <int D, int B, int S>
 __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
 {
     const int lane = threadIdx.x & 63;
@@ -1031,7 +1034,6 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
     }
     if (m >= a.n) return;
     const GemvMat &M = a.mat[m];
-    const float *x = static_cast<const float *>(a.x);
     const int64_t C = a.d_in / D;
     float acc = 0.0f;
     for (int64_t c = lane; c < C; c += 64) {
@@ -1039,12 +1041,12 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
 #pragma unroll
         for (int j = 0; j < D; ++j) {
             const int64_t col = c * D + j;
-            xv[j] = (a.k > 0 && is_protected(M.idx, a.k, col)) ? 0.0f : x[col];
+            xv[j] = (a.k > 0 && is_protected(M.idx, a.k, col)) ? 0.0f : load_x(a.x, col, a.x_bf16);
         }
         const int64_t off = tile_index(row, c, a.pitch);
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-            const uint32_t code = (D == 8) ? uint32_t(static_cast<const uint8_t *>(M.codes[s])[off])
+            const uint32_t code = (B == 8) ? uint32_t(static_cast<const uint8_t *>(M.codes[s])[off])
                                            : uint32_t(static_cast<const uint16_t *>(M.codes[s])[off]);
             const float gs = f16_bits_to_f32(M.gains[s][off]);
             const float *y = M.tab32[s] + size_t(code) * D;
@@ -1055,8 +1057,8 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
         }
     }
     for (int64_t p = lane; p < a.k; p += 64)
-        acc = __builtin_fmaf(payload_to_f32(uint8_t(M.q8[row * q8_pitch(a.k) + p]), a.pfmt), M.scale[p] * x[M.idx[p]],
-                             acc);
+        acc = __builtin_fmaf(payload_to_f32(uint8_t(M.q8[row * q8_pitch(a.k) + p]), a.pfmt),
+                             M.scale[p] * load_x(a.x, M.idx[p], a.x_bf16), acc);
     for (int q = lane; q < M.rank; q += 64) acc = __builtin_fmaf(bf16_to_f32(M.B[row * M.rank + q]), M.t[q], acc);
     for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o, 64);
     if (lane == 0) {
@@ -1065,15 +1067,15 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
     }
 }
 
-template <int D>
+template <int D, int B>
 hipError_t launch_f32(int stages, const GemvArgs &a, int64_t rows, hipStream_t st)
 {
     const dim3 grid(unsigned((rows + 3) / 4));
     switch (stages) {
-    case 1: hipLaunchKernelGGL((gemv_f32_kernel<D, 1>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((gemv_f32_kernel<D, 2>), grid, dim3(256), 0, st, a); break;
-    case 3: hipLaunchKernelGGL((gemv_f32_kernel<D, 3>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((gemv_f32_kernel<D, 4>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((gemv_f32_kernel<D, B, 1>), grid, dim3(256), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((gemv_f32_kernel<D, B, 2>), grid, dim3(256), 0, st, a); break;
+    case 3: hipLaunchKernelGGL((gemv_f32_kernel<D, B, 3>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((gemv_f32_kernel<D, B, 4>), grid, dim3(256), 0, st, a); break;
     }
     return hipGetLastError();
 }
@@ -1236,8 +1238,11 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
     int64_t rows_total = 0;
     for (int m = 0; m < n; ++m) rows_total += layers[m].d_out;
     if (rows_total == 0) return hipSuccess;
-    if (x_dtype != BSQ_BF16)
-        return (D == 8) ? launch_f32<8>(S, a, rows_total, st) : launch_f32<16>(S, a, rows_total, st);
+    if (x_dtype != BSQ_BF16 || cfg.b != cfg.d) {
+        if (cfg.b == cfg.d)
+            return (D == 8) ? launch_f32<8, 8>(S, a, rows_total, st) : launch_f32<16, 16>(S, a, rows_total, st);
+        return (D == 8) ? launch_f32<8, 16>(S, a, rows_total, st) : launch_f32<16, 8>(S, a, rows_total, st);
+    }
 
     if (D == 8 || gemv_split16(cfg)) {
         // row-lane kernel: one workgroup per (64-row group, slice of tiles)

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 6
+    assert bsq.bsq_version() == 7
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -63,10 +63,26 @@ def test_config_validation(kw, status):
     assert bsq.bsq_config_check(bsq.Config(**kw)) == status
 
 
-def test_code_bits_must_equal_chunk_length():
+def test_code_bits_other_than_chunk_length_need_the_linear_encoder():
+    """b (codebook_bits) may differ from d (codebook_dim) only with the
+    linear encoder (Section III-C's E_phi maps R^d to R^b); b and d are 8 or
+    16, and the identity decoder needs b = d."""
+    Lib = bsq.lib()
     c = bsq.Config().c()
     c.b = 16
-    assert bsq.lib().bsq_config_check(ct.byref(c)) == bsq.BSQ_ERR_UNSUPPORTED
+    assert Lib.bsq_config_check(ct.byref(c)) == bsq.BSQ_ERR_ARG
+    c.encoder = bsq.ENC_LINEAR
+    assert Lib.bsq_config_check(ct.byref(c)) == bsq.BSQ_OK
+    c.b = 12
+    assert Lib.bsq_config_check(ct.byref(c)) == bsq.BSQ_ERR_UNSUPPORTED
+    c.b = 8
+    assert Lib.bsq_config_check(ct.byref(c)) == bsq.BSQ_OK            # a linear encoder at b = d
+    ok = bsq.Config(d=16, codebook_bits=8, encoder=bsq.ENC_LINEAR)
+    assert bsq.bsq_config_check(ok) == bsq.BSQ_OK
+    assert bsq.bsq_config_check(bsq.Config(d=16, codebook_bits=8, encoder=bsq.ENC_LINEAR,
+                                           kind=bsq.DEC_IDENTITY, hidden=0)) == bsq.BSQ_ERR_ARG
+    c.encoder = 2
+    assert Lib.bsq_config_check(ct.byref(c)) == bsq.BSQ_ERR_ARG
 
 
 @pytest.mark.parametrize("d", [8, 16])
@@ -369,3 +385,29 @@ def test_row_axis_and_select_reject_before_launch():
     assert sel(Wg=FAKE + 4) == bsq.BSQ_ERR_ALIGN
     assert sel(ws_bytes=64) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
     assert bsq.bsq_workspace_bytes(cfg, bsq.OP_SELECT, 1, 25600, 5120) > 25600 * 8 * 4
+
+
+@pytest.mark.parametrize("d,b", [(8, 16), (16, 8), (8, 8), (16, 16)])
+@pytest.mark.parametrize("axis", [0, 1], ids=["cols", "rows"])
+def test_sizes_with_a_linear_encoder_match_oracle(d, b, axis):
+    """b bits per chunk and stage, b / 8 bytes per chunk in the code planes,
+    and the encoder's b d parameters in S_dec, as the oracle counts them."""
+    cfg = bsq.Config(d=d, codebook_bits=b, hidden=b, encoder=bsq.ENC_LINEAR, protect_axis=axis)
+    got = bsq.bsq_layer_sizes(cfg, 4096, 4096, 16)
+    ref = oracle.sizes(oracle.Config(d=d, b=b, stages=2, kind=oracle.KIND_MLP, hidden=b, protect_axis=axis,
+                                     encoder=oracle.ENC_LINEAR), 4096, 4096, 16)
+    for key in ("S_code", "S_dec", "S_8bit", "S_LoRA", "S_meta", "S_tot", "bpw_nominal", "bpw_real"):
+        assert got[key] == pytest.approx(ref[key], rel=1e-12), key
+    assert got["code_plane_bytes"] == 4096 * got["pitch"] * (b // 8)
+
+
+def test_codec_with_a_linear_encoder_needs_E():
+    Lib = bsq.lib()
+    cfg = bsq.Config(d=8, codebook_bits=16, hidden=16, encoder=bsq.ENC_LINEAR)
+    c = cfg.c()
+    need = bsq.bsq_codec_bytes(cfg)
+    # three tables of 2^16 x 8 entries per stage (fp32, bf16, fp16), then the two E copies
+    assert need == 2 * 65536 * 8 * 8 + 2 * 16 * 8 * 4
+    noE = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE, 0, 0, 0)] * 4)
+    assert Lib.bsq_codec_prepare(ct.byref(c), noE, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
+    assert Lib.bsq_codec_prepare(ct.byref(c), noE, ct.c_void_p(FAKE), need - 1, None) == bsq.BSQ_ERR_BUFFER_TOO_SMALL

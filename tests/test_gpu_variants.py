@@ -8,6 +8,10 @@ oracle's (found there by trying every code) and torch's own float8 cast, and
 the decoded slice must be torch's reading of those bytes, on the input-column
 axis and on the output-row axis. A second test writes all 256 bytes, NaN and
 infinity codes included, into a layer's payload and decodes them.
+
+The linear encoder z = E r (Section III-C) and code lengths b other than the
+chunk length d: encode, stage-parallel and sequential decode bit-exact, GEMV
+(bf16 and fp32 x) and GEMM against the oracle with LoRA.
 """
 import numpy as np
 import pytest
@@ -122,3 +126,76 @@ def test_every_stored_byte_decodes_to_its_value(fmt, d, gpu):
     nan = np.isnan(want)
     np.testing.assert_array_equal(np.isnan(got), nan)
     np.testing.assert_array_equal(got[~nan].view(np.uint32), want[~nan].view(np.uint32))
+
+
+# ---------------------------------------------------------------- linear encoder, b != d
+from test_gpu_parity import assert_layer_equal  # noqa: E402
+
+# (name, d_out, d_in, d, b, decoder kind, hidden, W dtype)
+ENC_CASES = [
+    ("enc-d8-b16", 96, 512, 8, 16, bsq.DEC_MLP, 16, torch.bfloat16),
+    ("enc-d16-b8", 80, 640, 16, 8, bsq.DEC_MLP, 8, torch.bfloat16),
+    ("enc-d8-b8", 120, 512, 8, 8, bsq.DEC_MLP, 8, torch.bfloat16),
+    ("enc-d16-b16-linear", 64, 512, 16, 16, bsq.DEC_LINEAR, 16, torch.float32),
+    ("enc-d8-b16-res1-e4m3", 70, 384, 8, 16, bsq.DEC_MLP_RES1, 12, torch.bfloat16),
+]
+
+
+def _make_enc(case, gpu, seed=41):
+    name, d_out, d_in, d, b, kind, h, dtype = case
+    fmt = bsq.PROT_E4M3 if "e4m3" in name else bsq.PROT_INT8
+    cfg = bsq.Config(d=d, codebook_bits=b, kind=kind, hidden=h, encoder=bsq.ENC_LINEAR, protect_format=fmt)
+    decs = synth.decoder_params(kind, d, b, h, cfg.stages, seed=seed, encoder=True)
+    W, _ = synth.weight(d_out, d_in, seed, k_outliers=cfg.k(d_in), dtype=dtype, device="cpu")
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W.to(gpu))
+    torch.cuda.synchronize()
+    oc = oracle.Config(d=d, b=b, stages=cfg.stages, kind=OKIND[kind], hidden=h, protect_format=OFMT[fmt],
+                       encoder=oracle.ENC_LINEAR)
+    tabs = oracle.decoder_table(oc, decs)
+    enc = oracle.encode(oc, decs, oracle.to_f32(W), tables=tabs)
+    return cfg, oc, decs, codec, layer, W, enc, tabs
+
+
+@pytest.mark.parametrize("case", ENC_CASES, ids=[c[0] for c in ENC_CASES])
+def test_linear_encoder_encode_decode_bit_exact(case, gpu):
+    say(f"encoder case {case[0]}")
+    cfg, oc, decs, codec, layer, W, enc, tabs = _make_enc(case, gpu)
+    assert layer.codes[0].dtype == (torch.uint8 if cfg.b == 8 else torch.int16)
+    assert_layer_equal(layer, enc, cfg)
+    w32 = bsq.bsq_decode(cfg, codec, layer, dtype=torch.float32)
+    w16 = bsq.bsq_decode(cfg, codec, layer, dtype=torch.bfloat16)
+    seq = torch.full_like(w32, float("nan"))
+    for s in range(cfg.stages):
+        bsq.bsq_decode_stage(cfg, codec, layer, s, s > 0, seq)
+    torch.cuda.synchronize()
+    ref = oracle.decode(oc, decs, enc, tables=tabs)
+    np.testing.assert_array_equal(w32.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+    assert torch.equal(w16.cpu().view(torch.int16), torch.from_numpy(ref).to(torch.bfloat16).view(torch.int16))
+    assert torch.equal(seq.view(torch.int32), w32.view(torch.int32))
+
+
+@pytest.mark.parametrize("case", ENC_CASES, ids=[c[0] for c in ENC_CASES])
+def test_linear_encoder_products_match_oracle(case, gpu):
+    say(f"encoder case {case[0]} products")
+    cfg, oc, decs, codec, layer, W, enc, tabs = _make_enc(case, gpu)
+    name, d_out, d_in = case[:3]
+    w_hat = oracle.decode(oc, decs, enc, tables=tabs)
+    A, Bm = synth.lora(d_out, d_in, 16, seed=43)
+    lref = (oracle.to_f32(A), oracle.to_f32(Bm))
+    fp32_path = cfg.b != cfg.d
+    for xdt in (torch.bfloat16, torch.float32):
+        x = synth.activation(d_in, seed=44, dtype=xdt)
+        y = bsq.bsq_gemv(cfg, codec, layer, x.to(gpu), loras=(A.to(gpu), Bm.to(gpu)), y_dtype=torch.float32)
+        torch.cuda.synchronize()
+        xf = oracle.to_f32(x)
+        kind = "fp32" if (fp32_path or xdt == torch.float32) else "gemv"
+        check_product(y.cpu().numpy(), oracle.dense_product(w_hat, xf, lref), kind, cfg, enc, tabs, w_hat, xf, lref,
+                      f"gemv x={xdt}", torch.float32)
+    for M in (1, 16, 100):
+        X = synth.activation(d_in, seed=45, dtype=torch.bfloat16, batch=M)
+        Y = bsq.bsq_gemm(cfg, codec, layer, X.to(gpu), lora=(A.to(gpu), Bm.to(gpu)), y_dtype=torch.float32)
+        torch.cuda.synchronize()
+        Xf = oracle.to_f32(X)
+        check_product(Y.cpu().numpy(), oracle.dense_product(w_hat, Xf, lref), "fp32" if fp32_path else "gemm", cfg,
+                      enc, tabs, w_hat, Xf, lref, f"gemm M={M}", torch.float32)
