@@ -97,6 +97,7 @@ def lib():
         L.orc_q8_rows.argtypes = [P, I64, I64, P, I64, I32, P, P]
         L.orc_encode_set.argtypes = [I32, I32, I32, P, P, P, I64, I64, I32, P, I64, I64, I32, P, P, P, P, I32]
         L.orc_max_threads.restype = I32
+        L.orc_train_decisions.argtypes = [I32, I32, I32, P, P, P, P, I64, P, P]
         for f in ("orc_decoder_eval", "orc_decoder_table", "orc_protect_select",
                   "orc_encode", "orc_decode", "orc_gemv_fused", "orc_topk", "orc_coupled_select",
                   "orc_encode_set"):
@@ -502,6 +503,24 @@ def to_f32(t) -> np.ndarray:
     except ImportError:
         pass
     return np.asarray(t, dtype=np.float32)
+
+
+def code_scale(b: int) -> float:
+    """fp32(1 / sqrt(b)), the magnitude of a spherical code entry."""
+    return float(lib().orc_code_scale(b))
+
+
+def train_decisions(b: int, h: int, E, W1, b1, x):
+    """fp32 decisions of a training forward pass over chunks x [n, d]: the
+    codes of z = E x and the ReLU masks [n, h] of the decoder's hidden layer
+    (orc_train_decisions)."""
+    x = _f32(x)
+    n, d = x.shape
+    E, W1, b1 = _f32(E), _f32(W1), _f32(b1)
+    codes = np.zeros(max(n, 1), dtype=np.uint32)
+    masks = np.zeros((max(n, 1), h), dtype=np.uint8)
+    lib().orc_train_decisions(d, b, h, _p(E), _p(W1), _p(b1), _p(x), n, _p(codes), _p(masks))
+    return codes[:n].copy(), masks[:n].copy()
 
 
 def max_threads() -> int:

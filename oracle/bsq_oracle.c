@@ -675,6 +675,39 @@ int orc_gemv_fused(int d, int b, int stages, const float *const *tables,
     return ORC_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Codec training (Section III-C, eq. codec_loss_terms): the decisions of one */
+/* forward pass, taken in fp32 so that the training kernels and the oracle   */
+/* agree on them exactly (the values of the pass are fp64 in oracle/train.py) */
+/* ------------------------------------------------------------------------ */
+
+/* For chunks x [n][d] (fp32): the code of z = E x (E [b][d], the fmaf chain
+ * from +0 in j order, bit m = (z_m >= 0)), and the ReLU mask of the decoder's
+ * hidden pre-activation at q = sign(z) / sqrt(b) (pre_k = fmaf chain from
+ * b1_k over j of W1[k][j] q_j; mask bit k = (pre_k > 0)). codes [n], masks
+ * [n][h] (0 or 1). */
+void orc_train_decisions(int d, int b, int h, const float *E, const float *W1, const float *b1,
+                         const float *x, int64_t n, uint32_t *codes, unsigned char *masks)
+{
+    float c = orc_code_scale(b);
+    for (int64_t i = 0; i < n; ++i) {
+        uint32_t code = 0;
+        float q[MAX_CODE_BITS];
+        for (int m = 0; m < b; ++m) {
+            float z = 0.0f;
+            for (int j = 0; j < d; ++j) z = fmaf(E[m * d + j], x[i * d + j], z);
+            if (z >= 0.0f) code |= 1u << m;
+            q[m] = (z >= 0.0f) ? c : -c;
+        }
+        codes[i] = code;
+        for (int k = 0; k < h; ++k) {
+            float acc = b1[k];
+            for (int j = 0; j < b; ++j) acc = fmaf(W1[k * b + j], q[j], acc);
+            masks[i * h + k] = (acc > 0.0f) ? 1 : 0;
+        }
+    }
+}
+
 int orc_max_threads(void)
 {
 #ifdef _OPENMP
