@@ -70,7 +70,7 @@
 extern "C" {
 #endif
 
-#define BSQ_ABI_VERSION 7
+#define BSQ_ABI_VERSION 8
 #define BSQ_MAX_STAGES 4
 #define BSQ_PITCH_ALIGN 16
 #define BSQ_MAX_HIDDEN 64
@@ -481,6 +481,65 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
                     const bsq_lora *lora, const void *X, int32_t x_dtype, int64_t M,
                     int64_t ldx, void *Y, int32_t y_dtype, int64_t ldy,
                     void *ws, size_t ws_bytes, int32_t *err, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Codec training (Section III-C; eq. codec_loss, eq. codec_loss_terms;
+ * Section III-G, category-batched codec optimisation).
+ *
+ * One stage codec with the LINEAR encoder and the symmetric decoder without
+ * residual block (cfg->encoder = BSQ_ENC_LINEAR, cfg->dec_kind = BSQ_DEC_MLP,
+ * d and b 8 or 16, h = cfg->hidden) is trained on weight chunks: for a
+ * mini-batch of N chunks x_i,
+ *   z = E x, u = z / ||z||, q = sign(u) / sqrt(b), x_hat = D(q) with the
+ *   straight-through estimator (the decoder reads q; the gradient reaching q
+ *   is passed to u; a chunk with z = 0 has u = 0 and passes none),
+ *   L_rec = 1/N sum ||x_hat - x||^2,  L_com = 1/N sum ||u - sg(q)||^2,
+ *   p_ij = [sigma(-t_ij), sigma(t_ij)], t_ij = 2 tau u_ij / sqrt(b),
+ *   L_ent = 1/N sum_i sum_j H(p_ij) - gamma sum_j H(mean_i p_ij),
+ *   L = L_rec + lambda_c L_com + lambda_e L_ent   (natural logarithms).
+ * The parameters are one fp32 vector theta, laid out
+ *   E [b][d] | W1 [h][b] | b1 [h] | W2 [d][h] | b2 [d]
+ * (bsq_train_param_count floats; the first b d and the decoder part are what
+ * bsq_codec_prepare takes as E, W1, b1, W2, b2). The code bits of z and the
+ * ReLU mask of the hidden layer are decided in fp32 by the same fmaf chains
+ * as the encoder's; every reduction runs in a fixed order, so a step is
+ * deterministic.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+    float lambda_c;  /* commitment weight */
+    float lambda_e;  /* entropy weight */
+    float gamma;     /* batch-entropy weight */
+    float tau;       /* bit-probability temperature */
+    float lr, beta1, beta2, eps;  /* Adam (Kingma & Ba 2015) */
+} bsq_train_hparams;
+
+bsq_status bsq_train_param_count(const bsq_config *cfg, int64_t *count);
+/* device workspace for a mini-batch of n chunks (256-byte aligned) */
+bsq_status bsq_train_workspace_bytes(const bsq_config *cfg, int64_t n, size_t *bytes);
+
+/* Loss and gradient of one mini-batch.
+ *   chunks   device [n_total][d], fp32 or bf16 (x_dtype): the chunks of a
+ *            category, e.g. its stacked layers [n_mats][d_out][d_in] viewed
+ *            as n_mats d_out d_in / d chunks (row-major chunks are contiguous)
+ *   idx      device int64 [n] chunk indices of the mini-batch, or NULL for
+ *            chunks 0 .. n-1; an index outside [0, n_total) ORs
+ *            BSQ_DEVERR_BAD_SET into *err and reads chunk 0
+ *   theta    device fp32 [P] (read)
+ *   grad     device fp32 [P] (written): dL/dtheta
+ *   loss     device fp32 [4] (written): L, L_rec, L_com, L_ent
+ *   err      device int32 error word or NULL
+ *   ws       device workspace of bsq_train_workspace_bytes(cfg, n) */
+bsq_status bsq_train_grad(const bsq_config *cfg, const bsq_train_hparams *hp, const void *chunks, int32_t x_dtype,
+                          int64_t n_total, const int64_t *idx, int64_t n, const float *theta, float *grad,
+                          float *loss, int32_t *err, void *ws, size_t ws_bytes, void *stream);
+
+/* One Adam step in place, bias-corrected, step = 1, 2, ...:
+ *   m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2;
+ *   theta -= lr (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ * theta, m, v device fp32 [P] (m, v zero before step 1); grad as written by
+ * bsq_train_grad. */
+bsq_status bsq_train_adam(const bsq_config *cfg, const bsq_train_hparams *hp, int32_t step, float *theta,
+                          const float *grad, float *m, float *v, void *stream);
 
 #ifdef __cplusplus
 }

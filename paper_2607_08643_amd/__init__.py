@@ -12,5 +12,6 @@ from ._binding import (  # noqa: F401
     bsq_decode, bsq_decode_stage, bsq_decoder,
     bsq_encode, bsq_encode_with_set,
     bsq_gemm, bsq_gemv, bsq_gemv_noalloc, bsq_layer, bsq_layer_sizes, bsq_lora, bsq_sizes, bsq_version, bsq_workspace_bytes,
+    TrainHyper, bsq_train_adam, bsq_train_grad, bsq_train_hparams, bsq_train_param_count, bsq_train_workspace_bytes,
     layer_empty, lib, status_str,
 )

@@ -77,10 +77,11 @@ class bsq_sizes(ct.Structure):
 EXPORTS = ("bsq_version", "bsq_status_str", "bsq_config_check", "bsq_layer_sizes", "bsq_workspace_bytes",
            "bsq_codec_bytes", "bsq_codec_prepare", "bsq_encode", "bsq_decode", "bsq_gemv", "bsq_gemv_prepare",
            "bsq_gemv_run", "bsq_gemm", "bsq_encode_with_set", "bsq_coupled_select",
-           "bsq_debug_set_wait_limit", "bsq_decode_stage", "bsq_gemv_noalloc")
+           "bsq_debug_set_wait_limit", "bsq_decode_stage", "bsq_gemv_noalloc", "bsq_train_param_count",
+           "bsq_train_workspace_bytes", "bsq_train_grad", "bsq_train_adam")
 
 # struct layouts above follow this version of include/bsq.h
-ABI_VERSION = 7
+ABI_VERSION = 8
 
 _lib = None
 
@@ -114,6 +115,10 @@ def lib():
     L.bsq_gemv_noalloc.argtypes = [P, I32, P, P, P, P, I32, P, I32, I32, P, P]
     L.bsq_encode_with_set.argtypes = [P, P, P, I32, I64, I64, I64, P, P, P, P, SZ, P]
     L.bsq_coupled_select.argtypes = [P, P, P, P, I32, I64, I64, P, P, P, P, P, P, P, SZ, P]
+    L.bsq_train_param_count.argtypes = [P, ct.POINTER(I64)]
+    L.bsq_train_workspace_bytes.argtypes = [P, I64, ct.POINTER(SZ)]
+    L.bsq_train_grad.argtypes = [P, P, P, I32, I64, P, I64, P, P, P, P, P, SZ, P]
+    L.bsq_train_adam.argtypes = [P, P, I32, P, P, P, P, P]
     for f in EXPORTS[2:]:
         getattr(L, f).restype = I32
     if L.bsq_version() != ABI_VERSION:
@@ -580,3 +585,68 @@ def bsq_debug_set_wait_limit(polls: int) -> int:
     finishing workgroup gives up waiting; 0 forces every such wait to give
     up, a negative value restores the default. Returns the previous value."""
     return int(lib().bsq_debug_set_wait_limit(int(polls)))
+
+
+# ---------------------------------------------------------------- codec training
+class bsq_train_hparams(ct.Structure):
+    _fields_ = [(n, ct.c_float) for n in ("lambda_c", "lambda_e", "gamma", "tau", "lr", "beta1", "beta2", "eps")]
+
+
+@dataclass(frozen=True)
+class TrainHyper:
+    """Codec-training hyperparameters (bsq_train_hparams)."""
+    lambda_c: float = 0.25
+    lambda_e: float = 0.1
+    gamma: float = 1.0
+    tau: float = 1.0
+    lr: float = 1e-3
+    beta1: float = 0.9
+    beta2: float = 0.999
+    eps: float = 1e-8
+
+    def c(self) -> bsq_train_hparams:
+        return bsq_train_hparams(self.lambda_c, self.lambda_e, self.gamma, self.tau, self.lr, self.beta1,
+                                 self.beta2, self.eps)
+
+
+def bsq_train_param_count(cfg: Config) -> int:
+    out = ct.c_int64()
+    c = cfg.c()
+    _check(lib().bsq_train_param_count(ct.byref(c), ct.byref(out)), "bsq_train_param_count")
+    return out.value
+
+
+def bsq_train_workspace_bytes(cfg: Config, n: int) -> int:
+    out = ct.c_size_t()
+    c = cfg.c()
+    _check(lib().bsq_train_workspace_bytes(ct.byref(c), n, ct.byref(out)), "bsq_train_workspace_bytes")
+    return out.value
+
+
+def bsq_train_grad(cfg: Config, hp: TrainHyper, chunks, theta, idx=None, n=None, grad=None, loss=None, err=None,
+                   ws=None, stream=None):
+    """Loss [4] (L, L_rec, L_com, L_ent) and gradient [P] of one mini-batch.
+    chunks: a device tensor (fp32 or bf16) whose elements are the category's
+    chunks back to back (any shape with numel a multiple of d); idx: device
+    int64 chunk indices or None for the first n chunks."""
+    dev = chunks.device
+    x_dtype = BSQ_BF16 if chunks.dtype == torch.bfloat16 else BSQ_F32
+    n_total = chunks.numel() // cfg.d
+    if n is None:
+        n = idx.numel() if idx is not None else n_total
+    P = bsq_train_param_count(cfg)
+    grad = torch.empty(P, dtype=torch.float32, device=dev) if grad is None else grad
+    loss = torch.empty(4, dtype=torch.float32, device=dev) if loss is None else loss
+    if ws is None:
+        ws = _empty_aligned(bsq_train_workspace_bytes(cfg, n), dev)
+    c, h = cfg.c(), hp.c()
+    _check(lib().bsq_train_grad(ct.byref(c), ct.byref(h), _ptr(chunks), x_dtype, n_total, _ptr(idx), n, _ptr(theta),
+                                _ptr(grad), _ptr(loss), _ptr(err), _ptr(ws), ws.numel(), _stream(stream)),
+           "bsq_train_grad")
+    return loss, grad
+
+
+def bsq_train_adam(cfg: Config, hp: TrainHyper, step: int, theta, grad, m, v, stream=None):
+    c, h = cfg.c(), hp.c()
+    _check(lib().bsq_train_adam(ct.byref(c), ct.byref(h), step, _ptr(theta), _ptr(grad), _ptr(m), _ptr(v),
+                                _stream(stream)), "bsq_train_adam")

@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libbsq.so")
-SOURCES = ["api.hip", "codec.hip", "encode.hip", "decode.hip", "gemv.hip", "gemm.hip", "rows.hip"]
+SOURCES = ["api.hip", "codec.hip", "encode.hip", "decode.hip", "gemv.hip", "gemm.hip", "rows.hip", "train.hip"]
 ARCH = os.environ.get("BSQ_OFFLOAD_ARCH", "gfx950")
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=off",

@@ -552,4 +552,72 @@ bsq_status bsq_gemm(const bsq_config *cfg, const void *codec, const bsq_layer *l
     return from_hip(launch_gemm_rows(*layer, cfg->protect_format, lora, X, M, ldx, Y, y_dtype, ldy, gemm_lora_t(ws), st));
 }
 
+
+namespace {
+bsq_status check_train_cfg(const bsq_config *cfg)
+{
+    bsq_status s = check_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (cfg->encoder != BSQ_ENC_LINEAR || cfg->dec_kind != BSQ_DEC_MLP) return BSQ_ERR_UNSUPPORTED;
+    return BSQ_OK;
+}
+
+bool finite_hparams(const bsq_train_hparams *hp)
+{
+    const float v[8] = {hp->lambda_c, hp->lambda_e, hp->gamma, hp->tau, hp->lr, hp->beta1, hp->beta2, hp->eps};
+    for (float f : v)
+        if (!(f == f) || f > 3.0e38f || f < -3.0e38f) return false;
+    return hp->beta1 >= 0.0f && hp->beta1 < 1.0f && hp->beta2 >= 0.0f && hp->beta2 < 1.0f && hp->eps >= 0.0f;
+}
+}  // namespace
+
+bsq_status bsq_train_param_count(const bsq_config *cfg, int64_t *count)
+{
+    bsq_status s = check_train_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!count) return BSQ_ERR_ARG;
+    *count = train_param_count(*cfg);
+    return BSQ_OK;
+}
+
+bsq_status bsq_train_workspace_bytes(const bsq_config *cfg, int64_t n, size_t *bytes)
+{
+    bsq_status s = check_train_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!bytes || n < 1) return BSQ_ERR_ARG;
+    if (n > (int64_t(1) << 26)) return BSQ_ERR_UNSUPPORTED;
+    *bytes = train_ws_bytes(*cfg, n);
+    return BSQ_OK;
+}
+
+bsq_status bsq_train_grad(const bsq_config *cfg, const bsq_train_hparams *hp, const void *chunks, int32_t x_dtype,
+                          int64_t n_total, const int64_t *idx, int64_t n, const float *theta, float *grad,
+                          float *loss, int32_t *err, void *ws, size_t ws_bytes, void *stream)
+{
+    bsq_status s = check_train_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!hp || !chunks || !theta || !grad || !loss || !ws) return BSQ_ERR_ARG;
+    if (!finite_hparams(hp)) return BSQ_ERR_ARG;
+    if (x_dtype != BSQ_F32 && x_dtype != BSQ_BF16) return BSQ_ERR_DTYPE;
+    if (n < 1 || n_total < 1 || (!idx && n > n_total)) return BSQ_ERR_SHAPE;
+    if (n > (int64_t(1) << 26)) return BSQ_ERR_UNSUPPORTED;
+    if (!aligned(chunks, x_dtype == BSQ_F32 ? 4 : 2) || !aligned(theta, 4) || !aligned(grad, 4) ||
+        !aligned(loss, 4) || !aligned(ws, 256) || (idx && !aligned(idx, 8)) || (err && !aligned(err, 4)))
+        return BSQ_ERR_ALIGN;
+    if (ws_bytes < train_ws_bytes(*cfg, n)) return BSQ_ERR_BUFFER_TOO_SMALL;
+    return from_hip(launch_train_grad(*cfg, *hp, chunks, x_dtype, n_total, idx, n, theta, grad, loss, err, ws,
+                                      static_cast<hipStream_t>(stream)));
+}
+
+bsq_status bsq_train_adam(const bsq_config *cfg, const bsq_train_hparams *hp, int32_t step, float *theta,
+                          const float *grad, float *m, float *v, void *stream)
+{
+    bsq_status s = check_train_cfg(cfg);
+    if (s != BSQ_OK) return s;
+    if (!hp || !theta || !grad || !m || !v || step < 1) return BSQ_ERR_ARG;
+    if (!finite_hparams(hp)) return BSQ_ERR_ARG;
+    if (!aligned(theta, 4) || !aligned(grad, 4) || !aligned(m, 4) || !aligned(v, 4)) return BSQ_ERR_ALIGN;
+    return from_hip(launch_train_adam(*cfg, *hp, step, theta, grad, m, v, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

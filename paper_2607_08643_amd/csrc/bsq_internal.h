@@ -253,6 +253,17 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
                        const bsq_lora *lora, const void *X, int64_t M, int64_t ldx, void *Y,
                        int y_dtype, int64_t ldy, void *ws, int32_t *err, hipStream_t st);
 
+// Codec training (train.hip): parameters of one stage codec, floats per chunk
+// record, workspace bytes for a batch of n chunks, and the two launches.
+int64_t train_param_count(const bsq_config &cfg);
+int64_t train_record_floats(const bsq_config &cfg);
+size_t train_ws_bytes(const bsq_config &cfg, int64_t n);
+hipError_t launch_train_grad(const bsq_config &cfg, const bsq_train_hparams &hp, const void *x, int x_dtype,
+                             int64_t n_total, const int64_t *idx, int64_t n, const float *theta, float *grad,
+                             float *loss, int32_t *err, void *ws, hipStream_t st);
+hipError_t launch_train_adam(const bsq_config &cfg, const bsq_train_hparams &hp, int step, float *theta,
+                             const float *grad, float *m, float *v, hipStream_t st);
+
 // Polls a finishing workgroup makes for another workgroup's partial result
 // before it gives up (reports BSQ_DEVERR_TIMEOUT and poisons the workspace).
 // Workgroups run in dispatch order, so the wait is never expected to give

@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for name in names:
         assert hasattr(L, name), name
     assert set(names) == set(B.EXPORTS)
-    assert bsq.bsq_version() == 7
+    assert bsq.bsq_version() == 8
     for s in range(0, 9):
         assert bsq.status_str(s) != "unknown status"
     assert bsq.status_str(99) == "unknown status"
@@ -411,3 +411,42 @@ def test_codec_with_a_linear_encoder_needs_E():
     noE = (B.bsq_decoder * 4)(*[B.bsq_decoder(FAKE, FAKE, FAKE, FAKE, 0, 0, 0)] * 4)
     assert Lib.bsq_codec_prepare(ct.byref(c), noE, ct.c_void_p(FAKE), need, None) == bsq.BSQ_ERR_ARG
     assert Lib.bsq_codec_prepare(ct.byref(c), noE, ct.c_void_p(FAKE), need - 1, None) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+
+
+def test_training_entry_points_validate_before_launch():
+    """Codec training takes the linear encoder and the plain symmetric
+    decoder; parameter count b d + h b + h + d h + d; every bad argument is
+    refused on the host."""
+    Lib = bsq.lib()
+    cfg = bsq.Config(d=8, hidden=8, encoder=bsq.ENC_LINEAR)
+    assert bsq.bsq_train_param_count(cfg) == 64 + 64 + 8 + 64 + 8
+    assert bsq.bsq_train_param_count(bsq.Config(d=8, codebook_bits=16, hidden=12, encoder=bsq.ENC_LINEAR)) == \
+        16 * 8 + 12 * 16 + 12 + 8 * 12 + 8
+    for bad in (bsq.Config(d=8, hidden=8), bsq.Config(d=8, hidden=8, encoder=bsq.ENC_LINEAR, kind=bsq.DEC_MLP_RES1),
+                bsq.Config(d=8, encoder=bsq.ENC_LINEAR, kind=bsq.DEC_LINEAR)):
+        with pytest.raises(bsq.BsqError) as e:
+            bsq.bsq_train_param_count(bad)
+        assert e.value.status == bsq.BSQ_ERR_UNSUPPORTED
+    ws = bsq.bsq_train_workspace_bytes(cfg, 4096)
+    assert ws > 4096 * (2 * 8 + 2 * 8 + 2 * 8) * 4
+    c = cfg.c()
+    hp = bsq.TrainHyper().c()
+    F = ct.c_void_p(FAKE)
+    ok = dict(chunks=F, x=bsq.BSQ_F32, nt=4096, idx=None, n=4096, th=F, g=F, l=F, err=None, ws=F, wsb=ws)
+
+    def call(**kw):
+        a = {**ok, **kw}
+        return Lib.bsq_train_grad(ct.byref(c), ct.byref(a.get("hp", hp)), a["chunks"], a["x"], a["nt"], a["idx"],
+                                  a["n"], a["th"], a["g"], a["l"], a["err"], a["ws"], a["wsb"], None)
+    assert call(n=0) == bsq.BSQ_ERR_SHAPE
+    assert call(n=4097) == bsq.BSQ_ERR_SHAPE          # more than the chunks, with no index list
+    assert call(wsb=ws - 1) == bsq.BSQ_ERR_BUFFER_TOO_SMALL
+    assert call(x=7) == bsq.BSQ_ERR_DTYPE
+    assert call(th=None) == bsq.BSQ_ERR_ARG
+    assert call(ws=ct.c_void_p(FAKE + 64)) == bsq.BSQ_ERR_ALIGN
+    assert call(idx=ct.c_void_p(FAKE + 4)) == bsq.BSQ_ERR_ALIGN
+    nan_hp = bsq.TrainHyper(lr=float("nan")).c()
+    assert call(hp=nan_hp) == bsq.BSQ_ERR_ARG
+    assert call(hp=bsq.TrainHyper(beta2=1.0).c()) == bsq.BSQ_ERR_ARG
+    assert Lib.bsq_train_adam(ct.byref(c), ct.byref(hp), 0, F, F, F, F, None) == bsq.BSQ_ERR_ARG
+    assert Lib.bsq_train_adam(ct.byref(c), ct.byref(hp), 1, F, None, F, F, None) == bsq.BSQ_ERR_ARG
