@@ -389,6 +389,56 @@ def variants(bsq, synth, torch, dev, s):
     return out
 
 
+def training(bsq, synth, torch, dev, d=8, b=8, batch=1 << 16, steps=40):
+    """Codec training (Section III-C; category-batched, Section III-G): one
+    step = loss and straight-through gradient of a mini-batch of chunks drawn
+    from the 36-layer Qwen3-8B-shaped q_proj category (bf16, 75.5 M chunks at
+    d = 8) plus one Adam step; indices drawn before the timed region."""
+    import numpy as np
+    h = b
+    cfg = bsq.Config(d=d, codebook_bits=b, hidden=h, encoder=bsq.ENC_LINEAR, stages=1)
+    hp = bsq.TrainHyper(lr=2e-3)
+    W, _ = synth.weight(4096, 4096, seed=77, dtype=torch.bfloat16, device=dev, n_mats=36)
+    n_total = W.numel() // d
+    dec = synth.decoder_params(synth.DEC_MLP, d, b, h, 1, seed=78, encoder=True)[0]
+    theta = torch.from_numpy(np.concatenate([np.ravel(v) for v in (dec.E, dec.W1, dec.b1, dec.W2, dec.b2)])
+                             .astype(np.float32)).to(dev)
+    P = theta.numel()
+    m, v = torch.zeros(P, device=dev), torch.zeros(P, device=dev)
+    grad, loss = torch.empty(P, device=dev), torch.empty(4, device=dev)
+    ws = torch.empty(bsq.bsq_train_workspace_bytes(cfg, batch) + 256, dtype=torch.uint8, device=dev)
+    ws = ws[(-ws.data_ptr()) % 256:]
+    gen = torch.Generator(device=dev).manual_seed(79)
+    idx = torch.randint(0, n_total, (steps + 4, batch), generator=gen, device=dev, dtype=torch.int64)
+    losses = []
+
+    def step(k):
+        bsq.bsq_train_grad(cfg, hp, W, theta, idx=idx[k], grad=grad, loss=loss, ws=ws)
+        bsq.bsq_train_adam(cfg, hp, k + 1, theta, grad, m, v)
+
+    for k in range(4):
+        step(k)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    first = None
+    e0.record()
+    for k in range(4, steps + 4):
+        step(k)
+        if k == 4:
+            first = loss.clone()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    out = {"d": d, "b": b, "h": h, "batch_chunks": batch, "category_chunks": n_total, "ms_per_step": round(ms, 4),
+           "mchunks_per_s": round(batch / ms / 1e3, 1), "loss_first": round(float(first[0]), 5),
+           "loss_last": round(float(loss[0]), 5)}
+    log(f"[bench] codec training d={d} b={b}: {ms * 1e3:.1f} us per step of {batch} chunks "
+        f"({out['mchunks_per_s']} M chunks/s), loss {out['loss_first']} -> {out['loss_last']}")
+    del W
+    torch.cuda.empty_cache()
+    return out
+
+
 def tiny_latency(bsq, synth, torch, dev):
     """The 256x256 fp32 layer (d = 8, no protection): GPU time of one encode,
     one fp32 decode and one fp32 GEMV, each by graph replay."""
@@ -483,6 +533,13 @@ def cpu_baseline(blk, bsq, torch):
            "tiny_encode_us": round(ete / rte * 1e6, 1), "tiny_decode_us": round(etd / rtd * 1e6, 1),
            "tiny_gemv_us": round(etg / rtg * 1e6, 1),
            "cpu_model": model, "affinity_cores": len(os.sched_getaffinity(0))}
+    # one codec-training step (loss and gradient, fp64 numpy) on 65536 chunks
+    import oracle.train as OT
+    tdec = synth.decoder_params(synth.DEC_MLP, 8, 8, 8, 1, seed=9, encoder=True)[0]
+    th = OT.pack(tdec.E, tdec.W1, tdec.b1, tdec.W2, tdec.b2)
+    Xc = Wf.reshape(-1, 8)[:65536]
+    rt, et = rate(lambda: OT.loss_and_grad(th, Xc, 8, 8, 8, OT.Hyper()), 2.0)
+    res["train_step_mchunks_per_s"] = round(rt * 65536 / et / 1e6, 3)
     log(f"[bench] cpu oracle: encode {res['encode_mchunks_per_s']} Mchunks/s, decode {res['decode_gbs']} GB/s; "
         f"tiny encode {res['tiny_encode_us']} us, decode {res['tiny_decode_us']} us, gemv {res['tiny_gemv_us']} us")
     return res
@@ -637,6 +694,7 @@ def main():
     line["gemm"] = gemm
     line["comparator"] = comp
     line["variants"] = variants(bsq, synth, torch, dev, s)
+    line["codec_training"] = {f"d{dd}_b{bb}": training(bsq, synth, torch, dev, dd, bb) for dd, bb in ((8, 8), (8, 16))}
     line["tiny"] = tiny_latency(bsq, synth, torch, dev)
     line["copy_reference_gbs"] = round(copy_reference(torch, dev), 1)
     if "cpu_baseline" not in line:

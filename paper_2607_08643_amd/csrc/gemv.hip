@@ -1038,10 +1038,15 @@ __global__ __launch_bounds__(256) void gemv_f32_kernel(const GemvArgs a)
     float acc = 0.0f;
     for (int64_t c = lane; c < C; c += 64) {
         float xv[D];
+        // protected inputs of the chunk: from the bitmap when the layer has
+        // one (one word per chunk, D divides 32), else by search of the list
+        uint32_t pm = 0;
+        if (a.k > 0 && M.bits) pm = (M.bits[(c * D) >> 5] >> ((c * D) & 31)) & uint32_t((uint64_t(1) << D) - 1u);
 #pragma unroll
         for (int j = 0; j < D; ++j) {
             const int64_t col = c * D + j;
-            xv[j] = (a.k > 0 && is_protected(M.idx, a.k, col)) ? 0.0f : load_x(a.x, col, a.x_bf16);
+            const bool prot = M.bits ? ((pm >> j) & 1u) : (a.k > 0 && is_protected(M.idx, a.k, col));
+            xv[j] = prot ? 0.0f : load_x(a.x, col, a.x_bf16);
         }
         const int64_t off = tile_index(row, c, a.pitch);
 #pragma unroll

@@ -27,7 +27,7 @@ namespace bsq {
 namespace {
 
 constexpr int TB = 256;        // threads per block in the per-chunk kernels
-constexpr int PG = 64;         // chunk groups of the parameter reduction
+constexpr int PG = 512;        // chunk groups of the parameter reduction
 
 struct TrainArgs {
     const void *x;             // chunks [n_total][d], fp32 or bf16
