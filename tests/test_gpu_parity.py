@@ -223,7 +223,7 @@ GEMM_CASES = [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11], SMALL[14], SMAL
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[c[0] for c in GEMM_CASES])
-@pytest.mark.parametrize("M", [1, 5, 16, 64, 100, 256])
+@pytest.mark.parametrize("M", [1, 5, 16, 20, 40, 64, 100, 256])
 def test_gemm_matches_oracle(case, M, gpu):
     say(f"case {case[0]} M={M}")
     cfg, decs, codec, layer, W, encs, tabs = _make(*case, gpu)
@@ -427,8 +427,8 @@ def test_full_size_encode_and_gemv(case, gpu):
 @pytest.mark.parametrize("d", [8, 16])
 def test_full_size_gemm(d, M, gpu):
     """Qwen3-8B o_proj shape at the batched sizes of the workload, with the
-    rank-16 LoRA (M = 16 runs the streaming small-M kernel at d = 8, the
-    others the tiled one)."""
+    rank-16 LoRA (at d = 8, M = 16 and 64 run the streaming kernel with one
+    and four token groups, M = 256 the tiled one)."""
     say(f"qwen3-8b o_proj 4096x4096 gemm M={M} d={d}")
     cfg = bsq.Config(d=d, hidden=d)
     oc = ocfg(cfg)

@@ -89,8 +89,8 @@ def test_gemv_wait_give_up_poisons_workspace(d, gpu):
 @pytest.mark.parametrize("d,M", [(8, 16), (8, 64), (16, 64)])
 def test_gemm_wait_give_up_poisons_workspace(d, M, gpu):
     # 256 rows x 4096 inputs: the K range of every output tile is split over
-    # several workgroups (M = 16 at d = 8: the streaming kernel's slices;
-    # otherwise the tiled kernel's split-K blocks)
+    # several workgroups (d = 8: the streaming kernel's slices, with one and
+    # four token groups; d = 16: the tiled kernel's split-K blocks)
     say(f"gemm forced wait give-up d={d} M={M}")
     cfg, codec, layer = _layer(d, 256, 4096, gpu, seed=7)
     X = synth.activation(4096, seed=8, device=gpu, batch=M)
