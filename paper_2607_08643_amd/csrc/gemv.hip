@@ -110,7 +110,12 @@ struct GemvMat {
 };
 
 struct GemvArgs {
-    GemvMat mat[BSQ_MAX_GROUP];
+    // first block of each member in the row-lane kernel's tile grid (INT32_MAX
+    // past the last member), the LoRA workgroups ahead of them, and the tile
+    // counts: what every workgroup reads first, together, at the front of the
+    // arguments (one batch of scalar loads before the member's own fields)
+    int32_t bb[BSQ_MAX_GROUP];
+    int32_t lora_blocks32;
     int n, stages;
     int64_t d_in, pitch, k, nseg, rs, rpb;
     int64_t nblk, q;   // row-lane kernel: 16-chunk blocks per row, slices per 64-row group
@@ -123,6 +128,7 @@ struct GemvArgs {
     int32_t *err;      // caller's device error word, or null
     int spin_limit;    // polls before a wait gives up (wait_limit())
     int pfmt;          // bsq_prot_format of the protected payload
+    GemvMat mat[BSQ_MAX_GROUP];
 };
 
 __device__ __forceinline__ float load_x(const void *x, int64_t j, int bf)
@@ -426,15 +432,22 @@ struct LaneBlk {
     uint4 g[S][2];      // 16 fp16 gains
 };
 
+// The member's plane pointers, read from the kernel arguments once.
+template <int S>
+struct LanePlanes {
+    const uint8_t *codes[S];
+    const uint16_t *gains[S];
+};
+
 template <int D, int S>
-__device__ __forceinline__ void lane_load(LaneBlk<D, S> &b, const GemvMat &M, int64_t off)
+__device__ __forceinline__ void lane_load(LaneBlk<D, S> &b, const LanePlanes<S> &P, int64_t off)
 {
 #pragma unroll
     for (int s = 0; s < S; ++s) {
-        const uint4 *cp = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(M.codes[s]) + off * (D / 8));
+        const uint4 *cp = reinterpret_cast<const uint4 *>(P.codes[s] + off * (D / 8));
 #pragma unroll
         for (int h = 0; h < D / 8; ++h) b.c[s][h] = cp[h];
-        const uint4 *gp = reinterpret_cast<const uint4 *>(M.gains[s] + off);
+        const uint4 *gp = reinterpret_cast<const uint4 *>(P.gains[s] + off);
         b.g[s][0] = gp[0];
         b.g[s][1] = gp[1];
     }
@@ -814,17 +827,66 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     const int t = threadIdx.x, lane = t & 63;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
 
-    if (int64_t(blockIdx.x) < a.lora_blocks) {  // the LoRA vectors, ahead of every tile
+    // The kernel arguments reach the workgroup by scalar loads whose round
+    // trips would add up if each waited for the one before: the member comes
+    // from the first blocks of all members (one batch of loads), then the
+    // member's pointers that the prologue needs are read together (a second
+    // batch), each batch forced to complete at once by an empty asm that
+    // takes the values.
+    const int32_t bid = int32_t(blockIdx.x) - a.lora_blocks32;
+    int m = 0;
+    int32_t bbm = 0;  // the member's first block (a.bb[m], selected, not reloaded)
+#pragma unroll
+    for (int i = 1; i < BSQ_MAX_GROUP; ++i) {
+        const int32_t bbi = a.bb[i];
+        m += (bid >= bbi) ? 1 : 0;
+        bbm = (bid >= bbi) ? bbi : bbm;
+    }
+    {
+        const int64_t nb_ = a.nblk, q_ = a.q, k_ = a.k, din_ = a.d_in;
+        const void *x_ = a.x;
+        asm volatile("" ::"s"(m), "s"(nb_), "s"(q_), "s"(k_), "s"(din_), "s"(x_));
+    }
+    if (bid < 0) {  // the LoRA vectors, ahead of every tile
         lane_lora_block(a, reinterpret_cast<float *>(s_mem));
         return;
     }
-    const int64_t bid = int64_t(blockIdx.x) - a.lora_blocks;
-    int m = 0;
-    while (m + 1 < a.n && bid >= a.mat[m + 1].block_begin) ++m;
     const GemvMat &M = a.mat[m];
+    LanePlanes<S> PL;
+#pragma unroll
+    for (int s = 0; s < S; ++s) {
+        PL.codes[s] = static_cast<const uint8_t *>(M.codes[s]);
+        PL.gains[s] = M.gains[s];
+    }
+    const uint4 *tabp[S];
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+        tabp[s] = (D == 8) ? reinterpret_cast<const uint4 *>(M.tab16[s]) : reinterpret_cast<const uint4 *>(M.split[s]);
+    const int8_t *q8p = M.q8;
+    const int32_t *idxp = M.idx;
+    const float *scalep = M.scale;
+    const int64_t d_out_m = M.d_out;
+    asm volatile("" ::"s"(PL.codes[0]), "s"(PL.gains[0]), "s"(tabp[0]), "s"(q8p), "s"(idxp), "s"(scalep),
+                 "s"(d_out_m));
+    if constexpr (S > 1) asm volatile("" ::"s"(PL.codes[S - 1]), "s"(PL.gains[S - 1]), "s"(tabp[S - 1]));
+    // Prologue in a fixed issue order (vector-memory completions are counted
+    // in order): the decoder table straight to LDS by DMA
+    // (global_load_lds_dwordx4, 64 entries per wave instruction), then the
+    // first tiles, so that the wait before the barrier covers the table but
+    // not the tiles. Tile indices are clamped so every load is in bounds and
+    // unconditional (a wave without tiles reloads its row group's first tile).
+    // The table goes first, before the workgroup's index arithmetic.
+    static_assert(TAB % NT == 0, "table chunks are shared out evenly");
+#pragma unroll
+    for (int r = 0; r < TAB / NT; ++r) {
+        const int c = r * WV + wave;  // 1 KiB chunk of the table: 64 lanes x 16 B
+        const uint4 *src = (D == 8) ? tabp[c >> 2] + (c & 3) * 64 + lane : tabp[c >> 4] + (c & 15) * 64 + lane;
+        __builtin_amdgcn_global_load_lds(src, s_tab + c * 64, 16, 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     const int64_t nblk = a.nblk, Q = a.q;
-    const int64_t unit = bid - M.block_begin;  // row group * Q + slice
-    const int64_t rg = unit / Q, q = unit - rg * Q;
+    const int32_t unit = bid - bbm;  // row group * Q + slice
+    const int64_t rg = uint32_t(unit) / uint32_t(Q), q = unit - rg * Q;
     const int64_t tbase = ((rg * nblk) << 10) + (int64_t(lane) << 4);
     // this wave's tiles [b0, b1); those whose 128 columns are all real go
     // through the pipelined loop, a ragged last tile of the row (d_in not a
@@ -834,27 +896,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // (floor or ceil of nblk / (Q WV) each, at most TPW), in order, so no wave
     // is left idle while another carries a whole extra tile set
     const int64_t nw = Q * WV, wq = q * WV + wave;
-    const int64_t b0 = (wq * nblk) / nw;
-    const int64_t b1 = ((wq + 1) * nblk) / nw;
-    const int64_t sb0 = (q * nblk) / Q;  // the slice's first block (wave 0's b0)
+    const int64_t b0 = uint32_t(wq * nblk) / uint32_t(nw);  // (products below 2^31: checked at launch)
+    const int64_t b1 = uint32_t((wq + 1) * nblk) / uint32_t(nw);
+    const int64_t sb0 = uint32_t(q * nblk) / uint32_t(Q);  // the slice's first block (wave 0's b0)
     const int64_t nt = ((b1 < full_blocks) ? b1 : full_blocks) - b0;  // may be <= 0
     const bool ragged = b0 <= full_blocks && full_blocks < b1;
     const bool fin = q == Q - 1;  // this slice finishes the row group
 
-    // Prologue in a fixed issue order (vector-memory completions are counted
-    // in order): the decoder table straight to LDS by DMA
-    // (global_load_lds_dwordx4, 64 entries per wave instruction), then the
-    // first tiles, so that the wait before the barrier covers the table but
-    // not the tiles. Tile indices are clamped so every load is in bounds and
-    // unconditional (a wave without tiles reloads its row group's first tile).
-    static_assert(TAB % NT == 0, "table chunks are shared out evenly");
-#pragma unroll
-    for (int r = 0; r < TAB / NT; ++r) {
-        const int c = r * WV + wave;  // 1 KiB chunk of the table: 64 lanes x 16 B
-        const uint4 *src = (D == 8) ? reinterpret_cast<const uint4 *>(M.tab16[c >> 2]) + (c & 3) * 64 + lane
-                                    : reinterpret_cast<const uint4 *>(M.split[c >> 4]) + (c & 15) * 64 + lane;
-        __builtin_amdgcn_global_load_lds(src, s_tab + c * 64, 16, 0, 0);
-    }
     if constexpr (D == 16) {
         // the slice's records, 16 per wave instruction (four lanes per 64-byte
         // slot); chunks past the row's padded end read the last slot (unused)
@@ -873,8 +921,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     // the finishing slice brings its row group's int8 rows to LDS the same way
     // (rows past d_out get clamped copies and are never read)
     if (fin && a.k > 0 && q8_lds) {
-        const int8_t *src = M.q8 + rg * 64 * kp;
-        const int64_t avail = ((M.d_out - rg * 64 < 64) ? M.d_out - rg * 64 : 64) * kp;
+        const int8_t *src = q8p + rg * 64 * kp;
+        const int64_t avail = ((d_out_m - rg * 64 < 64) ? d_out_m - rg * 64 : 64) * kp;
         for (int64_t o = int64_t(wave) * 1024; o < 64 * kp; o += WV * 1024) {
             const int64_t e = o + lane * 16;
             const int64_t es = (e < avail) ? e : avail - 16;
@@ -887,14 +935,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
     const int64_t blast = (nt > 0) ? b0 + nt - 1 : sb0;
     LaneBlk<D, S> buf[PF];
 #pragma unroll
-    for (int u = 0; u < PF; ++u) lane_load<D, S>(buf[u], M, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
+    for (int u = 0; u < PF; ++u) lane_load<D, S>(buf[u], PL, tbase + (((b0 + u < blast) ? b0 + u : blast) << 10));
     __builtin_amdgcn_sched_barrier(0);
     // protected index and scale of this thread's column, used at the end
     // (unconditional loads, so that every path has the same loads in flight;
     // with no protected columns they read x and are ignored)
     const int64_t pt = (a.k > 0) ? ((t < a.k) ? t : a.k - 1) : 0;
-    const int32_t pj_raw = ((a.k > 0) ? M.idx : static_cast<const int32_t *>(a.x))[pt];
-    const float psc = ((a.k > 0) ? M.scale : static_cast<const float *>(a.x))[pt];
+    const int32_t pj_raw = ((a.k > 0) ? idxp : static_cast<const int32_t *>(a.x))[pt];
+    const float psc = ((a.k > 0) ? scalep : static_cast<const float *>(a.x))[pt];
     const int32_t pj = (a.k > 0) ? pj_raw : -1;
     // the workspace's poison word, read by the finishing slice before it
     // consumes any slot (unconditional, like the loads above)
@@ -924,12 +972,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
             else acc += lane_tile16<S>(buf[u % PF], s_rec, RCH, int(b - sb0), s_tab, 0.0f);
         }
         if (u + PF < TPW)
-            lane_load<D, S>(buf[u % PF], M, tbase + (((b0 + u + PF < blast) ? b0 + u + PF : blast) << 10));
+            lane_load<D, S>(buf[u % PF], PL, tbase + (((b0 + u + PF < blast) ? b0 + u + PF : blast) << 10));
     }
     if constexpr (D == 8) {
         if (ragged) {
             const int64_t b = full_blocks;
-            lane_load<D, S>(buf[0], M, tbase + (b << 10));
+            lane_load<D, S>(buf[0], PL, tbase + (b << 10));
             acc = lane_tile_ragged<S>(buf[0], static_cast<const uint32_t *>(a.x), a.d_in, bsrc, kmask, b, s_tab,
                                       acc);
         }
@@ -1272,6 +1320,9 @@ hipError_t launch_gemv_run(const bsq_config &cfg, int n, const void *const *code
         }
         a.lora_blocks = lora_blocks;
         blocks += lora_blocks;
+        if (blocks > INT32_MAX || a.q * 4 * a.nblk > INT32_MAX) return hipErrorInvalidConfiguration;
+        a.lora_blocks32 = int32_t(lora_blocks);
+        for (int m = 0; m < BSQ_MAX_GROUP; ++m) a.bb[m] = (m < n) ? int32_t(a.mat[m].block_begin) : INT32_MAX;
         const int64_t kp = q8_pitch(a.k);
         // dynamic LDS: the d = 16 records, wave sums, scaled protected
         // activations, the finishing slice's int8 rows (the table is static)
