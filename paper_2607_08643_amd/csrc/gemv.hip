@@ -508,53 +508,53 @@ __device__ __forceinline__ float q8_block(uint4 qv, const float *xs, float acc, 
     return q8_block_t<BSQ_PROT_INT8>(qv, xs, acc);
 }
 
-// The int8 protected columns of one row (row < d_out) added to acc, the
-// row's int8 codes read from global memory: four 16-byte words at a time,
-// all issued before any is used (indices clamped to the padded row, words
-// past it zeroed), then one word after the other.
+// The protected columns of 16-column words w0, w0 + step, ... of one row
+// (row < d_out) added to acc, the row's stored bytes read from global
+// memory: four words at a time, all issued before any is used (indices
+// clamped to the padded row, words past it zeroed), then one after the other.
 __device__ __forceinline__ float lane_q8_global(const GemvArgs &a, const GemvMat &M, const float *s_xs, int64_t row,
-                                                float acc)
+                                                int64_t w0, int64_t step, float acc)
 {
     const int64_t nw = q8_pitch(a.k) / 16;  // 16-byte words per row
     const uint4 *qr = reinterpret_cast<const uint4 *>(M.q8 + row * q8_pitch(a.k));
-    for (int64_t w0 = 0; w0 < nw; w0 += 4) {
+    for (int64_t w = w0; w < nw; w += 4 * step) {
         uint4 qv[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) qv[u] = qr[(w0 + u < nw) ? w0 + u : nw - 1];
+        for (int u = 0; u < 4; ++u) qv[u] = qr[(w + u * step < nw) ? w + u * step : nw - 1];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const uint4 q = (w0 + u < nw) ? qv[u] : make_uint4(0, 0, 0, 0);
-            acc = q8_block(q, s_xs + 16 * ((w0 + u < nw) ? w0 + u : nw - 1), acc, a.pfmt);
+            const int64_t wu = w + u * step;
+            const uint4 q = (wu < nw) ? qv[u] : make_uint4(0, 0, 0, 0);
+            acc = q8_block(q, s_xs + 16 * ((wu < nw) ? wu : nw - 1), acc, a.pfmt);
             asm volatile("" : "+v"(acc));  // one word's activations live at a time
         }
     }
     return acc;
 }
 
-// The terms of one row (row < d_out) that do not come from the codes: the
-// int8 protected columns, with the row's codes in LDS (s_q8 [64][kp], this
-// lane's row at lane * kp) or else in global memory, then the LoRA term;
-// added to acc in that order.
-__device__ __forceinline__ float lane_extras(const GemvArgs &a, const GemvMat &M, const float *s_xs,
-                                             const int8_t *s_q8, bool q8_lds, int64_t row, float acc,
-                                             const float (&tv)[BSQ_MAX_LORA_RANK])
+// The protected columns of words w0, w0 + step, ... of one row (row <
+// d_out), with the row's stored bytes in LDS (s_q8 [64][kp], this lane's row
+// at (row % 64) kp) or else in global memory, added to acc in word order.
+__device__ __forceinline__ float lane_q8_term(const GemvArgs &a, const GemvMat &M, const float *s_xs,
+                                              const int8_t *s_q8, bool q8_lds, int64_t row, int64_t w0, int64_t step,
+                                              float acc)
 {
     if (a.k > 0) {
         if (q8_lds) {
             const int64_t nw = q8_pitch(a.k) / 16;
             const uint4 *qr = reinterpret_cast<const uint4 *>(s_q8 + (row & 63) * q8_pitch(a.k));
-            int64_t w = 0;
-            for (; w + 2 <= nw; w += 2) {  // two words per step, their LDS reads together
-                const uint4 q0 = qr[w], q1 = qr[w + 1];
+            int64_t w = w0;
+            for (; w + step < nw; w += 2 * step) {  // two words per step, their LDS reads together
+                const uint4 q0 = qr[w], q1 = qr[w + step];
                 acc = q8_block(q0, s_xs + 16 * w, acc, a.pfmt);
-                acc = q8_block(q1, s_xs + 16 * (w + 1), acc, a.pfmt);
+                acc = q8_block(q1, s_xs + 16 * (w + step), acc, a.pfmt);
             }
             if (w < nw) acc = q8_block(qr[w], s_xs + 16 * w, acc, a.pfmt);
         } else {
-            acc = lane_q8_global(a, M, s_xs, row, acc);
+            acc = lane_q8_global(a, M, s_xs, row, w0, step, acc);
         }
     }
-    return lane_lora_term(M, row, acc, tv);
+    return acc;
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -983,14 +983,19 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
         }
     }
 
-    // scaled protected activations for the epilogue (indices loaded above),
-    // only in the finishing slice
-    if (fin) {
+    // the finishing slice's protected columns: the scaled activations to LDS
+    // (indices loaded above), then each wave adds every fourth 16-column
+    // word of its lane's row to its own sum (the four shares are added with
+    // the wave sums, in wave order), off the finishing wave's serial path
+    if (fin && a.k > 0) {
         if (t < kp) s_xs[t] = (t < a.k && pj >= 0 && pj < a.d_in) ? psc * load_x(a.x, pj, 1) : 0.0f;
         for (int64_t p = NT + t; p < kp; p += NT) {  // more protected columns than threads
             const int32_t j = (p < a.k) ? M.idx[p] : -1;
             s_xs[p] = (j >= 0 && j < a.d_in) ? M.scale[p] * load_x(a.x, j, 1) : 0.0f;
         }
+        __syncthreads();
+        const int64_t row_w = rg * 64 + lane;
+        if (row_w < M.d_out) acc = lane_q8_term(a, M, s_xs, s_q8, q8_lds, row_w, wave, WV, acc);
     }
     // the four wave sums of each row, in wave order
     s_red[wave * 64 + lane] = acc;
@@ -1014,12 +1019,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(S <= 2 ? 4 
         if (row < M.d_out) lane_store(a, M, row, __builtin_nanf(""));
         return;
     }
-    // the finishing slice adds the protected and LoRA terms to its own sum
-    // first: they do not depend on the other slices, so this work overlaps
-    // the wait for them
+    // the finishing slice adds the LoRA term to its own sum (and protected
+    // shares) first: it does not depend on the other slices, so this work
+    // overlaps the wait for them
     float tv[BSQ_MAX_LORA_RANK];
     const bool ok = lane_lora_vector(a, M, rg, tv);
-    if (row < M.d_out) v = lane_extras(a, M, s_xs, s_q8, q8_lds, row, v, tv);
+    if (row < M.d_out) v = lane_lora_term(M, row, v, tv);
     float tot = 0.0f;
     bool timed_out = false;
     // the other slices' slots, eight at a time, all eight loads in flight
