@@ -429,6 +429,7 @@ struct EncodeArgs {
     int8_t *q8;
     const float *scale;
     const int32_t *colmap;
+    const int32_t *idx;  // protected columns [n_mats][k] (the payload pass)
     const uint32_t *bitmap;
     int32_t *err;
     int pfmt;  // bsq_prot_format of q8
@@ -439,7 +440,11 @@ struct EncodeArgs {
 // matrix m, row i, chunk c, at plane position gid. D inputs per chunk, B code
 // bits; ENC: the stage code is the sign pattern of z = E r (E [B][D] in LDS,
 // s_E), else of r itself (B = D). The decoder table is in LDS (s_tab) for
-// D = B = 8, else read from the fp32 table in global memory.
+// D = B = 8, as [S][2][256][4] (the two halves of an entry 4 KiB apart, so
+// that each 16-byte read of a wave spreads over the banks by the code), else
+// read from the fp32 table in global memory. The protected columns of the
+// chunk are masked out of the stages (their payload bytes are written by the
+// kernel's separate payload pass).
 template <int D, int B, int S, typename T, bool ENC>
 __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, const float *s_E,
                                                int64_t m, int64_t i, int64_t c, int64_t gid)
@@ -477,25 +482,11 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
     for (int j = 0; j < D; ++j) finite &= __builtin_isfinite(w[j]);
     if (!finite) atomicOr(a.err, int32_t(BSQ_DEVERR_NONFINITE));
 
-    // zero padding of the row's int8 payload
-    if (c == 0) {
-        for (int64_t p = a.k; p < q8_pitch(a.k); ++p) a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p] = 0;
-    }
-    // protected positions of this chunk: Q8 payload, then masked out of BSQ
+    // protected positions of this chunk, masked out of BSQ
     uint32_t pm = 0;
     if (a.bitmap) {
         const int64_t col0 = c * D;
         pm = (a.bitmap[m * a.words + (col0 >> 5)] >> (col0 & 31)) & ((1u << D) - 1u);
-        if (pm) {
-#pragma unroll
-            for (int j = 0; j < D; ++j) {
-                if (!((pm >> j) & 1u)) continue;
-                const int32_t p = a.colmap[m * a.d_in + col0 + j];
-                const float sc = a.scale[m * a.k + p];
-                a.q8[(m * a.d_out + i) * q8_pitch(a.k) + p] =
-                    (sc != 0.0f) ? int8_t(payload_from_f32(w[j] / sc, a.pfmt)) : int8_t(0);
-            }
-        }
     }
     float r[D];
 #pragma unroll
@@ -517,25 +508,34 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
 #pragma unroll
             for (int j = 0; j < D; ++j) code |= (r[j] >= 0.0f ? 1u : 0u) << j;
         }
-        const float *y = TAB_LDS ? (s_tab + (s * 256 + code) * 8) : (a.tab32[s] + size_t(code) * D);
         float yv[D];
-        if constexpr (D == 8) {
+        if constexpr (TAB_LDS) {
+            const float4 *y4 = reinterpret_cast<const float4 *>(s_tab) + s * 512 + code;
+            float4 lo = y4[0], hi = y4[256];
+            yv[0] = lo.x; yv[1] = lo.y; yv[2] = lo.z; yv[3] = lo.w;
+            yv[4] = hi.x; yv[5] = hi.y; yv[6] = hi.z; yv[7] = hi.w;
+        } else if constexpr (D == 8) {
+            const float *y = a.tab32[s] + size_t(code) * D;
             const float4 *y4 = reinterpret_cast<const float4 *>(y);
             float4 lo = y4[0], hi = y4[1];
             yv[0] = lo.x; yv[1] = lo.y; yv[2] = lo.z; yv[3] = lo.w;
             yv[4] = hi.x; yv[5] = hi.y; yv[6] = hi.z; yv[7] = hi.w;
         } else {
-            const float4 *y4 = reinterpret_cast<const float4 *>(y);
+            const float4 *y4 = reinterpret_cast<const float4 *>(a.tab32[s] + size_t(code) * D);
 #pragma unroll
             for (int v = 0; v < D / 4; ++v) {
                 float4 q = y4[v];
                 yv[4 * v + 0] = q.x; yv[4 * v + 1] = q.y; yv[4 * v + 2] = q.z; yv[4 * v + 3] = q.w;
             }
         }
+        // protected positions take y = +0 (their r is +0): each of their terms
+        // then adds an exact +0 to a sum that is never -0, and leaves r at +0,
+        // the same as skipping them
+#pragma unroll
+        for (int j = 0; j < D; ++j) yv[j] = ((pm >> j) & 1u) ? 0.0f : yv[j];
         float num = 0.0f, den = 0.0f;
 #pragma unroll
         for (int j = 0; j < D; ++j) {
-            if ((pm >> j) & 1u) continue;
             num = __builtin_fmaf(r[j], yv[j], num);
             den = __builtin_fmaf(yv[j], yv[j], den);
         }
@@ -544,10 +544,7 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
         const uint16_t gh = gain_to_f16(alpha);
         const float ga = f16_bits_to_f32(gh);
 #pragma unroll
-        for (int j = 0; j < D; ++j) {
-            if ((pm >> j) & 1u) continue;
-            r[j] = __builtin_fmaf(-ga, yv[j], r[j]);
-        }
+        for (int j = 0; j < D; ++j) r[j] = __builtin_fmaf(-ga, yv[j], r[j]);
         static_cast<code_t *>(a.codes[s])[gid] = code_t(code);
         a.gains[s][gid] = gh;
     }
@@ -565,9 +562,10 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
     constexpr bool TAB_LDS = (D == 8 && B == 8);
     float *s_E = s_tab + (TAB_LDS ? S * 256 * 8 : 0);
     if constexpr (TAB_LDS) {
+        // entry c of stage s: floats 0-3 at float4 (s 512 + c), 4-7 at (s 512 + 256 + c)
         for (int e = threadIdx.x; e < S * 256 * 8; e += blockDim.x) {
-            int s = e / (256 * 8), r = e - s * 256 * 8;
-            s_tab[e] = a.tab32[s][r];
+            const int s = e / (256 * 8), r = e - s * 256 * 8, code = r >> 3, f = r & 7;
+            s_tab[((s * 512 + (f >> 2) * 256 + code) << 2) + (f & 3)] = a.tab32[s][r];
         }
     }
     if constexpr (ENC) {
@@ -588,6 +586,36 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
         for (int q = 0; q < 4; ++q) {
             const int e = q * 256 + int(threadIdx.x);
             encode_element<D, B, S, T, ENC>(a, s_tab, s_E, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), (tile << 10) + e);
+        }
+    }
+    // the payload pass: four bytes of a padded payload row per thread, each
+    // byte the protected weight over its column's scale in the payload
+    // format (zero past k, and where the scale is zero)
+    if (a.q8 && a.k > 0) {
+        const int64_t kp = q8_pitch(a.k), kp4 = kp >> 2;
+        const int64_t n4 = (a.total / plane_elems(a.d_out, a.pitch)) * a.d_out * kp4;
+        for (int64_t e = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; e < n4; e += int64_t(gridDim.x) * blockDim.x) {
+            const int64_t mi = e / kp4, p0 = (e - mi * kp4) << 2;  // mi = m d_out + i
+            const int64_t m = mi / a.d_out;
+            uint32_t word = 0;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const int64_t p = p0 + u;
+                if (p >= a.k) break;
+                // (a rejected given set leaves entries of the index list
+                // unwritten: any index out of range reads as column 0, and
+                // the call reports the set)
+                int32_t col = a.idx[m * a.k + p];
+                col = (col >= 0 && col < a.d_in) ? col : 0;
+                const float sc = a.scale[m * a.k + p];
+                const T wv = static_cast<const T *>(a.W)[mi * a.d_in + col];
+                float w;
+                if constexpr (sizeof(T) == 4) w = wv;
+                else w = bf16_to_f32(wv);
+                const uint32_t b = (sc != 0.0f) ? uint32_t(uint8_t(payload_from_f32(w / sc, a.pfmt))) : 0u;
+                word |= b << (8 * u);
+            }
+            reinterpret_cast<uint32_t *>(a.q8)[e] = word;
         }
     }
 }
@@ -755,6 +783,7 @@ hipError_t launch_encode(const bsq_config &cfg, const void *codec, const void *W
     a.q8 = rows ? nullptr : out.prot_q8;
     a.scale = out.prot_scale;
     a.colmap = ws.colmap;
+    a.idx = out.prot_idx;
     a.bitmap = (k > 0 && !rows) ? out.prot_bits : nullptr;
     a.err = err;
     a.pfmt = cfg.protect_format;
