@@ -445,9 +445,30 @@ struct EncodeArgs {
 // read from the fp32 table in global memory. The protected columns of the
 // chunk are masked out of the stages (their payload bytes are written by the
 // kernel's separate payload pass).
+// The raw words of one chunk and its protected-position mask, fetched ahead
+// of the chunk's arithmetic (a thread's four chunks of a tile are requested
+// together, so that their loads are in flight at once).
+template <int D, typename T>
+struct ChunkIn {
+    static constexpr int NV = D * int(sizeof(T)) / 16;
+    uint4 raw[NV];
+    uint32_t pmw;  // the bitmap word of the chunk's columns (shifted and masked where used)
+};
+
+template <int D, typename T>
+__device__ __forceinline__ void encode_fetch(const EncodeArgs &a, int64_t m, int64_t i, int64_t c, ChunkIn<D, T> &in)
+{
+    in.pmw = 0;
+    if (c >= a.C || i >= a.d_out) return;
+    const T *src = static_cast<const T *>(a.W) + (m * a.d_out + i) * a.d_in + c * D;
+#pragma unroll
+    for (int v = 0; v < ChunkIn<D, T>::NV; ++v) in.raw[v] = reinterpret_cast<const uint4 *>(src)[v];
+    if (a.bitmap) in.pmw = a.bitmap[m * a.words + ((c * D) >> 5)];
+}
+
 template <int D, int B, int S, typename T, bool ENC>
 __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float *s_tab, const float *s_E,
-                                               int64_t m, int64_t i, int64_t c, int64_t gid)
+                                               int64_t m, int64_t i, int64_t c, int64_t gid, const ChunkIn<D, T> &in)
 {
     using code_t = typename std::conditional<B == 8, uint8_t, uint16_t>::type;
     constexpr bool TAB_LDS = (D == 8 && B == 8);
@@ -461,19 +482,14 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
         return;
     }
 
-    // load the chunk
+    // the chunk
     float w[D];
-    const T *src = static_cast<const T *>(a.W) + (m * a.d_out + i) * a.d_in + c * D;
-    constexpr int NV = D * int(sizeof(T)) / 16;
-    uint4 raw[NV];
-#pragma unroll
-    for (int v = 0; v < NV; ++v) raw[v] = reinterpret_cast<const uint4 *>(src)[v];
     if constexpr (sizeof(T) == 4) {
-        const float *f = reinterpret_cast<const float *>(raw);
+        const float *f = reinterpret_cast<const float *>(in.raw);
 #pragma unroll
         for (int j = 0; j < D; ++j) w[j] = f[j];
     } else {
-        const uint16_t *h = reinterpret_cast<const uint16_t *>(raw);
+        const uint16_t *h = reinterpret_cast<const uint16_t *>(in.raw);
 #pragma unroll
         for (int j = 0; j < D; ++j) w[j] = bf16_to_f32(h[j]);
     }
@@ -483,11 +499,7 @@ __device__ __forceinline__ void encode_element(const EncodeArgs &a, const float 
     if (!finite) atomicOr(a.err, int32_t(BSQ_DEVERR_NONFINITE));
 
     // protected positions of this chunk, masked out of BSQ
-    uint32_t pm = 0;
-    if (a.bitmap) {
-        const int64_t col0 = c * D;
-        pm = (a.bitmap[m * a.words + (col0 >> 5)] >> (col0 & 31)) & ((1u << D) - 1u);
-    }
+    const uint32_t pm = (in.pmw >> ((c * D) & 31)) & ((1u << D) - 1u);
     float r[D];
 #pragma unroll
     for (int j = 0; j < D; ++j) r[j] = ((pm >> j) & 1u) ? 0.0f : w[j];
@@ -582,10 +594,17 @@ __global__ __launch_bounds__(256) void encode_kernel(EncodeArgs a)
         const int64_t m = tile / tiles_per_mat;
         const int64_t rem = tile - m * tiles_per_mat;
         const int64_t rg = rem / nb, blk = rem - rg * nb;
+        ChunkIn<D, T> in[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = q * 256 + int(threadIdx.x);
-            encode_element<D, B, S, T, ENC>(a, s_tab, s_E, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), (tile << 10) + e);
+            encode_fetch<D, T>(a, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), in[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = q * 256 + int(threadIdx.x);
+            encode_element<D, B, S, T, ENC>(a, s_tab, s_E, m, rg * 64 + (e >> 4), blk * 16 + (e & 15), (tile << 10) + e,
+                                            in[q]);
         }
     }
     // the payload pass: four bytes of a padded payload row per thread, each
