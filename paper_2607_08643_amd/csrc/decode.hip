@@ -26,13 +26,15 @@ struct DecodeArgs {
 };
 
 // A block walks the tiles of one matrix (grid-stride, so the decoder tables
-// and the protected-column metadata are set up once per block). Thread t
-// handles the four consecutive chunks 4 (t % 4) .. + 3 of row t / 4 of the
-// tile: one 4- or 8-byte code load and one 8-byte gain load per stage, and a
-// 64-byte (bf16, d = 8) run of W_hat per thread, 256 contiguous bytes per row
-// and wave. Tiles always lie inside the padded planes, so the loads of the
-// next tile are issued unconditionally while the current one is assembled;
-// only the stores check the row and chunk bounds.
+// and the protected-column metadata are set up once per block). The four
+// threads 4 r .. 4 r + 3 share row r of the tile: each loads the row's 16
+// codes and gains of every stage (the four lanes read the same words) and
+// assembles chunks t % 4 + 4 u, u = 0 .. 3, so that at each u the four lanes
+// write adjacent chunks (64 contiguous bytes of W_hat per row at d = 8 bf16)
+// and every store instruction of a wave fills whole runs. Tiles always lie
+// inside the padded planes, so the loads of the next tile are issued
+// unconditionally while the current one is assembled; only the stores check
+// the row and chunk bounds.
 //
 // Protected columns: the position p of column j in the ascending index list
 // is the number of protected columns before it, i.e. the rank of the first
@@ -43,7 +45,6 @@ struct DecodeArgs {
 template <int D, int B, int S, bool BF16OUT>
 __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 {
-    typedef typename std::conditional<B == 8, uint32_t, uint2>::type CodeWord;
     constexpr bool TAB_LDS = (D == 8 && B == 8);
     extern __shared__ uint32_t s_mem[];
     // [words4] protected bitmap, [words4] rank of each word's first protected
@@ -70,9 +71,12 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
         }
     }
     if constexpr (TAB_LDS) {
+        // entry c of stage s: floats 0-3 at float4 (s 512 + c), 4-7 at
+        // (s 512 + 256 + c): the two 16-byte reads of a wave spread over the
+        // banks by the code
         for (int e = t; e < S * 256 * 8; e += blockDim.x) {
-            int s = e / (256 * 8), r = e - s * 256 * 8;
-            s_tab[e] = a.tab32[s][r];
+            const int s = e / (256 * 8), r = e - s * 256 * 8, code = r >> 3, f = r & 7;
+            s_tab[((s * 512 + (f >> 2) * 256 + code) << 2) + (f & 3)] = a.tab32[s][r];
         }
     }
     __syncthreads();
@@ -80,26 +84,33 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
     const int64_t nb = a.pitch / 16;                 // tiles per 64-row group
     const int64_t tiles = (a.d_out + 63) / 64 * nb;  // tiles of this matrix
     const int64_t kp = q8_pitch(a.k);
-    const int64_t pbase = m * plane_elems(a.d_out, a.pitch) + 4 * t;
-    const int r = t >> 2, cc0 = 4 * (t & 3);  // row and first chunk within the tile
+    const int r = t >> 2, cl = t & 3;  // row within the tile, first chunk (chunks cl + 4 u)
+    const int64_t pbase = m * plane_elems(a.d_out, a.pitch) + 16 * r;
 
-    CodeWord code[2][S];
-    uint2 gain[2][S];
+    // the row's 16 codes (B / 8 16-byte words) and 16 gains (two words) per stage
+    uint4 code[2][S][B / 8];
+    uint4 gain[2][S][2];
     auto load = [&](int P, int64_t tile) {
         const int64_t e = pbase + tile * 1024;
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-            if constexpr (B == 8) code[P][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
-            else code[P][s] = *reinterpret_cast<const uint2 *>(static_cast<const uint16_t *>(a.codes[s]) + e);
-            gain[P][s] = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
+            const uint4 *cp = reinterpret_cast<const uint4 *>(static_cast<const uint8_t *>(a.codes[s]) + e * (B / 8));
+#pragma unroll
+            for (int h = 0; h < B / 8; ++h) code[P][s][h] = cp[h];
+            const uint4 *gp = reinterpret_cast<const uint4 *>(a.gains[s] + e);
+            gain[P][s][0] = gp[0];
+            gain[P][s][1] = gp[1];
         }
     };
+    // 32-bit word w of a 16-byte word
+    auto word = [](const uint4 &v, int w) { return (w == 0) ? v.x : (w == 1) ? v.y : (w == 2) ? v.z : v.w; };
     auto body = [&](int P, int64_t tile) {
         const int64_t rg = tile / nb, cb = tile - rg * nb;
         const int64_t i = rg * 64 + r;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-            const int64_t c = cb * 16 + cc0 + u;
+            const int cc = cl + 4 * u;  // chunk within the tile's row
+            const int64_t c = cb * 16 + cc;
             const int64_t o = (m * a.d_out + i) * a.d_in + c * D;
             const bool live = i < a.d_out && c < a.C;
             float v[D];
@@ -121,15 +132,14 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a)
 #pragma unroll
             for (int s = 0; s < S; ++s) {
                 uint32_t cw;
-                if constexpr (B == 8) cw = (code[P][s] >> (8 * u)) & 0xffu;
-                else cw = ((u < 2 ? code[P][s].x : code[P][s].y) >> (16 * (u & 1))) & 0xffffu;
-                const uint32_t gw = (u < 2) ? gain[P][s].x : gain[P][s].y;
-                const float g = f16_bits_to_f32(uint16_t(gw >> (16 * (u & 1))));
-                const float *y = TAB_LDS ? (s_tab + (s * 256 + cw) * 8) : (a.tab32[s] + size_t(cw) * D);
-                const float4 *y4 = reinterpret_cast<const float4 *>(y);
+                if constexpr (B == 8) cw = (word(code[P][s][0], cc >> 2) >> (8 * (cc & 3))) & 0xffu;
+                else cw = (word(code[P][s][cc >> 3], (cc >> 1) & 3) >> (16 * (cc & 1))) & 0xffffu;
+                const uint32_t gw = word(gain[P][s][cc >> 3], (cc >> 1) & 3);
+                const float g = f16_bits_to_f32(uint16_t(gw >> (16 * (cc & 1))));
 #pragma unroll
                 for (int q = 0; q < D / 4; ++q) {
-                    float4 tv = y4[q];
+                    const float4 tv = TAB_LDS ? reinterpret_cast<const float4 *>(s_tab)[s * 512 + q * 256 + cw]
+                                              : reinterpret_cast<const float4 *>(a.tab32[s] + size_t(cw) * D)[q];
                     v[4 * q + 0] = __builtin_fmaf(g, tv.x, v[4 * q + 0]);
                     v[4 * q + 1] = __builtin_fmaf(g, tv.y, v[4 * q + 1]);
                     v[4 * q + 2] = __builtin_fmaf(g, tv.z, v[4 * q + 2]);
