@@ -465,7 +465,7 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
  *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M),
  *      256-byte aligned, ZERO-FILLED before its first use: a 256-byte header
- *      (its first word is the poison word), then 8 MiB of flagged fp32
+ *      (its first word is the poison word), then 32 MiB of flagged fp32
  *      partial tiles of the split-K reduction, which every call leaves at
  *      zero again; the rest is scratch (X with the protected columns zeroed,
  *      the gathered protected activations, X A^T). One workspace serves GEMM

@@ -50,7 +50,9 @@ constexpr int BK = 128;    // inputs per K step
 // written there, so one workspace serves calls of different shapes. The K
 // split is capped to fit.
 constexpr int64_t GEMM_HDR = 256;
-constexpr int64_t GEMM_SLOT_BYTES = int64_t(8) << 20;
+constexpr int64_t GEMM_SLOT_BYTES = int64_t(32) << 20;
+// the part of the slot area the streaming kernel's tile-count rule plans for
+constexpr int64_t LANE_SLOT_BYTES = int64_t(8) << 20;
 
 // Eight stored protected bytes (two words, byte e of the pair at bits
 // 8 (e % 4) of word e / 4) times their scales, in format FMT; the run-time
@@ -559,8 +561,55 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
         }
     }
 
+    // LoRA (finishing split, by the kh = 1 waves): T B^T through the same
+    // MFMA. T (fp32) is split exactly into three bf16 parts, hi + mid + lo,
+    // whose sum equals T to 2^-24 relative; k-inputs 0..15 of the first
+    // product carry hi and 16..31 mid, both against B[:, 0..15] (bf16,
+    // exact), the second product lo. Every product of bf16 parts is exact in
+    // fp32, so the term is T B^T to within the fp32 accumulation.
+    if (kh == 1 && z == a.ksplit - 1 && a.rank > 0) {
+        const int q0 = 8 * (g & 1);
+        u32x4_t bl[NT], bz[NT];
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+            const int64_t n = n0 + 16 * (NT * rs + j) + r16;
+            const int64_t nc = (n < a.d_out) ? n : a.d_out - 1;
+            float b[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) b[e] = (q0 + e < a.rank) ? bf16_to_f32(a.B[nc * a.rank + q0 + e]) : 0.0f;
+            bl[j] = u32x4_t{pack_bf16x2(b[0], b[1]), pack_bf16x2(b[2], b[3]), pack_bf16x2(b[4], b[5]), pack_bf16x2(b[6], b[7])};
+            bz[j] = (g < 2) ? bl[j] : u32x4_t{0u, 0u, 0u, 0u};
+        }
+#pragma unroll
+        for (int i = 0; i < MT; ++i) {
+            const float4 *tp = reinterpret_cast<const float4 *>(a.T + (m0 + 16 * i + r16) * BSQ_MAX_LORA_RANK + q0);
+            const float4 t0 = tp[0], t1 = tp[1];
+            const float tv8[8] = {t0.x, t0.y, t0.z, t0.w, t1.x, t1.y, t1.z, t1.w};
+            uint32_t hi[4], mid[4], lo[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                hi[e] = pack_bf16x2(tv8[2 * e], tv8[2 * e + 1]);
+                const float r0 = tv8[2 * e] - __uint_as_float(hi[e] << 16);
+                const float r1 = tv8[2 * e + 1] - __uint_as_float(hi[e] & 0xffff0000u);
+                mid[e] = pack_bf16x2(r0, r1);
+                lo[e] = pack_bf16x2(r0 - __uint_as_float(mid[e] << 16), r1 - __uint_as_float(mid[e] & 0xffff0000u));
+            }
+            const uint32_t *p1 = (g < 2) ? hi : mid;
+            const u32x4_t a1 = u32x4_t{p1[0], p1[1], p1[2], p1[3]};
+            const u32x4_t a2 = u32x4_t{lo[0], lo[1], lo[2], lo[3]};
+#pragma unroll
+            for (int j = 0; j < NT; ++j) {
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a1),
+                                                                     __builtin_bit_cast(bf16x8_t, bl[j]), acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a2),
+                                                                     __builtin_bit_cast(bf16x8_t, bz[j]), acc[i][j], 0, 0, 0);
+            }
+        }
+    }
+
     // the kh = 1 half of every row set hands its tile to the kh = 0 half
-    // through LDS (the X~ ring, free now); the sum is kh 0 + kh 1
+    // through LDS (the X~ ring, free now), which adds it (kh 0 + kh 1) and
+    // puts the block's tile in LDS as fp32 [BM][BN + 4] rows
     f32x4_t *s_red = reinterpret_cast<f32x4_t *>(s_mem);
     if (kh == 1) {
 #pragma unroll
@@ -576,130 +625,141 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
             for (int j = 0; j < NT; ++j) acc[i][j] = acc[i][j] + s_red[((rs * MT + i) * NT + j) * 64 + lane];
     }
     lds_barrier();  // the exchange area is free again
-
-    bool timed_out = false;
-    if (a.ksplit > 1) {
-        // partial tile in MFMA fragment order: slot ((rs MT + i) NT + j) 256
-        // + 64 r + lane of the split's [BM * BN] range
-        const int64_t tile = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-        uint64_t *tp = a.slots + tile * int64_t(a.ksplit - 1) * (G::BM * G::BN) + lane;
-        auto slot = [&](int zz, int i, int j, int r) { return tp + int64_t(zz) * (G::BM * G::BN) + ((rs * MT + i) * NT + j) * 256 + 64 * r; };
-        if (z < a.ksplit - 1) {  // (uniform over the workgroup)
-            if (kh == 0) {
-#pragma unroll
-                for (int i = 0; i < MT; ++i)
-#pragma unroll
-                    for (int j = 0; j < NT; ++j)
-#pragma unroll
-                        for (int r = 0; r < 4; ++r)
-                            __hip_atomic_store(slot(z, i, j, r), (uint64_t(1) << 32) | __float_as_uint(acc[i][j][r]),
-                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            return;
-        }
-        // the finishing split (kh = 0 waves): per token group, the partials
-        // of splits 0 .. ksplit - 2 (polled SPL splits at a time, their loads
-        // in flight together), added in split order, then its own
-        if (kh == 0) {
-            constexpr int SPL = (MT <= 2) ? 4 : 1;
-            // a workspace poisoned by an earlier give-up may hold flags of no
-            // block of this call: then the sums are discarded and nothing is
-            // cleared (this call's blocks still set every flag, so the polls
-            // end; the word's load overlaps them)
-            const bool poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-#pragma unroll
-            for (int i = 0; i < MT; ++i) {
-                if (timed_out) break;
-                f32x4_t sum[NT];
-#pragma unroll
-                for (int j = 0; j < NT; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-                for (int z0 = 0; z0 < a.ksplit - 1; z0 += SPL) {
-                    uint64_t pw[SPL][NT][4];
-                    for (int spin = 0;; ++spin) {
-                        if (spin >= a.spin_limit) {  // never expected: report, rather than hang
-                            timed_out = true;
-                            break;
-                        }
-                        bool ready = true;
-#pragma unroll
-                        for (int zi = 0; zi < SPL; ++zi) {
-                            const int zz = (z0 + zi < a.ksplit - 1) ? z0 + zi : a.ksplit - 2;  // (clamped: a re-read)
-#pragma unroll
-                            for (int j = 0; j < NT; ++j)
-#pragma unroll
-                                for (int r = 0; r < 4; ++r) {
-                                    pw[zi][j][r] = __hip_atomic_load(slot(zz, i, j, r), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                                    ready &= (pw[zi][j][r] >> 32) != 0;
-                                }
-                        }
-                        if (__all(ready)) break;
-                        __builtin_amdgcn_s_sleep(2);
-                    }
-                    if (timed_out) break;
-#pragma unroll
-                    for (int zi = 0; zi < SPL; ++zi) {
-                        if (z0 + zi >= a.ksplit - 1) break;
-#pragma unroll
-                        for (int j = 0; j < NT; ++j)
-#pragma unroll
-                            for (int r = 0; r < 4; ++r) sum[j][r] += __uint_as_float(uint32_t(pw[zi][j][r]));
-                    }
-                }
-#pragma unroll
-                for (int j = 0; j < NT; ++j) acc[i][j] = sum[j] + acc[i][j];
-            }
-            // every slot consumed: clear them for the next call (after a
-            // give-up they stay, and the workspace is marked)
-            if (!poisoned && !timed_out) {
-                for (int zz = 0; zz < a.ksplit - 1; ++zz)
-#pragma unroll
-                    for (int i = 0; i < MT; ++i)
-#pragma unroll
-                        for (int j = 0; j < NT; ++j)
-#pragma unroll
-                            for (int r = 0; r < 4; ++r)
-                                __hip_atomic_store(slot(zz, i, j, r), uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            gemm_report(a, poisoned, timed_out);
-            timed_out = timed_out || poisoned;
-        }
-    }
-
-    // epilogue (all of LDS is free now): the kh = 0 waves add LoRA and put
-    // the tile in LDS as fp32 [BM][BN + 4]; then every thread stores
-    // 8-output segments of the tile's rows (one 16-byte store per bf16
-    // segment, two per fp32 segment, when Y allows; element stores at a
-    // ragged edge)
     constexpr int OS = G::BN + 4;  // row stride of the staged tile (floats)
     static_assert(size_t(G::BM) * OS * 4 <= G::LDS, "the output tile fits in LDS");
     float *s_out = reinterpret_cast<float *>(s_mem);
     if (kh == 0) {
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-            const int nl = 16 * (NT * rs + j) + r16;
-            const int64_t n = n0 + nl;
-            const int64_t nc = (n < a.d_out) ? n : a.d_out - 1;
-            float bl[BSQ_MAX_LORA_RANK];
+        for (int j = 0; j < NT; ++j)
 #pragma unroll
-            for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) bl[q] = (q < a.rank) ? bf16_to_f32(a.B[nc * a.rank + q]) : 0.0f;
+            for (int i = 0; i < MT; ++i)
 #pragma unroll
-            for (int i = 0; i < MT; ++i) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int ml = 16 * i + 4 * g + r;
-                    float v = timed_out ? __builtin_nanf("") : acc[i][j][r];
-                    if (a.rank > 0) {
-                        const float *Tm = a.T + (m0 + ml) * BSQ_MAX_LORA_RANK;
-#pragma unroll
-                        for (int q = 0; q < BSQ_MAX_LORA_RANK; ++q) v = __builtin_fmaf(bl[q], Tm[q], v);
-                    }
-                    s_out[ml * OS + nl] = v;
-                }
-            }
-        }
+                for (int r = 0; r < 4; ++r) s_out[(16 * i + 4 * g + r) * OS + 16 * (NT * rs + j) + r16] = acc[i][j][r];
     }
     lds_barrier();
-    for (int e = t; e < G::BM * (G::BN / 8); e += 512) {
+
+    // From here every thread works on 8-output segments of the tile's rows:
+    // segment e = token row e / (BN / 8), outputs 8 (e % (BN / 8)) .. + 8.
+    constexpr int SEGS = G::BM * (G::BN / 8);
+    constexpr int NSEG = (SEGS + 511) / 512;  // segments per thread (t + 512 k)
+    static_assert(SEGS % 128 == 0, "a wave has all or none of its k-th segments");
+    bool timed_out = false;
+    if (a.ksplit > 1) {
+        // the split's partial tile as flagged slots, [BM * BN] per split in
+        // thread order: value c of the k-th segment of thread t at
+        // (8 k + c) TPS + t, so that every slot load and store instruction of
+        // a wave covers 512 contiguous bytes
+        constexpr int TPS = (SEGS < 512) ? SEGS : 512;  // threads with segments
+        const int64_t tile = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
+        uint64_t *tp = a.slots + tile * int64_t(a.ksplit - 1) * (G::BM * G::BN) + t;
+        auto seg_slot = [&](int zz, int k) { return tp + int64_t(zz) * (G::BM * G::BN) + (8 * k) * TPS; };
+        if (z < a.ksplit - 1) {  // (uniform over the workgroup)
+            // {1, value} per slot
+#pragma unroll
+            for (int k = 0; k < NSEG; ++k) {
+                const int e = t + 512 * k;
+                if (e >= SEGS) break;
+                const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
+                uint64_t *sp = seg_slot(z, k);
+#pragma unroll
+                for (int c = 0; c < 8; ++c)
+                    __hip_atomic_store(sp + c * TPS, (uint64_t(1) << 32) | __float_as_uint(s_out[ml * OS + nl + c]),
+                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            return;
+        }
+        // the finishing split: every thread takes the partials of its
+        // segments from splits 0 .. ksplit - 2, SPL splits per round with all
+        // their loads in flight together, and adds them to its own value in
+        // split order (so the result does not depend on timing). A workspace
+        // poisoned by an earlier give-up may hold flags of no block of this
+        // call: then the sums are discarded and nothing is cleared (this
+        // call's blocks still set every flag, so the polls end).
+        constexpr int SPL = (NSEG >= 4) ? 2 : (NSEG == 2) ? 4 : 8;
+        const bool poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+        float v[NSEG][8];
+#pragma unroll
+        for (int k = 0; k < NSEG; ++k) {
+            const int e = t + 512 * k;
+            const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
+#pragma unroll
+            for (int c = 0; c < 8; ++c) v[k][c] = (e < SEGS) ? s_out[ml * OS + nl + c] : 0.0f;
+        }
+        for (int z0 = 0; z0 < a.ksplit - 1 && !timed_out; z0 += SPL) {
+            uint64_t pw[SPL][NSEG][8];
+            for (int spin = 0;; ++spin) {
+                if (spin >= a.spin_limit) {  // never expected: report, rather than hang
+                    timed_out = true;
+                    break;
+                }
+                bool ready = true;
+#pragma unroll
+                for (int zi = 0; zi < SPL; ++zi) {
+                    const int zz = (z0 + zi < a.ksplit - 1) ? z0 + zi : a.ksplit - 2;  // (clamped: a re-read)
+#pragma unroll
+                    for (int k = 0; k < NSEG; ++k) {
+                        // (uniform over a wave: SEGS is a multiple of 128;
+                        // a thread without a k-th segment reads nothing, so
+                        // it never sees a slot its owner has cleared)
+                        const int e = t + 512 * k;
+#pragma unroll
+                        for (int c = 0; c < 8; ++c) pw[zi][k][c] = 0;
+                        if (e < SEGS) {
+                            const uint64_t *sp = seg_slot(zz, k);
+#pragma unroll
+                            for (int c = 0; c < 8; ++c) {
+                                pw[zi][k][c] = __hip_atomic_load(sp + c * TPS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                                ready &= (pw[zi][k][c] >> 32) != 0;
+                            }
+                        }
+                    }
+                }
+                if (__all(ready)) break;
+                __builtin_amdgcn_s_sleep(2);
+            }
+            if (timed_out) break;
+#pragma unroll
+            for (int zi = 0; zi < SPL; ++zi) {
+                if (z0 + zi >= a.ksplit - 1) break;
+#pragma unroll
+                for (int k = 0; k < NSEG; ++k)
+#pragma unroll
+                    for (int c = 0; c < 8; ++c) v[k][c] += __uint_as_float(uint32_t(pw[zi][k][c]));
+            }
+        }
+        timed_out = __any(timed_out);
+        // every slot consumed: clear them for the next call (after a give-up
+        // they stay, and the workspace is marked)
+        if (!poisoned && !timed_out) {
+            for (int zz = 0; zz < a.ksplit - 1; ++zz)
+#pragma unroll
+                for (int k = 0; k < NSEG; ++k) {
+                    const int e = t + 512 * k;
+                    if (e >= SEGS) break;
+                    uint64_t *sp = seg_slot(zz, k);
+#pragma unroll
+                    for (int c = 0; c < 8; ++c) __hip_atomic_store(sp + c * TPS, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+        }
+        gemm_report(a, poisoned, timed_out);
+        timed_out = timed_out || poisoned;
+#pragma unroll
+        for (int k = 0; k < NSEG; ++k) {
+            const int e = t + 512 * k;
+            if (e >= SEGS) break;
+            const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
+#pragma unroll
+            for (int c = 0; c < 8; ++c) s_out[ml * OS + nl + c] = timed_out ? __builtin_nanf("") : v[k][c];
+        }
+    }
+
+    // store: one 16-byte store per bf16 segment, two per fp32 segment, when
+    // Y allows; element stores at a ragged edge (each thread stores the
+    // segments it staged, so no barrier is needed)
+#pragma unroll
+    for (int k = 0; k < NSEG; ++k) {
+        const int e = t + 512 * k;
+        if (e >= SEGS) break;
         const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
         const int64_t m = m0 + ml, n = n0 + nl;
         if (m >= a.M || n >= a.d_out) continue;
@@ -1106,7 +1166,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 3
 // SIMD, four times the MFMA work per tile): the smallest tile count whose grid
 // fits in one wave per SIMD (1024 waves), which measured fastest on the
 // Qwen3-8B shapes (the q projection at 2 tiles, gate and up at 8). Then raised
-// while the slices' partials would not fit in GEMM_SLOT_BYTES (1024 MT
+// while the slices' partials would not fit in LANE_SLOT_BYTES (1024 MT
 // flagged values per slice but the last).
 int lane_gemm_tpw(int64_t units, int64_t nblk, int mt)
 {
@@ -1122,8 +1182,8 @@ int lane_gemm_tpw(int64_t units, int64_t nblk, int mt)
     } else {
         while (tpw < 16 && units * slices(tpw) * 4 > 1024) tpw *= 2;
     }
-    while (tpw < 16 && slot_bytes(tpw) > GEMM_SLOT_BYTES) tpw *= 2;
-    return (slot_bytes(tpw) > GEMM_SLOT_BYTES) ? 0 : tpw;  // 0: does not fit
+    while (tpw < 16 && slot_bytes(tpw) > LANE_SLOT_BYTES) tpw *= 2;
+    return (slot_bytes(tpw) > LANE_SLOT_BYTES) ? 0 : tpw;  // 0: does not fit
 }
 
 template <int S, int TPW, int MT>
@@ -1286,11 +1346,13 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     // one workgroup per compute unit (the LDS rings take most of its LDS):
     // split K as far as one round of workgroups over the 256 compute units
     // allows (a second, partial round would double the time), keeping at least
-    // 2 K steps per split and the flagged partials within GEMM_SLOT_BYTES
+    // 2 K steps per split, at most 8 splits (the finishing block adds the
+    // others' partials, two splits per round trip) and the flagged partials
+    // within GEMM_SLOT_BYTES
     int64_t ks = 256 / (tiles > 0 ? tiles : 1);
     ks = std::min<int64_t>(ks, p.ksteps / 2);
     ks = std::min<int64_t>(ks, 1 + GEMM_SLOT_BYTES / std::max<int64_t>(1, tiles * p.bm * p.bn * 8));
-    ks = std::min<int64_t>(ks, 64);
+    ks = std::min<int64_t>(ks, 8);
     p.ksplit = std::max<int64_t>(ks, 1);
     p.t_off = size_t(GEMM_HDR + GEMM_SLOT_BYTES);
     p.xt_off = p.t_off + align256(size_t(p.Mp) * BSQ_MAX_LORA_RANK * 4);

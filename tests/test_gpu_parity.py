@@ -249,7 +249,7 @@ def test_gemm_matches_oracle(case, M, gpu):
 def test_gemm_workspace_reuse(d, gpu):
     """One zero-filled workspace for calls of different token counts: each
     result equals the one from a fresh workspace, and the poison word and the
-    split-K slots (the first 256 B + 8 MiB) are back at zero after every
+    split-K slots (the first 256 B + 32 MiB) are back at zero after every
     call."""
     say(f"gemm workspace reuse d={d}")
     cfg = bsq.Config(d=d, hidden=d)
@@ -269,7 +269,7 @@ def test_gemm_workspace_reuse(d, gpu):
         Y_fresh = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.float32)
         torch.cuda.synchronize()
         assert torch.equal(Y, Y_fresh), f"M={M}: shared-workspace result differs"
-        assert int(torch.count_nonzero(ws[:256 + (8 << 20)])) == 0, f"M={M}: poison word or split-K slots not clear"
+        assert int(torch.count_nonzero(ws[:256 + (32 << 20)])) == 0, f"M={M}: poison word or split-K slots not clear"
 
 
 @pytest.mark.parametrize("d", [8, 16])
@@ -577,11 +577,14 @@ def test_gemv_lora_and_protected_terms(case, gpu):
     assert term_bar(y_0, y_m, q8t, total, len(enc.idx), "protected term") > 100
 
 
-@pytest.mark.parametrize("d,M,fmt", [(8, 16, bsq.PROT_INT8), (8, 64, bsq.PROT_INT8), (16, 16, bsq.PROT_INT8),
-                                     (16, 256, bsq.PROT_INT8), (8, 64, bsq.PROT_E4M3), (16, 16, bsq.PROT_E5M2)])
+@pytest.mark.parametrize("d,M,fmt", [(8, 16, bsq.PROT_INT8), (8, 64, bsq.PROT_INT8), (8, 256, bsq.PROT_INT8),
+                                     (16, 16, bsq.PROT_INT8), (16, 256, bsq.PROT_INT8), (8, 64, bsq.PROT_E4M3),
+                                     (16, 16, bsq.PROT_E5M2)])
 def test_gemm_lora_and_protected_terms(d, M, fmt, gpu):
-    """As for the GEMV, on the fused GEMM: the LoRA term (fp32) to within fp32
-    rounding; the protected term goes through the MFMA as bf16(q8 scale), so
+    """As for the GEMV, on the fused GEMM: the LoRA term to within fp32
+    rounding (the streaming kernel adds it in fp32; the tiled kernel (d = 16,
+    or M > 64) through the MFMA, T split exactly into three bf16 parts); the
+    protected term goes through the MFMA as bf16(q8 scale), so
     its bar adds the sub-Gaussian bound of those roundings."""
     say(f"gemm term presence d={d} M={M} format={fmt}")
     cfg, decs, codec, layer, W, encs, tabs = _make("gemm-terms", 320, 2048, dict(d=d, hidden=d, protect_format=fmt),
