@@ -465,15 +465,18 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
  *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M),
  *      256-byte aligned, ZERO-FILLED before its first use: a 256-byte header
- *      (its first word is the poison word), then 32 MiB of flagged fp32
- *      partial tiles of the split-K reduction, which every call leaves at
- *      zero again; the rest is scratch (X with the protected columns zeroed,
- *      the gathered protected activations, X A^T). One workspace serves GEMM
- *      calls of any shape; it must not be shared with a GEMV workspace, and
- *      calls that share it must not overlap.
- *   err device int32 error word or NULL, as for bsq_gemv.
+ *      (its first word is the poison word), then 8 MiB of flagged fp32
+ *      partial tiles that the small-M (d = 8, M <= 64) kernel's blocks hand
+ *      on, which every call leaves at zero again; the rest is scratch (X
+ *      with the protected columns zeroed, the gathered protected
+ *      activations, X A^T, the tiled kernel's split-K partials). One
+ *      workspace serves GEMM calls of any shape; it must not be shared with a
+ *      GEMV workspace, and calls that share it must not overlap.
+ *   err device int32 error word or NULL, as for bsq_gemv (only the small-M
+ *      kernel waits for other blocks, so only it reports a wait's give-up).
  * The K steps of a tile may be split over several blocks; their fp32
- * partials are summed in a fixed order, so results are deterministic. With
+ * partials are summed in a fixed order (the tiled kernel's by a second
+ * launch on the same stream), so results are deterministic. With
  * protect_axis = 1 each protected row's column of Y is written afterwards as
  * scale_p X q8[p, :]^T + (X A^T) B[row]^T (same stream); that pass takes four
  * tokens per block, so M <= 262140 there (BSQ_ERR_UNSUPPORTED beyond). */

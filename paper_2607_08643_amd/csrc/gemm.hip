@@ -22,12 +22,13 @@
 // its activation as bf16 exactly once.
 //
 // Split K: when weight blocks x token tiles alone would leave the chip mostly
-// idle, the K steps are divided over ksplit blocks per tile (grid z). Splits
-// z < ksplit - 1 store their fp32 partial tile as flagged 64-bit slots
-// {1, value} (device-coherent stores, no fence) and exit; the last split,
-// dispatched after all the others, polls the slots, sums the partials in
-// split order (so the result does not depend on timing), clears the slots,
-// and runs the epilogue.
+// idle, the K steps are divided over ksplit blocks per tile (grid z). Every
+// split stores its fp32 partial tile to a scratch area of the workspace, and
+// a second kernel sums the partials in split order (so the result does not
+// depend on timing) and stores Y. (A finishing block that gathered the other
+// splits' partials itself read them at the rate one compute unit reaches on
+// device-coherent loads, 20-30 GB/s, which made a 1024-row projection at 256
+// tokens take 55 us.)
 #include <algorithm>
 #include <type_traits>
 
@@ -44,15 +45,14 @@ constexpr int BK = 128;    // inputs per K step
 
 // The workspace starts with a 256-byte header whose first word is the
 // poison word (nonzero once a call gave up waiting for a partial tile and
-// left flagged slots behind). The flagged partial slots follow at a fixed
-// place, GEMM_SLOT_BYTES from offset GEMM_HDR, whatever the shape: every
-// call leaves them at zero, and no other data of any GEMM call is ever
-// written there, so one workspace serves calls of different shapes. The K
-// split is capped to fit.
+// left flagged slots behind). The streaming kernel's flagged partial slots
+// follow at a fixed place, GEMM_SLOT_BYTES from offset GEMM_HDR, whatever
+// the shape: every call leaves them at zero, and no other data of any GEMM
+// call is ever written there, so one workspace serves calls of different
+// shapes. Its slice count is capped to fit. The tiled kernel's split-K
+// partials go to scratch after the prepared activations.
 constexpr int64_t GEMM_HDR = 256;
-constexpr int64_t GEMM_SLOT_BYTES = int64_t(32) << 20;
-// the part of the slot area the streaming kernel's tile-count rule plans for
-constexpr int64_t LANE_SLOT_BYTES = int64_t(8) << 20;
+constexpr int64_t GEMM_SLOT_BYTES = int64_t(8) << 20;
 
 // Eight stored protected bytes (two words, byte e of the pair at bits
 // 8 (e % 4) of word e / 4) times their scales, in format FMT; the run-time
@@ -93,7 +93,9 @@ struct GemmArgs {
     int y_bf16;
     int y_vec;         // Y 16-byte aligned with 16-byte row pitch: vector stores
     int ksplit;        // blocks per tile along K (grid z)
-    uint64_t *slots;   // [tiles][ksplit - 1][BM * BN] flagged partials, zero between calls
+    float *part;       // split-K partials [ksplit][Mp][np] (ksplit > 1)
+    int64_t np;        // row pitch of the partials (d_out padded to whole blocks)
+    uint64_t *slots;   // the streaming kernel's flagged partials, zero between calls
     uint32_t *poison;  // the workspace's poison word
     int32_t *err;      // caller's device error word, or null
     int spin_limit;    // polls before a wait gives up (wait_limit())
@@ -642,120 +644,25 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
     // segment e = token row e / (BN / 8), outputs 8 (e % (BN / 8)) .. + 8.
     constexpr int SEGS = G::BM * (G::BN / 8);
     constexpr int NSEG = (SEGS + 511) / 512;  // segments per thread (t + 512 k)
-    static_assert(SEGS % 128 == 0, "a wave has all or none of its k-th segments");
-    bool timed_out = false;
     if (a.ksplit > 1) {
-        // the split's partial tile as flagged slots, [BM * BN] per split in
-        // thread order: value c of the k-th segment of thread t at
-        // (8 k + c) TPS + t, so that every slot load and store instruction of
-        // a wave covers 512 contiguous bytes
-        constexpr int TPS = (SEGS < 512) ? SEGS : 512;  // threads with segments
-        const int64_t tile = int64_t(blockIdx.y) * gridDim.x + blockIdx.x;
-        uint64_t *tp = a.slots + tile * int64_t(a.ksplit - 1) * (G::BM * G::BN) + t;
-        auto seg_slot = [&](int zz, int k) { return tp + int64_t(zz) * (G::BM * G::BN) + (8 * k) * TPS; };
-        if (z < a.ksplit - 1) {  // (uniform over the workgroup)
-            // {1, value} per slot
-#pragma unroll
-            for (int k = 0; k < NSEG; ++k) {
-                const int e = t + 512 * k;
-                if (e >= SEGS) break;
-                const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
-                uint64_t *sp = seg_slot(z, k);
-#pragma unroll
-                for (int c = 0; c < 8; ++c)
-                    __hip_atomic_store(sp + c * TPS, (uint64_t(1) << 32) | __float_as_uint(s_out[ml * OS + nl + c]),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            }
-            return;
-        }
-        // the finishing split: every thread takes the partials of its
-        // segments from splits 0 .. ksplit - 2, SPL splits per round with all
-        // their loads in flight together, and adds them to its own value in
-        // split order (so the result does not depend on timing). A workspace
-        // poisoned by an earlier give-up may hold flags of no block of this
-        // call: then the sums are discarded and nothing is cleared (this
-        // call's blocks still set every flag, so the polls end).
-        constexpr int SPL = (NSEG >= 4) ? 2 : (NSEG == 2) ? 4 : 8;
-        const bool poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-        float v[NSEG][8];
-#pragma unroll
-        for (int k = 0; k < NSEG; ++k) {
-            const int e = t + 512 * k;
-            const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
-#pragma unroll
-            for (int c = 0; c < 8; ++c) v[k][c] = (e < SEGS) ? s_out[ml * OS + nl + c] : 0.0f;
-        }
-        for (int z0 = 0; z0 < a.ksplit - 1 && !timed_out; z0 += SPL) {
-            uint64_t pw[SPL][NSEG][8];
-            for (int spin = 0;; ++spin) {
-                if (spin >= a.spin_limit) {  // never expected: report, rather than hang
-                    timed_out = true;
-                    break;
-                }
-                bool ready = true;
-#pragma unroll
-                for (int zi = 0; zi < SPL; ++zi) {
-                    const int zz = (z0 + zi < a.ksplit - 1) ? z0 + zi : a.ksplit - 2;  // (clamped: a re-read)
-#pragma unroll
-                    for (int k = 0; k < NSEG; ++k) {
-                        // (uniform over a wave: SEGS is a multiple of 128;
-                        // a thread without a k-th segment reads nothing, so
-                        // it never sees a slot its owner has cleared)
-                        const int e = t + 512 * k;
-#pragma unroll
-                        for (int c = 0; c < 8; ++c) pw[zi][k][c] = 0;
-                        if (e < SEGS) {
-                            const uint64_t *sp = seg_slot(zz, k);
-#pragma unroll
-                            for (int c = 0; c < 8; ++c) {
-                                pw[zi][k][c] = __hip_atomic_load(sp + c * TPS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                                ready &= (pw[zi][k][c] >> 32) != 0;
-                            }
-                        }
-                    }
-                }
-                if (__all(ready)) break;
-                __builtin_amdgcn_s_sleep(2);
-            }
-            if (timed_out) break;
-#pragma unroll
-            for (int zi = 0; zi < SPL; ++zi) {
-                if (z0 + zi >= a.ksplit - 1) break;
-#pragma unroll
-                for (int k = 0; k < NSEG; ++k)
-#pragma unroll
-                    for (int c = 0; c < 8; ++c) v[k][c] += __uint_as_float(uint32_t(pw[zi][k][c]));
-            }
-        }
-        timed_out = __any(timed_out);
-        // every slot consumed: clear them for the next call (after a give-up
-        // they stay, and the workspace is marked)
-        if (!poisoned && !timed_out) {
-            for (int zz = 0; zz < a.ksplit - 1; ++zz)
-#pragma unroll
-                for (int k = 0; k < NSEG; ++k) {
-                    const int e = t + 512 * k;
-                    if (e >= SEGS) break;
-                    uint64_t *sp = seg_slot(zz, k);
-#pragma unroll
-                    for (int c = 0; c < 8; ++c) __hip_atomic_store(sp + c * TPS, uint64_t(0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-        }
-        gemm_report(a, poisoned, timed_out);
-        timed_out = timed_out || poisoned;
+        // the split's partial tile to part[z] (rows of the padded token
+        // range, whole blocks of rows: every element the sum reads is written)
+        const int64_t mp = int64_t(gridDim.y) * G::BM;
+        float *pz = a.part + (int64_t(z) * mp + m0) * a.np + n0;
 #pragma unroll
         for (int k = 0; k < NSEG; ++k) {
             const int e = t + 512 * k;
             if (e >= SEGS) break;
             const int ml = e / (G::BN / 8), nl = 8 * (e % (G::BN / 8));
-#pragma unroll
-            for (int c = 0; c < 8; ++c) s_out[ml * OS + nl + c] = timed_out ? __builtin_nanf("") : v[k][c];
+            float4 *dst = reinterpret_cast<float4 *>(pz + ml * a.np + nl);
+            dst[0] = *reinterpret_cast<const float4 *>(s_out + ml * OS + nl);
+            dst[1] = *reinterpret_cast<const float4 *>(s_out + ml * OS + nl + 4);
         }
+        return;
     }
 
     // store: one 16-byte store per bf16 segment, two per fp32 segment, when
-    // Y allows; element stores at a ragged edge (each thread stores the
-    // segments it staged, so no barrier is needed)
+    // Y allows; element stores at a ragged edge
 #pragma unroll
     for (int k = 0; k < NSEG; ++k) {
         const int e = t + 512 * k;
@@ -1166,7 +1073,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 3
 // SIMD, four times the MFMA work per tile): the smallest tile count whose grid
 // fits in one wave per SIMD (1024 waves), which measured fastest on the
 // Qwen3-8B shapes (the q projection at 2 tiles, gate and up at 8). Then raised
-// while the slices' partials would not fit in LANE_SLOT_BYTES (1024 MT
+// while the slices' partials would not fit in GEMM_SLOT_BYTES (1024 MT
 // flagged values per slice but the last).
 int lane_gemm_tpw(int64_t units, int64_t nblk, int mt)
 {
@@ -1182,8 +1089,8 @@ int lane_gemm_tpw(int64_t units, int64_t nblk, int mt)
     } else {
         while (tpw < 16 && units * slices(tpw) * 4 > 1024) tpw *= 2;
     }
-    while (tpw < 16 && slot_bytes(tpw) > LANE_SLOT_BYTES) tpw *= 2;
-    return (slot_bytes(tpw) > LANE_SLOT_BYTES) ? 0 : tpw;  // 0: does not fit
+    while (tpw < 16 && slot_bytes(tpw) > GEMM_SLOT_BYTES) tpw *= 2;
+    return (slot_bytes(tpw) > GEMM_SLOT_BYTES) ? 0 : tpw;  // 0: does not fit
 }
 
 template <int S, int TPW, int MT>
@@ -1326,7 +1233,8 @@ hipError_t launch_generic_t(int stages, const GenericGemmArgs &g, hipStream_t st
 struct GemmPlan {
     int mt, nt;  // token groups and 64-row groups per block
     int64_t bm, bn, mtiles, nblk, ksteps, ksplit, Mp, Kp, kp32;
-    size_t t_off, xt_off, xp_off, total;
+    int64_t np;  // d_out padded to whole blocks (partials' row pitch)
+    size_t t_off, xt_off, xp_off, part_off, total;
 };
 
 GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
@@ -1346,19 +1254,54 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     // one workgroup per compute unit (the LDS rings take most of its LDS):
     // split K as far as one round of workgroups over the 256 compute units
     // allows (a second, partial round would double the time), keeping at least
-    // 2 K steps per split, at most 8 splits (the finishing block adds the
-    // others' partials, two splits per round trip) and the flagged partials
-    // within GEMM_SLOT_BYTES
+    // 2 K steps per split and at most 8 splits (the partials of all splits
+    // are written and read once more: at most 256 tiles' worth, 16 MiB)
     int64_t ks = 256 / (tiles > 0 ? tiles : 1);
     ks = std::min<int64_t>(ks, p.ksteps / 2);
-    ks = std::min<int64_t>(ks, 1 + GEMM_SLOT_BYTES / std::max<int64_t>(1, tiles * p.bm * p.bn * 8));
     ks = std::min<int64_t>(ks, 8);
     p.ksplit = std::max<int64_t>(ks, 1);
     p.t_off = size_t(GEMM_HDR + GEMM_SLOT_BYTES);
     p.xt_off = p.t_off + align256(size_t(p.Mp) * BSQ_MAX_LORA_RANK * 4);
     p.xp_off = p.xt_off + align256(size_t(p.Mp) * size_t(p.Kp) * 2);
-    p.total = p.xp_off + align256(size_t(p.Mp) * size_t(std::max<int64_t>(p.kp32, 32)) * 2);
+    p.part_off = p.xp_off + align256(size_t(p.Mp) * size_t(std::max<int64_t>(p.kp32, 32)) * 2);
+    p.np = p.nblk * p.bn;
+    p.total = p.part_off + ((p.ksplit > 1) ? size_t(p.ksplit) * size_t(p.Mp) * size_t(p.np) * 4 : 0);
     return p;
+}
+
+// Split-K sum: one thread per 8-output segment of Y, the partials added in
+// split order (z = 0, 1, ...), stored as the tiled kernel stores.
+__global__ __launch_bounds__(256) void gemm_splitk_sum(const GemmArgs a, int64_t mp)
+{
+    const int64_t nseg = (a.d_out + 7) / 8;
+    const int64_t e = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (e >= a.M * nseg) return;
+    const int64_t m = e / nseg, n = 8 * (e - m * nseg);
+    const float *src = a.part + m * a.np + n;
+    float4 lo = reinterpret_cast<const float4 *>(src)[0], hi = reinterpret_cast<const float4 *>(src)[1];
+    for (int z = 1; z < a.ksplit; ++z) {
+        const float4 *pz = reinterpret_cast<const float4 *>(src + int64_t(z) * mp * a.np);
+        const float4 l = pz[0], h = pz[1];
+        lo.x += l.x; lo.y += l.y; lo.z += l.z; lo.w += l.w;
+        hi.x += h.x; hi.y += h.y; hi.z += h.z; hi.w += h.w;
+    }
+    const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+    if (a.y_vec && n + 8 <= a.d_out) {
+        if (a.y_bf16) {
+            *reinterpret_cast<u32x4_t *>(static_cast<uint16_t *>(a.Y) + m * a.ldy + n) =
+                u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
+        } else {
+            float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.Y) + m * a.ldy + n);
+            dst[0] = lo;
+            dst[1] = hi;
+        }
+    } else {
+        for (int c = 0; c < 8; ++c) {
+            if (n + c >= a.d_out) break;
+            if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n + c] = f32_to_bf16(v[c]);
+            else static_cast<float *>(a.Y)[m * a.ldy + n + c] = v[c];
+        }
+    }
 }
 
 template <int D, int S, int MT, int NT>
@@ -1374,6 +1317,12 @@ hipError_t launch_main(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
     }
     const dim3 grid = dim3(unsigned(p.nblk), unsigned(p.mtiles), unsigned(p.ksplit));
     hipLaunchKernelGGL((gemm_kernel<D, S, MT, NT>), grid, dim3(512), G::LDS, st, a);
+    if (p.ksplit > 1) {
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const int64_t segs = a.M * ((a.d_out + 7) / 8);
+        hipLaunchKernelGGL(gemm_splitk_sum, dim3(unsigned((segs + 255) / 256)), dim3(256), 0, st, a, p.Mp);
+    }
     return hipGetLastError();
 }
 
@@ -1433,6 +1382,8 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     }
     a.rank = 0;
     a.ksplit = int(p.ksplit);
+    a.part = reinterpret_cast<float *>(wb + p.part_off);
+    a.np = p.np;
     a.slots = reinterpret_cast<uint64_t *>(wb + GEMM_HDR);
     a.poison = static_cast<uint32_t *>(ws);
     a.err = err;

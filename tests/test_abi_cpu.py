@@ -283,10 +283,9 @@ def test_wait_limit_is_settable_and_restorable():
 
 def test_product_workspaces_hold_a_header():
     """GEMV and GEMM workspaces start with a 256-byte header for the poison
-    word, so they exceed their slot and scratch areas by at least that (the
-    GEMM's split-K slots take 32 MiB)."""
+    word, so they exceed their slot and scratch areas by at least that."""
     cfg = bsq.Config()
-    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 64, 256, 1) >= 256 + (32 << 20)
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 64, 256, 1) >= 256 + (8 << 20)
     assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 1, 64, 256) >= 256 + 8 * 16 * 4
 
 

@@ -249,7 +249,7 @@ def test_gemm_matches_oracle(case, M, gpu):
 def test_gemm_workspace_reuse(d, gpu):
     """One zero-filled workspace for calls of different token counts: each
     result equals the one from a fresh workspace, and the poison word and the
-    split-K slots (the first 256 B + 32 MiB) are back at zero after every
+    split-K slots (the first 256 B + 8 MiB) are back at zero after every
     call."""
     say(f"gemm workspace reuse d={d}")
     cfg = bsq.Config(d=d, hidden=d)
@@ -269,7 +269,7 @@ def test_gemm_workspace_reuse(d, gpu):
         Y_fresh = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.float32)
         torch.cuda.synchronize()
         assert torch.equal(Y, Y_fresh), f"M={M}: shared-workspace result differs"
-        assert int(torch.count_nonzero(ws[:256 + (32 << 20)])) == 0, f"M={M}: poison word or split-K slots not clear"
+        assert int(torch.count_nonzero(ws[:256 + (8 << 20)])) == 0, f"M={M}: poison word or split-K slots not clear"
 
 
 @pytest.mark.parametrize("d", [8, 16])
