@@ -127,6 +127,7 @@ struct PrepArgs {
     const uint16_t *X;
     int64_t ldx, M, d_in, Kp, k, kp32;
     const int32_t *idx;
+    const uint32_t *bits;  // protected-column bitmap of the layer (k > 0)
     const uint16_t *A;  // LoRA A [rank][d_in] or null
     int rank;
     uint16_t *Xt;
@@ -139,7 +140,6 @@ __global__ __launch_bounds__(256) void gemm_prep(const PrepArgs a)
     // workgroup (m, y): token row m < Mp; y < ncb: X~ columns [2048 y, 2048 y
     // + 2048); y == ncb: the gathered protected activations (and the zero
     // LoRA entries past the rank); y = ncb + 1 + r: T[m][r] for rank index r
-    __shared__ uint32_t s_bits[PREP_COLS / 32];  // protected bitmap of the column block
     __shared__ float s_red[4];
     const int t = threadIdx.x;
     const int64_t m = blockIdx.x;
@@ -148,28 +148,19 @@ __global__ __launch_bounds__(256) void gemm_prep(const PrepArgs a)
     const bool live = m < a.M;
     const uint16_t *xr = a.X + m * a.ldx;
     if (y < ncb) {
-        const int64_t c0 = y * PREP_COLS;
-        if (t < PREP_COLS / 32) s_bits[t] = 0u;
-        __syncthreads();
-        for (int64_t p = t; p < a.k; p += 256) {
-            const int32_t j = a.idx[p];
-            if (j >= 0 && j < a.d_in && j >= c0 && j < c0 + PREP_COLS) atomicOr(&s_bits[(j - c0) >> 5], 1u << (j & 31));
-        }
-        __syncthreads();
-        // X~: one 8-input segment per thread; protected inputs, inputs past
-        // d_in and rows past M are zero
-        const int64_t j0 = c0 + 8 * t;
+        // X~: one 8-input segment per thread; protected inputs (the layer's
+        // bitmap, read with the segment), inputs past d_in and rows past M
+        // are zero
+        const int64_t j0 = y * PREP_COLS + 8 * t;
         if (j0 < a.Kp) {
             u32x4_t v = u32x4_t{0u, 0u, 0u, 0u};
             if (live && j0 < a.d_in) {
                 v = *reinterpret_cast<const u32x4_t *>(xr + j0);
-                const uint32_t pm = (s_bits[(8 * t) >> 5] >> ((8 * t) & 31)) & 0xffu;
-                if (pm) {
+                const uint32_t pm = (a.k > 0 && a.bits) ? (a.bits[j0 >> 5] >> (j0 & 31)) & 0xffu : 0u;
 #pragma unroll
-                    for (int h = 0; h < 4; ++h) {
-                        const uint32_t keep = (((pm >> (2 * h)) & 1u) ? 0u : 0xffffu) | (((pm >> (2 * h + 1)) & 1u) ? 0u : 0xffff0000u);
-                        v[h] &= keep;
-                    }
+                for (int h = 0; h < 4; ++h) {
+                    const uint32_t keep = (((pm >> (2 * h)) & 1u) ? 0u : 0xffffu) | (((pm >> (2 * h + 1)) & 1u) ? 0u : 0xffff0000u);
+                    v[h] &= keep;
                 }
             }
             *reinterpret_cast<u32x4_t *>(a.Xt + m * a.Kp + j0) = v;
@@ -1399,6 +1390,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     pa.k = L.k;
     pa.kp32 = p.kp32;
     pa.idx = L.prot_idx;
+    pa.bits = L.prot_bits;
     pa.Xt = reinterpret_cast<uint16_t *>(wb + p.xt_off);
     pa.Xp = reinterpret_cast<uint16_t *>(wb + p.xp_off);
     pa.T = reinterpret_cast<float *>(wb + p.t_off);
