@@ -96,7 +96,7 @@ typedef enum {
  *              bsq_coupled_select);
  *   BAD_SET    a given protected set is not strictly ascending or out of
  *              range (bsq_encode_with_set);
- *   TIMEOUT    a product's finishing workgroup gave up waiting for another
+ *   TIMEOUT    a GEMV's finishing workgroup gave up waiting for another
  *              workgroup's partial result (never expected: workgroups run in
  *              dispatch order, and the wait is bounded only so that a fault
  *              elsewhere cannot hang the queue). The affected outputs are NaN
@@ -236,8 +236,9 @@ typedef enum { BSQ_OP_ENCODE = 0, BSQ_OP_GEMV = 1, BSQ_OP_GEMM = 2, BSQ_OP_SELEC
 /* Library ABI version (BSQ_ABI_VERSION). */
 int32_t bsq_version(void);
 
-/* Testing aid: the number of polls a product's finishing workgroup makes for
- * another workgroup's partial result before it gives up (BSQ_DEVERR_TIMEOUT).
+/* Testing aid: the number of polls a GEMV's finishing workgroup makes for
+ * another workgroup's partial result before it gives up (BSQ_DEVERR_TIMEOUT;
+ * bsq_gemm has no such wait).
  * 0 makes every such wait give up at once, so that the timeout and poison
  * handling can be exercised with every kernel still exiting normally; a
  * negative value restores the default (about a second of polling). Applies
@@ -464,19 +465,17 @@ bsq_status bsq_gemv_run(const bsq_config *cfg, int32_t n, const void *const *cod
  *   X  device bf16 [M][ldx] (ldx >= d_in, multiple of 8)
  *   Y  device [M][ldy] of y_dtype (bf16 or fp32), ldy >= d_out
  *   ws device workspace of bsq_workspace_bytes(GEMM, 1, d_out, d_in, M),
- *      256-byte aligned, ZERO-FILLED before its first use: a 256-byte header
- *      (its first word is the poison word), then 8 MiB of flagged fp32
- *      partial tiles that the small-M (d = 8, M <= 64) kernel's blocks hand
- *      on, which every call leaves at zero again; the rest is scratch (X
- *      with the protected columns zeroed, the gathered protected
- *      activations, X A^T, the tiled kernel's split-K partials). One
- *      workspace serves GEMM calls of any shape; it must not be shared with a
- *      GEMV workspace, and calls that share it must not overlap.
- *   err device int32 error word or NULL, as for bsq_gemv (only the small-M
- *      kernel waits for other blocks, so only it reports a wait's give-up).
+ *      256-byte aligned, any contents: a 256-byte header the call leaves
+ *      untouched, then scratch (X with the protected columns zeroed, the
+ *      gathered protected activations, X A^T, split-K partials). One
+ *      workspace serves GEMM calls of any shape; calls that share it must
+ *      not overlap.
+ *   err device int32 error word or NULL (accepted for symmetry with
+ *      bsq_gemv; no workgroup of the product waits for another, so nothing
+ *      is reported).
  * The K steps of a tile may be split over several blocks; their fp32
- * partials are summed in a fixed order (the tiled kernel's by a second
- * launch on the same stream), so results are deterministic. With
+ * partials are summed in a fixed order by a second launch on the same
+ * stream, so results are deterministic. With
  * protect_axis = 1 each protected row's column of Y is written afterwards as
  * scale_p X q8[p, :]^T + (X A^T) B[row]^T (same stream); that pass takes four
  * tokens per block, so M <= 262140 there (BSQ_ERR_UNSUPPORTED beyond). */

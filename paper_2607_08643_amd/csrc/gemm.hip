@@ -43,16 +43,11 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 128;    // inputs per K step
 
-// The workspace starts with a 256-byte header whose first word is the
-// poison word (nonzero once a call gave up waiting for a partial tile and
-// left flagged slots behind). The streaming kernel's flagged partial slots
-// follow at a fixed place, GEMM_SLOT_BYTES from offset GEMM_HDR, whatever
-// the shape: every call leaves them at zero, and no other data of any GEMM
-// call is ever written there, so one workspace serves calls of different
-// shapes. Its slice count is capped to fit. The tiled kernel's split-K
-// partials go to scratch after the prepared activations.
+// The workspace starts with a 256-byte header that the product leaves
+// untouched (no block of it waits for another, so there is no poison word
+// or flagged slot to keep); the scratch of a call follows: T = X A^T, X~, the
+// gathered protected activations and the split-K partials.
 constexpr int64_t GEMM_HDR = 256;
-constexpr int64_t GEMM_SLOT_BYTES = int64_t(8) << 20;
 
 // Eight stored protected bytes (two words, byte e of the pair at bits
 // 8 (e % 4) of word e / 4) times their scales, in format FMT; the run-time
@@ -95,27 +90,8 @@ struct GemmArgs {
     int ksplit;        // blocks per tile along K (grid z)
     float *part;       // split-K partials [ksplit][Mp][np] (ksplit > 1)
     int64_t np;        // row pitch of the partials (d_out padded to whole blocks)
-    uint64_t *slots;   // the streaming kernel's flagged partials, zero between calls
-    uint32_t *poison;  // the workspace's poison word
-    int32_t *err;      // caller's device error word, or null
-    int spin_limit;    // polls before a wait gives up (wait_limit())
     int pfmt;          // bsq_prot_format of q8
 };
-
-// The finishing block's outcome when it could not use the other blocks'
-// partials: lane 0 reports it in the caller's error word, and after a
-// give-up marks the workspace so that no later call consumes a flag a late
-// block may still set.
-__device__ __forceinline__ void gemm_report(const GemmArgs &a, bool poisoned, bool timed_out)
-{
-    if ((threadIdx.x & 63) != 0) return;
-    if (poisoned) {
-        if (a.err) atomicOr(a.err, int32_t(BSQ_DEVERR_POISONED));
-    } else if (timed_out) {
-        __hip_atomic_store(a.poison, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (a.err) atomicOr(a.err, int32_t(BSQ_DEVERR_TIMEOUT));
-    }
-}
 
 // ---------------------------------------------------------------------------
 // Prep: one workgroup per (padded token row m < Mp, block of PREP_COLS X~
@@ -685,433 +661,6 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
 }
 
 // ---------------------------------------------------------------------------
-// Streaming kernel (d = 8, M up to a few token tiles): the organisation of the
-// batch-1 GEMV with MFMA products. A workgroup of four waves owns a slice of
-// 4 TPW consecutive 64-row x 128-input plane tiles of one 64-row group and a
-// token tile of 16 MT tokens; a wave takes TPW of the tiles, loading each
-// lane's code and gain words straight from the tile (row 16 j + lane % 16,
-// chunks 4 g .. 4 g + 3, g = lane / 16), two tiles ahead. Its X~ fragments
-// come from the prepared activations one tile ahead: the fragments of
-// k-slice q of the next tile are requested as soon as the current tile's have
-// gone into their MFMAs. Per tile and k-slice q the lane decodes chunk
-// 4 g + q of its four rows into B fragments (fp32 fma chain over fp16 gains
-// and LDS fp16 table entries, rounded to bf16) for v_mfma_f32_16x16x32_bf16
-// against each of the MT token groups, so that one decode serves 16 MT
-// tokens. The four wave tiles are added in wave order in LDS, token group by
-// token group, and wave i keeps group i; the slices of a (row group, token
-// tile) hand their partials to the last one through flagged 64-bit slots
-// (in-order dispatch makes the wait safe), whose wave i adds them in slice
-// order for group i and applies the protected term, LoRA and the store. No
-// barrier inside the tile loop.
-// ---------------------------------------------------------------------------
-// largest padded protected row (bytes) that the finishing workgroup stages in
-// LDS for one token group; longer rows are read from global memory
-constexpr int LANE_GEMM_PROT_MAX = 256;
-// largest token group count of the streaming kernel (one per wave)
-constexpr int LANE_GEMM_MAX_MT = 4;
-// largest M routed to the streaming kernel (token tiles of 64 beyond 64)
-constexpr int64_t LANE_GEMM_MAX_M = 64;
-
-struct LaneGemmArgs {
-    GemmArgs g;
-    int64_t nblk;    // 128-input tiles per row (K steps)
-    int64_t q;       // slices per (64-row group, token tile)
-    int64_t rgs;     // 64-row groups
-    int64_t mtiles;  // token tiles of 16 MT tokens
-};
-
-template <int S>
-struct LaneWords {
-    uint32_t code[4][S];  // chunks 4 g .. + 3 of row 16 j + lane % 16
-    uint2 gain[4][S];
-};
-
-template <int S>
-__device__ __forceinline__ void lane_gemm_words(LaneWords<S> &T, const GemmArgs &a, int64_t e0)
-{
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int s = 0; s < S; ++s) {
-            const int64_t e = e0 + 256 * j;
-            T.code[j][s] = *reinterpret_cast<const uint32_t *>(static_cast<const uint8_t *>(a.codes[s]) + e);
-            T.gain[j][s] = *reinterpret_cast<const uint2 *>(a.gains[s] + e);
-        }
-}
-
-// X~ fragments of one k-slice for the MT token groups (rows 16 i apart)
-template <int MT>
-__device__ __forceinline__ void lane_gemm_x(u32x4_t (&x)[MT], const uint16_t *p, int64_t Kp)
-{
-#pragma unroll
-    for (int i = 0; i < MT; ++i) x[i] = *reinterpret_cast<const u32x4_t *>(p + 16 * i * Kp);
-}
-
-// B fragment of k-slice q, row block j: chunk 4 g + q of row 16 j + lane % 16
-template <int S>
-__device__ __forceinline__ u32x4_t lane_gemm_decode(const LaneWords<S> &T, const uint16_t *s_tab, int q, int j)
-{
-    typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
-    f16x8_t tv[S];
-#pragma unroll
-    for (int s = 0; s < S; ++s)
-        tv[s] = *reinterpret_cast<const f16x8_t *>(s_tab + (s * 256 + ((T.code[j][s] >> (8 * q)) & 0xffu)) * 8);
-    float v[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = 0.0f;
-#pragma unroll
-    for (int s = 0; s < S; ++s) {
-        const uint32_t gw = (q < 2) ? T.gain[j][s].x : T.gain[j][s].y;
-        const float gs = f16_bits_to_f32(uint16_t(gw >> (16 * (q & 1))));
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = __builtin_fmaf(gs, float(tv[s][e]), v[e]);
-    }
-    return u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
-}
-
-template <int S, int TPW, int MT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT == 1 ? 3 : 2))) void gemm_lane_kernel(
-    const LaneGemmArgs la)
-{
-    constexpr int WV = 4, PF = TPW < 2 ? TPW : 2;
-    static_assert(MT >= 1 && MT <= LANE_GEMM_MAX_MT && MT <= WV, "one token group per wave");
-    // protected staging limit per token group (bytes of a padded row)
-    constexpr int PM = (MT == 1) ? LANE_GEMM_PROT_MAX : LANE_GEMM_PROT_MAX / 2;
-    constexpr int OS = 68;  // row pitch (floats) of a wave's staged output tile [16][64 + 4]
-    const GemmArgs &a = la.g;
-    __shared__ __attribute__((aligned(16))) uint4 s_tab_mem[S * 256];  // fp16 tables [S][256][8]
-    // wave tiles [WV][4][64] f32x4; then each finishing wave's output tile
-    __shared__ __attribute__((aligned(16))) float s_rm[WV * 16 * OS];
-    // finishing workgroup: its rows' protected bytes [64][kp], the scales [k]
-    // and the tile's protected activations [16 MT][kp32], when kp <= PM
-    __shared__ __attribute__((aligned(16))) uint4 s_prot_mem[(64 * PM + 4 * PM + 32 * MT * PM) / 16];
-    static_assert(WV * 4 * 64 * 4 <= WV * 16 * OS, "the wave tiles fit the output staging");
-    uint4 *s_tab4 = s_tab_mem;  // (plain pointers: the LDS DMA builtin takes one)
-    uint4 *s_prot4 = s_prot_mem;
-    f32x4_t *s_red = reinterpret_cast<f32x4_t *>(s_rm);
-    const uint16_t *s_tab = reinterpret_cast<const uint16_t *>(s_tab4);
-    const int t = threadIdx.x, lane = t & 63, g = lane >> 4, r16 = lane & 15;
-    const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-    const int64_t Q = la.q;
-    const int64_t unit = int64_t(blockIdx.x) / Q, q = int64_t(blockIdx.x) - unit * Q;
-    const int64_t rg = unit / la.mtiles, mtile = unit - rg * la.mtiles;
-    const int64_t mt0 = mtile * (16 * MT);  // first token of the tile
-    const int64_t nb = a.pitch / 16;
-    const int64_t b0 = (q * WV + wave) * TPW;
-    const int64_t nt = ((b0 + TPW < la.nblk) ? b0 + TPW : la.nblk) - b0;  // this wave's tiles (may be <= 0)
-    const int64_t blast = (nt > 0) ? b0 + nt - 1 : 0;                   // a wave without tiles reloads tile 0
-    const bool fin = q == Q - 1;
-
-    // tables by DMA, then the first tiles (unconditional, clamped)
-    for (int v = wave; v < S * 4; v += WV) {
-        const uint4 *src = reinterpret_cast<const uint4 *>(a.tabh[v >> 2]) + (v & 3) * 64 + lane;
-        __builtin_amdgcn_global_load_lds(src, s_tab4 + 64 * v, 16, 0, 0);
-    }
-    // the finishing workgroup's protected-column data: payload rows and the
-    // tile's activations by DMA (rows past d_out clamped: those bytes are
-    // never read), the scales by plain loads once the tiles are requested
-    const int64_t kp = q8_pitch(a.k);
-    const bool prot_lds = fin && a.k > 0 && kp <= PM;
-    int8_t *s_q8 = reinterpret_cast<int8_t *>(s_prot4);
-    float *s_sc = reinterpret_cast<float *>(s_prot4 + 4 * PM);
-    uint16_t *s_xp = reinterpret_cast<uint16_t *>(s_prot4 + 4 * PM + PM / 4);
-    if (prot_lds) {
-        const int64_t n0p = rg * 64;
-        const int64_t avail = ((a.d_out - n0p < 64) ? a.d_out - n0p : 64) * kp;  // bytes of real rows
-        const int nq8 = int((64 * kp) / 1024 + ((64 * kp) % 1024 != 0));
-        for (int v = wave; v < nq8; v += WV) {
-            const int64_t e = int64_t(v) * 1024 + 16 * lane;
-            const int64_t es = (e + 16 <= avail) ? e : avail - 16;
-            __builtin_amdgcn_global_load_lds(reinterpret_cast<const uint4 *>(a.q8 + n0p * kp + es), s_prot4 + 64 * v, 16, 0, 0);
-        }
-        // 16 MT rows x kp32 bf16, whole KiB (kp32 % 32 == 0)
-        const int nxp = int((32 * MT * a.kp32) / 1024);
-        const uint4 *xsrc = reinterpret_cast<const uint4 *>(a.Xp + mt0 * a.kp32);
-        for (int v = wave; v < nxp; v += WV)
-            __builtin_amdgcn_global_load_lds(xsrc + 64 * v + lane, s_prot4 + 4 * PM + PM / 4 + 64 * v, 16, 0, 0);
-    }
-    const int64_t ebase = ((rg * nb) << 10) + (int64_t(r16) << 4) + 4 * g;  // row r16 of the group, chunk 4 g of tile 0
-    const uint16_t *xbase = a.Xt + (mt0 + r16) * a.Kp + 32 * g;
-    LaneWords<S> buf[PF];
-    u32x4_t xr[4][MT];
-    // the scales (one per thread, k <= 256) into a register, stored to LDS
-    // after the tiles; then the words of the first PF tiles and the first
-    // tile's X~ fragments. The load of the scale is unconditional (a valid
-    // dummy address where it is not needed) so that nothing waits for it
-    // here. The wait before the barrier leaves the second tile's words and the
-    // X~ fragments in flight (issue order: DMAs, scale, words, X~).
-    constexpr int LPT = 8 * S;
-    const float *scp = prot_lds ? a.scale + ((t < a.k) ? t : a.k - 1) : reinterpret_cast<const float *>(a.Xt);
-    const float scv = *scp;
-#pragma unroll
-    for (int u = 0; u < PF; ++u) {
-        const int64_t b = (b0 + u < blast) ? b0 + u : blast;
-        lane_gemm_words<S>(buf[u], a, ebase + (b << 10));
-    }
-    {
-        const int64_t b = (b0 < blast) ? b0 : blast;
-#pragma unroll
-        for (int qs = 0; qs < 4; ++qs) lane_gemm_x<MT>(xr[qs], xbase + b * BK + 8 * qs, a.Kp);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-    wait_vm<(PF - 1) * LPT + 4 * MT>();
-    lds_barrier();
-
-    f32x4_t acc[MT][4];
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int u = 0; u < TPW; ++u) {
-        if (u < nt) {
-            const int64_t bn = (b0 + u + 1 < blast) ? b0 + u + 1 : blast;
-#pragma unroll
-            for (int qs = 0; qs < 4; ++qs) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const u32x4_t bq = lane_gemm_decode<S>(buf[u % PF], s_tab, qs, j);
-#pragma unroll
-                    for (int i = 0; i < MT; ++i)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xr[qs][i]),
-                                                                            __builtin_bit_cast(bf16x8_t, bq), acc[i][j], 0, 0, 0);
-                }
-                if (u + 1 < TPW) lane_gemm_x<MT>(xr[qs], xbase + bn * BK + 8 * qs, a.Kp);
-                // keep the next tile's k-slice loads right behind this
-                // slice's MFMAs (the scheduler would sink them to the end
-                // of the tile and expose their latency)
-                __builtin_amdgcn_sched_barrier(0);
-            }
-        }
-        if (u + PF < TPW) {
-            const int64_t b = (b0 + u + PF < blast) ? b0 + u + PF : blast;
-            lane_gemm_words<S>(buf[u % PF], a, ebase + (b << 10));
-        }
-    }
-
-    // the four wave tiles of each token group, added in wave order; wave i
-    // keeps group i
-    if (prot_lds && t < a.k) s_sc[t] = scv;
-    f32x4_t sum[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) sum[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) s_red[(wave * 4 + j) * 64 + lane] = acc[i][j];
-        __syncthreads();
-        if (wave == i) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                sum[j] = s_red[j * 64 + lane];
-#pragma unroll
-                for (int w = 1; w < WV; ++w) sum[j] = sum[j] + s_red[(w * 4 + j) * 64 + lane];
-            }
-        }
-        __syncthreads();
-    }
-    if (wave >= MT) return;
-    const int ig = wave;                     // this wave's token group
-    const int64_t m0 = mt0 + 16 * ig;        // its first token
-
-    bool timed_out = false;
-    if (Q > 1) {
-        uint64_t *slots = a.slots + ((unit * (Q - 1)) * MT + ig) * 1024 + lane;
-        if (!fin) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    __hip_atomic_store(slots + q * (1024 * MT) + (4 * j + r) * 64, (uint64_t(1) << 32) | __float_as_uint(sum[j][r]),
-                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            return;
-        }
-        f32x4_t part[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) part[j] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
-        // a workspace poisoned by an earlier give-up may hold flags of no
-        // slice of this call: then the sums are discarded and nothing is
-        // cleared (this call's slices still set every flag, so the polls end;
-        // the word's load overlaps them)
-        const bool poisoned = __hip_atomic_load(a.poison, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-        // two slices per round trip (the second clamped to the last slice:
-        // a re-read), added in slice order
-        for (int64_t q0 = 0; q0 < Q - 1 && !timed_out; q0 += 2) {
-            uint64_t pw[2][16];
-            const int64_t qs[2] = {q0, (q0 + 1 < Q - 1) ? q0 + 1 : Q - 2};
-            for (int spin = 0;; ++spin) {
-                if (spin >= a.spin_limit) {  // never expected: report, rather than hang
-                    timed_out = true;
-                    break;
-                }
-                bool ready = true;
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-#pragma unroll
-                    for (int e = 0; e < 16; ++e) {
-                        pw[h][e] = __hip_atomic_load(slots + qs[h] * (1024 * MT) + e * 64, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-                        ready &= (pw[h][e] >> 32) != 0;
-                    }
-                if (__all(ready)) break;
-                __builtin_amdgcn_s_sleep(1);
-            }
-            if (timed_out) break;
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                if (q0 + h >= Q - 1) break;
-#pragma unroll
-                for (int e = 0; e < 16; ++e) part[e >> 2][e & 3] += __uint_as_float(uint32_t(pw[h][e]));
-            }
-        }
-        // every slot consumed: clear them for the next call (after a give-up
-        // they stay, and the workspace is marked)
-        if (!poisoned && !timed_out) {
-            for (int64_t q0 = 0; q0 < Q - 1; ++q0)
-#pragma unroll
-                for (int e = 0; e < 16; ++e)
-                    __hip_atomic_store(slots + q0 * (1024 * MT) + e * 64, uint64_t(0), __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
-        }
-        gemm_report(a, poisoned, timed_out);
-        timed_out = timed_out || poisoned;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) sum[j] = part[j] + sum[j];
-    }
-
-    const int64_t n0 = rg * 64;
-    // protected term: X[:, idx] (bf16) times bf16(value(q8) s), from LDS when staged
-    if (a.k > 0) {
-        for (int64_t qq = 0; qq < a.kp32 / 32; ++qq) {
-            const int64_t p0 = 32 * qq + 8 * g;
-            float sc[8];
-#pragma unroll
-            for (int e = 0; e < 8; ++e) sc[e] = (p0 + e < a.k) ? (prot_lds ? s_sc[p0 + e] : a.scale[p0 + e]) : 0.0f;
-            const u32x4_t xv = prot_lds ? *reinterpret_cast<const u32x4_t *>(s_xp + (16 * ig + r16) * a.kp32 + p0)
-                                        : *reinterpret_cast<const u32x4_t *>(a.Xp + (m0 + r16) * a.kp32 + p0);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int64_t row = n0 + 16 * j + r16;
-                uint2 qv = make_uint2(0u, 0u);
-                if (row < a.d_out && p0 < kp)
-                    qv = prot_lds ? *reinterpret_cast<const uint2 *>(s_q8 + (16 * j + r16) * kp + p0)
-                                  : *reinterpret_cast<const uint2 *>(a.q8 + row * kp + p0);
-                float v[8];
-                payload8(qv, sc, v, a.pfmt);
-                const u32x4_t bp = u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
-                                           pack_bf16x2(v[6], v[7])};
-                sum[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, xv),
-                                                                 __builtin_bit_cast(bf16x8_t, bp), sum[j], 0, 0, 0);
-            }
-        }
-    }
-    // LoRA into the tile (element r of sum[j] is token m0 + 4 g + r, row
-    // n0 + 16 j + lane % 16), staged in this wave's part of LDS as fp32
-    // [16][64 + 4], then Y in 8-output segments (16-byte stores when Y allows)
-    float *s_out = s_rm + ig * (16 * OS);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int64_t n = n0 + 16 * j + r16;
-        const int64_t nc = (n < a.d_out) ? n : a.d_out - 1;
-        float bl[BSQ_MAX_LORA_RANK];
-#pragma unroll
-        for (int qr = 0; qr < BSQ_MAX_LORA_RANK; ++qr) bl[qr] = (qr < a.rank) ? bf16_to_f32(a.B[nc * a.rank + qr]) : 0.0f;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int64_t m = 4 * g + r;
-            float v = timed_out ? __builtin_nanf("") : sum[j][r];
-            if (a.rank > 0) {
-                const float *Tm = a.T + (m0 + m) * BSQ_MAX_LORA_RANK;
-#pragma unroll
-                for (int qr = 0; qr < BSQ_MAX_LORA_RANK; ++qr) v = __builtin_fmaf(bl[qr], Tm[qr], v);
-            }
-            s_out[m * OS + 16 * j + r16] = v;
-        }
-    }
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // this wave's LDS writes (the region is its own)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const int e = h * 64 + lane, ml = e >> 3, nl = 8 * (e & 7);  // 16 tokens x 8 segments
-        const int64_t m = m0 + ml, n = n0 + nl;
-        if (m >= a.M || n >= a.d_out) continue;
-        const float4 lo = *reinterpret_cast<const float4 *>(s_out + ml * OS + nl);
-        const float4 hi = *reinterpret_cast<const float4 *>(s_out + ml * OS + nl + 4);
-        const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-        if (a.y_vec && n + 8 <= a.d_out) {
-            if (a.y_bf16) {
-                *reinterpret_cast<u32x4_t *>(static_cast<uint16_t *>(a.Y) + m * a.ldy + n) =
-                    u32x4_t{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7])};
-            } else {
-                float4 *dst = reinterpret_cast<float4 *>(static_cast<float *>(a.Y) + m * a.ldy + n);
-                dst[0] = lo;
-                dst[1] = hi;
-            }
-        } else {
-#pragma unroll
-            for (int c = 0; c < 8; ++c) {
-                if (n + c >= a.d_out) break;
-                if (a.y_bf16) static_cast<uint16_t *>(a.Y)[m * a.ldy + n + c] = f32_to_bf16(v[c]);
-                else static_cast<float *>(a.Y)[m * a.ldy + n + c] = v[c];
-            }
-        }
-    }
-}
-
-// Tiles per wave of the streaming kernel for `units` (64-row group, token
-// tile) pairs of MT token groups. One token group: the largest of 4, 2, 1
-// whose grid still holds 2048 waves (a wave's tiles are short, so more of them
-// in flight hide the latency). Four token groups (192 VGPRs, two waves per
-// SIMD, four times the MFMA work per tile): the smallest tile count whose grid
-// fits in one wave per SIMD (1024 waves), which measured fastest on the
-// Qwen3-8B shapes (the q projection at 2 tiles, gate and up at 8). Then raised
-// while the slices' partials would not fit in GEMM_SLOT_BYTES (1024 MT
-// flagged values per slice but the last).
-int lane_gemm_tpw(int64_t units, int64_t nblk, int mt)
-{
-    auto slices = [&](int tpw) { return (nblk + 4 * tpw - 1) / (4 * tpw); };
-    auto slot_bytes = [&](int tpw) { return (slices(tpw) - 1) * units * 1024 * mt * 8; };
-    int tpw = 1;
-    if (mt == 1) {
-        for (int c = 4; c > 1; c >>= 1)
-            if (units * slices(c) * 4 >= 2048) {
-                tpw = c;
-                break;
-            }
-    } else {
-        while (tpw < 16 && units * slices(tpw) * 4 > 1024) tpw *= 2;
-    }
-    while (tpw < 16 && slot_bytes(tpw) > GEMM_SLOT_BYTES) tpw *= 2;
-    return (slot_bytes(tpw) > GEMM_SLOT_BYTES) ? 0 : tpw;  // 0: does not fit
-}
-
-template <int S, int TPW, int MT>
-hipError_t launch_lane_t(const LaneGemmArgs &la, hipStream_t st)
-{
-    hipLaunchKernelGGL((gemm_lane_kernel<S, TPW, MT>), dim3(unsigned(la.rgs * la.mtiles * la.q)), dim3(256), 0, st, la);
-    return hipGetLastError();
-}
-
-template <int S, int MT>
-hipError_t launch_lane_m(const LaneGemmArgs &la, int tpw, hipStream_t st)
-{
-    switch (tpw) {
-    case 1: return launch_lane_t<S, 1, MT>(la, st);
-    case 2: return launch_lane_t<S, 2, MT>(la, st);
-    case 4: return launch_lane_t<S, 4, MT>(la, st);
-    case 8: return launch_lane_t<S, 8, MT>(la, st);
-    default: return launch_lane_t<S, 16, MT>(la, st);
-    }
-}
-
-template <int S>
-hipError_t launch_lane(const LaneGemmArgs &la, int tpw, int mt, hipStream_t st)
-{
-    if (mt == 1) return launch_lane_m<S, 1>(la, tpw, st);
-    if (mt == 2) return launch_lane_m<S, 2>(la, tpw, st);
-    return launch_lane_m<S, 4>(la, tpw, st);
-}
-
-// ---------------------------------------------------------------------------
 // Codes of b != d bits per chunk (a codec with a linear encoder): the
 // 2^b-entry decoder table does not suit the MFMA paths' decode, so the
 // product runs in fp32 over LDS tiles of decoded weights. A workgroup of 256
@@ -1251,7 +800,7 @@ GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     ks = std::min<int64_t>(ks, p.ksteps / 2);
     ks = std::min<int64_t>(ks, 8);
     p.ksplit = std::max<int64_t>(ks, 1);
-    p.t_off = size_t(GEMM_HDR + GEMM_SLOT_BYTES);
+    p.t_off = size_t(GEMM_HDR);
     p.xt_off = p.t_off + align256(size_t(p.Mp) * BSQ_MAX_LORA_RANK * 4);
     p.xp_off = p.xt_off + align256(size_t(p.Mp) * size_t(p.Kp) * 2);
     p.part_off = p.xp_off + align256(size_t(p.Mp) * size_t(std::max<int64_t>(p.kp32, 32)) * 2);
@@ -1329,7 +878,7 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 
 const float *gemm_lora_t(const void *ws)
 {
-    return reinterpret_cast<const float *>(static_cast<const char *>(ws) + GEMM_HDR + GEMM_SLOT_BYTES);
+    return reinterpret_cast<const float *>(static_cast<const char *>(ws) + GEMM_HDR);
 }
 
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M)
@@ -1375,10 +924,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
     a.ksplit = int(p.ksplit);
     a.part = reinterpret_cast<float *>(wb + p.part_off);
     a.np = p.np;
-    a.slots = reinterpret_cast<uint64_t *>(wb + GEMM_HDR);
-    a.poison = static_cast<uint32_t *>(ws);
-    a.err = err;
-    a.spin_limit = wait_limit();
+    (void)err;  // (no block waits for another: there is nothing to report)
     a.pfmt = cfg.protect_format;
 
     PrepArgs pa{};
@@ -1435,26 +981,6 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
         g.ldy = ldy;
         g.Y = Y;
         return (cfg.d == 8) ? launch_generic_t<8, 16>(S, g, st) : launch_generic_t<16, 8>(S, g, st);
-    }
-    if (cfg.d == 8 && M <= LANE_GEMM_MAX_M) {
-        // small and moderate M: the streaming kernel, when its slices'
-        // partials fit
-        LaneGemmArgs la{};
-        la.g = a;
-        const int mt = (M <= 16) ? 1 : (M <= 32) ? 2 : LANE_GEMM_MAX_MT;
-        la.nblk = p.ksteps;
-        la.rgs = (L.d_out + 63) / 64;
-        la.mtiles = (M + 16 * mt - 1) / (16 * mt);
-        const int tpw = lane_gemm_tpw(la.rgs * la.mtiles, la.nblk, mt);
-        if (tpw > 0) {
-            la.q = (la.nblk + 4 * tpw - 1) / (4 * tpw);
-            switch (S) {
-            case 1: return launch_lane<1>(la, tpw, mt, st);
-            case 2: return launch_lane<2>(la, tpw, mt, st);
-            case 3: return launch_lane<3>(la, tpw, mt, st);
-            default: return launch_lane<4>(la, tpw, mt, st);
-            }
-        }
     }
     if (cfg.d == 8) {
         switch (S) {

@@ -285,7 +285,7 @@ def test_product_workspaces_hold_a_header():
     """GEMV and GEMM workspaces start with a 256-byte header for the poison
     word, so they exceed their slot and scratch areas by at least that."""
     cfg = bsq.Config()
-    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 64, 256, 1) >= 256 + (8 << 20)
+    assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMM, 1, 64, 256, 1) >= 256 + 16 * 16 * 4
     assert bsq.bsq_workspace_bytes(cfg, bsq.OP_GEMV, 1, 64, 256) >= 256 + 8 * 16 * 4
 
 
