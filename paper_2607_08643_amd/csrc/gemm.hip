@@ -777,11 +777,15 @@ struct GemmPlan {
     size_t t_off, xt_off, xp_off, part_off, total;
 };
 
-GemmPlan gemm_plan(int64_t d_out, int64_t d_in, int64_t M, int64_t k)
+GemmPlan gemm_plan(int d, int64_t d_out, int64_t d_in, int64_t M, int64_t k)
 {
     GemmPlan p{};
     p.mt = (M <= 16) ? 1 : (M <= 64) ? 4 : 8;
-    p.nt = 2;
+    // d = 8: 64-row blocks up to 16 tokens, and up to 64 tokens where both
+    // dimensions are at most 4096 (twice the blocks, so fewer K splits and a
+    // lighter split-K sum; they measured faster there, not on the longer
+    // projections); 128-row blocks otherwise
+    p.nt = (d == 8 && (M <= 16 || (M <= 64 && d_out <= 4096 && d_in <= 4096))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -869,7 +873,12 @@ hipError_t launch_main(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 template <int D, int S>
 hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 {
-    if (p.mt == 1) return launch_main<D, S, 1, 2>(a, p, st);
+    if constexpr (D == 8) {
+        if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
+        if (p.mt == 4 && p.nt == 1) return launch_main<D, S, 4, 1>(a, p, st);
+    } else {
+        if (p.mt == 1) return launch_main<D, S, 1, 2>(a, p, st);
+    }
     if (p.mt == 4) return launch_main<D, S, 4, 2>(a, p, st);
     return launch_main<D, S, 8, 2>(a, p, st);
 }
@@ -884,7 +893,7 @@ const float *gemm_lora_t(const void *ws)
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M)
 {
     const int64_t k = cfg.protect_num ? (d_in * cfg.protect_num + cfg.protect_den - 1) / cfg.protect_den : 0;
-    return gemm_plan(d_out, d_in, M, k).total;
+    return gemm_plan(cfg.d, d_out, d_in, M, k).total;
 }
 
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &L, const bsq_lora *lora,
@@ -892,7 +901,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
                        int32_t *err, hipStream_t st)
 {
     if (M == 0 || L.d_out == 0) return hipSuccess;
-    const GemmPlan p = gemm_plan(L.d_out, L.d_in, M, L.k);
+    const GemmPlan p = gemm_plan(cfg.d, L.d_out, L.d_in, M, L.k);
     char *wb = static_cast<char *>(ws);
     GemmArgs a{};
     const char *cb = static_cast<const char *>(codec);
