@@ -781,11 +781,12 @@ GemmPlan gemm_plan(int d, int64_t d_out, int64_t d_in, int64_t M, int64_t k)
 {
     GemmPlan p{};
     p.mt = (M <= 16) ? 1 : (M <= 64) ? 4 : 8;
-    // d = 8: 64-row blocks up to 16 tokens, and up to 64 tokens where both
-    // dimensions are at most 4096 (twice the blocks, so fewer K splits and a
-    // lighter split-K sum; they measured faster there, not on the longer
-    // projections); 128-row blocks otherwise
-    p.nt = (d == 8 && (M <= 16 || (M <= 64 && d_out <= 4096 && d_in <= 4096))) ? 1 : 2;
+    // d = 8: 64-row blocks up to 16 tokens, up to 64 tokens where both
+    // dimensions are at most 4096, and for at most 2048 rows of at most 4096
+    // inputs (twice the blocks, so fewer K splits and a lighter split-K sum;
+    // they measured faster there, not on the longer projections); 128-row
+    // blocks otherwise
+    p.nt = (d == 8 && (M <= 16 || (d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048)))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -876,6 +877,7 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
     if constexpr (D == 8) {
         if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
         if (p.mt == 4 && p.nt == 1) return launch_main<D, S, 4, 1>(a, p, st);
+        if (p.mt == 8 && p.nt == 1) return launch_main<D, S, 8, 1>(a, p, st);
     } else {
         if (p.mt == 1) return launch_main<D, S, 1, 2>(a, p, st);
     }
