@@ -13,13 +13,13 @@
 // bf16), so the weight tile never goes through LDS.
 // The inputs of one K step (128) are permuted identically on both operands so
 // that a lane's fragments are whole chunks: MFMA input group g = lane / 16 and
-// fragment q cover inputs 32 g + 8 q .. + 8 of the step. X~ tiles reach LDS
-// through registers into two LDS slots (loaded two steps ahead, stored one
-// step ahead), the code and gain words two steps ahead in registers; one
-// barrier per step. The protected term X[:, idx] (q8 s)^T and LoRA are added in the
-// epilogue; the protected products go through the same MFMA with the
-// dequantised int8 weights rounded to bf16, so every weight of W_hat meets
-// its activation as bf16 exactly once.
+// fragment q cover inputs 32 g + 8 q .. + 8 of the step. The X~ tile and the
+// code and gain words of a K step reach LDS by DMA (global_load_lds) into
+// rings of NS slots, issued NS - 1 steps ahead; one barrier per step. The
+// protected term X[:, idx] (q8 s)^T and LoRA are added in the epilogue, both
+// through the same MFMA: the dequantised int8 weights rounded to bf16 (so
+// every weight of W_hat meets its activation as bf16 exactly once), and T
+// split exactly into three bf16 parts against bf16 B.
 //
 // Split K: when weight blocks x token tiles alone would leave the chip mostly
 // idle, the K steps are divided over ksplit blocks per tile (grid z). Every
@@ -218,6 +218,17 @@ __device__ __forceinline__ void wait_vm()
 // LDS of one workgroup (gfx950: 160 KiB per compute unit).
 constexpr int GEMM_LDS_BYTES = 160 * 1024;
 
+// Workgroups per compute unit of the main kernel. The 16-token, 64-row block
+// at d = 8 (57 VGPRs) runs three where three fit in LDS (1 or 2 stages: 4
+// ring slots of X~ and weight words and one table copy each): its steps are
+// short, and three blocks' waits overlap. Every other shape runs one, with
+// as many ring slots as fit. The plan sizes its K splits by the same count.
+constexpr int gemm_wg_per_cu(int d, int s, int mt, int nt)
+{
+    return (d == 8 && mt == 1 && nt == 1 && 3 * (4 * (16 * mt * 256 + nt * s * 192 * 16) + s * 4096) <= GEMM_LDS_BYTES)
+               ? 3 : 1;
+}
+
 // Shape of the main kernel. A workgroup of 8 waves owns BN = 64 NT weight
 // rows and BM = 16 MT tokens. Wave w owns the row set rs = w % 4 (NT groups of
 // 16 rows: block rows 16 (NT rs + j) + lane % 16) and the half kh = w / 4 of
@@ -235,19 +246,21 @@ struct GemmShape {
     static constexpr int WU = (D == 8) ? 192 : 128;
     static constexpr int XSLOT = BM * 256;            // bytes: [BM][128] bf16
     static constexpr int WSLOT = NT * S * WU * 16;    // bytes: [NT][S][codes | gains]
+    static constexpr int WG_PER_CU = gemm_wg_per_cu(D, S, MT, NT);
     // fp16 decoder tables (d = 8) [S][256 codes][TC copies][8]: lane l reads
     // copy l % TC, which spreads the random lookups of a wave over the LDS
     // banks; 8 copies where three ring slots still fit, else one
-    static constexpr int TC = (D == 8 && (GEMM_LDS_BYTES - S * 4096 * 8) / (XSLOT + WSLOT) >= 3) ? 8 : 1;
+    static constexpr int TC = (D == 8 && WG_PER_CU == 1 && (GEMM_LDS_BYTES - S * 4096 * 8) / (XSLOT + WSLOT) >= 3) ? 8 : 1;
     static constexpr int TAB = (D == 8) ? S * 4096 * TC : 0;
-    static constexpr int NS_FIT = (GEMM_LDS_BYTES - TAB) / (XSLOT + WSLOT);
-    static constexpr int NS = NS_FIT < 8 ? NS_FIT : 8;
+    static constexpr int NS_FIT = (GEMM_LDS_BYTES / WG_PER_CU - TAB) / (XSLOT + WSLOT);
+    static constexpr int NS = (WG_PER_CU > 1) ? 4 : NS_FIT < 8 ? NS_FIT : 8;
     static constexpr int NXI = BM / 4;              // X~ DMA wave instructions per step
     static constexpr int NWI = NT * S * WU / 64;    // weight DMA wave instructions per step
     static constexpr int NI = NXI + NWI;            // wave w issues instructions w, w + 8, ... < NI
     static constexpr int PMAX = (NI + 7) / 8, PMIN = NI / 8;  // DMA instructions per wave and step
     static constexpr size_t LDS = size_t(NS) * (XSLOT + WSLOT) + TAB;
     static_assert(NS >= 2, "two pipeline stages fit in LDS");
+    static_assert(LDS * WG_PER_CU <= size_t(GEMM_LDS_BYTES), "the workgroups of a compute unit fit in its LDS");
     static_assert(MT * NT * 4096 <= NS * XSLOT, "the exchange of the two K halves fits in the X~ ring");
     static_assert((NS - 1) * PMAX <= 63, "wait count fits vmcnt");
     static_assert(WU % 64 == 0, "a DMA instruction stays within one (tile, stage)");
@@ -266,7 +279,8 @@ struct GemmShape {
 // lane's fragment is a whole chunk (d = 8) or half a chunk (d = 16): MFMA
 // input group g = lane / 16 of k-slice q covers inputs 32 g + 8 q .. + 8.
 template <int D, int S, int MT, int NT>
-__global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(GemmShape<D, S, MT, NT>::WG_PER_CU * 2)))
+void gemm_kernel(const GemmArgs a)
 {
     using G = GemmShape<D, S, MT, NT>;
     typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
@@ -280,9 +294,26 @@ __global__ __launch_bounds__(512) void gemm_kernel(const GemmArgs a)
     const int t = threadIdx.x, lane = t & 63, g = lane >> 4, r16 = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
     const int rs = wave & 3, kh = wave >> 2;
-    const int64_t n0 = int64_t(blockIdx.x) * G::BN;  // first row of the block
-    const int64_t m0 = int64_t(blockIdx.y) * G::BM;  // first token of the block
-    const int z = blockIdx.z;
+    // Tile of the block. The workgroups of a launch go to the 8 XCDs in turn
+    // (linear id mod 8), each XCD with its own L2. With K split and token
+    // tiles of 64 or more, consecutive tiles in (token tile, row block,
+    // split) order are given to one XCD, so that an XCD reads only its splits'
+    // share of X~ and keeps both token tiles of a row block (which share its
+    // weights); a bijection whenever the block count is a multiple of 8.
+    int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+    if (MT >= 4 && a.ksplit > 1) {
+        const int nx = gridDim.x, ny = gridDim.y, total = nx * ny * int(gridDim.z);
+        if ((total & 7) == 0) {
+            const int lin = bx + nx * (by + ny * bz);
+            const int lg = (lin & 7) * (total >> 3) + (lin >> 3);
+            by = lg % ny;
+            bx = (lg / ny) % nx;
+            bz = lg / (ny * nx);
+        }
+    }
+    const int64_t n0 = int64_t(bx) * G::BN;  // first row of the block
+    const int64_t m0 = int64_t(by) * G::BM;  // first token of the block
+    const int z = bz;
     const int64_t kb = a.ksteps * z / a.ksplit, ke = a.ksteps * (z + 1) / a.ksplit;
     const int64_t nb = a.pitch / 16;                 // 16-chunk blocks per row
     const int64_t rbmax = (a.d_out + 63) / 64 - 1;   // last 64-row tile of the planes
@@ -777,16 +808,20 @@ struct GemmPlan {
     size_t t_off, xt_off, xp_off, part_off, total;
 };
 
-GemmPlan gemm_plan(int d, int64_t d_out, int64_t d_in, int64_t M, int64_t k)
+GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, int64_t k)
 {
     GemmPlan p{};
-    p.mt = (M <= 16) ? 1 : (M <= 64) ? 4 : 8;
-    // d = 8: 64-row blocks up to 16 tokens, up to 64 tokens where both
+    // token tiles of 16 tokens up to 16 tokens, and at d = 8 up to 32 tokens
+    // and for projections of at most 2048 rows up to 64 tokens (these blocks
+    // run three per compute unit, and a block's token tiles share its
+    // weights through L2); 64-token tiles up to 64 tokens, else 128
+    p.mt = (M <= 16 || (d == 8 && (M <= 32 || (M <= 64 && d_out <= 2048)))) ? 1 : (M <= 64) ? 4 : 8;
+    // d = 8: 64-row blocks with 16-token tiles, up to 64 tokens where both
     // dimensions are at most 4096, and for at most 2048 rows of at most 4096
     // inputs (twice the blocks, so fewer K splits and a lighter split-K sum;
     // they measured faster there, not on the longer projections); 128-row
     // blocks otherwise
-    p.nt = (d == 8 && (M <= 16 || (d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048)))) ? 1 : 2;
+    p.nt = (d == 8 && (p.mt == 1 || (d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048)))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -800,10 +835,14 @@ GemmPlan gemm_plan(int d, int64_t d_out, int64_t d_in, int64_t M, int64_t k)
     // split K as far as one round of workgroups over the 256 compute units
     // allows (a second, partial round would double the time), keeping at least
     // 2 K steps per split and at most 8 splits (the partials of all splits
-    // are written and read once more: at most 256 tiles' worth, 16 MiB)
-    int64_t ks = 256 / (tiles > 0 ? tiles : 1);
-    ks = std::min<int64_t>(ks, p.ksteps / 2);
-    ks = std::min<int64_t>(ks, 8);
+    // are written and read once more: at most 256 tiles' worth, 16 MiB).
+    // Blocks that run three per compute unit: up to 768 workgroups, with at
+    // least 8 K steps per split (shorter splits measured slower), but never
+    // fewer splits than the rule above.
+    const int64_t nt_ = std::max<int64_t>(tiles, 1);
+    int64_t ks = std::min<int64_t>({256 / nt_, p.ksteps / 2, 8});
+    const int wpc = gemm_wg_per_cu(d, stages, int(p.mt), int(p.nt));
+    if (wpc > 1) ks = std::max(ks, std::min<int64_t>({256 * wpc / nt_, p.ksteps / 8, 8}));
     p.ksplit = std::max<int64_t>(ks, 1);
     p.t_off = size_t(GEMM_HDR);
     p.xt_off = p.t_off + align256(size_t(p.Mp) * BSQ_MAX_LORA_RANK * 4);
@@ -895,7 +934,7 @@ const float *gemm_lora_t(const void *ws)
 size_t gemm_ws_bytes(const bsq_config &cfg, int64_t d_out, int64_t d_in, int64_t M)
 {
     const int64_t k = cfg.protect_num ? (d_in * cfg.protect_num + cfg.protect_den - 1) / cfg.protect_den : 0;
-    return gemm_plan(cfg.d, d_out, d_in, M, k).total;
+    return gemm_plan(cfg.d, cfg.stages, d_out, d_in, M, k).total;
 }
 
 hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer &L, const bsq_lora *lora,
@@ -903,7 +942,7 @@ hipError_t launch_gemm(const bsq_config &cfg, const void *codec, const bsq_layer
                        int32_t *err, hipStream_t st)
 {
     if (M == 0 || L.d_out == 0) return hipSuccess;
-    const GemmPlan p = gemm_plan(cfg.d, L.d_out, L.d_in, M, L.k);
+    const GemmPlan p = gemm_plan(cfg.d, cfg.stages, L.d_out, L.d_in, M, L.k);
     char *wb = static_cast<char *>(ws);
     GemmArgs a{};
     const char *cb = static_cast<const char *>(codec);

@@ -214,7 +214,7 @@ def test_gemv_d16_activation_range(scale, gpu):
 
 
 # Long rows: the K steps of a tile are split over several blocks (ragged
-# split sizes, a partial last step) and reduced by the last block to arrive.
+# split sizes, a partial last step) and summed in split order by a second launch.
 SPLITK = [
     ("splitk-200x2600-d8", 200, 2600, dict(d=8, hidden=8), torch.bfloat16, 1, False),
     ("splitk-130x2608-d16", 130, 2608, dict(d=16, hidden=16), torch.bfloat16, 1, False),
