@@ -518,17 +518,19 @@ void gemm_kernel(const GemmArgs a)
 
     // protected term (split 0, by the kh = 1 waves): X[:, idx] (bf16) times
     // bf16(value(q8) s), the weights of lane row 16 (NT rs + j) + lane % 16 at
-    // positions 32 qq + 8 g + e; two slices of 32 positions per round, all
+    // positions 32 qq + 8 g + e; two slices of 32 positions per round (one
+    // with 256-token tiles, whose activations fill the registers), all
     // their loads issued together (stored bytes as one 8-byte word per row;
     // positions past k read as zero)
     if (kh == 1 && z == 0 && a.k > 0) {
         const int64_t kp = q8_pitch(a.k), nq = a.kp32 / 32;
-        for (int64_t q0 = 0; q0 < nq; q0 += 2) {
-            uint2 qv[2][NT];
-            float sc[2][8];
-            u32x4_t xv[2][MT];
+        constexpr int H = (MT > 8) ? 1 : 2;
+        for (int64_t q0 = 0; q0 < nq; q0 += H) {
+            uint2 qv[H][NT];
+            float sc[H][8];
+            u32x4_t xv[H][MT];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < H; ++h) {
                 const bool live = q0 + h < nq;
                 const int64_t p0 = 32 * (q0 + h) + 8 * g;
 #pragma unroll
@@ -545,7 +547,7 @@ void gemm_kernel(const GemmArgs a)
                                     : u32x4_t{0u, 0u, 0u, 0u};
             }
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
+            for (int h = 0; h < H; ++h) {
 #pragma unroll
                 for (int j = 0; j < NT; ++j) {
                     float v[8];
@@ -814,14 +816,18 @@ GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, in
     // token tiles of 16 tokens up to 16 tokens, and at d = 8 up to 32 tokens
     // and for projections of at most 2048 rows up to 64 tokens (these blocks
     // run three per compute unit, and a block's token tiles share its
-    // weights through L2); 64-token tiles up to 64 tokens, else 128
-    p.mt = (M <= 16 || (d == 8 && (M <= 32 || (M <= 64 && d_out <= 2048)))) ? 1 : (M <= 64) ? 4 : 8;
+    // weights through L2); 64-token tiles up to 64 tokens, else 128; at
+    // d = 16 above 128 tokens one 256-token tile of 64-row blocks, so that
+    // each chunk's entry of the 2^16-entry table is gathered once per block
+    // rather than once per token tile (at d = 8 the 256-token tile measured
+    // slower: its decode is cheap and two ring slots are too few)
+    p.mt = (M <= 16 || (d == 8 && (M <= 32 || (M <= 64 && d_out <= 2048)))) ? 1 : (M <= 64) ? 4 : (d == 16 && M > 128) ? 16 : 8;
     // d = 8: 64-row blocks with 16-token tiles, up to 64 tokens where both
     // dimensions are at most 4096, and for at most 2048 rows of at most 4096
     // inputs (twice the blocks, so fewer K splits and a lighter split-K sum;
     // they measured faster there, not on the longer projections); 128-row
     // blocks otherwise
-    p.nt = (d == 8 && (p.mt == 1 || (d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048)))) ? 1 : 2;
+    p.nt = (p.mt == 16) ? 1 : (d == 8 && (p.mt == 1 || (d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048)))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -919,6 +925,7 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
         if (p.mt == 8 && p.nt == 1) return launch_main<D, S, 8, 1>(a, p, st);
     } else {
         if (p.mt == 1) return launch_main<D, S, 1, 2>(a, p, st);
+        if (p.mt == 16) return launch_main<D, S, 16, 1>(a, p, st);
     }
     if (p.mt == 4) return launch_main<D, S, 4, 2>(a, p, st);
     return launch_main<D, S, 8, 2>(a, p, st);
