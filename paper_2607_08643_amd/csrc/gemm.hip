@@ -219,14 +219,17 @@ __device__ __forceinline__ void wait_vm()
 constexpr int GEMM_LDS_BYTES = 160 * 1024;
 
 // Workgroups per compute unit of the main kernel. The 16-token, 64-row block
-// at d = 8 (57 VGPRs) runs three where three fit in LDS (1 or 2 stages: 4
-// ring slots of X~ and weight words and one table copy each): its steps are
-// short, and three blocks' waits overlap. Every other shape runs one, with
-// as many ring slots as fit. The plan sizes its K splits by the same count.
+// (56-74 VGPRs) runs three where three fit in LDS (4 ring slots of X~ and
+// weight words each, plus one table copy at d = 8, where 1 or 2 stages fit;
+// the d = 16 tables stay in global memory): its steps are short, and three
+// blocks' waits (the DMAs, and at d = 16 the table gathers) overlap. Every
+// other shape runs one, with as many ring slots as fit. The plan sizes its
+// K splits by the same count.
 constexpr int gemm_wg_per_cu(int d, int s, int mt, int nt)
 {
-    return (d == 8 && mt == 1 && nt == 1 && 3 * (4 * (16 * mt * 256 + nt * s * 192 * 16) + s * 4096) <= GEMM_LDS_BYTES)
-               ? 3 : 1;
+    if (mt != 1 || nt != 1) return 1;
+    if (d == 16) return 3;
+    return (d == 8 && 3 * (4 * (16 * mt * 256 + nt * s * 192 * 16) + s * 4096) <= GEMM_LDS_BYTES) ? 3 : 1;
 }
 
 // Shape of the main kernel. A workgroup of 8 waves owns BN = 64 NT weight
@@ -813,21 +816,21 @@ struct GemmPlan {
 GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, int64_t k)
 {
     GemmPlan p{};
-    // token tiles of 16 tokens up to 16 tokens, and at d = 8 up to 32 tokens
-    // and for projections of at most 2048 rows up to 64 tokens (these blocks
+    // token tiles of 16 tokens up to 16 tokens, for projections of at most
+    // 2048 rows up to 64 tokens, and at d = 8 up to 32 tokens (these blocks
     // run three per compute unit, and a block's token tiles share its
     // weights through L2); 64-token tiles up to 64 tokens, else 128; at
     // d = 16 above 128 tokens one 256-token tile of 64-row blocks, so that
     // each chunk's entry of the 2^16-entry table is gathered once per block
     // rather than once per token tile (at d = 8 the 256-token tile measured
     // slower: its decode is cheap and two ring slots are too few)
-    p.mt = (M <= 16 || (d == 8 && (M <= 32 || (M <= 64 && d_out <= 2048)))) ? 1 : (M <= 64) ? 4 : (d == 16 && M > 128) ? 16 : 8;
-    // d = 8: 64-row blocks with 16-token tiles, up to 64 tokens where both
-    // dimensions are at most 4096, and for at most 2048 rows of at most 4096
-    // inputs (twice the blocks, so fewer K splits and a lighter split-K sum;
-    // they measured faster there, not on the longer projections); 128-row
-    // blocks otherwise
-    p.nt = (p.mt == 16) ? 1 : (d == 8 && (p.mt == 1 || (d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048)))) ? 1 : 2;
+    p.mt = (M <= 16 || (M <= 64 && d_out <= 2048) || (d == 8 && M <= 32)) ? 1 : (M <= 64) ? 4 : (d == 16 && M > 128) ? 16 : 8;
+    // 64-row blocks with 16- and 256-token tiles, and at d = 8 up to 64 tokens
+    // where both dimensions are at most 4096 and for at most 2048 rows of at
+    // most 4096 inputs (twice the blocks, so fewer K splits and a lighter
+    // split-K sum; they measured faster there, not on the longer
+    // projections); 128-row blocks otherwise
+    p.nt = (p.mt == 1 || p.mt == 16 || (d == 8 && d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -924,7 +927,7 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
         if (p.mt == 4 && p.nt == 1) return launch_main<D, S, 4, 1>(a, p, st);
         if (p.mt == 8 && p.nt == 1) return launch_main<D, S, 8, 1>(a, p, st);
     } else {
-        if (p.mt == 1) return launch_main<D, S, 1, 2>(a, p, st);
+        if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
         if (p.mt == 16) return launch_main<D, S, 16, 1>(a, p, st);
     }
     if (p.mt == 4) return launch_main<D, S, 4, 2>(a, p, st);
