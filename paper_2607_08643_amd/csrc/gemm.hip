@@ -222,11 +222,15 @@ constexpr int GEMM_LDS_BYTES = 160 * 1024;
 // (56-74 VGPRs) runs three where three fit in LDS (4 ring slots of X~ and
 // weight words each, plus one table copy at d = 8, where 1 or 2 stages fit;
 // the d = 16 tables stay in global memory): its steps are short, and three
-// blocks' waits (the DMAs, and at d = 16 the table gathers) overlap. Every
-// other shape runs one, with as many ring slots as fit. The plan sizes its
-// K splits by the same count.
+// blocks' waits (the DMAs, and at d = 16 the table gathers) overlap. The
+// 64-token block (100-122 VGPRs) runs two where two fit with three ring
+// slots each. Every other shape runs one, with as many ring slots as fit.
+// The plan sizes its K splits by the same count.
 constexpr int gemm_wg_per_cu(int d, int s, int mt, int nt)
 {
+    if (mt == 4)
+        return (2 * (3 * (16 * mt * 256 + nt * s * (d == 8 ? 192 : 128) * 16) + (d == 8 ? s * 4096 : 0)) <= GEMM_LDS_BYTES)
+                   ? 2 : 1;
     if (mt != 1 || nt != 1) return 1;
     if (d == 16) return 3;
     return (d == 8 && 3 * (4 * (16 * mt * 256 + nt * s * 192 * 16) + s * 4096) <= GEMM_LDS_BYTES) ? 3 : 1;
@@ -256,7 +260,7 @@ struct GemmShape {
     static constexpr int TC = (D == 8 && WG_PER_CU == 1 && (GEMM_LDS_BYTES - S * 4096 * 8) / (XSLOT + WSLOT) >= 3) ? 8 : 1;
     static constexpr int TAB = (D == 8) ? S * 4096 * TC : 0;
     static constexpr int NS_FIT = (GEMM_LDS_BYTES / WG_PER_CU - TAB) / (XSLOT + WSLOT);
-    static constexpr int NS = (WG_PER_CU > 1) ? 4 : NS_FIT < 8 ? NS_FIT : 8;
+    static constexpr int NS = (WG_PER_CU > 1) ? (NS_FIT < 4 ? NS_FIT : 4) : NS_FIT < 8 ? NS_FIT : 8;
     static constexpr int NXI = BM / 4;              // X~ DMA wave instructions per step
     static constexpr int NWI = NT * S * WU / 64;    // weight DMA wave instructions per step
     static constexpr int NI = NXI + NWI;            // wave w issues instructions w, w + 8, ... < NI
@@ -825,12 +829,13 @@ GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, in
     // rather than once per token tile (at d = 8 the 256-token tile measured
     // slower: its decode is cheap and two ring slots are too few)
     p.mt = (M <= 16 || (M <= 64 && d_out <= 2048) || (d == 8 && M <= 32)) ? 1 : (M <= 64) ? 4 : (d == 16 && M > 128) ? 16 : 8;
-    // 64-row blocks with 16- and 256-token tiles, and at d = 8 up to 64 tokens
+    // 64-row blocks with 16- and 256-token tiles, at d = 16 with 64-token
+    // tiles (two per compute unit), and at d = 8 up to 64 tokens
     // where both dimensions are at most 4096 and for at most 2048 rows of at
     // most 4096 inputs (twice the blocks, so fewer K splits and a lighter
     // split-K sum; they measured faster there, not on the longer
     // projections); 128-row blocks otherwise
-    p.nt = (p.mt == 1 || p.mt == 16 || (d == 8 && d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048))) ? 1 : 2;
+    p.nt = (p.mt == 1 || p.mt == 16 || (d == 16 && p.mt == 4) || (d == 8 && d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
@@ -845,9 +850,9 @@ GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, in
     // allows (a second, partial round would double the time), keeping at least
     // 2 K steps per split and at most 8 splits (the partials of all splits
     // are written and read once more: at most 256 tiles' worth, 16 MiB).
-    // Blocks that run three per compute unit: up to 768 workgroups, with at
-    // least 8 K steps per split (shorter splits measured slower), but never
-    // fewer splits than the rule above.
+    // Blocks that run two or three per compute unit: up to 512 or 768
+    // workgroups, with at least 8 K steps per split (shorter splits measured
+    // slower), but never fewer splits than the rule above.
     const int64_t nt_ = std::max<int64_t>(tiles, 1);
     int64_t ks = std::min<int64_t>({256 / nt_, p.ksteps / 2, 8});
     const int wpc = gemm_wg_per_cu(d, stages, int(p.mt), int(p.nt));
@@ -928,6 +933,7 @@ hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
         if (p.mt == 8 && p.nt == 1) return launch_main<D, S, 8, 1>(a, p, st);
     } else {
         if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
+        if (p.mt == 4) return launch_main<D, S, 4, 1>(a, p, st);
         if (p.mt == 16) return launch_main<D, S, 16, 1>(a, p, st);
     }
     if (p.mt == 4) return launch_main<D, S, 4, 2>(a, p, st);
