@@ -823,19 +823,26 @@ GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, in
     // token tiles of 16 tokens up to 16 tokens, for projections of at most
     // 2048 rows up to 64 tokens, and at d = 8 up to 32 tokens (these blocks
     // run three per compute unit, and a block's token tiles share its
-    // weights through L2); 64-token tiles up to 64 tokens, else 128; at
-    // d = 16 above 128 tokens one 256-token tile of 64-row blocks, so that
-    // each chunk's entry of the 2^16-entry table is gathered once per block
-    // rather than once per token tile (at d = 8 the 256-token tile measured
-    // slower: its decode is cheap and two ring slots are too few)
-    p.mt = (M <= 16 || (M <= 64 && d_out <= 2048) || (d == 8 && M <= 32)) ? 1 : (M <= 64) ? 4 : (d == 16 && M > 128) ? 16 : 8;
+    // weights through L2); 64-token tiles up to 64 tokens, and at d = 8 of
+    // 64-row blocks (two per compute unit) for projections of at most 4096 x
+    // 4096 up to 128 tokens and of at most 2048 rows up to 256 tokens, else
+    // 128-token tiles; at d = 16 above 128 tokens one 256-token tile of
+    // 64-row blocks, so that each chunk's entry of the 2^16-entry table is
+    // gathered once per block rather than once per token tile (at d = 8 the
+    // 256-token tile measured slower: its decode is cheap and two ring slots
+    // are too few)
+    const bool mid8 = d == 8 && M > 64 && d_in <= 4096 && ((M <= 128 && d_out <= 4096) || (M <= 256 && d_out <= 2048));
+    p.mt = (M <= 16 || (M <= 64 && d_out <= 2048) || (d == 8 && M <= 32)) ? 1
+           : (M <= 64 || mid8)                                          ? 4
+           : (d == 16 && M > 128)                                       ? 16
+                                                                        : 8;
     // 64-row blocks with 16- and 256-token tiles, at d = 16 with 64-token
-    // tiles (two per compute unit), and at d = 8 up to 64 tokens
-    // where both dimensions are at most 4096 and for at most 2048 rows of at
-    // most 4096 inputs (twice the blocks, so fewer K splits and a lighter
-    // split-K sum; they measured faster there, not on the longer
-    // projections); 128-row blocks otherwise
-    p.nt = (p.mt == 1 || p.mt == 16 || (d == 16 && p.mt == 4) || (d == 8 && d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048))) ? 1 : 2;
+    // tiles (two per compute unit), with the 64-token tiles above 64 tokens
+    // named above, and at d = 8 up to 64 tokens where both dimensions are at
+    // most 4096 and for at most 2048 rows of at most 4096 inputs (twice the
+    // blocks, so fewer K splits and a lighter split-K sum; they measured
+    // faster there, not on the longer projections); 128-row blocks otherwise
+    p.nt = (p.mt == 1 || p.mt == 16 || (d == 16 && p.mt == 4) || mid8 || (d == 8 && d_out <= 4096 && d_in <= 4096 && (M <= 64 || d_out <= 2048))) ? 1 : 2;
     p.bm = 16 * p.mt;
     p.bn = 64 * p.nt;
     p.mtiles = (M + p.bm - 1) / p.bm;
