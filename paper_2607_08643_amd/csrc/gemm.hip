@@ -875,7 +875,10 @@ GemmPlan gemm_plan(int d, int stages, int64_t d_out, int64_t d_in, int64_t M, in
 }
 
 // Split-K sum: one thread per 8-output segment of Y, the partials added in
-// split order (z = 0, 1, ...), stored as the tiled kernel stores.
+// split order (z = 0, 1, ...), stored as the tiled kernel stores. KS is the
+// split count, so that all of a thread's loads are issued before the first
+// add (a loop over a run-time count waited for each split's loads in turn).
+template <int KS>
 __global__ __launch_bounds__(256) void gemm_splitk_sum(const GemmArgs a, int64_t mp)
 {
     const int64_t nseg = (a.d_out + 7) / 8;
@@ -883,12 +886,18 @@ __global__ __launch_bounds__(256) void gemm_splitk_sum(const GemmArgs a, int64_t
     if (e >= a.M * nseg) return;
     const int64_t m = e / nseg, n = 8 * (e - m * nseg);
     const float *src = a.part + m * a.np + n;
-    float4 lo = reinterpret_cast<const float4 *>(src)[0], hi = reinterpret_cast<const float4 *>(src)[1];
-    for (int z = 1; z < a.ksplit; ++z) {
+    float4 l[KS], h[KS];
+#pragma unroll
+    for (int z = 0; z < KS; ++z) {
         const float4 *pz = reinterpret_cast<const float4 *>(src + int64_t(z) * mp * a.np);
-        const float4 l = pz[0], h = pz[1];
-        lo.x += l.x; lo.y += l.y; lo.z += l.z; lo.w += l.w;
-        hi.x += h.x; hi.y += h.y; hi.z += h.z; hi.w += h.w;
+        l[z] = pz[0];
+        h[z] = pz[1];
+    }
+    float4 lo = l[0], hi = h[0];
+#pragma unroll
+    for (int z = 1; z < KS; ++z) {
+        lo.x += l[z].x; lo.y += l[z].y; lo.z += l[z].z; lo.w += l[z].w;
+        hi.x += h[z].x; hi.y += h[z].y; hi.z += h[z].z; hi.w += h[z].w;
     }
     const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
     if (a.y_vec && n + 8 <= a.d_out) {
@@ -926,7 +935,16 @@ hipError_t launch_main(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         const int64_t segs = a.M * ((a.d_out + 7) / 8);
-        hipLaunchKernelGGL(gemm_splitk_sum, dim3(unsigned((segs + 255) / 256)), dim3(256), 0, st, a, p.Mp);
+        const dim3 sg(unsigned((segs + 255) / 256));
+        switch (p.ksplit) {
+        case 2: hipLaunchKernelGGL(gemm_splitk_sum<2>, sg, dim3(256), 0, st, a, p.Mp); break;
+        case 3: hipLaunchKernelGGL(gemm_splitk_sum<3>, sg, dim3(256), 0, st, a, p.Mp); break;
+        case 4: hipLaunchKernelGGL(gemm_splitk_sum<4>, sg, dim3(256), 0, st, a, p.Mp); break;
+        case 5: hipLaunchKernelGGL(gemm_splitk_sum<5>, sg, dim3(256), 0, st, a, p.Mp); break;
+        case 6: hipLaunchKernelGGL(gemm_splitk_sum<6>, sg, dim3(256), 0, st, a, p.Mp); break;
+        case 7: hipLaunchKernelGGL(gemm_splitk_sum<7>, sg, dim3(256), 0, st, a, p.Mp); break;
+        default: hipLaunchKernelGGL(gemm_splitk_sum<8>, sg, dim3(256), 0, st, a, p.Mp); break;
+        }
     }
     return hipGetLastError();
 }
