@@ -223,13 +223,13 @@ constexpr int GEMM_LDS_BYTES = 160 * 1024;
 // weight words each, plus one table copy at d = 8, where 1 or 2 stages fit;
 // the d = 16 tables stay in global memory): its steps are short, and three
 // blocks' waits (the DMAs, and at d = 16 the table gathers) overlap. The
-// 64-token block (100-122 VGPRs) runs two where two fit with three ring
-// slots each. Every other shape runs one, with as many ring slots as fit.
+// 64-token block (100-122 VGPRs) runs two where two fit with at least two
+// ring slots each (up to four). Every other shape runs one, with as many ring slots as fit.
 // The plan sizes its K splits by the same count.
 constexpr int gemm_wg_per_cu(int d, int s, int mt, int nt)
 {
     if (mt == 4)
-        return (2 * (3 * (16 * mt * 256 + nt * s * (d == 8 ? 192 : 128) * 16) + (d == 8 ? s * 4096 : 0)) <= GEMM_LDS_BYTES)
+        return (2 * (2 * (16 * mt * 256 + nt * s * (d == 8 ? 192 : 128) * 16) + (d == 8 ? s * 4096 : 0)) <= GEMM_LDS_BYTES)
                    ? 2 : 1;
     if (mt != 1 || nt != 1) return 1;
     if (d == 16) return 3;
