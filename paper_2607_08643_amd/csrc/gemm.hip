@@ -224,8 +224,8 @@ constexpr int GEMM_LDS_BYTES = 160 * 1024;
 // the d = 16 tables stay in global memory): its steps are short, and three
 // blocks' waits (the DMAs, and at d = 16 the table gathers) overlap. The
 // 64-token block (100-122 VGPRs) runs two where two fit with at least two
-// ring slots each (up to four). Every other shape runs one, with as many ring slots as fit.
-// The plan sizes its K splits by the same count.
+// ring slots each (up to four). Every other shape runs one, with as many
+// ring slots as fit. The plan sizes its K splits by the same count.
 constexpr int gemm_wg_per_cu(int d, int s, int mt, int nt)
 {
     if (mt == 4)
@@ -952,17 +952,17 @@ hipError_t launch_main(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 template <int D, int S>
 hipError_t launch_gemm_t(const GemmArgs &a, const GemmPlan &p, hipStream_t st)
 {
+    // the shapes gemm_plan chooses, and only those
     if constexpr (D == 8) {
         if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
-        if (p.mt == 4 && p.nt == 1) return launch_main<D, S, 4, 1>(a, p, st);
-        if (p.mt == 8 && p.nt == 1) return launch_main<D, S, 8, 1>(a, p, st);
+        if (p.mt == 4) return (p.nt == 1) ? launch_main<D, S, 4, 1>(a, p, st) : launch_main<D, S, 4, 2>(a, p, st);
+        return (p.nt == 1) ? launch_main<D, S, 8, 1>(a, p, st) : launch_main<D, S, 8, 2>(a, p, st);
     } else {
         if (p.mt == 1) return launch_main<D, S, 1, 1>(a, p, st);
         if (p.mt == 4) return launch_main<D, S, 4, 1>(a, p, st);
         if (p.mt == 16) return launch_main<D, S, 16, 1>(a, p, st);
+        return launch_main<D, S, 8, 2>(a, p, st);
     }
-    if (p.mt == 4) return launch_main<D, S, 4, 2>(a, p, st);
-    return launch_main<D, S, 8, 2>(a, p, st);
 }
 
 }  // namespace
