@@ -219,7 +219,14 @@ SPLITK = [
     ("splitk-200x2600-d8", 200, 2600, dict(d=8, hidden=8), torch.bfloat16, 1, False),
     ("splitk-130x2608-d16", 130, 2608, dict(d=16, hidden=16), torch.bfloat16, 1, False),
 ]
-GEMM_CASES = [SMALL[1], SMALL[2], SMALL[3], SMALL[6], SMALL[11], SMALL[14], SMALL[15], SMALL[16], SMALL[17]] + SPLITK
+# Stage counts 1 and 3 at d = 8 and 3 and 4 at d = 16, so that every kernel
+# shape of the GEMM (token tile x row block x stages) runs at some M.
+GEMM_STAGES = [
+    ("mlp-3stage-70x1000-d8", 70, 1000, dict(d=8, hidden=8, stages=3), torch.bfloat16, 1, False),
+    ("mlp-4stage-90x640-d16", 90, 640, dict(d=16, hidden=16, stages=4), torch.bfloat16, 1, False),
+]
+GEMM_CASES = ([SMALL[1], SMALL[2], SMALL[3], SMALL[5], SMALL[6], SMALL[11], SMALL[12], SMALL[14], SMALL[15], SMALL[16],
+               SMALL[17]] + GEMM_STAGES + SPLITK)
 
 
 @pytest.mark.parametrize("case", GEMM_CASES, ids=[c[0] for c in GEMM_CASES])
