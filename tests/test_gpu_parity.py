@@ -457,6 +457,34 @@ def test_full_size_gemm(d, M, gpu):
                   torch.bfloat16)
 
 
+@pytest.mark.parametrize("d_out,d_in,M", [(2304, 4608, 64), (512, 1024, 300)], ids=["2304x4608-M64", "512x1024-M300"])
+def test_gemm_wide_and_long_shapes(d_out, d_in, M, gpu):
+    """The d = 8 shapes no other case selects: 64-token tiles of 128-row
+    blocks (more than 4096 inputs, at most 64 tokens, two blocks per compute
+    unit) and 128-token tiles of 64-row blocks (at most 2048 rows, more than
+    256 tokens), with rank-16 LoRA and 1% protected columns."""
+    say(f"gemm {d_out}x{d_in} M={M} d=8")
+    cfg = bsq.Config(d=8, hidden=8)
+    oc = ocfg(cfg)
+    decs = decoders(cfg, seed=12)
+    W, _ = synth.weight(d_out, d_in, seed=78, k_outliers=cfg.k(d_in), device=gpu)
+    codec = bsq.bsq_codec_prepare(cfg, decs, device=gpu)
+    layer = bsq.bsq_encode(cfg, codec, W)
+    X = synth.activation(d_in, seed=10, device=gpu, batch=M)
+    A, Bm = synth.lora(d_out, d_in, 16, seed=11, device=gpu)
+    Y = bsq.bsq_gemm(cfg, codec, layer, X, lora=(A, Bm), y_dtype=torch.float32)
+    torch.cuda.synchronize()
+    tabs = oracle.decoder_table(oc, decs)
+    enc = oracle.encode(oc, decs, oracle.to_f32(W), tables=tabs)
+    assert_layer_equal(layer, enc, cfg)
+    lref = (oracle.to_f32(A), oracle.to_f32(Bm))
+    w_hat = oracle.decode(oc, decs, enc, tables=tabs)
+    Xf = oracle.to_f32(X)
+    Y_ref = oracle.dense_product(w_hat, Xf, lref)
+    check_product(Y.cpu().numpy(), Y_ref, "gemm", cfg, enc, tabs, w_hat, Xf, lref, f"gemm {d_out}x{d_in} M={M}",
+                  torch.float32)
+
+
 @pytest.mark.parametrize("n_mats,d_out,d_in", [(8, 1024, 4096), (64, 1024, 5120)],
                          ids=["8x1024x4096", "64x1024x5120"])
 def test_category_batched_stack_encode(n_mats, d_out, d_in, gpu):
